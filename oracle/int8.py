@@ -1,0 +1,249 @@
+"""Exact-integer oracle of the low-bit (INT8) inverse path (test infrastructure only).
+
+The paper (Section 3.5 and Appendix G) runs the masked truncated Neumann
+expansion and the residual correction on integer hardware with a uniform
+symmetric quantiser q(x) = clip(round(x / Delta), qmin, qmax) and a
+per-tensor scale, and keeps the order low (N <= 3) so that the dynamic range
+of the powers stays small.  It does not spell out the integer mechanics.
+This module fixes them (one reading, applied identically by the GPU path):
+
+  * A matrix is stored as int8 codes q in [-127, 127] and one exponent e per
+    tile (value = q * 2^e, Delta = 2^e: a power-of-two per-tile scale).
+    Unit lower-triangular matrices (T^(0), sum E^s, T_hat) are stored as
+    I + (int8 strict part) * 2^e: the unit diagonal is kept exact.
+  * quantize(x): e = smallest integer with max|x| / 2^e <= 127,
+    q = round-half-even(x / 2^e).
+  * Every int8 x int8 product is accumulated exactly in int32
+    (|acc| <= C * 127^2 < 2^21 for C <= 64), then requantised ("per-power
+    rescaling"): s = smallest s >= 0 with rne(max|acc| / 2^s) <= 127,
+    q = rne(acc / 2^s), e = e1 + e2 + s.
+  * Sums align their terms at a common exponent e* and add exactly in
+    int32.  e* is the finest exponent present, raised where needed so that no
+    aligned term exceeds 2^23 in magnitude (terms below e* are shifted right
+    with round-half-even).  A term is present when the matrix it comes from
+    is not identically zero (a product is present when both factors are).
+  * The diagonal mask M^(N) is applied to every power before it is
+    quantised (in exact arithmetic M (sum L^n) = sum M L^n, and masking first
+    keeps the deep sub-diagonal outliers out of every scale).
+  * E is formed exactly as Lm + Lm N0 - N0 (= I - (I - Lm)(I + N0)) in int32
+    and its band i - j <= N, exactly zero in real arithmetic, is set to 0.
+  * The residual powers run as P_s = E P_{s-1} (equal to P_{s-1} E in exact
+    arithmetic; fixing the side fixes which quantised factor is used).
+
+All arithmetic here is on Python/numpy integers; no floating point enters
+after quantize().
+"""
+
+from __future__ import annotations
+
+from typing import List, Tuple
+
+import numpy as np
+
+QMAX = 127
+ALIGN_BITS = 23  # aligned terms stay below 2^23 in magnitude
+
+
+# ----------------------------------------------------------------------------
+# rounding primitives
+
+
+def rne_shift(y: np.ndarray, s) -> np.ndarray:
+    """round-half-even(y / 2^s) for integer y and integer s >= 0 (per element
+    or broadcast)."""
+    y = np.asarray(y, dtype=np.int64)
+    assert np.all(np.abs(y) < (1 << 60))
+    s = np.asarray(s, dtype=np.int64)
+    # |y| < 2^60 gives |y| / 2^s < 1/2 for s >= 62: the result is 0, which
+    # shifting by 62 also yields (floor 0 or -1, remainder below one half).
+    s_b = np.minimum(np.broadcast_to(s, y.shape), 62)
+    out = y.copy()
+    pos = s_b > 0
+    if np.any(pos):
+        ss = np.where(pos, s_b, 0)
+        q = y >> ss  # floor
+        r = y - (q << ss)
+        half = np.where(pos, np.int64(1) << np.maximum(ss - 1, 0), 0)
+        up = (r > half) | ((r == half) & ((q & 1) == 1))
+        out = np.where(pos, q + up.astype(np.int64), y)
+    return out
+
+
+def _tile_amax(q: np.ndarray) -> np.ndarray:
+    return np.max(np.abs(q), axis=(-1, -2))
+
+
+def requant(acc: np.ndarray, e: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per tile: smallest shift s >= 0 with rne(max|acc| / 2^s) <= 127;
+    returns (q int64 codes, e + s).  An all-zero tile gets e = 0."""
+    acc = np.asarray(acc, dtype=np.int64)
+    e = np.asarray(e, dtype=np.int64)
+    amax = _tile_amax(acc)
+    s = np.zeros_like(amax)
+    while True:
+        big = rne_shift(amax, s) > QMAX
+        if not np.any(big):
+            break
+        s = s + big.astype(np.int64)
+    q = rne_shift(acc, s[..., None, None])
+    e_out = np.where(amax > 0, e + s, 0)
+    return q, e_out
+
+
+# ----------------------------------------------------------------------------
+# quantisation of the float input
+
+
+def quantize(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Symmetric per-tile quantiser with a power-of-two scale.
+
+    x float32 tiles [..., C, C].  e = ceil(log2(amax / 127)) computed exactly
+    from frexp: amax = m 2^p, m in [0.5, 1) gives amax / 2^(p-7) = 128 m,
+    which is <= 127 unless m > 127/128.  q = rne(x / 2^e).  All-zero tiles
+    get q = 0, e = 0."""
+    x = np.asarray(x, dtype=np.float32).astype(np.float64)
+    amax = np.max(np.abs(x), axis=(-1, -2))
+    m, p = np.frexp(amax)
+    e = (p.astype(np.int64) - 7) + (m * 128.0 > 127.0).astype(np.int64)
+    e = np.where(amax > 0, e, 0)
+    q = np.rint(np.ldexp(x, -e[..., None, None])).astype(np.int64)
+    assert np.all(np.abs(q) <= QMAX)
+    return q, e
+
+
+# ----------------------------------------------------------------------------
+# exact aligned sums
+
+
+def _acc_bits(C: int) -> int:
+    # |acc| <= C * 127^2 < C * 2^14
+    return 14 + int(np.ceil(np.log2(C)))
+
+
+def aligned_sum(terms: List[Tuple[np.ndarray, np.ndarray, np.ndarray, int]]):
+    """Exact int32 sum of q_k * 2^(e_k) at a common exponent e*.
+
+    terms: list of (q, e, present, bits) with q [..., C, C] int, e [...] int,
+    present [...] bool, bits = log2 bound of |q| (7 for int8 codes, 14+log2 C
+    for raw products).  e* = max(min e_k, max(e_k + bits_k) - 23) over the
+    present terms; each present term is shifted to e* (left exactly, or right
+    with round-half-even).  Returns (sum, e*, any_present)."""
+    shape = terms[0][0].shape[:-2]
+    BIG = np.int64(1 << 40)
+    e_min = np.full(shape, BIG)
+    top = np.full(shape, -BIG)
+    anyp = np.zeros(shape, dtype=bool)
+    for q, e, p, bits in terms:
+        e_min = np.where(p, np.minimum(e_min, e), e_min)
+        top = np.where(p, np.maximum(top, e + bits), top)
+        anyp |= p
+    e_star = np.maximum(e_min, top - ALIGN_BITS)
+    e_star = np.where(anyp, e_star, 0)
+    total = np.zeros(terms[0][0].shape, dtype=np.int64)
+    for q, e, p, bits in terms:
+        q = np.asarray(q, np.int64)
+        d = (e - e_star)[..., None, None]
+        left = q << np.maximum(d, 0)
+        right = rne_shift(q, np.maximum(-d, 0))
+        t = np.where(d >= 0, left, right)
+        total = total + np.where(p[..., None, None], t, 0)
+    assert np.all(np.abs(total) < (1 << 31))
+    return total, e_star, anyp
+
+
+# ----------------------------------------------------------------------------
+# the INT8 pipeline
+
+
+def _subdiag(C: int) -> np.ndarray:
+    i = np.arange(C)[:, None]
+    j = np.arange(C)[None, :]
+    return i - j
+
+
+def neumann_inverse_int8(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
+    """Integer T_hat(N, S) from the quantised GDN matrix (qA, eA).
+
+    qA int [..., C, C] (only i > j is read), eA int [...].
+    Returns (qT, eT): T_hat = I + qT * 2^eT, qT int8-range codes of the
+    strict lower part (zero on and above the diagonal), and the parts
+    dictionary for inspection."""
+    qA = np.asarray(qA, np.int64)
+    eA = np.asarray(eA, np.int64)
+    C = qA.shape[-1]
+    d = _subdiag(C)
+    strict = d > 0
+    band = (d > 0) & (d <= N)
+    accb = _acc_bits(C)
+
+    qL = np.where(strict, -qA, 0)
+    eL = eA
+    nzL = _tile_amax(qL) > 0
+
+    # Section 3.1 / 3.3: masked powers B_n = M (Lm^n), B_n = M (B_{n-1} Lm)
+    powers = []
+    if N >= 1:
+        qB = np.where(band, qL, 0)
+        qB, eB = requant(qB, eL)
+        powers.append((qB, eB, _tile_amax(qB) > 0))
+        for _n in range(2, N + 1):
+            qP, eP, nzP = powers[-1]
+            acc = np.where(band, qP @ qL, 0)
+            q, e = requant(acc, eP + eL)
+            powers.append((q, e, (_tile_amax(q) > 0)))
+
+    # N0 = strict part of T^(0) = sum_n B_n
+    if powers:
+        s_, e_, p_ = aligned_sum([(q, e, p, 7) for (q, e, p) in powers])
+        qN0, eN0 = requant(s_, e_)
+    else:
+        qN0 = np.zeros_like(qL)
+        eN0 = np.zeros_like(eL)
+    nzN0 = _tile_amax(qN0) > 0
+
+    # E = I - (I + A) T0 = Lm + Lm N0 - N0, band zeroed (Section 3.4)
+    s_, e_, _ = aligned_sum([
+        (qL, eL, nzL, 7),
+        (qL @ qN0, eL + eN0, nzL & nzN0, accb),
+        (-qN0, eN0, nzN0, 7),
+    ])
+    s_ = np.where(d > N, s_, 0)
+    qE, eE = requant(s_, e_)
+    nzE = _tile_amax(qE) > 0
+
+    # residual powers P_s = E P_{s-1}, G strict part = sum_{s=1}^{S} P_s
+    chain = []
+    if S >= 1:
+        chain.append((qE, eE, nzE))
+        for _s in range(2, S + 1):
+            qP, eP, nzP = chain[-1]
+            q, e = requant(qE @ qP, eE + eP)
+            chain.append((q, e, (_tile_amax(q) > 0)))
+    if chain:
+        s_, e_, _ = aligned_sum([(q, e, p, 7) for (q, e, p) in chain])
+        qG, eG = requant(s_, e_)
+    else:
+        qG = np.zeros_like(qL)
+        eG = np.zeros_like(eL)
+    nzG = _tile_amax(qG) > 0
+
+    # T_hat = (I + N0)(I + Gs) = I + N0 + Gs + N0 Gs
+    s_, e_, _ = aligned_sum([
+        (qN0, eN0, nzN0, 7),
+        (qG, eG, nzG, 7),
+        (qN0 @ qG, eN0 + eG, nzN0 & nzG, accb),
+    ])
+    s_ = np.where(strict, s_, 0)
+    qT, eT = requant(s_, e_)
+    parts = {"N0": (qN0, eN0), "E": (qE, eE), "G": (qG, eG), "powers": powers, "chain": chain}
+    return qT, eT, parts
+
+
+def dequant_unit(qT: np.ndarray, eT: np.ndarray) -> np.ndarray:
+    """I + qT * 2^eT as float64."""
+    C = qT.shape[-1]
+    return np.eye(C) + np.ldexp(np.asarray(qT, np.float64), np.asarray(eT)[..., None, None])
+
+
+def dequant(q: np.ndarray, e: np.ndarray) -> np.ndarray:
+    return np.ldexp(np.asarray(q, np.float64), np.asarray(e)[..., None, None])
