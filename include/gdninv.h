@@ -1,0 +1,149 @@
+/*
+ * gdninv.h -- C ABI of the MI355X (gfx950) chunk-inverse library for
+ * chunk-wise Gated DeltaNet.
+ *
+ * Problem (arXiv 2606.06034, Section 2.1): for every (batch, head, chunk)
+ * tile, invert the unit lower-triangular C x C matrix (I + A), where
+ *     A_ij = beta_i (k_i . k_j) exp(g_i - g_j)   for i > j,   else 0,
+ * and apply the inverse to the chunk's keys and values.  The paper writes
+ * the inverse as (I - A)^-1; this library uses the Gated DeltaNet sign, so
+ * every paper formula holds with Lm := -A.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  All tensor pointers are DEVICE pointers (HIP global memory of
+ *   the current device) owned by the caller; the library allocates no device
+ *   memory and keeps no state between calls apart from loaded code objects.
+ *   Tensors are dense, row-major and contiguous; every pointer must be
+ *   16-byte aligned.  Outputs must not overlap inputs.
+ * Layouts.  K [B, L, H, dk], V [B, L, H, dv], W [B, L, H, dk],
+ *   U [B, L, H, dv], beta [B, L, H] fp32, g [B, L, H] fp32 (g is the
+ *   within-chunk inclusive cumulative sum of the per-token log-decay).
+ *   Tile tensors A / Tinv: [B, H, L/C, C, C], so tile t = (b H + h) L/C + chunk,
+ *   row i = the later token.  INT8 tiles have the same layout in int8 with one
+ *   int32 exponent per tile.
+ * dtypes.  GDN_F32 stores fp32 and computes with fp32 MFMA.  GDN_BF16 stores
+ *   bf16 and rounds every MFMA operand to bf16 (round to nearest even);
+ *   products accumulate in fp32, and sums, identity additions and the
+ *   residual are formed in fp32.  beta and g are always fp32.
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Every
+ *   call only enqueues work on that stream and returns; results are valid
+ *   once the stream has synchronised.  No call synchronises the device.
+ *   Calls are thread-safe.
+ * Errors.  Return GDN_OK (0) or a negative GDN_ERR_* code.  Arguments are
+ *   validated before anything is enqueued, so an error return means nothing
+ *   was launched.  GDN_ERR_HIP reports a failed launch (hipGetLastError);
+ *   faults inside a kernel surface at the caller's next synchronisation.
+ *   n_tiles == 0 (or B == 0) is a no-op returning GDN_OK.
+ * Sizes.  C in {16, 32, 64, 128}; L % C == 0; dk, dv in {64, 128};
+ *   0 <= N <= C - 1 and 0 <= S <= C - 1 (C = 128: N, S <= 63, see below).
+ */
+#ifndef GDNINV_H
+#define GDNINV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GDN_ABI_VERSION 1
+
+enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1, GDN_I8 = 2 };
+
+enum gdn_status {
+  GDN_OK = 0,
+  GDN_ERR_NULL = -1,        /* a required pointer is NULL                     */
+  GDN_ERR_SHAPE = -2,       /* a size is out of range or L % C != 0           */
+  GDN_ERR_PARAM = -3,       /* N or S out of range                            */
+  GDN_ERR_DTYPE = -4,       /* unknown or unsupported dtype combination       */
+  GDN_ERR_ALIGN = -5,       /* a pointer is not 16-byte aligned               */
+  GDN_ERR_ALIAS = -6,       /* an output overlaps an input                    */
+  GDN_ERR_HIP = -7,         /* the HIP runtime rejected a launch              */
+  GDN_ERR_UNSUPPORTED = -8  /* valid request this build does not implement    */
+};
+
+/* Version of this ABI (GDN_ABI_VERSION). */
+int gdn_abi_version(void);
+
+/* Static, NUL-terminated description of a status code; never NULL. */
+const char* gdn_status_string(int status);
+
+/* Default (N, S) per chunk size: 16 -> (3, 2), 32 -> (3, 4) (Section 4.3),
+ * 64 -> (3, 8) (Section 4.1), 128 -> (3, 8) per 64-block (Appendix H).
+ * Writes *N, *S; GDN_ERR_SHAPE for other C, GDN_ERR_NULL for NULL outputs. */
+int gdn_default_order(int C, int* N, int* S);
+
+/* Build the chunk matrices A (Section 2.1 with the Gated DeltaNet gate):
+ *   A[t, i, j] = beta_i (k_i . k_j) exp(g_i - g_j) for i > j, 0 otherwise,
+ * with i, j tokens of chunk t.  The gate is evaluated as the exponential of
+ * the difference.  K: [B, L, H, dk] in k_dtype (GDN_F32 or GDN_BF16);
+ * beta, g: [B, L, H] fp32; A: [B, H, L/C, C, C] in a_dtype (GDN_F32 or
+ * GDN_BF16; the upper triangle and diagonal are written as 0).  The Gram
+ * product accumulates in fp32. */
+int gdn_build_A(const void* K, const float* beta, const float* g, void* A,
+                int B, int L, int H, int dk, int C, int k_dtype, int a_dtype,
+                void* stream);
+
+/* MatMul-only approximate inverse (Sections 3.1-3.4, Algorithm 1):
+ *   T0   = M^(N) (Hadamard) sum_{n=0}^{N} Lm^n,  M^(N)_ij = [i - j <= N],
+ *   E    = I - (I + A) T0,
+ *   Tinv = T0 sum_{s=0}^{S} E^s            (the ordering of Section 3.4 and
+ *                                            Appendix D).
+ * A: n_tiles tiles of C x C (entries on/above the diagonal are ignored);
+ * Tinv: same shape, written with exact unit diagonal and zero upper
+ * triangle.  dtype GDN_F32 or GDN_BF16 for both A and Tinv.  C = 128 is
+ * computed block-wise (Appendix E, Appendix H): both 64 x 64 diagonal blocks
+ * by the formula above with the given (N, S), joined by
+ * Tinv_21 = -Tinv_22 A_21 Tinv_11. */
+int gdn_chunk_inverse_neumann(const void* A, void* Tinv, int64_t n_tiles, int C,
+                              int N, int S, int dtype, void* stream);
+
+/* Exact inverse (I + A)^-1 by forward substitution (Section 2.2): row by
+ * row, n_i = -a_i - a_i N_{0:i,0:i} over the finished rows, Tinv = I + N.
+ * Computed in fp32 whatever the storage dtype.  A, Tinv as above. */
+int gdn_chunk_inverse_fwdsub(const void* A, void* Tinv, int64_t n_tiles, int C,
+                             int dtype, void* stream);
+
+/* WY application: per chunk, W = Tinv diag(beta) K and U = Tinv diag(beta) V.
+ * Tinv: [B, H, L/C, C, C], K/W: [B, L, H, dk], V/U: [B, L, H, dv], all in
+ * `dtype` (GDN_F32 or GDN_BF16); beta fp32.  Only the lower triangle of
+ * Tinv is read. */
+int gdn_wy_apply(const void* Tinv, const void* K, const void* V, const float* beta,
+                 void* W, void* U, int B, int L, int H, int dk, int dv, int C,
+                 int dtype, void* stream);
+
+/* Fused path in one launch: gdn_build_A, gdn_chunk_inverse_neumann and
+ * gdn_wy_apply with every intermediate kept on chip.  Tinv may be NULL;
+ * otherwise the approximate inverse is also written ([B, H, L/C, C, C]).
+ * dtype applies to K, V, W, U and Tinv.  A is formed in fp32 and rounded to
+ * the compute dtype as an MFMA operand. */
+int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const float* g,
+                       void* W, void* U, void* Tinv, int B, int L, int H, int dk,
+                       int dv, int C, int N, int S, int dtype, void* stream);
+
+/* INT8 mode, step 1 (Appendix G quantiser): per tile, e = the smallest
+ * integer with max|A| / 2^e <= 127 and Aq = round-half-even(A / 2^e).
+ * A: fp32 tiles; Aq: int8 tiles (same layout); eA: int32 [n_tiles].  An
+ * all-zero tile gets Aq = 0, eA = 0.  Only the strictly lower part of A is
+ * read (the rest is taken as 0 and written as 0). */
+int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles,
+                          int C, void* stream);
+
+/* INT8 mode, step 2: the approximate inverse of gdn_chunk_inverse_neumann in
+ * integer arithmetic (Section 3.5): int8 x int8 MFMA products accumulated
+ * exactly in int32 and requantised to int8 after every product with a
+ * per-tile power-of-two rescale; the mask is applied to every power before
+ * it is quantised; sums align their terms exactly in int32.  Outputs:
+ * Tinv = I + Tq * 2^eT, Tq int8 tiles holding the strict lower part (0 on
+ * and above the diagonal), eT int32 [n_tiles]; Tdeq (nullable) receives
+ * I + Tq * 2^eT in fp32.  C in {16, 32, 64}.  Requires finite inputs. */
+int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq,
+                                 int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
+                                 int N, int S, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDNINV_H */

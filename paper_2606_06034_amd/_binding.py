@@ -1,0 +1,210 @@
+"""ctypes marshalling for libgdninv.so (see include/gdninv.h for the contract)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgdninv.so")
+
+GDN_F32, GDN_BF16, GDN_I8 = 0, 1, 2
+
+_c_int, _c_i64, _vp = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
+
+# name -> argtypes (all return int unless noted)
+_SIGS = {
+    "gdn_abi_version": [],
+    "gdn_status_string": [_c_int],
+    "gdn_default_order": [_c_int, ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)],
+    "gdn_build_A": [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_inverse_neumann": [_vp, _vp, _c_i64, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_inverse_fwdsub": [_vp, _vp, _c_i64, _c_int, _c_int, _vp],
+    "gdn_wy_apply": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                     _c_int, _vp],
+    "gdn_chunk_wy_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int,
+                           _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_quantize_tiles_i8": [_vp, _vp, _vp, _c_i64, _c_int, _vp],
+    "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int, _vp],
+}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2606_06034_amd.csrc.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    for name, args in _SIGS.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_char_p if name == "gdn_status_string" else _c_int
+    return L
+
+
+lib = _load()
+
+
+def abi_symbols():
+    return list(_SIGS)
+
+
+class GdnError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        self.code = code
+        super().__init__(f"{fn}: {code} ({lib.gdn_status_string(code).decode()})")
+
+
+def _check(fn: str, code: int):
+    if code != 0:
+        raise GdnError(fn, code)
+
+
+def gdn_abi_version() -> int:
+    return lib.gdn_abi_version()
+
+
+def gdn_status_string(code: int) -> str:
+    return lib.gdn_status_string(code).decode()
+
+
+def gdn_default_order(C: int) -> Tuple[int, int]:
+    n, s = _c_int(), _c_int()
+    _check("gdn_default_order", lib.gdn_default_order(C, ctypes.byref(n), ctypes.byref(s)))
+    return n.value, s.value
+
+
+# ---------------------------------------------------------------------------
+
+_FDT = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}
+_TDT = {GDN_F32: torch.float32, GDN_BF16: torch.bfloat16}
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    return t.data_ptr()
+
+
+def _fdtype(t: torch.Tensor, name: str) -> int:
+    if t.dtype not in _FDT:
+        raise TypeError(f"{name}: dtype {t.dtype} not supported (float32 or bfloat16)")
+    return _FDT[t.dtype]
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _tiles(A: torch.Tensor) -> Tuple[int, int]:
+    if A.dim() < 2 or A.shape[-1] != A.shape[-2]:
+        raise ValueError("tile tensor must end in (C, C)")
+    C = A.shape[-1]
+    return A.numel() // (C * C), C
+
+
+def gdn_build_A(K: torch.Tensor, beta: torch.Tensor, g: torch.Tensor, C: int,
+                a_dtype: Optional[torch.dtype] = None, A: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """A [B, H, L/C, C, C] from K [B, L, H, dk], beta, g [B, L, H] (fp32)."""
+    B, L, H, dk = K.shape
+    kdt = _fdtype(K, "K")
+    adt = _FDT[a_dtype] if a_dtype is not None else (_fdtype(A, "A") if A is not None else kdt)
+    if A is None:
+        A = torch.empty((B, H, L // C if C else 0, C, C), dtype=_TDT[adt], device=K.device)
+    _check("gdn_build_A", lib.gdn_build_A(
+        _dev(K, "K"), _dev(beta, "beta", torch.float32), _dev(g, "g", torch.float32),
+        _dev(A, "A", _TDT[adt]), B, L, H, dk, C, kdt, adt, _stream(stream)))
+    return A
+
+
+def gdn_chunk_inverse_neumann(A: torch.Tensor, N: int, S: int, Tinv: Optional[torch.Tensor] = None,
+                              stream=None) -> torch.Tensor:
+    """T_hat(N, S) of every C x C tile of A (same shape and dtype)."""
+    n, C = _tiles(A)
+    dt = _fdtype(A, "A")
+    if Tinv is None:
+        Tinv = torch.empty_like(A)
+    _check("gdn_chunk_inverse_neumann", lib.gdn_chunk_inverse_neumann(
+        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype), n, C, N, S, dt, _stream(stream)))
+    return Tinv
+
+
+def gdn_chunk_inverse_fwdsub(A: torch.Tensor, Tinv: Optional[torch.Tensor] = None,
+                             stream=None) -> torch.Tensor:
+    """Exact (I + A)^-1 of every tile by forward substitution."""
+    n, C = _tiles(A)
+    dt = _fdtype(A, "A")
+    if Tinv is None:
+        Tinv = torch.empty_like(A)
+    _check("gdn_chunk_inverse_fwdsub", lib.gdn_chunk_inverse_fwdsub(
+        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype), n, C, dt, _stream(stream)))
+    return Tinv
+
+
+def gdn_wy_apply(Tinv: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor, C: int,
+                 W: Optional[torch.Tensor] = None, U: Optional[torch.Tensor] = None,
+                 stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """W = T diag(beta) K, U = T diag(beta) V per chunk."""
+    B, L, H, dk = K.shape
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    W = torch.empty_like(K) if W is None else W
+    U = torch.empty_like(V) if U is None else U
+    _check("gdn_wy_apply", lib.gdn_wy_apply(
+        _dev(Tinv, "Tinv", K.dtype), _dev(K, "K"), _dev(V, "V", K.dtype),
+        _dev(beta, "beta", torch.float32), _dev(W, "W", K.dtype), _dev(U, "U", K.dtype),
+        B, L, H, dk, dv, C, dt, _stream(stream)))
+    return W, U
+
+
+def gdn_chunk_wy_fused(K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor, g: torch.Tensor,
+                       C: int, N: int, S: int, want_T: bool = False,
+                       W: Optional[torch.Tensor] = None, U: Optional[torch.Tensor] = None,
+                       Tinv: Optional[torch.Tensor] = None, stream=None):
+    """Fused build A -> T_hat(N, S) -> (W, U[, Tinv])."""
+    B, L, H, dk = K.shape
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    W = torch.empty_like(K) if W is None else W
+    U = torch.empty_like(V) if U is None else U
+    if want_T and Tinv is None:
+        Tinv = torch.empty((B, H, L // C, C, C), dtype=K.dtype, device=K.device)
+    tp = _dev(Tinv, "Tinv", K.dtype) if Tinv is not None else None
+    _check("gdn_chunk_wy_fused", lib.gdn_chunk_wy_fused(
+        _dev(K, "K"), _dev(V, "V", K.dtype), _dev(beta, "beta", torch.float32),
+        _dev(g, "g", torch.float32), _dev(W, "W", K.dtype), _dev(U, "U", K.dtype), tp,
+        B, L, H, dk, dv, C, N, S, dt, _stream(stream)))
+    return (W, U, Tinv) if Tinv is not None else (W, U)
+
+
+def gdn_quantize_tiles_i8(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
+                          eA: Optional[torch.Tensor] = None, stream=None):
+    """(Aq int8 tiles, eA int32 per tile) with A ~ Aq * 2^eA."""
+    n, C = _tiles(A)
+    Aq = torch.empty(A.shape, dtype=torch.int8, device=A.device) if Aq is None else Aq
+    eA = torch.empty(n, dtype=torch.int32, device=A.device) if eA is None else eA
+    _check("gdn_quantize_tiles_i8", lib.gdn_quantize_tiles_i8(
+        _dev(A, "A", torch.float32), _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32),
+        n, C, _stream(stream)))
+    return Aq, eA
+
+
+def gdn_chunk_inverse_neumann_i8(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: int,
+                                 want_deq: bool = False, stream=None):
+    """(Tq int8, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT."""
+    n, C = _tiles(Aq)
+    Tq = torch.empty_like(Aq)
+    eT = torch.empty_like(eA)
+    Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device) if want_deq else None
+    _check("gdn_chunk_inverse_neumann_i8", lib.gdn_chunk_inverse_neumann_i8(
+        _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32), _dev(Tq, "Tq"), _dev(eT, "eT"),
+        _dev(Td, "Tdeq") if Td is not None else None, n, C, N, S, _stream(stream)))
+    return (Tq, eT, Td) if want_deq else (Tq, eT)

@@ -1,0 +1,207 @@
+// api.cpp -- the extern "C" boundary declared in include/gdninv.h.
+// Validates every argument before anything is enqueued, then dispatches to
+// the launchers.  Holds no state.
+#include "gdninv.h"
+
+#include <stdint.h>
+
+#include "launch.hpp"
+
+namespace {
+
+constexpr int64_t kMaxTiles = 0x7fffffff;  // one workgroup per tile, 1-D grid
+
+bool valid_C(int C) { return C == 16 || C == 32 || C == 64 || C == 128; }
+bool valid_d(int d) { return d == 64 || d == 128; }
+bool fdtype(int t) { return t == GDN_F32 || t == GDN_BF16; }
+int64_t esize(int t) { return t == GDN_F32 ? 4 : (t == GDN_BF16 ? 2 : 1); }
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// [p, p + bytes) and [q, q + qbytes) intersect
+bool overlap(const void* p, int64_t bytes, const void* q, int64_t qbytes) {
+  if (!p || !q || bytes <= 0 || qbytes <= 0) return false;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+  return a < b + (uintptr_t)qbytes && b < a + (uintptr_t)bytes;
+}
+
+int order_ok(int C, int N, int S) {
+  const int lim = (C == 128 ? 64 : C) - 1;  // C = 128 runs 64-blocks
+  return N >= 0 && S >= 0 && N <= lim && S <= lim;
+}
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return GDN_OK;
+  if (e == hipErrorNotSupported) return GDN_ERR_UNSUPPORTED;
+  return GDN_ERR_HIP;
+}
+
+// common checks of the [B, L, H, d] entry points; fills the tile count
+int check_chunked(int B, int L, int H, int C, int64_t* n_tiles) {
+  if (B < 0 || L < 0 || H < 0 || !valid_C(C) || L % C != 0) return GDN_ERR_SHAPE;
+  const int64_t n = (int64_t)B * H * (L / C);
+  if (n > kMaxTiles) return GDN_ERR_SHAPE;
+  *n_tiles = n;
+  return GDN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int gdn_abi_version(void) { return GDN_ABI_VERSION; }
+
+const char* gdn_status_string(int status) {
+  switch (status) {
+    case GDN_OK: return "ok";
+    case GDN_ERR_NULL: return "a required pointer is NULL";
+    case GDN_ERR_SHAPE: return "size out of range (C in {16,32,64,128}, L % C == 0, d in {64,128})";
+    case GDN_ERR_PARAM: return "order out of range (0 <= N, S <= C - 1; 63 for C = 128)";
+    case GDN_ERR_DTYPE: return "unsupported dtype";
+    case GDN_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case GDN_ERR_ALIAS: return "an output overlaps an input";
+    case GDN_ERR_HIP: return "HIP runtime error at launch";
+    case GDN_ERR_UNSUPPORTED: return "combination not implemented by this build";
+  }
+  return "unknown status";
+}
+
+int gdn_default_order(int C, int* N, int* S) {
+  if (!N || !S) return GDN_ERR_NULL;
+  switch (C) {
+    case 16: *N = 3; *S = 2; return GDN_OK;
+    case 32: *N = 3; *S = 4; return GDN_OK;
+    case 64: *N = 3; *S = 8; return GDN_OK;
+    case 128: *N = 3; *S = 8; return GDN_OK;
+  }
+  return GDN_ERR_SHAPE;
+}
+
+int gdn_build_A(const void* K, const float* beta, const float* g, void* A, int B, int L, int H,
+                int dk, int C, int k_dtype, int a_dtype, void* stream) {
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk)) return GDN_ERR_SHAPE;
+  if (!fdtype(k_dtype) || !fdtype(a_dtype)) return GDN_ERR_DTYPE;
+  if (n == 0) return GDN_OK;
+  if (!K || !beta || !g || !A) return GDN_ERR_NULL;
+  if (!aligned(K) || !aligned(beta) || !aligned(g) || !aligned(A)) return GDN_ERR_ALIGN;
+  const int64_t tok = (int64_t)B * L * H;
+  const int64_t a_bytes = n * C * C * esize(a_dtype);
+  if (overlap(A, a_bytes, K, tok * dk * esize(k_dtype)) || overlap(A, a_bytes, beta, tok * 4) ||
+      overlap(A, a_bytes, g, tok * 4))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_build_A(K, beta, g, A, B, L, H, dk, C, k_dtype, a_dtype,
+                                        (hipStream_t)stream));
+}
+
+int gdn_chunk_inverse_neumann(const void* A, void* Tinv, int64_t n_tiles, int C, int N, int S,
+                              int dtype, void* stream) {
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (n_tiles == 0) return GDN_OK;
+  if (!A || !Tinv) return GDN_ERR_NULL;
+  if (!aligned(A) || !aligned(Tinv)) return GDN_ERR_ALIGN;
+  const int64_t bytes = n_tiles * C * C * esize(dtype);
+  if (overlap(A, bytes, Tinv, bytes)) return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_neumann(A, Tinv, n_tiles, C, N, S, dtype, (hipStream_t)stream));
+}
+
+int gdn_chunk_inverse_fwdsub(const void* A, void* Tinv, int64_t n_tiles, int C, int dtype,
+                             void* stream) {
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (n_tiles == 0) return GDN_OK;
+  if (!A || !Tinv) return GDN_ERR_NULL;
+  if (!aligned(A) || !aligned(Tinv)) return GDN_ERR_ALIGN;
+  const int64_t bytes = n_tiles * C * C * esize(dtype);
+  if (overlap(A, bytes, Tinv, bytes)) return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_fwdsub(A, Tinv, n_tiles, C, dtype, (hipStream_t)stream));
+}
+
+int gdn_wy_apply(const void* Tinv, const void* K, const void* V, const float* beta, void* W,
+                 void* U, int B, int L, int H, int dk, int dv, int C, int dtype, void* stream) {
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (n == 0) return GDN_OK;
+  if (!Tinv || !K || !V || !beta || !W || !U) return GDN_ERR_NULL;
+  if (!aligned(Tinv) || !aligned(K) || !aligned(V) || !aligned(beta) || !aligned(W) ||
+      !aligned(U))
+    return GDN_ERR_ALIGN;
+  const int64_t tok = (int64_t)B * L * H, es = esize(dtype);
+  const int64_t tb = n * C * C * es, kb = tok * dk * es, vb = tok * dv * es, bb = tok * 4;
+  const void* ins[4] = {Tinv, K, V, beta};
+  const int64_t inb[4] = {tb, kb, vb, bb};
+  for (int i = 0; i < 4; ++i)
+    if (overlap(W, kb, ins[i], inb[i]) || overlap(U, vb, ins[i], inb[i])) return GDN_ERR_ALIAS;
+  if (overlap(W, kb, U, vb)) return GDN_ERR_ALIAS;
+  return hip_status(
+      gdn::launch_wy(Tinv, K, V, beta, W, U, B, L, H, dk, dv, C, dtype, (hipStream_t)stream));
+}
+
+int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
+                       void* U, void* Tinv, int B, int L, int H, int dk, int dv, int C, int N,
+                       int S, int dtype, void* stream) {
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
+  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (n == 0) return GDN_OK;
+  if (!K || !V || !beta || !g || !W || !U) return GDN_ERR_NULL;
+  if (!aligned(K) || !aligned(V) || !aligned(beta) || !aligned(g) || !aligned(W) ||
+      !aligned(U) || (Tinv && !aligned(Tinv)))
+    return GDN_ERR_ALIGN;
+  const int64_t tok = (int64_t)B * L * H, es = esize(dtype);
+  const int64_t kb = tok * dk * es, vb = tok * dv * es, bb = tok * 4, tb = n * C * C * es;
+  const void* ins[4] = {K, V, beta, g};
+  const int64_t inb[4] = {kb, vb, bb, bb};
+  for (int i = 0; i < 4; ++i)
+    if (overlap(W, kb, ins[i], inb[i]) || overlap(U, vb, ins[i], inb[i]) ||
+        overlap(Tinv, tb, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(W, kb, U, vb) || overlap(W, kb, Tinv, tb) || overlap(U, vb, Tinv, tb))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_fused(K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, N, S, dtype,
+                                      (hipStream_t)stream));
+}
+
+int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
+                          void* stream) {
+  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+    return GDN_ERR_SHAPE;
+  if (n_tiles == 0) return GDN_OK;
+  if (!A || !Aq || !eA) return GDN_ERR_NULL;
+  if (!aligned(A) || !aligned(Aq) || !aligned(eA)) return GDN_ERR_ALIGN;
+  const int64_t ab = n_tiles * C * C * 4, qb = n_tiles * C * C, eb = n_tiles * 4;
+  if (overlap(Aq, qb, A, ab) || overlap(eA, eb, A, ab) || overlap(Aq, qb, eA, eb))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_quantize_i8(A, Aq, eA, n_tiles, C, (hipStream_t)stream));
+}
+
+int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                                 float* Tdeq, int64_t n_tiles, int C, int N, int S,
+                                 void* stream) {
+  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+    return GDN_ERR_SHAPE;
+  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (n_tiles == 0) return GDN_OK;
+  if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
+  if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
+    return GDN_ERR_ALIGN;
+  const int64_t qb = n_tiles * C * C, eb = n_tiles * 4, db = n_tiles * C * C * 4;
+  const void* ins[2] = {Aq, eA};
+  const int64_t inb[2] = {qb, eb};
+  for (int i = 0; i < 2; ++i)
+    if (overlap(Tq, qb, ins[i], inb[i]) || overlap(eT, eb, ins[i], inb[i]) ||
+        overlap(Tdeq, db, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
+    return GDN_ERR_ALIAS;
+  return hip_status(
+      gdn::launch_neumann_i8(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, (hipStream_t)stream));
+}
+
+}  // extern "C"

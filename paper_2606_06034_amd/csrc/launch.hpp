@@ -1,0 +1,28 @@
+// launch.hpp -- host-side launchers behind the C ABI (internal).
+// Every launcher assumes validated arguments, enqueues on `st` and returns
+// hipGetLastError() (hipErrorNotSupported for combinations not built).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gdn {
+
+hipError_t launch_neumann(const void* A, void* T, int64_t n_tiles, int C, int N, int S,
+                          int dtype, hipStream_t st);
+hipError_t launch_fwdsub(const void* A, void* T, int64_t n_tiles, int C, int dtype,
+                         hipStream_t st);
+hipError_t launch_build_A(const void* K, const float* beta, const float* g, void* A, int B,
+                          int L, int H, int dk, int C, int k_dtype, int a_dtype, hipStream_t st);
+hipError_t launch_wy(const void* T, const void* K, const void* V, const float* beta, void* W,
+                     void* U, int B, int L, int H, int dk, int dv, int C, int dtype,
+                     hipStream_t st);
+hipError_t launch_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
+                        void* U, void* T, int B, int L, int H, int dk, int dv, int C, int N,
+                        int S, int dtype, hipStream_t st);
+hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
+                              hipStream_t st);
+hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                             float* Tdeq, int64_t n_tiles, int C, int N, int S, hipStream_t st);
+
+}  // namespace gdn

@@ -1,0 +1,151 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments before anything reaches the GPU.
+
+No call here passes validation with a non-zero amount of work, so no kernel
+is launched (there is no GPU in the build container)."""
+
+import os
+import re
+
+import pytest
+
+import paper_2606_06034_amd as g
+
+HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "gdninv.h")
+
+OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP = 0, -1, -2, -3, -4, -5, -6, -7, -8
+P1, P2, P3, P4, P5, P6, P7 = (0x10000 * k for k in range(1, 8))  # aligned fake addresses
+BIG = 1 << 40  # far apart so nothing overlaps unless intended
+
+
+def _declared():
+    src = open(HDR).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(gdn_\w+)\s*\(", src, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert len(names) == 10
+    for n in names:
+        assert hasattr(g.lib, n), n
+    assert sorted(g.abi_symbols()) == names
+
+
+def test_version_and_status_strings():
+    assert g.gdn_abi_version() == 1
+    for code in (OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP, 12345):
+        assert isinstance(g.gdn_status_string(code), str) and g.gdn_status_string(code)
+
+
+def test_default_order():
+    assert g.gdn_default_order(16) == (3, 2)
+    assert g.gdn_default_order(32) == (3, 4)
+    assert g.gdn_default_order(64) == (3, 8)
+    assert g.gdn_default_order(128) == (3, 8)
+    with pytest.raises(g.GdnError):
+        g.gdn_default_order(48)
+    assert g.lib.gdn_default_order(64, None, None) == NULL
+
+
+L = g.lib
+
+
+def test_neumann_validation():
+    f = L.gdn_chunk_inverse_neumann
+    assert f(P1, BIG, 4, 48, 3, 8, 0, None) == SHAPE
+    assert f(P1, BIG, -1, 64, 3, 8, 0, None) == SHAPE
+    assert f(P1, BIG, 1 << 31, 64, 3, 8, 0, None) == SHAPE
+    assert f(P1, BIG, 4, 64, 64, 8, 0, None) == PARAM
+    assert f(P1, BIG, 4, 64, 3, -1, 0, None) == PARAM
+    assert f(P1, BIG, 4, 128, 3, 64, 0, None) == PARAM  # 64-blocks at C = 128
+    assert f(P1, BIG, 4, 64, 3, 8, 2, None) == DTYPE
+    assert f(P1, BIG, 4, 64, 3, 8, 7, None) == DTYPE
+    assert f(None, BIG, 4, 64, 3, 8, 0, None) == NULL
+    assert f(P1, None, 4, 64, 3, 8, 0, None) == NULL
+    assert f(P1 + 4, BIG, 4, 64, 3, 8, 0, None) == ALIGN
+    assert f(P1, P1 + 64, 4, 64, 3, 8, 0, None) == ALIAS
+    assert f(P1, P1, 4, 64, 3, 8, 1, None) == ALIAS
+    # zero tiles: a no-op, even with NULL pointers
+    assert f(None, None, 0, 64, 3, 8, 0, None) == OK
+
+
+def test_fwdsub_validation():
+    f = L.gdn_chunk_inverse_fwdsub
+    assert f(P1, BIG, 4, 8, 0, None) == SHAPE
+    assert f(P1, BIG, 4, 64, 3, None) == DTYPE
+    assert f(None, BIG, 4, 64, 0, None) == NULL
+    assert f(P1, BIG + 8, 4, 64, 0, None) == ALIGN
+    assert f(P1, P1 + 16, 4, 64, 0, None) == ALIAS
+    assert f(None, None, 0, 32, 1, None) == OK
+
+
+def test_build_A_validation():
+    f = L.gdn_build_A
+    # K, beta, g, A, B, L, H, dk, C, kdt, adt, stream
+    assert f(P1, P2, P3, BIG, 1, 100, 4, 128, 64, 1, 1, None) == SHAPE  # L % C
+    assert f(P1, P2, P3, BIG, 1, 128, 4, 96, 64, 1, 1, None) == SHAPE  # dk
+    assert f(P1, P2, P3, BIG, -1, 128, 4, 128, 64, 1, 1, None) == SHAPE
+    assert f(P1, P2, P3, BIG, 1, 128, 4, 128, 64, 2, 1, None) == DTYPE
+    assert f(P1, None, P3, BIG, 1, 128, 4, 128, 64, 1, 1, None) == NULL
+    assert f(P1, P2 + 8, P3, BIG, 1, 128, 4, 128, 64, 1, 1, None) == ALIGN
+    # A overlapping K
+    assert f(BIG, P2, P3, BIG + 4096, 1, 128, 4, 128, 64, 1, 1, None) == ALIAS
+    assert f(None, None, None, None, 0, 128, 4, 128, 64, 1, 1, None) == OK
+    assert f(None, None, None, None, 1, 0, 4, 128, 64, 1, 1, None) == OK
+
+
+def test_wy_validation():
+    f = L.gdn_wy_apply
+    # T, K, V, beta, W, U, B, L, H, dk, dv, C, dtype, stream
+    args = [P1, P2, P3, P4, BIG, 2 * BIG, 1, 128, 4, 128, 128, 64, 1, None]
+    bad = list(args); bad[10] = 32
+    assert f(*bad) == SHAPE
+    bad = list(args); bad[12] = 5
+    assert f(*bad) == DTYPE
+    bad = list(args); bad[4] = None
+    assert f(*bad) == NULL
+    bad = list(args); bad[5] = BIG  # W == U
+    assert f(*bad) == ALIAS
+    bad = list(args); bad[4] = P2  # W == K
+    assert f(*bad) == ALIAS
+
+
+def test_fused_validation():
+    f = L.gdn_chunk_wy_fused
+    # K, V, beta, g, W, U, T, B, L, H, dk, dv, C, N, S, dtype, stream
+    base = [P1, P2, P3, P4, BIG, 2 * BIG, None, 1, 128, 4, 128, 128, 64, 3, 8, 1, None]
+    bad = list(base); bad[13] = 64
+    assert f(*bad) == PARAM
+    bad = list(base); bad[8] = 96
+    assert f(*bad) == SHAPE
+    bad = list(base); bad[3] = None
+    assert f(*bad) == NULL
+    bad = list(base); bad[6] = P1  # Tinv over K
+    assert f(*bad) == ALIAS
+    bad = list(base); bad[6] = 3 * BIG + 4
+    assert f(*bad) == ALIGN
+    zero = list(base); zero[7] = 0
+    zero[0] = zero[1] = None
+    assert f(*zero) == OK
+
+
+def test_int8_validation():
+    q = L.gdn_quantize_tiles_i8
+    assert q(P1, BIG, 2 * BIG, 4, 128, None) == SHAPE
+    assert q(P1, None, 2 * BIG, 4, 64, None) == NULL
+    assert q(P1, P1, 2 * BIG, 4, 64, None) == ALIAS
+    assert q(None, None, None, 0, 64, None) == OK
+    n = L.gdn_chunk_inverse_neumann_i8
+    assert n(P1, P2, BIG, 2 * BIG, None, 4, 64, 64, 8, None) == PARAM
+    assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, None) == NULL
+    assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
+    assert n(None, None, None, None, None, 0, 64, 3, 8, None) == OK
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    A = torch.zeros(2, 64, 64)
+    with pytest.raises(ValueError):
+        g.gdn_chunk_inverse_neumann(A, 3, 8)
+    with pytest.raises(TypeError):
+        g.gdn_chunk_inverse_neumann(A.to(torch.float16), 3, 8)

@@ -1,0 +1,293 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Inputs are seeded (workloads); the oracle computes from exactly the values
+the GPU sees (rounded to the storage dtype, upcast to float64).  Tolerances
+are the stated ones: max abs error <= 1e-5 in fp32 mode and <= 2e-2 in bf16
+mode; W and U scale them by max(1, max |ref|).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import gdn
+
+import paper_2606_06034_amd as G
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def dev(x, dt="f32"):
+    x = np.asarray(x, dtype=np.float32)
+    if dt == "bf16":
+        x = wl.round_to_bf16(x)
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(TDT[dt])
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def stored(x, dt):
+    """The values a tensor of dtype dt holds, as float64."""
+    x = np.asarray(x, dtype=np.float32)
+    return (wl.round_to_bf16(x) if dt == "bf16" else x).astype(np.float64)
+
+
+def gdn_tiles(C, n_heads=2, L=None, stress=False, seed=0):
+    """A tiles [n, C, C] (float64) from the tiny workload or the stress set."""
+    w = wl.workload("tiny")
+    L = L or 4 * max(C, 64)
+    if stress:
+        heads = [wl.gen_stress_head(L, w.dk, C, seed=seed + h) for h in range(n_heads)]
+    else:
+        heads = [wl.gen_head(w.with_(L=L), 0, h, C=C, want_v=False) for h in range(n_heads)]
+    K = wl.as_blhd(*[x[0] for x in heads])
+    beta = wl.as_blhd(*[x[1] for x in heads])
+    g = wl.as_blhd(*[x[2] for x in heads])
+    return gdn.tiles_flat(gdn.build_A(K, beta, g, C))
+
+
+def maxerr(a, b):
+    return float(np.max(np.abs(a - b))) if a.size else 0.0
+
+
+# ---------------------------------------------------------------------------
+# approximate inverse
+
+
+ORDERS = {16: [(3, 2), (3, 1), (3, 3), (0, 5), (2, 0)],
+          32: [(3, 4), (3, 1), (3, 7), (1, 3)],
+          64: [(3, 8), (3, 1), (3, 15), (4, 3), (0, 2)],
+          128: [(3, 8), (3, 1), (3, 15)]}
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+@pytest.mark.parametrize("stress", [False, True])
+def test_neumann_matches_oracle(C, dt, stress):
+    A = stored(gdn_tiles(C, stress=stress), dt)
+    dA = dev(A, dt)
+    for N, S in ORDERS[C]:
+        T = host(G.gdn_chunk_inverse_neumann(dA, N, S))
+        if C == 128:
+            ref = gdn.neumann_inverse_blocked(A, N, S)
+        else:
+            ref = gdn.neumann_inverse(A, N, S)
+        err = maxerr(T, ref)
+        # stress tiles leave the workload range (|T| up to ~7): bf16 rounding
+        # then scales with the magnitude of the result
+        tol = TOL[dt] * (max(1.0, np.max(np.abs(ref))) if stress else 1.0)
+        print(f"C={C} {dt} stress={stress} N={N} S={S} n={A.shape[0]} max|err|={err:.3e} "
+              f"tol={tol:.1e}", flush=True)
+        assert err <= tol, (N, S, err)
+        # structure is exact
+        assert np.all(np.triu(T, 1) == 0)
+        assert np.all(np.diagonal(T, axis1=-2, axis2=-1) == 1)
+
+
+def test_neumann_exact_orders_reach_inverse():
+    """(S + 1)(N + 1) >= C makes T_hat the exact inverse: compare with X."""
+    for C, (N, S) in [(16, (3, 3)), (32, (3, 7)), (64, (3, 15))]:
+        A = stored(gdn_tiles(C, stress=True), "f32")
+        T = host(G.gdn_chunk_inverse_neumann(dev(A), N, S))
+        X = gdn.forward_substitution_inverse(A)
+        assert maxerr(T, X) <= 1e-5
+
+
+def test_neumann_many_tiles_odd_count():
+    """67 tiles (not a multiple of anything) of the bf16 Qwen3.5 workload."""
+    w = wl.workload("qwen35_prefill")
+    K, beta, g, _ = wl.gen_inputs(w.with_(L=67 * 64, H=1), want_v=False)
+    A = stored(gdn.tiles_flat(gdn.build_A(K, beta, g, 64)), "bf16")
+    assert A.shape[0] == 67
+    T = host(G.gdn_chunk_inverse_neumann(dev(A, "bf16"), 3, 8))
+    assert maxerr(T, gdn.neumann_inverse(A, 3, 8)) <= TOL["bf16"]
+
+
+def test_neumann_edge_cases():
+    for C in (16, 32, 64, 128):
+        # A = 0 -> identity, exactly
+        Z = torch.zeros((3, C, C), device="cuda")
+        assert np.array_equal(host(G.gdn_chunk_inverse_neumann(Z, 3, 8 if C > 16 else 2)),
+                              np.broadcast_to(np.eye(C), (3, C, C)))
+        # all-ones strictly lower (GDN sign): exact bidiagonal inverse
+        A1 = np.tril(np.ones((2, C, C)), -1)
+        T = host(G.gdn_chunk_inverse_neumann(dev(A1), 3, 4))
+        assert np.array_equal(T, np.broadcast_to(np.eye(C) - np.eye(C, k=-1), (2, C, C)))
+        # entries on and above the diagonal are ignored
+        A = stored(gdn_tiles(C, n_heads=1), "f32")
+        junk = A + np.triu(np.random.default_rng(C).uniform(-5, 5, A.shape))
+        for dt in ("f32", "bf16"):
+            a = host(G.gdn_chunk_inverse_neumann(dev(stored(A, dt), dt), 3, 4))
+            b = host(G.gdn_chunk_inverse_neumann(dev(stored(junk, dt), dt), 3, 4))
+            assert np.array_equal(a, b)
+    # extreme orders
+    A = stored(gdn_tiles(64), "f32")
+    for N, S in [(63, 0), (0, 63), (63, 63), (1, 1), (0, 0)]:
+        T = host(G.gdn_chunk_inverse_neumann(dev(A), N, S))
+        assert maxerr(T, gdn.neumann_inverse(A, N, S)) <= 1e-5, (N, S)
+    # on the stress set the full-order sums cancel powers up to ~1e3 x |T|
+    # (Section 3.2): fp32 error is relative to the largest power
+    A = stored(gdn_tiles(64, stress=True), "f32")
+    P = np.broadcast_to(np.eye(64), A.shape).copy()
+    big = 1.0
+    for _ in range(63):
+        P = P @ -A
+        big = max(big, np.max(np.abs(P)))
+    for N, S in [(63, 0), (0, 63)]:
+        T = host(G.gdn_chunk_inverse_neumann(dev(A), N, S))
+        assert maxerr(T, gdn.neumann_inverse(A, N, S)) <= 64 * 2.0 ** -24 * 64 * big, (N, S)
+
+
+def test_neumann_deterministic():
+    A = dev(stored(gdn_tiles(64, stress=True), "bf16"), "bf16")
+    a = G.gdn_chunk_inverse_neumann(A, 3, 8)
+    b = G.gdn_chunk_inverse_neumann(A, 3, 8)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# exact inverse by forward substitution
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_fwdsub_matches_exact(C, dt):
+    for stress in (False, True):
+        A = stored(gdn_tiles(C, stress=stress), dt)
+        T = host(G.gdn_chunk_inverse_fwdsub(dev(A, dt)))
+        X = gdn.forward_substitution_inverse(A)
+        tol = TOL[dt] if dt == "bf16" else 1e-5 * max(1.0, np.max(np.abs(X)))
+        err = maxerr(T, X)
+        print(f"fwdsub C={C} {dt} stress={stress} max|err|={err:.3e}", flush=True)
+        assert err <= tol
+        assert np.all(np.triu(T, 1) == 0) and np.all(np.diagonal(T, axis1=-2, axis2=-1) == 1)
+
+
+# ---------------------------------------------------------------------------
+# build A, WY, fused
+
+
+def head_inputs(w, C, n_heads, dt):
+    heads = [wl.gen_head(w, 0, h, C=C) for h in range(n_heads)]
+    K = wl.as_blhd(*[x[0] for x in heads])
+    beta = wl.as_blhd(*[x[1] for x in heads])
+    g = wl.as_blhd(*[x[2] for x in heads])
+    V = wl.as_blhd(*[x[3] for x in heads])
+    return K, beta, g, V
+
+
+@pytest.mark.parametrize("kdt,adt", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_build_A(C, kdt, adt):
+    w = wl.workload("tiny").with_(dtype=kdt, L=4 * max(C, 64))
+    K, beta, g, _ = head_inputs(w, C, 3, kdt)
+    ref = gdn.build_A(K, beta, g, C)
+    A = host(G.gdn_build_A(dev(K, kdt), dev(beta), dev(g), C, a_dtype=TDT[adt]))
+    assert A.shape == ref.shape
+    tol = 1e-5 if adt == "f32" else TOL["bf16"]
+    err = maxerr(A, ref)
+    print(f"build_A C={C} K={kdt} A={adt} max|err|={err:.3e}", flush=True)
+    assert err <= tol
+    assert np.all(np.triu(A) == 0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_wy_apply(C, dt):
+    w = wl.workload("tiny").with_(dtype=dt, L=4 * max(C, 64))
+    K, beta, g, V = head_inputs(w, C, 2, dt)
+    A = gdn.build_A(K, beta, g, C)
+    T = stored(gdn.forward_substitution_inverse(A), dt)
+    Wr, Ur = gdn.wy_apply(T, K, V, beta, C)
+    W, U = G.gdn_wy_apply(dev(T, dt), dev(K, dt), dev(V, dt), dev(beta), C)
+    W, U = host(W), host(U)
+    for got, ref in ((W, Wr), (U, Ur)):
+        tol = TOL[dt] * max(1.0, np.max(np.abs(ref)))
+        err = maxerr(got, ref)
+        print(f"wy C={C} {dt} max|err|={err:.3e} tol={tol:.1e}", flush=True)
+        assert err <= tol
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64])
+def test_fused(C, dt):
+    w = wl.workload("tiny").with_(dtype=dt, L=4 * max(C, 64))
+    K, beta, g, V = head_inputs(w, C, 2, dt)
+    N, S = gdn.default_order(C)
+    A = gdn.build_A(K, beta, g, C)
+    Tr = gdn.neumann_inverse(A, N, S)
+    Wr, Ur = gdn.wy_apply(Tr, K, V, beta, C)
+    W, U, T = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S, want_T=True)
+    T, W, U = host(T), host(W), host(U)
+    assert maxerr(T, Tr) <= TOL[dt]
+    for got, ref in ((W, Wr), (U, Ur)):
+        tol = TOL[dt] * max(1.0, np.max(np.abs(ref)))
+        err = maxerr(got, ref)
+        print(f"fused C={C} {dt} max|err|={err:.3e} tol={tol:.1e}", flush=True)
+        assert err <= tol
+    # without the optional Tinv output
+    W2, U2 = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S)
+    assert np.array_equal(host(W2), W) and np.array_equal(host(U2), U)
+
+
+def test_fused_matches_unfused_composition():
+    """build_A -> neumann -> wy_apply equals the fused kernel (fp32)."""
+    C = 64
+    w = wl.workload("tiny")
+    K, beta, g, V = head_inputs(w, C, 2, "f32")
+    dK, dV, db, dg = dev(K), dev(V), dev(beta), dev(g)
+    A = G.gdn_build_A(dK, db, dg, C)
+    T = G.gdn_chunk_inverse_neumann(A, 3, 8)
+    W1, U1 = G.gdn_wy_apply(T, dK, dV, db, C)
+    W2, U2, T2 = G.gdn_chunk_wy_fused(dK, dV, db, dg, C, 3, 8, want_T=True)
+    assert maxerr(host(T), host(T2)) <= 1e-5
+    assert maxerr(host(W1), host(W2)) <= 1e-5
+    assert maxerr(host(U1), host(U2)) <= 1e-5
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads, sampled tiles
+
+
+def _sampled_check(wname, C=None, n_sample=16, seed=0):
+    w = wl.workload(wname)
+    C = C or w.C
+    N, S = gdn.default_order(C)
+    K, beta, g, V = wl.gen_inputs(w, C=C)
+    dt = w.dtype
+    W, U, T = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S, want_T=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(seed)
+    n = w.B * w.H * (w.L // C)
+    picks = sorted(set(rng.integers(0, n, n_sample).tolist()) | {0, n - 1})
+    worst = 0.0
+    for t in picks:
+        b, h, c = wl.tile_coords(w, t, C)
+        sl = slice(c * C, (c + 1) * C)
+        Kt, bt, gt, Vt = (K[b:b + 1, sl, h:h + 1], beta[b:b + 1, sl, h:h + 1],
+                          g[b:b + 1, sl, h:h + 1], V[b:b + 1, sl, h:h + 1])
+        A = gdn.build_A(Kt, bt, gt, C)
+        Tr = gdn.neumann_inverse(A, N, S)
+        Wr, Ur = gdn.wy_apply(Tr, Kt, Vt, bt, C)
+        Tg = T.view(-1, C, C)[t].float().cpu().numpy()
+        Wg = W[b, sl, h].float().cpu().numpy()
+        Ug = U[b, sl, h].float().cpu().numpy()
+        assert maxerr(Tg, Tr[0, 0, 0]) <= TOL[dt]
+        for got, ref in ((Wg, Wr[0, :, 0]), (Ug, Ur[0, :, 0])):
+            e = maxerr(got, ref)
+            worst = max(worst, e)
+            assert e <= TOL[dt] * max(1.0, np.max(np.abs(ref))), (t, e)
+    print(f"{wname} C={C}: {len(picks)} sampled tiles, worst W/U err {worst:.3e}", flush=True)
+
+
+def test_qwen35_prefill_full_size_sampled():
+    """The benchmarked workload (2048 tiles), in the launch the bench times."""
+    _sampled_check("qwen35_prefill")
