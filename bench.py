@@ -73,7 +73,10 @@ def main():
     n_tiles = w.B * w.H * (w.L // C)
 
     # ---- inputs, resident in HBM before timing
-    K, beta, g, V = wl.gen_inputs(w, C=C)
+    want_v = a.path in ("fused", "unfused")
+    K, beta, g, V = wl.gen_inputs(w, C=C, want_v=want_v)
+    if V is None:
+        V = np.zeros((w.B, w.C, w.H, w.dv), np.float32)  # unused by the timed path
     dev = lambda x, t: torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(t)
     dK, dV = dev(K, dt), dev(V, dt)
     db, dg = dev(beta, torch.float32), dev(g, torch.float32)
@@ -167,7 +170,7 @@ def main():
                      "algorithmic_bytes": bytes_, "algorithmic_flops": flops},
     }
 
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and want_v:
         out["cpu_baseline"] = cpu_baseline(w, C, N, S, a, (K, beta, g, V), dK, dV, db, dg,
                                              torch, G)
     print(json.dumps(out), flush=True)

@@ -32,6 +32,8 @@ CFLAGS = [
     "-I", INCLUDE, "-I", HERE,
     # packed fp32 VALU ops are kept out of every code object
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in architectural VGPRs (no accumulator-register copies)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wno-unused-command-line-argument",
 ]
 

@@ -1,25 +1,29 @@
-// engine.hpp -- the MatMul-only approximate inverse of one C x C tile, held
-// in the registers of one wave (Sections 3.1-3.4 and Algorithm 1 of
-// arXiv 2606.06034), plus the tile load/store helpers.
+// engine.hpp -- the MatMul-only approximate inverse of one C x C tile in the
+// registers of one wave (Sections 3.1-3.4 and Algorithm 1 of arXiv
+// 2606.06034), plus tile load/store helpers.
 //
 // With Lm = -A (strictly lower):
-//   T0 = I + N0,  N0 = M^(N) (Hadamard) sum_{n=1}^{N} Lm^n   (mask keeps i-j <= N)
-//   E  = I - (I + A) T0 = Lm T0 - N0, which vanishes on i - j <= N
-//   T  = T0 sum_{s=0}^{S} E^s = T0 + T0 (E + E^2 + ... + E^S)
+//   T0 = M^(N) (Hadamard) sum_{n=0}^{N} Lm^n          (mask keeps i - j <= N)
+//   E  = I - (I + A) T0 = Lm T0 - (T0 - I), which vanishes on i - j <= N
+//   T  = T0 sum_{s=0}^{S} E^s = T0 + T0 Gs,  Gs = E + E^2 + ... + E^S
 //
-// Schedule on the tile forms of tile16.hpp:
-//   * powers P_n = Lm P_{n-1} in column form, only on the band blocks;
-//   * T0 kept in column form (right factor of Lm T0) and in row form (left
-//     factor of the final product; one identity-MFMA layout change);
-//   * E computed in both forms directly from Lm (row) and T0 (column);
-//     its band i - j <= N is set to its exact value 0, so E^s vanishes
-//     exactly on i - j < s (N + 1) and those blocks are skipped;
-//   * the residual powers run as P_s = E P_{s-1} (column form), the same
-//     powers as Algorithm 1's P E chain;
-//   * the final product T0 G is split as T0 + T0 Gs (Gs = G - I) so only the
-//     small strict part is rounded when the operands are bf16.
-// Operands F are bf16x4 (bf16 mode: every MFMA operand rounded to bf16) or
-// f32x4 (fp32 mode).  Products, sums and the identity parts stay in fp32.
+// Schedule (products are X * Y with X in row pairs, Y in column pairs):
+//   * T0 by Horner, H <- I + Lm H, the identity entering through the MFMA
+//     accumulator and the band mask applied after every step (entries of
+//     Lm H on i - j <= N only read entries of H on the band, so masking
+//     early equals masking the finished sum);
+//   * E = band_{i-j > N}(Lm T0) in both forms: on the band E is exactly 0,
+//     and off the band T0 vanishes so Lm T0 is E there;
+//   * residual powers P_s = E P_{s-1} in column form (the same powers as
+//     Algorithm 1's P E chain), Gs += P_s; E^s vanishes exactly on
+//     i - j < s (N + 1) and those blocks are skipped;
+//   * T = T0 + T0 Gs with T0 entering through the MFMA accumulator.
+// F = bf16x4 rounds every MFMA operand to bf16 (products accumulate in fp32,
+// sums and masks run in fp32); F = f32x4 computes in fp32 throughout.
+// SMALLN: the caller guarantees N <= 15, so T0's band lies in the diagonal
+// and first sub-diagonal blocks and everything beyond is compile-time zero.
+// NC, SC >= 0 fix N and S at compile time (every block skip and mask is then
+// resolved by the compiler); -1 takes them from the runtime arguments.
 #pragma once
 
 #include "tile16.hpp"
@@ -30,43 +34,53 @@ namespace gdn {
 // 4-element global IO
 
 __device__ __forceinline__ f32x4 load4(const float* p) { return *(const f32x4*)p; }
-__device__ __forceinline__ f32x4 load4(const __bf16* p) { return to_f32(*(const bf16x4*)p); }
+__device__ __forceinline__ f32x4 load4(const __bf16* p) {
+  return __builtin_convertvector(*(const bf16x4*)p, f32x4);
+}
 __device__ __forceinline__ void store4(float* p, f32x4 x) { *(f32x4*)p = x; }
-__device__ __forceinline__ void store4(__bf16* p, f32x4 x) { *(bf16x4*)p = to_bf16(x); }
+__device__ __forceinline__ void store4(__bf16* p, f32x4 x) {
+  *(bf16x4*)p = __builtin_convertvector(x, bf16x4);
+}
+__device__ __forceinline__ float load1(const float* p) { return *p; }
+__device__ __forceinline__ float load1(const __bf16* p) { return (float)*p; }
 
-// Lm = -A in row form from a row-major tile with row stride ldr; entries on
-// and above the diagonal are read as 0.
-template <int NB, typename F, typename TIO>
-__device__ __forceinline__ void load_neg_strict_row(const TIO* __restrict__ a, int ldr,
-                                                    F (&LQ)[nlower(NB)]) {
+// Lm = -A of a row-major tile (row stride ldr), both forms, f32 blocks:
+// row form  Lr: lane (g, c) reads 4 consecutive entries of row 16I + c;
+// column form Lc: lane (g, c) reads rows 16I + 4g + v of column 16J + c.
+// Entries on and above the diagonal are taken as 0.
+template <int NB, typename TIO>
+__device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int ldr, Acc<NB>& Lr,
+                                                Acc<NB>& Lc) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J) {
-      f32x4 x = load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g);
+      f32x4 r = load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g);
+      f32x4 q;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) x[v] = (dQ(I, J, v) > 0) ? -x[v] : 0.f;
-      LQ[bidx(I, J)] = Op<F>::from(x);
+      for (int v = 0; v < 4; ++v) q[v] = load1(a + (I * 16 + 4 * g + v) * ldr + J * 16 + c);
+      Lr.a[bidx(I, J)] = band_block<false>(-r, I - J, 1, 16 * NB);
+      Lc.a[bidx(I, J)] = band_block<true>(-q, I - J, 1, 16 * NB);
     }
 }
 
-// Store a unit lower-triangular tile given its strict part in row form:
-// diagonal written as exactly 1, upper triangle as 0.  ldr = row stride.
+// Store a unit lower-triangular tile from its row-form blocks (diagonal
+// written as exactly 1, the upper triangle as 0).  ldr = row stride.
 template <int NB, typename TIO>
-__device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr,
-                                               const f32x4 (&Tr)[nlower(NB)]) {
+__device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr, const Acc<NB>& Tr) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J < NB; ++J) {
       f32x4 x = zero4();
-      if (J <= I) {
-        x = Tr[bidx(I, J)];
+      if (J < I) x = Tr.a[bidx(I, J)];
+      if (J == I) {
+        x = Tr.a[bidx(I, J)];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int d = dQ(I, J, v);
+          const int d = drow(0, v);
           x[v] = d > 0 ? x[v] : (d == 0 ? 1.f : 0.f);
         }
       }
@@ -75,115 +89,126 @@ __device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr,
 }
 
 // ---------------------------------------------------------------------------
-// The approximate inverse.  In: Lm in row form (LQ) and column form (LC).
-// Out: strict lower part of T in row form (Tr); T's unit diagonal is
-// implicit (the caller writes it).
 
-template <int NB, typename F>
-__device__ __forceinline__ void neumann_engine(const F (&LQ)[nlower(NB)],
-                                               const F (&LC)[nlower(NB)], int N, int S,
-                                               f32x4 (&Tr)[nlower(NB)]) {
+template <bool SMALLN>
+__device__ __forceinline__ bool in_t0_band(int m, int N) {
+  if constexpr (SMALLN) {
+    if (m > 1) return false;
+  }
+  return blk_nz(m, 0, N);
+}
+
+// The approximate inverse.  In: Lm as row pairs (LR), column pairs (LC) and
+// f32 column blocks (Lc; only T0's band blocks are read).  Out: Tr, the
+// row-form blocks of T (strict part exact, diagonal blocks carry T0's unit
+// diagonal; callers write the diagonal as 1).
+template <int NB, typename F, bool SMALLN, int NC = -1, int SC = -1>
+__device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<NB>& Lc, int Nrt,
+                                               int Srt, Acc<NB>& Tr) {
   constexpr int C = 16 * NB;
-  constexpr int NL = nlower(NB);
+  const int N = NC >= 0 ? NC : Nrt;
+  const int S = SC >= 0 ? SC : Srt;
 
-  // ---- T0 = I + N0: masked truncated Neumann sum (Sections 3.1, 3.3)
-  f32x4 N0c[NL];
-  F Pc[NL];
+  // ---- T0 = I + (band of Lm + Lm^2 + ... + Lm^N), Horner, column form
+  Acc<NB> H;
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J) {
-      f32x4 x = Op<F>::f32(LC[bidx(I, J)]);
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (dP(I, J, v) > N) x[v] = 0.f;
-      N0c[bidx(I, J)] = x;
-      Pc[bidx(I, J)] = Op<F>::from(x);
-    }
-  for (int n = 2; n <= N; ++n) {
-    f32x4 D[NL];
-    lower_mm<NB, false>(D, LQ, 1, C - 1, Pc, n - 1, N, n, N);
-#pragma unroll
-    for (int I = 0; I < NB; ++I)
-#pragma unroll
-      for (int J = 0; J <= I; ++J) {
-        f32x4 x = D[bidx(I, J)];
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          if (dP(I, J, v) > N) x[v] = 0.f;
-        N0c[bidx(I, J)] += x;
-        Pc[bidx(I, J)] = Op<F>::from(x);
-      }
-  }
-
-  F T0c[NL], T0r[NL];
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      f32x4 x = N0c[bidx(I, J)];
+      f32x4 x = in_t0_band<SMALLN>(I - J, N) ? band_block<true>(Lc.a[bidx(I, J)], I - J, 1, N)
+                                             : zero4();
       if (I == J) x += eye4();
-      T0c[bidx(I, J)] = Op<F>::from(x);
+      H.a[bidx(I, J)] = x;
     }
-  {
-    f32x4 tmp[NL];
-    to_row<NB>(tmp, T0c, 0, N);
-    cvt_all<NB>(T0r, tmp);
-  }
-
-  // ---- E = Lm T0 - N0, exactly 0 on i - j <= N (Section 3.4)
-  F Er[NL];
-  f32x4 Gc[NL];  // strict part of G = sum_{s=0}^{S} E^s, column form
-  {
-    f32x4 D[NL];
-    lower_mm<NB, false>(D, LQ, 1, C - 1, T0c, 0, N, N + 1, C - 1);
+  ColP<NB, F> T0c;
+  to_colp(T0c, H);
+  auto horner_step = [&]() {
+    Acc<NB> D;
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int J = 0; J <= I; ++J) {
-        f32x4 x = D[bidx(I, J)];
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          if (dP(I, J, v) <= N || S < 1) x[v] = 0.f;
-        Gc[bidx(I, J)] = x;
-        Pc[bidx(I, J)] = Op<F>::from(x);
-      }
-    lower_mm<NB, true>(D, LQ, 1, C - 1, T0c, 0, N, N + 1, C - 1);
+      for (int J = 0; J <= I; ++J) D.a[bidx(I, J)] = (I == J) ? eye4() : zero4();
+    mm<NB, false, true>(D, LR, 1, C - 1, T0c, 0, N, 1, N);
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int J = 0; J <= I; ++J) {
-        f32x4 x = D[bidx(I, J)];
+      for (int J = 0; J <= I; ++J)
+        if (in_t0_band<SMALLN>(I - J, N))
+          D.a[bidx(I, J)] = band_block<true>(D.a[bidx(I, J)], I - J, 0, N);
+        else
+          D.a[bidx(I, J)] = zero4();
+    to_colp(T0c, D);
+  };
+  if constexpr (NC >= 0) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-          if (dQ(I, J, v) <= N) x[v] = 0.f;
-        Er[bidx(I, J)] = Op<F>::from(x);
-      }
+    for (int n = 2; n <= NC; ++n) horner_step();
+  } else {
+    for (int n = 2; n <= N; ++n) horner_step();
+  }
+  RowP<NB, F> T0R;
+  {
+    Acc<NB> t;
+    col_to_row(t, T0c, 0, N);
+    to_rowp(T0R, t);
   }
 
-  // ---- residual powers P_s = E P_{s-1}, accumulated into Gs
-  for (int s = 2; s <= S; ++s) {
-    f32x4 D[NL];
-    lower_mm<NB, false>(D, Er, N + 1, C - 1, Pc, (s - 1) * (N + 1), C - 1, s * (N + 1), C - 1);
+  // ---- E = band_{i-j > N}(Lm T0), both forms (Section 3.4)
+  RowP<NB, F> ER;
+  ColP<NB, F> P;
+  Acc<NB> G;  // Gs = E + ... + E^S, column form
+  {
+    Acc<NB> D;
+    mm<NB, true, false>(D, LR, 1, C - 1, T0c, 0, N, N + 1, C - 1);
 #pragma unroll
-    for (int b = 0; b < NL; ++b) {
-      Gc[b] += D[b];
-      Pc[b] = Op<F>::from(D[b]);
-    }
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        D.a[bidx(I, J)] = band_block<false>(D.a[bidx(I, J)], I - J, N + 1, C - 1);
+    to_rowp(ER, D);
+    mm<NB, false, false>(D, LR, 1, C - 1, T0c, 0, N, N + 1, C - 1);
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        G.a[bidx(I, J)] = S >= 1 ? band_block<true>(D.a[bidx(I, J)], I - J, N + 1, C - 1)
+                                 : zero4();
+    to_colp(P, G);
   }
 
-  // ---- T = T0 + T0 Gs, row form
-  F Gf[NL];
-  cvt_all<NB>(Gf, Gc);
-  lower_mm<NB, true>(Tr, T0r, 0, N, Gf, N + 1, C - 1, N + 1, C - 1);
+  // ---- residual powers P_s = E P_{s-1}
+  auto chain_step = [&](int s) {
+    const int plo = (s - 1) * (N + 1), lo = s * (N + 1);
+    Acc<NB> D;
+    mm<NB, false, false>(D, ER, N + 1, C - 1, P, plo, C - 1, lo, C - 1);
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        if (blk_nz(I - J, lo, C - 1)) {
+          G.a[bidx(I, J)] += D.a[bidx(I, J)];
+          pin(G.a[bidx(I, J)]);
+        }
+    to_colp(P, D);
+  };
+  if constexpr (SC >= 0) {
+#pragma unroll
+    for (int s = 2; s <= SC; ++s) chain_step(s);
+  } else {
+    for (int s = 2; s <= S; ++s) chain_step(s);
+  }
+
+  // ---- T = T0 + T0 Gs, row form; T0 (as rounded for the products) enters
+  // through the accumulator
+  ColP<NB, F> GC;
+  to_colp(GC, G);
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J) {
-      f32x4 t0 = Op<F>::f32(T0r[bidx(I, J)]);
-      if (I == J) t0 -= eye4();
-      Tr[bidx(I, J)] += t0;
+      const int p = J >> 1;
+      Tr.a[bidx(I, J)] = (J & 1) ? T0R.r[I][p].hi() : T0R.r[I][p].lo();
     }
+  mm<NB, true, true>(Tr, T0R, 0, N, GC, N + 1, C - 1, N + 1, C - 1);
 }
 
 }  // namespace gdn

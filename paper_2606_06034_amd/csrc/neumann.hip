@@ -9,88 +9,58 @@
 
 namespace gdn {
 
-template <int NB, typename F, typename TIO>
+template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO>
+__device__ __forceinline__ void invert_block(const TIO* __restrict__ a, TIO* __restrict__ t,
+                                             int ldr, int N, int S, Acc<NB>& Tr) {
+  Acc<NB> Lr, Lc;
+  load_neg_strict<NB>(a, ldr, Lr, Lc);
+  RowP<NB, F> LR;
+  to_rowp(LR, Lr);
+  neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
+  store_unit_row<NB>(t, ldr, Tr);
+}
+
+template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO>
 __global__ __launch_bounds__(64) void k_neumann(const TIO* __restrict__ A, TIO* __restrict__ T,
                                                 int N, int S) {
-  constexpr int C = 16 * NB, NL = nlower(NB);
+  constexpr int C = 16 * NB;
   const int64_t tile = blockIdx.x;
-  const TIO* a = A + tile * (C * C);
-  TIO* t = T + tile * (C * C);
-  F LQ[NL], LC[NL];
-  load_neg_strict_row<NB>(a, C, LQ);
-  {
-    f32x4 tmp[NL];
-    to_col<NB>(tmp, LQ, 1, C - 1);
-    cvt_all<NB>(LC, tmp);
-  }
-  f32x4 Tr[NL];
-  neumann_engine<NB>(LQ, LC, N, S, Tr);
-  store_unit_row<NB>(t, C, Tr);
+  Acc<NB> Tr;
+  invert_block<NB, F, SMALLN, NC, SC>(A + tile * (C * C), T + tile * (C * C), C, N, S, Tr);
 }
 
 // ---------------------------------------------------------------------------
 // C = 128 as 2 x 2 blocks of 64 (four 16-blocks each)
 
-template <typename F, typename TIO>
+template <typename F, bool SMALLN, int NC, int SC, typename TIO>
 __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
                                                    TIO* __restrict__ T, int N, int S) {
-  constexpr int C = 128, NB = 4, NL = nlower(NB);
+  constexpr int C = 128, NB = 4;
   const int64_t tile = blockIdx.x;
   const TIO* a = A + tile * (C * C);
   TIO* t = T + tile * (C * C);
   const int g = lane_g(), c = lane_c();
 
-  // T_22 first; keep it (unit lower, row form) as an operand.
-  F X22r[NL];
+  // T_22 (row pairs, unit diagonal): left factor of T_22 M
+  RowP<NB, F> X22;
   {
-    F LQ[NL], LC[NL];
-    load_neg_strict_row<NB>(a + 64 * C + 64, C, LQ);
-    f32x4 tmp[NL];
-    to_col<NB>(tmp, LQ, 1, 63);
-    cvt_all<NB>(LC, tmp);
-    f32x4 Tr[NL];
-    neumann_engine<NB>(LQ, LC, N, S, Tr);
-    store_unit_row<NB>(t + 64 * C + 64, C, Tr);
+    Acc<NB> Tr;
+    invert_block<NB, F, SMALLN, NC, SC>(a + 64 * C + 64, t + 64 * C + 64, C, N, S, Tr);
 #pragma unroll
-    for (int I = 0; I < NB; ++I)
-#pragma unroll
-      for (int J = 0; J <= I; ++J) {
-        f32x4 x = Tr[bidx(I, J)];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int d = dQ(I, J, v);
-          x[v] = d > 0 ? x[v] : (d == 0 ? 1.f : 0.f);
-        }
-        X22r[bidx(I, J)] = Op<F>::from(x);
-      }
+    for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
+    to_rowp(X22, Tr);
   }
-
-  // T_11, as a column-form operand (right factor of A_21 T_11)
-  F X11c[NL];
+  // T_11 (column pairs): right factor of A_21 T_11
+  ColP<NB, F> X11;
   {
-    F LQ[NL], LC[NL];
-    load_neg_strict_row<NB>(a, C, LQ);
-    f32x4 tmp[NL];
-    to_col<NB>(tmp, LQ, 1, 63);
-    cvt_all<NB>(LC, tmp);
-    f32x4 Tr[NL];
-    neumann_engine<NB>(LQ, LC, N, S, Tr);
-    store_unit_row<NB>(t, C, Tr);
-    F X11r[NL];
+    Acc<NB> Tr, Tc;
+    invert_block<NB, F, SMALLN, NC, SC>(a, t, C, N, S, Tr);
 #pragma unroll
-    for (int I = 0; I < NB; ++I)
-#pragma unroll
-      for (int J = 0; J <= I; ++J) {
-        f32x4 x = Tr[bidx(I, J)];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int d = dQ(I, J, v);
-          x[v] = d > 0 ? x[v] : (d == 0 ? 1.f : 0.f);
-        }
-        X11r[bidx(I, J)] = Op<F>::from(x);
-      }
-    to_col<NB>(tmp, X11r, 0, 63);
-    cvt_all<NB>(X11c, tmp);
+    for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
+    RowP<NB, F> X11r;
+    to_rowp(X11r, Tr);
+    row_to_col(Tc, X11r, 0, 63);
+    to_colp(X11, Tc);
   }
   // upper-right 64 x 64 block of the tile is zero
 #pragma unroll
@@ -98,29 +68,30 @@ __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
 #pragma unroll
     for (int J = 0; J < NB; ++J) store4(t + (I * 16 + c) * C + 64 + J * 16 + 4 * g, zero4());
 
-  // M = A_21 T_11 (dense 64 x 64, column form)
-  F Mc[NB * NB];
+  // M = A_21 T_11, dense 4 x 4 blocks, as column pairs of the next product
+  Pair<F> Mp[npair(NB)][NB];
   {
+    f32x4 M[NB][NB];
 #pragma unroll
     for (int I = 0; I < NB; ++I) {
-      F a21[NB];
+      Pair<F> ar[npair(NB)];
 #pragma unroll
-      for (int K = 0; K < NB; ++K)
-        a21[K] = Op<F>::from(load4(a + (64 + I * 16 + c) * C + K * 16 + 4 * g));
+      for (int p = 0; p < npair(NB); ++p)
+        ar[p] = Pair<F>::make(load4(a + (64 + I * 16 + c) * C + 32 * p + 4 * g),
+                              load4(a + (64 + I * 16 + c) * C + 32 * p + 16 + 4 * g));
 #pragma unroll
       for (int J = 0; J < NB; ++J) {
         f32x4 acc = zero4();
 #pragma unroll
-        for (int K = J; K < NB; K += 2) {
-          if (K + 1 < NB)
-            acc = Op<F>::template pair<false>(a21[K], a21[K + 1], X11c[bidx(K, J)],
-                                              X11c[bidx(K + 1, J)], acc);
-          else
-            acc = Op<F>::template one<false>(a21[K], X11c[bidx(K, J)], acc);
-        }
-        Mc[I * NB + J] = Op<F>::from(acc);
+        for (int p = 0; p < npair(NB); ++p)
+          if (2 * p + 1 >= J) acc = Pair<F>::template mma<false>(ar[p], X11.c[p][J], acc);
+        M[I][J] = acc;
       }
     }
+#pragma unroll
+    for (int p = 0; p < npair(NB); ++p)
+#pragma unroll
+      for (int J = 0; J < NB; ++J) Mp[p][J] = Pair<F>::make(M[2 * p][J], M[2 * p + 1][J]);
   }
   // T_21 = -T_22 M (row form), stored
 #pragma unroll
@@ -129,23 +100,34 @@ __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
     for (int J = 0; J < NB; ++J) {
       f32x4 acc = zero4();
 #pragma unroll
-      for (int K = 0; K <= I; K += 2) {
-        if (K + 1 <= I)
-          acc = Op<F>::template pair<true>(X22r[bidx(I, K)], X22r[bidx(I, K + 1)],
-                                           Mc[K * NB + J], Mc[(K + 1) * NB + J], acc);
-        else
-          acc = Op<F>::template one<true>(X22r[bidx(I, K)], Mc[K * NB + J], acc);
-      }
+      for (int p = 0; p < npair(NB); ++p)
+        if (2 * p <= I) acc = Pair<F>::template mma<true>(X22.r[I][p], Mp[p][J], acc);
       store4(t + (64 + I * 16 + c) * C + J * 16 + 4 * g, -acc);
     }
 }
 
 // ---------------------------------------------------------------------------
 
+// Default order of each chunk size (the table of gdn_default_order) runs a
+// kernel with (N, S) fixed at compile time; any other order runs the
+// runtime-order kernel.
+template <int NB> struct DefaultOrder;
+template <> struct DefaultOrder<1> { static constexpr int N = 3, S = 2; };
+template <> struct DefaultOrder<2> { static constexpr int N = 3, S = 4; };
+template <> struct DefaultOrder<4> { static constexpr int N = 3, S = 8; };
+
 template <int NB, typename F, typename TIO>
 static hipError_t run_neumann(const void* A, void* T, int64_t n, int N, int S, hipStream_t st) {
-  hipLaunchKernelGGL((k_neumann<NB, F, TIO>), dim3((unsigned)n), dim3(64), 0, st,
-                     (const TIO*)A, (TIO*)T, N, S);
+  constexpr int DN = DefaultOrder<NB>::N, DS = DefaultOrder<NB>::S;
+  if (N == DN && S == DS)
+    hipLaunchKernelGGL((k_neumann<NB, F, true, DN, DS, TIO>), dim3((unsigned)n), dim3(64), 0, st,
+                       (const TIO*)A, (TIO*)T, N, S);
+  else if (N <= 15)
+    hipLaunchKernelGGL((k_neumann<NB, F, true, -1, -1, TIO>), dim3((unsigned)n), dim3(64), 0, st,
+                       (const TIO*)A, (TIO*)T, N, S);
+  else
+    hipLaunchKernelGGL((k_neumann<NB, F, false, -1, -1, TIO>), dim3((unsigned)n), dim3(64), 0,
+                       st, (const TIO*)A, (TIO*)T, N, S);
   return hipGetLastError();
 }
 
@@ -157,8 +139,15 @@ static hipError_t run_neumann_c(const void* A, void* T, int64_t n, int C, int N,
     case 32: return run_neumann<2, F, TIO>(A, T, n, N, S, st);
     case 64: return run_neumann<4, F, TIO>(A, T, n, N, S, st);
     case 128:
-      hipLaunchKernelGGL((k_neumann128<F, TIO>), dim3((unsigned)n), dim3(64), 0, st,
-                         (const TIO*)A, (TIO*)T, N, S);
+      if (N == 3 && S == 8)
+        hipLaunchKernelGGL((k_neumann128<F, true, 3, 8, TIO>), dim3((unsigned)n), dim3(64), 0, st,
+                           (const TIO*)A, (TIO*)T, N, S);
+      else if (N <= 15)
+        hipLaunchKernelGGL((k_neumann128<F, true, -1, -1, TIO>), dim3((unsigned)n), dim3(64), 0,
+                           st, (const TIO*)A, (TIO*)T, N, S);
+      else
+        hipLaunchKernelGGL((k_neumann128<F, false, -1, -1, TIO>), dim3((unsigned)n), dim3(64),
+                           0, st, (const TIO*)A, (TIO*)T, N, S);
       return hipGetLastError();
   }
   return hipErrorNotSupported;

@@ -12,9 +12,6 @@
 
 namespace gdn {
 
-__device__ __forceinline__ float ld1(const float* p) { return *p; }
-__device__ __forceinline__ float ld1(const __bf16* p) { return (float)*p; }
-
 // Chunk bookkeeping for tile index `tile` of the [B, H, L/C, C, C] layout.
 struct Chunk {
   int b, h, t0;
@@ -44,34 +41,36 @@ __device__ __forceinline__ void load_gates(const float* __restrict__ beta,
   __syncthreads();
 }
 
-// Lower blocks of the chunk Gram matrix K K^T (fp32 accumulation).
-// OUTQ selects the result form.  kb points at (token t0, head h, feature 0).
-template <int NB, bool OUTQ, typename F, typename TK>
-__device__ __forceinline__ void gram_lower(f32x4 (&G)[nlower(NB)], const TK* __restrict__ kb,
-                                           int64_t ldk, int dk) {
+// Lower blocks of the chunk Gram matrix K K^T (fp32 accumulation), in the
+// form OUTQ selects.  kb points at (token t0, head h, feature 0).  Both
+// factors are rows of K: lane (g, c) loads 4 consecutive features of token
+// 16I + c for each 16-feature block.
+template <int NB, int DK, bool OUTQ, typename F, typename TK>
+__device__ __forceinline__ void gram_lower(Acc<NB>& G, const TK* __restrict__ kb, int64_t ldk) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
-  for (int b = 0; b < nlower(NB); ++b) G[b] = zero4();
-  for (int f = 0; f < dk; f += 32) {
-    F k0[NB], k1[NB];
+  for (int b = 0; b < nlower(NB); ++b) G.a[b] = zero4();
+#pragma unroll
+  for (int f = 0; f < DK / 32; ++f) {
+    Pair<F> k[NB];
 #pragma unroll
     for (int I = 0; I < NB; ++I) {
-      const TK* p = kb + (I * 16 + c) * ldk + f + 4 * g;
-      k0[I] = Op<F>::from(load4(p));
-      k1[I] = Op<F>::from(load4(p + 16));
+      const TK* p = kb + (I * 16 + c) * ldk + 32 * f + 4 * g;
+      k[I] = Pair<F>::make(load4(p), load4(p + 16));
     }
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
       for (int J = 0; J <= I; ++J)
-        G[bidx(I, J)] = Op<F>::template pair<OUTQ>(k0[I], k1[I], k0[J], k1[J], G[bidx(I, J)]);
+        G.a[bidx(I, J)] = Pair<F>::template mma<OUTQ>(k[I], k[J], G.a[bidx(I, J)]);
   }
 }
 
-// A from the Gram blocks (in place): form-aware element coordinates.
+// A (times `sign`) from the Gram blocks, in place; ROWFORM selects the
+// element coordinates of the blocks' form.
 template <int NB, bool ROWFORM>
-__device__ __forceinline__ void gate_scale(f32x4 (&G)[nlower(NB)], const float* sb,
-                                           const float* sg, float sign) {
+__device__ __forceinline__ void gate_scale(Acc<NB>& G, const float* sb, const float* sg,
+                                           float sign) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
@@ -81,40 +80,37 @@ __device__ __forceinline__ void gate_scale(f32x4 (&G)[nlower(NB)], const float* 
       for (int v = 0; v < 4; ++v) {
         const int i = ROWFORM ? I * 16 + c : I * 16 + 4 * g + v;
         const int j = ROWFORM ? J * 16 + 4 * g + v : J * 16 + c;
-        const float x = G[bidx(I, J)][v];
-        G[bidx(I, J)][v] = (i > j) ? sign * sb[i] * x * __expf(sg[i] - sg[j]) : 0.f;
+        const float x = G.a[bidx(I, J)][v];
+        G.a[bidx(I, J)][v] = (i > j) ? sign * sb[i] * x * __expf(sg[i] - sg[j]) : 0.f;
       }
 }
 
-// out = T diag(beta) X for one chunk.  Tq: unit lower T in row form;
+// out = T diag(beta) X for one chunk.  TR: unit lower T as row pairs;
 // xb / ob point at (token t0, head h, feature 0) of X and of the output.
-template <int NB, typename F, typename TIO>
-__device__ __forceinline__ void apply_lower(const F (&Tq)[nlower(NB)], const TIO* __restrict__ xb,
-                                            TIO* __restrict__ ob, int64_t ld, int d,
-                                            const float* sb) {
+template <int NB, int D, typename F, typename TIO>
+__device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, const TIO* __restrict__ xb,
+                                            TIO* __restrict__ ob, int64_t ld, const float* sb) {
   const int g = lane_g(), c = lane_c();
-  for (int f = 0; f < d; f += 16) {
-    F y[NB];
 #pragma unroll
-    for (int K = 0; K < NB; ++K) {
-      f32x4 x;
+  for (int f = 0; f < D; f += 16) {
+    Pair<F> y[npair(NB)];
+#pragma unroll
+    for (int p = 0; p < npair(NB); ++p) {
+      f32x4 x0, x1 = zero4();
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int r = K * 16 + 4 * g + v;
-        x[v] = sb[r] * ld1(xb + r * ld + f + c);
+        const int r0 = 32 * p + 4 * g + v, r1 = r0 + 16;
+        x0[v] = sb[r0] * load1(xb + r0 * ld + f + c);
+        if (2 * p + 1 < NB) x1[v] = sb[r1] * load1(xb + r1 * ld + f + c);
       }
-      y[K] = Op<F>::from(x);
+      y[p] = Pair<F>::make(x0, x1);
     }
 #pragma unroll
     for (int I = 0; I < NB; ++I) {
       f32x4 acc = zero4();
 #pragma unroll
-      for (int K = 0; K <= I; K += 2) {
-        if (K + 1 <= I)
-          acc = Op<F>::template pair<true>(Tq[bidx(I, K)], Tq[bidx(I, K + 1)], y[K], y[K + 1], acc);
-        else
-          acc = Op<F>::template one<true>(Tq[bidx(I, K)], y[K], acc);
-      }
+      for (int p = 0; p < npair(NB); ++p)
+        if (2 * p <= I) acc = Pair<F>::template mma<true>(TR.r[I][p], y[p], acc);
       store4(ob + (I * 16 + c) * ld + f + 4 * g, acc);
     }
   }
@@ -123,18 +119,18 @@ __device__ __forceinline__ void apply_lower(const F (&Tq)[nlower(NB)], const TIO
 // ---------------------------------------------------------------------------
 // gdn_build_A
 
-template <int NB, typename F, typename TK, typename TA>
+template <int NB, int DK, typename F, typename TK, typename TA>
 __global__ __launch_bounds__(64) void k_build_A(const TK* __restrict__ K,
                                                 const float* __restrict__ beta,
                                                 const float* __restrict__ g,
-                                                TA* __restrict__ A, int L, int H, int dk) {
-  constexpr int C = 16 * NB, NL = nlower(NB);
+                                                TA* __restrict__ A, int L, int H) {
+  constexpr int C = 16 * NB;
   __shared__ float sb[C], sg[C];
   const int64_t tile = blockIdx.x;
   const Chunk ch(tile, L, H, C);
   load_gates<C>(beta, g, ch, L, H, sb, sg);
-  f32x4 G[NL];
-  gram_lower<NB, true, F>(G, K + ch.row(0, L, H, dk), (int64_t)H * dk, dk);
+  Acc<NB> G;
+  gram_lower<NB, DK, true, F>(G, K + ch.row(0, L, H, DK), (int64_t)H * DK);
   gate_scale<NB, true>(G, sb, sg, 1.f);
   TA* a = A + tile * (C * C);
   const int gg = lane_g(), c = lane_c();
@@ -142,102 +138,108 @@ __global__ __launch_bounds__(64) void k_build_A(const TK* __restrict__ K,
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J < NB; ++J)
-      store4(a + (I * 16 + c) * C + J * 16 + 4 * gg, J <= I ? G[bidx(I, J)] : zero4());
+      store4(a + (I * 16 + c) * C + J * 16 + 4 * gg, J <= I ? G.a[bidx(I, J)] : zero4());
 }
 
 // ---------------------------------------------------------------------------
 // gdn_wy_apply
 
-template <int NB, typename F, typename TIO>
+template <int NB, int DK, int DV, typename F, typename TIO>
 __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO* __restrict__ K,
                                            const TIO* __restrict__ V,
                                            const float* __restrict__ beta, TIO* __restrict__ W,
-                                           TIO* __restrict__ U, int L, int H, int dk, int dv) {
-  constexpr int C = 16 * NB, NL = nlower(NB);
+                                           TIO* __restrict__ U, int L, int H) {
+  constexpr int C = 16 * NB;
   __shared__ float sb[C];
   const int64_t tile = blockIdx.x;
   const Chunk ch(tile, L, H, C);
   load_gates<C>(beta, beta, ch, L, H, sb, nullptr);
   const TIO* t = T + tile * (C * C);
   const int g = lane_g(), c = lane_c();
-  F Tq[NL];
+  Acc<NB> Tq;
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      f32x4 x = load4(t + (I * 16 + c) * C + J * 16 + 4 * g);
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (dQ(I, J, v) < 0) x[v] = 0.f;
-      Tq[bidx(I, J)] = Op<F>::from(x);
-    }
-  apply_lower<NB>(Tq, K + ch.row(0, L, H, dk), W + ch.row(0, L, H, dk), (int64_t)H * dk, dk, sb);
-  apply_lower<NB>(Tq, V + ch.row(0, L, H, dv), U + ch.row(0, L, H, dv), (int64_t)H * dv, dv, sb);
+    for (int J = 0; J <= I; ++J)
+      Tq.a[bidx(I, J)] =
+          band_block<false>(load4(t + (I * 16 + c) * C + J * 16 + 4 * g), I - J, 0, C);
+  RowP<NB, F> TR;
+  to_rowp(TR, Tq);
+  apply_lower<NB, DK>(TR, K + ch.row(0, L, H, DK), W + ch.row(0, L, H, DK), (int64_t)H * DK, sb);
+  apply_lower<NB, DV>(TR, V + ch.row(0, L, H, DV), U + ch.row(0, L, H, DV), (int64_t)H * DV, sb);
 }
 
 // ---------------------------------------------------------------------------
 // gdn_chunk_wy_fused: build A -> approximate inverse -> W, U, on chip
 
-template <int NB, typename F, typename TIO>
+template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO>
 __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               const TIO* __restrict__ V,
                                               const float* __restrict__ beta,
                                               const float* __restrict__ g, TIO* __restrict__ W,
                                               TIO* __restrict__ U, TIO* __restrict__ Tout, int L,
-                                              int H, int dk, int dv, int N, int S) {
-  constexpr int C = 16 * NB, NL = nlower(NB);
+                                              int H, int N, int S) {
+  constexpr int C = 16 * NB;
   __shared__ float sb[C], sg[C];
   const int64_t tile = blockIdx.x;
   const Chunk ch(tile, L, H, C);
   load_gates<C>(beta, g, ch, L, H, sb, sg);
 
-  F LQ[NL], LC[NL];
+  RowP<NB, F> LR;
+  Acc<NB> Lc;
   {
-    f32x4 G[NL];
-    gram_lower<NB, false, F>(G, K + ch.row(0, L, H, dk), (int64_t)H * dk, dk);
-    gate_scale<NB, false>(G, sb, sg, -1.f);  // Lm = -A, column form
-    cvt_all<NB>(LC, G);
-    to_row<NB>(G, LC, 1, C - 1);
-    cvt_all<NB>(LQ, G);
+    gram_lower<NB, DK, false, F>(Lc, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+    gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
+    ColP<NB, F> LC;
+    to_colp(LC, Lc);
+    Acc<NB> r;
+    col_to_row(r, LC, 1, C - 1);
+    to_rowp(LR, r);
   }
-  f32x4 Tr[NL];
-  neumann_engine<NB>(LQ, LC, N, S, Tr);
+  Acc<NB> Tr;
+  neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
   if (Tout) store_unit_row<NB>(Tout + tile * (C * C), C, Tr);
-
-  F Tq[NL];
 #pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      f32x4 x = Tr[bidx(I, J)];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int d = dQ(I, J, v);
-        x[v] = d > 0 ? x[v] : (d == 0 ? 1.f : 0.f);
-      }
-      Tq[bidx(I, J)] = Op<F>::from(x);
-    }
-  apply_lower<NB>(Tq, K + ch.row(0, L, H, dk), W + ch.row(0, L, H, dk), (int64_t)H * dk, dk, sb);
-  apply_lower<NB>(Tq, V + ch.row(0, L, H, dv), U + ch.row(0, L, H, dv), (int64_t)H * dv, dv, sb);
+  for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
+  RowP<NB, F> TR;
+  to_rowp(TR, Tr);
+  apply_lower<NB, DK>(TR, K + ch.row(0, L, H, DK), W + ch.row(0, L, H, DK), (int64_t)H * DK, sb);
+  apply_lower<NB, DV>(TR, V + ch.row(0, L, H, DV), U + ch.row(0, L, H, DV), (int64_t)H * DV, sb);
 }
 
 // ---------------------------------------------------------------------------
 // launchers
 
+#define GDN_DK_SWITCH(dk, BODY)          \
+  switch (dk) {                          \
+    case 64: { constexpr int DK = 64; BODY } \
+    case 128: { constexpr int DK = 128; BODY } \
+  }
+#define GDN_DV_SWITCH(dv, BODY)          \
+  switch (dv) {                          \
+    case 64: { constexpr int DV = 64; BODY } \
+    case 128: { constexpr int DV = 128; BODY } \
+  }
+
+template <int NB, typename F, typename TK, typename TA>
+static hipError_t run_build_A_nb(const void* K, const float* beta, const float* g, void* A,
+                                 int64_t n, int L, int H, int dk, hipStream_t st) {
+  GDN_DK_SWITCH(dk, {
+    hipLaunchKernelGGL((k_build_A<NB, DK, F, TK, TA>), dim3((unsigned)n), dim3(64), 0, st,
+                       (const TK*)K, beta, g, (TA*)A, L, H);
+    return hipGetLastError();
+  })
+  return hipErrorNotSupported;
+}
+
 template <typename F, typename TK, typename TA>
 static hipError_t run_build_A(const void* K, const float* beta, const float* g, void* A,
                               int64_t n, int L, int H, int dk, int C, hipStream_t st) {
   switch (C) {
-#define GDN_CASE(NB)                                                                        \
-  case 16 * NB:                                                                             \
-    hipLaunchKernelGGL((k_build_A<NB, F, TK, TA>), dim3((unsigned)n), dim3(64), 0, st,     \
-                       (const TK*)K, beta, g, (TA*)A, L, H, dk);                            \
-    return hipGetLastError();
-    GDN_CASE(1)
-    GDN_CASE(2)
-    GDN_CASE(4)
-    GDN_CASE(8)
-#undef GDN_CASE
+    case 16: return run_build_A_nb<1, F, TK, TA>(K, beta, g, A, n, L, H, dk, st);
+    case 32: return run_build_A_nb<2, F, TK, TA>(K, beta, g, A, n, L, H, dk, st);
+    case 64: return run_build_A_nb<4, F, TK, TA>(K, beta, g, A, n, L, H, dk, st);
+    case 128: return run_build_A_nb<8, F, TK, TA>(K, beta, g, A, n, L, H, dk, st);
   }
   return hipErrorNotSupported;
 }
@@ -256,21 +258,27 @@ hipError_t launch_build_A(const void* K, const float* beta, const float* g, void
   return hipErrorNotSupported;
 }
 
+template <int NB, typename F, typename TIO>
+static hipError_t run_wy_nb(const void* T, const void* K, const void* V, const float* beta,
+                            void* W, void* U, int64_t n, int L, int H, int dk, int dv,
+                            hipStream_t st) {
+  GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
+    hipLaunchKernelGGL((k_wy<NB, DK, DV, F, TIO>), dim3((unsigned)n), dim3(64), 0, st,
+                       (const TIO*)T, (const TIO*)K, (const TIO*)V, beta, (TIO*)W, (TIO*)U, L, H);
+    return hipGetLastError();
+  }))
+  return hipErrorNotSupported;
+}
+
 template <typename F, typename TIO>
 static hipError_t run_wy(const void* T, const void* K, const void* V, const float* beta,
                          void* W, void* U, int64_t n, int L, int H, int dk, int dv, int C,
                          hipStream_t st) {
   switch (C) {
-#define GDN_CASE(NB)                                                                         \
-  case 16 * NB:                                                                              \
-    hipLaunchKernelGGL((k_wy<NB, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, (const TIO*)T, \
-                       (const TIO*)K, (const TIO*)V, beta, (TIO*)W, (TIO*)U, L, H, dk, dv);  \
-    return hipGetLastError();
-    GDN_CASE(1)
-    GDN_CASE(2)
-    GDN_CASE(4)
-    GDN_CASE(8)
-#undef GDN_CASE
+    case 16: return run_wy_nb<1, F, TIO>(T, K, V, beta, W, U, n, L, H, dk, dv, st);
+    case 32: return run_wy_nb<2, F, TIO>(T, K, V, beta, W, U, n, L, H, dk, dv, st);
+    case 64: return run_wy_nb<4, F, TIO>(T, K, V, beta, W, U, n, L, H, dk, dv, st);
+    case 128: return run_wy_nb<8, F, TIO>(T, K, V, beta, W, U, n, L, H, dk, dv, st);
   }
   return hipErrorNotSupported;
 }
@@ -284,21 +292,42 @@ hipError_t launch_wy(const void* T, const void* K, const void* V, const float* b
   return hipErrorNotSupported;
 }
 
+template <int NB> struct FusedOrder;
+template <> struct FusedOrder<1> { static constexpr int N = 3, S = 2; };
+template <> struct FusedOrder<2> { static constexpr int N = 3, S = 4; };
+template <> struct FusedOrder<4> { static constexpr int N = 3, S = 8; };
+
+template <int NB, typename F, typename TIO>
+static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, const float* g,
+                               void* W, void* U, void* T, int64_t n, int L, int H, int dk,
+                               int dv, int N, int S, hipStream_t st) {
+  constexpr int DN = FusedOrder<NB>::N, DS = FusedOrder<NB>::S;
+  GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
+    if (N == DN && S == DS)
+      hipLaunchKernelGGL((k_fused<NB, DK, DV, F, true, DN, DS, TIO>), dim3((unsigned)n), dim3(64),
+                         0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, (TIO*)T,
+                         L, H, N, S);
+    else if (N <= 15)
+      hipLaunchKernelGGL((k_fused<NB, DK, DV, F, true, -1, -1, TIO>), dim3((unsigned)n),
+                         dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W,
+                         (TIO*)U, (TIO*)T, L, H, N, S);
+    else
+      hipLaunchKernelGGL((k_fused<NB, DK, DV, F, false, -1, -1, TIO>), dim3((unsigned)n),
+                         dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W,
+                         (TIO*)U, (TIO*)T, L, H, N, S);
+    return hipGetLastError();
+  }))
+  return hipErrorNotSupported;
+}
+
 template <typename F, typename TIO>
 static hipError_t run_fused(const void* K, const void* V, const float* beta, const float* g,
                             void* W, void* U, void* T, int64_t n, int L, int H, int dk, int dv,
                             int C, int N, int S, hipStream_t st) {
   switch (C) {
-#define GDN_CASE(NB)                                                                           \
-  case 16 * NB:                                                                                \
-    hipLaunchKernelGGL((k_fused<NB, F, TIO>), dim3((unsigned)n), dim3(64), 0, st,             \
-                       (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, H, \
-                       dk, dv, N, S);                                                          \
-    return hipGetLastError();
-    GDN_CASE(1)
-    GDN_CASE(2)
-    GDN_CASE(4)
-#undef GDN_CASE
+    case 16: return run_fused_nb<1, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
+    case 32: return run_fused_nb<2, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
+    case 64: return run_fused_nb<4, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
   }
   return hipErrorNotSupported;
 }
