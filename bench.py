@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "unfused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=512)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run 10 device-to-device copies of 512 MiB (to scale HBM "
+                         "byte counters) and exit")
     return ap.parse_args()
 
 
@@ -59,6 +62,15 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if a.copy_calibration:
+        src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_per_copy": 512 << 20, "copies": 10}))
+        return
 
     import paper_2606_06034_amd as G
 

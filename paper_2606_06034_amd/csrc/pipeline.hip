@@ -5,8 +5,9 @@
 //   W = T diag(beta) K,  U = T diag(beta) V
 //
 // K/V rows of a chunk are strided by H * d in the [B, L, H, d] layout; every
-// access is a 4-element (8 or 16 byte) run of one token's features (row form)
-// or a 16-lane run of one feature over consecutive lanes (column form).
+// global access is a run of 8 consecutive features of one token (16 bytes in
+// bf16).  Column-form (token-major) fragments of K and V are made on chip by
+// identity MFMAs.
 #include "engine.hpp"
 #include "launch.hpp"
 
@@ -42,28 +43,19 @@ __device__ __forceinline__ void load_gates(const float* __restrict__ beta,
 }
 
 // Lower blocks of the chunk Gram matrix K K^T (fp32 accumulation), in the
-// form OUTQ selects.  kb points at (token t0, head h, feature 0).  Both
-// factors are rows of K: lane (g, c) loads 4 consecutive features of token
-// 16I + c for each 16-feature block.
-template <int NB, int DK, bool OUTQ, typename F, typename TK>
-__device__ __forceinline__ void gram_lower(Acc<NB>& G, const TK* __restrict__ kb, int64_t ldk) {
-  const int g = lane_g(), c = lane_c();
+// form OUTQ selects, from the row pairs of K (load_rows): both factors are
+// rows of K and any feature order serves as the contraction order.
+template <int NB, int DK, bool OUTQ, typename F>
+__device__ __forceinline__ void gram_lower(Acc<NB>& G, const Pair<F> (&kp)[NB][DK / 32]) {
 #pragma unroll
-  for (int b = 0; b < nlower(NB); ++b) G.a[b] = zero4();
+  for (int I = 0; I < NB; ++I)
 #pragma unroll
-  for (int f = 0; f < DK / 32; ++f) {
-    Pair<F> k[NB];
+    for (int J = 0; J <= I; ++J) {
+      f32x4 acc = zero4();
 #pragma unroll
-    for (int I = 0; I < NB; ++I) {
-      const TK* p = kb + (I * 16 + c) * ldk + 32 * f + 4 * g;
-      k[I] = Pair<F>::make(load4(p), load4(p + 16));
+      for (int q = 0; q < DK / 32; ++q) acc = Pair<F>::template mma<OUTQ>(kp[I][q], kp[J][q], acc);
+      G.a[bidx(I, J)] = acc;
     }
-#pragma unroll
-    for (int I = 0; I < NB; ++I)
-#pragma unroll
-      for (int J = 0; J <= I; ++J)
-        G.a[bidx(I, J)] = Pair<F>::template mma<OUTQ>(k[I], k[J], G.a[bidx(I, J)]);
-  }
 }
 
 // A (times `sign`) from the Gram blocks, in place; ROWFORM selects the
@@ -85,35 +77,89 @@ __device__ __forceinline__ void gate_scale(Acc<NB>& G, const float* sb, const fl
       }
 }
 
-// out = T diag(beta) X for one chunk.  TR: unit lower T as row pairs;
-// xb / ob point at (token t0, head h, feature 0) of X and of the output.
+// 16-byte loads of a chunk of X [token][feature] (row stride ld): lane (g, c)
+// gets 8 consecutive features 32q + 8g .. 32q + 8g + 7 of token 16I + c, as
+// one row-form pair over two 16-feature halves.  Within chunk q the half h
+// holds features 32q + 8 (j / 4) + 4h + (j % 4) in block column j, so the
+// same permutation maps MFMA columns back to memory on store.
+template <typename F, typename TIO>
+__device__ __forceinline__ Pair<F> load_row8(const TIO* __restrict__ p);
+template <>
+__device__ __forceinline__ Pair<bf16x4> load_row8<bf16x4, __bf16>(const __bf16* __restrict__ p) {
+  return Pair<bf16x4>{*(const bf16x8*)p};
+}
+template <>
+__device__ __forceinline__ Pair<f32x4> load_row8<f32x4, float>(const float* __restrict__ p) {
+  return Pair<f32x4>{*(const f32x4*)p, *(const f32x4*)(p + 4)};
+}
+__device__ __forceinline__ void store_row8(__bf16* p, f32x4 lo, f32x4 hi) {
+  const bf16x4 a = __builtin_convertvector(lo, bf16x4), b = __builtin_convertvector(hi, bf16x4);
+  *(bf16x8*)p = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+__device__ __forceinline__ void store_row8(float* p, f32x4 lo, f32x4 hi) {
+  *(f32x4*)p = lo;
+  *(f32x4*)(p + 4) = hi;
+}
+
 template <int NB, int D, typename F, typename TIO>
-__device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, const TIO* __restrict__ xb,
-                                            TIO* __restrict__ ob, int64_t ld, const float* sb) {
+__device__ __forceinline__ void load_rows(Pair<F> (&xp)[NB][D / 32], const TIO* __restrict__ xb,
+                                          int64_t ld) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
-  for (int f = 0; f < D; f += 16) {
-    Pair<F> y[npair(NB)];
+  for (int I = 0; I < NB; ++I)
 #pragma unroll
-    for (int p = 0; p < npair(NB); ++p) {
-      f32x4 x0, x1 = zero4();
+    for (int q = 0; q < D / 32; ++q) xp[I][q] = load_row8<F>(xb + (I * 16 + c) * ld + 32 * q + 8 * g);
+}
+
+// out = T' X for one chunk, T' = T diag(beta) as row pairs (beta folded into
+// T's columns), X given by its row-form pairs xp.  Each 16 x 16 block of X
+// is moved to column form by an identity MFMA (X I), then W(I, .) =
+// sum_K T'(I, K) X(K, .) comes out in row form and is stored 8 features per
+// lane.  ob points at (token t0, head h, feature 0) of the output.
+template <int NB, int D, typename F, typename TIO>
+__device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, const Pair<F> (&xp)[NB][D / 32],
+                                            TIO* __restrict__ ob, int64_t ld) {
+  const int g = lane_g(), c = lane_c();
+  const f32x4 e = eye4();
+  const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r0 = 32 * p + 4 * g + v, r1 = r0 + 16;
-        x0[v] = sb[r0] * load1(xb + r0 * ld + f + c);
-        if (2 * p + 1 < NB) x1[v] = sb[r1] * load1(xb + r1 * ld + f + c);
+  for (int q = 0; q < D / 32; ++q) {
+    Pair<F> y[2][npair(NB)];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int p = 0; p < npair(NB); ++p) {
+        const f32x4 a = Pair<F>::template mma<false>(xp[2 * p][q], h ? id1 : id0, zero4());
+        const f32x4 b = (2 * p + 1 < NB)
+                            ? Pair<F>::template mma<false>(xp[2 * p + 1][q], h ? id1 : id0, zero4())
+                            : zero4();
+        y[h][p] = Pair<F>::make(a, b);
       }
-      y[p] = Pair<F>::make(x0, x1);
-    }
 #pragma unroll
     for (int I = 0; I < NB; ++I) {
-      f32x4 acc = zero4();
+      f32x4 acc[2] = {zero4(), zero4()};
 #pragma unroll
-      for (int p = 0; p < npair(NB); ++p)
-        if (2 * p <= I) acc = Pair<F>::template mma<true>(TR.r[I][p], y[p], acc);
-      store4(ob + (I * 16 + c) * ld + f + 4 * g, acc);
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int p = 0; p < npair(NB); ++p)
+          if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(TR.r[I][p], y[h][p], acc[h]);
+      store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
     }
   }
+}
+
+// T diag(beta) as row pairs from the row-form blocks of the unit lower T:
+// value v of lane (g, c) in block (I, J) sits in column 16J + 4g + v.
+template <int NB, typename F>
+__device__ __forceinline__ void scale_cols(RowP<NB, F>& TR, Acc<NB> T, const float* sb) {
+  const int g = lane_g();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) T.a[bidx(I, J)][v] *= sb[16 * J + 4 * g + v];
+  to_rowp(TR, T);
 }
 
 // ---------------------------------------------------------------------------
@@ -130,7 +176,11 @@ __global__ __launch_bounds__(64) void k_build_A(const TK* __restrict__ K,
   const Chunk ch(tile, L, H, C);
   load_gates<C>(beta, g, ch, L, H, sb, sg);
   Acc<NB> G;
-  gram_lower<NB, DK, true, F>(G, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+  {
+    Pair<F> kp[NB][DK / 32];
+    load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+    gram_lower<NB, DK, true>(G, kp);
+  }
   gate_scale<NB, true>(G, sb, sg, 1.f);
   TA* a = A + tile * (C * C);
   const int gg = lane_g(), c = lane_c();
@@ -164,9 +214,17 @@ __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO*
       Tq.a[bidx(I, J)] =
           band_block<false>(load4(t + (I * 16 + c) * C + J * 16 + 4 * g), I - J, 0, C);
   RowP<NB, F> TR;
-  to_rowp(TR, Tq);
-  apply_lower<NB, DK>(TR, K + ch.row(0, L, H, DK), W + ch.row(0, L, H, DK), (int64_t)H * DK, sb);
-  apply_lower<NB, DV>(TR, V + ch.row(0, L, H, DV), U + ch.row(0, L, H, DV), (int64_t)H * DV, sb);
+  scale_cols(TR, Tq, sb);
+  {
+    Pair<F> kp[NB][DK / 32];
+    load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+    apply_lower<NB, DK>(TR, kp, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+  }
+  {
+    Pair<F> vp[NB][DV / 32];
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
+    apply_lower<NB, DV>(TR, vp, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -185,10 +243,12 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
   const Chunk ch(tile, L, H, C);
   load_gates<C>(beta, g, ch, L, H, sb, sg);
 
+  Pair<F> kp[NB][DK / 32];
+  load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
   RowP<NB, F> LR;
   Acc<NB> Lc;
   {
-    gram_lower<NB, DK, false, F>(Lc, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+    gram_lower<NB, DK, false>(Lc, kp);
     gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
     ColP<NB, F> LC;
     to_colp(LC, Lc);
@@ -201,10 +261,12 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
   if (Tout) store_unit_row<NB>(Tout + tile * (C * C), C, Tr);
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
+  Pair<F> vp[NB][DV / 32];
+  load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
   RowP<NB, F> TR;
-  to_rowp(TR, Tr);
-  apply_lower<NB, DK>(TR, K + ch.row(0, L, H, DK), W + ch.row(0, L, H, DK), (int64_t)H * DK, sb);
-  apply_lower<NB, DV>(TR, V + ch.row(0, L, H, DV), U + ch.row(0, L, H, DV), (int64_t)H * DV, sb);
+  scale_cols(TR, Tr, sb);
+  apply_lower<NB, DK>(TR, kp, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+  apply_lower<NB, DV>(TR, vp, U + ch.row(0, L, H, DV), (int64_t)H * DV);
 }
 
 // ---------------------------------------------------------------------------
