@@ -17,11 +17,12 @@ This module fixes them (one reading, applied identically by the GPU path):
     (|acc| <= C * 127^2 < 2^21 for C <= 64), then requantised ("per-power
     rescaling"): s = smallest s >= 0 with rne(max|acc| / 2^s) <= 127,
     q = rne(acc / 2^s), e = e1 + e2 + s.
-  * Sums align their terms at a common exponent e* and add exactly in
-    int32.  e* is the finest exponent present, raised where needed so that no
-    aligned term exceeds 2^23 in magnitude (terms below e* are shifted right
-    with round-half-even).  A term is present when the matrix it comes from
-    is not identically zero (a product is present when both factors are).
+  * Sums run in int32 in the order the terms are produced, at an exponent
+    set by the first term (16 guard bits below an int8 quantum) and raised
+    only when a later term would pass 2^23; terms finer than the running
+    exponent are added with round-half-even (aligned_sum).  A term is present
+    when the matrix it comes from is not identically zero (a product is
+    present when both factors are).
   * The diagonal mask M^(N) is applied to every power before it is
     quantised (in exact arithmetic M (sum L^n) = sum M L^n, and masking first
     keeps the deep sub-diagonal outliers out of every scale).
@@ -112,7 +113,7 @@ def quantize(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 
 
 # ----------------------------------------------------------------------------
-# exact aligned sums
+# exact running sums
 
 
 def _acc_bits(C: int) -> int:
@@ -121,34 +122,39 @@ def _acc_bits(C: int) -> int:
 
 
 def aligned_sum(terms: List[Tuple[np.ndarray, np.ndarray, np.ndarray, int]]):
-    """Exact int32 sum of q_k * 2^(e_k) at a common exponent e*.
+    """Running int32 sum of q_k * 2^(e_k), terms taken in the given order.
 
     terms: list of (q, e, present, bits) with q [..., C, C] int, e [...] int,
     present [...] bool, bits = log2 bound of |q| (7 for int8 codes, 14+log2 C
-    for raw products).  e* = max(min e_k, max(e_k + bits_k) - 23) over the
-    present terms; each present term is shifted to e* (left exactly, or right
-    with round-half-even).  Returns (sum, e*, any_present)."""
+    for raw products).  Per tile, the sum keeps an exponent e_acc:
+      * the first present term sets e_acc = e + bits - 23 (its largest value
+        sits just below 2^23, leaving 16 guard bits under an int8 quantum);
+      * a later present term whose top e + bits would pass e_acc + 23 first
+        rebases the sum to e_acc' = e + bits - 23 (acc = rne(acc / 2^d));
+      * the term is then added exactly at e_acc (shifted left) or, when finer,
+        rounded to it (round-half-even right shift).
+    Absent terms are skipped.  Returns (sum, e_acc, any_present)."""
     shape = terms[0][0].shape[:-2]
-    BIG = np.int64(1 << 40)
-    e_min = np.full(shape, BIG)
-    top = np.full(shape, -BIG)
+    total = np.zeros(terms[0][0].shape, dtype=np.int64)
+    e_acc = np.zeros(shape, dtype=np.int64)
     anyp = np.zeros(shape, dtype=bool)
     for q, e, p, bits in terms:
-        e_min = np.where(p, np.minimum(e_min, e), e_min)
-        top = np.where(p, np.maximum(top, e + bits), top)
-        anyp |= p
-    e_star = np.maximum(e_min, top - ALIGN_BITS)
-    e_star = np.where(anyp, e_star, 0)
-    total = np.zeros(terms[0][0].shape, dtype=np.int64)
-    for q, e, p, bits in terms:
         q = np.asarray(q, np.int64)
-        d = (e - e_star)[..., None, None]
-        left = q << np.maximum(d, 0)
-        right = rne_shift(q, np.maximum(-d, 0))
-        t = np.where(d >= 0, left, right)
+        e = np.asarray(e, np.int64)
+        p = np.asarray(p, bool)
+        top = e + bits - ALIGN_BITS
+        first = p & ~anyp
+        rebase = p & anyp & (top > e_acc)
+        d = np.where(rebase, top - e_acc, 0)
+        total = np.where(rebase[..., None, None], rne_shift(total, d[..., None, None]), total)
+        e_acc = np.where(first | rebase, top, e_acc)
+        sh = (e - e_acc)[..., None, None]
+        t = np.where(sh >= 0, q << np.maximum(sh, 0), rne_shift(q, np.maximum(-sh, 0)))
         total = total + np.where(p[..., None, None], t, 0)
+        anyp |= p
+    e_acc = np.where(anyp, e_acc, 0)
     assert np.all(np.abs(total) < (1 << 31))
-    return total, e_star, anyp
+    return total, e_acc, anyp
 
 
 # ----------------------------------------------------------------------------

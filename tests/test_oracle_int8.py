@@ -69,20 +69,36 @@ def test_requant_smallest_shift():
             assert w == round(Fraction(v, 1 << s))
 
 
-def test_aligned_sum_is_exact_without_cap():
+def test_aligned_sum_is_exact_within_guard_bits():
+    """Terms no finer than 16 bits below the first term's quantum add
+    exactly; the sum carries q * 2^e of every term."""
     rng = np.random.default_rng(3)
     qa = rng.integers(-127, 128, (5, 4, 4))
     qb = rng.integers(-127, 128, (5, 4, 4))
     ea = rng.integers(-12, -4, 5)
-    eb = rng.integers(-12, -4, 5)
+    eb = ea - rng.integers(0, 17, 5)
     p = np.ones(5, bool)
     s, es, _ = qo.aligned_sum([(qa, ea, p, 7), (qb, eb, p, 7)])
+    assert np.all(es == ea - 16)
     for t in range(5):
         for i in range(4):
             for j in range(4):
                 want = Fraction(int(qa[t, i, j])) * Fraction(2) ** int(ea[t]) + \
                     Fraction(int(qb[t, i, j])) * Fraction(2) ** int(eb[t])
                 assert Fraction(int(s[t, i, j])) * Fraction(2) ** int(es[t]) == want
+
+
+def test_aligned_sum_rebases_on_larger_term():
+    """A later term above the running range rebases (rounding the sum) and
+    the result stays within int32 and within one rounding of the exact sum."""
+    qa = np.array([[[100, -3], [7, 1]]])
+    qb = np.array([[[127, 64], [-127, 0]]])
+    ea = np.array([-10]); eb = np.array([0])
+    p = np.ones(1, bool)
+    s, es, _ = qo.aligned_sum([(qa, ea, p, 7), (qb, eb, p, 7)])
+    assert es[0] == 0 + 7 - 23
+    exact = qa[0] * 2.0 ** -10 + qb[0] * 1.0
+    assert np.max(np.abs(s[0] * 2.0 ** float(es[0]) - exact)) <= 2.0 ** float(es[0])
 
 
 # ---------------------------------------------------------------------------
@@ -111,20 +127,25 @@ def _py_nz(M):
 
 
 def _py_sum(terms, C):
-    """terms: (M, e, present, bits)"""
-    pres = [(M, e, b) for (M, e, p, b) in terms if p]
-    if not pres:
-        return [[0] * C for _ in range(C)], 0
-    emin = min(e for _, e, _ in pres)
-    top = max(e + b for _, e, b in pres)
-    es = max(emin, top - 23)
+    """terms: (M, e, present, bits), summed in order with the running-exponent
+    rule (first term sets e = e0 + bits - 23; rebase when a term's top would
+    pass e + 23; finer terms rounded half-even)."""
     out = [[0] * C for _ in range(C)]
-    for M, e, _ in pres:
+    es = None
+    for M, e, p, b in terms:
+        if not p:
+            continue
+        top = e + b - 23
+        if es is None:
+            es = top
+        elif top > es:
+            out = [[_py_rne(v, top - es) for v in row] for row in out]
+            es = top
         for i in range(C):
             for j in range(C):
                 v = M[i][j]
                 out[i][j] += v << (e - es) if e >= es else _py_rne(v, es - e)
-    return out, es
+    return out, (0 if es is None else es)
 
 
 def _py_pipeline(qA, eA, N, S):
