@@ -1,14 +1,468 @@
-// int8.hip -- low-bit (INT8) path.  Placeholder launchers: not built yet.
+// int8.hip -- the low-bit (INT8) path: per-tile quantiser and the integer
+// masked-Neumann + residual inverse (Section 3.5, Appendix G of
+// arXiv 2606.06034), one wave per tile.
+//
+// Arithmetic (identical to the exact-integer reading the library documents):
+//   * a matrix is int8 codes q in [-127, 127] with one exponent e per tile
+//     (value q 2^e); unit lower-triangular matrices keep the identity implicit;
+//   * quantiser: e = smallest integer with max|x| / 2^e <= 127,
+//     q = round-half-even(x / 2^e);
+//   * int8 x int8 products accumulate exactly in int32 (v_mfma_i32_16x16x64_i8)
+//     and are requantised with the smallest round-half-even shift that brings
+//     max|acc| to <= 127 (exponents add);
+//   * sums run in int32 in production order: the first present term sets the
+//     exponent 16 guard bits below its quantum, a later term above 2^23 of
+//     range rebases the sum (round-half-even), finer terms are rounded in;
+//   * the band mask i - j <= N is applied to every power before it is
+//     quantised; E = Lm + Lm N0 - N0 exactly, band set to 0; the residual
+//     powers are P_s = E P_{s-1}; T = N0 + Gs + N0 Gs.
+// Exponents and "matrix is non-zero" flags are wave-uniform (SGPRs).
+//
+// Fragments: a "quad" holds 16 int8 per lane, four 16 x 16 blocks of 4 bytes:
+// row quad R[I] = blocks (I, 0..3) in row form, column quad Cq[J] = blocks
+// (0..3, J) in column form; one MFMA contracts all four k-blocks (zero blocks
+// where K > I or K < J).  C = 16, 32 use the leading one or two blocks.
+#include "tile16.hpp"
 #include "launch.hpp"
 
 namespace gdn {
+namespace i8 {
 
-hipError_t launch_quantize_i8(const float*, int8_t*, int32_t*, int64_t, int, hipStream_t) {
+constexpr int kAlignBits = 23;
+
+struct Quad {
+  i32x4 v;  // dword K = 4 bytes of block K
+};
+
+template <int NB> struct RowQ { Quad r[NB]; };
+template <int NB> struct ColQ { Quad c[NB]; };
+template <int NB> struct AccI { i32x4 a[nlower(NB)]; };
+
+__device__ __forceinline__ i32x4 zero_i4() { return i32x4{0, 0, 0, 0}; }
+
+// 4 int32 in [-128, 127] <-> 4 bytes (value v in byte v)
+__device__ __forceinline__ int pack4(i32x4 x) {
+  return (int)((uint32_t)(x[0] & 0xff) | ((uint32_t)(x[1] & 0xff) << 8) |
+               ((uint32_t)(x[2] & 0xff) << 16) | ((uint32_t)(x[3] & 0xff) << 24));
+}
+__device__ __forceinline__ i32x4 unpack4(int w) {
+  i32x4 r;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) r[v] = (int)(int8_t)(w >> (8 * v));
+  return r;
+}
+
+template <int NB>
+__device__ __forceinline__ i32x4 blki(const AccI<NB>& D, int I, int J) {
+  return (J <= I && I < NB) ? D.a[bidx(I, J)] : zero_i4();
+}
+template <int NB>
+__device__ __forceinline__ void to_rowq(RowQ<NB>& X, const AccI<NB>& D) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) X.r[I].v[K] = pack4(blki(D, I, K));
+}
+template <int NB>
+__device__ __forceinline__ void to_colq(ColQ<NB>& Y, const AccI<NB>& D) {
+#pragma unroll
+  for (int J = 0; J < NB; ++J)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) Y.c[J].v[K] = pack4(blki(D, K, J));
+}
+
+// D = X Y (lower), blocks outside [olo, ohi] set to 0; OUTQ: row-form result.
+template <int NB, bool OUTQ>
+__device__ __forceinline__ void mmi(AccI<NB>& D, const RowQ<NB>& X, const ColQ<NB>& Y, int olo,
+                                    int ohi) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 acc = zero_i4();
+      if (blk_nz(I - J, olo, ohi))
+        acc = OUTQ ? __builtin_amdgcn_mfma_i32_16x16x64_i8(Y.c[J].v, X.r[I].v, acc, 0, 0, 0)
+                   : __builtin_amdgcn_mfma_i32_16x16x64_i8(X.r[I].v, Y.c[J].v, acc, 0, 0, 0);
+      D.a[bidx(I, J)] = acc;
+    }
+}
+
+// identity as quads (row and column quads coincide)
+template <int NB>
+__device__ __forceinline__ void eye_quads(RowQ<NB>& R, ColQ<NB>& Cq) {
+  AccI<NB> e;
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b) e.a[b] = zero_i4();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) e.a[bidx(I, I)][v] = (c == 4 * g + v) ? 1 : 0;
+  to_rowq(R, e);
+  to_colq(Cq, e);
+}
+
+// zero entries outside lo <= i - j <= hi
+template <int NB, bool COLFORM>
+__device__ __forceinline__ void band_i(AccI<NB>& D, int lo, int hi) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      if (!blk_nz(I - J, lo, hi)) {
+        D.a[bidx(I, J)] = zero_i4();
+      } else if (!blk_all_in(I - J, lo, hi)) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int d = COLFORM ? dcol(I - J, v) : drow(I - J, v);
+          if (d < lo || d > hi) D.a[bidx(I, J)][v] = 0;
+        }
+      }
+    }
+}
+
+// round-half-even(y / 2^s) for s >= 0 and |y| < 2^30 (every value here stays
+// below 2^24, so s >= 31 always rounds to 0)
+__device__ __forceinline__ int rne_sh(int y, int s) {
+  if (s <= 0) return y;
+  if (s >= 31) return 0;
+  return (y + (1 << (s - 1)) - 1 + ((y >> s) & 1)) >> s;
+}
+
+__device__ __forceinline__ int wave_max(int x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = max(x, __shfl_xor(x, o));
+  return __builtin_amdgcn_readfirstlane(x);
+}
+
+template <int NB>
+__device__ __forceinline__ int amax_of(const AccI<NB>& D) {
+  int m = 0;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) m = max(m, abs(D.a[b][v]));
+  return wave_max(m);
+}
+
+// smallest s >= 0 with rne(amax / 2^s) <= 127
+__device__ __forceinline__ int shift_for(int amax) {
+  if (amax <= 127) return 0;
+  int s = (32 - __clz(amax)) - 7;
+  if (rne_sh(amax, s) > 127) ++s;
+  return s;
+}
+
+// requantise in place; returns (new exponent, non-zero flag) through refs
+template <int NB>
+__device__ __forceinline__ void requant(AccI<NB>& D, int e_in, int& e_out, bool& nz) {
+  const int amax = amax_of(D);
+  const int s = shift_for(amax);
+  if (s > 0) {
+#pragma unroll
+    for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) D.a[b][v] = rne_sh(D.a[b][v], s);
+  }
+  nz = amax > 0;
+  e_out = nz ? e_in + s : 0;
+}
+
+// exact running int32 sum
+template <int NB> struct RunSum {
+  AccI<NB> acc;
+  int e;
+  bool any;
+};
+template <int NB>
+__device__ __forceinline__ void rs_init(RunSum<NB>& R) {
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b) R.acc.a[b] = zero_i4();
+  R.e = 0;
+  R.any = false;
+}
+template <int NB>
+__device__ __forceinline__ void rs_add(RunSum<NB>& R, const AccI<NB>& t, int et, int bits,
+                                       bool present, bool negate = false) {
+  if (!present) return;
+  const int top = et + bits - kAlignBits;
+  if (!R.any) {
+    R.e = top;
+    R.any = true;
+  } else if (top > R.e) {
+    const int d = top - R.e;
+#pragma unroll
+    for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) R.acc.a[b][v] = rne_sh(R.acc.a[b][v], d);
+    R.e = top;
+  }
+  const int sh = et - R.e;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int x = negate ? -t.a[b][v] : t.a[b][v];
+      R.acc.a[b][v] += sh >= 0 ? (x << sh) : rne_sh(x, -sh);
+    }
+}
+
+template <int NB>
+__device__ __forceinline__ void rs_finish(RunSum<NB>& R, AccI<NB>& q, int& e, bool& nz) {
+  q = R.acc;
+  requant(q, R.any ? R.e : 0, e, nz);
+}
+
+template <int NB>
+__device__ __forceinline__ void unpack_row(AccI<NB>& D, const RowQ<NB>& X) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) D.a[bidx(I, J)] = unpack4(X.r[I].v[J]);
+}
+
+// ---------------------------------------------------------------------------
+
+template <int NB>
+__global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq,
+                                                   const int32_t* __restrict__ eA,
+                                                   int8_t* __restrict__ Tq,
+                                                   int32_t* __restrict__ eT,
+                                                   float* __restrict__ Tdeq, int N, int S) {
+  constexpr int C = 16 * NB;
+  constexpr int ACCB = 14 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |acc| < C * 2^14
+  const int64_t tile = blockIdx.x;
+  const int g = lane_g(), c = lane_c();
+  const int8_t* a = Aq + tile * (C * C);
+
+  RowQ<NB> Iq;
+  ColQ<NB> Ic;
+  eye_quads(Iq, Ic);
+
+  // ---- Lm = -A (row form), strictly lower
+  AccI<NB> Lr;
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      const int w = *(const int*)(a + (I * 16 + c) * C + J * 16 + 4 * g);
+      i32x4 x = unpack4(w);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
+      Lr.a[bidx(I, J)] = x;
+    }
+  const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
+  const bool nzL = amax_of(Lr) > 0;
+  RowQ<NB> LRq;
+  to_rowq(LRq, Lr);
+  ColQ<NB> LCq;
+  {
+    AccI<NB> t;
+    mmi<NB, false>(t, LRq, Ic, 1, C - 1);  // Lm I, column form
+    to_colq(LCq, t);
+  }
+
+  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm), row form
+  RunSum<NB> ns;
+  rs_init(ns);
+  if (N >= 1) {
+    AccI<NB> B = Lr;
+    band_i<NB, false>(B, 1, N);
+    int eB;
+    bool nzB;
+    requant(B, eL, eB, nzB);
+    rs_add(ns, B, eB, 7, nzB);
+    RowQ<NB> Bq;
+    to_rowq(Bq, B);
+    for (int n = 2; n <= N; ++n) {
+      AccI<NB> D;
+      mmi<NB, true>(D, Bq, LCq, n, N);
+      band_i<NB, false>(D, n, N);
+      requant(D, eB + eL, eB, nzB);
+      rs_add(ns, D, eB, 7, nzB);
+      to_rowq(Bq, D);
+    }
+  }
+  AccI<NB> N0r;
+  int eN0;
+  bool nzN0;
+  rs_finish(ns, N0r, eN0, nzN0);
+  RowQ<NB> N0q;
+  to_rowq(N0q, N0r);
+  ColQ<NB> N0c;
+  {
+    AccI<NB> t;
+    mmi<NB, false>(t, N0q, Ic, 0, C - 1);
+    to_colq(N0c, t);
+  }
+
+  // ---- E = Lm + Lm N0 - N0 (row form), band zeroed
+  RowQ<NB> ERq;
+  ColQ<NB> ECq;
+  AccI<NB> Ecol;
+  int eE;
+  bool nzE;
+  {
+    AccI<NB> LN;
+    mmi<NB, true>(LN, LRq, N0c, 1, C - 1);
+    RunSum<NB> es;
+    rs_init(es);
+    rs_add(es, Lr, eL, 7, nzL);
+    rs_add(es, LN, eL + eN0, ACCB, nzL && nzN0);
+    rs_add(es, N0r, eN0, 7, nzN0, true);
+    band_i<NB, false>(es.acc, N + 1, C - 1);
+    AccI<NB> Er;
+    rs_finish(es, Er, eE, nzE);
+    to_rowq(ERq, Er);
+    mmi<NB, false>(Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
+    to_colq(ECq, Ecol);
+  }
+
+  // ---- residual powers P_s = E P_{s-1} (column form), Gs = sum
+  RunSum<NB> gs;
+  rs_init(gs);
+  if (S >= 1) {
+    rs_add(gs, Ecol, eE, 7, nzE);
+    ColQ<NB> Pq = ECq;
+    int eP = eE;
+    bool nzP = nzE;
+    for (int s = 2; s <= S; ++s) {
+      AccI<NB> D;
+      mmi<NB, false>(D, ERq, Pq, 1, C - 1);
+      requant(D, eE + eP, eP, nzP);
+      rs_add(gs, D, eP, 7, nzP);
+      to_colq(Pq, D);
+    }
+  }
+  AccI<NB> Gc;
+  int eG;
+  bool nzG;
+  rs_finish(gs, Gc, eG, nzG);
+  ColQ<NB> GCq;
+  to_colq(GCq, Gc);
+  AccI<NB> Gr;
+  mmi<NB, true>(Gr, Iq, GCq, 1, C - 1);  // row form of Gs (exact codes)
+
+  // ---- T = N0 + Gs + N0 Gs (row form), strict part
+  AccI<NB> Tr;
+  int eTo;
+  bool nzT;
+  {
+    AccI<NB> NG;
+    mmi<NB, true>(NG, N0q, GCq, 1, C - 1);
+    RunSum<NB> ts;
+    rs_init(ts);
+    rs_add(ts, N0r, eN0, 7, nzN0);
+    rs_add(ts, Gr, eG, 7, nzG);
+    rs_add(ts, NG, eN0 + eG, ACCB, nzN0 && nzG);
+    band_i<NB, false>(ts.acc, 1, C - 1);
+    rs_finish(ts, Tr, eTo, nzT);
+  }
+
+  // ---- store
+  int8_t* t = Tq + tile * (C * C);
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J < NB; ++J)
+      *(int*)(t + (I * 16 + c) * C + J * 16 + 4 * g) = J <= I ? pack4(Tr.a[bidx(I, J)]) : 0;
+  if (lane_id() == 0) eT[tile] = eTo;
+  if (Tdeq) {
+    float* td = Tdeq + tile * (C * C);
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J < NB; ++J) {
+        f32x4 x = zero4();
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int d = 16 * (I - J) + c - 4 * g - v;
+          if (J <= I && d > 0) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], eTo);
+          if (d == 0) x[v] = 1.f;
+        }
+        *(f32x4*)(td + (I * 16 + c) * C + J * 16 + 4 * g) = x;
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// quantiser: e = smallest integer with amax / 2^e <= 127, q = rne(x / 2^e)
+
+template <int C>
+__global__ __launch_bounds__(64) void k_quantize_i8(const float* __restrict__ A,
+                                                    int8_t* __restrict__ Aq,
+                                                    int32_t* __restrict__ eA) {
+  constexpr int PER = C * C / 64 / 4;  // float4 per lane
+  const int64_t tile = blockIdx.x;
+  const float* a = A + tile * (C * C);
+  const int l = lane_id();
+  f32x4 x[PER];
+  float m = 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = (k * 64 + l) * 4;
+    x[k] = *(const f32x4*)(a + idx);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = (idx + v) / C, j = (idx + v) % C;
+      if (i <= j) x[k][v] = 0.f;
+      m = fmaxf(m, fabsf(x[k][v]));
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  const float amax = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(m)));
+  int e = 0;
+  if (amax > 0.f) {
+    int p;
+    const float mant = frexpf(amax, &p);
+    e = p - 7 + (mant * 128.f > 127.f ? 1 : 0);
+  }
+  int8_t* q = Aq + tile * (C * C);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    i32x4 r;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) r[v] = (int)rintf(ldexpf(x[k][v], -e));
+    *(int*)(q + (k * 64 + l) * 4) = pack4(r);
+  }
+  if (l == 0) eA[tile] = e;
+}
+
+}  // namespace i8
+
+hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n, int C,
+                              hipStream_t st) {
+  switch (C) {
+    case 16:
+      hipLaunchKernelGGL((i8::k_quantize_i8<16>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+    case 32:
+      hipLaunchKernelGGL((i8::k_quantize_i8<32>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+    case 64:
+      hipLaunchKernelGGL((i8::k_quantize_i8<64>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+  }
   return hipErrorNotSupported;
 }
 
-hipError_t launch_neumann_i8(const int8_t*, const int32_t*, int8_t*, int32_t*, float*, int64_t,
-                             int, int, int, hipStream_t) {
+hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                             float* Tdeq, int64_t n, int C, int N, int S, hipStream_t st) {
+  switch (C) {
+    case 16:
+      hipLaunchKernelGGL((i8::k_neumann_i8<1>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq, eT,
+                         Tdeq, N, S);
+      return hipGetLastError();
+    case 32:
+      hipLaunchKernelGGL((i8::k_neumann_i8<2>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq, eT,
+                         Tdeq, N, S);
+      return hipGetLastError();
+    case 64:
+      hipLaunchKernelGGL((i8::k_neumann_i8<4>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq, eT,
+                         Tdeq, N, S);
+      return hipGetLastError();
+  }
   return hipErrorNotSupported;
 }
 

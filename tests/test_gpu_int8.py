@@ -1,0 +1,222 @@
+"""Bit-exact parity of the INT8 path (through the C ABI) with the integer oracle.
+
+Both sides start from the same float32 A tiles (built by the oracle and
+rounded to float32), so the quantiser takes every rounding decision on the
+same values; from there on everything is integer arithmetic and the codes
+and exponents must agree exactly.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import gdn
+from oracle import int8 as oi
+
+import paper_2606_06034_amd as G
+
+pytestmark = pytest.mark.gpu
+
+ORDERS = {16: [(3, 2), (0, 3), (2, 0), (1, 1), (5, 4)],
+          32: [(3, 4), (0, 2), (3, 0), (2, 7), (6, 3)],
+          64: [(3, 8), (0, 5), (3, 0), (3, 15), (7, 7), (1, 2)]}
+
+
+def f32_tiles(C, L=None, H=2, gate="wide", stress=False, seed=0):
+    """float32 A tiles [n, C, C] of the low-bit workload's distributions."""
+    w = wl.workload("int8")
+    L = L or 4 * max(C, 64)
+    if stress:
+        heads = [wl.gen_stress_head(L, w.dk, C, seed=seed + h) for h in range(H)]
+    else:
+        w = w.with_(L=L, H=H, B=1, gate=gate)
+        heads = [wl.gen_head(w, 0, h, C=C, want_v=False) for h in range(H)]
+    K = wl.as_blhd(*[x[0] for x in heads])
+    beta = wl.as_blhd(*[x[1] for x in heads])
+    g = wl.as_blhd(*[x[2] for x in heads])
+    return gdn.tiles_flat(gdn.build_A(K, beta, g, C)).astype(np.float32)
+
+
+def random_codes(n, C, seed, density=1.0, emin=-12, emax=2):
+    """Random strictly lower int8 codes (dense or sparse) and exponents."""
+    rng = np.random.default_rng([seed, C])
+    q = rng.integers(-127, 128, size=(n, C, C))
+    if density < 1.0:
+        q = np.where(rng.random((n, C, C)) < density, q, 0)
+    q = np.tril(q, -1)
+    e = rng.integers(emin, emax + 1, size=n)
+    return q.astype(np.int64), e.astype(np.int64)
+
+
+def to_dev(x, dt):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dt).to("cuda")
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def run_engine(qA, eA, N, S, want_deq=True):
+    out = G.gdn_chunk_inverse_neumann_i8(to_dev(qA, torch.int8), to_dev(eA, torch.int32),
+                                         N, S, want_deq=want_deq)
+    return [host(t) for t in out]
+
+
+def check_engine(qA, eA, N, S, label):
+    qT, eT, Td = run_engine(qA, eA, N, S)
+    rq, re, _ = oi.neumann_inverse_int8(qA, eA, N, S)
+    bad = np.flatnonzero(np.any(qT.astype(np.int64) != rq, axis=(-1, -2)) |
+                         (eT.astype(np.int64) != re))
+    print(f"{label} N={N} S={S} n={qA.shape[0]} mismatching tiles={bad.size}", flush=True)
+    assert bad.size == 0, (label, N, S, bad[:8])
+    ref_deq = oi.dequant_unit(rq, re).astype(np.float32)
+    assert np.array_equal(Td, ref_deq)
+
+
+# ---------------------------------------------------------------------------
+# quantiser
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("src", ["workload", "default_gate", "stress"])
+def test_quantize_bit_exact(C, src):
+    A = f32_tiles(C, stress=(src == "stress"), gate="default" if src == "default_gate" else "wide")
+    Aq, eA = G.gdn_quantize_tiles_i8(to_dev(A, torch.float32))
+    rq, re = oi.quantize(A)
+    print(f"quantize C={C} {src} n={A.shape[0]}", flush=True)
+    assert np.array_equal(host(Aq).astype(np.int64), rq)
+    assert np.array_equal(host(eA).astype(np.int64), re)
+
+
+def test_quantize_reads_only_strict_lower():
+    C = 32
+    A = f32_tiles(C)
+    rng = np.random.default_rng(5)
+    junk = A + np.triu(rng.standard_normal(A.shape).astype(np.float32) * 100.0)
+    Aq, eA = G.gdn_quantize_tiles_i8(to_dev(junk, torch.float32))
+    rq, re = oi.quantize(A)
+    assert np.array_equal(host(Aq).astype(np.int64), rq)
+    assert np.array_equal(host(eA).astype(np.int64), re)
+
+
+def test_quantize_edge_values():
+    """Zero tiles, a tile whose max sits exactly on a power of two, a tile
+    whose max rounds past 127 at the first exponent, half-way codes and
+    tiny / large magnitudes."""
+    C = 16
+    tiles = np.zeros((6, C, C), np.float32)
+    tiles[1, 5, 2] = 1.0                      # amax a power of two
+    tiles[2, 9, 0] = 127.6 / 128.0            # 127.6 -> needs the next exponent
+    tiles[2, 3, 1] = 0.5 / 128.0
+    tiles[3, 1, 0] = 127.0
+    tiles[3, 2, 0] = 2.5                      # half-way code at e = 0 -> 2
+    tiles[3, 2, 1] = -3.5                     # -> -4
+    tiles[4, 7, 3] = 3e-30
+    tiles[4, 8, 3] = -1.7e-30
+    tiles[5, 15, 0] = 6e30
+    tiles[5, 15, 14] = 1e29
+    Aq, eA = G.gdn_quantize_tiles_i8(to_dev(tiles, torch.float32))
+    rq, re = oi.quantize(tiles)
+    assert np.array_equal(host(Aq).astype(np.int64), rq)
+    assert np.array_equal(host(eA).astype(np.int64), re)
+    assert host(eA)[0] == 0 and np.all(host(Aq)[0] == 0)
+
+
+# ---------------------------------------------------------------------------
+# integer inverse
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("src", ["workload", "stress", "random_dense", "random_sparse"])
+def test_neumann_i8_bit_exact(C, src):
+    if src.startswith("random"):
+        qA, eA = random_codes(48, C, seed=11 if src == "random_dense" else 12,
+                              density=1.0 if src == "random_dense" else 0.08)
+    else:
+        qA, eA = oi.quantize(f32_tiles(C, stress=(src == "stress")))
+    for N, S in ORDERS[C]:
+        check_engine(qA, eA, N, S, f"C={C} {src}")
+
+
+def test_neumann_i8_extreme_orders():
+    for C in (16, 32, 64):
+        qA, eA = oi.quantize(f32_tiles(C, stress=True, H=1))
+        for N, S in [(C - 1, 0), (0, C - 1), (C - 1, C - 1)]:
+            check_engine(qA, eA, N, S, f"C={C} extreme")
+
+
+def test_neumann_i8_edge_tiles():
+    for C in (16, 32, 64):
+        qA = np.zeros((5, C, C), np.int64)
+        eA = np.zeros(5, np.int64)
+        qA[1, C - 1, 0] = 127                 # one deep entry only
+        eA[1] = -3
+        qA[2, 1, 0] = -127                    # one sub-diagonal entry
+        qA[3] = np.tril(np.full((C, C), 127), -1)   # all-max codes
+        eA[3] = -9
+        qA[4] = np.tril(np.full((C, C), -1), -1)
+        eA[4] = 40
+        for N, S in [(3, 2), (0, 1), (3, 0)]:
+            check_engine(qA, eA, N, S, f"C={C} edge")
+        qT, eT, Td = run_engine(qA[:1], eA[:1], 3, 2)
+        assert np.all(qT == 0) and eT[0] == 0 and np.array_equal(Td[0], np.eye(C, dtype=np.float32))
+
+
+def test_i8_pipeline_many_tiles_odd_count():
+    """Quantiser then engine on 67 tiles, both on the GPU, as one chain."""
+    A = f32_tiles(64, L=67 * 64, H=1)
+    assert A.shape[0] == 67
+    Aq, eA = G.gdn_quantize_tiles_i8(to_dev(A, torch.float32))
+    qT, eT = G.gdn_chunk_inverse_neumann_i8(Aq, eA, 3, 8)
+    rqA, reA = oi.quantize(A)
+    rq, re, _ = oi.neumann_inverse_int8(rqA, reA, 3, 8)
+    assert np.array_equal(host(qT).astype(np.int64), rq)
+    assert np.array_equal(host(eT).astype(np.int64), re)
+
+
+def test_i8_deterministic():
+    qA, eA = random_codes(40, 64, seed=21)
+    a = run_engine(qA, eA, 3, 8)
+    b = run_engine(qA, eA, 3, 8)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_i8_output_without_dequant():
+    qA, eA = oi.quantize(f32_tiles(32, H=1))
+    qT, eT = run_engine(qA, eA, 3, 4, want_deq=False)
+    rq, re, _ = oi.neumann_inverse_int8(qA, eA, 3, 4)
+    assert np.array_equal(qT.astype(np.int64), rq) and np.array_equal(eT.astype(np.int64), re)
+
+
+def test_i8_full_size_sampled():
+    """Low-bit workload at full size (B=4, H=32, L=16384, C=64: 32768 tiles)
+    in one launch of each kernel, compared tile by tile on a sample."""
+    w = wl.workload("int8")
+    C = w.C
+    nc = w.L // C
+    A = np.empty((w.B * w.H * nc, C, C), np.float32)
+    for b in range(w.B):
+        for h in range(w.H):
+            K, beta, g, _ = wl.gen_head(w, b, h, want_v=False)
+            t0 = wl.tile_index(w, b, h, 0)
+            A[t0:t0 + nc] = gdn.tiles_flat(
+                gdn.build_A(K[None, :, None], beta[None, :, None], g[None, :, None], C))
+    print(f"int8 full size: {A.shape[0]} tiles generated", flush=True)
+    Aq, eA = G.gdn_quantize_tiles_i8(to_dev(A, torch.float32))
+    N, S = G.gdn_default_order(C)
+    qT, eT, Td = G.gdn_chunk_inverse_neumann_i8(Aq, eA, N, S, want_deq=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(77)
+    idx = np.sort(np.concatenate([[0, A.shape[0] - 1],
+                                  rng.choice(A.shape[0], 382, replace=False)]))
+    idx_t = torch.from_numpy(idx).to("cuda")
+    rqA, reA = oi.quantize(A[idx])
+    assert np.array_equal(host(Aq[idx_t]).astype(np.int64), rqA)
+    assert np.array_equal(host(eA[idx_t]).astype(np.int64), reA)
+    rq, re, _ = oi.neumann_inverse_int8(rqA, reA, N, S)
+    assert np.array_equal(host(qT[idx_t]).astype(np.int64), rq)
+    assert np.array_equal(host(eT[idx_t]).astype(np.int64), re)
+    assert np.array_equal(host(Td[idx_t]), oi.dequant_unit(rq, re).astype(np.float32))
