@@ -1,7 +1,7 @@
 """Benchmark of the chunk-wise Gated DeltaNet inverse path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--C C]
-                    [--path fused|inverse|fwdsub|unfused] [--no-cpu-baseline]
+                    [--path fused|inverse|fwdsub|unfused|int8] [--no-cpu-baseline]
 
 A step is one pass of the hot path over one batch of synthetic inputs
 already resident in HBM.  The default workload is the Qwen3.5-shaped prefill
@@ -12,6 +12,11 @@ Prints ONE JSON line: throughput in chunk inverses per second, the roofline
 of the dominant kernel (timed with HIP events on the stream it runs on), and
 the CPU oracle timed on a bounded sample of the same workload together with
 the GPU's max abs error against it on that sample.
+
+--path int8 runs the low-bit path (default workload "int8": B=4, H=32,
+L=16384, C=64, wide gates): build A in fp32 -> per-tile INT8 quantiser ->
+integer inverse T_hat(3, 8); its roofline is that of the integer inverse
+kernel, timed on its own.
 """
 
 from __future__ import annotations
@@ -32,6 +37,7 @@ import workloads as wl  # noqa: E402
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0   # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3    # dense fp32 MFMA
+INT8_PEAK_TOPS = 5000.0     # dense int8 MFMA
 METRIC = "C×C chunk inverses/sec + TFLOP/s vs MFMA peak; max abs err vs fp64 oracle"
 
 
@@ -44,9 +50,13 @@ def parse():
     ap.add_argument("--C", type=int, default=None)
     ap.add_argument("--N", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
-    ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "unfused"])
+    ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "unfused", "int8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=512)
+    ap.add_argument("--error-grid", action="store_true",
+                    help="instead of timing: max |T_hat(N, S) - X| and per-tile SNR for "
+                         "N = 1..6, S = 0..16 against the exact inverse X (fp32 forward "
+                         "substitution on the GPU), workload and stress tiles, fp32 and bf16")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 10 device-to-device copies of 512 MiB (to scale HBM "
                          "byte counters) and exit")
@@ -74,6 +84,12 @@ def main():
 
     import paper_2606_06034_amd as G
 
+    if a.error_grid:
+        print(json.dumps(error_grid(a, G, torch)), flush=True)
+        return
+
+    if a.path == "int8" and a.workload == "qwen35_prefill" and "--workload" not in sys.argv:
+        a.workload = "int8"
     w = wl.workload(a.workload)
     C = a.C or w.C
     w = w.with_(C=C)
@@ -106,6 +122,16 @@ def main():
             G.gdn_wy_apply(dT, dK, dV, db, C, W=dW, U=dU)
     elif a.path == "inverse":
         step = lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT)
+    elif a.path == "int8":
+        dA32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
+        dAq = torch.empty(dA32.shape, dtype=torch.int8, device="cuda")
+        deA = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
+        dTq, deT = torch.empty_like(dAq), torch.empty_like(deA)
+
+        def step():
+            G.gdn_build_A(dK, db, dg, C, A=dA32)
+            G.gdn_quantize_tiles_i8(dA32, Aq=dAq, eA=deA)
+            G.gdn_chunk_inverse_neumann_i8(dAq, deA, N, S, Tq=dTq, eT=deT)
     else:
         step = lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT)
 
@@ -124,6 +150,13 @@ def main():
     ev_ms = e0.elapsed_time(e1) / a.steps  # HIP-event time per step (one launch for fused/inverse/fwdsub)
     ms_per_step = wall * 1e3 / a.steps
     value = n_tiles / (ms_per_step * 1e-3)
+    if a.path == "int8":  # the integer inverse kernel alone, same stream
+        e0.record(stream)
+        for _ in range(a.steps):
+            G.gdn_chunk_inverse_neumann_i8(dAq, deA, N, S, Tq=dTq, eT=deT)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        step_ms, ev_ms = ev_ms, e0.elapsed_time(e1) / a.steps
 
     # ---- algorithmic work per launch (measurement section)
     f_inv = (N + S) * 2 * C ** 3 * n_tiles  # dense-equivalent, the paper's product count
@@ -152,6 +185,16 @@ def main():
         flops = n_tiles * (C ** 3 - C) // 3  # sum over i > j of (i - j) FMAs = (C^3 - C) / 6
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
         kernel = "k_fwdsub"
+    elif a.path == "int8":
+        bytes_ = n_tiles * (C * C * 2 + 8)
+        flops = (N + S) * 2 * C ** 3 * n_tiles  # int8 ops of the N + S products
+        if flops / bytes_ >= INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+            bound, peak, unit = "mfma", INT8_PEAK_TOPS, "TOP/s"
+            achieved = flops / (ev_ms * 1e-3) / 1e12
+        else:
+            bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
+            achieved = bytes_ / (ev_ms * 1e-3) / 1e9
+        kernel = "k_neumann_i8"
     else:
         bytes_ = None
         flops = f_inv
@@ -184,7 +227,13 @@ def main():
                      "algorithmic_bytes": bytes_, "algorithmic_flops": flops},
     }
 
-    if not a.no_cpu_baseline and want_v:
+    if a.path == "int8":
+        out["config"]["step_ms_build_quantize_inverse"] = round(step_ms, 6)
+        out["dtype"] = "i8"
+        if not a.no_cpu_baseline:
+            out["cpu_baseline"] = cpu_baseline_int8(w, C, N, S, a, (K, beta, g), dTq, deT,
+                                                    torch, G)
+    elif not a.no_cpu_baseline and want_v:
         out["cpu_baseline"] = cpu_baseline(w, C, N, S, a, (K, beta, g, V), dK, dV, db, dg,
                                              torch, G)
     print(json.dumps(out), flush=True)
@@ -262,6 +311,94 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
             "sample": f"{tiles} tiles ({len(heads)} heads x {nc} chunks) of {w.name}: "
                       f"build A + T_hat({N},{S}) + W/U in float64 numpy, {secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": err}
+
+
+def error_grid(a, G, torch):
+    """Approximation error of T_hat(N, S) against X = (I + A)^-1 per order.
+
+    Tiles: the first two heads of the sweep workload at each C, and two
+    stress heads (shared key direction, slow decay; |A| up to ~0.5).  A is
+    built on the GPU in fp32; X is the fp32 forward substitution of that A
+    (within ~1e-7 of the exact inverse, the floor of every figure here);
+    bf16 mode inverts A rounded to bf16.  Per (C, set, dtype, N, S): max abs
+    error over tiles and the per-tile SNR 10 log10(|X|_F^2 / |X - T_hat|_F^2),
+    mean and worst."""
+    Cs = [a.C] if a.C else [16, 32, 64, 128]
+    out = {"metric": "approximation error of T_hat(N, S) vs exact inverse", "grid": []}
+    for C in Cs:
+        w = wl.workload("sweep").with_(C=C, B=1, H=2)
+        sets = {"workload": wl.gen_inputs(w, C=C, want_v=False)[:3]}
+        heads = [wl.gen_stress_head(4096, w.dk, C, seed=900 + h) for h in range(2)]
+        sets["stress"] = tuple(wl.as_blhd(*[x[i] for x in heads]) for i in range(3))
+        lim = (64 if C == 128 else C) - 1
+        for name, (K, beta, g) in sets.items():
+            dK = torch.from_numpy(np.ascontiguousarray(K)).to("cuda")
+            db = torch.from_numpy(np.ascontiguousarray(beta)).to("cuda")
+            dg = torch.from_numpy(np.ascontiguousarray(g)).to("cuda")
+            A32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
+            X = G.gdn_chunk_inverse_fwdsub(A32).double()
+            xn = (X ** 2).sum(dim=(-1, -2))
+            for dtn, A in (("f32", A32), ("bf16", A32.to(torch.bfloat16))):
+                for N in range(1, 7):
+                    for S in range(0, 17):
+                        if N > lim or S > lim:
+                            continue
+                        T = G.gdn_chunk_inverse_neumann(A, N, S).double()
+                        d = T - X
+                        en = (d ** 2).sum(dim=(-1, -2))
+                        snr = 10 * torch.log10(xn / en.clamp_min(1e-300))
+                        out["grid"].append({
+                            "C": C, "set": name, "dtype": dtn, "N": N, "S": S,
+                            "tiles": int(T.numel() // (C * C)),
+                            "max_abs_err": float(d.abs().max()),
+                            "snr_db_mean": round(float(snr.mean()), 2),
+                            "snr_db_worst": round(float(snr.min()), 2)})
+    return out
+
+
+def _threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
+    """The integer oracle on the first `cpu_sample_tiles` tiles: build A in
+    float64, round to float32, quantise, integer T_hat.  Reports the GPU's
+    dequantised T_hat against it (the GPU builds A in fp32 itself, so an
+    A entry a rounding apart can move a code: this is an error figure, the
+    bit-exact checks live in the tests) and both against the exact inverse."""
+    from oracle import gdn
+    from oracle import int8 as oi
+
+    nc = w.L // C
+    want = max(1, a.cpu_sample_tiles)
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)][:max(1, -(-want // nc))]
+    K, beta, g = host_inputs
+    t0 = time.perf_counter()
+    Ks = np.stack([K[b, :, h] for b, h in heads], 1)[None]
+    bs = np.stack([beta[b, :, h] for b, h in heads], 1)[None]
+    gs = np.stack([g[b, :, h] for b, h in heads], 1)[None]
+    A = gdn.build_A(Ks, bs, gs, C).astype(np.float32)
+    qA, eA = oi.quantize(A)
+    qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S)
+    secs = time.perf_counter() - t0
+    Tr = oi.dequant_unit(qT, eT)[0]
+    X = gdn.forward_substitution_inverse(A.astype(np.float64))[0]
+    torch.cuda.synchronize()
+    Tg = np.stack([oi.dequant_unit(dTq[b, h].cpu().numpy().astype(np.int64),
+                                   deT.view(w.B, w.H, nc)[b, h].cpu().numpy().astype(np.int64))
+                   for b, h in heads], 0)
+    tiles = Tr.shape[0] * Tr.shape[1]
+    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": _threads(),
+            "kind": "oracle",
+            "sample": f"{tiles} tiles ({len(heads)} heads x {nc} chunks) of {w.name}: "
+                      f"build A + INT8 quantiser + integer T_hat({N},{S}), numpy, {secs:.2f} s",
+            "max_abs_err_gpu_vs_oracle": {"T": float(np.max(np.abs(Tg - Tr)))},
+            "max_abs_err_vs_exact_inverse": {"gpu": float(np.max(np.abs(Tg - X))),
+                                             "oracle": float(np.max(np.abs(Tr - X)))}}
 
 
 if __name__ == "__main__":

@@ -80,9 +80,13 @@ _FDT = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}
 _TDT = {GDN_F32: torch.float32, GDN_BF16: torch.bfloat16}
 
 
-def _dev(t: torch.Tensor, name: str, dtype=None) -> int:
+def _dev(t: torch.Tensor, name: str, dtype=None, numel: Optional[int] = None) -> int:
+    """Device pointer of a contiguous tensor, after checking its dtype and
+    element count (the C ABI takes sizes from the shape arguments alone)."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements (got {t.numel()})")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be a device tensor (got {t.device})")
     if not t.is_contiguous():
@@ -119,9 +123,11 @@ def gdn_build_A(K: torch.Tensor, beta: torch.Tensor, g: torch.Tensor, C: int,
     adt = _FDT[a_dtype] if a_dtype is not None else (_fdtype(A, "A") if A is not None else kdt)
     if A is None:
         A = torch.empty((B, H, L // C if C else 0, C, C), dtype=_TDT[adt], device=K.device)
+    tok = B * L * H
     _check("gdn_build_A", lib.gdn_build_A(
-        _dev(K, "K"), _dev(beta, "beta", torch.float32), _dev(g, "g", torch.float32),
-        _dev(A, "A", _TDT[adt]), B, L, H, dk, C, kdt, adt, _stream(stream)))
+        _dev(K, "K"), _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
+        _dev(A, "A", _TDT[adt], B * H * (L // C if C else 0) * C * C), B, L, H, dk, C, kdt, adt,
+        _stream(stream)))
     return A
 
 
@@ -133,7 +139,7 @@ def gdn_chunk_inverse_neumann(A: torch.Tensor, N: int, S: int, Tinv: Optional[to
     if Tinv is None:
         Tinv = torch.empty_like(A)
     _check("gdn_chunk_inverse_neumann", lib.gdn_chunk_inverse_neumann(
-        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype), n, C, N, S, dt, _stream(stream)))
+        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype, A.numel()), n, C, N, S, dt, _stream(stream)))
     return Tinv
 
 
@@ -145,7 +151,7 @@ def gdn_chunk_inverse_fwdsub(A: torch.Tensor, Tinv: Optional[torch.Tensor] = Non
     if Tinv is None:
         Tinv = torch.empty_like(A)
     _check("gdn_chunk_inverse_fwdsub", lib.gdn_chunk_inverse_fwdsub(
-        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype), n, C, dt, _stream(stream)))
+        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype, A.numel()), n, C, dt, _stream(stream)))
     return Tinv
 
 
@@ -158,9 +164,11 @@ def gdn_wy_apply(Tinv: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: tor
     dt = _fdtype(K, "K")
     W = torch.empty_like(K) if W is None else W
     U = torch.empty_like(V) if U is None else U
+    tok = B * L * H
     _check("gdn_wy_apply", lib.gdn_wy_apply(
-        _dev(Tinv, "Tinv", K.dtype), _dev(K, "K"), _dev(V, "V", K.dtype),
-        _dev(beta, "beta", torch.float32), _dev(W, "W", K.dtype), _dev(U, "U", K.dtype),
+        _dev(Tinv, "Tinv", K.dtype, B * H * (L // C if C else 0) * C * C), _dev(K, "K"),
+        _dev(V, "V", K.dtype, tok * dv), _dev(beta, "beta", torch.float32, tok),
+        _dev(W, "W", K.dtype, tok * dk), _dev(U, "U", K.dtype, tok * dv),
         B, L, H, dk, dv, C, dt, _stream(stream)))
     return W, U
 
@@ -177,11 +185,13 @@ def gdn_chunk_wy_fused(K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor, g: 
     U = torch.empty_like(V) if U is None else U
     if want_T and Tinv is None:
         Tinv = torch.empty((B, H, L // C, C, C), dtype=K.dtype, device=K.device)
-    tp = _dev(Tinv, "Tinv", K.dtype) if Tinv is not None else None
+    tok = B * L * H
+    tp = (_dev(Tinv, "Tinv", K.dtype, B * H * (L // C if C else 0) * C * C)
+          if Tinv is not None else None)
     _check("gdn_chunk_wy_fused", lib.gdn_chunk_wy_fused(
-        _dev(K, "K"), _dev(V, "V", K.dtype), _dev(beta, "beta", torch.float32),
-        _dev(g, "g", torch.float32), _dev(W, "W", K.dtype), _dev(U, "U", K.dtype), tp,
-        B, L, H, dk, dv, C, N, S, dt, _stream(stream)))
+        _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv), _dev(beta, "beta", torch.float32, tok),
+        _dev(g, "g", torch.float32, tok), _dev(W, "W", K.dtype, tok * dk),
+        _dev(U, "U", K.dtype, tok * dv), tp, B, L, H, dk, dv, C, N, S, dt, _stream(stream)))
     return (W, U, Tinv) if Tinv is not None else (W, U)
 
 
@@ -192,19 +202,25 @@ def gdn_quantize_tiles_i8(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
     Aq = torch.empty(A.shape, dtype=torch.int8, device=A.device) if Aq is None else Aq
     eA = torch.empty(n, dtype=torch.int32, device=A.device) if eA is None else eA
     _check("gdn_quantize_tiles_i8", lib.gdn_quantize_tiles_i8(
-        _dev(A, "A", torch.float32), _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32),
-        n, C, _stream(stream)))
+        _dev(A, "A", torch.float32), _dev(Aq, "Aq", torch.int8, A.numel()),
+        _dev(eA, "eA", torch.int32, n), n, C, _stream(stream)))
     return Aq, eA
 
 
 def gdn_chunk_inverse_neumann_i8(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: int,
-                                 want_deq: bool = False, stream=None):
+                                 want_deq: bool = False, Tq: Optional[torch.Tensor] = None,
+                                 eT: Optional[torch.Tensor] = None,
+                                 Tdeq: Optional[torch.Tensor] = None, stream=None):
     """(Tq int8, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT."""
     n, C = _tiles(Aq)
-    Tq = torch.empty_like(Aq)
-    eT = torch.empty_like(eA)
-    Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device) if want_deq else None
+    Tq = torch.empty_like(Aq) if Tq is None else Tq
+    eT = torch.empty_like(eA) if eT is None else eT
+    Td = Tdeq
+    if want_deq and Td is None:
+        Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device)
     _check("gdn_chunk_inverse_neumann_i8", lib.gdn_chunk_inverse_neumann_i8(
-        _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32), _dev(Tq, "Tq"), _dev(eT, "eT"),
-        _dev(Td, "Tdeq") if Td is not None else None, n, C, N, S, _stream(stream)))
-    return (Tq, eT, Td) if want_deq else (Tq, eT)
+        _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32, n),
+        _dev(Tq, "Tq", torch.int8, Aq.numel()), _dev(eT, "eT", torch.int32, n),
+        _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
+        _stream(stream)))
+    return (Tq, eT, Td) if Td is not None else (Tq, eT)

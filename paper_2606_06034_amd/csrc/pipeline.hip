@@ -111,6 +111,37 @@ __device__ __forceinline__ void load_rows(Pair<F> (&xp)[NB][D / 32], const TIO* 
     for (int q = 0; q < D / 32; ++q) xp[I][q] = load_row8<F>(xb + (I * 16 + c) * ld + 32 * q + 8 * g);
 }
 
+// Asynchronous copy of a bf16 chunk of X into LDS (global -> LDS DMA, no
+// registers): the 16-byte run lane (g, c) would load in load_rows lands at
+// s + 512 (I * D / 32 + q) + 8 * lane.  Completion is tracked by vmcnt.
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glb_void;
+
+template <int NB, int D>
+__device__ __forceinline__ void prefetch_rows_lds(const __bf16* __restrict__ xb, int64_t ld,
+                                                  __bf16* s) {
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int q = 0; q < D / 32; ++q)
+      __builtin_amdgcn_global_load_lds((glb_void*)(xb + (I * 16 + c) * ld + 32 * q + 8 * g),
+                                       (lds_void*)(s + 512 * (I * (D / 32) + q)), 16, 0, 0);
+}
+
+// wait for every outstanding vector-memory operation of this wave
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+template <int NB, int D>
+__device__ __forceinline__ void load_rows_lds(Pair<bf16x4> (&xp)[NB][D / 32], const __bf16* s) {
+  const int l = lane_id();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int q = 0; q < D / 32; ++q)
+      xp[I][q] = Pair<bf16x4>{*(const bf16x8*)(s + 512 * (I * (D / 32) + q) + 8 * l)};
+}
+
 // out = T' X for one chunk, T' = T diag(beta) as row pairs (beta folded into
 // T's columns), X given by its row-form pairs xp.  Each 16 x 16 block of X
 // is moved to column form by an identity MFMA (X I), then W(I, .) =
@@ -238,7 +269,11 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               TIO* __restrict__ U, TIO* __restrict__ Tout, int L,
                                               int H, int N, int S) {
   constexpr int C = 16 * NB;
+  // bf16: V goes to LDS by DMA and arrives while the inverse is computed
+  // (16 KB per wave at C = 64, DV = 128)
+  constexpr bool PREF = sizeof(TIO) == 2;
   __shared__ float sb[C], sg[C];
+  __shared__ __attribute__((aligned(16))) TIO sv[PREF ? NB * (DV / 32) * 512 : 8];
   const int64_t tile = blockIdx.x;
   const Chunk ch(tile, L, H, C);
   load_gates<C>(beta, g, ch, L, H, sb, sg);
@@ -249,6 +284,14 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
   Acc<NB> Lc;
   {
     gram_lower<NB, DK, false>(Lc, kp);
+    // issued once K has been consumed: the compiler counts DMA completions
+    // as unordered with plain loads and would otherwise wait for V before
+    // the Gram; the inverse below touches no global memory
+    if constexpr (PREF) {
+      __builtin_amdgcn_sched_barrier(0);
+      prefetch_rows_lds<NB, DV>(V + ch.row(0, L, H, DV), (int64_t)H * DV, sv);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
     ColP<NB, F> LC;
     to_colp(LC, Lc);
@@ -262,7 +305,12 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
   Pair<F> vp[NB][DV / 32];
-  load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
+  if constexpr (PREF) {
+    wait_vmem();
+    load_rows_lds<NB, DV>(vp, sv);
+  } else {
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
+  }
   RowP<NB, F> TR;
   scale_cols(TR, Tr, sb);
   apply_lower<NB, DK>(TR, kp, W + ch.row(0, L, H, DK), (int64_t)H * DK);

@@ -291,3 +291,24 @@ def _sampled_check(wname, C=None, n_sample=16, seed=0):
 def test_qwen35_prefill_full_size_sampled():
     """The benchmarked workload (2048 tiles), in the launch the bench times."""
     _sampled_check("qwen35_prefill")
+
+
+def test_binding_rejects_wrong_sizes():
+    """Caller-supplied tensors of the wrong element count never reach a kernel."""
+    A = torch.zeros((4, 64, 64), device="cuda")
+    with pytest.raises(ValueError, match="Tinv"):
+        G.gdn_chunk_inverse_neumann(A, 3, 8, Tinv=torch.empty((3, 64, 64), device="cuda"))
+    with pytest.raises(ValueError, match="Tinv"):
+        G.gdn_chunk_inverse_fwdsub(A, Tinv=torch.empty((5, 64, 64), device="cuda"))
+    K = torch.zeros((1, 128, 2, 128), device="cuda", dtype=torch.bfloat16)
+    b = torch.zeros((1, 128, 2), device="cuda")
+    with pytest.raises(ValueError, match="beta"):
+        G.gdn_build_A(K, b[:, :64], b, 64)
+    with pytest.raises(ValueError, match="W"):
+        G.gdn_chunk_wy_fused(K, K, b, b, 64, 3, 8, W=torch.empty_like(K)[:, :64])
+    with pytest.raises(ValueError, match="eA"):
+        G.gdn_quantize_tiles_i8(A, eA=torch.empty(3, dtype=torch.int32, device="cuda"))
+    Aq, eA = G.gdn_quantize_tiles_i8(A)
+    with pytest.raises(ValueError, match="Tq"):
+        G.gdn_chunk_inverse_neumann_i8(Aq, eA, 3, 8, Tq=Aq[:2])
+    torch.cuda.synchronize()
