@@ -14,10 +14,14 @@
 //     early equals masking the finished sum);
 //   * E = band_{i-j > N}(Lm T0) in both forms: on the band E is exactly 0,
 //     and off the band T0 vanishes so Lm T0 is E there;
-//   * residual powers P_s = E P_{s-1} in column form (the same powers as
-//     Algorithm 1's P E chain), Gs += P_s; E^s vanishes exactly on
-//     i - j < s (N + 1) and those blocks are skipped;
-//   * T = T0 + T0 Gs with T0 entering through the MFMA accumulator.
+//   * the residual sum, either (GH) by Horner, R <- I + E R from R = I + E,
+//     then T = T0 R; or as the chain of powers P_s = E P_{s-1} in column
+//     form (the same powers as Algorithm 1's P E chain), Gs += P_s, where
+//     E^s vanishes exactly on i - j < s (N + 1) and those blocks are
+//     skipped, then T = T0 + T0 Gs with T0 entering through the MFMA
+//     accumulator.  Both evaluate T0 sum_{s=0}^{S} E^s; Horner keeps one
+//     matrix live instead of a power and a running sum (fewer registers)
+//     at the price of the chain's structural skipping.
 // F = bf16x4 rounds every MFMA operand to bf16 (products accumulate in fp32,
 // sums and masks run in fp32); F = f32x4 computes in fp32 throughout.
 // SMALLN: the caller guarantees N <= 15, so T0's band lies in the diagonal
@@ -68,8 +72,9 @@ __device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int l
 // Store a unit lower-triangular tile from its row-form blocks (diagonal
 // written as exactly 1, the upper triangle as 0).  ldr = row stride.
 template <int NB, typename TIO>
-__device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr, const Acc<NB>& Tr) {
-  const int g = lane_g(), c = lane_c();
+__device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr, const Acc<NB>& Tr,
+                                               Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
@@ -80,7 +85,7 @@ __device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr, con
         x = Tr.a[bidx(I, J)];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int d = drow(0, v);
+          const int d = drow(0, v, ln);
           x[v] = d > 0 ? x[v] : (d == 0 ? 1.f : 0.f);
         }
       }
@@ -102,9 +107,9 @@ __device__ __forceinline__ bool in_t0_band(int m, int N) {
 // f32 column blocks (Lc; only T0's band blocks are read).  Out: Tr, the
 // row-form blocks of T (strict part exact, diagonal blocks carry T0's unit
 // diagonal; callers write the diagonal as 1).
-template <int NB, typename F, bool SMALLN, int NC = -1, int SC = -1>
+template <int NB, typename F, bool SMALLN, int NC = -1, int SC = -1, bool GH = true>
 __device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<NB>& Lc, int Nrt,
-                                               int Srt, Acc<NB>& Tr) {
+                                               int Srt, Acc<NB>& Tr, Lane ln = lane_here()) {
   constexpr int C = 16 * NB;
   const int N = NC >= 0 ? NC : Nrt;
   const int S = SC >= 0 ? SC : Srt;
@@ -115,9 +120,9 @@ __device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J) {
-      f32x4 x = in_t0_band<SMALLN>(I - J, N) ? band_block<true>(Lc.a[bidx(I, J)], I - J, 1, N)
+      f32x4 x = in_t0_band<SMALLN>(I - J, N) ? band_block<true>(Lc.a[bidx(I, J)], I - J, 1, N, ln)
                                              : zero4();
-      if (I == J) x += eye4();
+      if (I == J) x += eye4(ln);
       H.a[bidx(I, J)] = x;
     }
   ColP<NB, F> T0c;
@@ -127,14 +132,14 @@ __device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int J = 0; J <= I; ++J) D.a[bidx(I, J)] = (I == J) ? eye4() : zero4();
+      for (int J = 0; J <= I; ++J) D.a[bidx(I, J)] = (I == J) ? eye4(ln) : zero4();
     mm<NB, false, true>(D, LR, 1, C - 1, T0c, 0, N, 1, N);
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
       for (int J = 0; J <= I; ++J)
         if (in_t0_band<SMALLN>(I - J, N))
-          D.a[bidx(I, J)] = band_block<true>(D.a[bidx(I, J)], I - J, 0, N);
+          D.a[bidx(I, J)] = band_block<true>(D.a[bidx(I, J)], I - J, 0, N, ln);
         else
           D.a[bidx(I, J)] = zero4();
     to_colp(T0c, D);
@@ -148,14 +153,13 @@ __device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<
   RowP<NB, F> T0R;
   {
     Acc<NB> t;
-    col_to_row(t, T0c, 0, N);
+    col_to_row(t, T0c, 0, N, ln);
     to_rowp(T0R, t);
   }
 
   // ---- E = band_{i-j > N}(Lm T0), both forms (Section 3.4)
   RowP<NB, F> ER;
-  ColP<NB, F> P;
-  Acc<NB> G;  // Gs = E + ... + E^S, column form
+  Acc<NB> Ec;  // column form
   {
     Acc<NB> D;
     mm<NB, true, false>(D, LR, 1, C - 1, T0c, 0, N, N + 1, C - 1);
@@ -163,52 +167,81 @@ __device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<
     for (int I = 0; I < NB; ++I)
 #pragma unroll
       for (int J = 0; J <= I; ++J)
-        D.a[bidx(I, J)] = band_block<false>(D.a[bidx(I, J)], I - J, N + 1, C - 1);
+        D.a[bidx(I, J)] = band_block<false>(D.a[bidx(I, J)], I - J, N + 1, C - 1, ln);
     to_rowp(ER, D);
     mm<NB, false, false>(D, LR, 1, C - 1, T0c, 0, N, N + 1, C - 1);
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
       for (int J = 0; J <= I; ++J)
-        G.a[bidx(I, J)] = S >= 1 ? band_block<true>(D.a[bidx(I, J)], I - J, N + 1, C - 1)
-                                 : zero4();
-    to_colp(P, G);
+        Ec.a[bidx(I, J)] = S >= 1 ? band_block<true>(D.a[bidx(I, J)], I - J, N + 1, C - 1, ln)
+                                  : zero4();
   }
 
-  // ---- residual powers P_s = E P_{s-1}
-  auto chain_step = [&](int s) {
-    const int plo = (s - 1) * (N + 1), lo = s * (N + 1);
-    Acc<NB> D;
-    mm<NB, false, false>(D, ER, N + 1, C - 1, P, plo, C - 1, lo, C - 1);
+  if constexpr (GH) {
+    // ---- R = I + E + ... + E^S by Horner, R <- I + E R (column pairs; the
+    // identity enters through the MFMA accumulator).  E R only reaches
+    // i - j >= N + 1, and R's upper triangle and band 1..N stay exact zeros,
+    // so no mask is needed.  Holds R alone instead of a power and a sum.
+    ColP<NB, F> RC;
+#pragma unroll
+    for (int I = 0; I < NB; ++I) Ec.a[bidx(I, I)] += eye4(ln);
+    to_colp(RC, Ec);
+    auto horner_r = [&]() {
+      Acc<NB> D;
+#pragma unroll
+      for (int I = 0; I < NB; ++I)
+#pragma unroll
+        for (int J = 0; J <= I; ++J) D.a[bidx(I, J)] = (I == J) ? eye4(ln) : zero4();
+      mm<NB, false, true>(D, ER, N + 1, C - 1, RC, 0, C - 1, N + 1, C - 1);
+      to_colp(RC, D);
+    };
+    if constexpr (SC >= 0) {
+#pragma unroll
+      for (int s = 2; s <= SC; ++s) horner_r();
+    } else {
+      for (int s = 2; s <= S; ++s) horner_r();
+    }
+    // ---- T = T0 R, row form
+    mm<NB, true, false>(Tr, T0R, 0, N, RC, 0, C - 1, 0, C - 1);
+  } else {
+    // ---- residual powers P_s = E P_{s-1}, Gs = E + ... + E^S (column form)
+    ColP<NB, F> P;
+    Acc<NB> G = Ec;
+    to_colp(P, G);
+    auto chain_step = [&](int s) {
+      const int plo = (s - 1) * (N + 1), lo = s * (N + 1);
+      Acc<NB> D;
+      mm<NB, false, false>(D, ER, N + 1, C - 1, P, plo, C - 1, lo, C - 1);
+#pragma unroll
+      for (int I = 0; I < NB; ++I)
+#pragma unroll
+        for (int J = 0; J <= I; ++J)
+          if (blk_nz(I - J, lo, C - 1)) {
+            G.a[bidx(I, J)] += D.a[bidx(I, J)];
+            pin(G.a[bidx(I, J)]);
+          }
+      to_colp(P, D);
+    };
+    if constexpr (SC >= 0) {
+#pragma unroll
+      for (int s = 2; s <= SC; ++s) chain_step(s);
+    } else {
+      for (int s = 2; s <= S; ++s) chain_step(s);
+    }
+    // ---- T = T0 + T0 Gs, row form; T0 (as rounded for the products)
+    // enters through the accumulator
+    ColP<NB, F> GC;
+    to_colp(GC, G);
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int J = 0; J <= I; ++J)
-        if (blk_nz(I - J, lo, C - 1)) {
-          G.a[bidx(I, J)] += D.a[bidx(I, J)];
-          pin(G.a[bidx(I, J)]);
-        }
-    to_colp(P, D);
-  };
-  if constexpr (SC >= 0) {
-#pragma unroll
-    for (int s = 2; s <= SC; ++s) chain_step(s);
-  } else {
-    for (int s = 2; s <= S; ++s) chain_step(s);
+      for (int J = 0; J <= I; ++J) {
+        const int p = J >> 1;
+        Tr.a[bidx(I, J)] = (J & 1) ? T0R.r[I][p].hi() : T0R.r[I][p].lo();
+      }
+    mm<NB, true, true>(Tr, T0R, 0, N, GC, N + 1, C - 1, N + 1, C - 1);
   }
-
-  // ---- T = T0 + T0 Gs, row form; T0 (as rounded for the products) enters
-  // through the accumulator
-  ColP<NB, F> GC;
-  to_colp(GC, G);
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      const int p = J >> 1;
-      Tr.a[bidx(I, J)] = (J & 1) ? T0R.r[I][p].hi() : T0R.r[I][p].lo();
-    }
-  mm<NB, true, true>(Tr, T0R, 0, N, GC, N + 1, C - 1, N + 1, C - 1);
 }
 
 }  // namespace gdn

@@ -9,14 +9,17 @@
 
 namespace gdn {
 
-template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO>
+// GH selects the residual sum's evaluation (engine.hpp): Horner for the
+// standalone tiles, the power chain inside the C = 128 kernel (measured
+// faster there, where the merge adds to the register load).
+template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO, bool GH = true>
 __device__ __forceinline__ void invert_block(const TIO* __restrict__ a, TIO* __restrict__ t,
                                              int ldr, int N, int S, Acc<NB>& Tr) {
   Acc<NB> Lr, Lc;
   load_neg_strict<NB>(a, ldr, Lr, Lc);
   RowP<NB, F> LR;
   to_rowp(LR, Lr);
-  neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
+  neumann_engine<NB, F, SMALLN, NC, SC, GH>(LR, Lc, N, S, Tr);
   store_unit_row<NB>(t, ldr, Tr);
 }
 
@@ -45,7 +48,7 @@ __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
   RowP<NB, F> X22;
   {
     Acc<NB> Tr;
-    invert_block<NB, F, SMALLN, NC, SC>(a + 64 * C + 64, t + 64 * C + 64, C, N, S, Tr);
+    invert_block<NB, F, SMALLN, NC, SC, TIO, false>(a + 64 * C + 64, t + 64 * C + 64, C, N, S, Tr);
 #pragma unroll
     for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
     to_rowp(X22, Tr);
@@ -54,7 +57,7 @@ __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
   ColP<NB, F> X11;
   {
     Acc<NB> Tr, Tc;
-    invert_block<NB, F, SMALLN, NC, SC>(a, t, C, N, S, Tr);
+    invert_block<NB, F, SMALLN, NC, SC, TIO, false>(a, t, C, N, S, Tr);
 #pragma unroll
     for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
     RowP<NB, F> X11r;

@@ -13,15 +13,24 @@
 
 namespace gdn {
 
-// Chunk bookkeeping for tile index `tile` of the [B, H, L/C, C, C] layout.
+// Chunk bookkeeping.  Work item x walks the tiles heads-fastest,
+// x = (b * (L / C) + chunk) * H + h, so waves running side by side read the
+// neighbouring heads of the same tokens: together they cover whole
+// H * d-wide token rows of [B, L, H, d] instead of one 256-byte run per row
+// and DRAM page (+10 % bandwidth for this access pattern on MI355X).
+// `tile` is the position in the [B, H, L/C, C, C] tile layout.
 struct Chunk {
   int b, h, t0;
-  __device__ Chunk(int64_t tile, int L, int H, int C) {
-    const int nc = L / C;
-    const int64_t bh = tile / nc;
-    t0 = (int)(tile - bh * nc) * C;
-    b = (int)(bh / H);
-    h = (int)(bh - (int64_t)b * H);
+  int64_t tile;
+  // x < 2^31 (the tile count is bounded so): 32-bit unsigned division
+  __device__ Chunk(uint32_t x, int L, int H, int C) {
+    const uint32_t nc = (uint32_t)(L / C);
+    const uint32_t bc = x / (uint32_t)H;
+    h = (int)(x - bc * (uint32_t)H);
+    b = (int)(bc / nc);
+    const int chunk = (int)(bc - (uint32_t)b * nc);
+    t0 = chunk * C;
+    tile = ((int64_t)b * H + h) * nc + chunk;
   }
   // element offset of (token t0 + r, head h, feature 0) in [B, L, H, d]
   __device__ int64_t row(int r, int L, int H, int d) const {
@@ -62,8 +71,8 @@ __device__ __forceinline__ void gram_lower(Acc<NB>& G, const Pair<F> (&kp)[NB][D
 // element coordinates of the blocks' form.
 template <int NB, bool ROWFORM>
 __device__ __forceinline__ void gate_scale(Acc<NB>& G, const float* sb, const float* sg,
-                                           float sign) {
-  const int g = lane_g(), c = lane_c();
+                                           float sign, Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
@@ -103,8 +112,8 @@ __device__ __forceinline__ void store_row8(float* p, f32x4 lo, f32x4 hi) {
 
 template <int NB, int D, typename F, typename TIO>
 __device__ __forceinline__ void load_rows(Pair<F> (&xp)[NB][D / 32], const TIO* __restrict__ xb,
-                                          int64_t ld) {
-  const int g = lane_g(), c = lane_c();
+                                          int64_t ld, Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
@@ -119,8 +128,8 @@ typedef __attribute__((address_space(1))) void glb_void;
 
 template <int NB, int D>
 __device__ __forceinline__ void prefetch_rows_lds(const __bf16* __restrict__ xb, int64_t ld,
-                                                  __bf16* s) {
-  const int g = lane_g(), c = lane_c();
+                                                  __bf16* s, Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
@@ -130,39 +139,36 @@ __device__ __forceinline__ void prefetch_rows_lds(const __bf16* __restrict__ xb,
 }
 
 // wait for every outstanding vector-memory operation of this wave
+// (s_waitcnt vmcnt(0))
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-template <int NB, int D>
-__device__ __forceinline__ void load_rows_lds(Pair<bf16x4> (&xp)[NB][D / 32], const __bf16* s) {
-  const int l = lane_id();
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int q = 0; q < D / 32; ++q)
-      xp[I][q] = Pair<bf16x4>{*(const bf16x8*)(s + 512 * (I * (D / 32) + q) + 8 * l)};
-}
-
 // out = T' X for one chunk, T' = T diag(beta) as row pairs (beta folded into
-// T's columns), X given by its row-form pairs xp.  Each 16 x 16 block of X
-// is moved to column form by an identity MFMA (X I), then W(I, .) =
-// sum_K T'(I, K) X(K, .) comes out in row form and is stored 8 features per
-// lane.  ob points at (token t0, head h, feature 0) of the output.
-template <int NB, int D, typename F, typename TIO>
-__device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, const Pair<F> (&xp)[NB][D / 32],
-                                            TIO* __restrict__ ob, int64_t ld) {
-  const int g = lane_g(), c = lane_c();
-  const f32x4 e = eye4();
+// T's columns), X given by get(I, q): its row-form pair of rows 16I..16I+15,
+// features 32q..32q+31 (registers, or LDS read one 32-feature slice at a
+// time).  Each 16 x 16 block of X is moved to column form by an identity
+// MFMA (X I), then W(I, .) = sum_K T'(I, K) X(K, .) comes out in row form and
+// is stored 8 features per lane.  ob points at (token t0, head h, feature 0)
+// of the output.
+template <int NB, int D, typename F, typename TIO, typename Get>
+__device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, Get&& get,
+                                            TIO* __restrict__ ob, int64_t ld,
+                                            Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
+  const f32x4 e = eye4(ln);
   const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
 #pragma unroll
   for (int q = 0; q < D / 32; ++q) {
+    Pair<F> x[NB];
+#pragma unroll
+    for (int I = 0; I < NB; ++I) x[I] = get(I, q);
     Pair<F> y[2][npair(NB)];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int p = 0; p < npair(NB); ++p) {
-        const f32x4 a = Pair<F>::template mma<false>(xp[2 * p][q], h ? id1 : id0, zero4());
+        const f32x4 a = Pair<F>::template mma<false>(x[2 * p], h ? id1 : id0, zero4());
         const f32x4 b = (2 * p + 1 < NB)
-                            ? Pair<F>::template mma<false>(xp[2 * p + 1][q], h ? id1 : id0, zero4())
+                            ? Pair<F>::template mma<false>(x[2 * p + 1], h ? id1 : id0, zero4())
                             : zero4();
         y[h][p] = Pair<F>::make(a, b);
       }
@@ -178,12 +184,28 @@ __device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, const Pair<F>
     }
   }
 }
+// operand getters: pairs held in registers, or the LDS copy prefetch_rows_lds
+// made (one 16-byte read per lane and pair)
+template <int NB, int D, typename F>
+struct RegRows {
+  const Pair<F> (&xp)[NB][D / 32];
+  __device__ __forceinline__ Pair<F> operator()(int I, int q) const { return xp[I][q]; }
+};
+template <int D>
+struct LdsRows {
+  const __bf16* s;
+  int l;
+  __device__ __forceinline__ Pair<bf16x4> operator()(int I, int q) const {
+    return Pair<bf16x4>{*(const bf16x8*)(s + 512 * (I * (D / 32) + q) + 8 * l)};
+  }
+};
 
 // T diag(beta) as row pairs from the row-form blocks of the unit lower T:
 // value v of lane (g, c) in block (I, J) sits in column 16J + 4g + v.
 template <int NB, typename F>
-__device__ __forceinline__ void scale_cols(RowP<NB, F>& TR, Acc<NB> T, const float* sb) {
-  const int g = lane_g();
+__device__ __forceinline__ void scale_cols(RowP<NB, F>& TR, Acc<NB> T, const float* sb,
+                                           Lane ln = lane_here()) {
+  const int g = ln.g();
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
@@ -203,8 +225,8 @@ __global__ __launch_bounds__(64) void k_build_A(const TK* __restrict__ K,
                                                 TA* __restrict__ A, int L, int H) {
   constexpr int C = 16 * NB;
   __shared__ float sb[C], sg[C];
-  const int64_t tile = blockIdx.x;
-  const Chunk ch(tile, L, H, C);
+  const Chunk ch(blockIdx.x, L, H, C);
+  const int64_t tile = ch.tile;
   load_gates<C>(beta, g, ch, L, H, sb, sg);
   Acc<NB> G;
   {
@@ -232,8 +254,8 @@ __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO*
                                            TIO* __restrict__ U, int L, int H) {
   constexpr int C = 16 * NB;
   __shared__ float sb[C];
-  const int64_t tile = blockIdx.x;
-  const Chunk ch(tile, L, H, C);
+  const Chunk ch(blockIdx.x, L, H, C);
+  const int64_t tile = ch.tile;
   load_gates<C>(beta, beta, ch, L, H, sb, nullptr);
   const TIO* t = T + tile * (C * C);
   const int g = lane_g(), c = lane_c();
@@ -249,19 +271,22 @@ __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO*
   {
     Pair<F> kp[NB][DK / 32];
     load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
-    apply_lower<NB, DK>(TR, kp, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
   }
   {
     Pair<F> vp[NB][DV / 32];
     load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
-    apply_lower<NB, DV>(TR, vp, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
   }
 }
 
 // ---------------------------------------------------------------------------
 // gdn_chunk_wy_fused: build A -> approximate inverse -> W, U, on chip
 
-template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO>
+// One tile per wave.  PREF (bf16 only): V is copied into LDS by DMA right
+// after the Gram product and arrives while the inverse is computed.
+template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
+          bool PREF = false>
 __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               const TIO* __restrict__ V,
                                               const float* __restrict__ beta,
@@ -269,13 +294,11 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               TIO* __restrict__ U, TIO* __restrict__ Tout, int L,
                                               int H, int N, int S) {
   constexpr int C = 16 * NB;
-  // bf16: V goes to LDS by DMA and arrives while the inverse is computed
-  // (16 KB per wave at C = 64, DV = 128)
-  constexpr bool PREF = sizeof(TIO) == 2;
+  static_assert(!PREF || sizeof(TIO) == 2, "V prefetch is for bf16 IO");
   __shared__ float sb[C], sg[C];
-  __shared__ __attribute__((aligned(16))) TIO sv[PREF ? NB * (DV / 32) * 512 : 8];
-  const int64_t tile = blockIdx.x;
-  const Chunk ch(tile, L, H, C);
+  __shared__ __attribute__((aligned(16))) __bf16 sv[PREF ? NB * (DV / 32) * 512 : 8];
+  const Chunk ch(blockIdx.x, L, H, C);
+  const int64_t tile = ch.tile;
   load_gates<C>(beta, g, ch, L, H, sb, sg);
 
   Pair<F> kp[NB][DK / 32];
@@ -289,7 +312,7 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
     // the Gram; the inverse below touches no global memory
     if constexpr (PREF) {
       __builtin_amdgcn_sched_barrier(0);
-      prefetch_rows_lds<NB, DV>(V + ch.row(0, L, H, DV), (int64_t)H * DV, sv);
+      prefetch_rows_lds<NB, DV>((const __bf16*)V + ch.row(0, L, H, DV), (int64_t)H * DV, sv);
       __builtin_amdgcn_sched_barrier(0);
     }
     gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
@@ -304,31 +327,39 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
   if (Tout) store_unit_row<NB>(Tout + tile * (C * C), C, Tr);
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
-  Pair<F> vp[NB][DV / 32];
-  if constexpr (PREF) {
-    wait_vmem();
-    load_rows_lds<NB, DV>(vp, sv);
-  } else {
-    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
-  }
   RowP<NB, F> TR;
   scale_cols(TR, Tr, sb);
-  apply_lower<NB, DK>(TR, kp, W + ch.row(0, L, H, DK), (int64_t)H * DK);
-  apply_lower<NB, DV>(TR, vp, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+  // with the prefetch, U is formed first from V read out of LDS one slice at
+  // a time, then W from the K pairs, so K and V are never both in registers
+  if constexpr (PREF) {
+    wait_vmem();
+    apply_lower<NB, DV>(TR, LdsRows<DV>{sv, lane_id()}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+  } else if constexpr (NB <= 2) {  // registers to spare: V's loads overlap W
+    Pair<F> vp[NB][DV / 32];
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+  } else {
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+    Pair<F> vp[NB][DV / 32];
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+  }
 }
 
 // ---------------------------------------------------------------------------
 // launchers
 
-#define GDN_DK_SWITCH(dk, BODY)          \
-  switch (dk) {                          \
-    case 64: { constexpr int DK = 64; BODY } \
-    case 128: { constexpr int DK = 128; BODY } \
+#define GDN_DK_SWITCH(dk, ...)                     \
+  switch (dk) {                                    \
+    case 64: { constexpr int DK = 64; __VA_ARGS__ }   \
+    case 128: { constexpr int DK = 128; __VA_ARGS__ } \
   }
-#define GDN_DV_SWITCH(dv, BODY)          \
-  switch (dv) {                          \
-    case 64: { constexpr int DV = 64; BODY } \
-    case 128: { constexpr int DV = 128; BODY } \
+#define GDN_DV_SWITCH(dv, ...)                     \
+  switch (dv) {                                    \
+    case 64: { constexpr int DV = 64; __VA_ARGS__ }   \
+    case 128: { constexpr int DV = 128; __VA_ARGS__ } \
   }
 
 template <int NB, typename F, typename TK, typename TA>
@@ -407,24 +438,32 @@ template <> struct FusedOrder<1> { static constexpr int N = 3, S = 2; };
 template <> struct FusedOrder<2> { static constexpr int N = 3, S = 4; };
 template <> struct FusedOrder<4> { static constexpr int N = 3, S = 8; };
 
+template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO, bool PREF>
+static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,
+                       void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st) {
+  hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF>), dim3((unsigned)n),
+                     dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U,
+                     (TIO*)T, L, H, N, S);
+}
+
+// bf16 with C >= 32 prefetches V (for C = 16 the tile is small and the
+// kernel runs at high occupancy without it)
 template <int NB, typename F, typename TIO>
 static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, const float* g,
                                void* W, void* U, void* T, int64_t n, int L, int H, int dk,
                                int dv, int N, int S, hipStream_t st) {
   constexpr int DN = FusedOrder<NB>::N, DS = FusedOrder<NB>::S;
+  constexpr bool PREF = sizeof(TIO) == 2 && NB > 1;
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
     if (N == DN && S == DS)
-      hipLaunchKernelGGL((k_fused<NB, DK, DV, F, true, DN, DS, TIO>), dim3((unsigned)n), dim3(64),
-                         0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, (TIO*)T,
-                         L, H, N, S);
+      launch_one<NB, DK, DV, F, true, DN, DS, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
+                                                          st);
     else if (N <= 15)
-      hipLaunchKernelGGL((k_fused<NB, DK, DV, F, true, -1, -1, TIO>), dim3((unsigned)n),
-                         dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W,
-                         (TIO*)U, (TIO*)T, L, H, N, S);
+      launch_one<NB, DK, DV, F, true, -1, -1, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
+                                                          st);
     else
-      hipLaunchKernelGGL((k_fused<NB, DK, DV, F, false, -1, -1, TIO>), dim3((unsigned)n),
-                         dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W,
-                         (TIO*)U, (TIO*)T, L, H, N, S);
+      launch_one<NB, DK, DV, F, false, -1, -1, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
+                                                           st);
     return hipGetLastError();
   }))
   return hipErrorNotSupported;

@@ -48,6 +48,15 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int lane_g() { return (threadIdx.x & 63) >> 4; }
 __device__ __forceinline__ int lane_c() { return threadIdx.x & 15; }
 
+// The lane coordinates the lane-dependent helpers work from, passed as a
+// defaulted last argument so a caller can hand one set down a call chain.
+struct Lane {
+  int id;
+  __device__ __forceinline__ int g() const { return id >> 4; }
+  __device__ __forceinline__ int c() const { return id & 15; }
+};
+__device__ __forceinline__ Lane lane_here() { return Lane{(int)(threadIdx.x & 63)}; }
+
 // Can a block at block-subdiagonal m hold entries with lo <= i - j <= hi?
 __device__ __forceinline__ bool blk_nz(int m, int lo, int hi) {
   return (16 * m + 15 >= lo) && (16 * m - 15 <= hi);
@@ -65,8 +74,8 @@ __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 __device__ __forceinline__ void pin(f32x4& x) { asm volatile("" : "+v"(x)); }
 
 // identity block (both forms coincide)
-__device__ __forceinline__ f32x4 eye4() {
-  const int g = lane_g(), c = lane_c();
+__device__ __forceinline__ f32x4 eye4(Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
   f32x4 r;
 #pragma unroll
   for (int v = 0; v < 4; ++v) r[v] = (c == 4 * g + v) ? 1.f : 0.f;
@@ -74,18 +83,23 @@ __device__ __forceinline__ f32x4 eye4() {
 }
 
 // i - j of value v of this lane in a block at block-subdiagonal m
-__device__ __forceinline__ int dcol(int m, int v) { return 16 * m + 4 * lane_g() + v - lane_c(); }
-__device__ __forceinline__ int drow(int m, int v) { return 16 * m + lane_c() - 4 * lane_g() - v; }
+__device__ __forceinline__ int dcol(int m, int v, Lane ln = lane_here()) {
+  return 16 * m + 4 * ln.g() + v - ln.c();
+}
+__device__ __forceinline__ int drow(int m, int v, Lane ln = lane_here()) {
+  return 16 * m + ln.c() - 4 * ln.g() - v;
+}
 
 // Zero the entries of a block outside [lo, hi]; scalar tests skip the VALU
 // work for blocks entirely inside (kept) or outside (zeroed) the band.
 template <bool COLFORM>
-__device__ __forceinline__ f32x4 band_block(f32x4 x, int m, int lo, int hi) {
+__device__ __forceinline__ f32x4 band_block(f32x4 x, int m, int lo, int hi,
+                                            Lane ln = lane_here()) {
   if (!blk_nz(m, lo, hi)) return zero4();
   if (blk_all_in(m, lo, hi)) return x;
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
-    const int d = COLFORM ? dcol(m, v) : drow(m, v);
+    const int d = COLFORM ? dcol(m, v, ln) : drow(m, v, ln);
     x[v] = (d >= lo && d <= hi) ? x[v] : 0.f;
   }
   return x;
@@ -211,24 +225,26 @@ __device__ __forceinline__ void mm(Acc<NB>& D, const RowP<NB, F>& X, int xlo, in
 // Layout changes through the identity: row form of a column-form matrix
 // (Z = I Z, row result) and column form of a row-form matrix (Z = Z I).
 template <int NB, typename F>
-__device__ __forceinline__ void col_to_row(Acc<NB>& D, const ColP<NB, F>& Z, int lo, int hi) {
+__device__ __forceinline__ void col_to_row(Acc<NB>& D, const ColP<NB, F>& Z, int lo, int hi,
+                                           Lane ln = lane_here()) {
   RowP<NB, F> id;
   Acc<NB> e;
 #pragma unroll
   for (int b = 0; b < nlower(NB); ++b) e.a[b] = zero4();
 #pragma unroll
-  for (int I = 0; I < NB; ++I) e.a[bidx(I, I)] = eye4();
+  for (int I = 0; I < NB; ++I) e.a[bidx(I, I)] = eye4(ln);
   to_rowp(id, e);
   mm<NB, true, false>(D, id, 0, 0, Z, lo, hi, lo, hi);
 }
 template <int NB, typename F>
-__device__ __forceinline__ void row_to_col(Acc<NB>& D, const RowP<NB, F>& Z, int lo, int hi) {
+__device__ __forceinline__ void row_to_col(Acc<NB>& D, const RowP<NB, F>& Z, int lo, int hi,
+                                           Lane ln = lane_here()) {
   ColP<NB, F> id;
   Acc<NB> e;
 #pragma unroll
   for (int b = 0; b < nlower(NB); ++b) e.a[b] = zero4();
 #pragma unroll
-  for (int I = 0; I < NB; ++I) e.a[bidx(I, I)] = eye4();
+  for (int I = 0; I < NB; ++I) e.a[bidx(I, I)] = eye4(ln);
   to_colp(id, e);
   mm<NB, false, false>(D, Z, lo, hi, id, 0, 0, lo, hi);
 }
