@@ -117,7 +117,11 @@ int gdn_wy_apply(const void* Tinv, const void* K, const void* V, const float* be
  * gdn_wy_apply with every intermediate kept on chip.  Tinv may be NULL;
  * otherwise the approximate inverse is also written ([B, H, L/C, C, C]).
  * dtype applies to K, V, W, U and Tinv.  A is formed in fp32 and rounded to
- * the compute dtype as an MFMA operand. */
+ * the compute dtype as an MFMA operand.  C = 128 uses the block form of
+ * Appendix E with the 64-row halves 1, 2: W_1 = X_11 diag(beta_1) K_1 and
+ * W_2 = X_22 (diag(beta_2) K_2 - A_21 W_1) (the same for U), which equals
+ * Tinv diag(beta) K for the block inverse gdn_chunk_inverse_neumann
+ * computes; X_21 = -X_22 A_21 X_11 is formed only when Tinv is requested. */
 int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const float* g,
                        void* W, void* U, void* Tinv, int B, int L, int H, int dk,
                        int dv, int C, int N, int S, int dtype, void* stream);

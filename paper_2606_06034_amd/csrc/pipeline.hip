@@ -148,11 +148,12 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 // time).  Each 16 x 16 block of X is moved to column form by an identity
 // MFMA (X I), then W(I, .) = sum_K T'(I, K) X(K, .) comes out in row form and
 // is stored 8 features per lane.  ob points at (token t0, head h, feature 0)
-// of the output.
+// of the output; lds_copy (optional) receives the output pairs in the slot
+// layout LdsRows reads.
 template <int NB, int D, typename F, typename TIO, typename Get>
 __device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, Get&& get,
                                             TIO* __restrict__ ob, int64_t ld,
-                                            Lane ln = lane_here()) {
+                                            Lane ln = lane_here(), TIO* lds_copy = nullptr) {
   const int g = ln.g(), c = ln.c();
   const f32x4 e = eye4(ln);
   const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
@@ -181,6 +182,7 @@ __device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, Get&& get,
         for (int p = 0; p < npair(NB); ++p)
           if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(TR.r[I][p], y[h][p], acc[h]);
       store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
+      if (lds_copy) store_row8(lds_copy + 512 * (I * (D / 32) + q) + 8 * ln.id, acc[0], acc[1]);
     }
   }
 }
@@ -191,12 +193,13 @@ struct RegRows {
   const Pair<F> (&xp)[NB][D / 32];
   __device__ __forceinline__ Pair<F> operator()(int I, int q) const { return xp[I][q]; }
 };
-template <int D>
+// slot (I, q) of an LDS copy: 8 elements per lane, lane-major
+template <int D, typename F = bf16x4, typename TIO = __bf16>
 struct LdsRows {
-  const __bf16* s;
+  const TIO* s;
   int l;
-  __device__ __forceinline__ Pair<bf16x4> operator()(int I, int q) const {
-    return Pair<bf16x4>{*(const bf16x8*)(s + 512 * (I * (D / 32) + q) + 8 * l)};
+  __device__ __forceinline__ Pair<F> operator()(int I, int q) const {
+    return load_row8<F>(s + 512 * (I * (D / 32) + q) + 8 * l);
   }
 };
 
@@ -349,6 +352,254 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
 }
 
 // ---------------------------------------------------------------------------
+// gdn_chunk_wy_fused at C = 128: the block form of Appendix E with two waves
+// per chunk.  With the 64-row halves 1, 2 of the chunk, X_kk the inverses of
+// (I + A_kk) by the engine and X_21 = -X_22 A_21 X_11,
+//   W_1 = X_11 diag(beta_1) K_1,
+//   W_2 = X_21 diag(beta_1) K_1 + X_22 diag(beta_2) K_2
+//       = X_22 (diag(beta_2) K_2 - A_21 W_1),
+// and the same for U with V, so X_21 itself is only formed for Tout.
+// Wave 0 runs the C = 64 pipeline on half 1 and leaves K_1, W_1 and U_1 in
+// LDS; wave 1 inverts its diagonal block meanwhile, then builds A_21 from
+// K_2 and the LDS copy of K_1 and forms Z = diag(beta_2) X_2 - A_21 X_1 slice
+// by slice (32 features) followed by X_22 Z.  Phases are separated by
+// workgroup barriers; every branch below is uniform per wave.
+
+// A_21 (times `sign`): rows in half 2, columns in half 1, all entries live;
+// row form, blocks [I][J]
+template <typename F>
+__device__ __forceinline__ void gate_rect(f32x4 (&G)[4][4], const float* sb2, const float* sg2,
+                                          const float* sg1, float sign, Lane ln) {
+  const int g = ln.g(), c = ln.c();
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = I * 16 + c, j = J * 16 + 4 * g + v;
+        G[I][J][v] = sign * sb2[i] * G[I][J][v] * __expf(sg2[i] - sg1[j]);
+      }
+}
+
+// one 32-feature slice of out_2 = X_22 (diag(beta_2) X_2 - A_21 out_1):
+// x2[I] the row pairs of X_2 (rows of half 2), o1[K] those of out_1 (half 1)
+template <typename F, typename TIO>
+__device__ __forceinline__ void block2_slice(const RowP<4, F>& X22R, const Pair<F> (&NA)[4][2],
+                                             const Pair<F> (&x2)[4], const Pair<F> (&o1)[4],
+                                             const float* sb2, TIO* __restrict__ ob, int64_t ld,
+                                             int q, Lane ln) {
+  const int g = ln.g(), c = ln.c();
+  const f32x4 e = eye4(ln);
+  const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
+  // out_1 slice in column form
+  Pair<F> y1[2][2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+      y1[h][p] = Pair<F>::make(Pair<F>::template mma<false>(o1[2 * p], h ? id1 : id0, zero4()),
+                               Pair<F>::template mma<false>(o1[2 * p + 1], h ? id1 : id0, zero4()));
+  // Z rows (row form, the feature order of the pairs), diag(beta_2) X_2 in
+  // the accumulator
+  Pair<F> z[4];
+#pragma unroll
+  for (int I = 0; I < 4; ++I) {
+    const float bi = sb2[I * 16 + c];
+    f32x4 acc[2] = {bi * x2[I].lo(), bi * x2[I].hi()};
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) acc[h] = Pair<F>::template mma<true>(NA[I][p], y1[h][p], acc[h]);
+    z[I] = Pair<F>::make(acc[0], acc[1]);
+  }
+  // X_22 Z
+  Pair<F> y2[2][2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+      y2[h][p] = Pair<F>::make(Pair<F>::template mma<false>(z[2 * p], h ? id1 : id0, zero4()),
+                               Pair<F>::template mma<false>(z[2 * p + 1], h ? id1 : id0, zero4()));
+#pragma unroll
+  for (int I = 0; I < 4; ++I) {
+    f32x4 acc[2] = {zero4(), zero4()};
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+        if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(X22R.r[I][p], y2[h][p], acc[h]);
+    store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
+  }
+}
+
+template <int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO>
+__global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
+                                                  const TIO* __restrict__ V,
+                                                  const float* __restrict__ beta,
+                                                  const float* __restrict__ g,
+                                                  TIO* __restrict__ W, TIO* __restrict__ U,
+                                                  TIO* __restrict__ Tout, int L, int H, int N,
+                                                  int S) {
+  constexpr int NB = 4, C = 128;
+  __shared__ float sb[C], sg[C];
+  __shared__ __attribute__((aligned(16))) TIO sK1[NB * (DK / 32) * 512];
+  __shared__ __attribute__((aligned(16))) TIO sW1[NB * (DK / 32) * 512];
+  __shared__ __attribute__((aligned(16))) TIO sU1[NB * (DV / 32) * 512];
+  const Chunk ch(blockIdx.x, L, H, C);
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const Lane ln = lane_here();
+  const int64_t ldk = (int64_t)H * DK, ldv = (int64_t)H * DV;
+  {
+    const int r = threadIdx.x;  // 128 threads, one row each
+    const int64_t o = ((int64_t)ch.b * L + ch.t0 + r) * H + ch.h;
+    sb[r] = beta[o];
+    sg[r] = g[o];
+  }
+  // ---- this wave's half: K rows, A_kk, X_kk
+  const int r0 = 64 * wv;
+  Pair<F> kp[NB][DK / 32];
+  load_rows<NB, DK>(kp, K + ch.row(r0, L, H, DK), ldk);
+  if (wv == 0) {
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int q = 0; q < DK / 32; ++q) {
+        TIO* d = sK1 + 512 * (I * (DK / 32) + q) + 8 * ln.id;
+        store_row8(d, kp[I][q].lo(), kp[I][q].hi());
+      }
+  }
+  __syncthreads();  // gates and K_1 in LDS
+  Acc<NB> Tr;
+  {
+    RowP<NB, F> LR;
+    Acc<NB> Lc;
+    gram_lower<NB, DK, false>(Lc, kp);
+    gate_scale<NB, false>(Lc, sb + r0, sg + r0, -1.f);  // Lm = -A_kk, column form
+    ColP<NB, F> LC;
+    to_colp(LC, Lc);
+    Acc<NB> r;
+    col_to_row(r, LC, 1, 63);
+    to_rowp(LR, r);
+    neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
+  }
+#pragma unroll
+  for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
+  if (wv == 0) {
+    // ---- half 1: Tout rows 0..63, then W_1, U_1 (to HBM and LDS)
+    if (Tout) {
+      TIO* t = Tout + ch.tile * (C * C);
+      store_unit_row<NB>(t, C, Tr);
+#pragma unroll
+      for (int I = 0; I < NB; ++I)
+#pragma unroll
+        for (int J = 0; J < NB; ++J) store4(t + (I * 16 + ln.c()) * C + 64 + J * 16 + 4 * ln.g(), zero4());
+    }
+    RowP<NB, F> TR;
+    scale_cols(TR, Tr, sb);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, sW1);
+    Pair<F> vp[NB][DV / 32];
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln, sU1);
+  }
+  __syncthreads();  // W_1, U_1 (and Tout rows 0..63) written
+  if (wv == 1) {
+    // ---- half 2
+    RowP<NB, F> X22R;
+    to_rowp(X22R, Tr);
+    Pair<F> NA[4][2];  // -A_21, row pairs
+    {
+      f32x4 G[4][4];
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int J = 0; J < 4; ++J) G[I][J] = zero4();
+#pragma unroll
+      for (int q = 0; q < DK / 32; ++q) {
+        Pair<F> k1[4];
+#pragma unroll
+        for (int J = 0; J < 4; ++J) k1[J] = LdsRows<DK, F, TIO>{sK1, ln.id}(J, q);
+#pragma unroll
+        for (int I = 0; I < 4; ++I)
+#pragma unroll
+          for (int J = 0; J < 4; ++J) G[I][J] = Pair<F>::template mma<true>(kp[I][q], k1[J], G[I][J]);
+      }
+      gate_rect<F>(G, sb + 64, sg + 64, sg, -1.f, ln);
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) NA[I][p] = Pair<F>::make(G[I][2 * p], G[I][2 * p + 1]);
+    }
+#pragma unroll
+    for (int q = 0; q < DK / 32; ++q) {
+      Pair<F> x2[4], o1[4];
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        x2[I] = kp[I][q];
+        o1[I] = LdsRows<DK, F, TIO>{sW1, ln.id}(I, q);
+      }
+      block2_slice<F>(X22R, NA, x2, o1, sb + 64, W + ch.row(64, L, H, DK), ldk, q, ln);
+    }
+#pragma unroll
+    for (int q = 0; q < DV / 32; ++q) {
+      Pair<F> x2[4], o1[4];
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        x2[I] = load_row8<F>(V + ch.row(64 + I * 16 + ln.c(), L, H, DV) + 32 * q + 8 * ln.g());
+        o1[I] = LdsRows<DV, F, TIO>{sU1, ln.id}(I, q);
+      }
+      block2_slice<F>(X22R, NA, x2, o1, sb + 64, U + ch.row(64, L, H, DV), ldv, q, ln);
+    }
+    if (Tout) {
+      // X_21 = X_22 (-A_21 X_11), X_11 read back from Tout (written by wave 0
+      // before the barrier), then X_22 itself
+      TIO* t = Tout + ch.tile * (C * C);
+      ColP<NB, F> X11C;
+      {
+        Acc<NB> x;
+#pragma unroll
+        for (int I = 0; I < NB; ++I)
+#pragma unroll
+          for (int J = 0; J <= I; ++J)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              x.a[bidx(I, J)][v] = load1(t + (I * 16 + 4 * ln.g() + v) * C + J * 16 + ln.c());
+        to_colp(X11C, x);
+      }
+      Pair<F> MC[2][4];  // M = -A_21 X_11, column pairs
+      {
+        f32x4 M[4][4];
+#pragma unroll
+        for (int I = 0; I < 4; ++I)
+#pragma unroll
+          for (int J = 0; J < 4; ++J) {
+            f32x4 acc = zero4();
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+              if (2 * p + 1 >= J) acc = Pair<F>::template mma<false>(NA[I][p], X11C.c[p][J], acc);
+            M[I][J] = acc;
+          }
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+          for (int J = 0; J < 4; ++J) MC[p][J] = Pair<F>::make(M[2 * p][J], M[2 * p + 1][J]);
+      }
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int J = 0; J < 4; ++J) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int p = 0; p < 2; ++p)
+            if (2 * p <= I) acc = Pair<F>::template mma<true>(X22R.r[I][p], MC[p][J], acc);
+          store4(t + (64 + I * 16 + ln.c()) * C + J * 16 + 4 * ln.g(), acc);
+        }
+      store_unit_row<NB>(t + 64 * C + 64, C, Tr);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 
 #define GDN_DK_SWITCH(dk, ...)                     \
@@ -470,10 +721,32 @@ static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, 
 }
 
 template <typename F, typename TIO>
+static hipError_t run_fused128(const void* K, const void* V, const float* beta, const float* g,
+                               void* W, void* U, void* T, int64_t n, int L, int H, int dk,
+                               int dv, int N, int S, hipStream_t st) {
+#define GDN_F128(SM, NC_, SC_)                                                                 \
+  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO>), dim3((unsigned)n), dim3(128), \
+                     0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, \
+                     H, N, S)
+  GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
+    if (N == 3 && S == 8)
+      GDN_F128(true, 3, 8);
+    else if (N <= 15)
+      GDN_F128(true, -1, -1);
+    else
+      GDN_F128(false, -1, -1);
+    return hipGetLastError();
+  }))
+#undef GDN_F128
+  return hipErrorNotSupported;
+}
+
+template <typename F, typename TIO>
 static hipError_t run_fused(const void* K, const void* V, const float* beta, const float* g,
                             void* W, void* U, void* T, int64_t n, int L, int H, int dk, int dv,
                             int C, int N, int S, hipStream_t st) {
   switch (C) {
+    case 128: return run_fused128<F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
     case 16: return run_fused_nb<1, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
     case 32: return run_fused_nb<2, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
     case 64: return run_fused_nb<4, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);

@@ -216,14 +216,21 @@ def test_wy_apply(C, dt):
         assert err <= tol
 
 
+def ref_inverse(A, N, S):
+    """The oracle's T_hat(N, S); C = 128 by the two-block form."""
+    if A.shape[-1] == 128:
+        return gdn.neumann_inverse_blocked(A, N, S)
+    return gdn.neumann_inverse(A, N, S)
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
 def test_fused(C, dt):
     w = wl.workload("tiny").with_(dtype=dt, L=4 * max(C, 64))
     K, beta, g, V = head_inputs(w, C, 2, dt)
     N, S = gdn.default_order(C)
     A = gdn.build_A(K, beta, g, C)
-    Tr = gdn.neumann_inverse(A, N, S)
+    Tr = ref_inverse(A, N, S)
     Wr, Ur = gdn.wy_apply(Tr, K, V, beta, C)
     W, U, T = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S, want_T=True)
     T, W, U = host(T), host(W), host(U)
@@ -236,6 +243,34 @@ def test_fused(C, dt):
     # without the optional Tinv output
     W2, U2 = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S)
     assert np.array_equal(host(W2), W) and np.array_equal(host(U2), U)
+
+
+FUSED_ORDERS = {16: [(0, 5), (2, 0)], 32: [(1, 3), (3, 7)], 64: [(4, 3), (3, 15), (0, 2)],
+                128: [(3, 1), (4, 3), (3, 15)]}
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_fused_stress_and_orders(C, dt):
+    """Stress heads (|A| up to ~0.5) at non-default orders, and dk = dv = 64."""
+    for dk in (128, 64):
+        heads = [wl.gen_stress_head(2 * max(C, 64), dk, C, seed=40 + h, dv=dk) for h in range(2)]
+        K, beta, g, V = (stored(wl.as_blhd(*[x[i] for x in heads]), dt if i in (0, 3) else "f32")
+                         for i in range(4))
+        A = gdn.build_A(K, beta, g, C)
+        for N, S in FUSED_ORDERS[C]:
+            Tr = ref_inverse(A, N, S)
+            Wr, Ur = gdn.wy_apply(Tr, K, V, beta, C)
+            W, U, T = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S,
+                                           want_T=True)
+            scale = max(1.0, np.max(np.abs(Tr)))
+            eT = maxerr(host(T), Tr)
+            eW, eU = maxerr(host(W), Wr), maxerr(host(U), Ur)
+            print(f"fused stress C={C} {dt} dk={dk} N={N} S={S} T {eT:.2e} W {eW:.2e} "
+                  f"U {eU:.2e}", flush=True)
+            assert eT <= TOL[dt] * scale
+            assert eW <= TOL[dt] * scale * max(1.0, np.max(np.abs(Wr)))
+            assert eU <= TOL[dt] * scale * max(1.0, np.max(np.abs(Ur)))
 
 
 def test_fused_matches_unfused_composition():
@@ -258,13 +293,18 @@ def test_fused_matches_unfused_composition():
 
 
 def _sampled_check(wname, C=None, n_sample=16, seed=0):
+    """Fused launch over the whole workload; the oracle recomputes sampled
+    tiles from their heads' inputs (regenerated per head)."""
     w = wl.workload(wname)
     C = C or w.C
     N, S = gdn.default_order(C)
-    K, beta, g, V = wl.gen_inputs(w, C=C)
     dt = w.dtype
-    W, U, T = G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N, S, want_T=True)
+    K, beta, g, V = wl.gen_inputs(w, C=C)
+    dK, dV = dev(K, dt), dev(V, dt)
+    del K, V
+    W, U, T = G.gdn_chunk_wy_fused(dK, dV, dev(beta), dev(g), C, N, S, want_T=True)
     torch.cuda.synchronize()
+    del dK, dV
     rng = np.random.default_rng(seed)
     n = w.B * w.H * (w.L // C)
     picks = sorted(set(rng.integers(0, n, n_sample).tolist()) | {0, n - 1})
@@ -272,10 +312,10 @@ def _sampled_check(wname, C=None, n_sample=16, seed=0):
     for t in picks:
         b, h, c = wl.tile_coords(w, t, C)
         sl = slice(c * C, (c + 1) * C)
-        Kt, bt, gt, Vt = (K[b:b + 1, sl, h:h + 1], beta[b:b + 1, sl, h:h + 1],
-                          g[b:b + 1, sl, h:h + 1], V[b:b + 1, sl, h:h + 1])
+        Kh, bh, gh, Vh = wl.gen_head(w, b, h, C=C)
+        Kt, bt, gt, Vt = (x[sl][None, :, None] for x in (Kh, bh, gh, Vh))
         A = gdn.build_A(Kt, bt, gt, C)
-        Tr = gdn.neumann_inverse(A, N, S)
+        Tr = ref_inverse(A, N, S)
         Wr, Ur = gdn.wy_apply(Tr, Kt, Vt, bt, C)
         Tg = T.view(-1, C, C)[t].float().cpu().numpy()
         Wg = W[b, sl, h].float().cpu().numpy()
@@ -291,6 +331,11 @@ def _sampled_check(wname, C=None, n_sample=16, seed=0):
 def test_qwen35_prefill_full_size_sampled():
     """The benchmarked workload (2048 tiles), in the launch the bench times."""
     _sampled_check("qwen35_prefill")
+
+
+def test_sweep_c128_full_size_sampled():
+    """Chunk-size sweep at C = 128 (B=4, H=32, L=16384: 16384 tiles), fused."""
+    _sampled_check("sweep", C=128)
 
 
 def test_binding_rejects_wrong_sizes():
