@@ -25,6 +25,10 @@
 #include "tile16.hpp"
 #include "launch.hpp"
 
+// wave reductions of the ROCm device library
+extern "C" __device__ __attribute__((const)) int __ockl_wfred_max_i32(int);
+extern "C" __device__ __attribute__((const)) float __ockl_wfred_max_f32(float);
+
 namespace gdn {
 namespace i8 {
 
@@ -121,18 +125,35 @@ __device__ __forceinline__ void band_i(AccI<NB>& D, int lo, int hi) {
     }
 }
 
-// round-half-even(y / 2^s) for s >= 0 and |y| < 2^30 (every value here stays
-// below 2^24, so s >= 31 always rounds to 0)
+// round-half-even(y / 2^s) for 1 <= s <= 30 and |y| < 2^30 (every value
+// here stays below 2^24)
+__device__ __forceinline__ int rne_pos(int y, int s) {
+  return (y + (1 << (s - 1)) - 1 + ((y >> s) & 1)) >> s;
+}
+// any s >= 0 (s >= 31 rounds every |y| < 2^30 to 0)
 __device__ __forceinline__ int rne_sh(int y, int s) {
   if (s <= 0) return y;
   if (s >= 31) return 0;
-  return (y + (1 << (s - 1)) - 1 + ((y >> s) & 1)) >> s;
+  return rne_pos(y, s);
 }
 
+// wave-wide maximum (the device library's DPP reduction), as a scalar
 __device__ __forceinline__ int wave_max(int x) {
+  return __builtin_amdgcn_readfirstlane(__ockl_wfred_max_i32(x));
+}
+
+// every entry rounded by a wave-uniform shift s >= 1
+template <int NB>
+__device__ __forceinline__ void shift_all(AccI<NB>& D, int s) {
+  if (s >= 31) {
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = max(x, __shfl_xor(x, o));
-  return __builtin_amdgcn_readfirstlane(x);
+    for (int b = 0; b < nlower(NB); ++b) D.a[b] = zero_i4();
+    return;
+  }
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) D.a[b][v] = rne_pos(D.a[b][v], s);
 }
 
 template <int NB>
@@ -158,12 +179,7 @@ template <int NB>
 __device__ __forceinline__ void requant(AccI<NB>& D, int e_in, int& e_out, bool& nz) {
   const int amax = amax_of(D);
   const int s = shift_for(amax);
-  if (s > 0) {
-#pragma unroll
-    for (int b = 0; b < nlower(NB); ++b)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) D.a[b][v] = rne_sh(D.a[b][v], s);
-  }
+  if (s > 0) shift_all(D, s);
   nz = amax > 0;
   e_out = nz ? e_in + s : 0;
 }
@@ -190,21 +206,28 @@ __device__ __forceinline__ void rs_add(RunSum<NB>& R, const AccI<NB>& t, int et,
     R.e = top;
     R.any = true;
   } else if (top > R.e) {
-    const int d = top - R.e;
+    shift_all(R.acc, top - R.e);
+    R.e = top;
+  }
+  // the shift is wave-uniform: one branch, not a select per entry
+  const int sh = et - R.e;
+  if (sh >= 0) {
 #pragma unroll
     for (int b = 0; b < nlower(NB); ++b)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) R.acc.a[b][v] = rne_sh(R.acc.a[b][v], d);
-    R.e = top;
+      for (int v = 0; v < 4; ++v) {
+        const int x = negate ? -t.a[b][v] : t.a[b][v];
+        R.acc.a[b][v] += x << sh;
+      }
+  } else if (sh > -31) {
+#pragma unroll
+    for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = negate ? -t.a[b][v] : t.a[b][v];
+        R.acc.a[b][v] += rne_pos(x, -sh);
+      }
   }
-  const int sh = et - R.e;
-#pragma unroll
-  for (int b = 0; b < nlower(NB); ++b)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int x = negate ? -t.a[b][v] : t.a[b][v];
-      R.acc.a[b][v] += sh >= 0 ? (x << sh) : rne_sh(x, -sh);
-    }
 }
 
 template <int NB>
@@ -409,9 +432,7 @@ __global__ __launch_bounds__(64) void k_quantize_i8(const float* __restrict__ A,
       m = fmaxf(m, fabsf(x[k][v]));
     }
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-  const float amax = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(m)));
+  const float amax = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
   int e = 0;
   if (amax > 0.f) {
     int p;
