@@ -60,19 +60,25 @@ template <int NB>
 __device__ __forceinline__ i32x4 blki(const AccI<NB>& D, int I, int J) {
   return (J <= I && I < NB) ? D.a[bidx(I, J)] : zero_i4();
 }
+// Quads from blocks; blocks that cannot meet the band [lo, hi] (structurally
+// zero) are packed as constant zeros.
 template <int NB>
-__device__ __forceinline__ void to_rowq(RowQ<NB>& X, const AccI<NB>& D) {
+__device__ __forceinline__ void to_rowq(RowQ<NB>& X, const AccI<NB>& D, int lo = 0,
+                                        int hi = 16 * NB) {
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
-    for (int K = 0; K < 4; ++K) X.r[I].v[K] = pack4(blki(D, I, K));
+    for (int K = 0; K < 4; ++K)
+      X.r[I].v[K] = (K <= I && I < NB && blk_nz(I - K, lo, hi)) ? pack4(D.a[bidx(I, K)]) : 0;
 }
 template <int NB>
-__device__ __forceinline__ void to_colq(ColQ<NB>& Y, const AccI<NB>& D) {
+__device__ __forceinline__ void to_colq(ColQ<NB>& Y, const AccI<NB>& D, int lo = 0,
+                                        int hi = 16 * NB) {
 #pragma unroll
   for (int J = 0; J < NB; ++J)
 #pragma unroll
-    for (int K = 0; K < 4; ++K) Y.c[J].v[K] = pack4(blki(D, K, J));
+    for (int K = 0; K < 4; ++K)
+      Y.c[J].v[K] = (K >= J && K < NB && blk_nz(K - J, lo, hi)) ? pack4(D.a[bidx(K, J)]) : 0;
 }
 
 // D = X Y (lower), blocks outside [olo, ohi] set to 0; OUTQ: row-form result.
@@ -156,13 +162,20 @@ __device__ __forceinline__ void shift_all(AccI<NB>& D, int s) {
     for (int v = 0; v < 4; ++v) D.a[b][v] = rne_pos(D.a[b][v], s);
 }
 
+// The helpers below visit only the blocks that can meet a band [lo, hi] of
+// sub-diagonals; every other block of their operand is exactly zero by the
+// structure of the computation, so skipping it changes no result.
+
 template <int NB>
-__device__ __forceinline__ int amax_of(const AccI<NB>& D) {
+__device__ __forceinline__ int amax_of(const AccI<NB>& D, int lo, int hi) {
   int m = 0;
 #pragma unroll
-  for (int b = 0; b < nlower(NB); ++b)
+  for (int I = 0; I < NB; ++I)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) m = max(m, abs(D.a[b][v]));
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) m = max(m, abs(D.a[bidx(I, J)][v]));
   return wave_max(m);
 }
 
@@ -174,66 +187,94 @@ __device__ __forceinline__ int shift_for(int amax) {
   return s;
 }
 
+// every entry rounded by a wave-uniform shift s >= 1
+template <int NB>
+__device__ __forceinline__ void shift_all(AccI<NB>& D, int s, int lo, int hi) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, lo, hi)) {
+        if (s >= 31) {
+          D.a[bidx(I, J)] = zero_i4();
+        } else {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) D.a[bidx(I, J)][v] = rne_pos(D.a[bidx(I, J)][v], s);
+        }
+      }
+}
+
 // requantise in place; returns (new exponent, non-zero flag) through refs
 template <int NB>
-__device__ __forceinline__ void requant(AccI<NB>& D, int e_in, int& e_out, bool& nz) {
-  const int amax = amax_of(D);
+__device__ __forceinline__ void requant(AccI<NB>& D, int lo, int hi, int e_in, int& e_out,
+                                        bool& nz) {
+  const int amax = amax_of(D, lo, hi);
   const int s = shift_for(amax);
-  if (s > 0) shift_all(D, s);
+  if (s > 0) shift_all(D, s, lo, hi);
   nz = amax > 0;
   e_out = nz ? e_in + s : 0;
 }
 
-// exact running int32 sum
+// exact running int32 sum over the band [lo, hi] (the union of its terms')
 template <int NB> struct RunSum {
   AccI<NB> acc;
   int e;
   bool any;
+  int lo, hi;
 };
 template <int NB>
-__device__ __forceinline__ void rs_init(RunSum<NB>& R) {
+__device__ __forceinline__ void rs_init(RunSum<NB>& R, int lo, int hi) {
 #pragma unroll
   for (int b = 0; b < nlower(NB); ++b) R.acc.a[b] = zero_i4();
   R.e = 0;
   R.any = false;
+  R.lo = lo;
+  R.hi = hi;
 }
+// add the term t (band [tlo, thi] inside the sum's) of exponent et, |t| < 2^bits
 template <int NB>
-__device__ __forceinline__ void rs_add(RunSum<NB>& R, const AccI<NB>& t, int et, int bits,
-                                       bool present, bool negate = false) {
+__device__ __forceinline__ void rs_add(RunSum<NB>& R, const AccI<NB>& t, int tlo, int thi,
+                                       int et, int bits, bool present, bool negate = false) {
   if (!present) return;
   const int top = et + bits - kAlignBits;
   if (!R.any) {
     R.e = top;
     R.any = true;
   } else if (top > R.e) {
-    shift_all(R.acc, top - R.e);
+    shift_all(R.acc, top - R.e, R.lo, R.hi);
     R.e = top;
   }
   // the shift is wave-uniform: one branch, not a select per entry
   const int sh = et - R.e;
   if (sh >= 0) {
 #pragma unroll
-    for (int b = 0; b < nlower(NB); ++b)
+    for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int x = negate ? -t.a[b][v] : t.a[b][v];
-        R.acc.a[b][v] += x << sh;
-      }
+      for (int J = 0; J <= I; ++J)
+        if (blk_nz(I - J, tlo, thi))
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int x = negate ? -t.a[bidx(I, J)][v] : t.a[bidx(I, J)][v];
+            R.acc.a[bidx(I, J)][v] += x << sh;
+          }
   } else if (sh > -31) {
 #pragma unroll
-    for (int b = 0; b < nlower(NB); ++b)
+    for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int x = negate ? -t.a[b][v] : t.a[b][v];
-        R.acc.a[b][v] += rne_pos(x, -sh);
-      }
+      for (int J = 0; J <= I; ++J)
+        if (blk_nz(I - J, tlo, thi))
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int x = negate ? -t.a[bidx(I, J)][v] : t.a[bidx(I, J)][v];
+            R.acc.a[bidx(I, J)][v] += rne_pos(x, -sh);
+          }
   }
 }
 
 template <int NB>
 __device__ __forceinline__ void rs_finish(RunSum<NB>& R, AccI<NB>& q, int& e, bool& nz) {
   q = R.acc;
-  requant(q, R.any ? R.e : 0, e, nz);
+  requant(q, R.lo, R.hi, R.any ? R.e : 0, e, nz);
 }
 
 template <int NB>
@@ -246,14 +287,18 @@ __device__ __forceinline__ void unpack_row(AccI<NB>& D, const RowQ<NB>& X) {
 
 // ---------------------------------------------------------------------------
 
-template <int NB>
+// NC, SC >= 0 fix N and S at compile time (every band and block skip is then
+// resolved by the compiler); -1 takes them from the arguments.
+template <int NB, int NC = -1, int SC = -1>
 __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq,
                                                    const int32_t* __restrict__ eA,
                                                    int8_t* __restrict__ Tq,
                                                    int32_t* __restrict__ eT,
-                                                   float* __restrict__ Tdeq, int N, int S) {
+                                                   float* __restrict__ Tdeq, int Nrt, int Srt) {
   constexpr int C = 16 * NB;
   constexpr int ACCB = 14 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |acc| < C * 2^14
+  const int N = NC >= 0 ? NC : Nrt;
+  const int S = SC >= 0 ? SC : Srt;
   const int64_t tile = blockIdx.x;
   const int g = lane_g(), c = lane_c();
   const int8_t* a = Aq + tile * (C * C);
@@ -275,35 +320,41 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
       Lr.a[bidx(I, J)] = x;
     }
   const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
-  const bool nzL = amax_of(Lr) > 0;
+  const bool nzL = amax_of(Lr, 1, C - 1) > 0;
   RowQ<NB> LRq;
-  to_rowq(LRq, Lr);
+  to_rowq(LRq, Lr, 1, C - 1);
   ColQ<NB> LCq;
   {
     AccI<NB> t;
     mmi<NB, false>(t, LRq, Ic, 1, C - 1);  // Lm I, column form
-    to_colq(LCq, t);
+    to_colq(LCq, t, 1, C - 1);
   }
 
-  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm), row form
+  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm) (band n..N), row form
   RunSum<NB> ns;
-  rs_init(ns);
+  rs_init(ns, 1, N);
   if (N >= 1) {
     AccI<NB> B = Lr;
     band_i<NB, false>(B, 1, N);
     int eB;
     bool nzB;
-    requant(B, eL, eB, nzB);
-    rs_add(ns, B, eB, 7, nzB);
+    requant(B, 1, N, eL, eB, nzB);
+    rs_add(ns, B, 1, N, eB, 7, nzB);
     RowQ<NB> Bq;
-    to_rowq(Bq, B);
-    for (int n = 2; n <= N; ++n) {
+    to_rowq(Bq, B, 1, N);
+    auto power = [&](int n) {
       AccI<NB> D;
       mmi<NB, true>(D, Bq, LCq, n, N);
       band_i<NB, false>(D, n, N);
-      requant(D, eB + eL, eB, nzB);
-      rs_add(ns, D, eB, 7, nzB);
-      to_rowq(Bq, D);
+      requant(D, n, N, eB + eL, eB, nzB);
+      rs_add(ns, D, n, N, eB, 7, nzB);
+      to_rowq(Bq, D, n, N);
+    };
+    if constexpr (NC >= 0) {
+#pragma unroll
+      for (int n = 2; n <= NC; ++n) power(n);
+    } else {
+      for (int n = 2; n <= N; ++n) power(n);
     }
   }
   AccI<NB> N0r;
@@ -311,15 +362,15 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   bool nzN0;
   rs_finish(ns, N0r, eN0, nzN0);
   RowQ<NB> N0q;
-  to_rowq(N0q, N0r);
+  to_rowq(N0q, N0r, 1, N);
   ColQ<NB> N0c;
   {
     AccI<NB> t;
-    mmi<NB, false>(t, N0q, Ic, 0, C - 1);
-    to_colq(N0c, t);
+    mmi<NB, false>(t, N0q, Ic, 1, N);
+    to_colq(N0c, t, 1, N);
   }
 
-  // ---- E = Lm + Lm N0 - N0 (row form), band zeroed
+  // ---- E = Lm + Lm N0 - N0 (row form), band 1..N zeroed
   RowQ<NB> ERq;
   ColQ<NB> ECq;
   AccI<NB> Ecol;
@@ -327,34 +378,42 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   bool nzE;
   {
     AccI<NB> LN;
-    mmi<NB, true>(LN, LRq, N0c, 1, C - 1);
+    mmi<NB, true>(LN, LRq, N0c, 2, C - 1);
     RunSum<NB> es;
-    rs_init(es);
-    rs_add(es, Lr, eL, 7, nzL);
-    rs_add(es, LN, eL + eN0, ACCB, nzL && nzN0);
-    rs_add(es, N0r, eN0, 7, nzN0, true);
+    rs_init(es, 1, C - 1);
+    rs_add(es, Lr, 1, C - 1, eL, 7, nzL);
+    rs_add(es, LN, 2, C - 1, eL + eN0, ACCB, nzL && nzN0);
+    rs_add(es, N0r, 1, N, eN0, 7, nzN0, true);
     band_i<NB, false>(es.acc, N + 1, C - 1);
+    es.lo = N + 1;
     AccI<NB> Er;
     rs_finish(es, Er, eE, nzE);
-    to_rowq(ERq, Er);
+    to_rowq(ERq, Er, N + 1, C - 1);
     mmi<NB, false>(Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
-    to_colq(ECq, Ecol);
+    to_colq(ECq, Ecol, N + 1, C - 1);
   }
 
-  // ---- residual powers P_s = E P_{s-1} (column form), Gs = sum
+  // ---- residual powers P_s = E P_{s-1} (column form, band s(N+1)..), Gs = sum
   RunSum<NB> gs;
-  rs_init(gs);
+  rs_init(gs, N + 1, C - 1);
   if (S >= 1) {
-    rs_add(gs, Ecol, eE, 7, nzE);
+    rs_add(gs, Ecol, N + 1, C - 1, eE, 7, nzE);
     ColQ<NB> Pq = ECq;
     int eP = eE;
     bool nzP = nzE;
-    for (int s = 2; s <= S; ++s) {
+    auto chain = [&](int s) {
+      const int lo = s * (N + 1);
       AccI<NB> D;
-      mmi<NB, false>(D, ERq, Pq, 1, C - 1);
-      requant(D, eE + eP, eP, nzP);
-      rs_add(gs, D, eP, 7, nzP);
-      to_colq(Pq, D);
+      mmi<NB, false>(D, ERq, Pq, lo, C - 1);
+      requant(D, lo, C - 1, eE + eP, eP, nzP);
+      rs_add(gs, D, lo, C - 1, eP, 7, nzP);
+      to_colq(Pq, D, lo, C - 1);
+    };
+    if constexpr (SC >= 0) {
+#pragma unroll
+      for (int s = 2; s <= SC; ++s) chain(s);
+    } else {
+      for (int s = 2; s <= S; ++s) chain(s);
     }
   }
   AccI<NB> Gc;
@@ -362,9 +421,9 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   bool nzG;
   rs_finish(gs, Gc, eG, nzG);
   ColQ<NB> GCq;
-  to_colq(GCq, Gc);
+  to_colq(GCq, Gc, N + 1, C - 1);
   AccI<NB> Gr;
-  mmi<NB, true>(Gr, Iq, GCq, 1, C - 1);  // row form of Gs (exact codes)
+  mmi<NB, true>(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
 
   // ---- T = N0 + Gs + N0 Gs (row form), strict part
   AccI<NB> Tr;
@@ -372,12 +431,12 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   bool nzT;
   {
     AccI<NB> NG;
-    mmi<NB, true>(NG, N0q, GCq, 1, C - 1);
+    mmi<NB, true>(NG, N0q, GCq, N + 2, C - 1);
     RunSum<NB> ts;
-    rs_init(ts);
-    rs_add(ts, N0r, eN0, 7, nzN0);
-    rs_add(ts, Gr, eG, 7, nzG);
-    rs_add(ts, NG, eN0 + eG, ACCB, nzN0 && nzG);
+    rs_init(ts, 1, C - 1);
+    rs_add(ts, N0r, 1, N, eN0, 7, nzN0);
+    rs_add(ts, Gr, N + 1, C - 1, eG, 7, nzG);
+    rs_add(ts, NG, N + 2, C - 1, eN0 + eG, ACCB, nzN0 && nzG);
     band_i<NB, false>(ts.acc, 1, C - 1);
     rs_finish(ts, Tr, eTo, nzT);
   }
@@ -468,21 +527,25 @@ hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n
   return hipErrorNotSupported;
 }
 
+template <int NB, int DN, int DS>
+static hipError_t run_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                                 float* Tdeq, int64_t n, int N, int S, hipStream_t st) {
+  if (N == DN && S == DS)
+    hipLaunchKernelGGL((i8::k_neumann_i8<NB, DN, DS>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA,
+                       Tq, eT, Tdeq, N, S);
+  else
+    hipLaunchKernelGGL((i8::k_neumann_i8<NB>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
+                       eT, Tdeq, N, S);
+  return hipGetLastError();
+}
+
+// the default orders (3, 2), (3, 4), (3, 8) run compile-time specialisations
 hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
                              float* Tdeq, int64_t n, int C, int N, int S, hipStream_t st) {
   switch (C) {
-    case 16:
-      hipLaunchKernelGGL((i8::k_neumann_i8<1>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq, eT,
-                         Tdeq, N, S);
-      return hipGetLastError();
-    case 32:
-      hipLaunchKernelGGL((i8::k_neumann_i8<2>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq, eT,
-                         Tdeq, N, S);
-      return hipGetLastError();
-    case 64:
-      hipLaunchKernelGGL((i8::k_neumann_i8<4>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq, eT,
-                         Tdeq, N, S);
-      return hipGetLastError();
+    case 16: return run_neumann_i8<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 32: return run_neumann_i8<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 64: return run_neumann_i8<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
   }
   return hipErrorNotSupported;
 }
