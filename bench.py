@@ -14,9 +14,9 @@ the CPU oracle timed on a bounded sample of the same workload together with
 the GPU's max abs error against it on that sample.
 
 --path int8 runs the low-bit path (default workload "int8": B=4, H=32,
-L=16384, C=64, wide gates): build A in fp32 -> per-tile INT8 quantiser ->
-integer inverse T_hat(3, 8); its roofline is that of the integer inverse
-kernel, timed on its own.
+L=16384, C=64, wide gates) in one launch: build A in fp32 -> per-tile INT8
+quantiser -> integer inverse T_hat(3, 8); the same path as three launches
+is timed beside it for context.
 """
 
 from __future__ import annotations
@@ -123,15 +123,9 @@ def main():
     elif a.path == "inverse":
         step = lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT)
     elif a.path == "int8":
-        dA32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
-        dAq = torch.empty(dA32.shape, dtype=torch.int8, device="cuda")
-        deA = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
-        dTq, deT = torch.empty_like(dAq), torch.empty_like(deA)
-
-        def step():
-            G.gdn_build_A(dK, db, dg, C, A=dA32)
-            G.gdn_quantize_tiles_i8(dA32, Aq=dAq, eA=deA)
-            G.gdn_chunk_inverse_neumann_i8(dAq, deA, N, S, Tq=dTq, eT=deT)
+        dTq = torch.empty((w.B, w.H, w.L // C, C, C), dtype=torch.int8, device="cuda")
+        deT = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
+        step = lambda: G.gdn_chunk_inverse_neumann_i8_fused(dK, db, dg, C, N, S, Tq=dTq, eT=deT)
     else:
         step = lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT)
 
@@ -150,13 +144,24 @@ def main():
     ev_ms = e0.elapsed_time(e1) / a.steps  # HIP-event time per step (one launch for fused/inverse/fwdsub)
     ms_per_step = wall * 1e3 / a.steps
     value = n_tiles / (ms_per_step * 1e-3)
-    if a.path == "int8":  # the integer inverse kernel alone, same stream
-        e0.record(stream)
-        for _ in range(a.steps):
-            G.gdn_chunk_inverse_neumann_i8(dAq, deA, N, S, Tq=dTq, eT=deT)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        step_ms, ev_ms = ev_ms, e0.elapsed_time(e1) / a.steps
+    if a.path == "int8":  # context: the same path as three launches
+        dA32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
+        dAq = torch.empty(dA32.shape, dtype=torch.int8, device="cuda")
+        deA = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
+        dTq2, deT2 = torch.empty_like(dAq), torch.empty_like(deA)
+        stages = [lambda: G.gdn_build_A(dK, db, dg, C, A=dA32),
+                  lambda: G.gdn_quantize_tiles_i8(dA32, Aq=dAq, eA=deA),
+                  lambda: G.gdn_chunk_inverse_neumann_i8(dAq, deA, N, S, Tq=dTq2, eT=deT2)]
+        stage_ms = []
+        for fn in stages:
+            fn()
+            e0.record(stream)
+            for _ in range(a.steps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            stage_ms.append(e0.elapsed_time(e1) / a.steps)
+        del dA32, dAq
 
     # ---- algorithmic work per launch (measurement section)
     f_inv = (N + S) * 2 * C ** 3 * n_tiles  # dense-equivalent, the paper's product count
@@ -186,7 +191,8 @@ def main():
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
         kernel = "k_fwdsub"
     elif a.path == "int8":
-        bytes_ = n_tiles * (C * C * 2 + 8)
+        # K (dk per token) and beta, g in; int8 T_hat codes and exponents out
+        bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C + 4)
         flops = (N + S) * 2 * C ** 3 * n_tiles  # int8 ops of the N + S products
         if flops / bytes_ >= INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
             bound, peak, unit = "mfma", INT8_PEAK_TOPS, "TOP/s"
@@ -194,7 +200,7 @@ def main():
         else:
             bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
             achieved = bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = "k_neumann_i8"
+        kernel = "k_inverse_i8_fused"
     else:
         bytes_ = None
         flops = f_inv
@@ -228,7 +234,9 @@ def main():
     }
 
     if a.path == "int8":
-        out["config"]["step_ms_build_quantize_inverse"] = round(step_ms, 6)
+        out["config"]["three_launch_ms"] = {"build_A_f32": round(stage_ms[0], 6),
+                                            "quantize": round(stage_ms[1], 6),
+                                            "inverse_i8": round(stage_ms[2], 6)}
         out["dtype"] = "i8"
         if not a.no_cpu_baseline:
             out["cpu_baseline"] = cpu_baseline_int8(w, C, N, S, a, (K, beta, g), dTq, deT,

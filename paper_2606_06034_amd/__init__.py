@@ -22,6 +22,7 @@ from ._binding import (  # noqa: F401
     gdn_chunk_inverse_fwdsub,
     gdn_chunk_inverse_neumann,
     gdn_chunk_inverse_neumann_i8,
+    gdn_chunk_inverse_neumann_i8_fused,
     gdn_chunk_wy_fused,
     gdn_default_order,
     gdn_quantize_tiles_i8,

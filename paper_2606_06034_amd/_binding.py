@@ -28,6 +28,8 @@ _SIGS = {
                            _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_quantize_tiles_i8": [_vp, _vp, _vp, _c_i64, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_inverse_neumann_i8_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
+                                           _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
 }
 
 
@@ -223,4 +225,29 @@ def gdn_chunk_inverse_neumann_i8(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: 
         _dev(Tq, "Tq", torch.int8, Aq.numel()), _dev(eT, "eT", torch.int32, n),
         _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
         _stream(stream)))
+    return (Tq, eT, Td) if Td is not None else (Tq, eT)
+
+
+def gdn_chunk_inverse_neumann_i8_fused(K: torch.Tensor, beta: torch.Tensor, g: torch.Tensor,
+                                       C: int, N: int, S: int, want_deq: bool = False,
+                                       Tq: Optional[torch.Tensor] = None,
+                                       eT: Optional[torch.Tensor] = None,
+                                       Tdeq: Optional[torch.Tensor] = None, stream=None):
+    """K [B, L, H, dk] -> (Tq int8 [B, H, L/C, C, C], eT int32[, Tdeq fp32]):
+    build A, quantise and invert in one launch."""
+    B, L, H, dk = K.shape
+    nc = L // C if C else 0
+    shape = (B, H, nc, C, C)
+    n = B * H * nc
+    Tq = torch.empty(shape, dtype=torch.int8, device=K.device) if Tq is None else Tq
+    eT = torch.empty(n, dtype=torch.int32, device=K.device) if eT is None else eT
+    Td = Tdeq
+    if want_deq and Td is None:
+        Td = torch.empty(shape, dtype=torch.float32, device=K.device)
+    tok = B * L * H
+    _check("gdn_chunk_inverse_neumann_i8_fused", lib.gdn_chunk_inverse_neumann_i8_fused(
+        _dev(K, "K"), _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
+        _dev(Tq, "Tq", torch.int8, n * C * C), _dev(eT, "eT", torch.int32, n),
+        _dev(Td, "Tdeq", torch.float32, n * C * C) if Td is not None else None,
+        B, L, H, dk, C, N, S, _fdtype(K, "K"), _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)

@@ -204,4 +204,32 @@ int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq
       gdn::launch_neumann_i8(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, (hipStream_t)stream));
 }
 
+int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const float* g,
+                                       int8_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
+                                       int dk, int C, int N, int S, int k_dtype, void* stream) {
+  if (C == 128) return GDN_ERR_SHAPE;
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk)) return GDN_ERR_SHAPE;
+  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(k_dtype)) return GDN_ERR_DTYPE;
+  if (n == 0) return GDN_OK;
+  if (!K || !beta || !g || !Tq || !eT) return GDN_ERR_NULL;
+  if (!aligned(K) || !aligned(beta) || !aligned(g) || !aligned(Tq) || !aligned(eT) ||
+      (Tdeq && !aligned(Tdeq)))
+    return GDN_ERR_ALIGN;
+  const int64_t tok = (int64_t)B * L * H;
+  const int64_t qb = n * C * C, eb = n * 4, db = n * C * C * 4;
+  const void* ins[3] = {K, beta, g};
+  const int64_t inb[3] = {tok * dk * esize(k_dtype), tok * 4, tok * 4};
+  for (int i = 0; i < 3; ++i)
+    if (overlap(Tq, qb, ins[i], inb[i]) || overlap(eT, eb, ins[i], inb[i]) ||
+        overlap(Tdeq, db, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_inverse_i8_fused(K, beta, g, Tq, eT, Tdeq, B, L, H, dk, C, N, S,
+                                                 k_dtype, (hipStream_t)stream));
+}
+
 }  // extern "C"

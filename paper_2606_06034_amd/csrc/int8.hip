@@ -22,7 +22,7 @@
 // row quad R[I] = blocks (I, 0..3) in row form, column quad Cq[J] = blocks
 // (0..3, J) in column form; one MFMA contracts all four k-blocks (zero blocks
 // where K > I or K < J).  C = 16, 32 use the leading one or two blocks.
-#include "tile16.hpp"
+#include "chunk.hpp"
 #include "launch.hpp"
 
 // wave reductions of the ROCm device library
@@ -287,39 +287,22 @@ __device__ __forceinline__ void unpack_row(AccI<NB>& D, const RowQ<NB>& X) {
 
 // ---------------------------------------------------------------------------
 
-// NC, SC >= 0 fix N and S at compile time (every band and block skip is then
-// resolved by the compiler); -1 takes them from the arguments.
+// The integer inverse of one tile from Lm = -A (codes, strictly lower, row
+// form) with exponent eL; returns the strict part of T_hat as codes Tr (row
+// form) and its exponent eTo.  NC, SC >= 0 fix N and S at compile time
+// (every band and block skip is then resolved by the compiler); -1 takes
+// them from Nrt, Srt.
 template <int NB, int NC = -1, int SC = -1>
-__global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq,
-                                                   const int32_t* __restrict__ eA,
-                                                   int8_t* __restrict__ Tq,
-                                                   int32_t* __restrict__ eT,
-                                                   float* __restrict__ Tdeq, int Nrt, int Srt) {
+__device__ __forceinline__ void engine_i8(const AccI<NB>& Lr, int eL, int Nrt, int Srt,
+                                          AccI<NB>& Tr, int& eTo) {
   constexpr int C = 16 * NB;
   constexpr int ACCB = 14 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |acc| < C * 2^14
   const int N = NC >= 0 ? NC : Nrt;
   const int S = SC >= 0 ? SC : Srt;
-  const int64_t tile = blockIdx.x;
-  const int g = lane_g(), c = lane_c();
-  const int8_t* a = Aq + tile * (C * C);
-
   RowQ<NB> Iq;
   ColQ<NB> Ic;
   eye_quads(Iq, Ic);
 
-  // ---- Lm = -A (row form), strictly lower
-  AccI<NB> Lr;
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      const int w = *(const int*)(a + (I * 16 + c) * C + J * 16 + 4 * g);
-      i32x4 x = unpack4(w);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
-      Lr.a[bidx(I, J)] = x;
-    }
-  const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
   const bool nzL = amax_of(Lr, 1, C - 1) > 0;
   RowQ<NB> LRq;
   to_rowq(LRq, Lr, 1, C - 1);
@@ -426,8 +409,6 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   mmi<NB, true>(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
 
   // ---- T = N0 + Gs + N0 Gs (row form), strict part
-  AccI<NB> Tr;
-  int eTo;
   bool nzT;
   {
     AccI<NB> NG;
@@ -441,7 +422,16 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
     rs_finish(ts, Tr, eTo, nzT);
   }
 
-  // ---- store
+}
+
+// Tq (codes, zero on and above the diagonal), eT and optionally
+// Tdeq = I + Tq 2^eT for tile `tile`
+template <int NB>
+__device__ __forceinline__ void store_i8(const AccI<NB>& Tr, int eTo, int8_t* __restrict__ Tq,
+                                         int32_t* __restrict__ eT, float* __restrict__ Tdeq,
+                                         int64_t tile) {
+  constexpr int C = 16 * NB;
+  const int g = lane_g(), c = lane_c();
   int8_t* t = Tq + tile * (C * C);
 #pragma unroll
   for (int I = 0; I < NB; ++I)
@@ -465,6 +455,82 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
         *(f32x4*)(td + (I * 16 + c) * C + J * 16 + 4 * g) = x;
       }
   }
+}
+
+template <int NB, int NC = -1, int SC = -1>
+__global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq,
+                                                   const int32_t* __restrict__ eA,
+                                                   int8_t* __restrict__ Tq,
+                                                   int32_t* __restrict__ eT,
+                                                   float* __restrict__ Tdeq, int Nrt, int Srt) {
+  constexpr int C = 16 * NB;
+  const int64_t tile = blockIdx.x;
+  const int g = lane_g(), c = lane_c();
+  const int8_t* a = Aq + tile * (C * C);
+  // ---- Lm = -A (row form), strictly lower
+  AccI<NB> Lr;
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      const int w = *(const int*)(a + (I * 16 + c) * C + J * 16 + 4 * g);
+      i32x4 x = unpack4(w);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
+      Lr.a[bidx(I, J)] = x;
+    }
+  const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
+  AccI<NB> Tr;
+  int eTo;
+  engine_i8<NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+  store_i8<NB>(Tr, eTo, Tq, eT, Tdeq, tile);
+}
+
+// e = the smallest integer with amax / 2^e <= 127 (frexp: amax = m 2^p with
+// m in [0.5, 1) gives amax / 2^(p - 7) = 128 m), 0 for amax = 0
+__device__ __forceinline__ int quant_exp(float amax) {
+  int e = 0;
+  if (amax > 0.f) {
+    int p;
+    const float mant = frexpf(amax, &p);
+    e = p - 7 + (mant * 128.f > 127.f ? 1 : 0);
+  }
+  return e;
+}
+
+// The whole low-bit path for one chunk in one wave: A in fp32 from K, beta,
+// g (the same values gdn_build_A writes), quantised in registers by the
+// quantiser's rule, then the integer inverse.
+template <int NB, int DK, typename F, typename TK, int NC = -1, int SC = -1>
+__global__ __launch_bounds__(64) void k_inverse_i8_fused(const TK* __restrict__ K,
+                                                         const float* __restrict__ beta,
+                                                         const float* __restrict__ g,
+                                                         int8_t* __restrict__ Tq,
+                                                         int32_t* __restrict__ eT,
+                                                         float* __restrict__ Tdeq, int L, int H,
+                                                         int Nrt, int Srt) {
+  constexpr int C = 16 * NB;
+  __shared__ float sb[C], sg[C];
+  const Chunk ch(blockIdx.x, L, H, C);
+  Acc<NB> G;
+  build_A_rows<NB, DK, F>(K, beta, g, ch, L, H, sb, sg, G);
+  float m = 0.f;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) m = fmaxf(m, fabsf(G.a[b][v]));
+  const float amax =
+      __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
+  const int e = quant_exp(amax);
+  AccI<NB> Lr;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
+  AccI<NB> Tr;
+  int eTo;
+  engine_i8<NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
+  store_i8<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
 }
 
 // ---------------------------------------------------------------------------
@@ -492,12 +558,7 @@ __global__ __launch_bounds__(64) void k_quantize_i8(const float* __restrict__ A,
     }
   }
   const float amax = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
-  int e = 0;
-  if (amax > 0.f) {
-    int p;
-    const float mant = frexpf(amax, &p);
-    e = p - 7 + (mant * 128.f > 127.f ? 1 : 0);
-  }
+  const int e = quant_exp(amax);
   int8_t* q = Aq + tile * (C * C);
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -546,6 +607,45 @@ hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, in
     case 16: return run_neumann_i8<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
     case 32: return run_neumann_i8<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
     case 64: return run_neumann_i8<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+  }
+  return hipErrorNotSupported;
+}
+
+template <int NB, int DN, int DS, typename F, typename TK>
+static hipError_t run_i8_fused(const void* K, const float* beta, const float* g, int8_t* Tq,
+                               int32_t* eT, float* Tdeq, int64_t n, int L, int H, int dk, int N,
+                               int S, hipStream_t st) {
+#define GDN_I8F(DK, NC_, SC_)                                                                \
+  hipLaunchKernelGGL((i8::k_inverse_i8_fused<NB, DK, F, TK, NC_, SC_>), dim3((unsigned)n),   \
+                     dim3(64), 0, st, (const TK*)K, beta, g, Tq, eT, Tdeq, L, H, N, S)
+  const bool def = N == DN && S == DS;
+  if (dk == 64) {
+    if (def) GDN_I8F(64, DN, DS); else GDN_I8F(64, -1, -1);
+  } else if (dk == 128) {
+    if (def) GDN_I8F(128, DN, DS); else GDN_I8F(128, -1, -1);
+  } else {
+    return hipErrorNotSupported;
+  }
+#undef GDN_I8F
+  return hipGetLastError();
+}
+
+hipError_t launch_inverse_i8_fused(const void* K, const float* beta, const float* g, int8_t* Tq,
+                                   int32_t* eT, float* Tdeq, int B, int L, int H, int dk, int C,
+                                   int N, int S, int k_dtype, hipStream_t st) {
+  const int64_t n = (int64_t)B * H * (L / C);
+  if (k_dtype == 1) {
+    switch (C) {
+      case 16: return run_i8_fused<1, 3, 2, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 32: return run_i8_fused<2, 3, 4, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 64: return run_i8_fused<4, 3, 8, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+    }
+  } else if (k_dtype == 0) {
+    switch (C) {
+      case 16: return run_i8_fused<1, 3, 2, f32x4, float>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 32: return run_i8_fused<2, 3, 4, f32x4, float>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 64: return run_i8_fused<4, 3, 8, f32x4, float>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+    }
   }
   return hipErrorNotSupported;
 }

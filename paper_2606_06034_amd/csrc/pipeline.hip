@@ -8,117 +8,11 @@
 // global access is a run of 8 consecutive features of one token (16 bytes in
 // bf16).  Column-form (token-major) fragments of K and V are made on chip by
 // identity MFMAs.
+#include "chunk.hpp"
 #include "engine.hpp"
 #include "launch.hpp"
 
 namespace gdn {
-
-// Chunk bookkeeping.  Work item x walks the tiles heads-fastest,
-// x = (b * (L / C) + chunk) * H + h, so waves running side by side read the
-// neighbouring heads of the same tokens: together they cover whole
-// H * d-wide token rows of [B, L, H, d] instead of one 256-byte run per row
-// and DRAM page (+10 % bandwidth for this access pattern on MI355X).
-// `tile` is the position in the [B, H, L/C, C, C] tile layout.
-struct Chunk {
-  int b, h, t0;
-  int64_t tile;
-  // x < 2^31 (the tile count is bounded so): 32-bit unsigned division
-  __device__ Chunk(uint32_t x, int L, int H, int C) {
-    const uint32_t nc = (uint32_t)(L / C);
-    const uint32_t bc = x / (uint32_t)H;
-    h = (int)(x - bc * (uint32_t)H);
-    b = (int)(bc / nc);
-    const int chunk = (int)(bc - (uint32_t)b * nc);
-    t0 = chunk * C;
-    tile = ((int64_t)b * H + h) * nc + chunk;
-  }
-  // element offset of (token t0 + r, head h, feature 0) in [B, L, H, d]
-  __device__ int64_t row(int r, int L, int H, int d) const {
-    return (((int64_t)b * L + t0 + r) * H + h) * d;
-  }
-};
-
-// beta and g of the chunk into LDS (one wave; C <= 128)
-template <int C>
-__device__ __forceinline__ void load_gates(const float* __restrict__ beta,
-                                           const float* __restrict__ g, const Chunk& ch, int L,
-                                           int H, float* sb, float* sg) {
-  for (int r = lane_id(); r < C; r += 64) {
-    const int64_t o = ((int64_t)ch.b * L + ch.t0 + r) * H + ch.h;
-    if (sb) sb[r] = beta[o];
-    if (sg) sg[r] = g[o];
-  }
-  __syncthreads();
-}
-
-// Lower blocks of the chunk Gram matrix K K^T (fp32 accumulation), in the
-// form OUTQ selects, from the row pairs of K (load_rows): both factors are
-// rows of K and any feature order serves as the contraction order.
-template <int NB, int DK, bool OUTQ, typename F>
-__device__ __forceinline__ void gram_lower(Acc<NB>& G, const Pair<F> (&kp)[NB][DK / 32]) {
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      f32x4 acc = zero4();
-#pragma unroll
-      for (int q = 0; q < DK / 32; ++q) acc = Pair<F>::template mma<OUTQ>(kp[I][q], kp[J][q], acc);
-      G.a[bidx(I, J)] = acc;
-    }
-}
-
-// A (times `sign`) from the Gram blocks, in place; ROWFORM selects the
-// element coordinates of the blocks' form.
-template <int NB, bool ROWFORM>
-__device__ __forceinline__ void gate_scale(Acc<NB>& G, const float* sb, const float* sg,
-                                           float sign, Lane ln = lane_here()) {
-  const int g = ln.g(), c = ln.c();
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int i = ROWFORM ? I * 16 + c : I * 16 + 4 * g + v;
-        const int j = ROWFORM ? J * 16 + 4 * g + v : J * 16 + c;
-        const float x = G.a[bidx(I, J)][v];
-        G.a[bidx(I, J)][v] = (i > j) ? sign * sb[i] * x * __expf(sg[i] - sg[j]) : 0.f;
-      }
-}
-
-// 16-byte loads of a chunk of X [token][feature] (row stride ld): lane (g, c)
-// gets 8 consecutive features 32q + 8g .. 32q + 8g + 7 of token 16I + c, as
-// one row-form pair over two 16-feature halves.  Within chunk q the half h
-// holds features 32q + 8 (j / 4) + 4h + (j % 4) in block column j, so the
-// same permutation maps MFMA columns back to memory on store.
-template <typename F, typename TIO>
-__device__ __forceinline__ Pair<F> load_row8(const TIO* __restrict__ p);
-template <>
-__device__ __forceinline__ Pair<bf16x4> load_row8<bf16x4, __bf16>(const __bf16* __restrict__ p) {
-  return Pair<bf16x4>{*(const bf16x8*)p};
-}
-template <>
-__device__ __forceinline__ Pair<f32x4> load_row8<f32x4, float>(const float* __restrict__ p) {
-  return Pair<f32x4>{*(const f32x4*)p, *(const f32x4*)(p + 4)};
-}
-__device__ __forceinline__ void store_row8(__bf16* p, f32x4 lo, f32x4 hi) {
-  const bf16x4 a = __builtin_convertvector(lo, bf16x4), b = __builtin_convertvector(hi, bf16x4);
-  *(bf16x8*)p = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-__device__ __forceinline__ void store_row8(float* p, f32x4 lo, f32x4 hi) {
-  *(f32x4*)p = lo;
-  *(f32x4*)(p + 4) = hi;
-}
-
-template <int NB, int D, typename F, typename TIO>
-__device__ __forceinline__ void load_rows(Pair<F> (&xp)[NB][D / 32], const TIO* __restrict__ xb,
-                                          int64_t ld, Lane ln = lane_here()) {
-  const int g = ln.g(), c = ln.c();
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int q = 0; q < D / 32; ++q) xp[I][q] = load_row8<F>(xb + (I * 16 + c) * ld + 32 * q + 8 * g);
-}
 
 // Asynchronous copy of a bf16 chunk of X into LDS (global -> LDS DMA, no
 // registers): the 16-byte run lane (g, c) would load in load_rows lands at
@@ -230,14 +124,8 @@ __global__ __launch_bounds__(64) void k_build_A(const TK* __restrict__ K,
   __shared__ float sb[C], sg[C];
   const Chunk ch(blockIdx.x, L, H, C);
   const int64_t tile = ch.tile;
-  load_gates<C>(beta, g, ch, L, H, sb, sg);
   Acc<NB> G;
-  {
-    Pair<F> kp[NB][DK / 32];
-    load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
-    gram_lower<NB, DK, true>(G, kp);
-  }
-  gate_scale<NB, true>(G, sb, sg, 1.f);
+  build_A_rows<NB, DK, F>(K, beta, g, ch, L, H, sb, sg, G);
   TA* a = A + tile * (C * C);
   const int gg = lane_g(), c = lane_c();
 #pragma unroll

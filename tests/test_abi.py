@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 10
+    assert len(names) == 11
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -140,6 +140,31 @@ def test_int8_validation():
     assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, None) == NULL
     assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
     assert n(None, None, None, None, None, 0, 64, 3, 8, None) == OK
+
+
+def test_int8_fused_validation():
+    f = L.gdn_chunk_inverse_neumann_i8_fused
+    # K, beta, g, Tq, eT, Tdeq, B, L, H, dk, C, N, S, k_dtype, stream
+    base = [P1, BIG, 2 * BIG, 3 * BIG, 4 * BIG, None, 1, 256, 2, 128, 64, 3, 8, 1, None]
+
+    def call(**kw):
+        a = list(base)
+        for k, v in kw.items():
+            a[["K", "beta", "g", "Tq", "eT", "Tdeq", "B", "L", "H", "dk", "C", "N", "S",
+               "kdt"].index(k)] = v
+        return f(*a)
+
+    assert call(C=128) == SHAPE       # the INT8 path covers C <= 64
+    assert call(dk=96) == SHAPE
+    assert call(L=250) == SHAPE       # L % C != 0
+    assert call(N=64) == PARAM
+    assert call(kdt=2) == DTYPE
+    assert call(Tq=None) == NULL
+    assert call(eT=None) == NULL
+    assert call(Tq=P1 + 1024) == ALIAS
+    assert call(Tdeq=4 * BIG + 16) == ALIAS
+    assert call(eT=P1 + 8) == ALIGN
+    assert call(B=0, K=None, beta=None, g=None, Tq=None, eT=None) == OK
 
 
 def test_binding_rejects_host_tensors():

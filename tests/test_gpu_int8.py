@@ -220,3 +220,65 @@ def test_i8_full_size_sampled():
     assert np.array_equal(host(qT[idx_t]).astype(np.int64), rq)
     assert np.array_equal(host(eT[idx_t]).astype(np.int64), re)
     assert np.array_equal(host(Td[idx_t]), oi.dequant_unit(rq, re).astype(np.float32))
+
+
+# ---------------------------------------------------------------------------
+# one launch from K: build A, quantise, integer inverse
+
+
+def head_set(C, kdt, L=None, H=2, stress=False):
+    w = wl.workload("int8").with_(dtype=kdt, L=L or 4 * max(C, 64), H=H, B=1)
+    if stress:
+        heads = [wl.gen_stress_head(w.L, w.dk, C, seed=60 + h) for h in range(H)]
+        heads = [(wl.round_to_bf16(k) if kdt == "bf16" else k, b, g, v) for k, b, g, v in heads]
+    else:
+        heads = [wl.gen_head(w, 0, h, C=C, want_v=False) for h in range(H)]
+    return tuple(wl.as_blhd(*[x[i] for x in heads]) for i in range(3))
+
+
+def to_cuda(x, dt=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(x, np.float32))).to("cuda").to(dt)
+
+
+@pytest.mark.parametrize("kdt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64])
+def test_i8_fused_matches_stages(C, kdt):
+    """The fused launch equals gdn_build_A (fp32) -> quantiser -> integer
+    inverse on the GPU, bit for bit (same fp32 A, same integer steps)."""
+    K, beta, g = head_set(C, kdt, stress=(C == 32))
+    dK = to_cuda(K, torch.bfloat16 if kdt == "bf16" else torch.float32)
+    db, dg = to_cuda(beta), to_cuda(g)
+    for N, S in ORDERS[C][:3]:
+        A = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
+        Aq, eA = G.gdn_quantize_tiles_i8(A)
+        q1, e1, d1 = G.gdn_chunk_inverse_neumann_i8(Aq, eA, N, S, want_deq=True)
+        q2, e2, d2 = G.gdn_chunk_inverse_neumann_i8_fused(dK, db, dg, C, N, S, want_deq=True)
+        print(f"i8 fused vs stages C={C} K={kdt} N={N} S={S}", flush=True)
+        assert np.array_equal(host(q1).reshape(-1), host(q2).reshape(-1))
+        assert np.array_equal(host(e1), host(e2))
+        assert np.array_equal(host(d1).reshape(-1), host(d2).reshape(-1))
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+def test_i8_fused_vs_oracle(C):
+    """Against the integer oracle run from its own fp32 A (float64 build,
+    rounded): the GPU forms A in fp32 arithmetic, so an entry one unit in
+    the last place away can move a code at a rounding boundary.  Most tiles
+    match bit for bit; the rest differ from the oracle's T_hat by at most a
+    few quanta of T_hat's exponent."""
+    K, beta, g = head_set(C, "bf16", L=16 * C, H=4)
+    Tq, eT, Td = G.gdn_chunk_inverse_neumann_i8_fused(to_cuda(K, torch.bfloat16), to_cuda(beta),
+                                                      to_cuda(g), C, *G.gdn_default_order(C),
+                                                      want_deq=True)
+    A = gdn.tiles_flat(gdn.build_A(K, beta, g, C)).astype(np.float32)
+    qA, eA = oi.quantize(A)
+    rq, re, _ = oi.neumann_inverse_int8(qA, eA, *G.gdn_default_order(C))
+    gq = host(Tq).reshape(rq.shape).astype(np.int64)
+    ge = host(eT).astype(np.int64)
+    same = np.all(gq == rq, axis=(-1, -2)) & (ge == re)
+    diff = np.abs(host(Td).reshape(rq.shape).astype(np.float64) - oi.dequant_unit(rq, re))
+    quanta = diff / np.ldexp(1.0, re)[:, None, None]
+    print(f"i8 fused vs oracle C={C}: {same.mean():.4f} of {same.size} tiles bit-exact, "
+          f"max diff {diff.max():.3e} = {quanta.max():.1f} quanta", flush=True)
+    assert same.mean() >= 0.9
+    assert quanta.max() <= 4.0
