@@ -249,7 +249,9 @@ def main():
 
 # committed rocprofv3 summaries carrying measured HBM traffic per launch
 PROFILES = {("fused", "qwen35_prefill", 64): ("k_fused_qwen35_prefill.md", "pipeline.hip"),
-            ("inverse", "sweep", 64): ("k_neumann_sweep_c64.md", "neumann.hip")}
+            ("fused", "long_context", 64): ("k_fused_long_context.md", "pipeline.hip"),
+            ("inverse", "sweep", 64): ("k_neumann_sweep_c64.md", "neumann.hip"),
+            ("int8", "int8", 64): ("k_inverse_i8_fused_int8.md", "int8.hip")}
 
 
 def measured_traffic(path, workload, C, N, S, default_order):
