@@ -52,7 +52,10 @@ def parse():
     ap.add_argument("--S", type=int, default=None)
     ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "unfused", "int8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tiles", type=int, default=512)
+    ap.add_argument("--cpu-sample-tiles", type=int, default=2048,
+                    help="tiles of the workload the CPU oracle runs on (whole heads)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="repeat oracle passes over the sample until this much time has passed")
     ap.add_argument("--error-grid", action="store_true",
                     help="instead of timing: max |T_hat(N, S) - X| and per-tile SNR for "
                          "N = 1..6, S = 0..16 against the exact inverse X (fp32 forward "
@@ -234,6 +237,9 @@ def main():
     }
 
     if a.path == "int8":
+        out["tops_int8_dense_equiv"] = out.pop("tflops_dense_equiv")
+        out["tops_vs_int8_peak"] = round(out.pop("tflops_vs_bf16_peak") * BF16_PEAK_TFLOPS
+                                         / INT8_PEAK_TOPS, 4)
         out["config"]["three_launch_ms"] = {"build_A_f32": round(stage_ms[0], 6),
                                             "quantize": round(stage_ms[1], 6),
                                             "inverse_i8": round(stage_ms[2], 6)}
@@ -276,8 +282,9 @@ def measured_traffic(path, workload, C, N, S, default_order):
 
 def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
     """The oracle (float64 numpy) on a bounded sample of the same workload:
-    the first `cpu_sample_tiles` tiles of head (0, 0), ... ; also the GPU's
-    max abs error against it on those tiles (fused path outputs)."""
+    whole heads (0, 0), (0, 1), ... up to `cpu_sample_tiles` tiles, passes
+    repeated until `cpu_seconds` have elapsed; also the GPU's max abs error
+    against it on those tiles (fused path outputs)."""
     from oracle import gdn
 
     try:
@@ -296,16 +303,25 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
             heads.append((b, h))
             n += nc
     K, beta, g, V = host_inputs
-    t0 = time.perf_counter()
     Ks = np.stack([K[b, :, h] for b, h in heads], 1)[None]
     bs = np.stack([beta[b, :, h] for b, h in heads], 1)[None]
     gs = np.stack([g[b, :, h] for b, h in heads], 1)[None]
     Vs = np.stack([V[b, :, h] for b, h in heads], 1)[None]
-    A = gdn.build_A(Ks, bs, gs, C)
-    T = gdn.neumann_inverse_blocked(A, N, S) if C == 128 else gdn.neumann_inverse(A, N, S)
-    Wr, Ur = gdn.wy_apply(T, Ks, Vs, bs, C)
-    secs = time.perf_counter() - t0
-    tiles = A.shape[1] * A.shape[2]
+
+    def one_pass():
+        A = gdn.build_A(Ks, bs, gs, C)
+        T = gdn.neumann_inverse_blocked(A, N, S) if C == 128 else gdn.neumann_inverse(A, N, S)
+        Wr, Ur = gdn.wy_apply(T, Ks, Vs, bs, C)
+        return A, T, Wr, Ur
+
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        A, T, Wr, Ur = one_pass()
+        passes += 1
+        secs = time.perf_counter() - t0
+        if secs >= a.cpu_seconds:
+            break
+    tiles = A.shape[1] * A.shape[2] * passes
     # GPU outputs of the same tiles
     W, U, Tg = G.gdn_chunk_wy_fused(dK, dV, db, dg, C, N, S, want_T=True) if C != 128 else (None, None, None)
     err = None
@@ -318,8 +334,9 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
                "U": float(np.max(np.abs(Ug - Ur)))}
     return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"{tiles} tiles ({len(heads)} heads x {nc} chunks) of {w.name}: "
-                      f"build A + T_hat({N},{S}) + W/U in float64 numpy, {secs:.2f} s",
+            "sample": f"{len(heads)} heads x {nc} chunks of {w.name} ({tiles // passes} "
+                      f"tiles), {passes} passes: build A + T_hat({N},{S}) + W/U in float64 "
+                      f"numpy, {secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": err}
 
 
@@ -375,8 +392,9 @@ def _threads():
 
 
 def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
-    """The integer oracle on the first `cpu_sample_tiles` tiles: build A in
-    float64, round to float32, quantise, integer T_hat.  Reports the GPU's
+    """The integer oracle on whole heads up to `cpu_sample_tiles` tiles,
+    passes repeated until `cpu_seconds` have elapsed: build A in float64,
+    round to float32, quantise, integer T_hat.  Reports the GPU's
     dequantised T_hat against it (the GPU builds A in fp32 itself, so an
     A entry a rounding apart can move a code: this is an error figure, the
     bit-exact checks live in the tests) and both against the exact inverse."""
@@ -387,14 +405,18 @@ def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
     want = max(1, a.cpu_sample_tiles)
     heads = [(b, h) for b in range(w.B) for h in range(w.H)][:max(1, -(-want // nc))]
     K, beta, g = host_inputs
-    t0 = time.perf_counter()
     Ks = np.stack([K[b, :, h] for b, h in heads], 1)[None]
     bs = np.stack([beta[b, :, h] for b, h in heads], 1)[None]
     gs = np.stack([g[b, :, h] for b, h in heads], 1)[None]
-    A = gdn.build_A(Ks, bs, gs, C).astype(np.float32)
-    qA, eA = oi.quantize(A)
-    qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S)
-    secs = time.perf_counter() - t0
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        A = gdn.build_A(Ks, bs, gs, C).astype(np.float32)
+        qA, eA = oi.quantize(A)
+        qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S)
+        passes += 1
+        secs = time.perf_counter() - t0
+        if secs >= a.cpu_seconds:
+            break
     Tr = oi.dequant_unit(qT, eT)[0]
     X = gdn.forward_substitution_inverse(A.astype(np.float64))[0]
     torch.cuda.synchronize()
@@ -402,10 +424,11 @@ def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
                                    deT.view(w.B, w.H, nc)[b, h].cpu().numpy().astype(np.int64))
                    for b, h in heads], 0)
     tiles = Tr.shape[0] * Tr.shape[1]
-    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": _threads(),
-            "kind": "oracle",
-            "sample": f"{tiles} tiles ({len(heads)} heads x {nc} chunks) of {w.name}: "
-                      f"build A + INT8 quantiser + integer T_hat({N},{S}), numpy, {secs:.2f} s",
+    return {"value": round(tiles * passes / secs, 1), "unit": "chunk inverses/s",
+            "cores": _threads(), "kind": "oracle",
+            "sample": f"{len(heads)} heads x {nc} chunks of {w.name} ({tiles} tiles), {passes} "
+                      f"passes: build A + INT8 quantiser + integer T_hat({N},{S}), numpy, "
+                      f"{secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"T": float(np.max(np.abs(Tg - Tr)))},
             "max_abs_err_vs_exact_inverse": {"gpu": float(np.max(np.abs(Tg - X))),
                                              "oracle": float(np.max(np.abs(Tr - X)))}}

@@ -62,11 +62,15 @@ def _includes(path: str, seen=None):
 
 
 def _digest(src: str) -> str:
+    """Hash of a source, the local headers it includes and the compile flags,
+    independent of where the repository is checked out."""
+    root = os.path.dirname(os.path.dirname(HERE))
     h = hashlib.sha256()
-    for p in sorted(_includes(src)):
+    for p in sorted(_includes(src), key=lambda q: os.path.relpath(q, root)):
+        h.update(os.path.relpath(p, root).encode())
         with open(p, "rb") as f:
             h.update(f.read())
-    h.update(" ".join(CFLAGS).encode())
+    h.update(" ".join(CFLAGS).replace(root, "<repo>").encode())
     return h.hexdigest()[:16]
 
 
