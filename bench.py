@@ -1,7 +1,8 @@
 """Benchmark of the chunk-wise Gated DeltaNet inverse path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--C C]
-                    [--path fused|inverse|fwdsub|unfused|int8] [--no-cpu-baseline]
+                    [--path fused|inverse|fwdsub|blockwise|unfused|int8]
+                    [--no-cpu-baseline]
 
 A step is one pass of the hot path over one batch of synthetic inputs
 already resident in HBM.  The default workload is the Qwen3.5-shaped prefill
@@ -50,7 +51,7 @@ def parse():
     ap.add_argument("--C", type=int, default=None)
     ap.add_argument("--N", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
-    ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "unfused", "int8"])
+    ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "blockwise", "unfused", "int8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=2048,
                     help="tiles of the workload the CPU oracle runs on (whole heads)")
@@ -129,6 +130,8 @@ def main():
         dTq = torch.empty((w.B, w.H, w.L // C, C, C), dtype=torch.int8, device="cuda")
         deT = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
         step = lambda: G.gdn_chunk_inverse_neumann_i8_fused(dK, db, dg, C, N, S, Tq=dTq, eT=deT)
+    elif a.path == "blockwise":
+        step = lambda: G.gdn_chunk_inverse_blockwise(dA, Tinv=dT)
     else:
         step = lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT)
 
@@ -188,11 +191,12 @@ def main():
             bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
             achieved = bytes_ / (ev_ms * 1e-3) / 1e9
         kernel = "k_neumann"
-    elif a.path == "fwdsub":
+    elif a.path in ("fwdsub", "blockwise"):
+        # the exact inverse: tile in, tile out; the arithmetic of substitution
         bytes_ = n_tiles * C * C * es * 2
         flops = n_tiles * (C ** 3 - C) // 3  # sum over i > j of (i - j) FMAs = (C^3 - C) / 6
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = "k_fwdsub"
+        kernel = "k_fwdsub" if a.path == "fwdsub" else "k_blockwise"
     elif a.path == "int8":
         # K (dk per token) and beta, g in; int8 T_hat codes and exponents out
         bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C + 4)

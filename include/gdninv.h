@@ -105,6 +105,18 @@ int gdn_chunk_inverse_neumann(const void* A, void* Tinv, int64_t n_tiles, int C,
 int gdn_chunk_inverse_fwdsub(const void* A, void* Tinv, int64_t n_tiles, int C,
                              int dtype, void* stream);
 
+/* Exact inverse (I + A)^-1 with matrix products only: the two-block
+ * recursion of Appendix E, X_21 = X_22 L_21 X_11 with L = -A, taken all the
+ * way down.  Inside each 16 x 16 diagonal block it runs on masked 16 x 16
+ * products (X_{k+1} = X_k + X_k O_k X_k, O_k the entries of L joining blocks
+ * of size 2^k); across the 16 x 16 blocks it continues as block forward
+ * substitution X_IJ = X_II sum_{K=J}^{I-1} L_IK X_KJ.  C = 128 joins two
+ * 64-blocks by Tinv_21 = -Tinv_22 A_21 Tinv_11.  Products in the compute
+ * dtype as for gdn_chunk_inverse_neumann (bf16 operands round to bf16).
+ * A, Tinv, n_tiles, C, dtype as for gdn_chunk_inverse_neumann. */
+int gdn_chunk_inverse_blockwise(const void* A, void* Tinv, int64_t n_tiles, int C, int dtype,
+                                void* stream);
+
 /* WY application: per chunk, W = Tinv diag(beta) K and U = Tinv diag(beta) V.
  * Tinv: [B, H, L/C, C, C], K/W: [B, L, H, dk], V/U: [B, L, H, dv], all in
  * `dtype` (GDN_F32 or GDN_BF16); beta fp32.  Only the lower triangle of

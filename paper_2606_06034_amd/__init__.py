@@ -20,6 +20,7 @@ from ._binding import (  # noqa: F401
     gdn_abi_version,
     gdn_build_A,
     gdn_chunk_inverse_fwdsub,
+    gdn_chunk_inverse_blockwise,
     gdn_chunk_inverse_neumann,
     gdn_chunk_inverse_neumann_i8,
     gdn_chunk_inverse_neumann_i8_fused,

@@ -22,6 +22,7 @@ _SIGS = {
     "gdn_build_A": [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_inverse_neumann": [_vp, _vp, _c_i64, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_inverse_fwdsub": [_vp, _vp, _c_i64, _c_int, _c_int, _vp],
+    "gdn_chunk_inverse_blockwise": [_vp, _vp, _c_i64, _c_int, _c_int, _vp],
     "gdn_wy_apply": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
                      _c_int, _vp],
     "gdn_chunk_wy_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int,
@@ -153,6 +154,18 @@ def gdn_chunk_inverse_fwdsub(A: torch.Tensor, Tinv: Optional[torch.Tensor] = Non
     if Tinv is None:
         Tinv = torch.empty_like(A)
     _check("gdn_chunk_inverse_fwdsub", lib.gdn_chunk_inverse_fwdsub(
+        _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype, A.numel()), n, C, dt, _stream(stream)))
+    return Tinv
+
+
+def gdn_chunk_inverse_blockwise(A: torch.Tensor, Tinv: Optional[torch.Tensor] = None,
+                                stream=None) -> torch.Tensor:
+    """Exact (I + A)^-1 of every tile by 16 x 16 block recursion (products only)."""
+    n, C = _tiles(A)
+    dt = _fdtype(A, "A")
+    if Tinv is None:
+        Tinv = torch.empty_like(A)
+    _check("gdn_chunk_inverse_blockwise", lib.gdn_chunk_inverse_blockwise(
         _dev(A, "A"), _dev(Tinv, "Tinv", A.dtype, A.numel()), n, C, dt, _stream(stream)))
     return Tinv
 

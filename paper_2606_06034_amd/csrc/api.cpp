@@ -119,6 +119,18 @@ int gdn_chunk_inverse_fwdsub(const void* A, void* Tinv, int64_t n_tiles, int C, 
   return hip_status(gdn::launch_fwdsub(A, Tinv, n_tiles, C, dtype, (hipStream_t)stream));
 }
 
+int gdn_chunk_inverse_blockwise(const void* A, void* Tinv, int64_t n_tiles, int C, int dtype,
+                                void* stream) {
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (n_tiles == 0) return GDN_OK;
+  if (!A || !Tinv) return GDN_ERR_NULL;
+  if (!aligned(A) || !aligned(Tinv)) return GDN_ERR_ALIGN;
+  const int64_t bytes = n_tiles * C * C * esize(dtype);
+  if (overlap(A, bytes, Tinv, bytes)) return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_blockwise(A, Tinv, n_tiles, C, dtype, (hipStream_t)stream));
+}
+
 int gdn_wy_apply(const void* Tinv, const void* K, const void* V, const float* beta, void* W,
                  void* U, int B, int L, int H, int dk, int dv, int C, int dtype, void* stream) {
   int64_t n = 0;

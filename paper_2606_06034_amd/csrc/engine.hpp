@@ -69,6 +69,19 @@ __device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int l
     }
 }
 
+// Lm = -A as row-form blocks only
+template <int NB, typename TIO>
+__device__ __forceinline__ void load_neg_strict_row(const TIO* __restrict__ a, int ldr,
+                                                    Acc<NB>& Lr) {
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      Lr.a[bidx(I, J)] =
+          band_block<false>(-load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g), I - J, 1, 16 * NB);
+}
+
 // Store a unit lower-triangular tile from its row-form blocks (diagonal
 // written as exactly 1, the upper triangle as 0).  ldr = row stride.
 template <int NB, typename TIO>
@@ -242,6 +255,82 @@ __device__ __forceinline__ void neumann_engine(const RowP<NB, F>& LR, const Acc<
       }
     mm<NB, true, true>(Tr, T0R, 0, N, GC, N + 1, C - 1, N + 1, C - 1);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Exact inverse by blocks: the two-block recursion of Appendix E,
+//   [[X_11, 0], [X_21, X_22]] with X_21 = X_22 L_21 X_11   (L = Lm = -A),
+// taken all the way down.  Inside each 16 x 16 diagonal block it runs on
+// masked 16 x 16 products: with O_k the entries of L that join two blocks
+// of size 2^k into one of size 2^(k+1), and X_k the inverse of the part of
+// (I - L) made of 2^k x 2^k diagonal blocks,
+//   X_{k+1} = X_k + X_k O_k X_k        (X_1 = I + O_0),
+// exact because O_k X_k O_k = 0; every intermediate is a principal
+// sub-block of X, so nothing grows beyond the inverse itself.  Across the
+// 16 x 16 blocks it continues as block forward substitution,
+//   X_IJ = X_II sum_{K=J}^{I-1} L_IK X_KJ   (I > J, rows in order).
+// Out: Tr, the row-form blocks of X (unit diagonal, zero upper triangle).
+
+// entry (i, j) of a 16 x 16 block belongs to O_k
+__device__ __forceinline__ bool in_level(int i, int j, int k) {
+  return i > j && (i >> k) != (j >> k) && (i >> (k + 1)) == (j >> (k + 1));
+}
+
+template <int NB, typename F>
+__device__ __forceinline__ void blockwise_inverse(const Acc<NB>& Lr, Acc<NB>& Tr,
+                                                  Lane ln = lane_here()) {
+  const int g = ln.g(), c = ln.c();
+  const f32x4 e = eye4(ln);
+  auto mk = [](f32x4 x) { return Pair<F>::make(x, zero4()); };
+  const Pair<F> Ic = mk(e);
+  f32x4 Xc[nlower(NB)];  // column form (right operands of later rows)
+#pragma unroll
+  for (int I = 0; I < NB; ++I) {
+    const f32x4 lr = Lr.a[bidx(I, I)];
+    const f32x4 lc = Pair<F>::template mma<false>(mk(lr), Ic, zero4());  // the block, column form
+    // X_1 = I + O_0 in both forms (row form: i = c, j = 4g + v; column: i = 4g + v, j = c)
+    f32x4 xr = e, xc = e;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if (in_level(c, 4 * g + v, 0)) xr[v] += lr[v];
+      if (in_level(4 * g + v, c, 0)) xc[v] += lc[v];
+    }
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      f32x4 oc;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) oc[v] = in_level(4 * g + v, c, k) ? lc[v] : 0.f;
+      const Pair<F> T = mk(Pair<F>::template mma<true>(mk(xr), mk(oc), zero4()));  // X_k O_k, row
+      const Pair<F> Xk = mk(xc);
+      const f32x4 nc = Pair<F>::template mma<false>(T, Xk, xc);
+      const f32x4 nr = Pair<F>::template mma<true>(T, Xk, xr);
+      xc = nc;
+      xr = nr;
+    }
+    Tr.a[bidx(I, I)] = xr;
+    Xc[bidx(I, I)] = xc;
+  }
+#pragma unroll
+  for (int I = 1; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J < I; ++J) {
+      // S = sum_{K=J}^{I-1} L_IK X_KJ (column form), k-blocks paired
+      f32x4 sc = zero4();
+#pragma unroll
+      for (int p = 0; p < npair(NB); ++p) {
+        const int k0 = 2 * p, k1 = 2 * p + 1;
+        const bool u0 = k0 >= J && k0 < I, u1 = k1 >= J && k1 < I;
+        if (!u0 && !u1) continue;
+        const Pair<F> x = Pair<F>::make(u0 ? Lr.a[bidx(I, k0)] : zero4(),
+                                        u1 ? Lr.a[bidx(I, k1)] : zero4());
+        const Pair<F> y = Pair<F>::make(u0 ? Xc[bidx(k0, J)] : zero4(),
+                                        u1 ? Xc[bidx(k1, J)] : zero4());
+        sc = Pair<F>::template mma<false>(x, y, sc);
+      }
+      const Pair<F> D = mk(Tr.a[bidx(I, I)]), Sc = mk(sc);
+      Xc[bidx(I, J)] = Pair<F>::template mma<false>(D, Sc, zero4());
+      Tr.a[bidx(I, J)] = Pair<F>::template mma<true>(D, Sc, zero4());
+    }
 }
 
 }  // namespace gdn

@@ -12,6 +12,8 @@ hipError_t launch_neumann(const void* A, void* T, int64_t n_tiles, int C, int N,
                           int dtype, hipStream_t st);
 hipError_t launch_fwdsub(const void* A, void* T, int64_t n_tiles, int C, int dtype,
                          hipStream_t st);
+hipError_t launch_blockwise(const void* A, void* T, int64_t n_tiles, int C, int dtype,
+                            hipStream_t st);
 hipError_t launch_build_A(const void* K, const float* beta, const float* g, void* A, int B,
                           int L, int H, int dk, int C, int k_dtype, int a_dtype, hipStream_t st);
 hipError_t launch_wy(const void* T, const void* K, const void* V, const float* beta, void* W,

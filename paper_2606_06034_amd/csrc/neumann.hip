@@ -11,15 +11,23 @@ namespace gdn {
 
 // GH selects the residual sum's evaluation (engine.hpp): Horner for the
 // standalone tiles, the power chain inside the C = 128 kernel (measured
-// faster there, where the merge adds to the register load).
-template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO, bool GH = true>
+// faster there, where the merge adds to the register load).  EXACT: the
+// exact block-wise inverse instead of T_hat(N, S).
+template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO, bool GH = true,
+          bool EXACT = false>
 __device__ __forceinline__ void invert_block(const TIO* __restrict__ a, TIO* __restrict__ t,
                                              int ldr, int N, int S, Acc<NB>& Tr) {
-  Acc<NB> Lr, Lc;
-  load_neg_strict<NB>(a, ldr, Lr, Lc);
-  RowP<NB, F> LR;
-  to_rowp(LR, Lr);
-  neumann_engine<NB, F, SMALLN, NC, SC, GH>(LR, Lc, N, S, Tr);
+  if constexpr (EXACT) {
+    Acc<NB> Lr;
+    load_neg_strict_row<NB>(a, ldr, Lr);
+    blockwise_inverse<NB, F>(Lr, Tr);
+  } else {
+    Acc<NB> Lr, Lc;
+    load_neg_strict<NB>(a, ldr, Lr, Lc);
+    RowP<NB, F> LR;
+    to_rowp(LR, Lr);
+    neumann_engine<NB, F, SMALLN, NC, SC, GH>(LR, Lc, N, S, Tr);
+  }
   store_unit_row<NB>(t, ldr, Tr);
 }
 
@@ -35,7 +43,7 @@ __global__ __launch_bounds__(64) void k_neumann(const TIO* __restrict__ A, TIO* 
 // ---------------------------------------------------------------------------
 // C = 128 as 2 x 2 blocks of 64 (four 16-blocks each)
 
-template <typename F, bool SMALLN, int NC, int SC, typename TIO>
+template <typename F, bool SMALLN, int NC, int SC, typename TIO, bool EXACT = false>
 __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
                                                    TIO* __restrict__ T, int N, int S) {
   constexpr int C = 128, NB = 4;
@@ -48,7 +56,7 @@ __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
   RowP<NB, F> X22;
   {
     Acc<NB> Tr;
-    invert_block<NB, F, SMALLN, NC, SC, TIO, false>(a + 64 * C + 64, t + 64 * C + 64, C, N, S, Tr);
+    invert_block<NB, F, SMALLN, NC, SC, TIO, false, EXACT>(a + 64 * C + 64, t + 64 * C + 64, C, N, S, Tr);
 #pragma unroll
     for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
     to_rowp(X22, Tr);
@@ -57,7 +65,7 @@ __global__ __launch_bounds__(64) void k_neumann128(const TIO* __restrict__ A,
   ColP<NB, F> X11;
   {
     Acc<NB> Tr, Tc;
-    invert_block<NB, F, SMALLN, NC, SC, TIO, false>(a, t, C, N, S, Tr);
+    invert_block<NB, F, SMALLN, NC, SC, TIO, false, EXACT>(a, t, C, N, S, Tr);
 #pragma unroll
     for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
     RowP<NB, F> X11r;
@@ -160,6 +168,42 @@ hipError_t launch_neumann(const void* A, void* T, int64_t n, int C, int N, int S
                           hipStream_t st) {
   if (dtype == 0) return run_neumann_c<f32x4, float>(A, T, n, C, N, S, st);
   if (dtype == 1) return run_neumann_c<bf16x4, __bf16>(A, T, n, C, N, S, st);
+  return hipErrorNotSupported;
+}
+
+// ---------------------------------------------------------------------------
+// exact block-wise inverse (C <= 64 one engine call; C = 128 two 64-blocks and
+// the merge above)
+
+template <int NB, typename F, typename TIO>
+__global__ __launch_bounds__(64) void k_blockwise(const TIO* __restrict__ A, TIO* __restrict__ T) {
+  constexpr int C = 16 * NB;
+  const int64_t tile = blockIdx.x;
+  Acc<NB> Tr;
+  invert_block<NB, F, true, 0, 0, TIO, true, true>(A + tile * (C * C), T + tile * (C * C), C, 0,
+                                                   0, Tr);
+}
+
+template <typename F, typename TIO>
+static hipError_t run_blockwise(const void* A, void* T, int64_t n, int C, hipStream_t st) {
+  const TIO* a = (const TIO*)A;
+  TIO* t = (TIO*)T;
+  switch (C) {
+    case 16: hipLaunchKernelGGL((k_blockwise<1, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, a, t); break;
+    case 32: hipLaunchKernelGGL((k_blockwise<2, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, a, t); break;
+    case 64: hipLaunchKernelGGL((k_blockwise<4, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, a, t); break;
+    case 128:
+      hipLaunchKernelGGL((k_neumann128<F, true, 0, 0, TIO, true>), dim3((unsigned)n), dim3(64), 0,
+                         st, a, t, 0, 0);
+      break;
+    default: return hipErrorNotSupported;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_blockwise(const void* A, void* T, int64_t n, int C, int dtype, hipStream_t st) {
+  if (dtype == 0) return run_blockwise<f32x4, float>(A, T, n, C, st);
+  if (dtype == 1) return run_blockwise<bf16x4, __bf16>(A, T, n, C, st);
   return hipErrorNotSupported;
 }
 

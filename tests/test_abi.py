@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 11
+    assert len(names) == 12
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -140,6 +140,17 @@ def test_int8_validation():
     assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, None) == NULL
     assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
     assert n(None, None, None, None, None, 0, 64, 3, 8, None) == OK
+
+
+def test_blockwise_validation():
+    f = L.gdn_chunk_inverse_blockwise
+    assert f(P1, P2, 4, 48, 1, None) == SHAPE
+    assert f(P1, P2, -1, 64, 1, None) == SHAPE
+    assert f(P1, P2, 4, 64, 2, None) == DTYPE
+    assert f(None, P2, 4, 64, 1, None) == NULL
+    assert f(P1, P1 + 256, 4, 64, 1, None) == ALIAS
+    assert f(P1 + 8, P2, 4, 64, 1, None) == ALIGN
+    assert f(None, None, 0, 64, 1, None) == OK
 
 
 def test_int8_fused_validation():

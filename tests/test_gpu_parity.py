@@ -216,6 +216,57 @@ def test_wy_apply(C, dt):
         assert err <= tol
 
 
+# ---------------------------------------------------------------------------
+# exact block-wise inverse
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+@pytest.mark.parametrize("stress", [False, True])
+def test_blockwise_matches_exact_inverse(C, dt, stress):
+    A = stored(gdn_tiles(C, stress=stress), dt)
+    X = gdn.forward_substitution_inverse(A)
+    T = host(G.gdn_chunk_inverse_blockwise(dev(A, dt)))
+    tol = TOL[dt] * (max(1.0, np.max(np.abs(X))) if stress else 1.0)
+    err = maxerr(T, X)
+    print(f"blockwise C={C} {dt} stress={stress} n={A.shape[0]} max|err|={err:.3e} tol={tol:.1e}",
+          flush=True)
+    assert err <= tol
+    assert np.all(np.triu(T, 1) == 0)
+    assert np.all(np.diagonal(T, axis1=-2, axis2=-1) == 1)
+
+
+def test_blockwise_edge_cases():
+    for C in (16, 32, 64, 128):
+        Z = torch.zeros((3, C, C), device="cuda")
+        assert np.array_equal(host(G.gdn_chunk_inverse_blockwise(Z)),
+                              np.broadcast_to(np.eye(C), (3, C, C)))
+        # all-ones strictly lower (GDN sign): the bidiagonal inverse; every
+        # intermediate is an integer below 2^24, so fp32 reaches it exactly
+        A1 = np.tril(np.ones((2, C, C)), -1)
+        X1 = np.eye(C) - np.eye(C, k=-1)
+        assert np.array_equal(host(G.gdn_chunk_inverse_blockwise(dev(A1))),
+                              np.broadcast_to(X1, (2, C, C)))
+        # entries on and above the diagonal are ignored
+        A = gdn_tiles(C, n_heads=1)[:2]
+        junk = A + np.triu(np.ones_like(A))
+        assert np.array_equal(host(G.gdn_chunk_inverse_blockwise(dev(junk))),
+                              host(G.gdn_chunk_inverse_blockwise(dev(A))))
+
+
+def test_blockwise_many_tiles_full_size_sampled():
+    """Sweep workload at C = 64 (32768 tiles) in one launch, sampled tiles
+    against the oracle's exact inverse."""
+    w = wl.workload("sweep")
+    C = 64
+    K, beta, g, _ = wl.gen_inputs(w.with_(H=4), C=C, want_v=False)
+    A = stored(gdn.tiles_flat(gdn.build_A(K, beta, g, C)), "bf16")
+    T = G.gdn_chunk_inverse_blockwise(dev(A, "bf16"))
+    idx = np.random.default_rng(3).choice(A.shape[0], 64, replace=False)
+    X = gdn.forward_substitution_inverse(A[idx])
+    assert maxerr(host(T)[idx], X) <= TOL["bf16"]
+
+
 def ref_inverse(A, N, S):
     """The oracle's T_hat(N, S); C = 128 by the two-block form."""
     if A.shape[-1] == 128:
