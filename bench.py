@@ -1,7 +1,7 @@
 """Benchmark of the chunk-wise Gated DeltaNet inverse path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--C C]
-                    [--path fused|inverse|fwdsub|blockwise|unfused|int8]
+                    [--path fused|fused_blockwise|inverse|fwdsub|blockwise|unfused|int8]
                     [--no-cpu-baseline]
 
 A step is one pass of the hot path over one batch of synthetic inputs
@@ -51,7 +51,8 @@ def parse():
     ap.add_argument("--C", type=int, default=None)
     ap.add_argument("--N", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
-    ap.add_argument("--path", default="fused", choices=["fused", "inverse", "fwdsub", "blockwise", "unfused", "int8"])
+    ap.add_argument("--path", default="fused", choices=["fused", "fused_blockwise", "inverse", "fwdsub", "blockwise",
+                             "unfused", "int8"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=2048,
                     help="tiles of the workload the CPU oracle runs on (whole heads)")
@@ -105,7 +106,7 @@ def main():
     n_tiles = w.B * w.H * (w.L // C)
 
     # ---- inputs, resident in HBM before timing
-    want_v = a.path in ("fused", "unfused")
+    want_v = a.path in ("fused", "fused_blockwise", "unfused")
     K, beta, g, V = wl.gen_inputs(w, C=C, want_v=want_v)
     if V is None:
         V = np.zeros((w.B, w.C, w.H, w.dv), np.float32)  # unused by the timed path
@@ -119,6 +120,8 @@ def main():
 
     if a.path == "fused":
         step = lambda: G.gdn_chunk_wy_fused(dK, dV, db, dg, C, N, S, W=dW, U=dU)
+    elif a.path == "fused_blockwise":
+        step = lambda: G.gdn_chunk_wy_fused_blockwise(dK, dV, db, dg, C, W=dW, U=dU)
     elif a.path == "unfused":
         def step():
             G.gdn_build_A(dK, db, dg, C, A=dA)
@@ -174,11 +177,11 @@ def main():
     if C == 128:
         f_inv = (2 * (N + S) + 2) * 2 * 64 ** 3 * n_tiles
     tok = w.B * w.L * w.H
-    if a.path == "fused":
+    if a.path in ("fused", "fused_blockwise"):
         bytes_ = tok * (w.dk + w.dv) * es * 2 + tok * 8
         flops = f_inv + n_tiles * (2 * C * C * w.dk + 2 * C * C * (w.dk + w.dv))
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = "k_fused"
+        kernel = "k_fused" if C < 128 else "k_fused128"
     elif a.path == "inverse":
         bytes_ = n_tiles * C * C * es * 2
         flops = f_inv
@@ -251,7 +254,7 @@ def main():
         if not a.no_cpu_baseline:
             out["cpu_baseline"] = cpu_baseline_int8(w, C, N, S, a, (K, beta, g), dTq, deT,
                                                     torch, G)
-    elif not a.no_cpu_baseline and want_v:
+    elif not a.no_cpu_baseline and a.path in ("fused", "unfused"):
         out["cpu_baseline"] = cpu_baseline(w, C, N, S, a, (K, beta, g, V), dK, dV, db, dg,
                                              torch, G)
     print(json.dumps(out), flush=True)

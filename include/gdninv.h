@@ -138,6 +138,14 @@ int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const fl
                        void* W, void* U, void* Tinv, int B, int L, int H, int dk,
                        int dv, int C, int N, int S, int dtype, void* stream);
 
+/* The fused path of gdn_chunk_wy_fused with the exact inverse of
+ * gdn_chunk_inverse_blockwise in place of T_hat(N, S): W = X diag(beta) K,
+ * U = X diag(beta) V with X = (I + A)^-1 (C = 128 in the same block form as
+ * gdn_chunk_wy_fused).  Arguments as gdn_chunk_wy_fused without N, S. */
+int gdn_chunk_wy_fused_blockwise(const void* K, const void* V, const float* beta, const float* g,
+                                 void* W, void* U, void* Tinv, int B, int L, int H, int dk, int dv,
+                                 int C, int dtype, void* stream);
+
 /* INT8 mode, step 1 (Appendix G quantiser): per tile, e = the smallest
  * integer with max|A| / 2^e <= 127 and Aq = round-half-even(A / 2^e).
  * A: fp32 tiles; Aq: int8 tiles (same layout); eA: int32 [n_tiles].  An

@@ -27,6 +27,8 @@ _SIGS = {
                      _c_int, _vp],
     "gdn_chunk_wy_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int,
                            _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_wy_fused_blockwise": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
+                                     _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_quantize_tiles_i8": [_vp, _vp, _vp, _c_i64, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i8_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
@@ -207,6 +209,28 @@ def gdn_chunk_wy_fused(K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor, g: 
         _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv), _dev(beta, "beta", torch.float32, tok),
         _dev(g, "g", torch.float32, tok), _dev(W, "W", K.dtype, tok * dk),
         _dev(U, "U", K.dtype, tok * dv), tp, B, L, H, dk, dv, C, N, S, dt, _stream(stream)))
+    return (W, U, Tinv) if Tinv is not None else (W, U)
+
+
+def gdn_chunk_wy_fused_blockwise(K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor,
+                                 g: torch.Tensor, C: int, want_T: bool = False,
+                                 W: Optional[torch.Tensor] = None, U: Optional[torch.Tensor] = None,
+                                 Tinv: Optional[torch.Tensor] = None, stream=None):
+    """Fused build A -> exact inverse (block-wise) -> (W, U[, Tinv])."""
+    B, L, H, dk = K.shape
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    W = torch.empty_like(K) if W is None else W
+    U = torch.empty_like(V) if U is None else U
+    if want_T and Tinv is None:
+        Tinv = torch.empty((B, H, L // C, C, C), dtype=K.dtype, device=K.device)
+    tok = B * L * H
+    tp = (_dev(Tinv, "Tinv", K.dtype, B * H * (L // C if C else 0) * C * C)
+          if Tinv is not None else None)
+    _check("gdn_chunk_wy_fused_blockwise", lib.gdn_chunk_wy_fused_blockwise(
+        _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv), _dev(beta, "beta", torch.float32, tok),
+        _dev(g, "g", torch.float32, tok), _dev(W, "W", K.dtype, tok * dk),
+        _dev(U, "U", K.dtype, tok * dv), tp, B, L, H, dk, dv, C, dt, _stream(stream)))
     return (W, U, Tinv) if Tinv is not None else (W, U)
 
 

@@ -153,13 +153,14 @@ int gdn_wy_apply(const void* Tinv, const void* K, const void* V, const float* be
       gdn::launch_wy(Tinv, K, V, beta, W, U, B, L, H, dk, dv, C, dtype, (hipStream_t)stream));
 }
 
-int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
-                       void* U, void* Tinv, int B, int L, int H, int dk, int dv, int C, int N,
-                       int S, int dtype, void* stream) {
+namespace {
+int wy_fused(const void* K, const void* V, const float* beta, const float* g, void* W, void* U,
+             void* Tinv, int B, int L, int H, int dk, int dv, int C, int N, int S, int dtype,
+             bool exact, void* stream) {
   int64_t n = 0;
   if (int r = check_chunked(B, L, H, C, &n)) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
-  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (n == 0) return GDN_OK;
   if (!K || !V || !beta || !g || !W || !U) return GDN_ERR_NULL;
@@ -177,7 +178,20 @@ int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const fl
   if (overlap(W, kb, U, vb) || overlap(W, kb, Tinv, tb) || overlap(U, vb, Tinv, tb))
     return GDN_ERR_ALIAS;
   return hip_status(gdn::launch_fused(K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, N, S, dtype,
-                                      (hipStream_t)stream));
+                                      exact, (hipStream_t)stream));
+}
+}  // namespace
+
+int gdn_chunk_wy_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
+                       void* U, void* Tinv, int B, int L, int H, int dk, int dv, int C, int N,
+                       int S, int dtype, void* stream) {
+  return wy_fused(K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, N, S, dtype, false, stream);
+}
+
+int gdn_chunk_wy_fused_blockwise(const void* K, const void* V, const float* beta, const float* g,
+                                 void* W, void* U, void* Tinv, int B, int L, int H, int dk, int dv,
+                                 int C, int dtype, void* stream) {
+  return wy_fused(K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, 0, 0, dtype, true, stream);
 }
 
 int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,

@@ -19,9 +19,10 @@ hipError_t launch_build_A(const void* K, const float* beta, const float* g, void
 hipError_t launch_wy(const void* T, const void* K, const void* V, const float* beta, void* W,
                      void* U, int B, int L, int H, int dk, int dv, int C, int dtype,
                      hipStream_t st);
+// exact: the exact block-wise inverse instead of T_hat(N, S)
 hipError_t launch_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
                         void* U, void* T, int B, int L, int H, int dk, int dv, int C, int N,
-                        int S, int dtype, hipStream_t st);
+                        int S, int dtype, bool exact, hipStream_t st);
 hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                               hipStream_t st);
 hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,

@@ -177,7 +177,7 @@ __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO*
 // One tile per wave.  PREF (bf16 only): V is copied into LDS by DMA right
 // after the Gram product and arrives while the inverse is computed.
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool PREF = false>
+          bool PREF = false, bool EXACT = false>
 __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               const TIO* __restrict__ V,
                                               const float* __restrict__ beta,
@@ -194,27 +194,38 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
 
   Pair<F> kp[NB][DK / 32];
   load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
-  RowP<NB, F> LR;
-  Acc<NB> Lc;
-  {
-    gram_lower<NB, DK, false>(Lc, kp);
-    // issued once K has been consumed: the compiler counts DMA completions
-    // as unordered with plain loads and would otherwise wait for V before
-    // the Gram; the inverse below touches no global memory
+  // issued once K has been consumed: the compiler counts DMA completions as
+  // unordered with plain loads and would otherwise wait for V before the
+  // Gram; the inverse that follows touches no global memory
+  auto prefetch_v = [&]() {
     if constexpr (PREF) {
       __builtin_amdgcn_sched_barrier(0);
       prefetch_rows_lds<NB, DV>((const __bf16*)V + ch.row(0, L, H, DV), (int64_t)H * DV, sv);
       __builtin_amdgcn_sched_barrier(0);
     }
-    gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
-    ColP<NB, F> LC;
-    to_colp(LC, Lc);
-    Acc<NB> r;
-    col_to_row(r, LC, 1, C - 1);
-    to_rowp(LR, r);
-  }
+  };
   Acc<NB> Tr;
-  neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
+  if constexpr (EXACT) {
+    Acc<NB> Lr;
+    gram_lower<NB, DK, true>(Lr, kp);
+    prefetch_v();
+    gate_scale<NB, true>(Lr, sb, sg, -1.f);  // Lm = -A, row form
+    blockwise_inverse<NB, F>(Lr, Tr);
+  } else {
+    RowP<NB, F> LR;
+    Acc<NB> Lc;
+    {
+      gram_lower<NB, DK, false>(Lc, kp);
+      prefetch_v();
+      gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
+      ColP<NB, F> LC;
+      to_colp(LC, Lc);
+      Acc<NB> r;
+      col_to_row(r, LC, 1, C - 1);
+      to_rowp(LR, r);
+    }
+    neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
+  }
   if (Tout) store_unit_row<NB>(Tout + tile * (C * C), C, Tr);
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
@@ -321,7 +332,8 @@ __device__ __forceinline__ void block2_slice(const RowP<4, F>& X22R, const Pair<
   }
 }
 
-template <int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO>
+template <int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
+          bool EXACT = false>
 __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
                                                   const TIO* __restrict__ V,
                                                   const float* __restrict__ beta,
@@ -359,7 +371,12 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
   }
   __syncthreads();  // gates and K_1 in LDS
   Acc<NB> Tr;
-  {
+  if constexpr (EXACT) {
+    Acc<NB> Lr;
+    gram_lower<NB, DK, true>(Lr, kp);
+    gate_scale<NB, true>(Lr, sb + r0, sg + r0, -1.f);  // Lm = -A_kk, row form
+    blockwise_inverse<NB, F>(Lr, Tr);
+  } else {
     RowP<NB, F> LR;
     Acc<NB> Lc;
     gram_lower<NB, DK, false>(Lc, kp);
@@ -577,10 +594,11 @@ template <> struct FusedOrder<1> { static constexpr int N = 3, S = 2; };
 template <> struct FusedOrder<2> { static constexpr int N = 3, S = 4; };
 template <> struct FusedOrder<4> { static constexpr int N = 3, S = 8; };
 
-template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO, bool PREF>
+template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO, bool PREF,
+          bool EXACT = false>
 static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,
                        void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st) {
-  hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF>), dim3((unsigned)n),
+  hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT>), dim3((unsigned)n),
                      dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U,
                      (TIO*)T, L, H, N, S);
 }
@@ -590,11 +608,14 @@ static void launch_one(const void* K, const void* V, const float* beta, const fl
 template <int NB, typename F, typename TIO>
 static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, const float* g,
                                void* W, void* U, void* T, int64_t n, int L, int H, int dk,
-                               int dv, int N, int S, hipStream_t st) {
+                               int dv, int N, int S, bool exact, hipStream_t st) {
   constexpr int DN = FusedOrder<NB>::N, DS = FusedOrder<NB>::S;
   constexpr bool PREF = sizeof(TIO) == 2 && NB > 1;
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
-    if (N == DN && S == DS)
+    if (exact)
+      launch_one<NB, DK, DV, F, true, 0, 0, TIO, PREF, true>(K, V, beta, g, W, U, T, n, L, H, N,
+                                                             S, st);
+    else if (N == DN && S == DS)
       launch_one<NB, DK, DV, F, true, DN, DS, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
                                                           st);
     else if (N <= 15)
@@ -611,18 +632,20 @@ static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, 
 template <typename F, typename TIO>
 static hipError_t run_fused128(const void* K, const void* V, const float* beta, const float* g,
                                void* W, void* U, void* T, int64_t n, int L, int H, int dk,
-                               int dv, int N, int S, hipStream_t st) {
-#define GDN_F128(SM, NC_, SC_)                                                                 \
-  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO>), dim3((unsigned)n), dim3(128), \
-                     0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, \
-                     H, N, S)
+                               int dv, int N, int S, bool exact, hipStream_t st) {
+#define GDN_F128(SM, NC_, SC_, EX)                                                            \
+  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO, EX>), dim3((unsigned)n),       \
+                     dim3(128), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, \
+                     (TIO*)T, L, H, N, S)
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
-    if (N == 3 && S == 8)
-      GDN_F128(true, 3, 8);
+    if (exact)
+      GDN_F128(true, 0, 0, true);
+    else if (N == 3 && S == 8)
+      GDN_F128(true, 3, 8, false);
     else if (N <= 15)
-      GDN_F128(true, -1, -1);
+      GDN_F128(true, -1, -1, false);
     else
-      GDN_F128(false, -1, -1);
+      GDN_F128(false, -1, -1, false);
     return hipGetLastError();
   }))
 #undef GDN_F128
@@ -632,24 +655,24 @@ static hipError_t run_fused128(const void* K, const void* V, const float* beta, 
 template <typename F, typename TIO>
 static hipError_t run_fused(const void* K, const void* V, const float* beta, const float* g,
                             void* W, void* U, void* T, int64_t n, int L, int H, int dk, int dv,
-                            int C, int N, int S, hipStream_t st) {
+                            int C, int N, int S, bool exact, hipStream_t st) {
   switch (C) {
-    case 128: return run_fused128<F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
-    case 16: return run_fused_nb<1, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
-    case 32: return run_fused_nb<2, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
-    case 64: return run_fused_nb<4, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, st);
+    case 128: return run_fused128<F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, exact, st);
+    case 16: return run_fused_nb<1, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, exact, st);
+    case 32: return run_fused_nb<2, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, exact, st);
+    case 64: return run_fused_nb<4, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, exact, st);
   }
   return hipErrorNotSupported;
 }
 
 hipError_t launch_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
                         void* U, void* T, int B, int L, int H, int dk, int dv, int C, int N,
-                        int S, int dtype, hipStream_t st) {
+                        int S, int dtype, bool exact, hipStream_t st) {
   const int64_t n = (int64_t)B * H * (L / C);
   if (dtype == 0)
-    return run_fused<f32x4, float>(K, V, beta, g, W, U, T, n, L, H, dk, dv, C, N, S, st);
+    return run_fused<f32x4, float>(K, V, beta, g, W, U, T, n, L, H, dk, dv, C, N, S, exact, st);
   if (dtype == 1)
-    return run_fused<bf16x4, __bf16>(K, V, beta, g, W, U, T, n, L, H, dk, dv, C, N, S, st);
+    return run_fused<bf16x4, __bf16>(K, V, beta, g, W, U, T, n, L, H, dk, dv, C, N, S, exact, st);
   return hipErrorNotSupported;
 }
 

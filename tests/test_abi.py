@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 12
+    assert len(names) == 13
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -126,6 +126,22 @@ def test_fused_validation():
     assert f(*bad) == ALIGN
     zero = list(base); zero[7] = 0
     zero[0] = zero[1] = None
+    assert f(*zero) == OK
+
+
+def test_fused_blockwise_validation():
+    f = L.gdn_chunk_wy_fused_blockwise
+    # K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, dtype, stream
+    base = [P1, BIG, 2 * BIG, 3 * BIG, 4 * BIG, 5 * BIG, None, 1, 256, 2, 128, 128, 64, 1, None]
+    bad = list(base); bad[12] = 48
+    assert f(*bad) == SHAPE
+    bad = list(base); bad[13] = 2
+    assert f(*bad) == DTYPE
+    bad = list(base); bad[4] = None
+    assert f(*bad) == NULL
+    bad = list(base); bad[4] = P1 + 512
+    assert f(*bad) == ALIAS
+    zero = list(base); zero[7] = 0
     assert f(*zero) == OK
 
 

@@ -324,6 +324,35 @@ def test_fused_stress_and_orders(C, dt):
             assert eU <= TOL[dt] * scale * max(1.0, np.max(np.abs(Ur)))
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_fused_blockwise_exact(C, dt):
+    """Fused path with the exact block-wise inverse: W, U, Tinv against the
+    oracle's exact inverse X (workload and stress heads, dk = dv = 128 / 64)."""
+    for stress, dk in ((False, 128), (True, 128), (True, 64)):
+        if stress:
+            heads = [wl.gen_stress_head(2 * max(C, 64), dk, C, seed=70 + h, dv=dk)
+                     for h in range(2)]
+            K, beta, g, V = (stored(wl.as_blhd(*[x[i] for x in heads]),
+                                    dt if i in (0, 3) else "f32") for i in range(4))
+        else:
+            w = wl.workload("tiny").with_(dtype=dt, L=4 * max(C, 64))
+            K, beta, g, V = head_inputs(w, C, 2, dt)
+        X = gdn.forward_substitution_inverse(gdn.build_A(K, beta, g, C))
+        Wr, Ur = gdn.wy_apply(X, K, V, beta, C)
+        W, U, T = G.gdn_chunk_wy_fused_blockwise(dev(K, dt), dev(V, dt), dev(beta), dev(g), C,
+                                                 want_T=True)
+        scale = max(1.0, np.max(np.abs(X)))
+        eT, eW, eU = maxerr(host(T), X), maxerr(host(W), Wr), maxerr(host(U), Ur)
+        print(f"fused exact C={C} {dt} stress={stress} dk={dk} T {eT:.2e} W {eW:.2e} U {eU:.2e}",
+              flush=True)
+        assert eT <= TOL[dt] * scale
+        assert eW <= TOL[dt] * scale * max(1.0, np.max(np.abs(Wr)))
+        assert eU <= TOL[dt] * scale * max(1.0, np.max(np.abs(Ur)))
+        W2, U2 = G.gdn_chunk_wy_fused_blockwise(dev(K, dt), dev(V, dt), dev(beta), dev(g), C)
+        assert np.array_equal(host(W2), host(W)) and np.array_equal(host(U2), host(U))
+
+
 def test_fused_matches_unfused_composition():
     """build_A -> neumann -> wy_apply equals the fused kernel (fp32)."""
     C = 64
