@@ -23,7 +23,10 @@ Modules:
         Newton form, block-wise inverse (Appendix E), WY application,
         accuracy metrics.
   int8  exact-integer oracle of the low-bit (INT8) pipeline.
+  gdn_forward  float64 oracle of the whole chunk-wise Gated DeltaNet forward
+        (token recurrence, and the chunk-wise form around the inverse).
 """
 
 from . import gdn  # noqa: F401
 from . import int8  # noqa: F401
+from . import gdn_forward  # noqa: F401

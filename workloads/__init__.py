@@ -12,7 +12,9 @@ Layouts (row-major, contiguous):
 Each (b, h) head draws from its own counter-addressed numpy stream
 (``default_rng([seed, b, h])``), so one head's inputs can be regenerated
 without generating the whole batch; within a head the draws come in the
-order K, beta, decay increments, V.
+order K, beta, decay increments, V, Q.  Queries are unit rows like the
+keys.  An initial state S0 [dk, dv] ~ N(0, 1) comes from a stream of its
+own (``default_rng([seed, b, h, 1])``).
 """
 
 from __future__ import annotations
@@ -30,6 +32,9 @@ __all__ = [
     "round_to_bf16",
     "bf16_bits",
     "gen_head",
+    "gen_head_qkv",
+    "gen_state",
+    "gen_forward_inputs",
     "gen_inputs",
     "gen_inputs_heads",
     "chunk_cumsum",
@@ -147,14 +152,7 @@ def chunk_cumsum(inc: np.ndarray, C: int, axis: int = 0) -> np.ndarray:
     return np.moveaxis(r.reshape(inc.shape), 0, axis)
 
 
-def gen_head(w: Workload, b: int, h: int, C: Optional[int] = None,
-             want_v: bool = True) -> Tuple[np.ndarray, np.ndarray, np.ndarray, Optional[np.ndarray]]:
-    """Inputs of one (b, h) head: K [L, dk], beta [L], g [L], V [L, dv].
-
-    K, V are rounded to the workload's storage dtype (returned as float32
-    arrays holding the stored values); beta and g are float32.
-    """
-    C = w.C if C is None else C
+def _draw_head(w: Workload, b: int, h: int, C: int, want_v: bool, want_q: bool):
     rng = np.random.default_rng([w.seed, b, h])
     z = rng.standard_normal((w.L, w.dk))
     k = z / np.linalg.norm(z, axis=1, keepdims=True)
@@ -167,9 +165,60 @@ def gen_head(w: Workload, b: int, h: int, C: Optional[int] = None,
     else:
         raise ValueError(w.gate)
     g = chunk_cumsum(inc, C)
-    v = rng.standard_normal((w.L, w.dv)) if want_v else None
+    v = rng.standard_normal((w.L, w.dv)) if (want_v or want_q) else None
+    q = None
+    if want_q:
+        z = rng.standard_normal((w.L, w.dk))
+        q = z / np.linalg.norm(z, axis=1, keepdims=True)
+    return k, beta, g, v, q
+
+
+def gen_head(w: Workload, b: int, h: int, C: Optional[int] = None,
+             want_v: bool = True) -> Tuple[np.ndarray, np.ndarray, np.ndarray, Optional[np.ndarray]]:
+    """Inputs of one (b, h) head: K [L, dk], beta [L], g [L], V [L, dv].
+
+    K, V are rounded to the workload's storage dtype (returned as float32
+    arrays holding the stored values); beta and g are float32.
+    """
+    C = w.C if C is None else C
+    k, beta, g, v, _ = _draw_head(w, b, h, C, want_v, False)
     return (_store(k, w.dtype), beta.astype(np.float32), g.astype(np.float32),
             None if v is None else _store(v, w.dtype))
+
+
+def gen_head_qkv(w: Workload, b: int, h: int, C: Optional[int] = None):
+    """Inputs of one (b, h) head for the whole layer: Q [L, dk], K [L, dk],
+    V [L, dv] (storage dtype values as float32), beta [L], g [L] (float32).
+    K, beta, g, V are the values gen_head returns."""
+    C = w.C if C is None else C
+    k, beta, g, v, q = _draw_head(w, b, h, C, True, True)
+    return (_store(q, w.dtype), _store(k, w.dtype), _store(v, w.dtype),
+            beta.astype(np.float32), g.astype(np.float32))
+
+
+def gen_state(w: Workload, b: int, h: int) -> np.ndarray:
+    """Initial state S0 [dk, dv] of one head, float32 ~ N(0, 1)."""
+    rng = np.random.default_rng([w.seed, b, h, 1])
+    return rng.standard_normal((w.dk, w.dv)).astype(np.float32)
+
+
+def gen_forward_inputs(w: Workload, C: Optional[int] = None, want_state: bool = True):
+    """Full-size layer inputs: Q, K [B, L, H, dk], V [B, L, H, dv],
+    beta, g [B, L, H], S0 [B, H, dk, dv] (or None); float32 arrays holding
+    the stored values."""
+    C = w.C if C is None else C
+    Q = np.empty((w.B, w.L, w.H, w.dk), np.float32)
+    K = np.empty_like(Q)
+    V = np.empty((w.B, w.L, w.H, w.dv), np.float32)
+    beta = np.empty((w.B, w.L, w.H), np.float32)
+    g = np.empty_like(beta)
+    S0 = np.empty((w.B, w.H, w.dk, w.dv), np.float32) if want_state else None
+    for b in range(w.B):
+        for h in range(w.H):
+            Q[b, :, h], K[b, :, h], V[b, :, h], beta[b, :, h], g[b, :, h] = gen_head_qkv(w, b, h, C=C)
+            if want_state:
+                S0[b, h] = gen_state(w, b, h)
+    return Q, K, V, beta, g, S0
 
 
 def gen_inputs_heads(w: Workload, heads: Iterable[Tuple[int, int]], C: Optional[int] = None,
