@@ -60,7 +60,8 @@ enum gdn_status {
   GDN_ERR_ALIGN = -5,       /* a pointer is not 16-byte aligned               */
   GDN_ERR_ALIAS = -6,       /* an output overlaps an input                    */
   GDN_ERR_HIP = -7,         /* the HIP runtime rejected a launch              */
-  GDN_ERR_UNSUPPORTED = -8  /* valid request this build does not implement    */
+  GDN_ERR_UNSUPPORTED = -8, /* valid request this build does not implement    */
+  GDN_ERR_WORKSPACE = -9    /* the caller's workspace is smaller than needed  */
 };
 
 /* Version of this ABI (GDN_ABI_VERSION). */
@@ -177,6 +178,40 @@ int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq
 int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const float* g,
                                        int8_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                        int dk, int C, int N, int S, int k_dtype, void* stream);
+
+/* Chunk-wise Gated DeltaNet forward of one layer, built around the chunk
+ * inverse: the chunk-level recurrence of Gated DeltaNet that Section 1
+ * starts from, with Y = T^-1 X (Appendix E) evaluated per chunk.  Per head,
+ * with the [dk, dv] state S, the token recurrence it computes is
+ *   S_t = a_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
+ *   o_t = scale S_t^T q_t,   a_t = exp(g_t - g_{t-1}) inside a chunk,
+ * evaluated chunk by chunk: T = (I + A)^-1 (T_hat(N, S) of
+ * gdn_chunk_inverse_neumann, or the exact block-wise inverse when exact = 1),
+ * W = T diag(beta e^g) K, U = T diag(beta) V, V_new = U - W S,
+ * O = scale (diag(e^g) Q S + ((Q K^T) (.) D) V_new) with D_ij = e^{g_i - g_j}
+ * for i >= j (else 0), S' = e^{g_last} S + K^T diag(e^{g_last - g}) V_new.
+ * Q, K: [B, L, H, dk]; V, O: [B, L, H, dv], all in `dtype` (GDN_F32 or
+ * GDN_BF16); beta, g: [B, L, H] fp32 as for gdn_build_A.  S0 (nullable:
+ * zero state) and S_final (nullable: not written): [B, H, dk, dv] fp32;
+ * S_final may be S0 itself (updated in place) but must not overlap it
+ * otherwise.  bf16 mode rounds to bf16 every MFMA operand, including the
+ * state where it multiplies W and Q and V_new where it multiplies P and K^T;
+ * the state itself is carried in fp32.  workspace: device memory of at least
+ * gdn_chunk_forward_workspace() bytes, owned by the caller, contents
+ * undefined on return; it must not overlap any tensor argument.
+ * C in {16, 32, 64} (GDN_ERR_UNSUPPORTED for 128).  L = 0 with B H > 0
+ * copies S0 (or zeros) into S_final.  GDN_ERR_WORKSPACE if workspace_bytes
+ * is too small.  Two launches on `stream`: every chunk in parallel, then one
+ * wave per (batch, head, 16 value columns) walking the chunks in order. */
+int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* beta,
+                      const float* g, const float* S0, void* O, float* S_final, void* workspace,
+                      int64_t workspace_bytes, int B, int L, int H, int dk, int dv, int C, int N,
+                      int S, int exact, float scale, int dtype, void* stream);
+
+/* Workspace bytes gdn_chunk_forward needs for these sizes (0 when there is
+ * no chunk); GDN_ERR_SHAPE / GDN_ERR_DTYPE / GDN_ERR_NULL as for the call. */
+int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int dtype,
+                                int64_t* bytes);
 
 #ifdef __cplusplus
 }

@@ -1,7 +1,7 @@
 """MI355X (gfx950) MatMul-only chunk inversion for chunk-wise Gated DeltaNet.
 
 Python binding of the C ABI in include/gdninv.h (libgdninv.so, built in this
-directory by ``python -m paper_2606_06034_amd.csrc.build``).  Every function
+directory by ``python paper_2606_06034_amd/csrc/build.py``).  Every function
 here has the name of the C entry point it wraps and only marshals arguments:
 it checks that tensors are contiguous device tensors of the right dtype and
 shape, allocates outputs with torch when the caller passes none, and calls
@@ -19,6 +19,8 @@ from ._binding import (  # noqa: F401
     abi_symbols,
     gdn_abi_version,
     gdn_build_A,
+    gdn_chunk_forward,
+    gdn_chunk_forward_workspace,
     gdn_chunk_inverse_fwdsub,
     gdn_chunk_inverse_blockwise,
     gdn_chunk_inverse_neumann,

@@ -33,12 +33,17 @@ _SIGS = {
     "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i8_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
                                            _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_forward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int,
+                          _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_float,
+                          _c_int, _vp],
+    "gdn_chunk_forward_workspace": [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                    ctypes.POINTER(_c_i64)],
 }
 
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2606_06034_amd.csrc.build`")
+        raise ImportError(f"{LIB_PATH} is not built: run `python paper_2606_06034_amd/csrc/build.py`")
     L = ctypes.CDLL(LIB_PATH)
     for name, args in _SIGS.items():
         fn = getattr(L, name)
@@ -288,3 +293,48 @@ def gdn_chunk_inverse_neumann_i8_fused(K: torch.Tensor, beta: torch.Tensor, g: t
         _dev(Td, "Tdeq", torch.float32, n * C * C) if Td is not None else None,
         B, L, H, dk, C, N, S, _fdtype(K, "K"), _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)
+
+
+def gdn_chunk_forward_workspace(B: int, L: int, H: int, dk: int, dv: int, C: int,
+                                dtype: torch.dtype) -> int:
+    """Bytes of workspace gdn_chunk_forward needs for these sizes."""
+    n = _c_i64()
+    _check("gdn_chunk_forward_workspace", lib.gdn_chunk_forward_workspace(
+        B, L, H, dk, dv, C, _FDT[dtype], ctypes.byref(n)))
+    return n.value
+
+
+def gdn_chunk_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor,
+                      g: torch.Tensor, C: int, S0: Optional[torch.Tensor] = None,
+                      N: Optional[int] = None, S: Optional[int] = None, exact: bool = False,
+                      scale: Optional[float] = None, want_state: bool = True,
+                      O: Optional[torch.Tensor] = None, S_final: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None, stream=None):
+    """Chunk-wise Gated DeltaNet forward: (O [B, L, H, dv], S_final [B, H, dk, dv] fp32 or
+    None).  N, S default to gdn_default_order(C); scale defaults to dk ** -0.5.  The
+    workspace (a byte tensor of gdn_chunk_forward_workspace() bytes) is allocated when
+    not given."""
+    B, L, H, dk = K.shape
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    if N is None or S is None:
+        dn, ds = gdn_default_order(C) if C in (16, 32, 64, 128) else (0, 0)
+        N = dn if N is None else N
+        S = ds if S is None else S
+    scale = dk ** -0.5 if scale is None else float(scale)
+    tok = B * L * H
+    O = torch.empty_like(V) if O is None else O
+    if want_state and S_final is None:
+        S_final = torch.empty((B, H, dk, dv), dtype=torch.float32, device=K.device)
+    need = gdn_chunk_forward_workspace(B, L, H, dk, dv, C, K.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=K.device)
+    sp = _dev(S0, "S0", torch.float32, B * H * dk * dv) if S0 is not None else None
+    fp = _dev(S_final, "S_final", torch.float32, B * H * dk * dv) if S_final is not None else None
+    _check("gdn_chunk_forward", lib.gdn_chunk_forward(
+        _dev(Q, "Q", K.dtype, tok * dk), _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv),
+        _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok), sp,
+        _dev(O, "O", K.dtype, tok * dv), fp, _dev(workspace, "workspace"), workspace.numel() *
+        workspace.element_size(), B, L, H, dk, dv, C, N, S, int(bool(exact)), scale, dt,
+        _stream(stream)))
+    return O, S_final

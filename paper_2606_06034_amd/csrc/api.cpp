@@ -61,6 +61,7 @@ const char* gdn_status_string(int status) {
     case GDN_ERR_ALIAS: return "an output overlaps an input";
     case GDN_ERR_HIP: return "HIP runtime error at launch";
     case GDN_ERR_UNSUPPORTED: return "combination not implemented by this build";
+    case GDN_ERR_WORKSPACE: return "workspace smaller than gdn_chunk_forward_workspace()";
   }
   return "unknown status";
 }
@@ -256,6 +257,58 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
     return GDN_ERR_ALIAS;
   return hip_status(gdn::launch_inverse_i8_fused(K, beta, g, Tq, eT, Tdeq, B, L, H, dk, C, N, S,
                                                  k_dtype, (hipStream_t)stream));
+}
+
+int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int dtype,
+                                int64_t* bytes) {
+  if (!bytes) return GDN_ERR_NULL;
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (C == 128) return GDN_ERR_UNSUPPORTED;
+  *bytes = n * gdn::fwd_workspace_elems(C, dk, dv) * esize(dtype);
+  return GDN_OK;
+}
+
+int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* beta,
+                      const float* g, const float* S0, void* O, float* S_final, void* workspace,
+                      int64_t workspace_bytes, int B, int L, int H, int dk, int dv, int C, int N,
+                      int S, int exact, float scale, int dtype, void* stream) {
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
+  if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
+  if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (C == 128) return GDN_ERR_UNSUPPORTED;
+  if ((int64_t)B * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
+  const int64_t es = esize(dtype), tok = (int64_t)B * L * H;
+  const int64_t need = n * gdn::fwd_workspace_elems(C, dk, dv) * es;
+  const int64_t sb = (int64_t)B * H * dk * dv * 4;
+  if ((int64_t)B * H == 0) return GDN_OK;
+  if (n > 0 && (!Q || !K || !V || !beta || !g || !O || !workspace)) return GDN_ERR_NULL;
+  if (n > 0 && workspace_bytes < need) return GDN_ERR_WORKSPACE;
+  const void* ptrs[9] = {Q, K, V, beta, g, S0, O, S_final, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned(p)) return GDN_ERR_ALIGN;
+  const int64_t qb = tok * dk * es, vb = tok * dv * es, bb = tok * 4;
+  // inputs (S0 apart) against the outputs and the workspace
+  const void* ins[6] = {Q, K, V, beta, g, S0};
+  const int64_t inb[6] = {qb, qb, vb, bb, bb, sb};
+  const void* outs[3] = {O, workspace, S_final};
+  const int64_t outb[3] = {vb, need, sb};
+  for (int o = 0; o < 3; ++o) {
+    for (int i = 0; i < 6; ++i) {
+      if (o == 2 && i == 5 && S_final == S0) continue;  // in-place state update
+      if (overlap(outs[o], outb[o], ins[i], inb[i])) return GDN_ERR_ALIAS;
+    }
+    for (int o2 = o + 1; o2 < 3; ++o2)
+      if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return GDN_ERR_ALIAS;
+  }
+  return hip_status(gdn::launch_forward(Q, K, V, beta, g, S0, O, S_final, workspace, B, L, H, dk,
+                                        dv, C, N, S, exact != 0, scale, dtype,
+                                        (hipStream_t)stream));
 }
 
 }  // extern "C"

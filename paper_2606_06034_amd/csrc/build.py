@@ -1,6 +1,6 @@
 """Build libgdninv.so (gfx950) in-tree.
 
-    python -m paper_2606_06034_amd.csrc.build [--jobs N] [--verbose]
+    python paper_2606_06034_amd/csrc/build.py [--jobs N] [--verbose]
 
 Compiles every csrc/*.hip and csrc/*.cpp with hipcc for gfx950 only and links
 them into paper_2606_06034_amd/libgdninv.so.  Objects go to _build/ at the

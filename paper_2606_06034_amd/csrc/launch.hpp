@@ -8,6 +8,18 @@
 
 namespace gdn {
 
+// compile-time feature widths for the templated launchers
+#define GDN_DK_SWITCH(dk, ...)                     \
+  switch (dk) {                                    \
+    case 64: { constexpr int DK = 64; __VA_ARGS__ }   \
+    case 128: { constexpr int DK = 128; __VA_ARGS__ } \
+  }
+#define GDN_DV_SWITCH(dv, ...)                     \
+  switch (dv) {                                    \
+    case 64: { constexpr int DV = 64; __VA_ARGS__ }   \
+    case 128: { constexpr int DV = 128; __VA_ARGS__ } \
+  }
+
 hipError_t launch_neumann(const void* A, void* T, int64_t n_tiles, int C, int N, int S,
                           int dtype, hipStream_t st);
 hipError_t launch_fwdsub(const void* A, void* T, int64_t n_tiles, int C, int dtype,
@@ -23,6 +35,13 @@ hipError_t launch_wy(const void* T, const void* K, const void* V, const float* b
 hipError_t launch_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
                         void* U, void* T, int B, int L, int H, int dk, int dv, int C, int N,
                         int S, int dtype, bool exact, hipStream_t st);
+// chunk-wise Gated DeltaNet forward (two launches); ws holds
+// fwd_workspace_elems(C, dk, dv) elements of the IO type per chunk tile
+hipError_t launch_forward(const void* Q, const void* K, const void* V, const float* beta,
+                          const float* g, const float* S0, void* O, float* Sfin, void* ws, int B,
+                          int L, int H, int dk, int dv, int C, int N, int S, bool exact,
+                          float scale, int dtype, hipStream_t st);
+int64_t fwd_workspace_elems(int C, int dk, int dv);
 hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                               hipStream_t st);
 hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,

@@ -3,114 +3,10 @@
 //
 //   A_ij = beta_i (k_i . k_j) exp(g_i - g_j) for i > j       (Section 2.1)
 //   W = T diag(beta) K,  U = T diag(beta) V
-//
-// K/V rows of a chunk are strided by H * d in the [B, L, H, d] layout; every
-// global access is a run of 8 consecutive features of one token (16 bytes in
-// bf16).  Column-form (token-major) fragments of K and V are made on chip by
-// identity MFMAs.
-#include "chunk.hpp"
-#include "engine.hpp"
 #include "launch.hpp"
+#include "wy.hpp"
 
 namespace gdn {
-
-// Asynchronous copy of a bf16 chunk of X into LDS (global -> LDS DMA, no
-// registers): the 16-byte run lane (g, c) would load in load_rows lands at
-// s + 512 (I * D / 32 + q) + 8 * lane.  Completion is tracked by vmcnt.
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) void glb_void;
-
-template <int NB, int D>
-__device__ __forceinline__ void prefetch_rows_lds(const __bf16* __restrict__ xb, int64_t ld,
-                                                  __bf16* s, Lane ln = lane_here()) {
-  const int g = ln.g(), c = ln.c();
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int q = 0; q < D / 32; ++q)
-      __builtin_amdgcn_global_load_lds((glb_void*)(xb + (I * 16 + c) * ld + 32 * q + 8 * g),
-                                       (lds_void*)(s + 512 * (I * (D / 32) + q)), 16, 0, 0);
-}
-
-// wait for every outstanding vector-memory operation of this wave
-// (s_waitcnt vmcnt(0))
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
-// out = T' X for one chunk, T' = T diag(beta) as row pairs (beta folded into
-// T's columns), X given by get(I, q): its row-form pair of rows 16I..16I+15,
-// features 32q..32q+31 (registers, or LDS read one 32-feature slice at a
-// time).  Each 16 x 16 block of X is moved to column form by an identity
-// MFMA (X I), then W(I, .) = sum_K T'(I, K) X(K, .) comes out in row form and
-// is stored 8 features per lane.  ob points at (token t0, head h, feature 0)
-// of the output; lds_copy (optional) receives the output pairs in the slot
-// layout LdsRows reads.
-template <int NB, int D, typename F, typename TIO, typename Get>
-__device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, Get&& get,
-                                            TIO* __restrict__ ob, int64_t ld,
-                                            Lane ln = lane_here(), TIO* lds_copy = nullptr) {
-  const int g = ln.g(), c = ln.c();
-  const f32x4 e = eye4(ln);
-  const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
-#pragma unroll
-  for (int q = 0; q < D / 32; ++q) {
-    Pair<F> x[NB];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) x[I] = get(I, q);
-    Pair<F> y[2][npair(NB)];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int p = 0; p < npair(NB); ++p) {
-        const f32x4 a = Pair<F>::template mma<false>(x[2 * p], h ? id1 : id0, zero4());
-        const f32x4 b = (2 * p + 1 < NB)
-                            ? Pair<F>::template mma<false>(x[2 * p + 1], h ? id1 : id0, zero4())
-                            : zero4();
-        y[h][p] = Pair<F>::make(a, b);
-      }
-#pragma unroll
-    for (int I = 0; I < NB; ++I) {
-      f32x4 acc[2] = {zero4(), zero4()};
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int p = 0; p < npair(NB); ++p)
-          if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(TR.r[I][p], y[h][p], acc[h]);
-      store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
-      if (lds_copy) store_row8(lds_copy + 512 * (I * (D / 32) + q) + 8 * ln.id, acc[0], acc[1]);
-    }
-  }
-}
-// operand getters: pairs held in registers, or the LDS copy prefetch_rows_lds
-// made (one 16-byte read per lane and pair)
-template <int NB, int D, typename F>
-struct RegRows {
-  const Pair<F> (&xp)[NB][D / 32];
-  __device__ __forceinline__ Pair<F> operator()(int I, int q) const { return xp[I][q]; }
-};
-// slot (I, q) of an LDS copy: 8 elements per lane, lane-major
-template <int D, typename F = bf16x4, typename TIO = __bf16>
-struct LdsRows {
-  const TIO* s;
-  int l;
-  __device__ __forceinline__ Pair<F> operator()(int I, int q) const {
-    return load_row8<F>(s + 512 * (I * (D / 32) + q) + 8 * l);
-  }
-};
-
-// T diag(beta) as row pairs from the row-form blocks of the unit lower T:
-// value v of lane (g, c) in block (I, J) sits in column 16J + 4g + v.
-template <int NB, typename F>
-__device__ __forceinline__ void scale_cols(RowP<NB, F>& TR, Acc<NB> T, const float* sb,
-                                           Lane ln = lane_here()) {
-  const int g = ln.g();
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) T.a[bidx(I, J)][v] *= sb[16 * J + 4 * g + v];
-  to_rowp(TR, T);
-}
 
 // ---------------------------------------------------------------------------
 // gdn_build_A
@@ -205,27 +101,7 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
     }
   };
   Acc<NB> Tr;
-  if constexpr (EXACT) {
-    Acc<NB> Lr;
-    gram_lower<NB, DK, true>(Lr, kp);
-    prefetch_v();
-    gate_scale<NB, true>(Lr, sb, sg, -1.f);  // Lm = -A, row form
-    blockwise_inverse<NB, F>(Lr, Tr);
-  } else {
-    RowP<NB, F> LR;
-    Acc<NB> Lc;
-    {
-      gram_lower<NB, DK, false>(Lc, kp);
-      prefetch_v();
-      gate_scale<NB, false>(Lc, sb, sg, -1.f);  // Lm = -A, column form
-      ColP<NB, F> LC;
-      to_colp(LC, Lc);
-      Acc<NB> r;
-      col_to_row(r, LC, 1, C - 1);
-      to_rowp(LR, r);
-    }
-    neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
-  }
+  chunk_inverse<NB, DK, F, SMALLN, NC, SC, EXACT>(kp, sb, sg, N, S, Tr, prefetch_v);
   if (Tout) store_unit_row<NB>(Tout + tile * (C * C), C, Tr);
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
@@ -371,23 +247,7 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
   }
   __syncthreads();  // gates and K_1 in LDS
   Acc<NB> Tr;
-  if constexpr (EXACT) {
-    Acc<NB> Lr;
-    gram_lower<NB, DK, true>(Lr, kp);
-    gate_scale<NB, true>(Lr, sb + r0, sg + r0, -1.f);  // Lm = -A_kk, row form
-    blockwise_inverse<NB, F>(Lr, Tr);
-  } else {
-    RowP<NB, F> LR;
-    Acc<NB> Lc;
-    gram_lower<NB, DK, false>(Lc, kp);
-    gate_scale<NB, false>(Lc, sb + r0, sg + r0, -1.f);  // Lm = -A_kk, column form
-    ColP<NB, F> LC;
-    to_colp(LC, Lc);
-    Acc<NB> r;
-    col_to_row(r, LC, 1, 63);
-    to_rowp(LR, r);
-    neumann_engine<NB, F, SMALLN, NC, SC>(LR, Lc, N, S, Tr);
-  }
+  chunk_inverse<NB, DK, F, SMALLN, NC, SC, EXACT>(kp, sb + r0, sg + r0, N, S, Tr, [] {});
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
   if (wv == 0) {
@@ -506,17 +366,6 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
 
 // ---------------------------------------------------------------------------
 // launchers
-
-#define GDN_DK_SWITCH(dk, ...)                     \
-  switch (dk) {                                    \
-    case 64: { constexpr int DK = 64; __VA_ARGS__ }   \
-    case 128: { constexpr int DK = 128; __VA_ARGS__ } \
-  }
-#define GDN_DV_SWITCH(dv, ...)                     \
-  switch (dv) {                                    \
-    case 64: { constexpr int DV = 64; __VA_ARGS__ }   \
-    case 128: { constexpr int DV = 128; __VA_ARGS__ } \
-  }
 
 template <int NB, typename F, typename TK, typename TA>
 static hipError_t run_build_A_nb(const void* K, const float* beta, const float* g, void* A,

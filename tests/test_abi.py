@@ -13,7 +13,7 @@ import paper_2606_06034_amd as g
 
 HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "gdninv.h")
 
-OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP = 0, -1, -2, -3, -4, -5, -6, -7, -8
+OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP, WS = 0, -1, -2, -3, -4, -5, -6, -7, -8, -9
 P1, P2, P3, P4, P5, P6, P7 = (0x10000 * k for k in range(1, 8))  # aligned fake addresses
 BIG = 1 << 40  # far apart so nothing overlaps unless intended
 
@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 13
+    assert len(names) == 15
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     assert g.gdn_abi_version() == 1
-    for code in (OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP, 12345):
+    for code in (OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP, WS, 12345):
         assert isinstance(g.gdn_status_string(code), str) and g.gdn_status_string(code)
 
 
@@ -192,6 +192,58 @@ def test_int8_fused_validation():
     assert call(Tdeq=4 * BIG + 16) == ALIAS
     assert call(eT=P1 + 8) == ALIGN
     assert call(B=0, K=None, beta=None, g=None, Tq=None, eT=None) == OK
+
+
+def test_forward_workspace_size():
+    import ctypes
+    n = ctypes.c_int64()
+    f = L.gdn_chunk_forward_workspace
+    assert f(1, 8192, 16, 128, 128, 64, 1, ctypes.byref(n)) == OK
+    # per 64-token chunk: W 64x128, U 64x128, K^T 128 x 64, P 6 pair slots of 512
+    assert n.value == 2048 * (8192 + 8192 + 8192 + 6 * 512) * 2
+    assert f(1, 64, 1, 64, 64, 16, 0, ctypes.byref(n)) == OK
+    # C = 16: K^T pairs carry a zero half
+    assert n.value == 4 * (1 * 2 * 512 + 4 * 256 + 4 * 512 + 512) * 4
+    assert f(1, 64, 1, 64, 64, 16, 0, None) == NULL
+    assert f(1, 100, 1, 64, 64, 16, 0, ctypes.byref(n)) == SHAPE
+    assert f(1, 128, 1, 96, 64, 16, 0, ctypes.byref(n)) == SHAPE
+    assert f(1, 128, 1, 64, 64, 16, 2, ctypes.byref(n)) == DTYPE
+    assert f(1, 128, 1, 64, 64, 128, 1, ctypes.byref(n)) == UNSUP
+    assert f(0, 128, 1, 64, 64, 64, 1, ctypes.byref(n)) == OK and n.value == 0
+
+
+def test_forward_validation():
+    f = L.gdn_chunk_forward
+    names = ["Q", "K", "V", "beta", "g", "S0", "O", "Sf", "ws", "wsb", "B", "L", "H", "dk", "dv",
+             "C", "N", "S", "exact", "scale", "dt"]
+    need = 2 * (8192 + 8192 + 8192 + 6 * 512) * 2  # B = 1, L = 128, H = 1, C = 64, bf16
+    base = dict(Q=P1, K=BIG, V=2 * BIG, beta=3 * BIG, g=4 * BIG, S0=None, O=5 * BIG, Sf=None,
+                ws=6 * BIG, wsb=need, B=1, L=128, H=1, dk=128, dv=128, C=64, N=3, S=8, exact=0,
+                scale=1.0, dt=1)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return f(*[a[n] for n in names], None)
+
+    assert call(C=48) == SHAPE
+    assert call(L=100) == SHAPE
+    assert call(dv=32) == SHAPE
+    assert call(N=64) == PARAM
+    assert call(exact=2) == PARAM
+    assert call(dt=2) == DTYPE
+    assert call(C=128) == UNSUP
+    assert call(Q=None) == NULL
+    assert call(ws=None) == NULL
+    assert call(wsb=need - 1) == WS
+    assert call(O=5 * BIG + 4) == ALIGN
+    assert call(S0=7 * BIG + 8) == ALIGN
+    assert call(O=P1 + 256) == ALIAS            # O over Q
+    assert call(ws=BIG + 1024) == ALIAS         # workspace over K
+    assert call(ws=5 * BIG + 4096) == ALIAS     # workspace over O
+    assert call(S0=7 * BIG, Sf=7 * BIG + 1024) == ALIAS  # partial overlap of the states
+    assert call(Sf=4 * BIG) == ALIAS            # S_final over g
+    assert call(B=0) == OK
+    assert call(H=0, Q=None, K=None) == OK
 
 
 def test_binding_rejects_host_tensors():
