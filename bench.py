@@ -1,7 +1,7 @@
 """Benchmark of the chunk-wise Gated DeltaNet inverse path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--C C]
-                    [--path fused|fused_blockwise|inverse|fwdsub|blockwise|unfused|int8]
+                    [--path fused|fused_blockwise|inverse|fwdsub|blockwise|unfused|int8|forward]
                     [--no-cpu-baseline]
 
 A step is one pass of the hot path over one batch of synthetic inputs
@@ -13,6 +13,12 @@ Prints ONE JSON line: throughput in chunk inverses per second, the roofline
 of the dominant kernel (timed with HIP events on the stream it runs on), and
 the CPU oracle timed on a bounded sample of the same workload together with
 the GPU's max abs error against it on that sample.
+
+--path forward runs the whole chunk-wise Gated DeltaNet layer forward
+(gdn_chunk_forward: per-chunk factors, then the state recurrence and the
+output), times its two launches apart and, for context, the inverse alone
+(T_hat and forward substitution) on the same chunks, so the inverse's share
+of the layer can be read off.
 
 --path int8 runs the low-bit path (default workload "int8": B=4, H=32,
 L=16384, C=64, wide gates) in one launch: build A in fp32 -> per-tile INT8
@@ -52,7 +58,9 @@ def parse():
     ap.add_argument("--N", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
     ap.add_argument("--path", default="fused", choices=["fused", "fused_blockwise", "inverse", "fwdsub", "blockwise",
-                             "unfused", "int8"])
+                             "unfused", "int8", "forward"])
+    ap.add_argument("--exact", action="store_true",
+                    help="--path forward: the exact block-wise inverse instead of T_hat(N, S)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=2048,
                     help="tiles of the workload the CPU oracle runs on (whole heads)")
@@ -104,6 +112,9 @@ def main():
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     es = 2 if w.dtype == "bf16" else 4
     n_tiles = w.B * w.H * (w.L // C)
+
+    if a.path == "forward":
+        return bench_forward(a, w, C, N, S, (N0, S0), G, torch)
 
     # ---- inputs, resident in HBM before timing
     want_v = a.path in ("fused", "fused_blockwise", "unfused")
@@ -258,6 +269,145 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, C, N, S, a, (K, beta, g, V), dK, dV, db, dg,
                                              torch, G)
     print(json.dumps(out), flush=True)
+
+
+def _time(fn, steps, stream, torch):
+    """HIP-event time per call (ms) on `stream`, after one untimed call."""
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def bench_forward(a, w, C, N, S, default_order, G, torch):
+    """The layer forward (gdn_chunk_forward) on the workload's sizes."""
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    es = 2 if w.dtype == "bf16" else 4
+    n_tiles = w.B * w.H * (w.L // C)
+    tok = w.B * w.L * w.H
+    Q, K, V, beta, g, S0 = wl.gen_forward_inputs(w, C=C)
+    dev = lambda x, t: torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(t)
+    dQ, dK, dV = dev(Q, dt), dev(K, dt), dev(V, dt)
+    db, dg, dS0 = dev(beta, torch.float32), dev(g, torch.float32), dev(S0, torch.float32)
+    host = (Q, K, V, beta, g, S0) if not a.no_cpu_baseline else None
+    del Q, K, V
+    dO = torch.empty_like(dV)
+    dSf = torch.empty_like(dS0)
+    ws = torch.empty(G.gdn_chunk_forward_workspace(w.B, w.L, w.H, w.dk, w.dv, C, dt),
+                     dtype=torch.uint8, device="cuda")
+    scale = w.dk ** -0.5
+    stream = torch.cuda.current_stream()
+    step = lambda: G.gdn_chunk_forward(dQ, dK, dV, db, dg, C, S0=dS0, N=N, S=S, exact=a.exact,
+                                       scale=scale, O=dO, S_final=dSf, workspace=ws)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(a.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = e0.elapsed_time(e1) / a.steps
+    ms_per_step = wall * 1e3 / a.steps
+    # the two launches apart, and the inverse alone on the same chunks
+    prep_ms = _time(lambda: G.gdn_chunk_forward_prepare(dQ, dK, dV, db, dg, C, ws, N=N, S=S,
+                                                        exact=a.exact), a.steps, stream, torch)
+    state_ms = _time(lambda: G.gdn_chunk_forward_state(dQ, dg, C, ws, w.dv, S0=dS0, scale=scale,
+                                                       O=dO, S_final=dSf), a.steps, stream, torch)
+    del ws
+    dA = G.gdn_build_A(dK, db, dg, C, a_dtype=dt)
+    dT = torch.empty_like(dA)
+    inv_ms = _time(lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT), a.steps, stream, torch)
+    fws_ms = _time(lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT), max(1, a.steps // 4),
+                   stream, torch)
+    del dA, dT
+    # algorithmic bytes per launch (DESIGN.md, measurement section)
+    # workspace: W, U, K^T and the masked Q K^T per chunk, written once, read once
+    ws_b = G.gdn_chunk_forward_workspace(w.B, w.L, w.H, w.dk, w.dv, C, dt)
+    prep_bytes = tok * (2 * w.dk + w.dv) * es + tok * 8 + ws_b
+    state_bytes = ws_b + tok * (w.dk + w.dv) * es + tok * 4 + 2 * w.B * w.H * w.dk * w.dv * 4
+    if state_ms >= prep_ms:
+        kernel, kms, kbytes = "k_fwd_state", state_ms, state_bytes
+    else:
+        kernel, kms, kbytes = "k_fwd_chunk", prep_ms, prep_bytes
+    achieved = kbytes / (kms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(n_tiles / (ms_per_step * 1e-3), 1),
+        "unit": "chunk inverses/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "C": C, "dk": w.dk,
+                   "dv": w.dv, "N": N, "S": S, "tiles": n_tiles, "path": "forward",
+                   "inverse": "exact block-wise" if a.exact else f"T_hat({N},{S})",
+                   "parallelism": "none (1 GPU)"},
+        "tokens_per_s": round(w.B * w.L / (ms_per_step * 1e-3), 1),
+        "layer_ms": round(ev_ms, 6),
+        "prepare_ms": round(prep_ms, 6),
+        "state_ms": round(state_ms, 6),
+        "inverse_alone_ms": round(inv_ms, 6),
+        "fwdsub_alone_ms": round(fws_ms, 6),
+        "inverse_share_of_layer": round(inv_ms / ev_ms, 4),
+        "fwdsub_share_if_swapped_in": round(fws_ms / (ev_ms - inv_ms + fws_ms), 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": kernel, "kernel_ms": round(kms, 6),
+                     "algorithmic_bytes": kbytes},
+    }
+    if host is not None:
+        out["cpu_baseline"] = cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale):
+    """The forward oracle (float64 numpy, chunk-wise form) on whole heads of
+    the same workload, passes repeated until `cpu_seconds` have elapsed, and
+    the GPU's max abs error against it on those heads."""
+    from oracle import gdn, gdn_forward as fwd
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    Q, K, V, beta, g, S0 = host
+    nc = w.L // C
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)][:max(1, a.cpu_sample_tiles // nc)]
+    pick = lambda x: np.stack([x[b, :, h] for b, h in heads], 1)[None].astype(np.float64)
+    Qs, Ks, Vs, bs, gs = (pick(x) for x in (Q, K, V, beta, g))
+    S0s = np.stack([S0[b, h] for b, h in heads], 0)[None].astype(np.float64)
+    inv = (gdn.forward_substitution_inverse if a.exact else
+           (lambda A: gdn.neumann_inverse(A, N, S)))
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        Or, Sr = fwd.gdn_chunked(Qs, Ks, Vs, bs, gs, C, S0s, scale=scale, inverse=inv)
+        passes += 1
+        secs = time.perf_counter() - t0
+        if secs >= a.cpu_seconds:
+            break
+    tiles = len(heads) * nc * passes
+    Og = np.stack([dO[b, :, h].float().cpu().numpy() for b, h in heads], 1)[None]
+    Sg = np.stack([dSf[b, h].float().cpu().numpy() for b, h in heads], 0)[None]
+    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{len(heads)} heads x {nc} chunks of {w.name}, {passes} passes of the "
+                      f"chunk-wise forward in float64 numpy, {secs:.2f} s",
+            "max_abs_err_gpu_vs_oracle": {"O": float(np.max(np.abs(Og - Or))),
+                                          "S_final": float(np.max(np.abs(Sg - Sr)))}}
 
 
 # committed rocprofv3 summaries carrying measured HBM traffic per launch

@@ -208,6 +208,25 @@ int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* 
                       int64_t workspace_bytes, int B, int L, int H, int dk, int dv, int C, int N,
                       int S, int exact, float scale, int dtype, void* stream);
 
+/* gdn_chunk_forward in its two phases, for callers that schedule them apart
+ * (the first has no sequential dependence; the second carries the state).
+ * gdn_chunk_forward_prepare: every chunk in parallel, Q, K, V, beta, g ->
+ * workspace (T of T_hat(N, S) or exact as for gdn_chunk_forward, then the
+ * per-chunk factors).  gdn_chunk_forward_state: the recurrence over the
+ * chunks of each head, workspace (as the prepare call with the same sizes
+ * and dtype left it), Q, g, S0 -> O, S_final.  Run on one stream, prepare
+ * then state equals gdn_chunk_forward bit for bit.  Arguments, layouts and
+ * errors as for gdn_chunk_forward; the prepare call does not read S0 and
+ * writes neither O nor S_final. */
+int gdn_chunk_forward_prepare(const void* Q, const void* K, const void* V, const float* beta,
+                              const float* g, void* workspace, int64_t workspace_bytes, int B,
+                              int L, int H, int dk, int dv, int C, int N, int S, int exact,
+                              int dtype, void* stream);
+int gdn_chunk_forward_state(const void* Q, const float* g, const float* S0, void* O,
+                            float* S_final, const void* workspace, int64_t workspace_bytes, int B,
+                            int L, int H, int dk, int dv, int C, float scale, int dtype,
+                            void* stream);
+
 /* Workspace bytes gdn_chunk_forward needs for these sizes (0 when there is
  * no chunk); GDN_ERR_SHAPE / GDN_ERR_DTYPE / GDN_ERR_NULL as for the call. */
 int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int dtype,

@@ -38,6 +38,10 @@ _SIGS = {
                           _c_int, _vp],
     "gdn_chunk_forward_workspace": [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
                                     ctypes.POINTER(_c_i64)],
+    "gdn_chunk_forward_prepare": [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
+                                  _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_forward_state": [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
+                                _c_int, _c_int, _c_int, ctypes.c_float, _c_int, _vp],
 }
 
 
@@ -337,4 +341,47 @@ def gdn_chunk_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: t
         _dev(O, "O", K.dtype, tok * dv), fp, _dev(workspace, "workspace"), workspace.numel() *
         workspace.element_size(), B, L, H, dk, dv, C, N, S, int(bool(exact)), scale, dt,
         _stream(stream)))
+    return O, S_final
+
+
+def gdn_chunk_forward_prepare(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                              beta: torch.Tensor, g: torch.Tensor, C: int,
+                              workspace: torch.Tensor, N: Optional[int] = None,
+                              S: Optional[int] = None, exact: bool = False, stream=None):
+    """First phase of gdn_chunk_forward: the per-chunk factors into `workspace`."""
+    B, L, H, dk = K.shape
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    if N is None or S is None:
+        dn, ds = gdn_default_order(C) if C in (16, 32, 64, 128) else (0, 0)
+        N = dn if N is None else N
+        S = ds if S is None else S
+    tok = B * L * H
+    _check("gdn_chunk_forward_prepare", lib.gdn_chunk_forward_prepare(
+        _dev(Q, "Q", K.dtype, tok * dk), _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv),
+        _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        B, L, H, dk, dv, C, N, S, int(bool(exact)), dt, _stream(stream)))
+    return workspace
+
+
+def gdn_chunk_forward_state(Q: torch.Tensor, g: torch.Tensor, C: int, workspace: torch.Tensor,
+                            dv: int, S0: Optional[torch.Tensor] = None,
+                            scale: Optional[float] = None, want_state: bool = True,
+                            O: Optional[torch.Tensor] = None,
+                            S_final: Optional[torch.Tensor] = None, stream=None):
+    """Second phase of gdn_chunk_forward: the state pass over a prepared workspace."""
+    B, L, H, dk = Q.shape
+    dt = _fdtype(Q, "Q")
+    scale = dk ** -0.5 if scale is None else float(scale)
+    tok = B * L * H
+    O = torch.empty((B, L, H, dv), dtype=Q.dtype, device=Q.device) if O is None else O
+    if want_state and S_final is None:
+        S_final = torch.empty((B, H, dk, dv), dtype=torch.float32, device=Q.device)
+    sp = _dev(S0, "S0", torch.float32, B * H * dk * dv) if S0 is not None else None
+    fp = _dev(S_final, "S_final", torch.float32, B * H * dk * dv) if S_final is not None else None
+    _check("gdn_chunk_forward_state", lib.gdn_chunk_forward_state(
+        _dev(Q, "Q"), _dev(g, "g", torch.float32, tok), sp, _dev(O, "O", Q.dtype, tok * dv), fp,
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        B, L, H, dk, dv, C, scale, dt, _stream(stream)))
     return O, S_final

@@ -271,29 +271,43 @@ int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int 
   return GDN_OK;
 }
 
-int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* beta,
-                      const float* g, const float* S0, void* O, float* S_final, void* workspace,
-                      int64_t workspace_bytes, int B, int L, int H, int dk, int dv, int C, int N,
-                      int S, int exact, float scale, int dtype, void* stream) {
+namespace {
+// phases: 1 = per-chunk launch only, 2 = state pass only, 3 = both
+int forward(const void* Q, const void* K, const void* V, const float* beta, const float* g,
+            const float* S0, void* O, float* S_final, void* workspace, int64_t workspace_bytes,
+            int B, int L, int H, int dk, int dv, int C, int N, int S, int exact, float scale,
+            int dtype, int phases, void* stream) {
   int64_t n = 0;
   if (int r = check_chunked(B, L, H, C, &n)) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
-  if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if ((phases & 1) && !exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (C == 128) return GDN_ERR_UNSUPPORTED;
   if ((int64_t)B * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
+  if ((int64_t)B * H == 0) return GDN_OK;
+  const bool prep = phases & 1, state = phases & 2;
   const int64_t es = esize(dtype), tok = (int64_t)B * L * H;
   const int64_t need = n * gdn::fwd_workspace_elems(C, dk, dv) * es;
-  const int64_t sb = (int64_t)B * H * dk * dv * 4;
-  if ((int64_t)B * H == 0) return GDN_OK;
-  if (n > 0 && (!Q || !K || !V || !beta || !g || !O || !workspace)) return GDN_ERR_NULL;
-  if (n > 0 && workspace_bytes < need) return GDN_ERR_WORKSPACE;
+  if (n > 0) {
+    if (!Q || !g || !workspace) return GDN_ERR_NULL;
+    if (prep && (!K || !V || !beta)) return GDN_ERR_NULL;
+    if (state && !O) return GDN_ERR_NULL;
+    if (workspace_bytes < need) return GDN_ERR_WORKSPACE;
+  } else if (!state) {
+    return GDN_OK;  // no chunk to prepare
+  }
+  if (!prep) K = V = nullptr, beta = nullptr;
+  if (!state) S0 = nullptr, O = nullptr, S_final = nullptr;
+  if (n == 0) workspace = nullptr, Q = nullptr, g = nullptr, O = nullptr;
   const void* ptrs[9] = {Q, K, V, beta, g, S0, O, S_final, workspace};
   for (const void* p : ptrs)
     if (p && !aligned(p)) return GDN_ERR_ALIGN;
   const int64_t qb = tok * dk * es, vb = tok * dv * es, bb = tok * 4;
-  // inputs (S0 apart) against the outputs and the workspace
+  const int64_t sb = (int64_t)B * H * dk * dv * 4;
+  // every input against every output, and the outputs against each other;
+  // the workspace is an output of the per-chunk launch and an input of the
+  // state pass, and overlaps neither side
   const void* ins[6] = {Q, K, V, beta, g, S0};
   const int64_t inb[6] = {qb, qb, vb, bb, bb, sb};
   const void* outs[3] = {O, workspace, S_final};
@@ -307,8 +321,33 @@ int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* 
       if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return GDN_ERR_ALIAS;
   }
   return hip_status(gdn::launch_forward(Q, K, V, beta, g, S0, O, S_final, workspace, B, L, H, dk,
-                                        dv, C, N, S, exact != 0, scale, dtype,
+                                        dv, C, N, S, exact != 0, scale, dtype, phases,
                                         (hipStream_t)stream));
+}
+}  // namespace
+
+int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* beta,
+                      const float* g, const float* S0, void* O, float* S_final, void* workspace,
+                      int64_t workspace_bytes, int B, int L, int H, int dk, int dv, int C, int N,
+                      int S, int exact, float scale, int dtype, void* stream) {
+  return forward(Q, K, V, beta, g, S0, O, S_final, workspace, workspace_bytes, B, L, H, dk, dv,
+                 C, N, S, exact, scale, dtype, 3, stream);
+}
+
+int gdn_chunk_forward_prepare(const void* Q, const void* K, const void* V, const float* beta,
+                              const float* g, void* workspace, int64_t workspace_bytes, int B,
+                              int L, int H, int dk, int dv, int C, int N, int S, int exact,
+                              int dtype, void* stream) {
+  return forward(Q, K, V, beta, g, nullptr, nullptr, nullptr, workspace, workspace_bytes, B, L,
+                 H, dk, dv, C, N, S, exact, 1.f, dtype, 1, stream);
+}
+
+int gdn_chunk_forward_state(const void* Q, const float* g, const float* S0, void* O,
+                            float* S_final, const void* workspace, int64_t workspace_bytes, int B,
+                            int L, int H, int dk, int dv, int C, float scale, int dtype,
+                            void* stream) {
+  return forward(Q, nullptr, nullptr, nullptr, g, S0, O, S_final, const_cast<void*>(workspace),
+                 workspace_bytes, B, L, H, dk, dv, C, 0, 0, 0, scale, dtype, 2, stream);
 }
 
 }  // extern "C"

@@ -506,14 +506,14 @@ template <int NB, int DK, int DV, typename F, typename TIO>
 static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, const float* beta,
                                  const float* g, const float* S0, void* O, float* Sfin, void* ws,
                                  int B, int L, int H, int N, int S, bool exact, float scale,
-                                 hipStream_t st) {
+                                 int phases, hipStream_t st) {
   constexpr int DN = FwdOrder<NB>::N, DS = FwdOrder<NB>::S;
   const int64_t n = (int64_t)B * H * (L / (16 * NB));
 #define GDN_FWD1(SM, NC_, SC_, EX)                                                           \
   hipLaunchKernelGGL((k_fwd_chunk<NB, DK, DV, F, SM, NC_, SC_, TIO, EX>), dim3((unsigned)n), \
                      dim3(64), 0, st, (const TIO*)Q, (const TIO*)K, (const TIO*)V, beta, g,  \
                      (TIO*)ws, n, L, H, N, S)
-  if (n > 0) {
+  if ((phases & 1) && n > 0) {
     if (exact)
       GDN_FWD1(true, 0, 0, true);
     else if (N == DN && S == DS)
@@ -524,9 +524,11 @@ static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, co
       GDN_FWD1(false, -1, -1, false);
   }
 #undef GDN_FWD1
-  const unsigned nwork = (unsigned)(B * H * (DV / 16));
-  hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO>), dim3(nwork), dim3(128), 0, st,
-                     (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L, H, scale);
+  if (phases & 2) {
+    const unsigned nwork = (unsigned)(B * H * (DV / 16));
+    hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO>), dim3(nwork), dim3(128), 0, st,
+                       (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L, H, scale);
+  }
   return hipGetLastError();
 }
 
@@ -534,11 +536,11 @@ template <typename F, typename TIO>
 static hipError_t run_forward(const void* Q, const void* K, const void* V, const float* beta,
                               const float* g, const float* S0, void* O, float* Sfin, void* ws,
                               int B, int L, int H, int dk, int dv, int C, int N, int S,
-                              bool exact, float scale, hipStream_t st) {
+                              bool exact, float scale, int phases, hipStream_t st) {
 #define GDN_FWD_NB(NB_)                                                                     \
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {                                                     \
     return run_forward_nb<NB_, DK, DV, F, TIO>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, N, \
-                                              S, exact, scale, st);                         \
+                                              S, exact, scale, phases, st);                 \
   }))
   switch (C) {
     case 16: GDN_FWD_NB(1) break;
@@ -552,13 +554,13 @@ static hipError_t run_forward(const void* Q, const void* K, const void* V, const
 hipError_t launch_forward(const void* Q, const void* K, const void* V, const float* beta,
                           const float* g, const float* S0, void* O, float* Sfin, void* ws, int B,
                           int L, int H, int dk, int dv, int C, int N, int S, bool exact,
-                          float scale, int dtype, hipStream_t st) {
+                          float scale, int dtype, int phases, hipStream_t st) {
   if (dtype == 0)
     return run_forward<f32x4, float>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S,
-                                     exact, scale, st);
+                                     exact, scale, phases, st);
   if (dtype == 1)
     return run_forward<bf16x4, __bf16>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N,
-                                       S, exact, scale, st);
+                                       S, exact, scale, phases, st);
   return hipErrorNotSupported;
 }
 

@@ -35,12 +35,14 @@ hipError_t launch_wy(const void* T, const void* K, const void* V, const float* b
 hipError_t launch_fused(const void* K, const void* V, const float* beta, const float* g, void* W,
                         void* U, void* T, int B, int L, int H, int dk, int dv, int C, int N,
                         int S, int dtype, bool exact, hipStream_t st);
-// chunk-wise Gated DeltaNet forward (two launches); ws holds
-// fwd_workspace_elems(C, dk, dv) elements of the IO type per chunk tile
+// chunk-wise Gated DeltaNet forward; ws holds fwd_workspace_elems(C, dk, dv)
+// elements of the IO type per chunk tile.  phases: bit 0 the per-chunk
+// launch (Q, K, V, beta, g -> ws), bit 1 the state pass (ws, Q, g, S0 -> O,
+// S_final)
 hipError_t launch_forward(const void* Q, const void* K, const void* V, const float* beta,
                           const float* g, const float* S0, void* O, float* Sfin, void* ws, int B,
                           int L, int H, int dk, int dv, int C, int N, int S, bool exact,
-                          float scale, int dtype, hipStream_t st);
+                          float scale, int dtype, int phases, hipStream_t st);
 int64_t fwd_workspace_elems(int C, int dk, int dv);
 hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                               hipStream_t st);

@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 15
+    assert len(names) == 17
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -244,6 +244,36 @@ def test_forward_validation():
     assert call(Sf=4 * BIG) == ALIAS            # S_final over g
     assert call(B=0) == OK
     assert call(H=0, Q=None, K=None) == OK
+
+
+def test_forward_phase_validation():
+    need = 2 * (8192 + 8192 + 8192 + 6 * 512) * 2  # B = 1, L = 128, H = 1, C = 64, bf16
+    p = L.gdn_chunk_forward_prepare
+    # Q, K, V, beta, g, ws, wsb, B, L, H, dk, dv, C, N, S, exact, dt
+    pb = [P1, BIG, 2 * BIG, 3 * BIG, 4 * BIG, 6 * BIG, need, 1, 128, 1, 128, 128, 64, 3, 8, 0, 1]
+    bad = list(pb); bad[13] = 70
+    assert p(*bad, None) == PARAM
+    bad = list(pb); bad[2] = None
+    assert p(*bad, None) == NULL
+    bad = list(pb); bad[6] = need - 2
+    assert p(*bad, None) == WS
+    bad = list(pb); bad[5] = 2 * BIG + 64  # workspace over V
+    assert p(*bad, None) == ALIAS
+    bad = list(pb); bad[8] = 0  # no chunk: nothing to prepare
+    assert p(*bad, None) == OK
+    s = L.gdn_chunk_forward_state
+    # Q, g, S0, O, S_final, ws, wsb, B, L, H, dk, dv, C, scale, dt
+    sb = [P1, 4 * BIG, None, 5 * BIG, None, 6 * BIG, need, 1, 128, 1, 128, 128, 64, 1.0, 1]
+    bad = list(sb); bad[3] = None
+    assert s(*bad, None) == NULL
+    bad = list(sb); bad[3] = 6 * BIG + 4096  # O over the workspace
+    assert s(*bad, None) == ALIAS
+    bad = list(sb); bad[6] = 16
+    assert s(*bad, None) == WS
+    bad = list(sb); bad[12] = 128
+    assert s(*bad, None) == UNSUP
+    bad = list(sb); bad[7] = 0
+    assert s(*bad, None) == OK
 
 
 def test_binding_rejects_host_tensors():

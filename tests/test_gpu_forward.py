@@ -241,3 +241,16 @@ def test_forward_binding_and_workspace_checks():
     with pytest.raises(G.GdnError) as e:  # C = 128 is not built for the forward
         G.gdn_chunk_forward(dev(Q, dt), dev(K, dt), dev(V, dt), dev32(beta), dev32(g), 128)
     assert e.value.code == -8
+
+
+@pytest.mark.parametrize("C", [16, 64])
+def test_forward_two_phases_equal_one_call(C):
+    dt = "bf16"
+    Q, K, V, beta, g, S0 = layer_inputs(C, dt, B=2, L=3 * C, H=4, seed=12)
+    O, Sf = run_gpu(Q, K, V, beta, g, S0, C, dt, scale=0.3)
+    q, k, v, b, gg = dev(Q, dt), dev(K, dt), dev(V, dt), dev32(beta), dev32(g)
+    need = G.gdn_chunk_forward_workspace(2, 3 * C, 4, 128, 128, C, torch.bfloat16)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    G.gdn_chunk_forward_prepare(q, k, v, b, gg, C, ws)
+    O2, S2 = G.gdn_chunk_forward_state(q, gg, C, ws, 128, S0=dev32(S0), scale=0.3)
+    assert np.array_equal(host(O2), O) and np.array_equal(host(S2), Sf)
