@@ -365,7 +365,9 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
         "fwdsub_share_if_swapped_in": round(fws_ms / (ev_ms - inv_ms + fws_ms), 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": kernel, "kernel_ms": round(kms, 6),
+                     "traffic": (measured_traffic("forward", w.name, C, N, S, default_order)
+                                 if kernel == "k_fwd_state" and not a.exact else None),
+                     "kernel": kernel, "kernel_ms": round(kms, 6),
                      "algorithmic_bytes": kbytes},
     }
     if host is not None:
@@ -414,7 +416,8 @@ def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale):
 PROFILES = {("fused", "qwen35_prefill", 64): ("k_fused_qwen35_prefill.md", "pipeline.hip"),
             ("fused", "long_context", 64): ("k_fused_long_context.md", "pipeline.hip"),
             ("inverse", "sweep", 64): ("k_neumann_sweep_c64.md", "neumann.hip"),
-            ("int8", "int8", 64): ("k_inverse_i8_fused_int8.md", "int8.hip")}
+            ("int8", "int8", 64): ("k_inverse_i8_fused_int8.md", "int8.hip"),
+            ("forward", "qwen35_prefill", 64): ("k_fwd_state_qwen35_prefill.md", "forward.hip")}
 
 
 def measured_traffic(path, workload, C, N, S, default_order):

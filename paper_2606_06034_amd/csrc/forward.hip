@@ -16,10 +16,10 @@
 // stores them in the workspace in exactly the register-fragment layouts
 // stage 2 feeds to its MFMAs, so stage 2 reads each operand with one 16-byte
 // load per lane from a contiguous 1 KB run per wave and changes no layout.
-// Stage 2, k_fwd_state: one wave per (batch, head, 16 value columns).  It
-// walks the chunks of its head in order with its dk x 16 slice of S in
-// registers (fp32); per chunk four product groups: W S, Q S, P V_new and
-// K^T V_new.
+// Stage 2, k_fwd_state: one workgroup per (batch, head, 16 value columns).
+// It walks the chunks of its head in order with its dk x 16 slice of S in
+// registers (fp32), spread over four waves; per chunk four product groups:
+// W S, Q S, P V_new and K^T V_new.
 //
 // Fragment conventions (tile16.hpp): a pair over 16-blocks {2p, 2p + 1}
 // gives slot s of lane (g, c) the index 32p + 16 (s / 4) + 4g + s % 4; a
@@ -275,54 +275,59 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
 // ---------------------------------------------------------------------------
 // stage 2
 //
-// Two waves per (batch, head, slice): wave 1 copies the operands of the next
-// chunk from the workspace (and Q, g from the inputs) into LDS by global ->
-// LDS DMA while wave 0 runs the recurrence on the current chunk from LDS.
-// NST = 2 stages: the copy of chunk ck + 1 overlaps the compute of chunk ck,
-// one workgroup barrier per chunk; NST = 1 (fp32 at C = 64, where a stage
-// would not fit twice): copy, barrier, compute, barrier.
+// One workgroup of four waves per (batch, head, slice of 16 value columns),
+// one wave per SIMD.  The chunk's work is split so that no wave reads more
+// than a quarter of the chunk's operands:
+//   wave w owns the state pair q = w (its 2 x 16 state rows) and updates it
+//     with K^T rows of those state blocks;
+//   wave w forms V_new and O for the row block I = w of the chunk.
+// Two small LDS exchanges per chunk connect them: every wave publishes its
+// state pair (bf16) before W S and Q S, and its V_new rows (bf16, plain and
+// decayed to the chunk end) before P V_new and the state update.  Each
+// wave's operands (W, Q, K^T, P rows, U block, gates) come straight from
+// global memory into registers, issued DEPTH - 1 chunks ahead into a ring
+// of register buffers, so the loads of a chunk overlap the compute of the
+// chunks before it.
 
-template <int NB, int DK, int DV, typename TIO>
-struct StageLayout {
-  static constexpr int NQ = DK / 32;
-  static constexpr int W = 0;                                   // NB * NQ slots
-  static constexpr int Q = W + NB * NQ * 512;                   // NB * NQ slots
-  static constexpr int KT = Q + NB * NQ * 512;                  // (DK/16) * npair slots
-  static constexpr int P = KT + (DK / 16) * npair(NB) * 512;   // npp slots
-  static constexpr int U = P + npp(NB) * 512;                   // NB blocks of this slice
-  static constexpr int size = U + NB * 256;                     // elements of TIO
-  static constexpr int bytes = size * (int)sizeof(TIO);
-  static constexpr int nst = 2 * bytes + 1024 <= 150 * 1024 ? 2 : 1;
+template <int NB, int DK, typename F>
+struct FwdOps {  // one wave's operands of one chunk
+  static constexpr int NQ = DK / 32, NP = npair(NB);
+  Pair<F> w[NQ];      // W row pairs (I, q)
+  Pair<F> q[NQ];      // Q row pairs (I, q)
+  Pair<F> kt[2][NP];  // K^T pairs of the owned state blocks
+  Pair<F> p[2];       // P row pairs (I, p), p <= I / 2
+  f32x4 u;            // U block (slice, I), column form
+  float gr, gl;       // gamma of row 16 I + c, gamma of the chunk's last row
+  f32x4 gv;           // gamma of rows 16 I + 4 g + v
 };
 
-// wave-wide copy of `bytes` contiguous bytes (a multiple of 16) to LDS in
-// runs of 1 KB, 16 bytes per lane
-__device__ __forceinline__ void dma_copy(const void* src, void* dst, int bytes, int l) {
-  const char* s = (const char*)src;
-  char* d = (char*)dst;
-  for (int o = 0; o < bytes; o += 1024)
-    if (o + 16 * l < bytes)
-      __builtin_amdgcn_global_load_lds((glb_void*)(s + o + 16 * l), (lds_void*)(d + o), 16, 0, 0);
+// half `hf` (block 2p + hf) of slot p
+__device__ __forceinline__ void slot_store_half(__bf16* s, f32x4 x, int hf, int l) {
+  *(bf16x4*)(s + 8 * l + 4 * hf) = __builtin_convertvector(x, bf16x4);
+}
+__device__ __forceinline__ void slot_store_half(float* s, f32x4 x, int hf, int l) {
+  *(f32x4*)(s + 256 * hf + 4 * l) = x;
 }
 
-template <int NB, int DK, int DV, typename F, typename TIO>
-__global__ __launch_bounds__(128) void k_fwd_state(const TIO* __restrict__ ws,
+template <int NB, int DK, int DV, typename F, typename TIO, int DEPTH>
+__global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
                                                    const TIO* __restrict__ Q,
                                                    const float* __restrict__ g,
                                                    const float* __restrict__ S0,
                                                    TIO* __restrict__ O, float* __restrict__ Sfin,
                                                    int64_t n_tiles, int B, int L, int H,
                                                    float scale) {
-  constexpr int C = 16 * NB, NQ = DK / 32, NM = DK / 16, NP = npair(NB), NS = DV / 16;
+  constexpr int C = 16 * NB, NQ = DK / 32, NP = npair(NB), NS = DV / 16;
+  // DEPTH: chunks whose operands are in registers at once (a ring of
+  // buffers, loads issued DEPTH - 1 chunks ahead)
   using LY = FwdLayout<NB, DK, DV>;
-  using SL = StageLayout<NB, DK, DV, TIO>;
-  constexpr int NST = SL::nst;
-  __shared__ __attribute__((aligned(16))) TIO stg[NST][SL::size];
-  __shared__ __attribute__((aligned(16))) float sgam[NST][C];
+  using Ops = FwdOps<NB, DK, F>;
+  __shared__ __attribute__((aligned(16))) TIO xs[2][NQ * 512];      // state pairs
+  __shared__ __attribute__((aligned(16))) TIO xv[2][2 * NP * 512];  // V_new, V_d pairs
   const int BH = B * H, nc = L / C;
   // work item -> (head bh = b H + h, slice j); when BH is a multiple of 8 the
   // slices of one head share an XCD (work items are dealt to the 8 XCDs in
-  // turn), so the W, K^T, P and Q runs all of them read meet in one L2
+  // turn), so the rows of W, K^T, P and Q all of them read meet in one L2
   const uint32_t x = blockIdx.x;
   int bh, j;
   if (BH % 8 == 0) {
@@ -336,166 +341,189 @@ __global__ __launch_bounds__(128) void k_fwd_state(const TIO* __restrict__ ws,
   const int b = bh / H, h = bh - b * H;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
-  const int l = ln.id;
-  const int64_t ldq = (int64_t)H * DK, ldo = (int64_t)H * DV;
-
-  if (wv == 1) {
-    // ---- producer
-    auto copy = [&](int ck, int st) {
-      const int64_t tile = (int64_t)bh * nc + ck;
-      const int64_t tok0 = (int64_t)b * L + ck * C;
-      TIO* s = stg[st];
-      dma_copy(ws + tile * LY::W, s + SL::W, (int)(LY::W * sizeof(TIO)), l);
-      dma_copy(ws + n_tiles * LY::W + tile * LY::U + j * NB * 256, s + SL::U,
-               NB * 256 * (int)sizeof(TIO), l);
-      dma_copy(ws + n_tiles * (LY::W + LY::U) + tile * LY::KT, s + SL::KT,
-               (int)(LY::KT * sizeof(TIO)), l);
-      dma_copy(ws + n_tiles * (LY::W + LY::U + LY::KT) + tile * LY::P, s + SL::P,
-               (int)(LY::P * sizeof(TIO)), l);
-      // Q rows gathered into slots (I, q); fp32 as two 16-byte halves
-#pragma unroll
-      for (int I = 0; I < NB; ++I)
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-          const TIO* src = Q + (tok0 + I * 16 + ln.c()) * ldq + (int64_t)h * DK + 32 * q + 8 * ln.g();
-          TIO* dst = s + SL::Q + (I * NQ + q) * 512;
-#pragma unroll
-          for (int p = 0; p < (int)sizeof(TIO) / 2; ++p)
-            __builtin_amdgcn_global_load_lds((glb_void*)(src + p * (16 / sizeof(TIO))),
-                                             (lds_void*)(dst + p * 256), 16, 0, 0);
-        }
-      if (l < C)
-        __builtin_amdgcn_global_load_lds((glb_void*)(g + (tok0 + l) * H + h),
-                                         (lds_void*)sgam[st], 4, 0, 0);
-    };
-    if (NST == 2 && nc > 0) copy(0, 0);
-    for (int ck = 0; ck < nc; ++ck) {
-      if (NST == 1) copy(ck, 0);
-      wait_vmem();  // chunk ck has landed
-      __syncthreads();
-      if (NST == 2) {
-        // the stage of chunk ck - 1 is free: wave 0 has passed this barrier
-        if (ck + 1 < nc) copy(ck + 1, (ck + 1) & 1);
-      } else {
-        __syncthreads();  // wave 0 is done with the stage
-      }
-    }
-    return;
-  }
-
-  // ---- consumer: the recurrence
-  const int gq = ln.g(), c = ln.c();
+  const int l = ln.id, gq = ln.g(), c = ln.c();
+  // roles of this wave (uniform; every wave has both at C = 64, dk = 128)
+  const bool rows = NB >= 4 || wv < NB, owner = NQ >= 4 || wv < NQ;
   const int jq = j >> 1, jh = j & 1;
   const int dvcol = 32 * jq + 8 * (c >> 2) + 4 * jh + (c & 3);  // column c of the slice
   const int ocol = 32 * jq + 8 * gq + 4 * jh;                   // columns 4g .. 4g + 3
   const int64_t sbase = (int64_t)bh * DK * DV;
-  f32x4 st[NM];
+  const int64_t ldq = (int64_t)H * DK, ldo = (int64_t)H * DV;
+  const TIO* wsW = ws;
+  const TIO* wsU = ws + n_tiles * LY::W;
+  const TIO* wsKT = wsU + n_tiles * LY::U;
+  const TIO* wsP = wsKT + n_tiles * LY::KT;
+
+  // the owned state blocks m = 2 wv, 2 wv + 1: rows dk = 32 wv + 8g + 4 hf + v
+  f32x4 st[2] = {zero4(), zero4()};
+  if (owner && S0) {
 #pragma unroll
-  for (int m = 0; m < NM; ++m)
+    for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int dk = 32 * (m >> 1) + 8 * gq + 4 * (m & 1) + v;
-      st[m][v] = S0 ? S0[sbase + (int64_t)dk * DV + dvcol] : 0.f;
-    }
-  // Per chunk four phases; each issues the LDS reads of the next phase's
-  // operands before its own MFMAs (sched_barrier keeps the order), so the
-  // reads of a phase arrive while the previous phase computes.
-  for (int ck = 0; ck < nc; ++ck) {
-    __syncthreads();  // chunk ck is in stage ck % NST
-    const TIO* s = stg[NST == 2 ? (ck & 1) : 0];
-    const float* gg = sgam[NST == 2 ? (ck & 1) : 0];
-    const int64_t tok0 = (int64_t)b * L + ck * C;
-    // phase 0: W and U reads; the state as MFMA operands
-    Pair<F> wq[NB][NQ];
-    f32x4 vn[NB];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) {
-      vn[I] = load4(s + SL::U + I * 256 + 4 * l);
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) wq[I][q] = slot_load<F>(s + SL::W + (I * NQ + q) * 512, l);
-    }
-    Pair<F> sp[NQ], nsp[NQ];
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      sp[q] = Pair<F>::make(st[2 * q], st[2 * q + 1]);
-      nsp[q] = Pair<F>::make(-st[2 * q], -st[2 * q + 1]);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    // phase 1: Q reads; V_new = U - W S (column form)
-    Pair<F> qq[NB][NQ];
-#pragma unroll
-    for (int I = 0; I < NB; ++I)
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) qq[I][q] = slot_load<F>(s + SL::Q + (I * NQ + q) * 512, l);
-#pragma unroll
-    for (int q = 0; q < NQ; ++q)
-#pragma unroll
-      for (int I = 0; I < NB; ++I) vn[I] = Pair<F>::template mma<false>(wq[I][q], nsp[q], vn[I]);
-    __builtin_amdgcn_sched_barrier(0);
-    // phase 2: K^T and P reads; O = e^gamma Q S (row form), from the state
-    // entering the chunk
-    Pair<F> kt[NM][NP], pp[npp(NB)];
-#pragma unroll
-    for (int m = 0; m < NM; ++m)
-#pragma unroll
-      for (int p = 0; p < NP; ++p) kt[m][p] = slot_load<F>(s + SL::KT + (m * NP + p) * 512, l);
-#pragma unroll
-    for (int k = 0; k < npp(NB); ++k) pp[k] = slot_load<F>(s + SL::P + k * 512, l);
-    const float glast = gg[C - 1];
-    f32x4 o[NB];
-#pragma unroll
-    for (int I = 0; I < NB; ++I) o[I] = zero4();
-#pragma unroll
-    for (int q = 0; q < NQ; ++q)
-#pragma unroll
-      for (int I = 0; I < NB; ++I) o[I] = Pair<F>::template mma<true>(qq[I][q], sp[q], o[I]);
-    __builtin_amdgcn_sched_barrier(0);
-    // phase 3: V_new as operands, decayed to the chunk end for the state
-    // update; O += P V_new; S = e^{gamma_last} S + K^T V_d
-    Pair<F> vp[NP], vdp[NP];
-    {
-      f32x4 vd[NB];
-#pragma unroll
-      for (int I = 0; I < NB; ++I)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) vd[I][v] = vn[I][v] * __expf(glast - gg[I * 16 + 4 * gq + v]);
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        vp[p] = Pair<F>::make(vn[2 * p], 2 * p + 1 < NB ? vn[2 * p + 1] : zero4());
-        vdp[p] = Pair<F>::make(vd[2 * p], 2 * p + 1 < NB ? vd[2 * p + 1] : zero4());
-      }
-    }
-    const float el = __expf(glast);
-#pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      f32x4 acc = el * st[m];
-#pragma unroll
-      for (int p = 0; p < NP; ++p) acc = Pair<F>::template mma<false>(kt[m][p], vdp[p], acc);
-      st[m] = acc;
-    }
-#pragma unroll
-    for (int I = 0; I < NB; ++I) {
-      o[I] *= __expf(gg[I * 16 + c]);
-#pragma unroll
-      for (int p = 0; 2 * p <= I; ++p)
-        o[I] = Pair<F>::template mma<true>(pp[pidx(I, p)], vp[p], o[I]);
-      store4(O + (tok0 + I * 16 + c) * ldo + (int64_t)h * DV + ocol, scale * o[I]);
-    }
-    if (NST == 1) __syncthreads();  // the stage may be refilled
+      for (int v = 0; v < 4; ++v)
+        st[hf][v] = S0[sbase + (int64_t)(32 * wv + 8 * gq + 4 * hf + v) * DV + dvcol];
   }
-  if (Sfin) {
+  wait_vmem();  // the initial state is in registers before the loop starts
+  if (NB == 1) {  // block 1 of the V_new pair does not exist: zero halves
 #pragma unroll
-    for (int m = 0; m < NM; ++m)
+    for (int k = 0; k < 2; ++k)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int dk = 32 * (m >> 1) + 8 * gq + 4 * (m & 1) + v;
-        Sfin[sbase + (int64_t)dk * DV + dvcol] = st[m][v];
+      for (int i = 0; i < 2; ++i) slot_store_half(xv[k] + i * NP * 512, zero4(), 1, l);
+  }
+
+  auto load = [&](Ops& op, int ck) {
+    const int64_t tile = (int64_t)bh * nc + ck;
+    const int64_t tok0 = (int64_t)b * L + ck * C;
+    if (rows) {
+      const int I = wv;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        op.w[q] = slot_load<F>(wsW + tile * LY::W + (I * NQ + q) * 512, l);
+        op.q[q] = load_row8<F>(Q + (tok0 + I * 16 + c) * ldq + (int64_t)h * DK + 32 * q + 8 * gq);
       }
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+        if (2 * p <= I) op.p[p] = slot_load<F>(wsP + tile * LY::P + pidx(I, p) * 512, l);
+      op.u = load4(wsU + tile * LY::U + (j * NB + I) * 256 + 4 * l);
+      const float* gg = g + tok0 * H + h;
+      op.gr = gg[(I * 16 + c) * H];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) op.gv[v] = gg[(I * 16 + 4 * gq + v) * H];
+      op.gl = gg[(C - 1) * H];
+    }
+    if (owner) {
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+          op.kt[hf][p] = slot_load<F>(wsKT + tile * LY::KT + ((2 * wv + hf) * NP + p) * 512, l);
+      if (!rows) op.gl = g[(tok0 + C - 1) * H + h];
+    }
+  };
+
+  auto compute = [&](const Ops& op, int ck) {
+    const int par = ck & 1;
+    const int64_t tok0 = (int64_t)b * L + ck * C;
+    if (owner) slot_store(xs[par] + wv * 512, Pair<F>::make(st[0], st[1]), l);
+    __syncthreads();  // state pairs published
+    f32x4 o = zero4();
+    if (rows) {
+      const int I = wv;
+      Pair<F> sp[NQ];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) sp[q] = slot_load<F>(xs[par] + q * 512, l);
+      f32x4 wsum = zero4();
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        wsum = Pair<F>::template mma<false>(op.w[q], sp[q], wsum);
+        o = Pair<F>::template mma<true>(op.q[q], sp[q], o);
+      }
+      const f32x4 vn = op.u - wsum;  // V_new rows 16 I + 4g + v, column form
+      f32x4 vd;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) vd[v] = vn[v] * __expf(op.gl - op.gv[v]);
+      slot_store_half(xv[par] + (I >> 1) * 512, vn, I & 1, l);
+      slot_store_half(xv[par] + (NP + (I >> 1)) * 512, vd, I & 1, l);
+    }
+    __syncthreads();  // V_new published
+    if (owner) {
+      const float el = __expf(op.gl);
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        f32x4 acc = el * st[hf];
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+          acc = Pair<F>::template mma<false>(op.kt[hf][p],
+                                             slot_load<F>(xv[par] + (NP + p) * 512, l), acc);
+        st[hf] = acc;
+      }
+    }
+    if (rows) {
+      const int I = wv;
+      o *= __expf(op.gr);
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+        if (2 * p <= I)
+          o = Pair<F>::template mma<true>(op.p[p], slot_load<F>(xv[par] + p * 512, l), o);
+      store4(O + (tok0 + I * 16 + c) * ldo + (int64_t)h * DV + ocol, scale * o);
+    }
+  };
+
+  if constexpr (DEPTH == 3) {
+    // ring r0, r1, r2; the chunk index of a load is clamped to the last
+    // chunk (a repeated load past the end is harmless), which keeps the
+    // loads free of branches
+    const int last = nc - 1;
+    Ops r0, r1, r2;
+    if (nc > 0) {
+      load(r0, 0);
+      load(r1, min(1, last));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    for (int ck = 0; ck < nc; ck += 3) {
+      load(r2, min(ck + 2, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(r0, ck);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ck + 1 >= nc) break;
+      load(r0, min(ck + 3, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(r1, ck + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ck + 2 >= nc) break;
+      load(r1, min(ck + 4, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(r2, ck + 2);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else if constexpr (DEPTH == 2) {
+    const int last = nc - 1;
+    Ops r0, r1;
+    if (nc > 0) load(r0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int ck = 0; ck < nc; ck += 2) {
+      load(r1, min(ck + 1, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(r0, ck);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ck + 1 >= nc) break;
+      load(r0, min(ck + 2, last));
+      __builtin_amdgcn_sched_barrier(0);
+      compute(r1, ck + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    for (int ck = 0; ck < nc; ++ck) {
+      Ops r;
+      load(r, ck);
+      compute(r, ck);
+    }
+  }
+  if (owner && Sfin) {
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        Sfin[sbase + (int64_t)(32 * wv + 8 * gq + 4 * hf + v) * DV + dvcol] = st[hf][v];
   }
 }
 
 // ---------------------------------------------------------------------------
 // launchers
+
+// compute units of the current device (cached per device)
+static int compute_units() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
 
 template <int NB> struct FwdOrder;
 template <> struct FwdOrder<1> { static constexpr int N = 3, S = 2; };
@@ -526,8 +554,17 @@ static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, co
 #undef GDN_FWD1
   if (phases & 2) {
     const unsigned nwork = (unsigned)(B * H * (DV / 16));
-    hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO>), dim3(nwork), dim3(128), 0, st,
-                       (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L, H, scale);
+#define GDN_FWD2(D)                                                                        \
+  hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO, D>), dim3(nwork), dim3(256), 0, st, \
+                     (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L, H, scale)
+    if constexpr (sizeof(TIO) != 2) {
+      GDN_FWD2(1);  // fp32 operands: twice the registers, no room for a ring
+    } else if (nwork <= (unsigned)compute_units()) {
+      GDN_FWD2(3);  // one workgroup per CU: the deepest ring
+    } else {
+      GDN_FWD2(2);  // more workgroups than CUs: a ring of two leaves room for two per CU
+    }
+#undef GDN_FWD2
   }
   return hipGetLastError();
 }
