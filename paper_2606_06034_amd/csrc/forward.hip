@@ -31,6 +31,8 @@
 //   dk = 32 q' + 8 g + 4 h' + v,
 // so that the pair (block 2q', block 2q' + 1) lines up with a run of 8
 // features of W and Q rows.
+#include <type_traits>
+
 #include "launch.hpp"
 #include "wy.hpp"
 
@@ -47,10 +49,9 @@ __host__ __device__ constexpr int npp(int NB) {
   for (int I = 0; I < NB; ++I) n += I / 2 + 1;
   return n;
 }
+// sum over i < I of (i / 2 + 1), in closed form (I may be a runtime value)
 __host__ __device__ constexpr int pidx(int I, int p) {
-  int n = 0;
-  for (int i = 0; i < I; ++i) n += i / 2 + 1;
-  return n + p;
+  return I + (I / 2) * ((I - 1) / 2) + p;
 }
 template <int NB, int DK, int DV>
 struct FwdLayout {
@@ -297,8 +298,7 @@ struct FwdOps {  // one wave's operands of one chunk
   Pair<F> kt[2][NP];  // K^T pairs of the owned state blocks
   Pair<F> p[2];       // P row pairs (I, p), p <= I / 2
   f32x4 u;            // U block (slice, I), column form
-  float gr, gl;       // gamma of row 16 I + c, gamma of the chunk's last row
-  f32x4 gv;           // gamma of rows 16 I + 4 g + v
+  float gam;          // gamma of chunk row `lane` (lanes >= C: of row C - 1)
 };
 
 // half `hf` (block 2p + hf) of slot p
@@ -371,42 +371,60 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
       for (int i = 0; i < 2; ++i) slot_store_half(xv[k] + i * NP * 512, zero4(), 1, l);
   }
 
-  auto load = [&](Ops& op, int ck) {
+  // loads of one chunk's operands in three parts (issued at three points of
+  // a step, so no wave stalls on a long burst of loads)
+  auto load_part = [&](Ops& op, int ck, int part) {
     const int64_t tile = (int64_t)bh * nc + ck;
     const int64_t tok0 = (int64_t)b * L + ck * C;
-    if (rows) {
+    if (part == 0 && rows) {
       const int I = wv;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         op.w[q] = slot_load<F>(wsW + tile * LY::W + (I * NQ + q) * 512, l);
         op.q[q] = load_row8<F>(Q + (tok0 + I * 16 + c) * ldq + (int64_t)h * DK + 32 * q + 8 * gq);
       }
-#pragma unroll
-      for (int p = 0; p < 2; ++p)
-        if (2 * p <= I) op.p[p] = slot_load<F>(wsP + tile * LY::P + pidx(I, p) * 512, l);
-      op.u = load4(wsU + tile * LY::U + (j * NB + I) * 256 + 4 * l);
-      const float* gg = g + tok0 * H + h;
-      op.gr = gg[(I * 16 + c) * H];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) op.gv[v] = gg[(I * 16 + 4 * gq + v) * H];
-      op.gl = gg[(C - 1) * H];
     }
-    if (owner) {
+    if (part == 1 && owner) {
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
         for (int p = 0; p < NP; ++p)
           op.kt[hf][p] = slot_load<F>(wsKT + tile * LY::KT + ((2 * wv + hf) * NP + p) * 512, l);
-      if (!rows) op.gl = g[(tok0 + C - 1) * H + h];
+    }
+    if (part == 2) {
+      if (rows) {
+        const int I = wv;
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+          if (2 * p <= I) op.p[p] = slot_load<F>(wsP + tile * LY::P + pidx(I, p) * 512, l);
+        op.u = load4(wsU + tile * LY::U + (j * NB + I) * 256 + 4 * l);
+      }
+      // the chunk's gates in one load, one row per lane; lanes take the
+      // rows they need from each other (ds_bpermute)
+      op.gam = g[(tok0 + min(l, C - 1)) * H + h];
     }
   };
+  auto load = [&](Ops& op, int ck) {
+    load_part(op, ck, 0);
+    load_part(op, ck, 1);
+    load_part(op, ck, 2);
+  };
 
-  auto compute = [&](const Ops& op, int ck) {
+  // one chunk; `nx`, chunk `cknx`: the buffer refilled meanwhile (a
+  // compile-time flag, so the loads carry no branches that would blur the
+  // compiler's count of loads in flight)
+  auto compute = [&](const Ops& op, int ck, Ops& nx, int cknx, auto refill_tag) {
+    constexpr bool refill = decltype(refill_tag)::value;
     const int par = ck & 1;
     const int64_t tok0 = (int64_t)b * L + ck * C;
     if (owner) slot_store(xs[par] + wv * 512, Pair<F>::make(st[0], st[1]), l);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (refill) load_part(nx, cknx, 0);
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();  // state pairs published
     f32x4 o = zero4();
+    const float gl = __builtin_bit_cast(
+        float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, op.gam), C - 1));
     if (rows) {
       const int I = wv;
       Pair<F> sp[NQ];
@@ -421,13 +439,16 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
       const f32x4 vn = op.u - wsum;  // V_new rows 16 I + 4g + v, column form
       f32x4 vd;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) vd[v] = vn[v] * __expf(op.gl - op.gv[v]);
+      for (int v = 0; v < 4; ++v) vd[v] = vn[v] * __expf(gl - __shfl(op.gam, I * 16 + 4 * gq + v));
       slot_store_half(xv[par] + (I >> 1) * 512, vn, I & 1, l);
       slot_store_half(xv[par] + (NP + (I >> 1)) * 512, vd, I & 1, l);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (refill) load_part(nx, cknx, 1);
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();  // V_new published
     if (owner) {
-      const float el = __expf(op.gl);
+      const float el = __expf(gl);
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         f32x4 acc = el * st[hf];
@@ -440,63 +461,54 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
     }
     if (rows) {
       const int I = wv;
-      o *= __expf(op.gr);
+      o *= __expf(__shfl(op.gam, I * 16 + c));
 #pragma unroll
       for (int p = 0; p < 2; ++p)
         if (2 * p <= I)
           o = Pair<F>::template mma<true>(op.p[p], slot_load<F>(xv[par] + p * 512, l), o);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (refill) load_part(nx, cknx, 2);
+      __builtin_amdgcn_sched_barrier(0);
       store4(O + (tok0 + I * 16 + c) * ldo + (int64_t)h * DV + ocol, scale * o);
+    } else if constexpr (refill) {
+      load_part(nx, cknx, 2);
     }
   };
+  using Refill = std::integral_constant<bool, true>;
+  using NoRefill = std::integral_constant<bool, false>;
 
   if constexpr (DEPTH == 3) {
-    // ring r0, r1, r2; the chunk index of a load is clamped to the last
-    // chunk (a repeated load past the end is harmless), which keeps the
-    // loads free of branches
+    // ring r0, r1, r2: while chunk ck computes from one buffer, the buffer
+    // freed by chunk ck - 1 is refilled with chunk ck + 2.  Chunk indices
+    // of loads are clamped to the last chunk (a repeated load past the end
+    // is harmless), which keeps the loads free of branches
     const int last = nc - 1;
     Ops r0, r1, r2;
     if (nc > 0) {
       load(r0, 0);
       load(r1, min(1, last));
     }
-    __builtin_amdgcn_sched_barrier(0);
     for (int ck = 0; ck < nc; ck += 3) {
-      load(r2, min(ck + 2, last));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(r0, ck);
-      __builtin_amdgcn_sched_barrier(0);
+      compute(r0, ck, r2, min(ck + 2, last), Refill{});
       if (ck + 1 >= nc) break;
-      load(r0, min(ck + 3, last));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(r1, ck + 1);
-      __builtin_amdgcn_sched_barrier(0);
+      compute(r1, ck + 1, r0, min(ck + 3, last), Refill{});
       if (ck + 2 >= nc) break;
-      load(r1, min(ck + 4, last));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(r2, ck + 2);
-      __builtin_amdgcn_sched_barrier(0);
+      compute(r2, ck + 2, r1, min(ck + 4, last), Refill{});
     }
   } else if constexpr (DEPTH == 2) {
     const int last = nc - 1;
     Ops r0, r1;
     if (nc > 0) load(r0, 0);
-    __builtin_amdgcn_sched_barrier(0);
     for (int ck = 0; ck < nc; ck += 2) {
-      load(r1, min(ck + 1, last));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(r0, ck);
-      __builtin_amdgcn_sched_barrier(0);
+      compute(r0, ck, r1, min(ck + 1, last), Refill{});
       if (ck + 1 >= nc) break;
-      load(r0, min(ck + 2, last));
-      __builtin_amdgcn_sched_barrier(0);
-      compute(r1, ck + 1);
-      __builtin_amdgcn_sched_barrier(0);
+      compute(r1, ck + 1, r0, min(ck + 2, last), Refill{});
     }
   } else {
     for (int ck = 0; ck < nc; ++ck) {
-      Ops r;
+      Ops r, unused;
       load(r, ck);
-      compute(r, ck);
+      compute(r, ck, unused, 0, NoRefill{});
     }
   }
   if (owner && Sfin) {
