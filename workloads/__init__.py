@@ -35,6 +35,8 @@ __all__ = [
     "gen_head_qkv",
     "gen_state",
     "gen_forward_inputs",
+    "varlen_lengths",
+    "gen_varlen",
     "gen_inputs",
     "gen_inputs_heads",
     "chunk_cumsum",
@@ -286,3 +288,63 @@ def as_blhd(*heads):
     """Stack per-head arrays ([L, d] or [L]) of one batch into [1, L, H, d]
     or [1, L, H]."""
     return np.stack(heads, axis=1)[None]
+
+
+# ----------------------------------------------------------------------------
+# packed variable-length sequences (serving)
+
+
+def varlen_lengths(total: int, seed: int = 3000, lo: int = 1, hi: int = 4096):
+    """Sequence lengths of a serving mix: log-uniform in [lo, hi], drawn until
+    they add up to `total` (the last one cut to fit)."""
+    rng = np.random.default_rng([seed, 5])
+    out = []
+    left = total
+    while left > 0:
+        n = int(np.exp(rng.uniform(np.log(lo), np.log(hi + 1))))
+        n = max(lo, min(n, hi, left))
+        out.append(n)
+        left -= n
+    return out
+
+
+def gen_varlen(w: Workload, lengths, C: Optional[int] = None, want_q: bool = False):
+    """Packed inputs of sequences with the given lengths: K [1, T, H, dk],
+    beta, g [1, T, H], V [1, T, H, dv] (and Q [1, T, H, dk] when asked),
+    cu_seqlens [n + 1] int32.  Sequence s, head h draws from
+    default_rng([seed, 2, s, h]) in the order K, beta, decay increments, V,
+    Q, with the workload's distributions; g is the within-chunk cumulative
+    sum with chunks restarting at every sequence start."""
+    C = w.C if C is None else C
+    lengths = [int(x) for x in lengths]
+    cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    T = int(cu[-1])
+    K = np.zeros((1, T, w.H, w.dk), np.float32)
+    V = np.zeros((1, T, w.H, w.dv), np.float32)
+    Q = np.zeros((1, T, w.H, w.dk), np.float32) if want_q else None
+    beta = np.zeros((1, T, w.H), np.float32)
+    g = np.zeros((1, T, w.H), np.float32)
+    for s, n in enumerate(lengths):
+        if n == 0:
+            continue
+        t0 = int(cu[s])
+        for h in range(w.H):
+            rng = np.random.default_rng([w.seed, 2, s, h])
+            z = rng.standard_normal((n, w.dk))
+            k = z / np.linalg.norm(z, axis=1, keepdims=True)
+            be = 1.0 / (1.0 + np.exp(-rng.standard_normal(n)))
+            x = rng.standard_normal(n)
+            inc = -_softplus(x + 3.0) if w.gate == "default" else -_softplus(2.0 * x + 1.0)
+            gg = np.empty(n)
+            for a in range(0, n, C):
+                gg[a:a + C] = np.cumsum(inc[a:a + C])
+            v = rng.standard_normal((n, w.dv))
+            K[0, t0:t0 + n, h] = _store(k, w.dtype)
+            V[0, t0:t0 + n, h] = _store(v, w.dtype)
+            beta[0, t0:t0 + n, h] = be
+            g[0, t0:t0 + n, h] = gg
+            if want_q:
+                z = rng.standard_normal((n, w.dk))
+                Q[0, t0:t0 + n, h] = _store(z / np.linalg.norm(z, axis=1, keepdims=True), w.dtype)
+    out = (K, beta, g, V, cu)
+    return out + (Q,) if want_q else out
