@@ -60,7 +60,10 @@ def parse():
     ap.add_argument("--path", default="fused", choices=["fused", "fused_blockwise", "inverse", "fwdsub", "blockwise",
                              "unfused", "int8", "forward"])
     ap.add_argument("--exact", action="store_true",
-                    help="--path forward: the exact block-wise inverse instead of T_hat(N, S)")
+                    help="--path forward / --varlen: the exact block-wise inverse instead of T_hat(N, S)")
+    ap.add_argument("--varlen", action="store_true",
+                    help="--path fused over packed sequences of a serving mix of lengths "
+                         "(log-uniform 1..4096, B*L tokens in total, ragged last chunks)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=2048,
                     help="tiles of the workload the CPU oracle runs on (whole heads)")
@@ -115,6 +118,8 @@ def main():
 
     if a.path == "forward":
         return bench_forward(a, w, C, N, S, (N0, S0), G, torch)
+    if a.varlen:
+        return bench_varlen(a, w, C, N, S, G, torch)
 
     # ---- inputs, resident in HBM before timing
     want_v = a.path in ("fused", "fused_blockwise", "unfused")
@@ -372,6 +377,92 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
     }
     if host is not None:
         out["cpu_baseline"] = cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale)
+    print(json.dumps(out), flush=True)
+
+
+def bench_varlen(a, w, C, N, S, G, torch):
+    """The fused path over packed sequences (gdn_chunk_wy_fused_varlen)."""
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    es = 2 if w.dtype == "bf16" else 4
+    lengths = wl.varlen_lengths(w.B * w.L)
+    K, beta, g, V, cu = wl.gen_varlen(w.with_(B=1), lengths, C=C)
+    T = int(cu[-1])
+    dev = lambda x, t: torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(t)
+    dK, dV, db, dg = dev(K, dt), dev(V, dt), dev(beta, torch.float32), dev(g, torch.float32)
+    tables = G.gdn_varlen_tables(cu, C)
+    n_chunks = tables[2]
+    n_tiles = n_chunks * w.H
+    dW, dU = torch.empty_like(dK), torch.empty_like(dV)
+    stream = torch.cuda.current_stream()
+    step = lambda: G.gdn_chunk_wy_fused_varlen(dK, dV, db, dg, tables, C, N=N, S=S,
+                                               exact=a.exact, W=dW, U=dU)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(a.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = e0.elapsed_time(e1) / a.steps
+    ms_per_step = wall * 1e3 / a.steps
+    tok = T * w.H
+    bytes_ = tok * (w.dk + w.dv) * es * 2 + tok * 8  # K, V in; W, U out; beta, g
+    achieved = bytes_ / (ev_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(n_tiles / (ms_per_step * 1e-3), 1),
+        "unit": "chunk inverses/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name + " packed serving mix", "sequences": len(lengths),
+                   "tokens": T, "H": w.H, "C": C, "dk": w.dk, "dv": w.dv, "N": N, "S": S,
+                   "chunks": n_chunks, "ragged_chunks": int(sum(1 for x in lengths if x % C)),
+                   "tiles": n_tiles, "path": "fused_varlen",
+                   "inverse": "exact block-wise" if a.exact else f"T_hat({N},{S})",
+                   "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_fused (packed)", "kernel_ms": round(ev_ms, 6),
+                     "algorithmic_bytes": bytes_},
+    }
+    if not a.no_cpu_baseline:
+        from oracle import gdn, varlen
+
+        try:
+            from threadpoolctl import threadpool_info
+            cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        except Exception:  # pragma: no cover
+            cores = os.cpu_count() or 1
+        # whole sequences from the start up to ~cpu_sample_tiles chunk tiles
+        nseq, tiles = 0, 0
+        while nseq < len(lengths) and tiles < a.cpu_sample_tiles:
+            tiles += -(-lengths[nseq] // C) * w.H
+            nseq += 1
+        te = int(cu[nseq])
+        inv = (gdn.forward_substitution_inverse if a.exact else
+               (lambda A: gdn.neumann_inverse(A, N, S)))
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            Wr, Ur, _ = varlen.wy_varlen(K[:, :te], V[:, :te], beta[:, :te], g[:, :te],
+                                         cu[:nseq + 1], C, inverse=inv)
+            passes += 1
+            secs = time.perf_counter() - t0
+            if secs >= a.cpu_seconds:
+                break
+        torch.cuda.synchronize()
+        err = {"W": float(np.max(np.abs(dW[:, :te].float().cpu().numpy() - Wr))),
+               "U": float(np.max(np.abs(dU[:, :te].float().cpu().numpy() - Ur)))}
+        out["cpu_baseline"] = {"value": round(tiles * passes / secs, 1), "unit": "chunk inverses/s",
+                               "cores": cores, "kind": "oracle",
+                               "sample": f"the first {nseq} sequences ({te} tokens, {tiles} chunk "
+                                         f"tiles), {passes} passes in float64 numpy, {secs:.2f} s",
+                               "max_abs_err_gpu_vs_oracle": err}
     print(json.dumps(out), flush=True)
 
 

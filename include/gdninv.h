@@ -147,6 +147,27 @@ int gdn_chunk_wy_fused_blockwise(const void* K, const void* V, const float* beta
                                  void* W, void* U, void* Tinv, int B, int L, int H, int dk, int dv,
                                  int C, int dtype, void* stream);
 
+/* gdn_chunk_wy_fused (exact = 0) or gdn_chunk_wy_fused_blockwise (exact = 1)
+ * over packed sequences of different lengths: K [1, T, H, dk], V [1, T, H,
+ * dv], beta, g [1, T, H] hold the sequences one after another; sequence s
+ * is tokens cu_seqlens[s] .. cu_seqlens[s + 1] - 1.  Chunks start at every
+ * sequence start, so the last chunk of a sequence holds m = l - C (ceil(l / C)
+ * - 1) <= C tokens; it is solved on its m x m system (Section 2.1 with the
+ * chunk's tokens only), and g must be the within-chunk cumulative sum for
+ * this chunking.  chunk_offsets[s] = sum over r < s of ceil(l_r / C), with
+ * chunk_offsets[nseq] = n_chunks.  Both tables are int32 DEVICE arrays of
+ * nseq + 1 entries, non-decreasing, cu_seqlens[0] = 0 and
+ * cu_seqlens[nseq] <= T; entries inconsistent with them make the affected
+ * chunks write nothing (never an access outside the arrays).  W, U:
+ * [1, T, H, d], rows of every token written.  Tinv (nullable):
+ * [H, n_chunks, C, C], the m x m inverse in the top left of each tile and the
+ * identity past m.  C in {16, 32, 64}. */
+int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, const float* g,
+                              void* W, void* U, void* Tinv, const int32_t* cu_seqlens,
+                              const int32_t* chunk_offsets, int nseq, int n_chunks, int T, int H,
+                              int dk, int dv, int C, int N, int S, int exact, int dtype,
+                              void* stream);
+
 /* INT8 mode, step 1 (Appendix G quantiser): per tile, e = the smallest
  * integer with max|A| / 2^e <= 127 and Aq = round-half-even(A / 2^e).
  * A: fp32 tiles; Aq: int8 tiles (same layout); eA: int32 [n_tiles].  An

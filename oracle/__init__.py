@@ -25,8 +25,11 @@ Modules:
   int8  exact-integer oracle of the low-bit (INT8) pipeline.
   gdn_forward  float64 oracle of the whole chunk-wise Gated DeltaNet forward
         (token recurrence, and the chunk-wise form around the inverse).
+  varlen  the chunk path over packed variable-length sequences (partial last
+        chunks).
 """
 
 from . import gdn  # noqa: F401
 from . import int8  # noqa: F401
 from . import gdn_forward  # noqa: F401
+from . import varlen  # noqa: F401

@@ -38,6 +38,9 @@ _SIGS = {
                           _c_int, _vp],
     "gdn_chunk_forward_workspace": [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
                                     ctypes.POINTER(_c_i64)],
+    "gdn_chunk_wy_fused_varlen": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int,
+                                  _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                  _c_int, _vp],
     "gdn_chunk_forward_prepare": [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
                                   _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_forward_state": [_vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
@@ -385,3 +388,51 @@ def gdn_chunk_forward_state(Q: torch.Tensor, g: torch.Tensor, C: int, workspace:
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         B, L, H, dk, dv, C, scale, dt, _stream(stream)))
     return O, S_final
+
+
+def gdn_varlen_tables(cu_seqlens, C: int, device="cuda"):
+    """Device tables for packed sequences from host-side sequence offsets
+    cu_seqlens (list, numpy array or CPU tensor of nseq + 1 ints): returns
+    (cu int32 device tensor, chunk offsets int32 device tensor, n_chunks).
+    This is host bookkeeping (a prefix sum of ceil(l / C)); nothing of the
+    method runs here."""
+    cu = [int(x) for x in (cu_seqlens.tolist() if hasattr(cu_seqlens, "tolist") else cu_seqlens)]
+    off = [0]
+    for s in range(len(cu) - 1):
+        off.append(off[-1] + max(0, cu[s + 1] - cu[s] + C - 1) // C)
+    dcu = torch.tensor(cu, dtype=torch.int32, device=device)
+    doff = torch.tensor(off, dtype=torch.int32, device=device)
+    return dcu, doff, off[-1]
+
+
+def gdn_chunk_wy_fused_varlen(K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor,
+                              g: torch.Tensor, tables, C: int, N: Optional[int] = None,
+                              S: Optional[int] = None, exact: bool = False, want_T: bool = False,
+                              W: Optional[torch.Tensor] = None, U: Optional[torch.Tensor] = None,
+                              Tinv: Optional[torch.Tensor] = None, stream=None):
+    """Fused build A -> inverse -> (W, U[, Tinv]) over packed sequences;
+    tables = gdn_varlen_tables(cu_seqlens, C)."""
+    dcu, doff, n_chunks = tables
+    B, T, H, dk = K.shape
+    if B != 1:
+        raise ValueError("packed sequences use B = 1")
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    if N is None or S is None:
+        dn, ds = gdn_default_order(C) if C in (16, 32, 64, 128) else (0, 0)
+        N = dn if N is None else N
+        S = ds if S is None else S
+    W = torch.empty_like(K) if W is None else W
+    U = torch.empty_like(V) if U is None else U
+    if want_T and Tinv is None:
+        Tinv = torch.empty((H, n_chunks, C, C), dtype=K.dtype, device=K.device)
+    tok = T * H
+    nseq = dcu.numel() - 1
+    tp = _dev(Tinv, "Tinv", K.dtype, H * n_chunks * C * C) if Tinv is not None else None
+    _check("gdn_chunk_wy_fused_varlen", lib.gdn_chunk_wy_fused_varlen(
+        _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv), _dev(beta, "beta", torch.float32, tok),
+        _dev(g, "g", torch.float32, tok), _dev(W, "W", K.dtype, tok * dk),
+        _dev(U, "U", K.dtype, tok * dv), tp, _dev(dcu, "cu_seqlens", torch.int32),
+        _dev(doff, "chunk_offsets", torch.int32, nseq + 1), nseq, n_chunks, T, H, dk, dv, C, N, S,
+        int(bool(exact)), dt, _stream(stream)))
+    return (W, U, Tinv) if Tinv is not None else (W, U)

@@ -195,6 +195,41 @@ int gdn_chunk_wy_fused_blockwise(const void* K, const void* V, const float* beta
   return wy_fused(K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, 0, 0, dtype, true, stream);
 }
 
+int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, const float* g,
+                              void* W, void* U, void* Tinv, const int32_t* cu_seqlens,
+                              const int32_t* chunk_offsets, int nseq, int n_chunks, int T, int H,
+                              int dk, int dv, int C, int N, int S, int exact, int dtype,
+                              void* stream) {
+  if (T < 0 || H < 0 || nseq < 0 || n_chunks < 0) return GDN_ERR_SHAPE;
+  if (!valid_C(C) || !valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
+  if (nseq == 0 && n_chunks != 0) return GDN_ERR_SHAPE;
+  if (n_chunks > T || (int64_t)n_chunks * H > kMaxTiles) return GDN_ERR_SHAPE;
+  if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
+  if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (C == 128) return GDN_ERR_UNSUPPORTED;
+  if (n_chunks == 0 || H == 0) return GDN_OK;
+  if (!K || !V || !beta || !g || !W || !U || !cu_seqlens || !chunk_offsets) return GDN_ERR_NULL;
+  if (!aligned(K) || !aligned(V) || !aligned(beta) || !aligned(g) || !aligned(W) ||
+      !aligned(U) || (Tinv && !aligned(Tinv)) || (reinterpret_cast<uintptr_t>(cu_seqlens) & 3) ||
+      (reinterpret_cast<uintptr_t>(chunk_offsets) & 3))
+    return GDN_ERR_ALIGN;
+  const int64_t tok = (int64_t)T * H, es = esize(dtype);
+  const int64_t kb = tok * dk * es, vb = tok * dv * es, bb = tok * 4;
+  const int64_t tb = (int64_t)H * n_chunks * C * C * es, qb = ((int64_t)nseq + 1) * 4;
+  const void* ins[6] = {K, V, beta, g, cu_seqlens, chunk_offsets};
+  const int64_t inb[6] = {kb, vb, bb, bb, qb, qb};
+  for (int i = 0; i < 6; ++i)
+    if (overlap(W, kb, ins[i], inb[i]) || overlap(U, vb, ins[i], inb[i]) ||
+        overlap(Tinv, tb, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(W, kb, U, vb) || overlap(W, kb, Tinv, tb) || overlap(U, vb, Tinv, tb))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_fused_varlen(K, V, beta, g, W, U, Tinv, cu_seqlens, chunk_offsets,
+                                             nseq, n_chunks, T, H, dk, dv, C, N, S, dtype,
+                                             exact != 0, (hipStream_t)stream));
+}
+
 int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                           void* stream) {
   if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)

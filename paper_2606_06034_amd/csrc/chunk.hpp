@@ -16,7 +16,9 @@ namespace gdn {
 // `tile` is the position in the [B, H, L/C, C, C] tile layout.
 struct Chunk {
   int b, h, t0;
+  int m;  // rows holding tokens: C, or fewer in the last chunk of a packed sequence
   int64_t tile;
+  __device__ Chunk() {}
   // x < 2^31 (the tile count is bounded so): 32-bit unsigned division
   __device__ Chunk(uint32_t x, int L, int H, int C) {
     const uint32_t nc = (uint32_t)(L / C);
@@ -25,7 +27,32 @@ struct Chunk {
     b = (int)(bc / nc);
     const int chunk = (int)(bc - (uint32_t)b * nc);
     t0 = chunk * C;
+    m = C;
     tile = ((int64_t)b * H + h) * nc + chunk;
+  }
+  // Packed sequences (B = 1, T tokens): sequence s holds tokens
+  // cu[s] .. cu[s + 1] - 1 and chunks off[s] .. off[s + 1] - 1, each chunk
+  // starting at a multiple of C from the sequence start.  Work item
+  // x = chunk * H + h; tile = h * nchunks + chunk.  Inconsistent tables give
+  // m = 0 (nothing to do), never an access outside the T tokens.
+  static __device__ Chunk packed(uint32_t x, int H, int C, int T, const int* __restrict__ cu,
+                                 const int* __restrict__ off, int nseq, int nchunks) {
+    Chunk ch;
+    const int chunk = (int)(x / (uint32_t)H);
+    ch.h = (int)(x - (uint32_t)chunk * (uint32_t)H);
+    ch.b = 0;
+    ch.tile = (int64_t)ch.h * nchunks + chunk;
+    // the last s with off[s] <= chunk (empty sequences repeat an offset)
+    int lo = 0, hi = nseq;  // off[lo] <= chunk is assumed, off[hi] = nchunks > chunk
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (off[mid] <= chunk) lo = mid; else hi = mid;
+    }
+    const int64_t t0 = (int64_t)cu[lo] + (int64_t)(chunk - off[lo]) * C;
+    const int64_t end = min((int64_t)cu[lo + 1], (int64_t)T);
+    ch.t0 = (t0 >= 0 && t0 < T) ? (int)t0 : 0;
+    ch.m = (t0 >= 0 && t0 < T) ? (int)max((int64_t)0, min((int64_t)C, end - t0)) : 0;
+    return ch;
   }
   // element offset of (token t0 + r, head h, feature 0) in [B, L, H, d]
   __device__ int64_t row(int r, int L, int H, int d) const {
@@ -33,14 +60,17 @@ struct Chunk {
   }
 };
 
-// beta and g of the chunk into LDS (one wave; C <= 128)
+// beta and g of the chunk into LDS (one wave; C <= 128).  Rows r >= m (past
+// the end of a packed sequence) get beta = 0, which makes them write nothing
+// (A's rows vanish, T is the identity there), and the last row's g.
 template <int C>
 __device__ __forceinline__ void load_gates(const float* __restrict__ beta,
                                            const float* __restrict__ g, const Chunk& ch, int L,
-                                           int H, float* sb, float* sg) {
+                                           int H, float* sb, float* sg, int m = C) {
   for (int r = lane_id(); r < C; r += 64) {
-    const int64_t o = ((int64_t)ch.b * L + ch.t0 + r) * H + ch.h;
-    if (sb) sb[r] = beta[o];
+    const int rr = r < m ? r : m - 1;
+    const int64_t o = ((int64_t)ch.b * L + ch.t0 + rr) * H + ch.h;
+    if (sb) sb[r] = r < m ? beta[o] : 0.f;
     if (sg) sg[r] = g[o];
   }
   __syncthreads();
@@ -105,14 +135,21 @@ __device__ __forceinline__ void store_row8(float* p, f32x4 lo, f32x4 hi) {
   *(f32x4*)(p + 4) = hi;
 }
 
+// Rows r >= m (past the end of a packed sequence) are read from row m - 1
+// and set to 0.
 template <int NB, int D, typename F, typename TIO>
 __device__ __forceinline__ void load_rows(Pair<F> (&xp)[NB][D / 32], const TIO* __restrict__ xb,
-                                          int64_t ld, Lane ln = lane_here()) {
+                                          int64_t ld, Lane ln = lane_here(), int m = 16 * NB) {
   const int g = ln.g(), c = ln.c();
 #pragma unroll
-  for (int I = 0; I < NB; ++I)
+  for (int I = 0; I < NB; ++I) {
+    const int r = I * 16 + c, rr = r < m ? r : m - 1;
 #pragma unroll
-    for (int q = 0; q < D / 32; ++q) xp[I][q] = load_row8<F>(xb + (I * 16 + c) * ld + 32 * q + 8 * g);
+    for (int q = 0; q < D / 32; ++q) {
+      xp[I][q] = load_row8<F>(xb + rr * ld + 32 * q + 8 * g);
+      if (r >= m) xp[I][q] = Pair<F>::zero();
+    }
+  }
 }
 
 // The strictly lower A of one chunk in fp32, row-form blocks (zero on and

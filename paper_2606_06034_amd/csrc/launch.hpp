@@ -44,6 +44,12 @@ hipError_t launch_forward(const void* Q, const void* K, const void* V, const flo
                           int L, int H, int dk, int dv, int C, int N, int S, bool exact,
                           float scale, int dtype, int phases, hipStream_t st);
 int64_t fwd_workspace_elems(int C, int dk, int dv);
+// the fused kernel over packed sequences (C <= 64): cu, off device tables of
+// nseq + 1 token / chunk offsets, nchunks chunks, Ttok tokens
+hipError_t launch_fused_varlen(const void* K, const void* V, const float* beta, const float* g,
+                               void* W, void* U, void* T, const int* cu, const int* off, int nseq,
+                               int nchunks, int Ttok, int H, int dk, int dv, int C, int N, int S,
+                               int dtype, bool exact, hipStream_t st);
 hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                               hipStream_t st);
 hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,

@@ -72,31 +72,43 @@ __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO*
 
 // One tile per wave.  PREF (bf16 only): V is copied into LDS by DMA right
 // after the Gram product and arrives while the inverse is computed.
+// VARLEN: packed sequences (B = 1, L = T tokens, chunk tables cu / off):
+// the last chunk of a sequence may hold m < C tokens; its rows past m are
+// neither read nor written (T is the identity there).
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool PREF = false, bool EXACT = false>
+          bool PREF = false, bool EXACT = false, bool VARLEN = false>
 __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               const TIO* __restrict__ V,
                                               const float* __restrict__ beta,
                                               const float* __restrict__ g, TIO* __restrict__ W,
                                               TIO* __restrict__ U, TIO* __restrict__ Tout, int L,
-                                              int H, int N, int S) {
+                                              int H, int N, int S, const int* __restrict__ cu,
+                                              const int* __restrict__ off, int nseq,
+                                              int nchunks) {
   constexpr int C = 16 * NB;
   static_assert(!PREF || sizeof(TIO) == 2, "V prefetch is for bf16 IO");
   __shared__ float sb[C], sg[C];
   __shared__ __attribute__((aligned(16))) __bf16 sv[PREF ? NB * (DV / 32) * 512 : 8];
-  const Chunk ch(blockIdx.x, L, H, C);
+  Chunk ch;
+  if constexpr (VARLEN)
+    ch = Chunk::packed(blockIdx.x, H, C, L, cu, off, nseq, nchunks);
+  else
+    ch = Chunk(blockIdx.x, L, H, C);
+  const int m = VARLEN ? ch.m : C;
+  if (VARLEN && m <= 0) return;
   const int64_t tile = ch.tile;
-  load_gates<C>(beta, g, ch, L, H, sb, sg);
+  load_gates<C>(beta, g, ch, L, H, sb, sg, m);
+  const Lane ln = lane_here();
 
   Pair<F> kp[NB][DK / 32];
-  load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+  load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK, ln, m);
   // issued once K has been consumed: the compiler counts DMA completions as
   // unordered with plain loads and would otherwise wait for V before the
   // Gram; the inverse that follows touches no global memory
   auto prefetch_v = [&]() {
     if constexpr (PREF) {
       __builtin_amdgcn_sched_barrier(0);
-      prefetch_rows_lds<NB, DV>((const __bf16*)V + ch.row(0, L, H, DV), (int64_t)H * DV, sv);
+      prefetch_rows_lds<NB, DV>((const __bf16*)V + ch.row(0, L, H, DV), (int64_t)H * DV, sv, ln, m);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -109,20 +121,21 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
   scale_cols(TR, Tr, sb);
   // with the prefetch, U is formed first from V read out of LDS one slice at
   // a time, then W from the K pairs, so K and V are never both in registers
+  const int64_t ldk = (int64_t)H * DK, ldv = (int64_t)H * DV;
   if constexpr (PREF) {
     wait_vmem();
-    apply_lower<NB, DV>(TR, LdsRows<DV>{sv, lane_id()}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
-    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+    apply_lower<NB, DV>(TR, LdsRows<DV>{sv, ln.id}, U + ch.row(0, L, H, DV), ldv, ln, (TIO*)nullptr, m);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, (TIO*)nullptr, m);
   } else if constexpr (NB <= 2) {  // registers to spare: V's loads overlap W
     Pair<F> vp[NB][DV / 32];
-    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
-    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
-    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv, ln, m);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, (TIO*)nullptr, m);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln, (TIO*)nullptr, m);
   } else {
-    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), (int64_t)H * DK);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, (TIO*)nullptr, m);
     Pair<F> vp[NB][DV / 32];
-    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), (int64_t)H * DV);
-    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), (int64_t)H * DV);
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv, ln, m);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln, (TIO*)nullptr, m);
   }
 }
 
@@ -443,13 +456,27 @@ template <> struct FusedOrder<1> { static constexpr int N = 3, S = 2; };
 template <> struct FusedOrder<2> { static constexpr int N = 3, S = 4; };
 template <> struct FusedOrder<4> { static constexpr int N = 3, S = 8; };
 
+// Packed sequences for the fused kernel: cu (nseq + 1 token offsets) and off
+// (nseq + 1 chunk offsets) device tables; nullptr for the fixed-length path.
+struct Packed {
+  const int* cu = nullptr;
+  const int* off = nullptr;
+  int nseq = 0, nchunks = 0;
+};
+
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO, bool PREF,
           bool EXACT = false>
 static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,
-                       void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st) {
-  hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT>), dim3((unsigned)n),
-                     dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U,
-                     (TIO*)T, L, H, N, S);
+                       void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st,
+                       const Packed& pk = Packed{}) {
+  if (pk.cu)
+    hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, true>),
+                       dim3((unsigned)n), dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g,
+                       (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, pk.cu, pk.off, pk.nseq, pk.nchunks);
+  else
+    hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, false>),
+                       dim3((unsigned)n), dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g,
+                       (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, nullptr, nullptr, 0, 0);
 }
 
 // bf16 with C >= 32 prefetches V (for C = 16 the tile is small and the
@@ -457,22 +484,23 @@ static void launch_one(const void* K, const void* V, const float* beta, const fl
 template <int NB, typename F, typename TIO>
 static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, const float* g,
                                void* W, void* U, void* T, int64_t n, int L, int H, int dk,
-                               int dv, int N, int S, bool exact, hipStream_t st) {
+                               int dv, int N, int S, bool exact, hipStream_t st,
+                               const Packed& pk = Packed{}) {
   constexpr int DN = FusedOrder<NB>::N, DS = FusedOrder<NB>::S;
   constexpr bool PREF = sizeof(TIO) == 2 && NB > 1;
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
     if (exact)
       launch_one<NB, DK, DV, F, true, 0, 0, TIO, PREF, true>(K, V, beta, g, W, U, T, n, L, H, N,
-                                                             S, st);
+                                                             S, st, pk);
     else if (N == DN && S == DS)
       launch_one<NB, DK, DV, F, true, DN, DS, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
-                                                          st);
+                                                          st, pk);
     else if (N <= 15)
       launch_one<NB, DK, DV, F, true, -1, -1, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
-                                                          st);
+                                                          st, pk);
     else
       launch_one<NB, DK, DV, F, false, -1, -1, TIO, PREF>(K, V, beta, g, W, U, T, n, L, H, N, S,
-                                                           st);
+                                                           st, pk);
     return hipGetLastError();
   }))
   return hipErrorNotSupported;
@@ -511,6 +539,32 @@ static hipError_t run_fused(const void* K, const void* V, const float* beta, con
     case 32: return run_fused_nb<2, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, exact, st);
     case 64: return run_fused_nb<4, F, TIO>(K, V, beta, g, W, U, T, n, L, H, dk, dv, N, S, exact, st);
   }
+  return hipErrorNotSupported;
+}
+
+hipError_t launch_fused_varlen(const void* K, const void* V, const float* beta, const float* g,
+                               void* W, void* U, void* T, const int* cu, const int* off, int nseq,
+                               int nchunks, int Ttok, int H, int dk, int dv, int C, int N, int S,
+                               int dtype, bool exact, hipStream_t st) {
+  const Packed pk{cu, off, nseq, nchunks};
+  const int64_t n = (int64_t)nchunks * H;
+#define GDN_FV(NB_, F_, T_)                                                                     \
+  return run_fused_nb<NB_, F_, T_>(K, V, beta, g, W, U, T, n, Ttok, H, dk, dv, N, S, exact, st, \
+                                   pk)
+  if (dtype == 0) {
+    switch (C) {
+      case 16: GDN_FV(1, f32x4, float);
+      case 32: GDN_FV(2, f32x4, float);
+      case 64: GDN_FV(4, f32x4, float);
+    }
+  } else if (dtype == 1) {
+    switch (C) {
+      case 16: GDN_FV(1, bf16x4, __bf16);
+      case 32: GDN_FV(2, bf16x4, __bf16);
+      case 64: GDN_FV(4, bf16x4, __bf16);
+    }
+  }
+#undef GDN_FV
   return hipErrorNotSupported;
 }
 

@@ -21,16 +21,21 @@ namespace gdn {
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void glb_void;
 
+// Rows r >= m are copied from row m - 1 (finite values that the zero
+// columns of T diag(beta) cancel).
 template <int NB, int D>
 __device__ __forceinline__ void prefetch_rows_lds(const __bf16* __restrict__ xb, int64_t ld,
-                                                  __bf16* s, Lane ln = lane_here()) {
+                                                  __bf16* s, Lane ln = lane_here(),
+                                                  int m = 16 * NB) {
   const int g = ln.g(), c = ln.c();
 #pragma unroll
-  for (int I = 0; I < NB; ++I)
+  for (int I = 0; I < NB; ++I) {
+    const int r = I * 16 + c, rr = r < m ? r : m - 1;
 #pragma unroll
     for (int q = 0; q < D / 32; ++q)
-      __builtin_amdgcn_global_load_lds((glb_void*)(xb + (I * 16 + c) * ld + 32 * q + 8 * g),
+      __builtin_amdgcn_global_load_lds((glb_void*)(xb + rr * ld + 32 * q + 8 * g),
                                        (lds_void*)(s + 512 * (I * (D / 32) + q)), 16, 0, 0);
+  }
 }
 
 // wait for every outstanding vector-memory operation of this wave
@@ -48,7 +53,8 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 template <int NB, int D, typename F, typename TIO, typename Get>
 __device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, Get&& get,
                                             TIO* __restrict__ ob, int64_t ld,
-                                            Lane ln = lane_here(), TIO* lds_copy = nullptr) {
+                                            Lane ln = lane_here(), TIO* lds_copy = nullptr,
+                                            int m = 16 * NB) {
   const int g = ln.g(), c = ln.c();
   const f32x4 e = eye4(ln);
   const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
@@ -76,7 +82,7 @@ __device__ __forceinline__ void apply_lower(const RowP<NB, F>& TR, Get&& get,
 #pragma unroll
         for (int p = 0; p < npair(NB); ++p)
           if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(TR.r[I][p], y[h][p], acc[h]);
-      store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
+      if (I * 16 + c < m) store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
       if (lds_copy) store_row8(lds_copy + 512 * (I * (D / 32) + q) + 8 * ln.id, acc[0], acc[1]);
     }
   }

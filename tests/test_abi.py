@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 17
+    assert len(names) == 18
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -274,6 +274,36 @@ def test_forward_phase_validation():
     assert s(*bad, None) == UNSUP
     bad = list(sb); bad[7] = 0
     assert s(*bad, None) == OK
+
+
+def test_fused_varlen_validation():
+    f = L.gdn_chunk_wy_fused_varlen
+    names = ["K", "V", "beta", "g", "W", "U", "Tinv", "cu", "off", "nseq", "nch", "T", "H", "dk",
+             "dv", "C", "N", "S", "exact", "dt"]
+    base = dict(K=P1, V=BIG, beta=2 * BIG, g=3 * BIG, W=4 * BIG, U=5 * BIG, Tinv=None,
+                cu=6 * BIG, off=6 * BIG + 4096, nseq=3, nch=5, T=200, H=2, dk=128, dv=128, C=64,
+                N=3, S=8, exact=0, dt=1)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return f(*[a[n] for n in names], None)
+
+    assert call(C=48) == SHAPE
+    assert call(nseq=-1) == SHAPE
+    assert call(nseq=0) == SHAPE        # chunks without sequences
+    assert call(nch=300) == SHAPE       # more chunks than tokens
+    assert call(dk=96) == SHAPE
+    assert call(N=64) == PARAM
+    assert call(exact=3) == PARAM
+    assert call(dt=2) == DTYPE
+    assert call(C=128) == UNSUP
+    assert call(cu=None) == NULL
+    assert call(W=None) == NULL
+    assert call(off=6 * BIG + 2) == ALIGN
+    assert call(U=4 * BIG + 256) == ALIAS   # U over W
+    assert call(W=6 * BIG) == ALIAS         # W over the tables
+    assert call(nch=0, K=None) == OK
+    assert call(H=0) == OK
 
 
 def test_binding_rejects_host_tensors():
