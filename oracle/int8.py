@@ -33,6 +33,13 @@ This module fixes them (one reading, applied identically by the GPU path):
 
 All arithmetic here is on Python/numpy integers; no floating point enters
 after quantize().
+
+INT16 (the paper's main integer setting, Section 3.5 and Appendix G) is the
+same recipe with 16-bit codes: |q| <= 32639 (= 127 * 256 + 127, so a code
+splits into two int8 limbs), the running sums 16 guard bits below a code's
+quantum (terms kept below 2^31, sums below 2^36), and products exact in
+int64.  SPEC8 and SPEC16 hold the two parameter sets; every function takes
+the spec (INT8 by default).
 """
 
 from __future__ import annotations
@@ -41,8 +48,22 @@ from typing import List, Tuple
 
 import numpy as np
 
-QMAX = 127
-ALIGN_BITS = 23  # aligned terms stay below 2^23 in magnitude
+import dataclasses
+
+
+@dataclasses.dataclass(frozen=True)
+class Spec:
+    qmax: int        # codes q in [-qmax, qmax]
+    qbits: int       # 2^(qbits - 1) <= qmax < 2^qbits
+    align_bits: int  # aligned sum terms stay below 2^align_bits
+    sum_bits: int    # running sums stay below 2^sum_bits
+
+
+SPEC8 = Spec(qmax=127, qbits=7, align_bits=23, sum_bits=31)
+SPEC16 = Spec(qmax=32639, qbits=15, align_bits=31, sum_bits=37)
+
+QMAX = SPEC8.qmax
+ALIGN_BITS = SPEC8.align_bits  # aligned terms stay below 2^23 in magnitude
 
 
 # ----------------------------------------------------------------------------
@@ -74,15 +95,16 @@ def _tile_amax(q: np.ndarray) -> np.ndarray:
     return np.max(np.abs(q), axis=(-1, -2))
 
 
-def requant(acc: np.ndarray, e: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
-    """Per tile: smallest shift s >= 0 with rne(max|acc| / 2^s) <= 127;
-    returns (q int64 codes, e + s).  An all-zero tile gets e = 0."""
+def requant(acc: np.ndarray, e: np.ndarray, spec: Spec = SPEC8) -> Tuple[np.ndarray, np.ndarray]:
+    """Per tile: smallest shift s >= 0 with rne(max|acc| / 2^s) <= qmax
+    (127 for INT8); returns (q int64 codes, e + s).  An all-zero tile gets
+    e = 0."""
     acc = np.asarray(acc, dtype=np.int64)
     e = np.asarray(e, dtype=np.int64)
     amax = _tile_amax(acc)
     s = np.zeros_like(amax)
     while True:
-        big = rne_shift(amax, s) > QMAX
+        big = rne_shift(amax, s) > spec.qmax
         if not np.any(big):
             break
         s = s + big.astype(np.int64)
@@ -95,20 +117,21 @@ def requant(acc: np.ndarray, e: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 # quantisation of the float input
 
 
-def quantize(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+def quantize(x: np.ndarray, spec: Spec = SPEC8) -> Tuple[np.ndarray, np.ndarray]:
     """Symmetric per-tile quantiser with a power-of-two scale.
 
-    x float32 tiles [..., C, C].  e = ceil(log2(amax / 127)) computed exactly
-    from frexp: amax = m 2^p, m in [0.5, 1) gives amax / 2^(p-7) = 128 m,
-    which is <= 127 unless m > 127/128.  q = rne(x / 2^e).  All-zero tiles
-    get q = 0, e = 0."""
+    x float32 tiles [..., C, C].  e = ceil(log2(amax / qmax)) computed
+    exactly from frexp: amax = m 2^p, m in [0.5, 1) gives
+    amax / 2^(p - qbits) = 2^qbits m, which is <= qmax unless
+    m > qmax / 2^qbits (INT8: 128 m <= 127 unless m > 127/128).
+    q = rne(x / 2^e).  All-zero tiles get q = 0, e = 0."""
     x = np.asarray(x, dtype=np.float32).astype(np.float64)
     amax = np.max(np.abs(x), axis=(-1, -2))
     m, p = np.frexp(amax)
-    e = (p.astype(np.int64) - 7) + (m * 128.0 > 127.0).astype(np.int64)
+    e = (p.astype(np.int64) - spec.qbits) + (m * float(1 << spec.qbits) > spec.qmax).astype(np.int64)
     e = np.where(amax > 0, e, 0)
     q = np.rint(np.ldexp(x, -e[..., None, None])).astype(np.int64)
-    assert np.all(np.abs(q) <= QMAX)
+    assert np.all(np.abs(q) <= spec.qmax)
     return q, e
 
 
@@ -116,12 +139,13 @@ def quantize(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 # exact running sums
 
 
-def _acc_bits(C: int) -> int:
-    # |acc| <= C * 127^2 < C * 2^14
-    return 14 + int(np.ceil(np.log2(C)))
+def _acc_bits(C: int, spec: Spec = SPEC8) -> int:
+    # |acc| <= C * qmax^2 < C * 2^(2 qbits)
+    return 2 * spec.qbits + int(np.ceil(np.log2(C)))
 
 
-def aligned_sum(terms: List[Tuple[np.ndarray, np.ndarray, np.ndarray, int]]):
+def aligned_sum(terms: List[Tuple[np.ndarray, np.ndarray, np.ndarray, int]],
+                spec: Spec = SPEC8):
     """Running int32 sum of q_k * 2^(e_k), terms taken in the given order.
 
     terms: list of (q, e, present, bits) with q [..., C, C] int, e [...] int,
@@ -142,7 +166,7 @@ def aligned_sum(terms: List[Tuple[np.ndarray, np.ndarray, np.ndarray, int]]):
         q = np.asarray(q, np.int64)
         e = np.asarray(e, np.int64)
         p = np.asarray(p, bool)
-        top = e + bits - ALIGN_BITS
+        top = e + bits - spec.align_bits
         first = p & ~anyp
         rebase = p & anyp & (top > e_acc)
         d = np.where(rebase, top - e_acc, 0)
@@ -153,7 +177,7 @@ def aligned_sum(terms: List[Tuple[np.ndarray, np.ndarray, np.ndarray, int]]):
         total = total + np.where(p[..., None, None], t, 0)
         anyp |= p
     e_acc = np.where(anyp, e_acc, 0)
-    assert np.all(np.abs(total) < (1 << 31))
+    assert np.all(np.abs(total) < (1 << spec.sum_bits))
     return total, e_acc, anyp
 
 
@@ -167,20 +191,23 @@ def _subdiag(C: int) -> np.ndarray:
     return i - j
 
 
-def neumann_inverse_int8(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
+def neumann_inverse_int8(qA: np.ndarray, eA: np.ndarray, N: int, S: int, spec: Spec = SPEC8):
     """Integer T_hat(N, S) from the quantised GDN matrix (qA, eA).
 
     qA int [..., C, C] (only i > j is read), eA int [...].
-    Returns (qT, eT): T_hat = I + qT * 2^eT, qT int8-range codes of the
-    strict lower part (zero on and above the diagonal), and the parts
-    dictionary for inspection."""
+    Returns (qT, eT): T_hat = I + qT * 2^eT, qT codes (int8 range, or
+    int16 range with SPEC16) of the strict lower part (zero on and above the
+    diagonal), and the parts dictionary for inspection."""
     qA = np.asarray(qA, np.int64)
     eA = np.asarray(eA, np.int64)
     C = qA.shape[-1]
     d = _subdiag(C)
     strict = d > 0
     band = (d > 0) & (d <= N)
-    accb = _acc_bits(C)
+    accb = _acc_bits(C, spec)
+    qb = spec.qbits
+    rq = lambda acc, e: requant(acc, e, spec)
+    asum = lambda terms: aligned_sum(terms, spec)
 
     qL = np.where(strict, -qA, 0)
     eL = eA
@@ -190,31 +217,31 @@ def neumann_inverse_int8(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
     powers = []
     if N >= 1:
         qB = np.where(band, qL, 0)
-        qB, eB = requant(qB, eL)
+        qB, eB = rq(qB, eL)
         powers.append((qB, eB, _tile_amax(qB) > 0))
         for _n in range(2, N + 1):
             qP, eP, nzP = powers[-1]
             acc = np.where(band, qP @ qL, 0)
-            q, e = requant(acc, eP + eL)
+            q, e = rq(acc, eP + eL)
             powers.append((q, e, (_tile_amax(q) > 0)))
 
     # N0 = strict part of T^(0) = sum_n B_n
     if powers:
-        s_, e_, p_ = aligned_sum([(q, e, p, 7) for (q, e, p) in powers])
-        qN0, eN0 = requant(s_, e_)
+        s_, e_, p_ = asum([(q, e, p, qb) for (q, e, p) in powers])
+        qN0, eN0 = rq(s_, e_)
     else:
         qN0 = np.zeros_like(qL)
         eN0 = np.zeros_like(eL)
     nzN0 = _tile_amax(qN0) > 0
 
     # E = I - (I + A) T0 = Lm + Lm N0 - N0, band zeroed (Section 3.4)
-    s_, e_, _ = aligned_sum([
-        (qL, eL, nzL, 7),
+    s_, e_, _ = asum([
+        (qL, eL, nzL, qb),
         (qL @ qN0, eL + eN0, nzL & nzN0, accb),
-        (-qN0, eN0, nzN0, 7),
+        (-qN0, eN0, nzN0, qb),
     ])
     s_ = np.where(d > N, s_, 0)
-    qE, eE = requant(s_, e_)
+    qE, eE = rq(s_, e_)
     nzE = _tile_amax(qE) > 0
 
     # residual powers P_s = E P_{s-1}, G strict part = sum_{s=1}^{S} P_s
@@ -223,26 +250,31 @@ def neumann_inverse_int8(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
         chain.append((qE, eE, nzE))
         for _s in range(2, S + 1):
             qP, eP, nzP = chain[-1]
-            q, e = requant(qE @ qP, eE + eP)
+            q, e = rq(qE @ qP, eE + eP)
             chain.append((q, e, (_tile_amax(q) > 0)))
     if chain:
-        s_, e_, _ = aligned_sum([(q, e, p, 7) for (q, e, p) in chain])
-        qG, eG = requant(s_, e_)
+        s_, e_, _ = asum([(q, e, p, qb) for (q, e, p) in chain])
+        qG, eG = rq(s_, e_)
     else:
         qG = np.zeros_like(qL)
         eG = np.zeros_like(eL)
     nzG = _tile_amax(qG) > 0
 
     # T_hat = (I + N0)(I + Gs) = I + N0 + Gs + N0 Gs
-    s_, e_, _ = aligned_sum([
-        (qN0, eN0, nzN0, 7),
-        (qG, eG, nzG, 7),
+    s_, e_, _ = asum([
+        (qN0, eN0, nzN0, qb),
+        (qG, eG, nzG, qb),
         (qN0 @ qG, eN0 + eG, nzN0 & nzG, accb),
     ])
     s_ = np.where(strict, s_, 0)
-    qT, eT = requant(s_, e_)
+    qT, eT = rq(s_, e_)
     parts = {"N0": (qN0, eN0), "E": (qE, eE), "G": (qG, eG), "powers": powers, "chain": chain}
     return qT, eT, parts
+
+
+def neumann_inverse_int16(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
+    """neumann_inverse_int8 with 16-bit codes (SPEC16)."""
+    return neumann_inverse_int8(qA, eA, N, S, SPEC16)
 
 
 def dequant_unit(qT: np.ndarray, eT: np.ndarray) -> np.ndarray:

@@ -1,4 +1,4 @@
-"""Pins of the exact-integer (INT8) oracle.
+"""Pins of the exact-integer (INT8 and INT16) oracle.
 
 The paper fixes the quantiser q(x) = clip(round(x / Delta), qmin, qmax)
 (Appendix G) and the method (Algorithm 1); the integer mechanics are this
@@ -109,10 +109,15 @@ def _py_rne(y, s):
     return y if s <= 0 else round(Fraction(y, 1 << s))
 
 
-def _py_requant(M, e):
+# (qmax, bits of a code, alignment bits) of the two integer settings
+PY8 = (127, 7, 23)
+PY16 = (32639, 15, 31)
+
+
+def _py_requant(M, e, P=PY8):
     amax = max(abs(v) for row in M for v in row)
     s = 0
-    while _py_rne(amax, s) > 127:
+    while _py_rne(amax, s) > P[0]:
         s += 1
     return [[_py_rne(v, s) for v in row] for row in M], (e + s if amax > 0 else 0)
 
@@ -126,16 +131,17 @@ def _py_nz(M):
     return any(v != 0 for row in M for v in row)
 
 
-def _py_sum(terms, C):
+def _py_sum(terms, C, P=PY8):
     """terms: (M, e, present, bits), summed in order with the running-exponent
-    rule (first term sets e = e0 + bits - 23; rebase when a term's top would
-    pass e + 23; finer terms rounded half-even)."""
+    rule (first term sets e = e0 + bits - a with a = 23 for INT8, 31 for
+    INT16; rebase when a term's top would pass e + a; finer terms rounded
+    half-even)."""
     out = [[0] * C for _ in range(C)]
     es = None
     for M, e, p, b in terms:
         if not p:
             continue
-        top = e + b - 23
+        top = e + b - P[2]
         if es is None:
             es = top
         elif top > es:
@@ -148,40 +154,43 @@ def _py_sum(terms, C):
     return out, (0 if es is None else es)
 
 
-def _py_pipeline(qA, eA, N, S):
+def _py_pipeline(qA, eA, N, S, P=PY8):
     C = len(qA)
-    bits = 14 + (C - 1).bit_length()
+    q = P[1]
+    bits = 2 * q + (C - 1).bit_length()
+    rq = lambda M, e: _py_requant(M, e, P)
+    sm = lambda terms: _py_sum(terms, C, P)
     L = [[-qA[i][j] if i > j else 0 for j in range(C)] for i in range(C)]
     band = lambda M: [[M[i][j] if 0 < i - j <= N else 0 for j in range(C)] for i in range(C)]
     pw = []
     if N >= 1:
-        B, eB = _py_requant(band(L), eA)
+        B, eB = rq(band(L), eA)
         pw.append((B, eB))
         for _ in range(2, N + 1):
-            B, eB = _py_requant(band(_py_mm(pw[-1][0], L)), pw[-1][1] + eA)
+            B, eB = rq(band(_py_mm(pw[-1][0], L)), pw[-1][1] + eA)
             pw.append((B, eB))
     if pw:
-        N0, eN = _py_requant(*_py_sum([(M, e, _py_nz(M), 7) for M, e in pw], C))
+        N0, eN = rq(*sm([(M, e, _py_nz(M), q) for M, e in pw]))
     else:
         N0, eN = [[0] * C for _ in range(C)], 0
     nzL, nzN = _py_nz(L), _py_nz(N0)
-    Es, ee = _py_sum([(L, eA, nzL, 7), (_py_mm(L, N0), eA + eN, nzL and nzN, bits),
-                      ([[-v for v in r] for r in N0], eN, nzN, 7)], C)
+    Es, ee = sm([(L, eA, nzL, q), (_py_mm(L, N0), eA + eN, nzL and nzN, bits),
+                 ([[-v for v in r] for r in N0], eN, nzN, q)])
     Es = [[Es[i][j] if i - j > N else 0 for j in range(C)] for i in range(C)]
-    E, eE = _py_requant(Es, ee)
+    E, eE = rq(Es, ee)
     ch = []
     if S >= 1:
         ch.append((E, eE))
         for _ in range(2, S + 1):
-            ch.append(_py_requant(_py_mm(E, ch[-1][0]), eE + ch[-1][1]))
+            ch.append(rq(_py_mm(E, ch[-1][0]), eE + ch[-1][1]))
     if ch:
-        G, eG = _py_requant(*_py_sum([(M, e, _py_nz(M), 7) for M, e in ch], C))
+        G, eG = rq(*sm([(M, e, _py_nz(M), q) for M, e in ch]))
     else:
         G, eG = [[0] * C for _ in range(C)], 0
     nzG = _py_nz(G)
-    Ts, et = _py_sum([(N0, eN, nzN, 7), (G, eG, nzG, 7), (_py_mm(N0, G), eN + eG, nzN and nzG, bits)], C)
+    Ts, et = sm([(N0, eN, nzN, q), (G, eG, nzG, q), (_py_mm(N0, G), eN + eG, nzN and nzG, bits)])
     Ts = [[Ts[i][j] if i > j else 0 for j in range(C)] for i in range(C)]
-    return _py_requant(Ts, et)
+    return rq(Ts, et)
 
 
 @pytest.mark.parametrize("C,N,S", [(8, 3, 2), (8, 1, 3), (16, 3, 2), (16, 2, 5), (8, 0, 3), (8, 3, 0)])
@@ -256,3 +265,142 @@ def test_int8_structure():
     assert np.all(parts["E"][0][:, d <= N] == 0)
     for s, (q, e, nz) in enumerate(parts["chain"], start=1):
         assert np.all(q[:, d < s * (N + 1)] == 0)
+
+
+# ---------------------------------------------------------------------------
+# INT16: the same recipe with 16-bit codes (|q| <= 32639), 31-bit aligned
+# terms; the pins above repeated at that width
+
+
+def test_int16_quantize_minimal_exponent_and_roundtrip():
+    rng = np.random.default_rng(11)
+    x = (rng.standard_normal((50, 16, 16)) * np.exp(rng.uniform(-20, 5, (50, 1, 1)))).astype(np.float32)
+    q, e = qo.quantize(x, qo.SPEC16)
+    amax = np.max(np.abs(x.astype(np.float64)), axis=(-1, -2))
+    assert np.all(amax <= 32639 * np.ldexp(1.0, e))
+    assert np.all(amax > 32639 * np.ldexp(1.0, e - 1))
+    assert np.all(np.abs(q) <= 32639) and np.max(np.abs(q)) > 16319
+    for t in range(50):
+        for v, w in zip(x[t].ravel().tolist(), q[t].ravel().tolist()):
+            assert w == round(Fraction(v) / Fraction(2) ** int(e[t]))
+    # codes at the range ends come back exactly
+    q0 = rng.integers(-32639, 32640, (10, 8, 8))
+    q0[:, 0, 0] = -32639
+    e0 = rng.integers(-40, 5, 10)
+    q1, e1 = qo.quantize(qo.dequant(q0, e0).astype(np.float32), qo.SPEC16)
+    # float32 holds 24 bits: every 15-bit code times a power of two is exact
+    assert np.array_equal(q1, q0) and np.array_equal(e1, e0)
+
+
+def test_int16_requant_smallest_shift():
+    rng = np.random.default_rng(12)
+    acc = rng.integers(-(1 << 36), 1 << 36, (100, 8, 8))
+    acc[:10] //= 1 << 25
+    acc[10] = rng.integers(-1000, 1000, (8, 8))
+    acc[10, 0, 0] = 32639 * 4 + 2  # 32639.5 * 4 rounds up to 32640: one more bit
+    q, e = qo.requant(acc, np.zeros(100, np.int64), qo.SPEC16)
+    assert np.all(np.abs(q) <= 32639)
+    assert e[10] == 3
+    for t in range(100):
+        s = int(e[t])
+        amax = int(np.max(np.abs(acc[t])))
+        assert round(Fraction(amax, 1 << s)) <= 32639
+        if s > 0:
+            assert round(Fraction(amax, 1 << (s - 1))) > 32639
+        for v, w in zip(acc[t].ravel().tolist(), q[t].ravel().tolist()):
+            assert w == round(Fraction(v, 1 << s))
+
+
+def test_int16_aligned_sum_is_exact_within_guard_bits():
+    rng = np.random.default_rng(13)
+    qa = rng.integers(-32639, 32640, (5, 4, 4))
+    qb = rng.integers(-32639, 32640, (5, 4, 4))
+    ea = rng.integers(-30, -4, 5)
+    eb = ea - rng.integers(0, 17, 5)
+    p = np.ones(5, bool)
+    s, es, _ = qo.aligned_sum([(qa, ea, p, 15), (qb, eb, p, 15)], qo.SPEC16)
+    assert np.all(es == ea - 16)
+    for t in range(5):
+        for i in range(4):
+            for j in range(4):
+                want = Fraction(int(qa[t, i, j])) * Fraction(2) ** int(ea[t]) + \
+                    Fraction(int(qb[t, i, j])) * Fraction(2) ** int(eb[t])
+                assert Fraction(int(s[t, i, j])) * Fraction(2) ** int(es[t]) == want
+
+
+@pytest.mark.parametrize("C,N,S", [(8, 3, 2), (16, 3, 2), (16, 2, 5), (8, 0, 3), (8, 3, 0)])
+def test_int16_pipeline_matches_independent_coding(C, N, S):
+    k, b, g, _ = wl.gen_stress_head(L=2 * C, dk=32, C=C, seed=C + N + S + 50)
+    A = gdn.tiles_flat(gdn.build_A(k[None, :, None], b[None, :, None], g[None, :, None], C))
+    qA, eA = qo.quantize(A.astype(np.float32), qo.SPEC16)
+    qT, eT, _ = qo.neumann_inverse_int16(qA, eA, N, S)
+    for t in range(A.shape[0]):
+        Tp, ep = _py_pipeline(qA[t].tolist(), int(eA[t]), N, S, PY16)
+        assert qT[t].tolist() == Tp
+        assert int(eT[t]) == ep
+
+
+def test_int16_all_ones_gdn_is_exact():
+    C = 64
+    A = np.tril(np.ones((1, C, C), np.float32), -1)
+    qA, eA = qo.quantize(A, qo.SPEC16)
+    qT, eT, parts = qo.neumann_inverse_int16(qA, eA, 3, 8)
+    assert np.array_equal(qo.dequant_unit(qT, eT)[0], np.eye(C) - np.eye(C, k=-1))
+    assert np.all(parts["E"][0] == 0)
+
+
+@pytest.mark.parametrize("gate", ["default", "wide"])
+def test_int16_close_to_float_approximation(gate):
+    """Each requantisation keeps 15 bits relative to its matrix's largest
+    entry: the dequantised INT16 T_hat(3, 8) stays within a small multiple of
+    2^-16 max|T_hat - I| of the float64 T_hat(3, 8), about 2^8 times closer
+    than INT8."""
+    w = wl.workload("int8" if gate == "wide" else "tiny")
+    k, b, g, _ = wl.gen_head(w, 0, 0, want_v=False)
+    A = gdn.tiles_flat(gdn.build_A(k[None, :256, None], b[None, :256, None], g[None, :256, None], 64))
+    T = gdn.neumann_inverse(A, 3, 8)
+    scale = np.max(np.abs(T - np.eye(64)), axis=(-1, -2))
+    q16, e16 = qo.quantize(A.astype(np.float32), qo.SPEC16)
+    qT, eT, _ = qo.neumann_inverse_int16(q16, e16, 3, 8)
+    err16 = np.max(np.abs(qo.dequant_unit(qT, eT) - T), axis=(-1, -2))
+    assert np.all(err16 <= 4 * 2.0 ** -16 * scale)
+    q8, e8 = qo.quantize(A.astype(np.float32))
+    qT8, eT8, _ = qo.neumann_inverse_int8(q8, e8, 3, 8)
+    err8 = np.max(np.abs(qo.dequant_unit(qT8, eT8) - T), axis=(-1, -2))
+    assert np.max(err16) * 32 < np.max(err8)
+
+
+def test_int16_stress_close_to_float():
+    k, b, g, _ = wl.gen_stress_head(L=256, dk=128, C=64, seed=9)
+    A = gdn.tiles_flat(gdn.build_A(k[None, :, None], b[None, :, None], g[None, :, None], 64))
+    qA, eA = qo.quantize(A.astype(np.float32), qo.SPEC16)
+    qT, eT, _ = qo.neumann_inverse_int16(qA, eA, 3, 8)
+    T = gdn.neumann_inverse(A, 3, 8)
+    scale = np.max(np.abs(T - np.eye(64)), axis=(-1, -2))
+    err = np.max(np.abs(qo.dequant_unit(qT, eT) - T), axis=(-1, -2))
+    assert np.all(err <= 16 * 2.0 ** -16 * scale)
+
+
+def test_int16_structure():
+    w = wl.workload("tiny")
+    k, b, g, _ = wl.gen_head(w, 0, 1, want_v=False)
+    A = gdn.tiles_flat(gdn.build_A(k[None, :128, None], b[None, :128, None], g[None, :128, None], 64))
+    qA, eA = qo.quantize(A.astype(np.float32), qo.SPEC16)
+    N, S = 3, 8
+    qT, eT, parts = qo.neumann_inverse_int16(qA, eA, N, S)
+    d = gdn.subdiag_index(64)
+    assert np.all(qT[:, d <= 0] == 0)
+    assert np.all(np.abs(qT) <= 32639) and np.max(np.abs(qT)) > 16319
+    assert np.all(parts["E"][0][:, d <= N] == 0)
+    for s, (q, e, nz) in enumerate(parts["chain"], start=1):
+        assert np.all(q[:, d < s * (N + 1)] == 0)
+
+
+def test_int16_limbs_split_every_code():
+    """32639 = 127 * 256 + 127: every INT16 code is hi * 256 + lo with both
+    limbs int8 codes, so a product of 16-bit codes is four int8 products."""
+    q = np.arange(-32639, 32640)
+    lo = ((q + 128) & 255) - 128
+    hi = (q - lo) >> 8
+    assert np.all(hi * 256 + lo == q)
+    assert lo.min() >= -128 and lo.max() <= 127 and hi.min() >= -127 and hi.max() <= 127
