@@ -1,7 +1,8 @@
 """Benchmark of the chunk-wise Gated DeltaNet inverse path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--C C]
-                    [--path fused|fused_blockwise|inverse|fwdsub|blockwise|unfused|int8|forward]
+                    [--path fused|fused_blockwise|inverse|fwdsub|blockwise|unfused|int8|int16|
+                            forward]
                     [--no-cpu-baseline]
 
 A step is one pass of the hot path over one batch of synthetic inputs
@@ -23,7 +24,8 @@ of the layer can be read off.
 --path int8 runs the low-bit path (default workload "int8": B=4, H=32,
 L=16384, C=64, wide gates) in one launch: build A in fp32 -> per-tile INT8
 quantiser -> integer inverse T_hat(3, 8); the same path as three launches
-is timed beside it for context.
+is timed beside it for context.  --path int16 does the same with 16-bit
+codes (each product four int8 MFMAs over the codes' limbs).
 """
 
 from __future__ import annotations
@@ -58,7 +60,7 @@ def parse():
     ap.add_argument("--N", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
     ap.add_argument("--path", default="fused", choices=["fused", "fused_blockwise", "inverse", "fwdsub", "blockwise",
-                             "unfused", "int8", "forward"])
+                             "unfused", "int8", "int16", "forward"])
     ap.add_argument("--exact", action="store_true",
                     help="--path forward / --varlen: the exact block-wise inverse instead of T_hat(N, S)")
     ap.add_argument("--varlen", action="store_true",
@@ -104,7 +106,8 @@ def main():
         print(json.dumps(error_grid(a, G, torch)), flush=True)
         return
 
-    if a.path == "int8" and a.workload == "qwen35_prefill" and "--workload" not in sys.argv:
+    low = a.path in ("int8", "int16")
+    if low and a.workload == "qwen35_prefill" and "--workload" not in sys.argv:
         a.workload = "int8"
     w = wl.workload(a.workload)
     C = a.C or w.C
@@ -145,10 +148,12 @@ def main():
             G.gdn_wy_apply(dT, dK, dV, db, C, W=dW, U=dU)
     elif a.path == "inverse":
         step = lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT)
-    elif a.path == "int8":
-        dTq = torch.empty((w.B, w.H, w.L // C, C, C), dtype=torch.int8, device="cuda")
+    elif low:
+        qdt, sfx = (torch.int8, "i8") if a.path == "int8" else (torch.int16, "i16")
+        fused = getattr(G, f"gdn_chunk_inverse_neumann_{sfx}_fused")
+        dTq = torch.empty((w.B, w.H, w.L // C, C, C), dtype=qdt, device="cuda")
         deT = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
-        step = lambda: G.gdn_chunk_inverse_neumann_i8_fused(dK, db, dg, C, N, S, Tq=dTq, eT=deT)
+        step = lambda: fused(dK, db, dg, C, N, S, Tq=dTq, eT=deT)
     elif a.path == "blockwise":
         step = lambda: G.gdn_chunk_inverse_blockwise(dA, Tinv=dT)
     else:
@@ -169,14 +174,16 @@ def main():
     ev_ms = e0.elapsed_time(e1) / a.steps  # HIP-event time per step (one launch for fused/inverse/fwdsub)
     ms_per_step = wall * 1e3 / a.steps
     value = n_tiles / (ms_per_step * 1e-3)
-    if a.path == "int8":  # context: the same path as three launches
+    if low:  # context: the same path as three launches
+        quant = getattr(G, f"gdn_quantize_tiles_{sfx}")
+        inv = getattr(G, f"gdn_chunk_inverse_neumann_{sfx}")
         dA32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
-        dAq = torch.empty(dA32.shape, dtype=torch.int8, device="cuda")
+        dAq = torch.empty(dA32.shape, dtype=qdt, device="cuda")
         deA = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
         dTq2, deT2 = torch.empty_like(dAq), torch.empty_like(deA)
         stages = [lambda: G.gdn_build_A(dK, db, dg, C, A=dA32),
-                  lambda: G.gdn_quantize_tiles_i8(dA32, Aq=dAq, eA=deA),
-                  lambda: G.gdn_chunk_inverse_neumann_i8(dAq, deA, N, S, Tq=dTq2, eT=deT2)]
+                  lambda: quant(dA32, Aq=dAq, eA=deA),
+                  lambda: inv(dAq, deA, N, S, Tq=dTq2, eT=deT2)]
         stage_ms = []
         for fn in stages:
             fn()
@@ -216,17 +223,19 @@ def main():
         flops = n_tiles * (C ** 3 - C) // 3  # sum over i > j of (i - j) FMAs = (C^3 - C) / 6
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
         kernel = "k_fwdsub" if a.path == "fwdsub" else "k_blockwise"
-    elif a.path == "int8":
-        # K (dk per token) and beta, g in; int8 T_hat codes and exponents out
-        bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C + 4)
-        flops = (N + S) * 2 * C ** 3 * n_tiles  # int8 ops of the N + S products
+    elif low:
+        # K (dk per token) and beta, g in; T_hat codes and exponents out.  An
+        # INT16 product is four int8 MFMA products over the codes' limbs.
+        qb = 1 if a.path == "int8" else 2
+        bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C * qb + 4)
+        flops = (N + S) * 2 * C ** 3 * n_tiles * qb * qb  # int8 MFMA ops of the N + S products
         if flops / bytes_ >= INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
             bound, peak, unit = "mfma", INT8_PEAK_TOPS, "TOP/s"
             achieved = flops / (ev_ms * 1e-3) / 1e12
         else:
             bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
             achieved = bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = "k_inverse_i8_fused"
+        kernel = f"k_inverse_{sfx}_fused"
     else:
         bytes_ = None
         flops = f_inv
@@ -259,17 +268,17 @@ def main():
                      "algorithmic_bytes": bytes_, "algorithmic_flops": flops},
     }
 
-    if a.path == "int8":
-        out["tops_int8_dense_equiv"] = out.pop("tflops_dense_equiv")
-        out["tops_vs_int8_peak"] = round(out.pop("tflops_vs_bf16_peak") * BF16_PEAK_TFLOPS
-                                         / INT8_PEAK_TOPS, 4)
+    if low:
+        out["tops_int8_dense_equiv"] = round(flops / (ev_ms * 1e-3) / 1e12, 2)
+        out["tops_vs_int8_peak"] = round(flops / (ev_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
+        del out["tflops_dense_equiv"], out["tflops_vs_bf16_peak"]
         out["config"]["three_launch_ms"] = {"build_A_f32": round(stage_ms[0], 6),
                                             "quantize": round(stage_ms[1], 6),
-                                            "inverse_i8": round(stage_ms[2], 6)}
-        out["dtype"] = "i8"
+                                            "inverse_" + sfx: round(stage_ms[2], 6)}
+        out["dtype"] = sfx
         if not a.no_cpu_baseline:
-            out["cpu_baseline"] = cpu_baseline_int8(w, C, N, S, a, (K, beta, g), dTq, deT,
-                                                    torch, G)
+            out["cpu_baseline"] = cpu_baseline_int(w, C, N, S, a, (K, beta, g), dTq, deT,
+                                                   torch, G, sfx)
     elif not a.no_cpu_baseline and a.path in ("fused", "unfused"):
         out["cpu_baseline"] = cpu_baseline(w, C, N, S, a, (K, beta, g, V), dK, dV, db, dg,
                                              torch, G)
@@ -508,6 +517,7 @@ PROFILES = {("fused", "qwen35_prefill", 64): ("k_fused_qwen35_prefill.md", "pipe
             ("fused", "long_context", 64): ("k_fused_long_context.md", "pipeline.hip"),
             ("inverse", "sweep", 64): ("k_neumann_sweep_c64.md", "neumann.hip"),
             ("int8", "int8", 64): ("k_inverse_i8_fused_int8.md", "int8.hip"),
+            ("int16", "int8", 64): ("k_inverse_i16_fused_int8.md", "int16.hip"),
             ("forward", "qwen35_prefill", 64): ("k_fwd_state_qwen35_prefill.md", "forward.hip")}
 
 
@@ -642,7 +652,7 @@ def _threads():
         return os.cpu_count() or 1
 
 
-def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
+def cpu_baseline_int(w, C, N, S, a, host_inputs, dTq, deT, torch, G, sfx):
     """The integer oracle on whole heads up to `cpu_sample_tiles` tiles,
     passes repeated until `cpu_seconds` have elapsed: build A in float64,
     round to float32, quantise, integer T_hat.  Reports the GPU's
@@ -652,6 +662,7 @@ def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
     from oracle import gdn
     from oracle import int8 as oi
 
+    spec = oi.SPEC8 if sfx == "i8" else oi.SPEC16
     nc = w.L // C
     want = max(1, a.cpu_sample_tiles)
     heads = [(b, h) for b in range(w.B) for h in range(w.H)][:max(1, -(-want // nc))]
@@ -662,8 +673,8 @@ def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
     passes, t0 = 0, time.perf_counter()
     while True:
         A = gdn.build_A(Ks, bs, gs, C).astype(np.float32)
-        qA, eA = oi.quantize(A)
-        qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S)
+        qA, eA = oi.quantize(A, spec)
+        qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S, spec)
         passes += 1
         secs = time.perf_counter() - t0
         if secs >= a.cpu_seconds:
@@ -678,7 +689,8 @@ def cpu_baseline_int8(w, C, N, S, a, host_inputs, dTq, deT, torch, G):
     return {"value": round(tiles * passes / secs, 1), "unit": "chunk inverses/s",
             "cores": _threads(), "kind": "oracle",
             "sample": f"{len(heads)} heads x {nc} chunks of {w.name} ({tiles} tiles), {passes} "
-                      f"passes: build A + INT8 quantiser + integer T_hat({N},{S}), numpy, "
+                      f"passes: build A + {sfx.upper().replace('I', 'INT')} quantiser + "
+                      f"integer T_hat({N},{S}), numpy, "
                       f"{secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"T": float(np.max(np.abs(Tg - Tr)))},
             "max_abs_err_vs_exact_inverse": {"gpu": float(np.max(np.abs(Tg - X))),

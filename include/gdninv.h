@@ -200,6 +200,43 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
                                        int8_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                        int dk, int C, int N, int S, int k_dtype, void* stream);
 
+/* INT16 mode, step 1: the quantiser of gdn_quantize_tiles_i8 with 16-bit
+ * codes (Appendix G lists INT16 activations for the inverse): per tile,
+ * e = the smallest integer with max|A| / 2^e <= 32639 and
+ * Aq = round-half-even(A / 2^e).  A: fp32 tiles; Aq: int16 tiles (same
+ * layout); eA: int32 [n_tiles].  An all-zero tile gets Aq = 0, eA = 0.  Only
+ * the strictly lower part of A is read (the rest is taken as 0 and written
+ * as 0). */
+int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_tiles,
+                           int C, void* stream);
+
+/* INT16 mode, step 2: the integer inverse of gdn_chunk_inverse_neumann_i8
+ * with 16-bit codes (Section 3.5): codes in [-32639, 32639], every product
+ * exact (each code split into two int8 limbs, four int8 MFMAs per product,
+ * recombined exactly in fp64) and requantised to 16 bits after every
+ * product with a per-tile power-of-two rescale; sums align their terms
+ * exactly below 2^31 (16 guard bits under a code's quantum).  Outputs:
+ * Tinv = I + Tq * 2^eT, Tq int16 tiles holding the strict lower part (0 on
+ * and above the diagonal), eT int32 [n_tiles]; Tdeq (nullable) receives
+ * I + Tq * 2^eT in fp32.  Aq codes must lie in [-32639, 32639], the range
+ * the quantiser writes (a negated code must split into two int8 limbs);
+ * a tile holding -32768 gets unspecified codes.  C in {16, 32, 64}. */
+int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
+                                  int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
+                                  int N, int S, void* stream);
+
+/* INT16 mode in one launch: A in fp32 from K, beta, g (the values
+ * gdn_build_A writes with a_dtype GDN_F32), quantised per tile in registers
+ * by the rule of gdn_quantize_tiles_i16, then the integer inverse of
+ * gdn_chunk_inverse_neumann_i16.  Arguments and layouts as
+ * gdn_chunk_inverse_neumann_i8_fused, with int16 Tq.  Given the same fp32 A
+ * tile the codes equal those of gdn_quantize_tiles_i16 followed by
+ * gdn_chunk_inverse_neumann_i16. */
+int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const float* g,
+                                        int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L,
+                                        int H, int dk, int C, int N, int S, int k_dtype,
+                                        void* stream);
+
 /* Chunk-wise Gated DeltaNet forward of one layer, built around the chunk
  * inverse: the chunk-level recurrence of Gated DeltaNet that Section 1
  * starts from, with Y = T^-1 X (Appendix E) evaluated per chunk.  Per head,

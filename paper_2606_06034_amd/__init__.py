@@ -28,12 +28,15 @@ from ._binding import (  # noqa: F401
     gdn_chunk_inverse_neumann,
     gdn_chunk_inverse_neumann_i8,
     gdn_chunk_inverse_neumann_i8_fused,
+    gdn_chunk_inverse_neumann_i16,
+    gdn_chunk_inverse_neumann_i16_fused,
     gdn_chunk_wy_fused,
     gdn_chunk_wy_fused_blockwise,
     gdn_chunk_wy_fused_varlen,
     gdn_varlen_tables,
     gdn_default_order,
     gdn_quantize_tiles_i8,
+    gdn_quantize_tiles_i16,
     gdn_status_string,
     gdn_wy_apply,
     lib,

@@ -33,6 +33,11 @@ _SIGS = {
     "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i8_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
                                            _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
+    "gdn_quantize_tiles_i16": [_vp, _vp, _vp, _c_i64, _c_int, _vp],
+    "gdn_chunk_inverse_neumann_i16": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
+                                      _vp],
+    "gdn_chunk_inverse_neumann_i16_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
+                                            _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_forward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int,
                           _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_float,
                           _c_int, _vp],
@@ -297,6 +302,62 @@ def gdn_chunk_inverse_neumann_i8_fused(K: torch.Tensor, beta: torch.Tensor, g: t
     _check("gdn_chunk_inverse_neumann_i8_fused", lib.gdn_chunk_inverse_neumann_i8_fused(
         _dev(K, "K"), _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
         _dev(Tq, "Tq", torch.int8, n * C * C), _dev(eT, "eT", torch.int32, n),
+        _dev(Td, "Tdeq", torch.float32, n * C * C) if Td is not None else None,
+        B, L, H, dk, C, N, S, _fdtype(K, "K"), _stream(stream)))
+    return (Tq, eT, Td) if Td is not None else (Tq, eT)
+
+
+def gdn_quantize_tiles_i16(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
+                           eA: Optional[torch.Tensor] = None, stream=None):
+    """(Aq int16 tiles, eA int32 per tile) with A ~ Aq * 2^eA."""
+    n, C = _tiles(A)
+    Aq = torch.empty(A.shape, dtype=torch.int16, device=A.device) if Aq is None else Aq
+    eA = torch.empty(n, dtype=torch.int32, device=A.device) if eA is None else eA
+    _check("gdn_quantize_tiles_i16", lib.gdn_quantize_tiles_i16(
+        _dev(A, "A", torch.float32), _dev(Aq, "Aq", torch.int16, A.numel()),
+        _dev(eA, "eA", torch.int32, n), n, C, _stream(stream)))
+    return Aq, eA
+
+
+def gdn_chunk_inverse_neumann_i16(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: int,
+                                  want_deq: bool = False, Tq: Optional[torch.Tensor] = None,
+                                  eT: Optional[torch.Tensor] = None,
+                                  Tdeq: Optional[torch.Tensor] = None, stream=None):
+    """(Tq int16, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT."""
+    n, C = _tiles(Aq)
+    Tq = torch.empty_like(Aq) if Tq is None else Tq
+    eT = torch.empty_like(eA) if eT is None else eT
+    Td = Tdeq
+    if want_deq and Td is None:
+        Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device)
+    _check("gdn_chunk_inverse_neumann_i16", lib.gdn_chunk_inverse_neumann_i16(
+        _dev(Aq, "Aq", torch.int16), _dev(eA, "eA", torch.int32, n),
+        _dev(Tq, "Tq", torch.int16, Aq.numel()), _dev(eT, "eT", torch.int32, n),
+        _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
+        _stream(stream)))
+    return (Tq, eT, Td) if Td is not None else (Tq, eT)
+
+
+def gdn_chunk_inverse_neumann_i16_fused(K: torch.Tensor, beta: torch.Tensor, g: torch.Tensor,
+                                        C: int, N: int, S: int, want_deq: bool = False,
+                                        Tq: Optional[torch.Tensor] = None,
+                                        eT: Optional[torch.Tensor] = None,
+                                        Tdeq: Optional[torch.Tensor] = None, stream=None):
+    """K [B, L, H, dk] -> (Tq int16 [B, H, L/C, C, C], eT int32[, Tdeq fp32]):
+    build A, quantise and invert in one launch."""
+    B, L, H, dk = K.shape
+    nc = L // C if C else 0
+    shape = (B, H, nc, C, C)
+    n = B * H * nc
+    Tq = torch.empty(shape, dtype=torch.int16, device=K.device) if Tq is None else Tq
+    eT = torch.empty(n, dtype=torch.int32, device=K.device) if eT is None else eT
+    Td = Tdeq
+    if want_deq and Td is None:
+        Td = torch.empty(shape, dtype=torch.float32, device=K.device)
+    tok = B * L * H
+    _check("gdn_chunk_inverse_neumann_i16_fused", lib.gdn_chunk_inverse_neumann_i16_fused(
+        _dev(K, "K"), _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
+        _dev(Tq, "Tq", torch.int16, n * C * C), _dev(eT, "eT", torch.int32, n),
         _dev(Td, "Tdeq", torch.float32, n * C * C) if Td is not None else None,
         B, L, H, dk, C, N, S, _fdtype(K, "K"), _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)

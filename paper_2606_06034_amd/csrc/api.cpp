@@ -294,6 +294,71 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
                                                  k_dtype, (hipStream_t)stream));
 }
 
+int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_tiles, int C,
+                           void* stream) {
+  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+    return GDN_ERR_SHAPE;
+  if (n_tiles == 0) return GDN_OK;
+  if (!A || !Aq || !eA) return GDN_ERR_NULL;
+  if (!aligned(A) || !aligned(Aq) || !aligned(eA)) return GDN_ERR_ALIGN;
+  const int64_t ab = n_tiles * C * C * 4, qb = n_tiles * C * C * 2, eb = n_tiles * 4;
+  if (overlap(Aq, qb, A, ab) || overlap(eA, eb, A, ab) || overlap(Aq, qb, eA, eb))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_quantize_i16(A, Aq, eA, n_tiles, C, (hipStream_t)stream));
+}
+
+int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
+                                  int32_t* eT, float* Tdeq, int64_t n_tiles, int C, int N, int S,
+                                  void* stream) {
+  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+    return GDN_ERR_SHAPE;
+  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (n_tiles == 0) return GDN_OK;
+  if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
+  if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
+    return GDN_ERR_ALIGN;
+  const int64_t qb = n_tiles * C * C * 2, eb = n_tiles * 4, db = n_tiles * C * C * 4;
+  const void* ins[2] = {Aq, eA};
+  const int64_t inb[2] = {qb, eb};
+  for (int i = 0; i < 2; ++i)
+    if (overlap(Tq, qb, ins[i], inb[i]) || overlap(eT, eb, ins[i], inb[i]) ||
+        overlap(Tdeq, db, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
+    return GDN_ERR_ALIAS;
+  return hip_status(
+      gdn::launch_neumann_i16(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, (hipStream_t)stream));
+}
+
+int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const float* g,
+                                        int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L,
+                                        int H, int dk, int C, int N, int S, int k_dtype,
+                                        void* stream) {
+  if (C == 128) return GDN_ERR_SHAPE;
+  int64_t n = 0;
+  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (!valid_d(dk)) return GDN_ERR_SHAPE;
+  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(k_dtype)) return GDN_ERR_DTYPE;
+  if (n == 0) return GDN_OK;
+  if (!K || !beta || !g || !Tq || !eT) return GDN_ERR_NULL;
+  if (!aligned(K) || !aligned(beta) || !aligned(g) || !aligned(Tq) || !aligned(eT) ||
+      (Tdeq && !aligned(Tdeq)))
+    return GDN_ERR_ALIGN;
+  const int64_t tok = (int64_t)B * L * H;
+  const int64_t qb = n * C * C * 2, eb = n * 4, db = n * C * C * 4;
+  const void* ins[3] = {K, beta, g};
+  const int64_t inb[3] = {tok * dk * esize(k_dtype), tok * 4, tok * 4};
+  for (int i = 0; i < 3; ++i)
+    if (overlap(Tq, qb, ins[i], inb[i]) || overlap(eT, eb, ins[i], inb[i]) ||
+        overlap(Tdeq, db, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_inverse_i16_fused(K, beta, g, Tq, eT, Tdeq, B, L, H, dk, C, N,
+                                                  S, k_dtype, (hipStream_t)stream));
+}
+
 int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int dtype,
                                 int64_t* bytes) {
   if (!bytes) return GDN_ERR_NULL;

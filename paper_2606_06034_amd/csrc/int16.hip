@@ -1,0 +1,631 @@
+// int16.hip -- the INT16 path: per-tile quantiser and the integer
+// masked-Neumann + residual inverse with 16-bit codes (Section 3.5,
+// Appendix G of arXiv 2606.06034: INT16 activations for the inverse), one
+// wave per tile.
+//
+// Arithmetic: the integer recipe of the INT8 path with 16-bit codes:
+//   * codes q in [-32639, 32639], one exponent per tile (value q 2^e);
+//   * quantiser: e = smallest integer with max|x| / 2^e <= 32639,
+//     q = round-half-even(x / 2^e);
+//   * products exact, requantised with the smallest round-half-even shift
+//     that brings max|acc| to <= 32639 (exponents add);
+//   * running sums exact in production order: the first present term sets the
+//     exponent 16 guard bits below its quantum (terms aligned below 2^31), a
+//     later term above that range rebases the sum (round-half-even), finer
+//     terms are rounded in;
+//   * the mask, E, the residual chain and T exactly as in the INT8 path.
+//
+// gfx950 has no 16-bit integer MFMA.  32639 = 127 * 256 + 127, so every code
+// splits into two int8 limbs q = 256 h + l (l in [-128, 127], h in
+// [-127, 127]) and a product of codes is four int8 MFMAs over the quad
+// fragments of intq.hpp:
+//   X Y = 2^16 Xh Yh + 2^8 (Xh Yl + Xl Yh) + Xl Yl,
+// with 2^8 Xh Yh + (Xh Yl + Xl Yh) exact in int32 (|.| < 2^29) and the sum
+// exact in fp64 (|X Y| < C 2^30 <= 2^36).  Products and running sums are
+// held as fp64 integers (exact below 2^53), codes as int32.  Rounding a
+// fp64 integer by 2^s is rint(ldexp(x, -s)): the scaling is exact and rint
+// rounds half to even.
+#include "chunk.hpp"
+#include "intq.hpp"
+#include "launch.hpp"
+
+namespace gdn {
+namespace i16 {
+
+using namespace iq;
+
+constexpr int kQmax = 32639;
+constexpr int kAlignBits = 31;
+
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+template <int NB> struct AccD { f64x4 a[nlower(NB)]; };  // fp64 integers
+
+// the two int8 limbs of a matrix of codes, as quads
+template <int NB> struct RowL { RowQ<NB> h, l; };
+template <int NB> struct ColL { ColQ<NB> h, l; };
+
+__device__ __forceinline__ int lo_limb(int x) { return ((x + 128) & 255) - 128; }
+
+// limbs of the blocks that can meet [lo, hi] (others zero)
+template <int NB>
+__device__ __forceinline__ void split(const AccI<NB>& D, AccI<NB>& Hi, AccI<NB>& Lo, int lo,
+                                      int hi) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 h = zero_i4(), l = zero_i4();
+      if (blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int x = D.a[bidx(I, J)][v];
+          l[v] = lo_limb(x);
+          h[v] = (x - l[v]) >> 8;
+        }
+      Hi.a[bidx(I, J)] = h;
+      Lo.a[bidx(I, J)] = l;
+    }
+}
+template <int NB>
+__device__ __forceinline__ void to_rowl(RowL<NB>& X, const AccI<NB>& D, int lo, int hi) {
+  AccI<NB> h, l;
+  split(D, h, l, lo, hi);
+  to_rowq(X.h, h, lo, hi);
+  to_rowq(X.l, l, lo, hi);
+}
+template <int NB>
+__device__ __forceinline__ void to_coll(ColL<NB>& Y, const AccI<NB>& D, int lo, int hi) {
+  AccI<NB> h, l;
+  split(D, h, l, lo, hi);
+  to_colq(Y.h, h, lo, hi);
+  to_colq(Y.l, l, lo, hi);
+}
+
+// D = X Y exactly, blocks outside [olo, ohi] set to 0; OUTQ: row-form result
+template <int NB, bool OUTQ>
+__device__ __forceinline__ void mml(AccD<NB>& D, const RowL<NB>& X, const ColL<NB>& Y, int olo,
+                                    int ohi) {
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      f64x4 r = f64x4{0.0, 0.0, 0.0, 0.0};
+      if (blk_nz(I - J, olo, ohi)) {
+        const i32x4 xh = X.h.r[I].v, xl = X.l.r[I].v, yh = Y.h.c[J].v, yl = Y.l.c[J].v;
+        const i32x4 z = zero_i4();
+        i32x4 hh, mx, ll;
+        if constexpr (OUTQ) {
+          hh = __builtin_amdgcn_mfma_i32_16x16x64_i8(yh, xh, z, 0, 0, 0);
+          mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(yl, xh, z, 0, 0, 0);
+          mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(yh, xl, mx, 0, 0, 0);
+          ll = __builtin_amdgcn_mfma_i32_16x16x64_i8(yl, xl, z, 0, 0, 0);
+        } else {
+          hh = __builtin_amdgcn_mfma_i32_16x16x64_i8(xh, yh, z, 0, 0, 0);
+          mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(xh, yl, z, 0, 0, 0);
+          mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(xl, yh, mx, 0, 0, 0);
+          ll = __builtin_amdgcn_mfma_i32_16x16x64_i8(xl, yl, z, 0, 0, 0);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          r[v] = __builtin_fma((double)(hh[v] * 256 + mx[v]), 256.0, (double)ll[v]);
+      }
+      D.a[bidx(I, J)] = r;
+    }
+}
+
+// codes of the limb matrices recombined: D = 256 H + L
+template <int NB>
+__device__ __forceinline__ void join(AccI<NB>& D, const AccI<NB>& H, const AccI<NB>& L) {
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b) D.a[b] = H.a[b] * 256 + L.a[b];
+}
+
+// Form changes through the identity, limb by limb (exact).
+// Column-form limbs (and, when wanted, codes) of a row-form matrix.
+template <int NB>
+__device__ __forceinline__ void row_to_col(ColL<NB>& Y, AccI<NB>* codes, const RowL<NB>& X,
+                                           const ColQ<NB>& Ic, int lo, int hi) {
+  AccI<NB> h, l;
+  mmi<NB, false>(h, X.h, Ic, lo, hi);
+  mmi<NB, false>(l, X.l, Ic, lo, hi);
+  to_colq(Y.h, h, lo, hi);
+  to_colq(Y.l, l, lo, hi);
+  if (codes) join(*codes, h, l);
+}
+// Row-form codes of a column-form matrix.
+template <int NB>
+__device__ __forceinline__ void col_to_row(AccI<NB>& D, const RowQ<NB>& Iq, const ColL<NB>& Y,
+                                           int lo, int hi) {
+  AccI<NB> h, l;
+  mmi<NB, true>(h, Iq, Y.h, lo, hi);
+  mmi<NB, true>(l, Iq, Y.l, lo, hi);
+  join(D, h, l);
+}
+
+// Smallest s >= 0 with round-half-even(amax / 2^s) <= 32639, from the high
+// dword of amax (an fp64 integer >= 0, lo dword dropped).  The test is
+// amax < 32639.5 2^s; the threshold has 16 significant bits, so its low
+// dword is zero and amax and its truncation to the high dword compare
+// alike with it.  amax = m 2^p, m in [0.5, 1): 2^15 m < 32639.5 gives
+// s = p - 15, else p - 14 (never below 0).
+__device__ __forceinline__ int shift_for_hi(int amax_hi) {
+  const double a = __hiloint2double(amax_hi, 0);
+  int p;
+  const double m = frexp(a, &p);
+  return max(0, p - 15 + (m * 32768.0 >= 32639.5 ? 1 : 0));
+}
+
+// requantise the band blocks of the fp64 integers D to codes q (other blocks
+// 0); exponent and non-zero flag through refs
+template <int NB>
+__device__ __forceinline__ void requant(const AccD<NB>& D, AccI<NB>& q, int lo, int hi, int e_in,
+                                        int& e_out, bool& nz) {
+  int m = 0;
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) m = max(m, __double2hiint(fabs(D.a[bidx(I, J)][v])));
+  const int amax_hi = wave_max(m);
+  const int s = shift_for_hi(amax_hi);
+  const double sc = ldexp(1.0, -s);
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 r = zero_i4();
+      if (blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) r[v] = (int)rint(D.a[bidx(I, J)][v] * sc);
+      q.a[bidx(I, J)] = r;
+    }
+  nz = amax_hi > 0;
+  e_out = nz ? e_in + s : 0;
+}
+// the same for a matrix of codes (|q| <= 32639: never shifted)
+template <int NB>
+__device__ __forceinline__ void requant_codes(const AccI<NB>& q, int lo, int hi, int e_in,
+                                              int& e_out, bool& nz) {
+  nz = amax_of(q, lo, hi) > 0;
+  e_out = nz ? e_in : 0;
+}
+
+// exact running fp64 sum over the band [lo, hi] (the union of its terms')
+template <int NB> struct RunSum {
+  AccD<NB> acc;
+  int e;
+  bool any;
+  int lo, hi;
+};
+template <int NB>
+__device__ __forceinline__ void rs_init(RunSum<NB>& R, int lo, int hi) {
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b) R.acc.a[b] = f64x4{0.0, 0.0, 0.0, 0.0};
+  R.e = 0;
+  R.any = false;
+  R.lo = lo;
+  R.hi = hi;
+}
+template <int NB>
+__device__ __forceinline__ f64x4 as_f64(const AccI<NB>& t, int b) {
+  return __builtin_convertvector(t.a[b], f64x4);
+}
+template <int NB>
+__device__ __forceinline__ f64x4 as_f64(const AccD<NB>& t, int b) {
+  return t.a[b];
+}
+// add the term t (codes or fp64 integers; band [tlo, thi] inside the sum's)
+// of exponent et, |t| < 2^bits
+template <int NB, typename Term>
+__device__ __forceinline__ void rs_add(RunSum<NB>& R, const Term& t, int tlo, int thi, int et,
+                                       int bits, bool present, bool negate = false) {
+  if (!present) return;
+  const int top = et + bits - kAlignBits;
+  if (!R.any) {
+    R.e = top;
+    R.any = true;
+  } else if (top > R.e) {
+    const double sc = ldexp(1.0, R.e - top);
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        if (blk_nz(I - J, R.lo, R.hi))
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            R.acc.a[bidx(I, J)][v] = rint(R.acc.a[bidx(I, J)][v] * sc);
+    R.e = top;
+  }
+  // a wave-uniform shift: exact scaling when it is >= 0, else rounded in
+  const int sh = et - R.e;
+  const double sc = negate ? -ldexp(1.0, sh) : ldexp(1.0, sh);
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, tlo, thi)) {
+        const f64x4 x = as_f64<NB>(t, bidx(I, J));
+        if (sh >= 0) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            R.acc.a[bidx(I, J)][v] = __builtin_fma(x[v], sc, R.acc.a[bidx(I, J)][v]);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) R.acc.a[bidx(I, J)][v] += rint(x[v] * sc);
+        }
+      }
+}
+
+template <int NB>
+__device__ __forceinline__ void rs_finish(const RunSum<NB>& R, AccI<NB>& q, int& e, bool& nz) {
+  requant(R.acc, q, R.lo, R.hi, R.any ? R.e : 0, e, nz);
+}
+
+// ---------------------------------------------------------------------------
+
+// The integer inverse of one tile from Lm = -A (codes, strictly lower, row
+// form) with exponent eL; returns the strict part of T_hat as codes Tr (row
+// form) and its exponent eTo.  NC, SC >= 0 fix N and S at compile time; -1
+// takes them from Nrt, Srt.
+template <int NB, int NC = -1, int SC = -1>
+__device__ __forceinline__ void engine_i16(const AccI<NB>& Lr, int eL, int Nrt, int Srt,
+                                           AccI<NB>& Tr, int& eTo) {
+  constexpr int C = 16 * NB;
+  constexpr int ACCB = 30 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |product| < C * 2^30
+  constexpr int QB = 15;                                      // |code| < 2^15
+  const int N = NC >= 0 ? NC : Nrt;
+  const int S = SC >= 0 ? SC : Srt;
+  RowQ<NB> Iq;
+  ColQ<NB> Ic;
+  eye_quads(Iq, Ic);
+
+  const bool nzL = amax_of(Lr, 1, C - 1) > 0;
+  RowL<NB> LRq;
+  to_rowl(LRq, Lr, 1, C - 1);
+  ColL<NB> LCq;
+  row_to_col<NB>(LCq, nullptr, LRq, Ic, 1, C - 1);
+
+  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm) (band n..N), row form
+  RunSum<NB> ns;
+  rs_init(ns, 1, N);
+  if (N >= 1) {
+    AccI<NB> B = Lr;
+    band_i<NB, false>(B, 1, N);
+    int eB;
+    bool nzB;
+    requant_codes(B, 1, N, eL, eB, nzB);
+    rs_add(ns, B, 1, N, eB, QB, nzB);
+    RowL<NB> Bq;
+    to_rowl(Bq, B, 1, N);
+    auto power = [&](int n) {
+      AccD<NB> D;
+      mml<NB, true>(D, Bq, LCq, n, N);
+      band_blocks<NB, false>(D.a, n, N);
+      AccI<NB> q;
+      requant(D, q, n, N, eB + eL, eB, nzB);
+      rs_add(ns, q, n, N, eB, QB, nzB);
+      to_rowl(Bq, q, n, N);
+    };
+    if constexpr (NC >= 0) {
+#pragma unroll
+      for (int n = 2; n <= NC; ++n) power(n);
+    } else {
+      for (int n = 2; n <= N; ++n) power(n);
+    }
+  }
+  AccI<NB> N0r;
+  int eN0;
+  bool nzN0;
+  rs_finish(ns, N0r, eN0, nzN0);
+  RowL<NB> N0q;
+  to_rowl(N0q, N0r, 1, N);
+  ColL<NB> N0c;
+  row_to_col<NB>(N0c, nullptr, N0q, Ic, 1, N);
+
+  // ---- E = Lm + Lm N0 - N0 (row form), band 1..N zeroed
+  RowL<NB> ERq;
+  ColL<NB> ECq;
+  AccI<NB> Ecol;
+  int eE;
+  bool nzE;
+  {
+    AccD<NB> LN;
+    mml<NB, true>(LN, LRq, N0c, 2, C - 1);
+    RunSum<NB> es;
+    rs_init(es, 1, C - 1);
+    rs_add(es, Lr, 1, C - 1, eL, QB, nzL);
+    rs_add(es, LN, 2, C - 1, eL + eN0, ACCB, nzL && nzN0);
+    rs_add(es, N0r, 1, N, eN0, QB, nzN0, true);
+    band_blocks<NB, false>(es.acc.a, N + 1, C - 1);
+    es.lo = N + 1;
+    AccI<NB> Er;
+    rs_finish(es, Er, eE, nzE);
+    to_rowl(ERq, Er, N + 1, C - 1);
+    row_to_col<NB>(ECq, &Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
+  }
+
+  // ---- residual powers P_s = E P_{s-1} (column form, band s(N+1)..), Gs = sum
+  RunSum<NB> gs;
+  rs_init(gs, N + 1, C - 1);
+  if (S >= 1) {
+    rs_add(gs, Ecol, N + 1, C - 1, eE, QB, nzE);
+    ColL<NB> Pq = ECq;
+    int eP = eE;
+    bool nzP = nzE;
+    auto chain = [&](int s) {
+      const int lo = s * (N + 1);
+      AccD<NB> D;
+      mml<NB, false>(D, ERq, Pq, lo, C - 1);
+      AccI<NB> q;
+      requant(D, q, lo, C - 1, eE + eP, eP, nzP);
+      rs_add(gs, q, lo, C - 1, eP, QB, nzP);
+      to_coll(Pq, q, lo, C - 1);
+    };
+    if constexpr (SC >= 0) {
+#pragma unroll
+      for (int s = 2; s <= SC; ++s) chain(s);
+    } else {
+      for (int s = 2; s <= S; ++s) chain(s);
+    }
+  }
+  AccI<NB> Gc;
+  int eG;
+  bool nzG;
+  rs_finish(gs, Gc, eG, nzG);
+  ColL<NB> GCq;
+  to_coll(GCq, Gc, N + 1, C - 1);
+  AccI<NB> Gr;
+  col_to_row<NB>(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
+
+  // ---- T = N0 + Gs + N0 Gs (row form), strict part
+  bool nzT;
+  {
+    AccD<NB> NG;
+    mml<NB, true>(NG, N0q, GCq, N + 2, C - 1);
+    RunSum<NB> ts;
+    rs_init(ts, 1, C - 1);
+    rs_add(ts, N0r, 1, N, eN0, QB, nzN0);
+    rs_add(ts, Gr, N + 1, C - 1, eG, QB, nzG);
+    rs_add(ts, NG, N + 2, C - 1, eN0 + eG, ACCB, nzN0 && nzG);
+    band_blocks<NB, false>(ts.acc.a, 1, C - 1);
+    rs_finish(ts, Tr, eTo, nzT);
+  }
+}
+
+// four int16 <-> two dwords
+__device__ __forceinline__ int2 pack4_16(i32x4 x) {
+  return int2{(int)((uint32_t)(x[0] & 0xffff) | ((uint32_t)x[1] << 16)),
+              (int)((uint32_t)(x[2] & 0xffff) | ((uint32_t)x[3] << 16))};
+}
+__device__ __forceinline__ i32x4 unpack4_16(int2 w) {
+  return i32x4{(int)(int16_t)(w.x & 0xffff), w.x >> 16, (int)(int16_t)(w.y & 0xffff), w.y >> 16};
+}
+
+// Tq (codes, zero on and above the diagonal), eT and optionally
+// Tdeq = I + Tq 2^eT for tile `tile`
+template <int NB>
+__device__ __forceinline__ void store_i16(const AccI<NB>& Tr, int eTo, int16_t* __restrict__ Tq,
+                                          int32_t* __restrict__ eT, float* __restrict__ Tdeq,
+                                          int64_t tile) {
+  constexpr int C = 16 * NB;
+  const int g = lane_g(), c = lane_c();
+  int16_t* t = Tq + tile * (C * C);
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J < NB; ++J)
+      *(int2*)(t + (I * 16 + c) * C + J * 16 + 4 * g) =
+          J <= I ? pack4_16(Tr.a[bidx(I, J)]) : int2{0, 0};
+  if (lane_id() == 0) eT[tile] = eTo;
+  if (Tdeq) {
+    float* td = Tdeq + tile * (C * C);
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J < NB; ++J) {
+        f32x4 x = zero4();
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int d = 16 * (I - J) + c - 4 * g - v;
+          if (J <= I && d > 0) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], eTo);
+          if (d == 0) x[v] = 1.f;
+        }
+        *(f32x4*)(td + (I * 16 + c) * C + J * 16 + 4 * g) = x;
+      }
+  }
+}
+
+template <int NB, int NC = -1, int SC = -1>
+__global__ __launch_bounds__(64) void k_neumann_i16(const int16_t* __restrict__ Aq,
+                                                    const int32_t* __restrict__ eA,
+                                                    int16_t* __restrict__ Tq,
+                                                    int32_t* __restrict__ eT,
+                                                    float* __restrict__ Tdeq, int Nrt, int Srt) {
+  constexpr int C = 16 * NB;
+  const int64_t tile = blockIdx.x;
+  const int g = lane_g(), c = lane_c();
+  const int16_t* a = Aq + tile * (C * C);
+  // ---- Lm = -A (row form), strictly lower
+  AccI<NB> Lr;
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 x = unpack4_16(*(const int2*)(a + (I * 16 + c) * C + J * 16 + 4 * g));
+#pragma unroll
+      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
+      Lr.a[bidx(I, J)] = x;
+    }
+  const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
+  AccI<NB> Tr;
+  int eTo;
+  engine_i16<NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+  store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, tile);
+}
+
+// e = the smallest integer with amax / 2^e <= 32639 (frexp: amax = m 2^p
+// with m in [0.5, 1) gives amax / 2^(p - 15) = 32768 m), 0 for amax = 0
+__device__ __forceinline__ int quant_exp(float amax) {
+  int e = 0;
+  if (amax > 0.f) {
+    int p;
+    const float mant = frexpf(amax, &p);
+    e = p - 15 + (mant * 32768.f > 32639.f ? 1 : 0);
+  }
+  return e;
+}
+
+// The whole INT16 path for one chunk in one wave: A in fp32 from K, beta, g
+// (the values gdn_build_A writes), quantised in registers, then the integer
+// inverse.
+template <int NB, int DK, typename F, typename TK, int NC = -1, int SC = -1>
+__global__ __launch_bounds__(64) void k_inverse_i16_fused(const TK* __restrict__ K,
+                                                          const float* __restrict__ beta,
+                                                          const float* __restrict__ g,
+                                                          int16_t* __restrict__ Tq,
+                                                          int32_t* __restrict__ eT,
+                                                          float* __restrict__ Tdeq, int L, int H,
+                                                          int Nrt, int Srt) {
+  __shared__ float sb[16 * NB], sg[16 * NB];
+  const Chunk ch(blockIdx.x, L, H, 16 * NB);
+  Acc<NB> G;
+  build_A_rows<NB, DK, F>(K, beta, g, ch, L, H, sb, sg, G);
+  float m = 0.f;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) m = fmaxf(m, fabsf(G.a[b][v]));
+  const float amax =
+      __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
+  const int e = quant_exp(amax);
+  AccI<NB> Lr;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
+  AccI<NB> Tr;
+  int eTo;
+  engine_i16<NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
+  store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
+}
+
+// quantiser: e = smallest integer with amax / 2^e <= 32639, q = rne(x / 2^e)
+template <int C>
+__global__ __launch_bounds__(64) void k_quantize_i16(const float* __restrict__ A,
+                                                     int16_t* __restrict__ Aq,
+                                                     int32_t* __restrict__ eA) {
+  constexpr int PER = C * C / 64 / 4;  // float4 per lane
+  const int64_t tile = blockIdx.x;
+  const float* a = A + tile * (C * C);
+  const int l = lane_id();
+  f32x4 x[PER];
+  float m = 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = (k * 64 + l) * 4;
+    x[k] = *(const f32x4*)(a + idx);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = (idx + v) / C, j = (idx + v) % C;
+      if (i <= j) x[k][v] = 0.f;
+      m = fmaxf(m, fabsf(x[k][v]));
+    }
+  }
+  const float amax =
+      __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
+  const int e = quant_exp(amax);
+  int16_t* q = Aq + tile * (C * C);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    i32x4 r;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) r[v] = (int)rintf(ldexpf(x[k][v], -e));
+    *(int2*)(q + (k * 64 + l) * 4) = pack4_16(r);
+  }
+  if (l == 0) eA[tile] = e;
+}
+
+}  // namespace i16
+
+hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n, int C,
+                               hipStream_t st) {
+  switch (C) {
+    case 16:
+      hipLaunchKernelGGL((i16::k_quantize_i16<16>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+    case 32:
+      hipLaunchKernelGGL((i16::k_quantize_i16<32>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+    case 64:
+      hipLaunchKernelGGL((i16::k_quantize_i16<64>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+  }
+  return hipErrorNotSupported;
+}
+
+template <int NB, int DN, int DS>
+static hipError_t run_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
+                                  float* Tdeq, int64_t n, int N, int S, hipStream_t st) {
+  if (N == DN && S == DS)
+    hipLaunchKernelGGL((i16::k_neumann_i16<NB, DN, DS>), dim3((unsigned)n), dim3(64), 0, st, Aq,
+                       eA, Tq, eT, Tdeq, N, S);
+  else
+    hipLaunchKernelGGL((i16::k_neumann_i16<NB>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
+                       eT, Tdeq, N, S);
+  return hipGetLastError();
+}
+
+// the default orders (3, 2), (3, 4), (3, 8) run compile-time specialisations
+hipError_t launch_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
+                              float* Tdeq, int64_t n, int C, int N, int S, hipStream_t st) {
+  switch (C) {
+    case 16: return run_neumann_i16<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 32: return run_neumann_i16<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 64: return run_neumann_i16<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+  }
+  return hipErrorNotSupported;
+}
+
+template <int NB, int DN, int DS, typename F, typename TK>
+static hipError_t run_i16_fused(const void* K, const float* beta, const float* g, int16_t* Tq,
+                                int32_t* eT, float* Tdeq, int64_t n, int L, int H, int dk, int N,
+                                int S, hipStream_t st) {
+#define GDN_I16F(DK, NC_, SC_)                                                               \
+  hipLaunchKernelGGL((i16::k_inverse_i16_fused<NB, DK, F, TK, NC_, SC_>), dim3((unsigned)n), \
+                     dim3(64), 0, st, (const TK*)K, beta, g, Tq, eT, Tdeq, L, H, N, S)
+  const bool def = N == DN && S == DS;
+  if (dk == 64) {
+    if (def) GDN_I16F(64, DN, DS); else GDN_I16F(64, -1, -1);
+  } else if (dk == 128) {
+    if (def) GDN_I16F(128, DN, DS); else GDN_I16F(128, -1, -1);
+  } else {
+    return hipErrorNotSupported;
+  }
+#undef GDN_I16F
+  return hipGetLastError();
+}
+
+hipError_t launch_inverse_i16_fused(const void* K, const float* beta, const float* g,
+                                    int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
+                                    int dk, int C, int N, int S, int k_dtype, hipStream_t st) {
+  const int64_t n = (int64_t)B * H * (L / C);
+  if (k_dtype == 1) {
+    switch (C) {
+      case 16: return run_i16_fused<1, 3, 2, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 32: return run_i16_fused<2, 3, 4, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 64: return run_i16_fused<4, 3, 8, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+    }
+  } else if (k_dtype == 0) {
+    switch (C) {
+      case 16: return run_i16_fused<1, 3, 2, f32x4, float>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 32: return run_i16_fused<2, 3, 4, f32x4, float>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+      case 64: return run_i16_fused<4, 3, 8, f32x4, float>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);
+    }
+  }
+  return hipErrorNotSupported;
+}
+
+}  // namespace gdn

@@ -18,118 +18,17 @@
 //     powers are P_s = E P_{s-1}; T = N0 + Gs + N0 Gs.
 // Exponents and "matrix is non-zero" flags are wave-uniform (SGPRs).
 //
-// Fragments: a "quad" holds 16 int8 per lane, four 16 x 16 blocks of 4 bytes:
-// row quad R[I] = blocks (I, 0..3) in row form, column quad Cq[J] = blocks
-// (0..3, J) in column form; one MFMA contracts all four k-blocks (zero blocks
-// where K > I or K < J).  C = 16, 32 use the leading one or two blocks.
+// Operands are the int8 quad fragments of intq.hpp.
 #include "chunk.hpp"
+#include "intq.hpp"
 #include "launch.hpp"
-
-// wave reductions of the ROCm device library
-extern "C" __device__ __attribute__((const)) int __ockl_wfred_max_i32(int);
-extern "C" __device__ __attribute__((const)) float __ockl_wfred_max_f32(float);
 
 namespace gdn {
 namespace i8 {
 
+using namespace iq;
+
 constexpr int kAlignBits = 23;
-
-struct Quad {
-  i32x4 v;  // dword K = 4 bytes of block K
-};
-
-template <int NB> struct RowQ { Quad r[NB]; };
-template <int NB> struct ColQ { Quad c[NB]; };
-template <int NB> struct AccI { i32x4 a[nlower(NB)]; };
-
-__device__ __forceinline__ i32x4 zero_i4() { return i32x4{0, 0, 0, 0}; }
-
-// 4 int32 in [-128, 127] <-> 4 bytes (value v in byte v)
-__device__ __forceinline__ int pack4(i32x4 x) {
-  return (int)((uint32_t)(x[0] & 0xff) | ((uint32_t)(x[1] & 0xff) << 8) |
-               ((uint32_t)(x[2] & 0xff) << 16) | ((uint32_t)(x[3] & 0xff) << 24));
-}
-__device__ __forceinline__ i32x4 unpack4(int w) {
-  i32x4 r;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) r[v] = (int)(int8_t)(w >> (8 * v));
-  return r;
-}
-
-template <int NB>
-__device__ __forceinline__ i32x4 blki(const AccI<NB>& D, int I, int J) {
-  return (J <= I && I < NB) ? D.a[bidx(I, J)] : zero_i4();
-}
-// Quads from blocks; blocks that cannot meet the band [lo, hi] (structurally
-// zero) are packed as constant zeros.
-template <int NB>
-__device__ __forceinline__ void to_rowq(RowQ<NB>& X, const AccI<NB>& D, int lo = 0,
-                                        int hi = 16 * NB) {
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int K = 0; K < 4; ++K)
-      X.r[I].v[K] = (K <= I && I < NB && blk_nz(I - K, lo, hi)) ? pack4(D.a[bidx(I, K)]) : 0;
-}
-template <int NB>
-__device__ __forceinline__ void to_colq(ColQ<NB>& Y, const AccI<NB>& D, int lo = 0,
-                                        int hi = 16 * NB) {
-#pragma unroll
-  for (int J = 0; J < NB; ++J)
-#pragma unroll
-    for (int K = 0; K < 4; ++K)
-      Y.c[J].v[K] = (K >= J && K < NB && blk_nz(K - J, lo, hi)) ? pack4(D.a[bidx(K, J)]) : 0;
-}
-
-// D = X Y (lower), blocks outside [olo, ohi] set to 0; OUTQ: row-form result.
-template <int NB, bool OUTQ>
-__device__ __forceinline__ void mmi(AccI<NB>& D, const RowQ<NB>& X, const ColQ<NB>& Y, int olo,
-                                    int ohi) {
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      i32x4 acc = zero_i4();
-      if (blk_nz(I - J, olo, ohi))
-        acc = OUTQ ? __builtin_amdgcn_mfma_i32_16x16x64_i8(Y.c[J].v, X.r[I].v, acc, 0, 0, 0)
-                   : __builtin_amdgcn_mfma_i32_16x16x64_i8(X.r[I].v, Y.c[J].v, acc, 0, 0, 0);
-      D.a[bidx(I, J)] = acc;
-    }
-}
-
-// identity as quads (row and column quads coincide)
-template <int NB>
-__device__ __forceinline__ void eye_quads(RowQ<NB>& R, ColQ<NB>& Cq) {
-  AccI<NB> e;
-  const int g = lane_g(), c = lane_c();
-#pragma unroll
-  for (int b = 0; b < nlower(NB); ++b) e.a[b] = zero_i4();
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) e.a[bidx(I, I)][v] = (c == 4 * g + v) ? 1 : 0;
-  to_rowq(R, e);
-  to_colq(Cq, e);
-}
-
-// zero entries outside lo <= i - j <= hi
-template <int NB, bool COLFORM>
-__device__ __forceinline__ void band_i(AccI<NB>& D, int lo, int hi) {
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      if (!blk_nz(I - J, lo, hi)) {
-        D.a[bidx(I, J)] = zero_i4();
-      } else if (!blk_all_in(I - J, lo, hi)) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int d = COLFORM ? dcol(I - J, v) : drow(I - J, v);
-          if (d < lo || d > hi) D.a[bidx(I, J)][v] = 0;
-        }
-      }
-    }
-}
 
 // round-half-even(y / 2^s) for 1 <= s <= 30 and |y| < 2^30 (every value
 // here stays below 2^24)
@@ -141,11 +40,6 @@ __device__ __forceinline__ int rne_sh(int y, int s) {
   if (s <= 0) return y;
   if (s >= 31) return 0;
   return rne_pos(y, s);
-}
-
-// wave-wide maximum (the device library's DPP reduction), as a scalar
-__device__ __forceinline__ int wave_max(int x) {
-  return __builtin_amdgcn_readfirstlane(__ockl_wfred_max_i32(x));
 }
 
 // every entry rounded by a wave-uniform shift s >= 1
@@ -165,19 +59,6 @@ __device__ __forceinline__ void shift_all(AccI<NB>& D, int s) {
 // The helpers below visit only the blocks that can meet a band [lo, hi] of
 // sub-diagonals; every other block of their operand is exactly zero by the
 // structure of the computation, so skipping it changes no result.
-
-template <int NB>
-__device__ __forceinline__ int amax_of(const AccI<NB>& D, int lo, int hi) {
-  int m = 0;
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J)
-      if (blk_nz(I - J, lo, hi))
-#pragma unroll
-        for (int v = 0; v < 4; ++v) m = max(m, abs(D.a[bidx(I, J)][v]));
-  return wave_max(m);
-}
 
 // smallest s >= 0 with rne(amax / 2^s) <= 127
 __device__ __forceinline__ int shift_for(int amax) {

@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 18
+    assert len(names) == 21
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -145,17 +145,22 @@ def test_fused_blockwise_validation():
     assert f(*zero) == OK
 
 
-def test_int8_validation():
-    q = L.gdn_quantize_tiles_i8
+@pytest.mark.parametrize("w", ["i8", "i16"])
+def test_int_validation(w):
+    q = getattr(L, "gdn_quantize_tiles_" + w)
     assert q(P1, BIG, 2 * BIG, 4, 128, None) == SHAPE
     assert q(P1, None, 2 * BIG, 4, 64, None) == NULL
     assert q(P1, P1, 2 * BIG, 4, 64, None) == ALIAS
     assert q(None, None, None, 0, 64, None) == OK
-    n = L.gdn_chunk_inverse_neumann_i8
+    n = getattr(L, "gdn_chunk_inverse_neumann_" + w)
     assert n(P1, P2, BIG, 2 * BIG, None, 4, 64, 64, 8, None) == PARAM
     assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, None) == NULL
     assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
     assert n(None, None, None, None, None, 0, 64, 3, 8, None) == OK
+    if w == "i16":
+        # Tq starting one int8 extent (4 tiles of 64 x 64 bytes) past Aq lies
+        # inside the int16 codes
+        assert n(P1, P2, P1 + 4 * 64 * 64, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
 
 
 def test_blockwise_validation():
@@ -169,8 +174,9 @@ def test_blockwise_validation():
     assert f(None, None, 0, 64, 1, None) == OK
 
 
-def test_int8_fused_validation():
-    f = L.gdn_chunk_inverse_neumann_i8_fused
+@pytest.mark.parametrize("w", ["i8", "i16"])
+def test_int_fused_validation(w):
+    f = getattr(L, "gdn_chunk_inverse_neumann_%s_fused" % w)
     # K, beta, g, Tq, eT, Tdeq, B, L, H, dk, C, N, S, k_dtype, stream
     base = [P1, BIG, 2 * BIG, 3 * BIG, 4 * BIG, None, 1, 256, 2, 128, 64, 3, 8, 1, None]
 
@@ -181,7 +187,7 @@ def test_int8_fused_validation():
                "kdt"].index(k)] = v
         return f(*a)
 
-    assert call(C=128) == SHAPE       # the INT8 path covers C <= 64
+    assert call(C=128) == SHAPE       # the integer paths cover C <= 64
     assert call(dk=96) == SHAPE
     assert call(L=250) == SHAPE       # L % C != 0
     assert call(N=64) == PARAM
