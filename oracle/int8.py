@@ -272,6 +272,65 @@ def neumann_inverse_int8(qA: np.ndarray, eA: np.ndarray, N: int, S: int, spec: S
     return qT, eT, parts
 
 
+def _scale_rne(y: np.ndarray, d: np.ndarray) -> np.ndarray:
+    """round-half-even(y * 2^-d) for integers y and any integer d (d < 0 is
+    an exact left shift)."""
+    y = np.asarray(y, np.int64)
+    d = np.broadcast_to(np.asarray(d, np.int64), y.shape)
+    return np.where(d >= 0, rne_shift(y, np.maximum(d, 0)), y << np.maximum(-d, 0))
+
+
+def fwdsub_inverse_int(qA: np.ndarray, eA: np.ndarray, spec: Spec = SPEC16):
+    """The forward-substitution baseline in integer arithmetic (this
+    library's reading of an INT16 forward substitution: the recurrence of
+    Section 2.2 on codes with one power-of-two exponent per tile, the
+    per-tensor scheme of Appendix G).
+
+    With Lm = -A (codes qL = -qA at eA), row i (i = 1 .. C-1) of the strict
+    part X of (I + A)^-1 is t + t X_{0:i, 0:i} with t = row i of Lm and X's
+    rows 0 .. i-1 already final, i.e. x_ij = -a_ij - sum_{j<k<i} a_ik x_kj.
+    X holds codes qX with one exponent eX per tile, starting at eA.  Per row:
+      * the two terms t (codes at eA, |t| < 2^qbits) and t X (exact products
+        at eA + eX, below C 2^(2 qbits)) are summed by aligned_sum (present:
+        t non-zero; t non-zero and X non-zero);
+      * eX grows by the smallest s >= 0 with rne(max|row| / 2^(eX + s)) <=
+        qmax; when s > 0 every earlier row is rounded to the new exponent
+        (qX = rne(qX / 2^s));
+      * the row's codes are rne(row / 2^eX), one rounding from the sum.
+    Returns (qX codes, strict lower, and eX per tile); T = I + qX 2^eX."""
+    qA = np.asarray(qA, np.int64)
+    eA = np.asarray(eA, np.int64)
+    C = qA.shape[-1]
+    L = -np.tril(qA, -1)
+    X = np.zeros_like(L)
+    eX = eA.copy()
+    accb = _acc_bits(C, spec)
+    for i in range(1, C):
+        t = L[..., i:i + 1, :]
+        P = t @ X
+        nzt = np.any(t != 0, axis=(-1, -2))
+        nzX = np.any(X != 0, axis=(-1, -2))
+        row, es, anyp = aligned_sum([(t, eA, nzt, spec.qbits), (P, eA + eX, nzt & nzX, accb)],
+                                    spec)
+        amax = np.max(np.abs(row), axis=(-1, -2))
+        u = es - eX
+        # start at a shift where amax 2^(u - s) < 2^16, then the smallest that fits
+        bl = np.array([int(v).bit_length() for v in amax.ravel()], np.int64).reshape(amax.shape)
+        s = np.where(amax > 0, np.maximum(0, bl + u - 16), 0)
+        s = np.maximum(0, s - 1)
+        while True:
+            big = (amax > 0) & (_scale_rne(amax, s - u) > spec.qmax)
+            if not np.any(big):
+                break
+            s = s + big.astype(np.int64)
+        X = np.where((s > 0)[..., None, None], _scale_rne(X, s[..., None, None]), X)
+        eX = eX + s
+        codes = _scale_rne(row, (eX - es)[..., None, None])
+        X[..., i, :] = np.where(anyp[..., None], codes[..., 0, :], 0)
+        assert np.all(np.abs(X) <= spec.qmax)
+    return X, eX
+
+
 def neumann_inverse_int16(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
     """neumann_inverse_int8 with 16-bit codes (SPEC16)."""
     return neumann_inverse_int8(qA, eA, N, S, SPEC16)

@@ -404,3 +404,117 @@ def test_int16_limbs_split_every_code():
     hi = (q - lo) >> 8
     assert np.all(hi * 256 + lo == q)
     assert lo.min() >= -128 and lo.max() <= 127 and hi.min() >= -127 and hi.max() <= 127
+
+
+# ---------------------------------------------------------------------------
+# the integer forward-substitution baseline (INT16)
+
+
+def _py_fwdsub(qA, eA, P=PY16):
+    """Second coding of the integer forward substitution: Python integers,
+    loops, the running-sum rule of _py_sum, the growth of the tile exponent
+    searched from 0 upwards."""
+    C = len(qA)
+    q = P[1]
+    bits = 2 * q + (C - 1).bit_length()
+    L = [[-qA[i][j] if i > j else 0 for j in range(C)] for i in range(C)]
+    X = [[0] * C for _ in range(C)]
+    eX = eA
+
+    def scale(y, d):  # rne(y / 2^d), any integer d
+        return _py_rne(y, d) if d >= 0 else y << -d
+
+    for i in range(1, C):
+        t = [L[i][:]]
+        Pm = [[sum(L[i][k] * X[k][j] for k in range(C)) for j in range(C)]]
+        nzt, nzX = _py_nz(t), _py_nz(X)
+        row, es = _py_sum_rows([(t, eA, nzt, q), (Pm, eA + eX, nzt and nzX, bits)], C, P)
+        amax = max(abs(v) for v in row)
+        s = 0
+        while amax > 0 and scale(amax, eX + s - es) > P[0]:
+            s += 1
+        if s:
+            X = [[_py_rne(v, s) for v in r] for r in X]
+            eX += s
+        X[i] = [scale(v, eX - es) for v in row] if nzt else [0] * C
+    return X, eX
+
+
+def _py_sum_rows(terms, C, P):
+    """_py_sum on 1 x C rows."""
+    out = [0] * C
+    es = None
+    for M, e, p, b in terms:
+        if not p:
+            continue
+        top = e + b - P[2]
+        if es is None:
+            es = top
+        elif top > es:
+            out = [_py_rne(v, top - es) for v in out]
+            es = top
+        for j in range(C):
+            v = M[0][j]
+            out[j] += v << (e - es) if e >= es else _py_rne(v, es - e)
+    return out, (0 if es is None else es)
+
+
+@pytest.mark.parametrize("C,src", [(8, "stress"), (16, "stress"), (16, "workload"),
+                                   (16, "minus_ones")])
+def test_int16_fwdsub_matches_independent_coding(C, src):
+    if src == "minus_ones":
+        A = -np.tril(np.ones((2, C, C)), -1)
+        A[1] *= 0.75
+    elif src == "stress":
+        k, b, g, _ = wl.gen_stress_head(L=2 * C, dk=32, C=C, seed=C + 70)
+        A = gdn.tiles_flat(gdn.build_A(k[None, :, None], b[None, :, None], g[None, :, None], C))
+    else:
+        k, b, g, _ = wl.gen_head(wl.workload("int8"), 0, 0, C=C, want_v=False)
+        A = gdn.tiles_flat(gdn.build_A(k[None, :3 * C, None], b[None, :3 * C, None],
+                                       g[None, :3 * C, None], C))
+    qA, eA = qo.quantize(A.astype(np.float32), qo.SPEC16)
+    qX, eX = qo.fwdsub_inverse_int(qA, eA)
+    for t in range(A.shape[0]):
+        Xp, ep = _py_fwdsub(qA[t].tolist(), int(eA[t]))
+        assert qX[t].tolist() == Xp
+        assert int(eX[t]) == ep
+
+
+def test_int16_fwdsub_exact_cases():
+    """All-ones A: the inverse I - Z, no exponent growth.  Minus-ones A at
+    C = 16: the inverse has x_ij = 2^(i-j-1) (up to 2^14), so the tile
+    exponent must grow from -14 to 0, rounding earlier rows each time, and
+    every step stays exact (power-of-two values on the grid)."""
+    C = 64
+    qA, eA = qo.quantize(np.tril(np.ones((1, C, C), np.float32), -1), qo.SPEC16)
+    qX, eX = qo.fwdsub_inverse_int(qA, eA)
+    assert eX[0] == eA[0]
+    assert np.array_equal(qo.dequant_unit(qX, eX)[0], np.eye(C) - np.eye(C, k=-1))
+    C = 16
+    qA, eA = qo.quantize(-np.tril(np.ones((1, C, C), np.float32), -1), qo.SPEC16)
+    qX, eX = qo.fwdsub_inverse_int(qA, eA)
+    d = gdn.subdiag_index(C)
+    want = np.where(d > 0, 2.0 ** np.maximum(d - 1, 0), 0.0) + np.eye(C)
+    assert eA[0] == -14 and eX[0] == 0
+    assert np.array_equal(qo.dequant_unit(qX, eX)[0], want)
+
+
+@pytest.mark.parametrize("src", ["workload", "wide", "stress"])
+def test_int16_fwdsub_close_to_exact_inverse(src):
+    """Against the exact inverse of the float64 A: the error stays a small
+    multiple of the 16-bit quantum of max|X - I| (the input quantisation
+    alone contributes about 2^-16 of it)."""
+    if src == "stress":
+        k, b, g, _ = wl.gen_stress_head(L=256, dk=128, C=64, seed=9)
+    else:
+        k, b, g, _ = wl.gen_head(wl.workload("int8" if src == "wide" else "tiny"), 0, 0,
+                                 want_v=False)
+    A = gdn.tiles_flat(gdn.build_A(k[None, :256, None], b[None, :256, None], g[None, :256, None], 64))
+    X = gdn.forward_substitution_inverse(A)
+    qA, eA = qo.quantize(A.astype(np.float32), qo.SPEC16)
+    qX, eX = qo.fwdsub_inverse_int(qA, eA)
+    scale = np.max(np.abs(X - np.eye(64)), axis=(-1, -2))
+    err = np.max(np.abs(qo.dequant_unit(qX, eX) - X), axis=(-1, -2))
+    assert np.all(err <= 8 * 2.0 ** -15 * scale)
+    d = gdn.subdiag_index(64)
+    assert np.all(qX[:, d <= 0] == 0) and np.all(np.abs(qX) <= 32639) and np.all(eX >= eA)
