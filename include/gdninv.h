@@ -225,6 +225,21 @@ int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t*
                                   int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
                                   int N, int S, void* stream);
 
+/* The forward-substitution baseline in INT16 (the integer counterpart of
+ * gdn_chunk_inverse_fwdsub, beside the integer Neumann inverse): Section
+ * 2.2's recurrence x_ij = -a_ij - sum_{j<k<i} a_ik x_kj run row by row on
+ * 16-bit codes with one power-of-two exponent per tile (the per-tensor
+ * scheme of Appendix G).  Row i is the exact sum of -a_i (codes at eA) and
+ * -a_i X (products at eA + eT), aligned as in
+ * gdn_chunk_inverse_neumann_i16; the tile exponent eT starts at eA and
+ * grows by the smallest shift that fits a new row (earlier rows rounded
+ * half-even to it); the row's codes are one half-even rounding of its sum.
+ * Aq, eA as for gdn_chunk_inverse_neumann_i16 (codes in [-32639, 32639]);
+ * outputs Tq, eT, Tdeq (nullable) likewise.  C in {16, 32, 64}. */
+int gdn_chunk_inverse_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
+                                 int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
+                                 void* stream);
+
 /* INT16 mode in one launch: A in fp32 from K, beta, g (the values
  * gdn_build_A writes with a_dtype GDN_F32), quantised per tile in registers
  * by the rule of gdn_quantize_tiles_i16, then the integer inverse of

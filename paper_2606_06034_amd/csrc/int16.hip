@@ -548,6 +548,102 @@ __global__ __launch_bounds__(64) void k_quantize_i16(const float* __restrict__ A
   if (l == 0) eA[tile] = e;
 }
 
+// ---------------------------------------------------------------------------
+// The forward-substitution baseline on 16-bit codes (Section 2.2's
+// recurrence, one exponent per tile): one lane per column j of X, rows in
+// order.  Row i is the exact aligned sum of t (codes of -A at eA) and t X
+// (products at eA + eX); the tile exponent grows by the smallest shift that
+// fits the row, earlier rows rounded to it; the row's codes are one
+// rounding of the sum.  Row i of A is wave-uniform (scalar loads).  Pairs of
+// products of codes are exact in int32 (|t x| < 2^30) and summed in fp64.
+
+// round-half-even(y / 2^s), s >= 1, |y| <= 32639
+__device__ __forceinline__ int rne_code(int y, int s) {
+  if (s >= 16) return 0;  // |y| / 2^16 < 1/2
+  return (y + (1 << (s - 1)) - 1 + ((y >> s) & 1)) >> s;
+}
+
+// code k of row i of a tile, read as a whole 32-bit word (wave-uniform
+// addresses go through the scalar unit)
+template <int C>
+__device__ __forceinline__ int code_at(const int16_t* __restrict__ a, int i, int k) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(a)[(i * C + k) >> 1];
+  return (k & 1) ? ((int)w >> 16) : (int)(int16_t)(w & 0xffff);
+}
+
+template <int C>
+__global__ __launch_bounds__(64) void k_fwdsub_i16(const int16_t* __restrict__ Aq,
+                                                   const int32_t* __restrict__ eA,
+                                                   int16_t* __restrict__ Tq,
+                                                   int32_t* __restrict__ eT,
+                                                   float* __restrict__ Tdeq) {
+  constexpr int ACCB = 30 + (C == 16 ? 4 : C == 32 ? 5 : 6);  // |t X| < C 2^30
+  const int64_t tile = blockIdx.x;
+  const int16_t* a = Aq + tile * (C * C);
+  const int j = lane_id();
+  const int ea = __builtin_amdgcn_readfirstlane(eA[tile]);
+  int ex = ea;
+  int x[C];  // codes X_kj of this lane's column
+#pragma unroll
+  for (int k = 0; k < C; ++k) x[k] = 0;
+  bool anyX = false;
+#pragma unroll
+  for (int i = 1; i < C; ++i) {
+    const int tj = j < i ? -(int)a[i * C + j] : 0;
+    const bool nzt = __builtin_amdgcn_ballot_w64(tj != 0) != 0;
+    if (!nzt) continue;  // the row stays zero
+    double p = 0.0;
+#pragma unroll
+    for (int k = 1; k < i; k += 2) {
+      int s2 = __mul24(-code_at<C>(a, i, k), x[k]);
+      if (k + 1 < i) s2 += __mul24(-code_at<C>(a, i, k + 1), x[k + 1]);
+      p += (double)s2;
+    }
+    // aligned sum of t (first) and t X
+    int es = ea + 15 - kAlignBits;
+    double acc = (double)tj * 65536.0;  // t 2^(ea - es), ea - es = 16
+    if (anyX) {
+      const int top = ea + ex + ACCB - kAlignBits;
+      if (top > es) {
+        acc = rint(acc * ldexp(1.0, es - top));
+        es = top;
+      }
+      const int sh = ea + ex - es;
+      acc += sh >= 0 ? p * ldexp(1.0, sh) : rint(p * ldexp(1.0, sh));
+    }
+    // grow the tile exponent until the row fits; round the earlier rows
+    const int amax_hi = wave_max(__double2hiint(fabs(acc)));
+    if (amax_hi > 0) {
+      int pe;
+      const double m = frexp(__hiloint2double(amax_hi, 0), &pe);
+      const int s = max(0, pe - 15 + (m * 32768.0 >= 32639.5 ? 1 : 0) - (ex - es));
+      if (s > 0) {
+        int nz = 0;
+#pragma unroll
+        for (int k = 1; k < i; ++k) {
+          x[k] = rne_code(x[k], s);
+          nz |= x[k];
+        }
+        ex += s;
+        anyX = __builtin_amdgcn_ballot_w64(nz != 0) != 0;
+      }
+    }
+    x[i] = (int)rint(acc * ldexp(1.0, es - ex));
+    anyX = anyX || __builtin_amdgcn_ballot_w64(x[i] != 0) != 0;
+  }
+  if (j < C) {
+    int16_t* t = Tq + tile * (C * C);
+#pragma unroll
+    for (int i = 0; i < C; ++i) t[i * C + j] = (int16_t)x[i];
+    if (Tdeq) {
+      float* td = Tdeq + tile * (C * C);
+#pragma unroll
+      for (int i = 0; i < C; ++i) td[i * C + j] = i == j ? 1.f : ldexpf((float)x[i], ex);
+    }
+  }
+  if (j == 0) eT[tile] = ex;
+}
+
 }  // namespace i16
 
 hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n, int C,
@@ -561,6 +657,25 @@ hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t
       return hipGetLastError();
     case 64:
       hipLaunchKernelGGL((i16::k_quantize_i16<64>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
+      return hipGetLastError();
+  }
+  return hipErrorNotSupported;
+}
+
+hipError_t launch_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
+                             float* Tdeq, int64_t n, int C, hipStream_t st) {
+  switch (C) {
+    case 16:
+      hipLaunchKernelGGL((i16::k_fwdsub_i16<16>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
+                         eT, Tdeq);
+      return hipGetLastError();
+    case 32:
+      hipLaunchKernelGGL((i16::k_fwdsub_i16<32>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
+                         eT, Tdeq);
+      return hipGetLastError();
+    case 64:
+      hipLaunchKernelGGL((i16::k_fwdsub_i16<64>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
+                         eT, Tdeq);
       return hipGetLastError();
   }
   return hipErrorNotSupported;

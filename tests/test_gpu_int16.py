@@ -284,3 +284,73 @@ def test_i16_fused_vs_oracle_and_float(C):
     scale = np.max(np.abs(T - np.eye(C)), axis=(-1, -2))
     err = np.max(np.abs(got - T), axis=(-1, -2))
     assert np.all(err <= 16 * 2.0 ** -16 * scale)
+
+
+# ---------------------------------------------------------------------------
+# the forward-substitution baseline on 16-bit codes
+
+
+def check_fwdsub(qA, eA, label):
+    print(f"i16 fwdsub {label} n={qA.shape[0]}", flush=True)
+    qT, eT, Td = [host(t) for t in G.gdn_chunk_inverse_fwdsub_i16(
+        to_dev(qA, torch.int16), to_dev(eA, torch.int32), want_deq=True)]
+    rq, re = oi.fwdsub_inverse_int(qA, eA)
+    bad = np.flatnonzero(np.any(qT.astype(np.int64) != rq, axis=(-1, -2)) |
+                         (eT.astype(np.int64) != re))
+    print(f"  mismatching tiles={bad.size}", flush=True)
+    assert bad.size == 0, (label, bad[:8])
+    assert np.array_equal(Td, oi.dequant_unit(rq, re).astype(np.float32))
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("src", ["workload", "stress", "random_dense", "random_sparse",
+                                 "limb_edges"])
+def test_fwdsub_i16_bit_exact(C, src):
+    if src.startswith("random") or src == "limb_edges":
+        qA, eA = random_codes(32, C, seed={"random_dense": 31, "random_sparse": 32}.get(src, 33),
+                              density=0.08 if src == "random_sparse" else 1.0,
+                              limb_edges=(src == "limb_edges"))
+    else:
+        qA, eA = oi.quantize(f32_tiles(C, stress=(src == "stress")), SPEC)
+    check_fwdsub(qA, eA, f"C={C} {src}")
+
+
+def test_fwdsub_i16_growth_and_edge_tiles():
+    """Tiles whose inverse outgrows A (minus-ones: x_ij = 2^(i-j-1)), so the
+    tile exponent grows row after row; all-max codes; zero and one-entry
+    tiles; a large exponent."""
+    for C in (16, 32, 64):
+        qA = np.zeros((7, C, C), np.int64)
+        eA = np.zeros(7, np.int64)
+        qA[1, C - 1, 0] = 32639
+        eA[1] = -3
+        qA[2, 1, 0] = -32639
+        qA[3] = np.tril(np.full((C, C), 32639), -1)
+        eA[3] = -20
+        qA[4] = np.tril(np.full((C, C), -1), -1)
+        eA[4] = 40
+        qA[5] = np.tril(np.full((C, C), -16384), -1)    # A = -1: x_ij = 2^(i-j-1)
+        eA[5] = -14
+        qA[6] = np.tril(np.full((C, C), -24575), -1)    # A ~ -0.75, growth with rounding
+        eA[6] = -15
+        check_fwdsub(qA, eA, f"C={C} growth/edge")
+        qT, eT = [host(t) for t in G.gdn_chunk_inverse_fwdsub_i16(
+            to_dev(qA[:1], torch.int16), to_dev(eA[:1], torch.int32))]
+        assert np.all(qT == 0) and eT[0] == 0
+
+
+def test_fwdsub_i16_many_tiles_and_accuracy():
+    """Quantiser then integer forward substitution on 131 workload tiles, on
+    the GPU; bit-exact, and within a few 16-bit quanta of the exact
+    inverse."""
+    A = f32_tiles(64, L=131 * 64, H=1)
+    Aq, eA = G.gdn_quantize_tiles_i16(to_dev(A, torch.float32))
+    qT, eT, Td = G.gdn_chunk_inverse_fwdsub_i16(Aq, eA, want_deq=True)
+    rqA, reA = oi.quantize(A, SPEC)
+    rq, re = oi.fwdsub_inverse_int(rqA, reA)
+    assert np.array_equal(host(qT).astype(np.int64), rq)
+    assert np.array_equal(host(eT).astype(np.int64), re)
+    X = gdn.forward_substitution_inverse(A.astype(np.float64))
+    scale = np.max(np.abs(X - np.eye(64)), axis=(-1, -2))
+    err = np.max(np.abs(host(Td).astype(np.float64) - X), axis=(-1, -2))
+    assert np.all(err <= 8 * 2.0 ** -15 * scale)
