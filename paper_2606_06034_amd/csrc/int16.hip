@@ -18,7 +18,7 @@
 // gfx950 has no 16-bit integer MFMA.  32639 = 127 * 256 + 127, so every code
 // splits into two int8 limbs q = 256 h + l (l in [-128, 127], h in
 // [-127, 127]) and a product of codes is four int8 MFMAs over the quad
-// fragments of intq.hpp:
+// fragments of intq.hpp (quads per limb, packed straight from the codes):
 //   X Y = 2^16 Xh Yh + 2^8 (Xh Yl + Xl Yh) + Xl Yl,
 // with 2^8 Xh Yh + (Xh Yl + Xl Yh) exact in int32 (|.| < 2^29) and the sum
 // exact in fp64 (|X Y| < C 2^30 <= 2^36).  Products and running sums are
@@ -45,41 +45,43 @@ template <int NB> struct AccD { f64x4 a[nlower(NB)]; };  // fp64 integers
 template <int NB> struct RowL { RowQ<NB> h, l; };
 template <int NB> struct ColL { ColQ<NB> h, l; };
 
-__device__ __forceinline__ int lo_limb(int x) { return ((x + 128) & 255) - 128; }
+// The limb bytes of a code c = 256 h + l (l in [-128, 127]): l's byte is
+// byte 0 of c, and c + 128 = 256 h + (l + 128) with 0 <= l + 128 <= 255, so
+// h's byte is byte 1 of c + 128.  Four codes of a block give one dword of a
+// quad per limb.
+__device__ __forceinline__ int pack_lo(i32x4 c) {
+  return (int)(((uint32_t)c[0] & 0xffu) | (((uint32_t)c[1] & 0xffu) << 8) |
+               (((uint32_t)c[2] & 0xffu) << 16) | ((uint32_t)c[3] << 24));
+}
+__device__ __forceinline__ int pack_hi(i32x4 c) {
+  const i32x4 u = c + 128;
+  return (int)((((uint32_t)u[0] >> 8) & 0xffu) | ((uint32_t)u[1] & 0xff00u) |
+               (((uint32_t)u[2] & 0xff00u) << 8) | (((uint32_t)u[3] & 0xff00u) << 16));
+}
 
-// limbs of the blocks that can meet [lo, hi] (others zero)
+// limb quads of the blocks that can meet [lo, hi] (others zero), row form
 template <int NB>
-__device__ __forceinline__ void split(const AccI<NB>& D, AccI<NB>& Hi, AccI<NB>& Lo, int lo,
-                                      int hi) {
+__device__ __forceinline__ void to_rowl(RowL<NB>& X, const AccI<NB>& D, int lo, int hi) {
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      i32x4 h = zero_i4(), l = zero_i4();
-      if (blk_nz(I - J, lo, hi))
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int x = D.a[bidx(I, J)][v];
-          l[v] = lo_limb(x);
-          h[v] = (x - l[v]) >> 8;
-        }
-      Hi.a[bidx(I, J)] = h;
-      Lo.a[bidx(I, J)] = l;
+    for (int K = 0; K < 4; ++K) {
+      const bool live = K <= I && I < NB && blk_nz(I - K, lo, hi);
+      X.h.r[I].v[K] = live ? pack_hi(D.a[bidx(I, K)]) : 0;
+      X.l.r[I].v[K] = live ? pack_lo(D.a[bidx(I, K)]) : 0;
     }
 }
-template <int NB>
-__device__ __forceinline__ void to_rowl(RowL<NB>& X, const AccI<NB>& D, int lo, int hi) {
-  AccI<NB> h, l;
-  split(D, h, l, lo, hi);
-  to_rowq(X.h, h, lo, hi);
-  to_rowq(X.l, l, lo, hi);
-}
+// the same in column form
 template <int NB>
 __device__ __forceinline__ void to_coll(ColL<NB>& Y, const AccI<NB>& D, int lo, int hi) {
-  AccI<NB> h, l;
-  split(D, h, l, lo, hi);
-  to_colq(Y.h, h, lo, hi);
-  to_colq(Y.l, l, lo, hi);
+#pragma unroll
+  for (int J = 0; J < NB; ++J)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) {
+      const bool live = K >= J && K < NB && blk_nz(K - J, lo, hi);
+      Y.h.c[J].v[K] = live ? pack_hi(D.a[bidx(K, J)]) : 0;
+      Y.l.c[J].v[K] = live ? pack_lo(D.a[bidx(K, J)]) : 0;
+    }
 }
 
 // D = X Y exactly, blocks outside [olo, ohi] set to 0; OUTQ: row-form result
@@ -156,6 +158,15 @@ __device__ __forceinline__ int shift_for_hi(int amax_hi) {
   return max(0, p - 15 + (m * 32768.0 >= 32639.5 ? 1 : 0));
 }
 
+// round-half-even(x) as int32 for an fp64 x with |x| < 2^31: x + 1.5 2^52
+// lies in [2^52, 2^53), where the fp64 spacing is 1, so the addition (fused
+// with the scaling) rounds x half to even and the low dword of the sum holds
+// the result in two's complement (1.5 2^52 has a zero low dword)
+constexpr double kRoundMagic = 6755399441055744.0;  // 1.5 * 2^52
+__device__ __forceinline__ int rne_scaled(double x, double sc) {
+  return __double2loint(__builtin_fma(x, sc, kRoundMagic));
+}
+
 // requantise the band blocks of the fp64 integers D to codes q (other blocks
 // 0); exponent and non-zero flag through refs
 template <int NB>
@@ -179,7 +190,7 @@ __device__ __forceinline__ void requant(const AccD<NB>& D, AccI<NB>& q, int lo, 
       i32x4 r = zero_i4();
       if (blk_nz(I - J, lo, hi))
 #pragma unroll
-        for (int v = 0; v < 4; ++v) r[v] = (int)rint(D.a[bidx(I, J)][v] * sc);
+        for (int v = 0; v < 4; ++v) r[v] = rne_scaled(D.a[bidx(I, J)][v], sc);
       q.a[bidx(I, J)] = r;
     }
   nz = amax_hi > 0;
