@@ -17,6 +17,11 @@ system padded with tokens that write nothing).
 
 Each chunk is computed on its own m x m matrices with the functions of
 oracle/gdn.py; nothing is padded in the arithmetic.
+
+The layer forward over packed sequences (forward_varlen_recurrent,
+forward_varlen_chunked) runs the gated delta rule of oracle/gdn_forward.py
+on every sequence from its own initial state: the token recurrence, and the
+chunk-wise form on every chunk's m x m system.
 """
 
 from __future__ import annotations
@@ -84,3 +89,78 @@ def wy_varlen(K, V, beta, g, cu_seqlens, C: int,
             tiles[h, n] = np.eye(C)
             tiles[h, n, :m, :m] = X
     return W[None], U[None], tiles
+
+
+# ---------------------------------------------------------------------------
+# the layer forward over packed sequences
+
+
+def varlen_log_decay(g, cu_seqlens, C: int) -> np.ndarray:
+    """Per-token log-decay inc from the within-chunk cumulative sum g over
+    packed sequences (inc_t = g_t - g_{t-1} inside a chunk, g_t at a chunk's
+    first token; chunks start at every sequence start).  g [T, ...]."""
+    g = np.asarray(g, np.float64)
+    inc = np.empty_like(g)
+    for _, t, m in chunk_table(cu_seqlens, C):
+        inc[t] = g[t]
+        inc[t + 1:t + m] = np.diff(g[t:t + m], axis=0)
+    return inc
+
+
+def forward_varlen_recurrent(Q, K, V, beta, g, cu_seqlens, C: int, S0=None, scale: float = 1.0):
+    """Token recurrence of the gated delta rule (oracle/gdn_forward.py's
+    gdn_recurrent) run on every packed sequence on its own, from its own
+    initial state.  Q, K [1, T, H, dk]; V [1, T, H, dv]; beta, g [1, T, H];
+    S0 [nseq, H, dk, dv] or None.  Returns O [1, T, H, dv], S_final
+    [nseq, H, dk, dv]."""
+    Q, K, V = (np.asarray(x, np.float64)[0] for x in (Q, K, V))
+    beta = np.asarray(beta, np.float64)[0]
+    a = np.exp(varlen_log_decay(np.asarray(g, np.float64)[0], cu_seqlens, C))
+    cu = [int(x) for x in cu_seqlens]
+    T_, H, dk = K.shape
+    dv = V.shape[-1]
+    ns = len(cu) - 1
+    Sf = np.zeros((ns, H, dk, dv)) if S0 is None else np.array(S0, np.float64)
+    O = np.zeros((T_, H, dv))
+    for s in range(ns):
+        S = Sf[s].copy()
+        for t in range(cu[s], cu[s + 1]):
+            k, v = K[t], V[t]                      # [H, dk], [H, dv]
+            kS = np.einsum("hk,hkv->hv", k, S)
+            S = a[t, :, None, None] * (S - beta[t, :, None, None] * k[:, :, None] * kS[:, None, :]) \
+                + beta[t, :, None, None] * k[:, :, None] * v[:, None, :]
+            O[t] = scale * np.einsum("hkv,hk->hv", S, Q[t])
+        Sf[s] = S
+    return O[None], Sf
+
+
+def forward_varlen_chunked(Q, K, V, beta, g, cu_seqlens, C: int, S0=None, scale: float = 1.0,
+                           inverse: Callable[[np.ndarray], np.ndarray] =
+                           gdn.forward_substitution_inverse):
+    """Chunk-wise form over packed sequences: every chunk of m <= C tokens
+    on its own m x m system (oracle/gdn_forward.py's gdn_chunked on the
+    chunk's tokens), the state carried through a sequence's chunks in order.
+    `inverse` maps a stack of strictly lower m x m tiles A to (I + A)^-1."""
+    Q, K, V = (np.asarray(x, np.float64)[0] for x in (Q, K, V))
+    beta = np.asarray(beta, np.float64)[0]
+    g = np.asarray(g, np.float64)[0]
+    T_, H, dk = K.shape
+    dv = V.shape[-1]
+    ns = len(cu_seqlens) - 1
+    Sf = np.zeros((ns, H, dk, dv)) if S0 is None else np.array(S0, np.float64)
+    O = np.zeros((T_, H, dv))
+    for s, t, m in chunk_table(cu_seqlens, C):
+        for h in range(H):
+            q, k, v = Q[t:t + m, h], K[t:t + m, h], V[t:t + m, h]
+            b, gg = beta[t:t + m, h], g[t:t + m, h]
+            A = gdn.strict_lower(b[:, None] * (k @ k.T) * np.exp(gg[:, None] - gg[None, :]))
+            X = inverse(A[None])[0]
+            W = X @ ((b * np.exp(gg))[:, None] * k)
+            U = X @ (b[:, None] * v)
+            S = Sf[s, h]
+            Vn = U - W @ S
+            D = np.tril(np.exp(gg[:, None] - gg[None, :]))
+            O[t:t + m, h] = scale * (np.exp(gg)[:, None] * (q @ S) + ((q @ k.T) * D) @ Vn)
+            last = gg[-1]
+            Sf[s, h] = np.exp(last) * S + (np.exp(last - gg)[:, None] * k).T @ Vn
+    return O[None], Sf

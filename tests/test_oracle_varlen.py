@@ -9,14 +9,19 @@
 * padding a partial chunk with tokens that write nothing (beta = 0) gives the
   same inverse with the identity on the padded rows and columns;
 * the chunk table covers every token once, and single-token chunks reduce to
-  W = beta k.
+  W = beta k;
+* the layer forward over packed sequences: its chunk-wise form equals the
+  token recurrence run on every sequence alone (ragged last chunks, empty
+  sequences, one state per sequence), equal lengths reproduce the
+  fixed-length forward, sequences do not interact, and a sequence split at
+  a chunk boundary continues from the first piece's final state.
 """
 
 import numpy as np
 import pytest
 
 import workloads as wl
-from oracle import gdn, varlen
+from oracle import gdn, gdn_forward, varlen
 
 
 def test_chunk_table_covers_tokens_once():
@@ -127,3 +132,69 @@ def test_varlen_generator_layout():
     assert np.allclose(varlen.varlen_cumsum(
         np.concatenate([[g[0, 0, 0]], np.diff(g[0, :5, 0])]), [0, 5], 64), g[0, :5, 0])
     assert g[0, 5 + 64, 0] > g[0, 5 + 63, 0]  # a new chunk starts at token 64 of sequence 2
+
+
+# ---------------------------------------------------------------------------
+# the layer forward over packed sequences
+
+
+def _fwd_inputs(lengths, C, H=2, dk=16, dv=8, seed=0):
+    rng = np.random.default_rng(seed)
+    cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    T = int(cu[-1])
+    z = rng.standard_normal((1, T, H, dk))
+    K = z / np.linalg.norm(z, axis=-1, keepdims=True)
+    Q = rng.standard_normal((1, T, H, dk))
+    V = rng.standard_normal((1, T, H, dv))
+    beta = rng.random((1, T, H))
+    g = varlen.varlen_cumsum(-0.3 * rng.random((T, H)), cu, C)[None]
+    S0 = rng.standard_normal((len(lengths), H, dk, dv))
+    return Q, K, V, beta, g, cu, S0
+
+
+@pytest.mark.parametrize("C", [8, 16])
+def test_forward_varlen_chunked_equals_recurrence(C):
+    """The chunk-wise form over packed sequences (ragged last chunks, empty
+    sequences, a state per sequence) equals the token recurrence run on
+    every sequence alone."""
+    Q, K, V, beta, g, cu, S0 = _fwd_inputs([5, 0, 70, 2 * C, 1, C + 1], C)
+    O1, S1 = varlen.forward_varlen_recurrent(Q, K, V, beta, g, cu, C, S0, 0.5)
+    O2, S2 = varlen.forward_varlen_chunked(Q, K, V, beta, g, cu, C, S0, 0.5)
+    assert np.allclose(O1, O2, rtol=0, atol=1e-12)
+    assert np.allclose(S1, S2, rtol=0, atol=1e-12)
+    assert np.array_equal(S2[1], S0[1])  # the empty sequence keeps its state
+
+
+def test_forward_varlen_equal_lengths_reduce_to_fixed_length():
+    C, B, L = 16, 3, 48
+    w = wl.workload("tiny").with_(B=B, L=L, H=2, dk=16, dv=8, C=C)
+    Q, K, V, beta, g, S0 = wl.gen_forward_inputs(w, C=C)
+    Of, Sf = gdn_forward.gdn_chunked(Q, K, V, beta, g, C, S0, 0.25)
+    pack = lambda x: x.reshape((1, -1) + x.shape[2:])
+    Ov, Sv = varlen.forward_varlen_chunked(pack(Q), pack(K), pack(V), pack(beta), pack(g),
+                                           np.arange(0, B * L + 1, L), C, S0.reshape(B * 2, 16, 8)
+                                           .reshape(B, 2, 16, 8), 0.25)
+    assert np.allclose(Ov, pack(Of), rtol=0, atol=1e-12)
+    assert np.allclose(Sv, Sf, rtol=0, atol=1e-12)
+
+
+def test_forward_varlen_sequences_are_independent_and_split_at_chunks():
+    """Changing one sequence leaves the others' outputs and states alone;
+    running a sequence as two pieces split at a chunk boundary, the second
+    starting from the first's final state, gives the one-piece result."""
+    C = 8
+    Q, K, V, beta, g, cu, S0 = _fwd_inputs([13, 24, 9], C, seed=1)
+    O, S = varlen.forward_varlen_chunked(Q, K, V, beta, g, cu, C, S0)
+    V2 = V.copy()
+    V2[:, cu[1]:cu[2]] *= -3.0
+    O2, S2 = varlen.forward_varlen_chunked(Q, K, V2, beta, g, cu, C, S0)
+    for s in (0, 2):
+        assert np.array_equal(O[:, cu[s]:cu[s + 1]], O2[:, cu[s]:cu[s + 1]])
+        assert np.array_equal(S[s], S2[s])
+    # sequence 1 (24 tokens) as 16 + 8 tokens
+    cut = [0, 13, 29, 37, 46]
+    Oa, Sa = varlen.forward_varlen_chunked(Q, K, V, beta, g, cut, C, np.stack([S0[0], S0[1], S0[1], S0[2]]))
+    Ob, Sb = varlen.forward_varlen_chunked(Q[:, 29:37], K[:, 29:37], V[:, 29:37], beta[:, 29:37],
+                                           g[:, 29:37], [0, 8], C, Sa[1:2])
+    assert np.allclose(Ob, O[:, 29:37], rtol=0, atol=1e-12)
+    assert np.allclose(Sb[0], S[1], rtol=0, atol=1e-12)
