@@ -305,6 +305,26 @@ int gdn_chunk_forward_state(const void* Q, const float* g, const float* S0, void
 int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int dtype,
                                 int64_t* bytes);
 
+/* The layer forward of gdn_chunk_forward over packed variable-length
+ * sequences (the layouts and chunk tables of gdn_chunk_wy_fused_varlen):
+ * every sequence runs the chunk-wise recurrence from its own initial state,
+ * its chunks starting at its first token; a last chunk of m < C tokens is
+ * the m x m system (its rows past m are neither read for output nor
+ * written).  Q, K: [1, T, H, dk]; V, O: [1, T, H, dv] in `dtype`; beta, g:
+ * [1, T, H] fp32 (g the within-chunk cumulative log-decay for this
+ * chunking).  S0, S_final (nullable; S_final may equal S0):
+ * [nseq, H, dk, dv] fp32, the state of every (sequence, head); an empty
+ * sequence keeps its initial state.  workspace: at least the bytes
+ * gdn_chunk_forward_workspace reports for B = 1, L = n_chunks * C.  The
+ * per-chunk launch and the state pass run back to back on `stream`.
+ * C in {16, 32, 64}. */
+int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const float* beta,
+                             const float* g, const float* S0, void* O, float* S_final,
+                             void* workspace, int64_t workspace_bytes,
+                             const int32_t* cu_seqlens, const int32_t* chunk_offsets, int nseq,
+                             int n_chunks, int T, int H, int dk, int dv, int C, int N, int S,
+                             int exact, float scale, int dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

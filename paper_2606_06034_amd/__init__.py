@@ -22,6 +22,7 @@ from ._binding import (  # noqa: F401
     gdn_chunk_forward,
     gdn_chunk_forward_prepare,
     gdn_chunk_forward_state,
+    gdn_chunk_forward_varlen,
     gdn_chunk_forward_workspace,
     gdn_chunk_inverse_fwdsub,
     gdn_chunk_inverse_blockwise,

@@ -42,6 +42,9 @@ _SIGS = {
     "gdn_chunk_forward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int,
                           _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_float,
                           _c_int, _vp],
+    "gdn_chunk_forward_varlen": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _vp, _vp,
+                                 _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                 _c_int, _c_int, ctypes.c_float, _c_int, _vp],
     "gdn_chunk_forward_workspace": [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
                                     ctypes.POINTER(_c_i64)],
     "gdn_chunk_wy_fused_varlen": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int,
@@ -518,3 +521,46 @@ def gdn_chunk_wy_fused_varlen(K: torch.Tensor, V: torch.Tensor, beta: torch.Tens
         _dev(doff, "chunk_offsets", torch.int32, nseq + 1), nseq, n_chunks, T, H, dk, dv, C, N, S,
         int(bool(exact)), dt, _stream(stream)))
     return (W, U, Tinv) if Tinv is not None else (W, U)
+
+
+def gdn_chunk_forward_varlen(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                             beta: torch.Tensor, g: torch.Tensor, tables, C: int,
+                             S0: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                             S: Optional[int] = None, exact: bool = False,
+                             scale: Optional[float] = None, want_state: bool = True,
+                             O: Optional[torch.Tensor] = None,
+                             S_final: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None, stream=None):
+    """Layer forward over packed sequences: (O [1, T, H, dv], S_final
+    [nseq, H, dk, dv] fp32 or None); tables = gdn_varlen_tables(cu_seqlens, C).
+    Defaults as gdn_chunk_forward."""
+    dcu, doff, n_chunks = tables
+    B, T, H, dk = K.shape
+    if B != 1:
+        raise ValueError("packed sequences use B = 1")
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    nseq = dcu.numel() - 1
+    if N is None or S is None:
+        dn, ds = gdn_default_order(C) if C in (16, 32, 64, 128) else (0, 0)
+        N = dn if N is None else N
+        S = ds if S is None else S
+    scale = dk ** -0.5 if scale is None else float(scale)
+    tok = T * H
+    O = torch.empty_like(V) if O is None else O
+    if want_state and S_final is None:
+        S_final = torch.empty((nseq, H, dk, dv), dtype=torch.float32, device=K.device)
+    need = gdn_chunk_forward_workspace(1, n_chunks * C, H, dk, dv, C, K.dtype) if n_chunks else 0
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=K.device)
+    sp = _dev(S0, "S0", torch.float32, nseq * H * dk * dv) if S0 is not None else None
+    fp = _dev(S_final, "S_final", torch.float32, nseq * H * dk * dv) if S_final is not None \
+        else None
+    _check("gdn_chunk_forward_varlen", lib.gdn_chunk_forward_varlen(
+        _dev(Q, "Q", K.dtype, tok * dk), _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv),
+        _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok), sp,
+        _dev(O, "O", K.dtype, tok * dv), fp, _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), _dev(dcu, "cu_seqlens", torch.int32),
+        _dev(doff, "chunk_offsets", torch.int32, nseq + 1), nseq, n_chunks, T, H, dk, dv, C, N, S,
+        int(bool(exact)), scale, dt, _stream(stream)))
+    return O, S_final

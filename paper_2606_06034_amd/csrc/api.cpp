@@ -230,6 +230,58 @@ int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, c
                                              exact != 0, (hipStream_t)stream));
 }
 
+int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const float* beta,
+                             const float* g, const float* S0, void* O, float* S_final,
+                             void* workspace, int64_t workspace_bytes,
+                             const int32_t* cu_seqlens, const int32_t* chunk_offsets, int nseq,
+                             int n_chunks, int T, int H, int dk, int dv, int C, int N, int S,
+                             int exact, float scale, int dtype, void* stream) {
+  if (T < 0 || H < 0 || nseq < 0 || n_chunks < 0) return GDN_ERR_SHAPE;
+  if (!valid_C(C) || !valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
+  if (nseq == 0 && n_chunks != 0) return GDN_ERR_SHAPE;
+  if (n_chunks > T || (int64_t)n_chunks * H > kMaxTiles) return GDN_ERR_SHAPE;
+  if ((int64_t)nseq * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
+  if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
+  if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!fdtype(dtype)) return GDN_ERR_DTYPE;
+  if (C == 128) return GDN_ERR_UNSUPPORTED;
+  if (nseq == 0 || H == 0) return GDN_OK;
+  const int64_t es = esize(dtype), tok = (int64_t)T * H;
+  const int64_t n = (int64_t)n_chunks * H;
+  const int64_t need = n * gdn::fwd_workspace_elems(C, dk, dv) * es;
+  if (!cu_seqlens || !chunk_offsets) return GDN_ERR_NULL;
+  if (n > 0) {
+    if (!Q || !K || !V || !beta || !g || !O || !workspace) return GDN_ERR_NULL;
+    if (workspace_bytes < need) return GDN_ERR_WORKSPACE;
+  } else {
+    Q = K = V = nullptr, beta = g = nullptr, O = nullptr, workspace = nullptr;
+  }
+  const void* ptrs[9] = {Q, K, V, beta, g, S0, O, S_final, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned(p)) return GDN_ERR_ALIGN;
+  if ((reinterpret_cast<uintptr_t>(cu_seqlens) & 3) ||
+      (reinterpret_cast<uintptr_t>(chunk_offsets) & 3))
+    return GDN_ERR_ALIGN;
+  const int64_t qb = tok * dk * es, vb = tok * dv * es, bb = tok * 4;
+  const int64_t sb = (int64_t)nseq * H * dk * dv * 4, tb = ((int64_t)nseq + 1) * 4;
+  const void* ins[8] = {Q, K, V, beta, g, S0, cu_seqlens, chunk_offsets};
+  const int64_t inb[8] = {qb, qb, vb, bb, bb, sb, tb, tb};
+  const void* outs[3] = {O, workspace, S_final};
+  const int64_t outb[3] = {vb, need, sb};
+  for (int o = 0; o < 3; ++o) {
+    for (int i = 0; i < 8; ++i) {
+      if (o == 2 && i == 5 && S_final == S0) continue;  // in-place state update
+      if (overlap(outs[o], outb[o], ins[i], inb[i])) return GDN_ERR_ALIAS;
+    }
+    for (int o2 = o + 1; o2 < 3; ++o2)
+      if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return GDN_ERR_ALIAS;
+  }
+  return hip_status(gdn::launch_forward_varlen(Q, K, V, beta, g, S0, O, S_final, workspace,
+                                               cu_seqlens, chunk_offsets, nseq, n_chunks, T, H,
+                                               dk, dv, C, N, S, exact != 0, scale, dtype,
+                                               (hipStream_t)stream));
+}
+
 int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                           void* stream) {
   if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)

@@ -71,6 +71,14 @@ struct Chunk {
   }
 };
 
+// Packed sequences: cu (nseq + 1 token offsets) and off (nseq + 1 chunk
+// offsets) device tables; nullptr for the fixed-length layout.
+struct Packed {
+  const int* cu = nullptr;
+  const int* off = nullptr;
+  int nseq = 0, nchunks = 0;
+};
+
 // beta and g of the chunk into LDS (one wave; C <= 128).  Rows r >= m (past
 // the end of a packed sequence) get beta = 0, which makes them write nothing
 // (A's rows vanish, T is the identity there), and the last row's g.

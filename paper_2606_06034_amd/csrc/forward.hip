@@ -176,15 +176,19 @@ __device__ __forceinline__ void apply_w_fwd(const RowP<NB, F>& TR,
 // ---------------------------------------------------------------------------
 // stage 1
 
+// VARLEN: packed sequences (B = 1, L = T tokens, chunk tables pk); a chunk's
+// rows past its m tokens are read from row m - 1 and carry beta = 0, so W, U
+// and K^T vanish there (T is the identity on them) and the state pass never
+// stores their outputs.
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool EXACT>
+          bool EXACT, bool VARLEN = false>
 __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
                                                   const TIO* __restrict__ K,
                                                   const TIO* __restrict__ V,
                                                   const float* __restrict__ beta,
                                                   const float* __restrict__ g,
                                                   TIO* __restrict__ ws, int64_t n_tiles, int L,
-                                                  int H, int N, int S) {
+                                                  int H, int N, int S, Packed pk) {
   constexpr int C = 16 * NB;
   constexpr int DMAX = DK > DV ? DK : DV;
   // bf16: V, then Q, arrive in LDS by DMA while registers are busy
@@ -192,9 +196,15 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
   using LY = FwdLayout<NB, DK, DV>;
   __shared__ float sb[C], sg[C], sbw[C];
   __shared__ __attribute__((aligned(16))) __bf16 sx[PREF ? NB * (DMAX / 32) * 512 : 8];
-  const Chunk ch(blockIdx.x, L, H, C);
+  Chunk ch;
+  if constexpr (VARLEN)
+    ch = Chunk::packed(blockIdx.x, H, C, L, pk.cu, pk.off, pk.nseq, pk.nchunks);
+  else
+    ch = Chunk(blockIdx.x, L, H, C);
+  const int m = VARLEN ? ch.m : C;
+  if (VARLEN && m <= 0) return;
   const Lane ln = lane_here();
-  load_gates<C>(beta, g, ch, L, H, sb, sg);
+  load_gates<C>(beta, g, ch, L, H, sb, sg, m);
   for (int r = ln.id; r < C; r += 64) sbw[r] = sb[r] * __expf(sg[r]);
   __syncthreads();
   TIO* wf = ws + ch.tile * LY::W;
@@ -204,11 +214,11 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
   const int64_t ldk = (int64_t)H * DK, ldv = (int64_t)H * DV;
 
   Pair<F> kp[NB][DK / 32];
-  load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), ldk);
+  load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), ldk, ln, m);
   auto prefetch_v = [&]() {
     if constexpr (PREF) {
       __builtin_amdgcn_sched_barrier(0);
-      prefetch_rows_lds<NB, DV>((const __bf16*)V + ch.row(0, L, H, DV), ldv, sx);
+      prefetch_rows_lds<NB, DV>((const __bf16*)V + ch.row(0, L, H, DV), ldv, sx, ln, m);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -224,11 +234,11 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
     apply_u_fwd<NB, DV, F>(TR, LdsRows<DV>{sx, ln.id}, uf, ln);
     // Q replaces V in LDS: every read of V above has returned its data
     __builtin_amdgcn_sched_barrier(0);
-    prefetch_rows_lds<NB, DK>((const __bf16*)Q + ch.row(0, L, H, DK), ldk, sx);
+    prefetch_rows_lds<NB, DK>((const __bf16*)Q + ch.row(0, L, H, DK), ldk, sx, ln, m);
     __builtin_amdgcn_sched_barrier(0);
   } else {
     Pair<F> vp[NB][DV / 32];
-    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv);
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv, ln, m);
     apply_u_fwd<NB, DV, F>(TR, RegRows<NB, DV, F>{vp}, uf, ln);
   }
   scale_cols(TR, Tr, sbw);
@@ -247,7 +257,8 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
       if constexpr (PREF)
         qp[I] = LdsRows<DK>{sx, ln.id}(I, q);
       else
-        qp[I] = load_row8<F>(Q + ch.row(I * 16 + ln.c(), L, H, DK) + 32 * q + 8 * ln.g());
+        qp[I] = load_row8<F>(Q + ch.row(min(I * 16 + ln.c(), m - 1), L, H, DK) + 32 * q +
+                             8 * ln.g());
     }
 #pragma unroll
     for (int I = 0; I < NB; ++I)
@@ -298,7 +309,7 @@ struct FwdOps {  // one wave's operands of one chunk
   Pair<F> kt[2][NP];  // K^T pairs of the owned state blocks
   Pair<F> p[2];       // P row pairs (I, p), p <= I / 2
   f32x4 u;            // U block (slice, I), column form
-  float gam;          // gamma of chunk row `lane` (lanes >= C: of row C - 1)
+  float gam;          // gamma of chunk row `lane` (lanes past the chunk's tokens: its last)
 };
 
 // half `hf` (block 2p + hf) of slot p
@@ -309,14 +320,19 @@ __device__ __forceinline__ void slot_store_half(float* s, f32x4 x, int hf, int l
   *(f32x4*)(s + 256 * hf + 4 * l) = x;
 }
 
-template <int NB, int DK, int DV, typename F, typename TIO, int DEPTH>
+// VARLEN: one state per (packed sequence, head); the sequence's chunks in
+// order, their tiles at h * nchunks + chunk; rows of a chunk past its m
+// tokens are read from row m - 1 (Q, g) and not stored (O).  Tables that do
+// not describe chunks of C tokens inside the T tokens and nchunks tiles make
+// the sequence empty (its final state is its initial one).
+template <int NB, int DK, int DV, typename F, typename TIO, int DEPTH, bool VARLEN = false>
 __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
                                                    const TIO* __restrict__ Q,
                                                    const float* __restrict__ g,
                                                    const float* __restrict__ S0,
                                                    TIO* __restrict__ O, float* __restrict__ Sfin,
                                                    int64_t n_tiles, int B, int L, int H,
-                                                   float scale) {
+                                                   float scale, Packed pk) {
   constexpr int C = 16 * NB, NQ = DK / 32, NP = npair(NB), NS = DV / 16;
   // DEPTH: chunks whose operands are in registers at once (a ring of
   // buffers, loads issued DEPTH - 1 chunks ahead)
@@ -324,7 +340,7 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
   using Ops = FwdOps<NB, DK, F>;
   __shared__ __attribute__((aligned(16))) TIO xs[2][NQ * 512];      // state pairs
   __shared__ __attribute__((aligned(16))) TIO xv[2][2 * NP * 512];  // V_new, V_d pairs
-  const int BH = B * H, nc = L / C;
+  const int BH = VARLEN ? pk.nseq * H : B * H;
   // work item -> (head bh = b H + h, slice j); when BH is a multiple of 8 the
   // slices of one head share an XCD (work items are dealt to the 8 XCDs in
   // turn), so the rows of W, K^T, P and Q all of them read meet in one L2
@@ -338,7 +354,22 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
     bh = (int)(x / NS);
     j = (int)(x % NS);
   }
-  const int b = bh / H, h = bh - b * H;
+  const int b = bh / H, h = bh - b * H;  // b: the sequence when VARLEN
+  // this head's chunks: c0 .. c0 + nc - 1, the first at token tokS; len tokens
+  int nc = L / C, c0 = 0, len = L;
+  int64_t tokS = (int64_t)b * L;
+  if constexpr (VARLEN) {
+    const int t0 = pk.cu[b], t1 = pk.cu[b + 1], o0 = pk.off[b], o1 = pk.off[b + 1];
+    len = t1 - t0;
+    nc = o1 - o0;
+    c0 = o0;
+    tokS = t0;
+    const bool ok = t0 >= 0 && len >= 0 && t1 <= L && o0 >= 0 && nc >= 0 && o1 <= pk.nchunks &&
+                    nc == (len + C - 1) / C;
+    if (!ok) nc = 0;
+  }
+  // tokens of chunk ck (C, or fewer in a sequence's last chunk)
+  auto rows_of = [&](int ck) { return VARLEN ? min(C, len - ck * C) : C; };
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
   const int l = ln.id, gq = ln.g(), c = ln.c();
@@ -373,15 +404,20 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
 
   // loads of one chunk's operands in three parts (issued at three points of
   // a step, so no wave stalls on a long burst of loads)
+  auto tile_of = [&](int ck) {
+    return VARLEN ? (int64_t)h * pk.nchunks + c0 + ck : (int64_t)bh * nc + ck;
+  };
   auto load_part = [&](Ops& op, int ck, int part) {
-    const int64_t tile = (int64_t)bh * nc + ck;
-    const int64_t tok0 = (int64_t)b * L + ck * C;
+    const int64_t tile = tile_of(ck);
+    const int64_t tok0 = tokS + (int64_t)ck * C;
+    const int m = rows_of(ck);
     if (part == 0 && rows) {
       const int I = wv;
+      const int r = min(I * 16 + c, m - 1);
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         op.w[q] = slot_load<F>(wsW + tile * LY::W + (I * NQ + q) * 512, l);
-        op.q[q] = load_row8<F>(Q + (tok0 + I * 16 + c) * ldq + (int64_t)h * DK + 32 * q + 8 * gq);
+        op.q[q] = load_row8<F>(Q + (tok0 + r) * ldq + (int64_t)h * DK + 32 * q + 8 * gq);
       }
     }
     if (part == 1 && owner) {
@@ -401,7 +437,7 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
       }
       // the chunk's gates in one load, one row per lane; lanes take the
       // rows they need from each other (ds_bpermute)
-      op.gam = g[(tok0 + min(l, C - 1)) * H + h];
+      op.gam = g[(tok0 + min(l, m - 1)) * H + h];
     }
   };
   auto load = [&](Ops& op, int ck) {
@@ -416,7 +452,7 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
   auto compute = [&](const Ops& op, int ck, Ops& nx, int cknx, auto refill_tag) {
     constexpr bool refill = decltype(refill_tag)::value;
     const int par = ck & 1;
-    const int64_t tok0 = (int64_t)b * L + ck * C;
+    const int64_t tok0 = tokS + (int64_t)ck * C;
     if (owner) slot_store(xs[par] + wv * 512, Pair<F>::make(st[0], st[1]), l);
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (refill) load_part(nx, cknx, 0);
@@ -469,7 +505,8 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (refill) load_part(nx, cknx, 2);
       __builtin_amdgcn_sched_barrier(0);
-      store4(O + (tok0 + I * 16 + c) * ldo + (int64_t)h * DV + ocol, scale * o);
+      if (!VARLEN || I * 16 + c < rows_of(ck))
+        store4(O + (tok0 + I * 16 + c) * ldo + (int64_t)h * DV + ocol, scale * o);
     } else if constexpr (refill) {
       load_part(nx, cknx, 2);
     }
@@ -546,13 +583,21 @@ template <int NB, int DK, int DV, typename F, typename TIO>
 static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, const float* beta,
                                  const float* g, const float* S0, void* O, float* Sfin, void* ws,
                                  int B, int L, int H, int N, int S, bool exact, float scale,
-                                 int phases, hipStream_t st) {
+                                 int phases, hipStream_t st, const Packed& pk) {
   constexpr int DN = FwdOrder<NB>::N, DS = FwdOrder<NB>::S;
-  const int64_t n = (int64_t)B * H * (L / (16 * NB));
-#define GDN_FWD1(SM, NC_, SC_, EX)                                                           \
-  hipLaunchKernelGGL((k_fwd_chunk<NB, DK, DV, F, SM, NC_, SC_, TIO, EX>), dim3((unsigned)n), \
-                     dim3(64), 0, st, (const TIO*)Q, (const TIO*)K, (const TIO*)V, beta, g,  \
-                     (TIO*)ws, n, L, H, N, S)
+  const bool packed = pk.cu != nullptr;
+  const int64_t n = packed ? (int64_t)pk.nchunks * H : (int64_t)B * H * (L / (16 * NB));
+#define GDN_FWD1(SM, NC_, SC_, EX)                                                             \
+  do {                                                                                         \
+    if (packed)                                                                                \
+      hipLaunchKernelGGL((k_fwd_chunk<NB, DK, DV, F, SM, NC_, SC_, TIO, EX, true>),            \
+                         dim3((unsigned)n), dim3(64), 0, st, (const TIO*)Q, (const TIO*)K,     \
+                         (const TIO*)V, beta, g, (TIO*)ws, n, L, H, N, S, pk);                 \
+    else                                                                                       \
+      hipLaunchKernelGGL((k_fwd_chunk<NB, DK, DV, F, SM, NC_, SC_, TIO, EX, false>),           \
+                         dim3((unsigned)n), dim3(64), 0, st, (const TIO*)Q, (const TIO*)K,     \
+                         (const TIO*)V, beta, g, (TIO*)ws, n, L, H, N, S, pk);                 \
+  } while (0)
   if ((phases & 1) && n > 0) {
     if (exact)
       GDN_FWD1(true, 0, 0, true);
@@ -565,11 +610,21 @@ static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, co
   }
 #undef GDN_FWD1
   if (phases & 2) {
-    const unsigned nwork = (unsigned)(B * H * (DV / 16));
-#define GDN_FWD2(D)                                                                        \
-  hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO, D>), dim3(nwork), dim3(256), 0, st, \
-                     (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L, H, scale)
-    if constexpr (sizeof(TIO) != 2) {
+    const unsigned nwork = (unsigned)((packed ? pk.nseq : B) * H * (DV / 16));
+#define GDN_FWD2(D)                                                                            \
+  do {                                                                                         \
+    if (packed)                                                                                \
+      hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO, D, true>), dim3(nwork), dim3(256), 0, \
+                         st, (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L, H,   \
+                         scale, pk);                                                           \
+    else                                                                                       \
+      hipLaunchKernelGGL((k_fwd_state<NB, DK, DV, F, TIO, D, false>), dim3(nwork), dim3(256),  \
+                         0, st, (const TIO*)ws, (const TIO*)Q, g, S0, (TIO*)O, Sfin, n, B, L,  \
+                         H, scale, pk);                                                        \
+  } while (0)
+    if (nwork == 0) {
+      // nothing to do
+    } else if constexpr (sizeof(TIO) != 2) {
       GDN_FWD2(1);  // fp32 operands: twice the registers, no room for a ring
     } else if (nwork <= (unsigned)compute_units()) {
       GDN_FWD2(3);  // one workgroup per CU: the deepest ring
@@ -585,11 +640,12 @@ template <typename F, typename TIO>
 static hipError_t run_forward(const void* Q, const void* K, const void* V, const float* beta,
                               const float* g, const float* S0, void* O, float* Sfin, void* ws,
                               int B, int L, int H, int dk, int dv, int C, int N, int S,
-                              bool exact, float scale, int phases, hipStream_t st) {
-#define GDN_FWD_NB(NB_)                                                                     \
-  GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {                                                     \
+                              bool exact, float scale, int phases, hipStream_t st,
+                              const Packed& pk) {
+#define GDN_FWD_NB(NB_)                                                                      \
+  GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {                                                      \
     return run_forward_nb<NB_, DK, DV, F, TIO>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, N, \
-                                              S, exact, scale, phases, st);                 \
+                                              S, exact, scale, phases, st, pk);              \
   }))
   switch (C) {
     case 16: GDN_FWD_NB(1) break;
@@ -600,17 +656,35 @@ static hipError_t run_forward(const void* Q, const void* K, const void* V, const
   return hipErrorNotSupported;
 }
 
+static hipError_t forward_dtype(const void* Q, const void* K, const void* V, const float* beta,
+                                const float* g, const float* S0, void* O, float* Sfin, void* ws,
+                                int B, int L, int H, int dk, int dv, int C, int N, int S,
+                                bool exact, float scale, int dtype, int phases, hipStream_t st,
+                                const Packed& pk) {
+  if (dtype == 0)
+    return run_forward<f32x4, float>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S,
+                                     exact, scale, phases, st, pk);
+  if (dtype == 1)
+    return run_forward<bf16x4, __bf16>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N,
+                                       S, exact, scale, phases, st, pk);
+  return hipErrorNotSupported;
+}
+
 hipError_t launch_forward(const void* Q, const void* K, const void* V, const float* beta,
                           const float* g, const float* S0, void* O, float* Sfin, void* ws, int B,
                           int L, int H, int dk, int dv, int C, int N, int S, bool exact,
                           float scale, int dtype, int phases, hipStream_t st) {
-  if (dtype == 0)
-    return run_forward<f32x4, float>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S,
-                                     exact, scale, phases, st);
-  if (dtype == 1)
-    return run_forward<bf16x4, __bf16>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N,
-                                       S, exact, scale, phases, st);
-  return hipErrorNotSupported;
+  return forward_dtype(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S, exact, scale,
+                       dtype, phases, st, Packed{});
+}
+
+hipError_t launch_forward_varlen(const void* Q, const void* K, const void* V, const float* beta,
+                                 const float* g, const float* S0, void* O, float* Sfin, void* ws,
+                                 const int* cu, const int* off, int nseq, int nchunks, int Ttok,
+                                 int H, int dk, int dv, int C, int N, int S, bool exact,
+                                 float scale, int dtype, hipStream_t st) {
+  return forward_dtype(Q, K, V, beta, g, S0, O, Sfin, ws, 1, Ttok, H, dk, dv, C, N, S, exact,
+                       scale, dtype, 3, st, Packed{cu, off, nseq, nchunks});
 }
 
 }  // namespace gdn

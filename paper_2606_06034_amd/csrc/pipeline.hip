@@ -456,14 +456,6 @@ template <> struct FusedOrder<1> { static constexpr int N = 3, S = 2; };
 template <> struct FusedOrder<2> { static constexpr int N = 3, S = 4; };
 template <> struct FusedOrder<4> { static constexpr int N = 3, S = 8; };
 
-// Packed sequences for the fused kernel: cu (nseq + 1 token offsets) and off
-// (nseq + 1 chunk offsets) device tables; nullptr for the fixed-length path.
-struct Packed {
-  const int* cu = nullptr;
-  const int* off = nullptr;
-  int nseq = 0, nchunks = 0;
-};
-
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO, bool PREF,
           bool EXACT = false>
 static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,

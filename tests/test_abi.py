@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 22
+    assert len(names) == 23
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -330,3 +330,40 @@ def test_binding_rejects_host_tensors():
         g.gdn_chunk_inverse_neumann(A, 3, 8)
     with pytest.raises(TypeError):
         g.gdn_chunk_inverse_neumann(A.to(torch.float16), 3, 8)
+
+
+def test_forward_varlen_validation():
+    import ctypes
+    f = L.gdn_chunk_forward_varlen
+    need = ctypes.c_int64()
+    assert L.gdn_chunk_forward_workspace(1, 4 * 64, 2, 128, 128, 64, 1, ctypes.byref(need)) == OK
+    # Q, K, V, beta, g, S0, O, S_final, ws, ws_bytes, cu, off, nseq, n_chunks, T, H, dk, dv, C,
+    # N, S, exact, scale, dtype, stream
+    b = [k * BIG for k in range(9)]  # far apart: nothing overlaps unless a case moves it
+    base = [b[1], b[2], b[3], b[4], b[5], None, b[6], None, b[7], need.value, b[8], b[8] + 64, 2,
+            4, 200, 2, 128, 128, 64, 3, 8, 0, 1.0, 1, None]
+    names = ["Q", "K", "V", "beta", "g", "S0", "O", "Sf", "ws", "wsb", "cu", "off", "nseq", "nch",
+             "T", "H", "dk", "dv", "C", "N", "S", "exact", "scale", "dt"]
+
+    def call(**kw):
+        a = list(base)
+        for k, v in kw.items():
+            a[names.index(k)] = v
+        return f(*a)
+
+    assert call(nseq=0) == SHAPE                 # chunks without sequences
+    assert call(nch=300) == SHAPE                # more chunks than tokens
+    assert call(C=48) == SHAPE
+    assert call(C=128) == UNSUP
+    assert call(exact=2) == PARAM
+    assert call(N=64) == PARAM
+    assert call(dt=2) == DTYPE
+    assert call(O=None) == NULL
+    assert call(cu=None) == NULL
+    assert call(wsb=need.value - 1) == WS
+    assert call(cu=b[8] + 2) == ALIGN
+    assert call(O=b[1] + 4096) == ALIAS          # O over Q
+    assert call(ws=b[8] - 16) == ALIAS           # workspace over the tables
+    assert call(Sf=b[6] + 64) == ALIAS           # S_final over O
+    assert call(nseq=0, nch=0) == OK
+    assert call(H=0) == OK
