@@ -21,6 +21,10 @@ output), times its two launches apart and, for context, the inverse alone
 (T_hat and forward substitution) on the same chunks, so the inverse's share
 of the layer can be read off.
 
+--varlen runs the fused path (or, with --path forward, the layer forward)
+over packed sequences of the serving mix: the workload's token count split
+into sequences of log-uniform lengths, chunks restarting at every sequence.
+
 --path int8 runs the low-bit path (default workload "int8": B=4, H=32,
 L=16384, C=64, wide gates) in one launch: build A in fp32 -> per-tile INT8
 quantiser -> integer inverse T_hat(3, 8); the same path as three launches
@@ -119,6 +123,8 @@ def main():
     es = 2 if w.dtype == "bf16" else 4
     n_tiles = w.B * w.H * (w.L // C)
 
+    if a.path == "forward" and a.varlen:
+        return bench_forward_varlen(a, w, C, N, S, G, torch)
     if a.path == "forward":
         return bench_forward(a, w, C, N, S, (N0, S0), G, torch)
     if a.varlen:
@@ -391,6 +397,108 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
     }
     if host is not None:
         out["cpu_baseline"] = cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale)
+    print(json.dumps(out), flush=True)
+
+
+def bench_forward_varlen(a, w, C, N, S, G, torch):
+    """The layer forward over packed sequences (gdn_chunk_forward_varlen) on
+    the serving mix of the workload's token count."""
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    es = 2 if w.dtype == "bf16" else 4
+    lengths = wl.varlen_lengths(w.B * w.L)
+    wv = w.with_(B=1)
+    K, beta, g, V, cu, Q = wl.gen_varlen(wv, lengths, C=C, want_q=True)
+    S0 = np.stack([np.stack([wl.gen_state(wv, s, h) for h in range(w.H)])
+                   for s in range(len(lengths))])
+    T = int(cu[-1])
+    dev = lambda x, t: torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(t)
+    dQ, dK, dV = dev(Q, dt), dev(K, dt), dev(V, dt)
+    db, dg, dS0 = dev(beta, torch.float32), dev(g, torch.float32), dev(S0, torch.float32)
+    tables = G.gdn_varlen_tables(cu, C)
+    n_chunks = tables[2]
+    n_tiles = n_chunks * w.H
+    dO, dSf = torch.empty_like(dV), torch.empty_like(dS0)
+    ws = torch.empty(G.gdn_chunk_forward_workspace(1, n_chunks * C, w.H, w.dk, w.dv, C, dt),
+                     dtype=torch.uint8, device="cuda")
+    scale = w.dk ** -0.5
+    stream = torch.cuda.current_stream()
+    step = lambda: G.gdn_chunk_forward_varlen(dQ, dK, dV, db, dg, tables, C, S0=dS0, N=N, S=S,
+                                              exact=a.exact, scale=scale, O=dO, S_final=dSf,
+                                              workspace=ws)
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(a.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = e0.elapsed_time(e1) / a.steps
+    ms_per_step = wall * 1e3 / a.steps
+    tok = T * w.H
+    ws_b = G.gdn_chunk_forward_workspace(1, n_chunks * C, w.H, w.dk, w.dv, C, dt)
+    layer_bytes = (tok * (2 * w.dk + w.dv) * es + tok * 8 + 2 * ws_b + tok * (w.dk + w.dv) * es
+                   + tok * 4 + 2 * len(lengths) * w.H * w.dk * w.dv * 4)
+    achieved = layer_bytes / (ev_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(n_tiles / (ms_per_step * 1e-3), 1),
+        "unit": "chunk inverses/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name + " serving mix", "tokens": T, "sequences": len(lengths),
+                   "ragged_sequences": int(sum(1 for x in lengths if x % C)), "H": w.H, "C": C,
+                   "dk": w.dk, "dv": w.dv, "N": N, "S": S, "tiles": n_tiles,
+                   "path": "forward varlen",
+                   "inverse": "exact block-wise" if a.exact else f"T_hat({N},{S})",
+                   "parallelism": "none (1 GPU)"},
+        "tokens_per_s": round(T / (ms_per_step * 1e-3), 1),
+        "layer_ms": round(ev_ms, 6),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_fwd_chunk + k_fwd_state (one call)",
+                     "kernel_ms": round(ev_ms, 6), "algorithmic_bytes": layer_bytes},
+    }
+    if not a.no_cpu_baseline:
+        from oracle import gdn, varlen
+        inv = gdn.forward_substitution_inverse if a.exact else \
+            (lambda A: gdn.neumann_inverse(A, N, S))
+        ns, chunks, t_end = 0, 0, 0
+        while ns < len(lengths) and chunks < max(1, a.cpu_sample_tiles // w.H):
+            chunks += -(-lengths[ns] // C)
+            t_end = int(cu[ns + 1])
+            ns += 1
+        sub = lambda x: x[:, :t_end]
+        cu_s = cu[:ns + 1]
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            Or, Sr = varlen.forward_varlen_chunked(sub(Q), sub(K), sub(V), sub(beta), sub(g), cu_s,
+                                                   C, S0[:ns], scale, inv)
+            passes += 1
+            secs = time.perf_counter() - t0
+            if secs >= a.cpu_seconds:
+                break
+        torch.cuda.synchronize()
+        Og = dO[:, :t_end].float().cpu().numpy()
+        Sg = dSf[:ns].cpu().numpy()
+        out["cpu_baseline"] = {
+            "value": round(chunks * w.H * passes / secs, 1), "unit": "chunk inverses/s",
+            "cores": _threads(), "kind": "oracle",
+            "sample": f"the first {ns} sequences ({t_end} tokens, {chunks} chunks per head, "
+                      f"{w.H} heads), {passes} passes of the packed chunk-wise forward in "
+                      f"float64 numpy, {secs:.2f} s",
+            "max_abs_err_gpu_vs_oracle": {"O": float(np.max(np.abs(Og - Or))),
+                                          "S_final": float(np.max(np.abs(Sg - Sr)))}}
     print(json.dumps(out), flush=True)
 
 
