@@ -190,9 +190,10 @@ def main():
         stages = [lambda: G.gdn_build_A(dK, db, dg, C, A=dA32),
                   lambda: quant(dA32, Aq=dAq, eA=deA),
                   lambda: inv(dAq, deA, N, S, Tq=dTq2, eT=deT2)]
-        if a.path == "int16":  # the integer forward-substitution baseline on the same codes
-            dTq3, deT3 = torch.empty_like(dAq), torch.empty_like(deA)
-            stages.append(lambda: G.gdn_chunk_inverse_fwdsub_i16(dAq, deA, Tq=dTq3, eT=deT3))
+        # the integer forward-substitution baseline on the same codes
+        fwd_int = getattr(G, f"gdn_chunk_inverse_fwdsub_{sfx}")
+        dTq3, deT3 = torch.empty_like(dAq), torch.empty_like(deA)
+        stages.append(lambda: fwd_int(dAq, deA, Tq=dTq3, eT=deT3))
         stage_ms = []
         for fn in stages:
             fn()
@@ -284,8 +285,7 @@ def main():
         out["config"]["three_launch_ms"] = {"build_A_f32": round(stage_ms[0], 6),
                                             "quantize": round(stage_ms[1], 6),
                                             "inverse_" + sfx: round(stage_ms[2], 6)}
-        if a.path == "int16":
-            out["config"]["fwdsub_i16_ms"] = round(stage_ms[3], 6)
+        out["config"]["fwdsub_" + sfx + "_ms"] = round(stage_ms[3], 6)
         out["dtype"] = sfx
         if not a.no_cpu_baseline:
             out["cpu_baseline"] = cpu_baseline_int(w, C, N, S, a, (K, beta, g), dTq, deT,
@@ -795,9 +795,9 @@ def cpu_baseline_int(w, C, N, S, a, host_inputs, dTq, deT, torch, G, sfx):
     Tr = oi.dequant_unit(qT, eT)[0]
     X = gdn.forward_substitution_inverse(A.astype(np.float64))[0]
     extra = {}
-    if sfx == "i16":  # accuracy of the integer forward substitution on the same codes
-        qF, eF = oi.fwdsub_inverse_int(qA, eA)
-        extra["fwdsub_i16_oracle"] = float(np.max(np.abs(oi.dequant_unit(qF, eF)[0] - X)))
+    # accuracy of the integer forward substitution on the same codes
+    qF, eF = oi.fwdsub_inverse_int(qA, eA, spec)
+    extra["fwdsub_" + sfx + "_oracle"] = float(np.max(np.abs(oi.dequant_unit(qF, eF)[0] - X)))
     torch.cuda.synchronize()
     Tg = np.stack([oi.dequant_unit(dTq[b, h].cpu().numpy().astype(np.int64),
                                    deT.view(w.B, w.H, nc)[b, h].cpu().numpy().astype(np.int64))

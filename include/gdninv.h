@@ -240,6 +240,13 @@ int gdn_chunk_inverse_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* 
                                  int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
                                  void* stream);
 
+/* The same forward substitution on 8-bit codes (the integer baseline beside
+ * gdn_chunk_inverse_neumann_i8): codes in [-127, 127], sum terms aligned
+ * below 2^23, with the arguments and layouts of gdn_chunk_inverse_neumann_i8
+ * (without N, S). */
+int gdn_chunk_inverse_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                                float* Tdeq, int64_t n_tiles, int C, void* stream);
+
 /* INT16 mode in one launch: A in fp32 from K, beta, g (the values
  * gdn_build_A writes with a_dtype GDN_F32), quantised per tile in registers
  * by the rule of gdn_quantize_tiles_i16, then the integer inverse of

@@ -30,6 +30,7 @@ from ._binding import (  # noqa: F401
     gdn_chunk_inverse_neumann_i8,
     gdn_chunk_inverse_neumann_i8_fused,
     gdn_chunk_inverse_fwdsub_i16,
+    gdn_chunk_inverse_fwdsub_i8,
     gdn_chunk_inverse_neumann_i16,
     gdn_chunk_inverse_neumann_i16_fused,
     gdn_chunk_wy_fused,

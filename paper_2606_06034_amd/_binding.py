@@ -37,6 +37,7 @@ _SIGS = {
     "gdn_chunk_inverse_neumann_i16": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
                                       _vp],
     "gdn_chunk_inverse_fwdsub_i16": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _vp],
+    "gdn_chunk_inverse_fwdsub_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i16_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
                                             _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_chunk_forward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int,
@@ -357,6 +358,26 @@ def gdn_chunk_inverse_fwdsub_i16(Aq: torch.Tensor, eA: torch.Tensor, want_deq: b
     _check("gdn_chunk_inverse_fwdsub_i16", lib.gdn_chunk_inverse_fwdsub_i16(
         _dev(Aq, "Aq", torch.int16), _dev(eA, "eA", torch.int32, n),
         _dev(Tq, "Tq", torch.int16, Aq.numel()), _dev(eT, "eT", torch.int32, n),
+        _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C,
+        _stream(stream)))
+    return (Tq, eT, Td) if Td is not None else (Tq, eT)
+
+
+def gdn_chunk_inverse_fwdsub_i8(Aq: torch.Tensor, eA: torch.Tensor, want_deq: bool = False,
+                                Tq: Optional[torch.Tensor] = None,
+                                eT: Optional[torch.Tensor] = None,
+                                Tdeq: Optional[torch.Tensor] = None, stream=None):
+    """(Tq int8, eT int32[, Tdeq fp32]): integer forward substitution,
+    T = I + Tq * 2^eT."""
+    n, C = _tiles(Aq)
+    Tq = torch.empty_like(Aq) if Tq is None else Tq
+    eT = torch.empty_like(eA) if eT is None else eT
+    Td = Tdeq
+    if want_deq and Td is None:
+        Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device)
+    _check("gdn_chunk_inverse_fwdsub_i8", lib.gdn_chunk_inverse_fwdsub_i8(
+        _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32, n),
+        _dev(Tq, "Tq", torch.int8, Aq.numel()), _dev(eT, "eT", torch.int32, n),
         _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C,
         _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)

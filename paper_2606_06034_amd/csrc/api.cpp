@@ -403,6 +403,26 @@ int gdn_chunk_inverse_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* 
       gdn::launch_fwdsub_i16(Aq, eA, Tq, eT, Tdeq, n_tiles, C, (hipStream_t)stream));
 }
 
+int gdn_chunk_inverse_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                                float* Tdeq, int64_t n_tiles, int C, void* stream) {
+  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+    return GDN_ERR_SHAPE;
+  if (n_tiles == 0) return GDN_OK;
+  if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
+  if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
+    return GDN_ERR_ALIGN;
+  const int64_t qb = n_tiles * C * C, eb = n_tiles * 4, db = n_tiles * C * C * 4;
+  const void* ins[2] = {Aq, eA};
+  const int64_t inb[2] = {qb, eb};
+  for (int i = 0; i < 2; ++i)
+    if (overlap(Tq, qb, ins[i], inb[i]) || overlap(eT, eb, ins[i], inb[i]) ||
+        overlap(Tdeq, db, ins[i], inb[i]))
+      return GDN_ERR_ALIAS;
+  if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
+    return GDN_ERR_ALIAS;
+  return hip_status(gdn::launch_fwdsub_i8(Aq, eA, Tq, eT, Tdeq, n_tiles, C, (hipStream_t)stream));
+}
+
 int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const float* g,
                                         int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L,
                                         int H, int dk, int C, int N, int S, int k_dtype,

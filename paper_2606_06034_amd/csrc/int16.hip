@@ -560,15 +560,29 @@ __global__ __launch_bounds__(64) void k_quantize_i16(const float* __restrict__ A
 }
 
 // ---------------------------------------------------------------------------
-// The forward-substitution baseline on 16-bit codes (Section 2.2's
-// recurrence, one exponent per tile): one lane per column j of X, rows in
-// order.  Row i is the exact aligned sum of t (codes of -A at eA) and t X
-// (products at eA + eX); the tile exponent grows by the smallest shift that
-// fits the row, earlier rows rounded to it; the row's codes are one
-// rounding of the sum.  Row i of A is wave-uniform (scalar loads).  Pairs of
-// products of codes are exact in int32 (|t x| < 2^30) and summed in fp64.
+// The forward-substitution baseline on integer codes (Section 2.2's
+// recurrence, one exponent per tile), for 16-bit and 8-bit codes: one lane
+// per column j of X, rows in order.  Row i is the exact aligned sum of t
+// (codes of -A at eA) and t X (products at eA + eX); the tile exponent grows
+// by the smallest shift that fits the row, earlier rows rounded to it; the
+// row's codes are one rounding of the sum.  Row i of A is wave-uniform
+// (scalar loads).  Pairs of products of codes are exact in int32
+// (|t x| < 2^30) and summed in fp64.
 
-// round-half-even(y / 2^s), s >= 1, |y| <= 32639
+// code width: bits of |code|, alignment of sum terms, and qmax + 1/2 (the
+// rounding threshold of the exponent growth; 16 significant bits at most,
+// so the high dword of a maximum decides every comparison with it)
+template <typename CODE> struct IntCodes;
+template <> struct IntCodes<int16_t> {
+  static constexpr int qbits = 15, align = 31;
+  static constexpr double qhalf = 32639.5;
+};
+template <> struct IntCodes<int8_t> {
+  static constexpr int qbits = 7, align = 23;
+  static constexpr double qhalf = 127.5;
+};
+
+// round-half-even(y / 2^s), s >= 1, |y| < 2^15
 __device__ __forceinline__ int rne_code(int y, int s) {
   if (s >= 16) return 0;  // |y| / 2^16 < 1/2
   return (y + (1 << (s - 1)) - 1 + ((y >> s) & 1)) >> s;
@@ -581,16 +595,22 @@ __device__ __forceinline__ int code_at(const int16_t* __restrict__ a, int i, int
   const uint32_t w = reinterpret_cast<const uint32_t*>(a)[(i * C + k) >> 1];
   return (k & 1) ? ((int)w >> 16) : (int)(int16_t)(w & 0xffff);
 }
-
 template <int C>
-__global__ __launch_bounds__(64) void k_fwdsub_i16(const int16_t* __restrict__ Aq,
+__device__ __forceinline__ int code_at(const int8_t* __restrict__ a, int i, int k) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(a)[(i * C + k) >> 2];
+  return (int)(int8_t)(w >> (8 * (k & 3)));
+}
+
+template <int C, typename CODE>
+__global__ __launch_bounds__(64) void k_fwdsub_int(const CODE* __restrict__ Aq,
                                                    const int32_t* __restrict__ eA,
-                                                   int16_t* __restrict__ Tq,
+                                                   CODE* __restrict__ Tq,
                                                    int32_t* __restrict__ eT,
                                                    float* __restrict__ Tdeq) {
-  constexpr int ACCB = 30 + (C == 16 ? 4 : C == 32 ? 5 : 6);  // |t X| < C 2^30
+  using Q = IntCodes<CODE>;
+  constexpr int ACCB = 2 * Q::qbits + (C == 16 ? 4 : C == 32 ? 5 : 6);  // |t X| < C 2^(2 qbits)
   const int64_t tile = blockIdx.x;
-  const int16_t* a = Aq + tile * (C * C);
+  const CODE* a = Aq + tile * (C * C);
   const int j = lane_id();
   const int ea = __builtin_amdgcn_readfirstlane(eA[tile]);
   int ex = ea;
@@ -611,10 +631,10 @@ __global__ __launch_bounds__(64) void k_fwdsub_i16(const int16_t* __restrict__ A
       p += (double)s2;
     }
     // aligned sum of t (first) and t X
-    int es = ea + 15 - kAlignBits;
-    double acc = (double)tj * 65536.0;  // t 2^(ea - es), ea - es = 16
+    int es = ea + Q::qbits - Q::align;
+    double acc = (double)tj * (double)(1 << (Q::align - Q::qbits));  // t 2^(ea - es)
     if (anyX) {
-      const int top = ea + ex + ACCB - kAlignBits;
+      const int top = ea + ex + ACCB - Q::align;
       if (top > es) {
         acc = rint(acc * ldexp(1.0, es - top));
         es = top;
@@ -627,7 +647,8 @@ __global__ __launch_bounds__(64) void k_fwdsub_i16(const int16_t* __restrict__ A
     if (amax_hi > 0) {
       int pe;
       const double m = frexp(__hiloint2double(amax_hi, 0), &pe);
-      const int s = max(0, pe - 15 + (m * 32768.0 >= 32639.5 ? 1 : 0) - (ex - es));
+      const int s = max(0, pe - Q::qbits + (m * (double)(1 << Q::qbits) >= Q::qhalf ? 1 : 0) -
+                               (ex - es));
       if (s > 0) {
         int nz = 0;
 #pragma unroll
@@ -643,9 +664,9 @@ __global__ __launch_bounds__(64) void k_fwdsub_i16(const int16_t* __restrict__ A
     anyX = anyX || __builtin_amdgcn_ballot_w64(x[i] != 0) != 0;
   }
   if (j < C) {
-    int16_t* t = Tq + tile * (C * C);
+    CODE* t = Tq + tile * (C * C);
 #pragma unroll
-    for (int i = 0; i < C; ++i) t[i * C + j] = (int16_t)x[i];
+    for (int i = 0; i < C; ++i) t[i * C + j] = (CODE)x[i];
     if (Tdeq) {
       float* td = Tdeq + tile * (C * C);
 #pragma unroll
@@ -673,23 +694,34 @@ hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t
   return hipErrorNotSupported;
 }
 
-hipError_t launch_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
-                             float* Tdeq, int64_t n, int C, hipStream_t st) {
+template <typename CODE>
+static hipError_t run_fwdsub_int(const CODE* Aq, const int32_t* eA, CODE* Tq, int32_t* eT,
+                                 float* Tdeq, int64_t n, int C, hipStream_t st) {
   switch (C) {
     case 16:
-      hipLaunchKernelGGL((i16::k_fwdsub_i16<16>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
-                         eT, Tdeq);
+      hipLaunchKernelGGL((i16::k_fwdsub_int<16, CODE>), dim3((unsigned)n), dim3(64), 0, st, Aq,
+                         eA, Tq, eT, Tdeq);
       return hipGetLastError();
     case 32:
-      hipLaunchKernelGGL((i16::k_fwdsub_i16<32>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
-                         eT, Tdeq);
+      hipLaunchKernelGGL((i16::k_fwdsub_int<32, CODE>), dim3((unsigned)n), dim3(64), 0, st, Aq,
+                         eA, Tq, eT, Tdeq);
       return hipGetLastError();
     case 64:
-      hipLaunchKernelGGL((i16::k_fwdsub_i16<64>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
-                         eT, Tdeq);
+      hipLaunchKernelGGL((i16::k_fwdsub_int<64, CODE>), dim3((unsigned)n), dim3(64), 0, st, Aq,
+                         eA, Tq, eT, Tdeq);
       return hipGetLastError();
   }
   return hipErrorNotSupported;
+}
+
+hipError_t launch_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
+                             float* Tdeq, int64_t n, int C, hipStream_t st) {
+  return run_fwdsub_int<int16_t>(Aq, eA, Tq, eT, Tdeq, n, C, st);
+}
+
+hipError_t launch_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                            float* Tdeq, int64_t n, int C, hipStream_t st) {
+  return run_fwdsub_int<int8_t>(Aq, eA, Tq, eT, Tdeq, n, C, st);
 }
 
 template <int NB, int DN, int DS>

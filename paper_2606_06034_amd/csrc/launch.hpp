@@ -68,6 +68,8 @@ hipError_t launch_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
                               float* Tdeq, int64_t n_tiles, int C, int N, int S, hipStream_t st);
 hipError_t launch_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
                              float* Tdeq, int64_t n_tiles, int C, hipStream_t st);
+hipError_t launch_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
+                            float* Tdeq, int64_t n_tiles, int C, hipStream_t st);
 hipError_t launch_inverse_i16_fused(const void* K, const float* beta, const float* g,
                                     int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                     int dk, int C, int N, int S, int k_dtype, hipStream_t st);

@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 23
+    assert len(names) == 24
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -174,12 +174,13 @@ def test_blockwise_validation():
     assert f(None, None, 0, 64, 1, None) == OK
 
 
-def test_fwdsub_i16_validation():
-    f = L.gdn_chunk_inverse_fwdsub_i16
+@pytest.mark.parametrize("w", ["i8", "i16"])
+def test_fwdsub_int_validation(w):
+    f = getattr(L, "gdn_chunk_inverse_fwdsub_" + w)
     assert f(P1, P2, BIG, 2 * BIG, None, 4, 128, None) == SHAPE
     assert f(P1, P2, BIG, 2 * BIG, None, -1, 64, None) == SHAPE
     assert f(P1, P2, BIG, None, None, 4, 64, None) == NULL
-    assert f(P1, P2, P1 + 4 * 64 * 64, 2 * BIG, None, 4, 64, None) == ALIAS
+    assert f(P1, P2, P1 + 4 * 64 * 64 - 16, 2 * BIG, None, 4, 64, None) == ALIAS
     assert f(P1, P2, BIG, 2 * BIG, BIG + 1024, 4, 64, None) == ALIAS
     assert f(P1, P2, BIG + 2, 2 * BIG, None, 4, 64, None) == ALIGN
     assert f(None, None, None, None, None, 0, 64, None) == OK

@@ -282,3 +282,57 @@ def test_i8_fused_vs_oracle(C):
           f"max diff {diff.max():.3e} = {quanta.max():.1f} quanta", flush=True)
     assert same.mean() >= 0.9
     assert quanta.max() <= 4.0
+
+
+# ---------------------------------------------------------------------------
+# the forward-substitution baseline on 8-bit codes
+
+
+def check_fwdsub(qA, eA, label):
+    print(f"i8 fwdsub {label} n={qA.shape[0]}", flush=True)
+    qT, eT, Td = [host(t) for t in G.gdn_chunk_inverse_fwdsub_i8(
+        to_dev(qA, torch.int8), to_dev(eA, torch.int32), want_deq=True)]
+    rq, re = oi.fwdsub_inverse_int(qA, eA, oi.SPEC8)
+    bad = np.flatnonzero(np.any(qT.astype(np.int64) != rq, axis=(-1, -2)) |
+                         (eT.astype(np.int64) != re))
+    print(f"  mismatching tiles={bad.size}", flush=True)
+    assert bad.size == 0, (label, bad[:8])
+    assert np.array_equal(Td, oi.dequant_unit(rq, re).astype(np.float32))
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("src", ["workload", "stress", "random_dense", "random_sparse"])
+def test_fwdsub_i8_bit_exact(C, src):
+    if src.startswith("random"):
+        qA, eA = random_codes(32, C, seed=41 if src == "random_dense" else 42,
+                              density=1.0 if src == "random_dense" else 0.08)
+    else:
+        qA, eA = oi.quantize(f32_tiles(C, stress=(src == "stress")))
+    check_fwdsub(qA, eA, f"C={C} {src}")
+
+
+def test_fwdsub_i8_growth_and_edge_tiles():
+    for C in (16, 32, 64):
+        qA = np.zeros((6, C, C), np.int64)
+        eA = np.zeros(6, np.int64)
+        qA[1, C - 1, 0] = 127
+        eA[1] = -3
+        qA[2] = np.tril(np.full((C, C), 127), -1)
+        eA[2] = -9
+        qA[3] = np.tril(np.full((C, C), -1), -1)
+        eA[3] = 40
+        qA[4] = np.tril(np.full((C, C), -64), -1)    # A = -1: x_ij = 2^(i-j-1)
+        eA[4] = -6
+        qA[5] = np.tril(np.full((C, C), -95), -1)
+        eA[5] = -7
+        check_fwdsub(qA, eA, f"C={C} growth/edge")
+
+
+def test_fwdsub_i8_chain_from_quantiser():
+    A = f32_tiles(64, L=67 * 64, H=1)
+    Aq, eA = G.gdn_quantize_tiles_i8(to_dev(A, torch.float32))
+    qT, eT = G.gdn_chunk_inverse_fwdsub_i8(Aq, eA)
+    rqA, reA = oi.quantize(A)
+    rq, re = oi.fwdsub_inverse_int(rqA, reA, oi.SPEC8)
+    assert np.array_equal(host(qT).astype(np.int64), rq)
+    assert np.array_equal(host(eT).astype(np.int64), re)

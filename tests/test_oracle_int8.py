@@ -518,3 +518,48 @@ def test_int16_fwdsub_close_to_exact_inverse(src):
     assert np.all(err <= 8 * 2.0 ** -15 * scale)
     d = gdn.subdiag_index(64)
     assert np.all(qX[:, d <= 0] == 0) and np.all(np.abs(qX) <= 32639) and np.all(eX >= eA)
+
+
+@pytest.mark.parametrize("C,src", [(8, "stress"), (16, "stress"), (16, "workload"),
+                                   (8, "minus_ones")])
+def test_int8_fwdsub_matches_independent_coding(C, src):
+    """The integer forward substitution at 8-bit codes (SPEC8) against the
+    second coding with INT8's parameters."""
+    if src == "minus_ones":
+        A = -np.tril(np.ones((2, C, C)), -1)
+        A[1] *= 0.75
+    elif src == "stress":
+        k, b, g, _ = wl.gen_stress_head(L=2 * C, dk=32, C=C, seed=C + 90)
+        A = gdn.tiles_flat(gdn.build_A(k[None, :, None], b[None, :, None], g[None, :, None], C))
+    else:
+        k, b, g, _ = wl.gen_head(wl.workload("int8"), 0, 1, C=C, want_v=False)
+        A = gdn.tiles_flat(gdn.build_A(k[None, :3 * C, None], b[None, :3 * C, None],
+                                       g[None, :3 * C, None], C))
+    qA, eA = qo.quantize(A.astype(np.float32))
+    qX, eX = qo.fwdsub_inverse_int(qA, eA, qo.SPEC8)
+    for t in range(A.shape[0]):
+        Xp, ep = _py_fwdsub(qA[t].tolist(), int(eA[t]), PY8)
+        assert qX[t].tolist() == Xp
+        assert int(eX[t]) == ep
+
+
+def test_int8_fwdsub_exact_cases_and_accuracy():
+    """Minus-ones A at C = 8 (x_ij = 2^(i-j-1) up to 64, the exponent growing
+    from -6 to 0, exact); workload tiles within a few 8-bit quanta of
+    max|X - I|."""
+    C = 8
+    qA, eA = qo.quantize(-np.tril(np.ones((1, C, C), np.float32), -1))
+    qX, eX = qo.fwdsub_inverse_int(qA, eA, qo.SPEC8)
+    d = gdn.subdiag_index(C)
+    assert eA[0] == -6 and eX[0] == 0
+    assert np.array_equal(qo.dequant_unit(qX, eX)[0],
+                          np.where(d > 0, 2.0 ** np.maximum(d - 1, 0), 0.0) + np.eye(C))
+    k, b, g, _ = wl.gen_head(wl.workload("int8"), 0, 0, want_v=False)
+    A = gdn.tiles_flat(gdn.build_A(k[None, :256, None], b[None, :256, None], g[None, :256, None], 64))
+    X = gdn.forward_substitution_inverse(A)
+    qA, eA = qo.quantize(A.astype(np.float32))
+    qX, eX = qo.fwdsub_inverse_int(qA, eA, qo.SPEC8)
+    scale = np.max(np.abs(X - np.eye(64)), axis=(-1, -2))
+    err = np.max(np.abs(qo.dequant_unit(qX, eX) - X), axis=(-1, -2))
+    assert np.all(err <= 8 * 2.0 ** -7 * scale)
+    assert np.all(np.abs(qX) <= 127)
