@@ -277,134 +277,60 @@ __device__ __forceinline__ void rs_finish(const RunSum<NB>& R, AccI<NB>& q, int&
 
 // ---------------------------------------------------------------------------
 
-// The integer inverse of one tile from Lm = -A (codes, strictly lower, row
-// form) with exponent eL; returns the strict part of T_hat as codes Tr (row
-// form) and its exponent eTo.  NC, SC >= 0 fix N and S at compile time; -1
-// takes them from Nrt, Srt.
-template <int NB, int NC = -1, int SC = -1>
-__device__ __forceinline__ void engine_i16(const AccI<NB>& Lr, int eL, int Nrt, int Srt,
-                                           AccI<NB>& Tr, int& eTo) {
-  constexpr int C = 16 * NB;
-  constexpr int ACCB = 30 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |product| < C * 2^30
-  constexpr int QB = 15;                                      // |code| < 2^15
-  const int N = NC >= 0 ? NC : Nrt;
-  const int S = SC >= 0 ? SC : Srt;
-  RowQ<NB> Iq;
-  ColQ<NB> Ic;
-  eye_quads(Iq, Ic);
-
-  const bool nzL = amax_of(Lr, 1, C - 1) > 0;
-  RowL<NB> LRq;
-  to_rowl(LRq, Lr, 1, C - 1);
-  ColL<NB> LCq;
-  row_to_col<NB>(LCq, nullptr, LRq, Ic, 1, C - 1);
-
-  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm) (band n..N), row form
-  RunSum<NB> ns;
-  rs_init(ns, 1, N);
-  if (N >= 1) {
-    AccI<NB> B = Lr;
-    band_i<NB, false>(B, 1, N);
-    int eB;
-    bool nzB;
-    requant_codes(B, 1, N, eL, eB, nzB);
-    rs_add(ns, B, 1, N, eB, QB, nzB);
-    RowL<NB> Bq;
-    to_rowl(Bq, B, 1, N);
-    auto power = [&](int n) {
-      AccD<NB> D;
-      mml<NB, true>(D, Bq, LCq, n, N);
-      band_blocks<NB, false>(D.a, n, N);
-      AccI<NB> q;
-      requant(D, q, n, N, eB + eL, eB, nzB);
-      rs_add(ns, q, n, N, eB, QB, nzB);
-      to_rowl(Bq, q, n, N);
-    };
-    if constexpr (NC >= 0) {
-#pragma unroll
-      for (int n = 2; n <= NC; ++n) power(n);
-    } else {
-      for (int n = 2; n <= N; ++n) power(n);
-    }
+// The INT16 width for the shared integer engine (int_engine of intq.hpp):
+// limb quads, products and running sums as fp64 integers.
+template <int NB> struct I16Ops {
+  using Row = RowL<NB>;
+  using Col = ColL<NB>;
+  using Prod = AccD<NB>;
+  using Sum = RunSum<NB>;
+  static constexpr int kQB = 15;                                      // |code| < 2^15
+  static constexpr int kAccB = 30 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |product| < C 2^30
+  static __device__ __forceinline__ void to_row(Row& X, const AccI<NB>& D, int lo, int hi) {
+    to_rowl(X, D, lo, hi);
   }
-  AccI<NB> N0r;
-  int eN0;
-  bool nzN0;
-  rs_finish(ns, N0r, eN0, nzN0);
-  RowL<NB> N0q;
-  to_rowl(N0q, N0r, 1, N);
-  ColL<NB> N0c;
-  row_to_col<NB>(N0c, nullptr, N0q, Ic, 1, N);
-
-  // ---- E = Lm + Lm N0 - N0 (row form), band 1..N zeroed
-  RowL<NB> ERq;
-  ColL<NB> ECq;
-  AccI<NB> Ecol;
-  int eE;
-  bool nzE;
-  {
-    AccD<NB> LN;
-    mml<NB, true>(LN, LRq, N0c, 2, C - 1);
-    RunSum<NB> es;
-    rs_init(es, 1, C - 1);
-    rs_add(es, Lr, 1, C - 1, eL, QB, nzL);
-    rs_add(es, LN, 2, C - 1, eL + eN0, ACCB, nzL && nzN0);
-    rs_add(es, N0r, 1, N, eN0, QB, nzN0, true);
-    band_blocks<NB, false>(es.acc.a, N + 1, C - 1);
-    es.lo = N + 1;
-    AccI<NB> Er;
-    rs_finish(es, Er, eE, nzE);
-    to_rowl(ERq, Er, N + 1, C - 1);
-    row_to_col<NB>(ECq, &Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
+  static __device__ __forceinline__ void to_col(Col& Y, const AccI<NB>& D, int lo, int hi) {
+    to_coll(Y, D, lo, hi);
   }
-
-  // ---- residual powers P_s = E P_{s-1} (column form, band s(N+1)..), Gs = sum
-  RunSum<NB> gs;
-  rs_init(gs, N + 1, C - 1);
-  if (S >= 1) {
-    rs_add(gs, Ecol, N + 1, C - 1, eE, QB, nzE);
-    ColL<NB> Pq = ECq;
-    int eP = eE;
-    bool nzP = nzE;
-    auto chain = [&](int s) {
-      const int lo = s * (N + 1);
-      AccD<NB> D;
-      mml<NB, false>(D, ERq, Pq, lo, C - 1);
-      AccI<NB> q;
-      requant(D, q, lo, C - 1, eE + eP, eP, nzP);
-      rs_add(gs, q, lo, C - 1, eP, QB, nzP);
-      to_coll(Pq, q, lo, C - 1);
-    };
-    if constexpr (SC >= 0) {
-#pragma unroll
-      for (int s = 2; s <= SC; ++s) chain(s);
-    } else {
-      for (int s = 2; s <= S; ++s) chain(s);
-    }
+  template <bool OUTQ>
+  static __device__ __forceinline__ void mm(Prod& D, const Row& X, const Col& Y, int lo, int hi) {
+    mml<NB, OUTQ>(D, X, Y, lo, hi);
   }
-  AccI<NB> Gc;
-  int eG;
-  bool nzG;
-  rs_finish(gs, Gc, eG, nzG);
-  ColL<NB> GCq;
-  to_coll(GCq, Gc, N + 1, C - 1);
-  AccI<NB> Gr;
-  col_to_row<NB>(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
-
-  // ---- T = N0 + Gs + N0 Gs (row form), strict part
-  bool nzT;
-  {
-    AccD<NB> NG;
-    mml<NB, true>(NG, N0q, GCq, N + 2, C - 1);
-    RunSum<NB> ts;
-    rs_init(ts, 1, C - 1);
-    rs_add(ts, N0r, 1, N, eN0, QB, nzN0);
-    rs_add(ts, Gr, N + 1, C - 1, eG, QB, nzG);
-    rs_add(ts, NG, N + 2, C - 1, eN0 + eG, ACCB, nzN0 && nzG);
-    band_blocks<NB, false>(ts.acc.a, 1, C - 1);
-    rs_finish(ts, Tr, eTo, nzT);
+  static __device__ __forceinline__ void band(Prod& D, int lo, int hi) {
+    band_blocks<NB, false>(D.a, lo, hi);
   }
-}
+  static __device__ __forceinline__ void requant(const Prod& D, AccI<NB>& q, int lo, int hi,
+                                                 int e_in, int& e_out, bool& nz) {
+    i16::requant(D, q, lo, hi, e_in, e_out, nz);
+  }
+  static __device__ __forceinline__ void requant_codes(const AccI<NB>& q, int lo, int hi,
+                                                       int e_in, int& e_out, bool& nz) {
+    i16::requant_codes(q, lo, hi, e_in, e_out, nz);
+  }
+  static __device__ __forceinline__ void row_to_col(Col& Y, AccI<NB>* codes, const Row& X,
+                                                    const ColQ<NB>& Ic, int lo, int hi) {
+    i16::row_to_col<NB>(Y, codes, X, Ic, lo, hi);
+  }
+  static __device__ __forceinline__ void col_to_row(AccI<NB>& D, const RowQ<NB>& Iq,
+                                                    const Col& Y, int lo, int hi) {
+    i16::col_to_row<NB>(D, Iq, Y, lo, hi);
+  }
+  static __device__ __forceinline__ void rs_init(Sum& R, int lo, int hi) {
+    i16::rs_init(R, lo, hi);
+  }
+  template <typename Term>
+  static __device__ __forceinline__ void rs_add(Sum& R, const Term& t, int tlo, int thi, int et,
+                                                int bits, bool present, bool negate = false) {
+    i16::rs_add(R, t, tlo, thi, et, bits, present, negate);
+  }
+  static __device__ __forceinline__ void rs_band(Sum& R, int lo, int hi) {
+    band_blocks<NB, false>(R.acc.a, lo, hi);
+    R.lo = lo;
+  }
+  static __device__ __forceinline__ void rs_finish(const Sum& R, AccI<NB>& q, int& e, bool& nz) {
+    i16::rs_finish(R, q, e, nz);
+  }
+};
 
 // four int16 <-> two dwords
 __device__ __forceinline__ int2 pack4_16(i32x4 x) {
@@ -473,7 +399,7 @@ __global__ __launch_bounds__(64) void k_neumann_i16(const int16_t* __restrict__ 
   const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
   AccI<NB> Tr;
   int eTo;
-  engine_i16<NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+  int_engine<I16Ops, NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
   store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, tile);
 }
 
@@ -519,7 +445,7 @@ __global__ __launch_bounds__(64) void k_inverse_i16_fused(const TK* __restrict__
     for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
   AccI<NB> Tr;
   int eTo;
-  engine_i16<NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
+  int_engine<I16Ops, NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
   store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
 }
 

@@ -158,152 +158,65 @@ __device__ __forceinline__ void rs_finish(RunSum<NB>& R, AccI<NB>& q, int& e, bo
   requant(q, R.lo, R.hi, R.any ? R.e : 0, e, nz);
 }
 
-template <int NB>
-__device__ __forceinline__ void unpack_row(AccI<NB>& D, const RowQ<NB>& X) {
-#pragma unroll
-  for (int I = 0; I < NB; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) D.a[bidx(I, J)] = unpack4(X.r[I].v[J]);
-}
-
 // ---------------------------------------------------------------------------
 
-// The integer inverse of one tile from Lm = -A (codes, strictly lower, row
-// form) with exponent eL; returns the strict part of T_hat as codes Tr (row
-// form) and its exponent eTo.  NC, SC >= 0 fix N and S at compile time
-// (every band and block skip is then resolved by the compiler); -1 takes
-// them from Nrt, Srt.
-template <int NB, int NC = -1, int SC = -1>
-__device__ __forceinline__ void engine_i8(const AccI<NB>& Lr, int eL, int Nrt, int Srt,
-                                          AccI<NB>& Tr, int& eTo) {
-  constexpr int C = 16 * NB;
-  constexpr int ACCB = 14 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |acc| < C * 2^14
-  const int N = NC >= 0 ? NC : Nrt;
-  const int S = SC >= 0 ? SC : Srt;
-  RowQ<NB> Iq;
-  ColQ<NB> Ic;
-  eye_quads(Iq, Ic);
-
-  const bool nzL = amax_of(Lr, 1, C - 1) > 0;
-  RowQ<NB> LRq;
-  to_rowq(LRq, Lr, 1, C - 1);
-  ColQ<NB> LCq;
-  {
+// The INT8 width for the shared integer engine (int_engine of intq.hpp):
+// quads, exact int32 products, int32 running sums.
+template <int NB> struct I8Ops {
+  using Row = RowQ<NB>;
+  using Col = ColQ<NB>;
+  using Prod = AccI<NB>;
+  using Sum = RunSum<NB>;
+  static constexpr int kQB = 7;                                       // |code| < 2^7
+  static constexpr int kAccB = 14 + (NB == 1 ? 4 : NB == 2 ? 5 : 6);  // |product| < C 2^14
+  static __device__ __forceinline__ void to_row(Row& X, const AccI<NB>& D, int lo, int hi) {
+    to_rowq(X, D, lo, hi);
+  }
+  static __device__ __forceinline__ void to_col(Col& Y, const AccI<NB>& D, int lo, int hi) {
+    to_colq(Y, D, lo, hi);
+  }
+  template <bool OUTQ>
+  static __device__ __forceinline__ void mm(Prod& D, const Row& X, const Col& Y, int lo, int hi) {
+    mmi<NB, OUTQ>(D, X, Y, lo, hi);
+  }
+  static __device__ __forceinline__ void band(Prod& D, int lo, int hi) {
+    band_i<NB, false>(D, lo, hi);
+  }
+  // the product is requantised in place and handed on as the codes
+  static __device__ __forceinline__ void requant(Prod& D, AccI<NB>& q, int lo, int hi, int e_in,
+                                                 int& e_out, bool& nz) {
+    i8::requant(D, lo, hi, e_in, e_out, nz);
+    q = D;
+  }
+  static __device__ __forceinline__ void requant_codes(AccI<NB>& q, int lo, int hi, int e_in,
+                                                       int& e_out, bool& nz) {
+    i8::requant(q, lo, hi, e_in, e_out, nz);
+  }
+  static __device__ __forceinline__ void row_to_col(Col& Y, AccI<NB>* codes, const Row& X,
+                                                    const ColQ<NB>& Ic, int lo, int hi) {
     AccI<NB> t;
-    mmi<NB, false>(t, LRq, Ic, 1, C - 1);  // Lm I, column form
-    to_colq(LCq, t, 1, C - 1);
+    mmi<NB, false>(t, X, Ic, lo, hi);
+    to_colq(Y, t, lo, hi);
+    if (codes) *codes = t;
   }
-
-  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm) (band n..N), row form
-  RunSum<NB> ns;
-  rs_init(ns, 1, N);
-  if (N >= 1) {
-    AccI<NB> B = Lr;
-    band_i<NB, false>(B, 1, N);
-    int eB;
-    bool nzB;
-    requant(B, 1, N, eL, eB, nzB);
-    rs_add(ns, B, 1, N, eB, 7, nzB);
-    RowQ<NB> Bq;
-    to_rowq(Bq, B, 1, N);
-    auto power = [&](int n) {
-      AccI<NB> D;
-      mmi<NB, true>(D, Bq, LCq, n, N);
-      band_i<NB, false>(D, n, N);
-      requant(D, n, N, eB + eL, eB, nzB);
-      rs_add(ns, D, n, N, eB, 7, nzB);
-      to_rowq(Bq, D, n, N);
-    };
-    if constexpr (NC >= 0) {
-#pragma unroll
-      for (int n = 2; n <= NC; ++n) power(n);
-    } else {
-      for (int n = 2; n <= N; ++n) power(n);
-    }
+  static __device__ __forceinline__ void col_to_row(AccI<NB>& D, const RowQ<NB>& Iq,
+                                                    const Col& Y, int lo, int hi) {
+    mmi<NB, true>(D, Iq, Y, lo, hi);
   }
-  AccI<NB> N0r;
-  int eN0;
-  bool nzN0;
-  rs_finish(ns, N0r, eN0, nzN0);
-  RowQ<NB> N0q;
-  to_rowq(N0q, N0r, 1, N);
-  ColQ<NB> N0c;
-  {
-    AccI<NB> t;
-    mmi<NB, false>(t, N0q, Ic, 1, N);
-    to_colq(N0c, t, 1, N);
+  static __device__ __forceinline__ void rs_init(Sum& R, int lo, int hi) { i8::rs_init(R, lo, hi); }
+  static __device__ __forceinline__ void rs_add(Sum& R, const AccI<NB>& t, int tlo, int thi,
+                                                int et, int bits, bool present,
+                                                bool negate = false) {
+    i8::rs_add(R, t, tlo, thi, et, bits, present, negate);
   }
-
-  // ---- E = Lm + Lm N0 - N0 (row form), band 1..N zeroed
-  RowQ<NB> ERq;
-  ColQ<NB> ECq;
-  AccI<NB> Ecol;
-  int eE;
-  bool nzE;
-  {
-    AccI<NB> LN;
-    mmi<NB, true>(LN, LRq, N0c, 2, C - 1);
-    RunSum<NB> es;
-    rs_init(es, 1, C - 1);
-    rs_add(es, Lr, 1, C - 1, eL, 7, nzL);
-    rs_add(es, LN, 2, C - 1, eL + eN0, ACCB, nzL && nzN0);
-    rs_add(es, N0r, 1, N, eN0, 7, nzN0, true);
-    band_i<NB, false>(es.acc, N + 1, C - 1);
-    es.lo = N + 1;
-    AccI<NB> Er;
-    rs_finish(es, Er, eE, nzE);
-    to_rowq(ERq, Er, N + 1, C - 1);
-    mmi<NB, false>(Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
-    to_colq(ECq, Ecol, N + 1, C - 1);
+  static __device__ __forceinline__ void rs_band(Sum& R, int lo, int hi) {
+    band_i<NB, false>(R.acc, lo, hi);
+    R.lo = lo;
   }
-
-  // ---- residual powers P_s = E P_{s-1} (column form, band s(N+1)..), Gs = sum
-  RunSum<NB> gs;
-  rs_init(gs, N + 1, C - 1);
-  if (S >= 1) {
-    rs_add(gs, Ecol, N + 1, C - 1, eE, 7, nzE);
-    ColQ<NB> Pq = ECq;
-    int eP = eE;
-    bool nzP = nzE;
-    auto chain = [&](int s) {
-      const int lo = s * (N + 1);
-      AccI<NB> D;
-      mmi<NB, false>(D, ERq, Pq, lo, C - 1);
-      requant(D, lo, C - 1, eE + eP, eP, nzP);
-      rs_add(gs, D, lo, C - 1, eP, 7, nzP);
-      to_colq(Pq, D, lo, C - 1);
-    };
-    if constexpr (SC >= 0) {
-#pragma unroll
-      for (int s = 2; s <= SC; ++s) chain(s);
-    } else {
-      for (int s = 2; s <= S; ++s) chain(s);
-    }
+  static __device__ __forceinline__ void rs_finish(Sum& R, AccI<NB>& q, int& e, bool& nz) {
+    i8::rs_finish(R, q, e, nz);
   }
-  AccI<NB> Gc;
-  int eG;
-  bool nzG;
-  rs_finish(gs, Gc, eG, nzG);
-  ColQ<NB> GCq;
-  to_colq(GCq, Gc, N + 1, C - 1);
-  AccI<NB> Gr;
-  mmi<NB, true>(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
-
-  // ---- T = N0 + Gs + N0 Gs (row form), strict part
-  bool nzT;
-  {
-    AccI<NB> NG;
-    mmi<NB, true>(NG, N0q, GCq, N + 2, C - 1);
-    RunSum<NB> ts;
-    rs_init(ts, 1, C - 1);
-    rs_add(ts, N0r, 1, N, eN0, 7, nzN0);
-    rs_add(ts, Gr, N + 1, C - 1, eG, 7, nzG);
-    rs_add(ts, NG, N + 2, C - 1, eN0 + eG, ACCB, nzN0 && nzG);
-    band_i<NB, false>(ts.acc, 1, C - 1);
-    rs_finish(ts, Tr, eTo, nzT);
-  }
-
-}
+};
 
 // Tq (codes, zero on and above the diagonal), eT and optionally
 // Tdeq = I + Tq 2^eT for tile `tile`
@@ -363,7 +276,7 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
   AccI<NB> Tr;
   int eTo;
-  engine_i8<NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+  int_engine<I8Ops, NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
   store_i8<NB>(Tr, eTo, Tq, eT, Tdeq, tile);
 }
 
@@ -410,7 +323,7 @@ __global__ __launch_bounds__(64) void k_inverse_i8_fused(const TK* __restrict__ 
     for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
   AccI<NB> Tr;
   int eTo;
-  engine_i8<NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
+  int_engine<I8Ops, NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
   store_i8<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
 }
 

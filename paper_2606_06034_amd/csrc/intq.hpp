@@ -142,5 +142,151 @@ __device__ __forceinline__ int amax_of(const AccI<NB>& D, int lo, int hi) {
   return wave_max(m);
 }
 
+
+// ---------------------------------------------------------------------------
+// The integer inverse of one tile (Section 3.5, Algorithm 1, in the integer
+// arithmetic the library reads from Appendix G): from Lm = -A as codes (row
+// form, strictly lower) with exponent eL, the masked Neumann powers
+// B_n = M(B_{n-1} Lm) summed into N0 (band 1..N), E = Lm + Lm N0 - N0 (band
+// 1..N set to its exact value 0), the residual powers P_s = E P_{s-1} summed
+// into Gs, and T = N0 + Gs + N0 Gs; every product requantised, every sum
+// exact in production order.  Returns the strict part of T_hat as codes Tr
+// (row form) and its exponent eTo.  NC, SC >= 0 fix N and S at compile time
+// (every band and block skip is then resolved by the compiler); -1 takes
+// them from Nrt, Srt.
+//
+// Ops<NB> supplies one code width: fragment types Row, Col (operands in row
+// and column form), Prod (an exact product) and Sum (an exact running sum);
+// kQB and kAccB, log2 bounds of a code's and a product's magnitude; to_row,
+// to_col (codes to fragments), mm<OUTQ> (exact product, blocks outside a
+// band zero), band, requant (product to codes), requant_codes, row_to_col,
+// col_to_row (form changes through the identity), rs_init, rs_add, rs_band,
+// rs_finish.  Every helper visits only the blocks that can meet the band of
+// sub-diagonals it is given; the other blocks are zero by the structure of
+// the computation.
+template <template <int> class Ops, int NB, int NC = -1, int SC = -1>
+__device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, int Srt,
+                                           AccI<NB>& Tr, int& eTo) {
+  using O = Ops<NB>;
+  constexpr int C = 16 * NB;
+  constexpr int QB = O::kQB, ACCB = O::kAccB;
+  const int N = NC >= 0 ? NC : Nrt;
+  const int S = SC >= 0 ? SC : Srt;
+  RowQ<NB> Iq;
+  ColQ<NB> Ic;
+  eye_quads(Iq, Ic);
+
+  const bool nzL = amax_of(Lr, 1, C - 1) > 0;
+  typename O::Row LRq;
+  O::to_row(LRq, Lr, 1, C - 1);
+  typename O::Col LCq;
+  O::row_to_col(LCq, nullptr, LRq, Ic, 1, C - 1);
+
+  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm) (band n..N), row form
+  typename O::Sum ns;
+  O::rs_init(ns, 1, N);
+  if (N >= 1) {
+    AccI<NB> B = Lr;
+    band_i<NB, false>(B, 1, N);
+    int eB;
+    bool nzB;
+    O::requant_codes(B, 1, N, eL, eB, nzB);
+    O::rs_add(ns, B, 1, N, eB, QB, nzB);
+    typename O::Row Bq;
+    O::to_row(Bq, B, 1, N);
+    auto power = [&](int n) {
+      typename O::Prod D;
+      O::template mm<true>(D, Bq, LCq, n, N);
+      O::band(D, n, N);
+      AccI<NB> q;
+      O::requant(D, q, n, N, eB + eL, eB, nzB);
+      O::rs_add(ns, q, n, N, eB, QB, nzB);
+      O::to_row(Bq, q, n, N);
+    };
+    if constexpr (NC >= 0) {
+#pragma unroll
+      for (int n = 2; n <= NC; ++n) power(n);
+    } else {
+      for (int n = 2; n <= N; ++n) power(n);
+    }
+  }
+  AccI<NB> N0r;
+  int eN0;
+  bool nzN0;
+  O::rs_finish(ns, N0r, eN0, nzN0);
+  typename O::Row N0q;
+  O::to_row(N0q, N0r, 1, N);
+  typename O::Col N0c;
+  O::row_to_col(N0c, nullptr, N0q, Ic, 1, N);
+
+  // ---- E = Lm + Lm N0 - N0 (row form), band 1..N zeroed
+  typename O::Row ERq;
+  typename O::Col ECq;
+  AccI<NB> Ecol;
+  int eE;
+  bool nzE;
+  {
+    typename O::Prod LN;
+    O::template mm<true>(LN, LRq, N0c, 2, C - 1);
+    typename O::Sum es;
+    O::rs_init(es, 1, C - 1);
+    O::rs_add(es, Lr, 1, C - 1, eL, QB, nzL);
+    O::rs_add(es, LN, 2, C - 1, eL + eN0, ACCB, nzL && nzN0);
+    O::rs_add(es, N0r, 1, N, eN0, QB, nzN0, true);
+    O::rs_band(es, N + 1, C - 1);
+    AccI<NB> Er;
+    O::rs_finish(es, Er, eE, nzE);
+    O::to_row(ERq, Er, N + 1, C - 1);
+    O::row_to_col(ECq, &Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
+  }
+
+  // ---- residual powers P_s = E P_{s-1} (column form, band s(N+1)..), Gs = sum
+  typename O::Sum gs;
+  O::rs_init(gs, N + 1, C - 1);
+  if (S >= 1) {
+    O::rs_add(gs, Ecol, N + 1, C - 1, eE, QB, nzE);
+    typename O::Col Pq = ECq;
+    int eP = eE;
+    bool nzP = nzE;
+    auto chain = [&](int s) {
+      const int lo = s * (N + 1);
+      typename O::Prod D;
+      O::template mm<false>(D, ERq, Pq, lo, C - 1);
+      AccI<NB> q;
+      O::requant(D, q, lo, C - 1, eE + eP, eP, nzP);
+      O::rs_add(gs, q, lo, C - 1, eP, QB, nzP);
+      O::to_col(Pq, q, lo, C - 1);
+    };
+    if constexpr (SC >= 0) {
+#pragma unroll
+      for (int s = 2; s <= SC; ++s) chain(s);
+    } else {
+      for (int s = 2; s <= S; ++s) chain(s);
+    }
+  }
+  AccI<NB> Gc;
+  int eG;
+  bool nzG;
+  O::rs_finish(gs, Gc, eG, nzG);
+  typename O::Col GCq;
+  O::to_col(GCq, Gc, N + 1, C - 1);
+  AccI<NB> Gr;
+  O::col_to_row(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
+
+  // ---- T = N0 + Gs + N0 Gs (row form), strict part
+  bool nzT;
+  {
+    typename O::Prod NG;
+    O::template mm<true>(NG, N0q, GCq, N + 2, C - 1);
+    typename O::Sum ts;
+    O::rs_init(ts, 1, C - 1);
+    O::rs_add(ts, N0r, 1, N, eN0, QB, nzN0);
+    O::rs_add(ts, Gr, N + 1, C - 1, eG, QB, nzG);
+    O::rs_add(ts, NG, N + 2, C - 1, eN0 + eG, ACCB, nzN0 && nzG);
+    O::rs_band(ts, 1, C - 1);
+    O::rs_finish(ts, Tr, eTo, nzT);
+  }
+}
+
 }  // namespace iq
 }  // namespace gdn
