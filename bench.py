@@ -88,8 +88,8 @@ def parse():
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU; --gpus {a.gpus} is not supported "
-              "(tiles are independent: a multi-GPU run would shard heads, see DESIGN.md)",
+        print(f"bench.py: runs on exactly one GPU; --gpus {a.gpus} is not supported "
+              "(tiles are independent: several GPUs would each take a share of the heads)",
               file=sys.stderr)
         sys.exit(2)
 
@@ -205,7 +205,7 @@ def main():
             stage_ms.append(e0.elapsed_time(e1) / a.steps)
         del dA32, dAq
 
-    # ---- algorithmic work per launch (measurement section)
+    # ---- algorithmic work per launch: the per-tile bytes and operations of each kernel
     f_inv = (N + S) * 2 * C ** 3 * n_tiles  # dense-equivalent, the paper's product count
     if C == 128:
         f_inv = (2 * (N + S) + 2) * 2 * 64 ** 3 * n_tiles
@@ -353,7 +353,7 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
     fws_ms = _time(lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT), max(1, a.steps // 4),
                    stream, torch)
     del dA, dT
-    # algorithmic bytes per launch (measurement section)
+    # algorithmic bytes per launch
     # workspace: W, U, K^T and the masked Q K^T per chunk, written once, read once
     ws_b = G.gdn_chunk_forward_workspace(w.B, w.L, w.H, w.dk, w.dv, C, dt)
     prep_bytes = tok * (2 * w.dk + w.dv) * es + tok * 8 + ws_b

@@ -60,7 +60,7 @@ enum gdn_status {
   GDN_ERR_ALIGN = -5,       /* a pointer is not 16-byte aligned               */
   GDN_ERR_ALIAS = -6,       /* an output overlaps an input                    */
   GDN_ERR_HIP = -7,         /* the HIP runtime rejected a launch              */
-  GDN_ERR_UNSUPPORTED = -8, /* valid request this build does not implement    */
+  GDN_ERR_UNSUPPORTED = -8, /* valid request the library does not implement   */
   GDN_ERR_WORKSPACE = -9    /* the caller's workspace is smaller than needed  */
 };
 

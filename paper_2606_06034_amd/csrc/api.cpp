@@ -60,7 +60,7 @@ const char* gdn_status_string(int status) {
     case GDN_ERR_ALIGN: return "pointer not 16-byte aligned";
     case GDN_ERR_ALIAS: return "an output overlaps an input";
     case GDN_ERR_HIP: return "HIP runtime error at launch";
-    case GDN_ERR_UNSUPPORTED: return "combination not implemented by this build";
+    case GDN_ERR_UNSUPPORTED: return "combination not implemented by the library";
     case GDN_ERR_WORKSPACE: return "workspace smaller than gdn_chunk_forward_workspace()";
   }
   return "unknown status";
