@@ -40,6 +40,12 @@ splits into two int8 limbs), the running sums 16 guard bits below a code's
 quantum (terms kept below 2^31, sums below 2^36), and products exact in
 int64.  SPEC8 and SPEC16 hold the two parameter sets; every function takes
 the spec (INT8 by default).
+
+C = 128 runs block-wise (Appendix E, with Appendix H's 64 x 64 blocks):
+quantize_blocked gives each of the blocks A11, A21, A22 its own exponent,
+and neumann_inverse_int_blocked inverts the diagonal blocks with the recipe
+above and forms X21 = -X22 A21 X11 as two requantised products (P = A21 X11,
+then X22 P), the identity parts of X11 and X22 kept exact.
 """
 
 from __future__ import annotations
@@ -334,6 +340,91 @@ def fwdsub_inverse_int(qA: np.ndarray, eA: np.ndarray, spec: Spec = SPEC16):
 def neumann_inverse_int16(qA: np.ndarray, eA: np.ndarray, N: int, S: int):
     """neumann_inverse_int8 with 16-bit codes (SPEC16)."""
     return neumann_inverse_int8(qA, eA, N, S, SPEC16)
+
+
+# ----------------------------------------------------------------------------
+# C = 128: block-wise (Appendix E; Appendix H fixes 64 x 64 as the smallest
+# block for the integer settings)
+
+
+def _blocks(C: int):
+    """(rows, cols) slices of the blocks 11, 21, 22 of a C x C tile split at
+    C / 2 (block 12 is zero in a lower-triangular matrix)."""
+    h = C // 2
+    return ((slice(0, h), slice(0, h)), (slice(h, C), slice(0, h)), (slice(h, C), slice(h, C)))
+
+
+def quantize_blocked(x: np.ndarray, spec: Spec = SPEC8) -> Tuple[np.ndarray, np.ndarray]:
+    """The quantiser of quantize() applied block by block: the strict lower
+    parts of the diagonal blocks A11, A22 and the whole block A21 each get
+    their own power-of-two exponent.  x float32 tiles [..., C, C] (only
+    i > j read).  Returns q [..., C, C] (zero on and above the diagonal)
+    and e [..., 3] for the blocks (11, 21, 22)."""
+    x = np.asarray(x, dtype=np.float32)
+    C = x.shape[-1]
+    x = np.where(_subdiag(C) > 0, x, np.float32(0))
+    q = np.zeros(x.shape, np.int64)
+    es = []
+    for rs, cs in _blocks(C):
+        qb, eb = quantize(x[..., rs, cs], spec)
+        q[..., rs, cs] = qb
+        es.append(eb)
+    return q, np.stack(es, axis=-1)
+
+
+def neumann_inverse_int_blocked(qA: np.ndarray, eA: np.ndarray, N: int, S: int,
+                                spec: Spec = SPEC8):
+    """Integer inverse of a tile split into two diagonal blocks (Appendix E:
+    X11 = T11^-1, X22 = T22^-1, X21 = -X22 T21 X11 with T21 = A21).
+
+    qA [..., C, C] codes with exponents eA [..., 3] for the blocks
+    (11, 21, 22) as quantize_blocked writes them.  The diagonal blocks are
+    inverted by neumann_inverse_int8 (X = I + N, codes N at one exponent).
+    The off-diagonal block is two requantised products whose identity parts
+    stay exact, taken from the right:
+      P   = A21 X11 = A21 + A21 N11,
+      X21 = -(X22 P) = -(P + N22 P),
+    each an aligned_sum of the code term and the exact product term (in
+    that order; a product is present when both factors are non-zero),
+    requantised; the sign is applied to the codes (round-half-even is
+    symmetric, so negating before or after rounding agrees).
+    Returns qT [..., C, C] (N11, X21 and N22 in their blocks, zero on and
+    above the diagonal) and eT [..., 3] for (N11, X21, N22): the inverse is
+    I + each block's codes * 2^(its exponent)."""
+    qA = np.asarray(qA, np.int64)
+    eA = np.asarray(eA, np.int64)
+    C = qA.shape[-1]
+    b11, b21, b22 = _blocks(C)
+    q11, e11, _ = neumann_inverse_int8(qA[(Ellipsis,) + b11], eA[..., 0], N, S, spec)
+    q22, e22, _ = neumann_inverse_int8(qA[(Ellipsis,) + b22], eA[..., 2], N, S, spec)
+    a21, ea = qA[(Ellipsis,) + b21], eA[..., 1]
+    accb = _acc_bits(C // 2, spec)
+    nzA = _tile_amax(a21) > 0
+    nz11 = _tile_amax(q11) > 0
+    nz22 = _tile_amax(q22) > 0
+    s_, e_, _ = aligned_sum([(a21, ea, nzA, spec.qbits),
+                             (a21 @ q11, ea + e11, nzA & nz11, accb)], spec)
+    qP, eP = requant(s_, e_, spec)
+    nzP = _tile_amax(qP) > 0
+    s_, e_, _ = aligned_sum([(qP, eP, nzP, spec.qbits),
+                             (q22 @ qP, e22 + eP, nz22 & nzP, accb)], spec)
+    q21, e21 = requant(s_, e_, spec)
+    qT = np.zeros_like(qA)
+    qT[(Ellipsis,) + b11] = q11
+    qT[(Ellipsis,) + b21] = -q21
+    qT[(Ellipsis,) + b22] = q22
+    return qT, np.stack([e11, e21, e22], axis=-1)
+
+
+def dequant_unit_blocked(qT: np.ndarray, eT: np.ndarray) -> np.ndarray:
+    """I + (each block's codes) * 2^(its exponent), float64; eT [..., 3]."""
+    qT = np.asarray(qT, np.float64)
+    eT = np.asarray(eT)
+    C = qT.shape[-1]
+    out = np.zeros(qT.shape)
+    for k, (rs, cs) in enumerate(_blocks(C)):
+        out[(Ellipsis, rs, cs)] = np.ldexp(qT[(Ellipsis, rs, cs)], eT[..., k][..., None, None])
+    return out + np.eye(C)
 
 
 def dequant_unit(qT: np.ndarray, eT: np.ndarray) -> np.ndarray:

@@ -563,3 +563,127 @@ def test_int8_fwdsub_exact_cases_and_accuracy():
     err = np.max(np.abs(qo.dequant_unit(qX, eX) - X), axis=(-1, -2))
     assert np.all(err <= 8 * 2.0 ** -7 * scale)
     assert np.all(np.abs(qX) <= 127)
+
+
+# ---------------------------------------------------------------------------
+# C = 128, block-wise (Appendix E with 64 x 64 blocks, Appendix H): three
+# exponents per tile, X21 = -X22 A21 X11 as two requantised products
+
+
+def _blocked_A(C, seed, stress=False):
+    if stress:
+        k, b, g, _ = wl.gen_stress_head(L=2 * C, dk=64, C=C, seed=seed)
+    else:
+        w = wl.workload("tiny").with_(seed=seed)
+        k, b, g, _ = wl.gen_head(w, 0, 0, C=C, want_v=False)
+        k, b, g = k[:2 * C], b[:2 * C], g[:2 * C]
+    return gdn.tiles_flat(gdn.build_A(k[None, :, None], b[None, :, None], g[None, :, None], C))
+
+
+@pytest.mark.parametrize("spec", [qo.SPEC8, qo.SPEC16])
+def test_blocked_quantize_per_block_minimal_exponent(spec):
+    A = _blocked_A(128, 1).astype(np.float32)
+    A[1, 64:, :64] = 0.0  # an all-zero off-diagonal block gets e = 0
+    q, e = qo.quantize_blocked(A, spec)
+    assert e.shape == (2, 3) and e[1, 1] == 0
+    d = gdn.subdiag_index(128)
+    assert np.all(q[:, d <= 0] == 0)
+    for k, (r, c) in enumerate([(0, 0), (1, 0), (1, 1)]):
+        rs, cs = slice(64 * r, 64 * r + 64), slice(64 * c, 64 * c + 64)
+        x = np.where(d[rs, cs] > 0, A[:, rs, cs], 0).astype(np.float64)
+        for t in range(2):
+            et = int(e[t, k])
+            if not np.any(x[t]):
+                assert et == 0 and not np.any(q[t, rs, cs])
+                continue
+            qb = q[t, rs, cs]
+            assert np.max(np.abs(qb)) <= spec.qmax
+            # smallest exponent: one lower would need a code above qmax
+            assert np.max(np.abs(x[t])) / 2.0 ** (et - 1) > spec.qmax
+            assert np.max(np.abs(qb * 2.0 ** et - x[t])) <= 2.0 ** (et - 1)
+
+
+def _py_blocked(qA, eA, N, S, P):
+    """Independent coding of the block-wise inverse on small tiles: the
+    diagonal blocks by _py_pipeline, then P = A21 + A21 N11 and
+    X21 = -(P + N22 P), each summed and requantised."""
+    C = len(qA)
+    h = C // 2
+    bits = 2 * P[1] + (h - 1).bit_length()
+    blk = lambda r, c: [row[c:c + h] for row in qA[r:r + h]]
+    N11, e11 = _py_pipeline(blk(0, 0), eA[0], N, S, P)
+    N22, e22 = _py_pipeline(blk(h, h), eA[2], N, S, P)
+    A21 = blk(h, 0)
+    nzA = _py_nz(A21)
+    Ps, ep = _py_sum([(A21, eA[1], nzA, P[1]),
+                      (_py_mm(A21, N11), eA[1] + e11, nzA and _py_nz(N11), bits)], h, P)
+    Pq, eP = _py_requant(Ps, ep, P)
+    Xs, ex = _py_sum([(Pq, eP, _py_nz(Pq), P[1]),
+                      (_py_mm(N22, Pq), e22 + eP, _py_nz(N22) and _py_nz(Pq), bits)], h, P)
+    X21, e21 = _py_requant(Xs, ex, P)
+    out = [[0] * C for _ in range(C)]
+    for i in range(h):
+        for j in range(h):
+            out[i][j] = N11[i][j]
+            out[h + i][h + j] = N22[i][j]
+            out[h + i][j] = -X21[i][j]
+    return out, [e11, e21, e22]
+
+
+@pytest.mark.parametrize("spec,P", [(qo.SPEC8, PY8), (qo.SPEC16, PY16)])
+@pytest.mark.parametrize("C,N,S", [(16, 3, 2), (16, 1, 3), (32, 2, 2)])
+def test_blocked_matches_independent_coding(spec, P, C, N, S):
+    A = _blocked_A(C, C + N, stress=True).astype(np.float32)
+    qA, eA = qo.quantize_blocked(A, spec)
+    qT, eT = qo.neumann_inverse_int_blocked(qA, eA, N, S, spec)
+    for t in range(A.shape[0]):
+        Tp, ep = _py_blocked(qA[t].tolist(), [int(v) for v in eA[t]], N, S, P)
+        assert qT[t].tolist() == Tp
+        assert [int(v) for v in eT[t]] == ep
+
+
+@pytest.mark.parametrize("spec", [qo.SPEC8, qo.SPEC16])
+def test_blocked_closed_forms(spec):
+    """A21 = 0: X21 = 0 and the diagonal blocks are the 64 x 64 integer
+    inverses; A11 = A22 = 0: A^2 = 0, so (I + A)^-1 = I - A and the codes of
+    X21 are those of -A21 at A21's exponent; all-ones A: the pipeline
+    reproduces the exact inverse I - Z (Z the unit sub-diagonal) across the
+    block boundary."""
+    A = _blocked_A(128, 2).astype(np.float32)
+    Ad = A.copy()
+    Ad[:, 64:, :64] = 0.0
+    qA, eA = qo.quantize_blocked(Ad, spec)
+    qT, eT = qo.neumann_inverse_int_blocked(qA, eA, 3, 8, spec)
+    assert not np.any(qT[:, 64:, :64]) and np.all(eT[:, 1] == 0)
+    for k, s in ((0, slice(0, 64)), (2, slice(64, 128))):
+        q1, e1 = qo.quantize(np.tril(A[:, s, s], -1), spec)
+        t1, f1, _ = qo.neumann_inverse_int8(q1, e1, 3, 8, spec)
+        assert np.array_equal(qT[:, s, s], t1) and np.array_equal(eT[:, k], f1)
+    Ao = np.zeros_like(A)
+    Ao[:, 64:, :64] = A[:, 64:, :64]
+    qA, eA = qo.quantize_blocked(Ao, spec)
+    qT, eT = qo.neumann_inverse_int_blocked(qA, eA, 3, 8, spec)
+    assert np.array_equal(qT[:, 64:, :64], -qA[:, 64:, :64]) and np.array_equal(eT[:, 1], eA[:, 1])
+    assert not np.any(qT[:, :64, :64]) and not np.any(qT[:, 64:, 64:])
+    ones = np.tril(np.ones((1, 128, 128), np.float32), -1)
+    qA, eA = qo.quantize_blocked(ones, spec)
+    qT, eT = qo.neumann_inverse_int_blocked(qA, eA, 3, 8, spec)
+    assert np.array_equal(qo.dequant_unit_blocked(qT, eT)[0], np.eye(128) - np.eye(128, k=-1))
+
+
+@pytest.mark.parametrize("spec,bits", [(qo.SPEC8, 8), (qo.SPEC16, 16)])
+@pytest.mark.parametrize("src", ["workload", "stress"])
+def test_blocked_close_to_float_approximation(spec, bits, src):
+    """Dequantised block-wise inverse against the float64 block-wise
+    T_hat(3, 8) (Appendix E formula on float64 diagonal inverses): the merge
+    adds two requantisations and X22's gain to the diagonal blocks' error."""
+    A = _blocked_A(128, 3, stress=src == "stress")
+    qA, eA = qo.quantize_blocked(A.astype(np.float32), spec)
+    qT, eT = qo.neumann_inverse_int_blocked(qA, eA, 3, 8, spec)
+    T = gdn.neumann_inverse_blocked(A, 3, 8)
+    scale = np.max(np.abs(T - np.eye(128)), axis=(-1, -2))
+    err = np.max(np.abs(qo.dequant_unit_blocked(qT, eT) - T), axis=(-1, -2))
+    assert np.all(err <= 16 * 2.0 ** -bits * scale)
+    # the 64 x 64 inverses alone: same bound as the unblocked pins
+    err11 = np.max(np.abs(qo.dequant_unit_blocked(qT, eT)[:, :64, :64] - T[:, :64, :64]))
+    assert err11 <= 16 * 2.0 ** -bits * np.max(scale)
