@@ -172,7 +172,11 @@ int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, c
  * integer with max|A| / 2^e <= 127 and Aq = round-half-even(A / 2^e).
  * A: fp32 tiles; Aq: int8 tiles (same layout); eA: int32 [n_tiles].  An
  * all-zero tile gets Aq = 0, eA = 0.  Only the strictly lower part of A is
- * read (the rest is taken as 0 and written as 0). */
+ * read (the rest is taken as 0 and written as 0).  C in {16, 32, 64, 128}.
+ * C = 128 is quantised block-wise (Appendix E with the 64 x 64 blocks of
+ * Appendix H): the strict lower parts of the diagonal blocks and the whole
+ * block 21 each get their own exponent, eA [n_tiles, 3] in the block order
+ * (11, 21, 22); block 12 is written as 0. */
 int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles,
                           int C, void* stream);
 
@@ -183,7 +187,14 @@ int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_til
  * it is quantised; sums align their terms exactly in int32.  Outputs:
  * Tinv = I + Tq * 2^eT, Tq int8 tiles holding the strict lower part (0 on
  * and above the diagonal), eT int32 [n_tiles]; Tdeq (nullable) receives
- * I + Tq * 2^eT in fp32.  C in {16, 32, 64}.  Requires finite inputs. */
+ * I + Tq * 2^eT in fp32.  C in {16, 32, 64, 128}.  C = 128 runs block-wise
+ * (Appendix E, Appendix H) on the codes of gdn_quantize_tiles_i8 at C = 128
+ * (eA [n_tiles, 3]): both 64 x 64 diagonal blocks by the integer inverse
+ * above (X = I + N per block), and X21 = -X22 A21 X11 as two requantised
+ * products, P = A21 + A21 N11, then X21 = -(P + N22 P), each sum formed by
+ * the same exact aligned rule; eT [n_tiles, 3] holds the exponents of N11,
+ * X21 and N22, so Tinv = I + (each block's codes) * 2^(its exponent), and
+ * N, S <= 63.  Requires finite inputs. */
 int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq,
                                  int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
                                  int N, int S, void* stream);
@@ -206,7 +217,8 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
  * Aq = round-half-even(A / 2^e).  A: fp32 tiles; Aq: int16 tiles (same
  * layout); eA: int32 [n_tiles].  An all-zero tile gets Aq = 0, eA = 0.  Only
  * the strictly lower part of A is read (the rest is taken as 0 and written
- * as 0). */
+ * as 0).  C = 128: block-wise with eA [n_tiles, 3], as for
+ * gdn_quantize_tiles_i8. */
 int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_tiles,
                            int C, void* stream);
 
@@ -220,7 +232,9 @@ int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_t
  * and above the diagonal), eT int32 [n_tiles]; Tdeq (nullable) receives
  * I + Tq * 2^eT in fp32.  Aq codes must lie in [-32639, 32639], the range
  * the quantiser writes (a negated code must split into two int8 limbs);
- * a tile holding -32768 gets unspecified codes.  C in {16, 32, 64}. */
+ * a tile holding -32768 gets unspecified codes.  C in {16, 32, 64, 128};
+ * C = 128 block-wise with eA, eT [n_tiles, 3], as for
+ * gdn_chunk_inverse_neumann_i8. */
 int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
                                   int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
                                   int N, int S, void* stream);

@@ -256,15 +256,23 @@ def gdn_chunk_wy_fused_blockwise(K: torch.Tensor, V: torch.Tensor, beta: torch.T
     return (W, U, Tinv) if Tinv is not None else (W, U)
 
 
+def _nexp(C: int) -> int:
+    """Exponents per tile of the integer paths (C = 128: blocks 11, 21, 22)."""
+    return 3 if C == 128 else 1
+
+
 def gdn_quantize_tiles_i8(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
                           eA: Optional[torch.Tensor] = None, stream=None):
-    """(Aq int8 tiles, eA int32 per tile) with A ~ Aq * 2^eA."""
+    """(Aq int8 tiles, eA int32 per tile) with A ~ Aq * 2^eA; C = 128:
+    eA [n, 3], one exponent per block (11, 21, 22)."""
     n, C = _tiles(A)
+    ne = _nexp(C)
     Aq = torch.empty(A.shape, dtype=torch.int8, device=A.device) if Aq is None else Aq
-    eA = torch.empty(n, dtype=torch.int32, device=A.device) if eA is None else eA
+    if eA is None:
+        eA = torch.empty((n, 3) if ne == 3 else n, dtype=torch.int32, device=A.device)
     _check("gdn_quantize_tiles_i8", lib.gdn_quantize_tiles_i8(
         _dev(A, "A", torch.float32), _dev(Aq, "Aq", torch.int8, A.numel()),
-        _dev(eA, "eA", torch.int32, n), n, C, _stream(stream)))
+        _dev(eA, "eA", torch.int32, n * ne), n, C, _stream(stream)))
     return Aq, eA
 
 
@@ -272,16 +280,18 @@ def gdn_chunk_inverse_neumann_i8(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: 
                                  want_deq: bool = False, Tq: Optional[torch.Tensor] = None,
                                  eT: Optional[torch.Tensor] = None,
                                  Tdeq: Optional[torch.Tensor] = None, stream=None):
-    """(Tq int8, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT."""
+    """(Tq int8, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT; C = 128:
+    block-wise, eA and eT [n, 3] (blocks 11, 21, 22)."""
     n, C = _tiles(Aq)
     Tq = torch.empty_like(Aq) if Tq is None else Tq
     eT = torch.empty_like(eA) if eT is None else eT
     Td = Tdeq
     if want_deq and Td is None:
         Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device)
+    ne = _nexp(C)
     _check("gdn_chunk_inverse_neumann_i8", lib.gdn_chunk_inverse_neumann_i8(
-        _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32, n),
-        _dev(Tq, "Tq", torch.int8, Aq.numel()), _dev(eT, "eT", torch.int32, n),
+        _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32, n * ne),
+        _dev(Tq, "Tq", torch.int8, Aq.numel()), _dev(eT, "eT", torch.int32, n * ne),
         _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
         _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)
@@ -314,13 +324,16 @@ def gdn_chunk_inverse_neumann_i8_fused(K: torch.Tensor, beta: torch.Tensor, g: t
 
 def gdn_quantize_tiles_i16(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
                            eA: Optional[torch.Tensor] = None, stream=None):
-    """(Aq int16 tiles, eA int32 per tile) with A ~ Aq * 2^eA."""
+    """(Aq int16 tiles, eA int32 per tile) with A ~ Aq * 2^eA; C = 128:
+    eA [n, 3], one exponent per block (11, 21, 22)."""
     n, C = _tiles(A)
+    ne = _nexp(C)
     Aq = torch.empty(A.shape, dtype=torch.int16, device=A.device) if Aq is None else Aq
-    eA = torch.empty(n, dtype=torch.int32, device=A.device) if eA is None else eA
+    if eA is None:
+        eA = torch.empty((n, 3) if ne == 3 else n, dtype=torch.int32, device=A.device)
     _check("gdn_quantize_tiles_i16", lib.gdn_quantize_tiles_i16(
         _dev(A, "A", torch.float32), _dev(Aq, "Aq", torch.int16, A.numel()),
-        _dev(eA, "eA", torch.int32, n), n, C, _stream(stream)))
+        _dev(eA, "eA", torch.int32, n * ne), n, C, _stream(stream)))
     return Aq, eA
 
 
@@ -328,16 +341,18 @@ def gdn_chunk_inverse_neumann_i16(Aq: torch.Tensor, eA: torch.Tensor, N: int, S:
                                   want_deq: bool = False, Tq: Optional[torch.Tensor] = None,
                                   eT: Optional[torch.Tensor] = None,
                                   Tdeq: Optional[torch.Tensor] = None, stream=None):
-    """(Tq int16, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT."""
+    """(Tq int16, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT; C = 128:
+    block-wise, eA and eT [n, 3] (blocks 11, 21, 22)."""
     n, C = _tiles(Aq)
     Tq = torch.empty_like(Aq) if Tq is None else Tq
     eT = torch.empty_like(eA) if eT is None else eT
     Td = Tdeq
     if want_deq and Td is None:
         Td = torch.empty(Aq.shape, dtype=torch.float32, device=Aq.device)
+    ne = _nexp(C)
     _check("gdn_chunk_inverse_neumann_i16", lib.gdn_chunk_inverse_neumann_i16(
-        _dev(Aq, "Aq", torch.int16), _dev(eA, "eA", torch.int32, n),
-        _dev(Tq, "Tq", torch.int16, Aq.numel()), _dev(eT, "eT", torch.int32, n),
+        _dev(Aq, "Aq", torch.int16), _dev(eA, "eA", torch.int32, n * ne),
+        _dev(Tq, "Tq", torch.int16, Aq.numel()), _dev(eT, "eT", torch.int32, n * ne),
         _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
         _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)

@@ -24,6 +24,9 @@ bool overlap(const void* p, int64_t bytes, const void* q, int64_t qbytes) {
   return a < b + (uintptr_t)qbytes && b < a + (uintptr_t)bytes;
 }
 
+// exponents per tile of the integer paths: C = 128 runs three blocks
+int64_t nexp(int C) { return C == 128 ? 3 : 1; }
+
 int order_ok(int C, int N, int S) {
   const int lim = (C == 128 ? 64 : C) - 1;  // C = 128 runs 64-blocks
   return N >= 0 && S >= 0 && N <= lim && S <= lim;
@@ -284,12 +287,12 @@ int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const 
 
 int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                           void* stream) {
-  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
     return GDN_ERR_SHAPE;
   if (n_tiles == 0) return GDN_OK;
   if (!A || !Aq || !eA) return GDN_ERR_NULL;
   if (!aligned(A) || !aligned(Aq) || !aligned(eA)) return GDN_ERR_ALIGN;
-  const int64_t ab = n_tiles * C * C * 4, qb = n_tiles * C * C, eb = n_tiles * 4;
+  const int64_t ab = n_tiles * C * C * 4, qb = n_tiles * C * C, eb = n_tiles * 4 * nexp(C);
   if (overlap(Aq, qb, A, ab) || overlap(eA, eb, A, ab) || overlap(Aq, qb, eA, eb))
     return GDN_ERR_ALIAS;
   return hip_status(gdn::launch_quantize_i8(A, Aq, eA, n_tiles, C, (hipStream_t)stream));
@@ -298,14 +301,14 @@ int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_til
 int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
                                  float* Tdeq, int64_t n_tiles, int C, int N, int S,
                                  void* stream) {
-  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
     return GDN_ERR_SHAPE;
   if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (n_tiles == 0) return GDN_OK;
   if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
   if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
     return GDN_ERR_ALIGN;
-  const int64_t qb = n_tiles * C * C, eb = n_tiles * 4, db = n_tiles * C * C * 4;
+  const int64_t qb = n_tiles * C * C, eb = n_tiles * 4 * nexp(C), db = n_tiles * C * C * 4;
   const void* ins[2] = {Aq, eA};
   const int64_t inb[2] = {qb, eb};
   for (int i = 0; i < 2; ++i)
@@ -348,12 +351,12 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
 
 int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                            void* stream) {
-  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
     return GDN_ERR_SHAPE;
   if (n_tiles == 0) return GDN_OK;
   if (!A || !Aq || !eA) return GDN_ERR_NULL;
   if (!aligned(A) || !aligned(Aq) || !aligned(eA)) return GDN_ERR_ALIGN;
-  const int64_t ab = n_tiles * C * C * 4, qb = n_tiles * C * C * 2, eb = n_tiles * 4;
+  const int64_t ab = n_tiles * C * C * 4, qb = n_tiles * C * C * 2, eb = n_tiles * 4 * nexp(C);
   if (overlap(Aq, qb, A, ab) || overlap(eA, eb, A, ab) || overlap(Aq, qb, eA, eb))
     return GDN_ERR_ALIAS;
   return hip_status(gdn::launch_quantize_i16(A, Aq, eA, n_tiles, C, (hipStream_t)stream));
@@ -362,14 +365,14 @@ int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_t
 int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
                                   int32_t* eT, float* Tdeq, int64_t n_tiles, int C, int N, int S,
                                   void* stream) {
-  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
     return GDN_ERR_SHAPE;
   if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (n_tiles == 0) return GDN_OK;
   if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
   if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
     return GDN_ERR_ALIGN;
-  const int64_t qb = n_tiles * C * C * 2, eb = n_tiles * 4, db = n_tiles * C * C * 4;
+  const int64_t qb = n_tiles * C * C * 2, eb = n_tiles * 4 * nexp(C), db = n_tiles * C * C * 4;
   const void* ins[2] = {Aq, eA};
   const int64_t inb[2] = {qb, eb};
   for (int i = 0; i < 2; ++i)

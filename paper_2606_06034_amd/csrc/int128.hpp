@@ -1,0 +1,238 @@
+// int128.hpp -- the integer inverse at C = 128, block-wise (Appendix E of
+// arXiv 2606.06034, with the 64 x 64 blocks that Appendix H names as the
+// smallest for the integer settings), for either code width.
+//
+// A C = 128 tile of codes holds three blocks with an exponent each, in the
+// order (11, 21, 22): the strict lower parts of the two diagonal blocks and
+// the whole block 21 (block 12 of a lower-triangular tile is zero).
+//
+// Inverse, two waves per tile: wave w inverts diagonal block w with the
+// one-tile engine (int_engine, X_ww = I + N_ww), then wave 1 forms the
+// off-diagonal block from the right,
+//   P = A21 X11 = A21 + A21 N11,      X21 = -(X22 P) = -(P + N22 P),
+// each an exact product added to its code term by the engine's running-sum
+// rules (code term first; a product is present when both factors are
+// non-zero) and requantised; N11 reaches wave 1 through LDS.
+//
+// W (one code width) supplies: Code (the storage type), load4 / store4 (four
+// consecutive codes <-> i32x4), qexp (the quantiser's exponent of a block
+// maximum), engine<NC, SC> (the one-tile inverse of a 64 x 64 block), Row,
+// Col, to_row, to_col (the engine's fragments of lower matrices), to_frow
+// (row-form fragments of a full matrix), frow_to_col (row-form fragments to
+// column-form ones, exact), FProd and fmm<OUTQ> (an exact product over all
+// 16 output blocks) and sum2 (code term + product term, summed and
+// requantised to codes).
+#pragma once
+
+#include "intq.hpp"
+
+namespace gdn {
+namespace iq {
+
+// Tdeq of a diagonal block (row stride 128): I + codes * 2^e on the strict
+// lower part, 0 above the diagonal
+__device__ __forceinline__ void store_deq_diag(float* td, const AccI<4>& Tr, int e) {
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J) {
+      f32x4 x = zero4();
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int d = 16 * (I - J) + c - 4 * g - v;
+        if (J <= I && d > 0) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], e);
+        if (d == 0) x[v] = 1.f;
+      }
+      *(f32x4*)(td + (I * 16 + c) * 128 + J * 16 + 4 * g) = x;
+    }
+}
+
+template <typename W, int NC, int SC>
+__global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* __restrict__ Aq,
+                                                        const int32_t* __restrict__ eA,
+                                                        typename W::Code* __restrict__ Tq,
+                                                        int32_t* __restrict__ eT,
+                                                        float* __restrict__ Tdeq, int Nrt,
+                                                        int Srt) {
+  using Code = typename W::Code;
+  constexpr int C = 128, LD = 68;  // LD: padded row stride of the N11 hand-over (ints)
+  __shared__ __attribute__((aligned(16))) int sN[64 * LD];  // sN[j * LD + i] = N11[i][j]
+  __shared__ int sInfo[2];
+  const int64_t tile = blockIdx.x;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane_g(), c = lane_c();
+  const int r0 = 64 * wv;
+  const Code* a = Aq + tile * (C * C);
+  Code* t = Tq + tile * (C * C);
+  float* td = Tdeq ? Tdeq + tile * (C * C) : nullptr;
+
+  // ---- this wave's diagonal block: Lm = -A_ww (row form), strictly lower
+  AccI<4> Lr;
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 x = W::load4(a + (r0 + I * 16 + c) * C + r0 + J * 16 + 4 * g);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
+      Lr.a[bidx(I, J)] = x;
+    }
+  const int eL = __builtin_amdgcn_readfirstlane(eA[3 * tile + 2 * wv]);
+  AccI<4> Tr;
+  int eTo;
+  W::template engine<NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+
+  // ---- the diagonal block out (wave 0 also writes block 12, all zero)
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J)
+      W::store4(t + (r0 + I * 16 + c) * C + r0 + J * 16 + 4 * g,
+                J <= I ? Tr.a[bidx(I, J)] : zero_i4());
+  if (wv == 0)
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J) W::store4(t + (I * 16 + c) * C + 64 + J * 16 + 4 * g, zero_i4());
+  if (lane_id() == 0) eT[3 * tile + 2 * wv] = eTo;
+  if (td) {
+    store_deq_diag(td + r0 * C + r0, Tr, eTo);
+    if (wv == 0)
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int J = 0; J < 4; ++J) *(f32x4*)(td + (I * 16 + c) * C + 64 + J * 16 + 4 * g) = zero4();
+  }
+  const bool nzT = amax_of(Tr, 1, 63) > 0;
+  if (wv == 0) {
+    // N11 (row form: lane (g, c) holds row 16 I + c, columns 16 J + 4 g + v)
+    // to LDS transposed, so that wave 1 reads its column form as 16 bytes
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sN[(16 * J + 4 * g + v) * LD + 16 * I + c] = Tr.a[bidx(I, J)][v];
+    if (lane_id() == 0) {
+      sInfo[0] = eTo;
+      sInfo[1] = nzT ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  if (wv == 0) return;
+
+  // ---- wave 1: X21 = -(X22 (A21 X11))
+  AccI<4> N11c;  // column form: lane (g, c) holds rows 16 K + 4 g + v of column 16 J + c
+#pragma unroll
+  for (int J = 0; J < 4; ++J)
+#pragma unroll
+    for (int K = J; K < 4; ++K) N11c.a[bidx(K, J)] = *(const i32x4*)&sN[(16 * J + c) * LD + 16 * K + 4 * g];
+  const int e11 = __builtin_amdgcn_readfirstlane(sInfo[0]);
+  const bool nz11 = __builtin_amdgcn_readfirstlane(sInfo[1]) != 0;
+  typename W::Col N11q;
+  W::to_col(N11q, N11c, 1, 63);
+
+  FullI A21;
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J) A21.a[4 * I + J] = W::load4(a + (64 + I * 16 + c) * C + J * 16 + 4 * g);
+  const int ea = __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]);
+  const bool nzA = amax_full(A21) > 0;
+
+  typename W::Row X;  // A21, then P, as row-form fragments (sum2 reads the codes back)
+  typename W::FProd D;
+  W::to_frow(X, A21);
+  W::template fmm<true>(D, X, N11q);  // A21 N11, row form
+  FullI P;
+  int eP;
+  bool nzP;
+  W::sum2(P, eP, nzP, X, ea, nzA, D, ea + e11, nzA && nz11);
+
+  RowQ<4> Iq;
+  ColQ<4> Ic;
+  eye_quads(Iq, Ic);
+  W::to_frow(X, P);
+  typename W::Col Pc;
+  W::frow_to_col(Pc, X, Ic);
+  typename W::Row N22q;
+  W::to_row(N22q, Tr, 1, 63);
+  W::template fmm<true>(D, N22q, Pc);  // N22 P, row form
+  FullI Xs;
+  int e21;
+  bool nz21;
+  W::sum2(Xs, e21, nz21, X, eP, nzP, D, eTo + eP, nzT && nzP);
+
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J)
+      W::store4(t + (64 + I * 16 + c) * C + J * 16 + 4 * g, zero_i4() - Xs.a[4 * I + J]);
+  if (lane_id() == 0) eT[3 * tile + 1] = e21;
+  if (td)
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        f32x4 x;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) x[v] = ldexpf((float)-Xs.a[4 * I + J][v], e21);
+        *(f32x4*)(td + (64 + I * 16 + c) * C + J * 16 + 4 * g) = x;
+      }
+}
+
+// Quantiser at C = 128: four waves per tile, wave w on the 64 x 64 quadrant
+// (w >> 1, w & 1).  The strict lower parts of the diagonal blocks and the
+// whole block 21 each get their own exponent (the per-tile rule applied to
+// the block: the smallest e with max|x| / 2^e <= qmax, codes
+// round-half-even(x / 2^e)); block 12 is written as 0.  eA[3 tile + k] for
+// the blocks k = 0 (11), 1 (21), 2 (22).
+template <typename W>
+__global__ __launch_bounds__(256) void k_quantize_int128(const float* __restrict__ A,
+                                                         typename W::Code* __restrict__ Aq,
+                                                         int32_t* __restrict__ eA) {
+  constexpr int C = 128, PER = 16;  // float4 per lane of a 64 x 64 block
+  const int64_t tile = blockIdx.x;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int qr = wv >> 1, qc = wv & 1;
+  const int l = lane_id();
+  typename W::Code* q = Aq + tile * (C * C) + (64 * qr) * C + 64 * qc;
+  if (qr == 0 && qc == 1) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = k * 64 + l;
+      W::store4(q + (idx >> 4) * C + (idx & 15) * 4, zero_i4());
+    }
+    return;
+  }
+  const float* a = A + tile * (C * C) + (64 * qr) * C + 64 * qc;
+  f32x4 x[PER];
+  float m = 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = k * 64 + l;
+    const int row = idx >> 4, col = (idx & 15) * 4;
+    x[k] = *(const f32x4*)(a + row * C + col);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if (qr == qc && row <= col + v) x[k][v] = 0.f;
+      m = fmaxf(m, fabsf(x[k][v]));
+    }
+  }
+  const float amax =
+      __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
+  const int e = W::qexp(amax);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = k * 64 + l;
+    i32x4 r;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) r[v] = (int)rintf(ldexpf(x[k][v], -e));
+    W::store4(q + (idx >> 4) * C + (idx & 15) * 4, r);
+  }
+  if (l == 0) eA[3 * tile + qr + qc] = e;
+}
+
+}  // namespace iq
+}  // namespace gdn

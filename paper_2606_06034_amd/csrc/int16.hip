@@ -26,6 +26,7 @@
 // fp64 integer by 2^s is rint(ldexp(x, -s)): the scaling is exact and rint
 // rounds half to even.
 #include "chunk.hpp"
+#include "int128.hpp"
 #include "intq.hpp"
 #include "launch.hpp"
 
@@ -449,6 +450,140 @@ __global__ __launch_bounds__(64) void k_inverse_i16_fused(const TK* __restrict__
   store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
 }
 
+// ---------------------------------------------------------------------------
+// The INT16 width at C = 128 (k_neumann_int128, k_quantize_int128): the
+// engine's limb fragments plus full 64 x 64 blocks with products as fp64
+// integers.
+
+struct FullD {
+  f64x4 a[16];  // block (I, J) at 4 I + J
+};
+
+__device__ __forceinline__ void to_rowl_full(RowL<4>& X, const FullI& D) {
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) {
+      X.h.r[I].v[K] = pack_hi(D.a[4 * I + K]);
+      X.l.r[I].v[K] = pack_lo(D.a[4 * I + K]);
+    }
+}
+
+// D = X Y exactly over all 16 output blocks; OUTQ: row-form result
+template <bool OUTQ>
+__device__ __forceinline__ void mml_full(FullD& D, const RowL<4>& X, const ColL<4>& Y) {
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J) {
+      const i32x4 xh = X.h.r[I].v, xl = X.l.r[I].v, yh = Y.h.c[J].v, yl = Y.l.c[J].v;
+      const i32x4 z = zero_i4();
+      i32x4 hh, mx, ll;
+      if constexpr (OUTQ) {
+        hh = __builtin_amdgcn_mfma_i32_16x16x64_i8(yh, xh, z, 0, 0, 0);
+        mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(yl, xh, z, 0, 0, 0);
+        mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(yh, xl, mx, 0, 0, 0);
+        ll = __builtin_amdgcn_mfma_i32_16x16x64_i8(yl, xl, z, 0, 0, 0);
+      } else {
+        hh = __builtin_amdgcn_mfma_i32_16x16x64_i8(xh, yh, z, 0, 0, 0);
+        mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(xh, yl, z, 0, 0, 0);
+        mx = __builtin_amdgcn_mfma_i32_16x16x64_i8(xl, yh, mx, 0, 0, 0);
+        ll = __builtin_amdgcn_mfma_i32_16x16x64_i8(xl, yl, z, 0, 0, 0);
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        D.a[4 * I + J][v] = __builtin_fma((double)(hh[v] * 256 + mx[v]), 256.0, (double)ll[v]);
+    }
+}
+
+struct I16W : I16Ops<4> {
+  using Code = int16_t;
+  using FProd = FullD;
+  static __device__ __forceinline__ i32x4 load4(const int16_t* p) {
+    return unpack4_16(*(const int2*)p);
+  }
+  static __device__ __forceinline__ void store4(int16_t* p, i32x4 q) { *(int2*)p = pack4_16(q); }
+  static __device__ __forceinline__ int qexp(float amax) { return quant_exp(amax); }
+  template <int NC, int SC>
+  static __device__ __forceinline__ void engine(const AccI<4>& Lr, int eL, int N, int S,
+                                                AccI<4>& Tr, int& eTo) {
+    int_engine<I16Ops, 4, NC, SC>(Lr, eL, N, S, Tr, eTo);
+  }
+  static __device__ __forceinline__ void to_frow(Row& X, const FullI& D) { to_rowl_full(X, D); }
+  // limb by limb through the identity (exact)
+  static __device__ __forceinline__ void frow_to_col(Col& Y, const Row& X, const ColQ<4>& Ic) {
+    FullI h, l;
+    mmi_full<false>(h, X.h, Ic);
+    mmi_full<false>(l, X.l, Ic);
+    to_colq_full(Y.h, h);
+    to_colq_full(Y.l, l);
+  }
+  template <bool OUTQ>
+  static __device__ __forceinline__ void fmm(FProd& D, const Row& X, const Col& Y) {
+    mml_full<OUTQ>(D, X, Y);
+  }
+  // the codes 256 h + l of block (I, K) of a row-form limb fragment
+  static __device__ __forceinline__ i32x4 codes(const Row& X, int I, int K) {
+    return unpack4(X.h.r[I].v[K]) * 256 + unpack4(X.l.r[I].v[K]);
+  }
+  // The running sum of two terms, requantised: the codes of the fragments
+  // t1 (exponent e1), then the exact product t2 (exponent e2), by the
+  // engine's rules (the first present term 16 guard bits under its quantum,
+  // a larger later term rebases the sum, a finer one is rounded in).  The
+  // exponent plan is wave-uniform, so the sum is one pass per entry, in
+  // place in t2.
+  static __device__ __forceinline__ void sum2(FullI& out, int& eo, bool& nz, const Row& t1,
+                                              int e1, bool p1, FullD& t2, int e2, bool p2) {
+    int e = 0, sh = 0;
+    bool any = false, reb = false;
+    double scr = 1.0;
+    if (p1) {
+      e = e1 + kQB - kAlignBits;
+      any = true;
+    }
+    if (p2) {
+      const int top = e2 + kAccB - kAlignBits;
+      if (!any) {
+        e = top;
+        any = true;
+      } else if (top > e) {
+        reb = true;
+        scr = ldexp(1.0, e - top);
+        e = top;
+      }
+      sh = e2 - e;
+    }
+    const double sc1 = ldexp(1.0, kAlignBits - kQB), sc2 = ldexp(1.0, sh);
+    int m = 0;
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int K = 0; K < 4; ++K) {
+        const i32x4 c1 = codes(t1, I, K);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          double x = p1 ? (double)c1[v] * sc1 : 0.0;
+          if (reb) x = rint(x * scr);
+          if (p2) {
+            const double y = t2.a[4 * I + K][v];
+            x = sh >= 0 ? __builtin_fma(y, sc2, x) : x + rint(y * sc2);
+          }
+          t2.a[4 * I + K][v] = x;
+          m = max(m, __double2hiint(fabs(x)));
+        }
+      }
+    const int amax_hi = wave_max(m);
+    const int s = shift_for_hi(amax_hi);
+    const double sc = ldexp(1.0, -s);
+#pragma unroll
+    for (int b = 0; b < 16; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out.a[b][v] = rne_scaled(t2.a[b][v], sc);
+    nz = amax_hi > 0;
+    eo = nz ? (any ? e : 0) + s : 0;
+  }
+};
+
 // quantiser: e = smallest integer with amax / 2^e <= 32639, q = rne(x / 2^e)
 template <int C>
 __global__ __launch_bounds__(64) void k_quantize_i16(const float* __restrict__ A,
@@ -616,6 +751,10 @@ hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t
     case 64:
       hipLaunchKernelGGL((i16::k_quantize_i16<64>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
       return hipGetLastError();
+    case 128:
+      hipLaunchKernelGGL((iq::k_quantize_int128<i16::I16W>), dim3((unsigned)n), dim3(256), 0, st,
+                         A, Aq, eA);
+      return hipGetLastError();
   }
   return hipErrorNotSupported;
 }
@@ -669,6 +808,14 @@ hipError_t launch_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
     case 16: return run_neumann_i16<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
     case 32: return run_neumann_i16<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
     case 64: return run_neumann_i16<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 128:
+      if (N == 3 && S == 8)
+        hipLaunchKernelGGL((iq::k_neumann_int128<i16::I16W, 3, 8>), dim3((unsigned)n), dim3(128),
+                           0, st, Aq, eA, Tq, eT, Tdeq, N, S);
+      else
+        hipLaunchKernelGGL((iq::k_neumann_int128<i16::I16W, -1, -1>), dim3((unsigned)n),
+                           dim3(128), 0, st, Aq, eA, Tq, eT, Tdeq, N, S);
+      return hipGetLastError();
   }
   return hipErrorNotSupported;
 }

@@ -20,6 +20,7 @@
 //
 // Operands are the int8 quad fragments of intq.hpp.
 #include "chunk.hpp"
+#include "int128.hpp"
 #include "intq.hpp"
 #include "launch.hpp"
 
@@ -328,6 +329,92 @@ __global__ __launch_bounds__(64) void k_inverse_i8_fused(const TK* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// The INT8 width at C = 128 (k_neumann_int128, k_quantize_int128): the
+// engine's fragments plus full 64 x 64 blocks with exact int32 products.
+
+__device__ __forceinline__ void shift_full(FullI& D, int s) {
+#pragma unroll
+  for (int b = 0; b < 16; ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) D.a[b][v] = s >= 31 ? 0 : rne_pos(D.a[b][v], s);
+}
+
+struct I8W : I8Ops<4> {
+  using Code = int8_t;
+  using FProd = FullI;
+  static __device__ __forceinline__ i32x4 load4(const int8_t* p) { return unpack4(*(const int*)p); }
+  static __device__ __forceinline__ void store4(int8_t* p, i32x4 q) { *(int*)p = pack4(q); }
+  static __device__ __forceinline__ int qexp(float amax) { return quant_exp(amax); }
+  template <int NC, int SC>
+  static __device__ __forceinline__ void engine(const AccI<4>& Lr, int eL, int N, int S,
+                                                AccI<4>& Tr, int& eTo) {
+    int_engine<I8Ops, 4, NC, SC>(Lr, eL, N, S, Tr, eTo);
+  }
+  static __device__ __forceinline__ void to_frow(Row& X, const FullI& D) { to_rowq_full(X, D); }
+  static __device__ __forceinline__ void frow_to_col(Col& Y, const Row& X, const ColQ<4>& Ic) {
+    FullI t;
+    mmi_full<false>(t, X, Ic);
+    to_colq_full(Y, t);
+  }
+  template <bool OUTQ>
+  static __device__ __forceinline__ void fmm(FProd& D, const Row& X, const Col& Y) {
+    mmi_full<OUTQ>(D, X, Y);
+  }
+  // the codes of block (I, K) of a row-form fragment
+  static __device__ __forceinline__ i32x4 codes(const Row& X, int I, int K) {
+    return unpack4(X.r[I].v[K]);
+  }
+  // The running sum of two terms, requantised: the codes of the fragments
+  // t1 (exponent e1), then the exact product t2 (exponent e2), by the
+  // engine's rules (the first present term 16 guard bits under its quantum,
+  // a larger later term rebases the sum, a finer one is rounded in).  The
+  // exponent plan is wave-uniform, so the sum is one pass per entry, in
+  // place in t2.
+  static __device__ __forceinline__ void sum2(FullI& out, int& eo, bool& nz, const Row& t1,
+                                              int e1, bool p1, FullI& t2, int e2, bool p2) {
+    int e = 0, reb = 0, sh = 0;
+    bool any = false;
+    if (p1) {
+      e = e1 + kQB - kAlignBits;
+      any = true;
+    }
+    if (p2) {
+      const int top = e2 + kAccB - kAlignBits;
+      if (!any) {
+        e = top;
+        any = true;
+      } else if (top > e) {
+        reb = top - e;
+        e = top;
+      }
+      sh = e2 - e;
+    }
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int K = 0; K < 4; ++K) {
+        const i32x4 c1 = codes(t1, I, K);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          int x = p1 ? c1[v] << (kAlignBits - kQB) : 0;
+          if (reb > 0) x = reb >= 31 ? 0 : rne_pos(x, reb);
+          if (p2) {
+            const int y = t2.a[4 * I + K][v];
+            x += sh >= 0 ? y << sh : (sh > -31 ? rne_pos(y, -sh) : 0);
+          }
+          t2.a[4 * I + K][v] = x;
+        }
+      }
+    const int amax = amax_full(t2);
+    const int s = shift_for(amax);
+    if (s > 0) shift_full(t2, s);
+    out = t2;
+    nz = amax > 0;
+    eo = nz ? (any ? e : 0) + s : 0;
+  }
+};
+
+// ---------------------------------------------------------------------------
 // quantiser: e = smallest integer with amax / 2^e <= 127, q = rne(x / 2^e)
 
 template <int C>
@@ -378,6 +465,10 @@ hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n
     case 64:
       hipLaunchKernelGGL((i8::k_quantize_i8<64>), dim3((unsigned)n), dim3(64), 0, st, A, Aq, eA);
       return hipGetLastError();
+    case 128:
+      hipLaunchKernelGGL((iq::k_quantize_int128<i8::I8W>), dim3((unsigned)n), dim3(256), 0, st, A,
+                         Aq, eA);
+      return hipGetLastError();
   }
   return hipErrorNotSupported;
 }
@@ -401,6 +492,14 @@ hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, in
     case 16: return run_neumann_i8<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
     case 32: return run_neumann_i8<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
     case 64: return run_neumann_i8<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 128:
+      if (N == 3 && S == 8)
+        hipLaunchKernelGGL((iq::k_neumann_int128<i8::I8W, 3, 8>), dim3((unsigned)n), dim3(128), 0,
+                           st, Aq, eA, Tq, eT, Tdeq, N, S);
+      else
+        hipLaunchKernelGGL((iq::k_neumann_int128<i8::I8W, -1, -1>), dim3((unsigned)n), dim3(128),
+                           0, st, Aq, eA, Tq, eT, Tdeq, N, S);
+      return hipGetLastError();
   }
   return hipErrorNotSupported;
 }

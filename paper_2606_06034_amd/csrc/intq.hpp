@@ -144,6 +144,48 @@ __device__ __forceinline__ int amax_of(const AccI<NB>& D, int lo, int hi) {
 
 
 // ---------------------------------------------------------------------------
+// Full 64 x 64 matrices (all 4 x 4 blocks; the off-diagonal block of a
+// C = 128 tile), values as int32 blocks, block (I, J) at 4 I + J.
+
+struct FullI {
+  i32x4 a[16];
+};
+
+__device__ __forceinline__ void to_rowq_full(RowQ<4>& X, const FullI& D) {
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) X.r[I].v[K] = pack4(D.a[4 * I + K]);
+}
+// D in column form
+__device__ __forceinline__ void to_colq_full(ColQ<4>& Y, const FullI& D) {
+#pragma unroll
+  for (int J = 0; J < 4; ++J)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) Y.c[J].v[K] = pack4(D.a[4 * K + J]);
+}
+// D = X Y over all 16 output blocks (X or Y may be lower: its quads carry
+// the zero blocks); OUTQ: row-form result
+template <bool OUTQ>
+__device__ __forceinline__ void mmi_full(FullI& D, const RowQ<4>& X, const ColQ<4>& Y) {
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J)
+      D.a[4 * I + J] =
+          OUTQ ? __builtin_amdgcn_mfma_i32_16x16x64_i8(Y.c[J].v, X.r[I].v, zero_i4(), 0, 0, 0)
+               : __builtin_amdgcn_mfma_i32_16x16x64_i8(X.r[I].v, Y.c[J].v, zero_i4(), 0, 0, 0);
+}
+__device__ __forceinline__ int amax_full(const FullI& D) {
+  int m = 0;
+#pragma unroll
+  for (int b = 0; b < 16; ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) m = max(m, abs(D.a[b][v]));
+  return wave_max(m);
+}
+
+// ---------------------------------------------------------------------------
 // The integer inverse of one tile (Section 3.5, Algorithm 1, in the integer
 // arithmetic the library reads from Appendix G): from Lm = -A as codes (row
 // form, strictly lower) with exponent eL, the masked Neumann powers

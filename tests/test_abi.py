@@ -148,7 +148,9 @@ def test_fused_blockwise_validation():
 @pytest.mark.parametrize("w", ["i8", "i16"])
 def test_int_validation(w):
     q = getattr(L, "gdn_quantize_tiles_" + w)
-    assert q(P1, BIG, 2 * BIG, 4, 128, None) == SHAPE
+    assert q(P1, BIG, 2 * BIG, 4, 48, None) == SHAPE
+    # C = 128: three exponents per tile (48 bytes for 4 tiles)
+    assert q(BIG, 2 * BIG, BIG + 4 * 128 * 128 * 4 - 16, 4, 128, None) == ALIAS
     assert q(P1, None, 2 * BIG, 4, 64, None) == NULL
     assert q(P1, P1, 2 * BIG, 4, 64, None) == ALIAS
     assert q(None, None, None, 0, 64, None) == OK
@@ -157,6 +159,10 @@ def test_int_validation(w):
     assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, None) == NULL
     assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
     assert n(None, None, None, None, None, 0, 64, 3, 8, None) == OK
+    # C = 128: orders up to 63 (64-blocks); eA, eT hold 3 exponents per tile
+    assert n(P1, 2 * BIG, 3 * BIG, 4 * BIG, None, 4, 128, 64, 8, None) == PARAM
+    assert n(P1, 2 * BIG, 3 * BIG, 2 * BIG + 16, None, 4, 128, 63, 8, None) == ALIAS
+    assert n(None, None, None, None, None, 0, 128, 3, 8, None) == OK
     if w == "i16":
         # Tq starting one int8 extent (4 tiles of 64 x 64 bytes) past Aq lies
         # inside the int16 codes

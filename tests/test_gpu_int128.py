@@ -1,0 +1,190 @@
+"""Bit-exact parity of the integer paths at C = 128 (block-wise, three
+exponents per tile; through the C ABI) with the integer oracle, at 8- and
+16-bit codes.
+
+Both sides start from the same float32 A tiles, so the quantiser takes every
+rounding decision on the same values; from there on everything is integer
+arithmetic, and codes and exponents must agree exactly.  Cases: the workload
+distributions (default and wide gates, stress tiles), random codes with
+independent block exponents (every rebase path of the merge's sums), tiles
+with zero blocks (absent terms), compile-time and run-time orders, many tiles
+with a ragged count, and the low-bit workload at full size, sampled.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import gdn
+from oracle import int8 as oi
+
+import paper_2606_06034_amd as G
+
+pytestmark = pytest.mark.gpu
+
+C = 128
+WIDTHS = {
+    "i8": (oi.SPEC8, torch.int8, G.gdn_quantize_tiles_i8, G.gdn_chunk_inverse_neumann_i8),
+    "i16": (oi.SPEC16, torch.int16, G.gdn_quantize_tiles_i16, G.gdn_chunk_inverse_neumann_i16),
+}
+
+
+def f32_tiles(L=512, H=2, gate="wide", stress=False, seed=0):
+    """float32 A tiles [n, 128, 128] of the low-bit workload's distributions."""
+    w = wl.workload("int8")
+    if stress:
+        heads = [wl.gen_stress_head(L, w.dk, C, seed=seed + h) for h in range(H)]
+    else:
+        w = w.with_(L=L, H=H, B=1, gate=gate, seed=w.seed + seed)
+        heads = [wl.gen_head(w, 0, h, C=C, want_v=False) for h in range(H)]
+    K = wl.as_blhd(*[x[0] for x in heads])
+    beta = wl.as_blhd(*[x[1] for x in heads])
+    g = wl.as_blhd(*[x[2] for x in heads])
+    return gdn.tiles_flat(gdn.build_A(K, beta, g, C)).astype(np.float32)
+
+
+def random_codes(n, spec, seed, density=1.0, emin=-30, emax=2):
+    """Random codes in the block layout (strictly lower diagonal blocks, full
+    block 21, zero block 12) with independent exponents per block."""
+    rng = np.random.default_rng([seed, spec.qmax])
+    q = rng.integers(-spec.qmax, spec.qmax + 1, size=(n, C, C))
+    if density < 1.0:
+        q = np.where(rng.random((n, C, C)) < density, q, 0)
+    q = np.tril(q, -1)
+    e = rng.integers(emin, emax + 1, size=(n, 3))
+    return q.astype(np.int64), e.astype(np.int64)
+
+
+def to_dev(x, dt):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dt).to("cuda")
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def check_inverse(width, qA, eA, N, S, label):
+    spec, cdt, _, inv = WIDTHS[width]
+    print(f"{width} C=128 inverse {label} N={N} S={S} n={qA.shape[0]}", flush=True)
+    qT, eT, Td = (host(t) for t in inv(to_dev(qA, cdt), to_dev(eA, torch.int32), N, S,
+                                        want_deq=True))
+    rq, re = oi.neumann_inverse_int_blocked(qA, eA, N, S, spec)
+    assert eT.shape == (qA.shape[0], 3)
+    for t in range(qA.shape[0]):
+        assert np.array_equal(qT[t].astype(np.int64), rq[t]), f"codes of tile {t}"
+        assert np.array_equal(eT[t].astype(np.int64), re[t]), f"exponents of tile {t}"
+    assert np.array_equal(Td, oi.dequant_unit_blocked(rq, re).astype(np.float32))
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+@pytest.mark.parametrize("src", ["default", "wide", "stress"])
+def test_quantize_blocked_bit_exact(width, src):
+    spec, cdt, quant, _ = WIDTHS[width]
+    A = f32_tiles(gate="default" if src == "default" else "wide", stress=src == "stress")
+    A[1, 64:, :64] = 0.0   # a zero block 21
+    A[2, :64, :64] = 0.0   # a zero block 11
+    # entries on and above the diagonal are ignored
+    junk = A + np.triu(np.full((C, C), 1e30, np.float32))
+    print(f"{width} C=128 quantise {src} n={A.shape[0]}", flush=True)
+    qd, ed = quant(to_dev(junk, torch.float32))
+    rq, re = oi.quantize_blocked(A, spec)
+    assert np.array_equal(host(qd).astype(np.int64), rq)
+    assert np.array_equal(host(ed).astype(np.int64), re)
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+@pytest.mark.parametrize("src", ["default", "wide", "stress"])
+def test_inverse_blocked_bit_exact(width, src):
+    spec = WIDTHS[width][0]
+    A = f32_tiles(gate="default" if src == "default" else "wide", stress=src == "stress",
+                  seed=3)
+    qA, eA = oi.quantize_blocked(A, spec)
+    check_inverse(width, qA, eA, 3, 8, src)
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+@pytest.mark.parametrize("N,S", [(3, 8), (0, 5), (3, 0), (2, 3), (7, 7)])
+def test_inverse_blocked_orders_random_codes(width, N, S):
+    spec = WIDTHS[width][0]
+    qA, eA = random_codes(6, spec, seed=N * 16 + S, density=0.3)
+    # block exponents far apart in both directions (rebase and round-in paths)
+    eA[0] = [-20, 3, -20]
+    eA[1] = [2, -25, 2]
+    check_inverse(width, qA, eA, N, S, "random")
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+def test_inverse_blocked_zero_blocks(width):
+    spec = WIDTHS[width][0]
+    A = f32_tiles(H=1, L=768, seed=5)  # 6 tiles
+    A[0] = 0.0                       # all zero: X = I
+    A[1, 64:, :64] = 0.0             # A21 = 0: X21 = 0
+    A[2, :64, :64] = 0.0             # A11 = 0: X11 = I
+    A[3, 64:, 64:] = 0.0             # A22 = 0: X22 = I
+    A[4, :64, :64] = 0.0
+    A[4, 64:, 64:] = 0.0             # only A21: X21 = -A21
+    A[5] = np.tril(np.ones((C, C), np.float32), -1)  # all ones: X = I - Z exactly
+    qA, eA = oi.quantize_blocked(A, spec)
+    check_inverse(width, qA, eA, 3, 8, "zero blocks")
+    _, cdt, _, inv = WIDTHS[width]
+    qT, eT = (host(t) for t in inv(to_dev(qA, cdt), to_dev(eA, torch.int32), 3, 8))
+    assert not np.any(qT[0]) and not np.any(eT[0])
+    assert np.array_equal(qT[4, 64:, :64].astype(np.int64), -qA[4, 64:, :64])
+    assert np.array_equal(oi.dequant_unit_blocked(qT[5:6], eT[5:6])[0],
+                          np.eye(C) - np.eye(C, k=-1))
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+def test_blocked_many_tiles_odd_count_and_without_dequant(width):
+    spec, cdt, quant, inv = WIDTHS[width]
+    A = f32_tiles(H=3, L=1280, seed=7)[:29]
+    print(f"{width} C=128 pipeline n={A.shape[0]}", flush=True)
+    qd, ed = quant(to_dev(A, torch.float32))
+    qT, eT = inv(qd, ed, 3, 8)
+    qT2, eT2, _ = inv(qd, ed, 3, 8, want_deq=True)
+    rq, re = oi.quantize_blocked(A, spec)
+    rT, rE = oi.neumann_inverse_int_blocked(rq, re, 3, 8, spec)
+    assert np.array_equal(host(qT).astype(np.int64), rT)
+    assert np.array_equal(host(eT).astype(np.int64), rE)
+    assert torch.equal(qT, qT2) and torch.equal(eT, eT2)
+
+
+@pytest.fixture(scope="module")
+def full_size_tiles():
+    """The low-bit workload at C = 128 and full size (B=4, H=32, L=16384:
+    16384 tiles), float32 A built by the oracle head by head."""
+    w = wl.workload("int8").with_(C=C)
+    nc = w.L // C
+    A = np.empty((w.B * w.H * nc, C, C), np.float32)
+    for b in range(w.B):
+        for h in range(w.H):
+            K, beta, g, _ = wl.gen_head(w, b, h, C=C, want_v=False)
+            t0 = (b * w.H + h) * nc
+            A[t0:t0 + nc] = gdn.tiles_flat(
+                gdn.build_A(K[None, :, None], beta[None, :, None], g[None, :, None], C))
+    print(f"C=128 full size: {A.shape[0]} tiles generated", flush=True)
+    return A
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+def test_blocked_full_size_sampled(width, full_size_tiles):
+    """One launch of each kernel over all 16384 tiles; a sample of tiles (the
+    first, the last and 126 drawn) compared with the oracle."""
+    spec, cdt, quant, inv = WIDTHS[width]
+    A = full_size_tiles
+    qd, ed = quant(to_dev(A, torch.float32))
+    qT, eT, Td = inv(qd, ed, 3, 8, want_deq=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(128)
+    idx = np.sort(np.concatenate([[0, A.shape[0] - 1],
+                                  rng.choice(np.arange(1, A.shape[0] - 1), 126, replace=False)]))
+    idx_t = torch.from_numpy(idx).to("cuda")
+    rq, re = oi.quantize_blocked(A[idx], spec)
+    assert np.array_equal(host(qd[idx_t]).astype(np.int64), rq)
+    assert np.array_equal(host(ed[idx_t]).astype(np.int64), re)
+    rT, rE = oi.neumann_inverse_int_blocked(rq, re, 3, 8, spec)
+    assert np.array_equal(host(qT[idx_t]).astype(np.int64), rT)
+    assert np.array_equal(host(eT[idx_t]).astype(np.int64), rE)
+    assert np.array_equal(host(Td[idx_t]), oi.dequant_unit_blocked(rT, rE).astype(np.float32))
