@@ -157,46 +157,20 @@ def main():
     elif low:
         qdt, sfx = (torch.int8, "i8") if a.path == "int8" else (torch.int16, "i16")
         dTq = torch.empty((w.B, w.H, w.L // C, C, C), dtype=qdt, device="cuda")
-        if C < 128:
-            fused = getattr(G, f"gdn_chunk_inverse_neumann_{sfx}_fused")
-            deT = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
-            step = lambda: fused(dK, db, dg, C, N, S, Tq=dTq, eT=deT)
-        else:
-            # C = 128 (block-wise, three exponents per tile): build A in fp32,
-            # quantise, integer inverse; the inverse launch is timed inside
-            # the step by an event pair of its own
-            quant128 = getattr(G, f"gdn_quantize_tiles_{sfx}")
-            inv128 = getattr(G, f"gdn_chunk_inverse_neumann_{sfx}")
-            dA128 = torch.empty((w.B, w.H, w.L // C, C, C), dtype=torch.float32, device="cuda")
-            dAq128 = torch.empty_like(dTq)
-            deA128 = torch.empty((n_tiles, 3), dtype=torch.int32, device="cuda")
-            deT = torch.empty_like(deA128)
-            inv_events = []
-
-            def step():
-                G.gdn_build_A(dK, db, dg, C, A=dA128)
-                quant128(dA128, Aq=dAq128, eA=deA128)
-                if timing[0]:
-                    ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                    ev[0].record(stream)
-                    inv128(dAq128, deA128, N, S, Tq=dTq, eT=deT)
-                    ev[1].record(stream)
-                    inv_events.append(ev)
-                else:
-                    inv128(dAq128, deA128, N, S, Tq=dTq, eT=deT)
+        fused = getattr(G, f"gdn_chunk_inverse_neumann_{sfx}_fused")
+        # C = 128: block-wise, three exponents per tile
+        deT = torch.empty((n_tiles, 3) if C == 128 else n_tiles, dtype=torch.int32, device="cuda")
+        step = lambda: fused(dK, db, dg, C, N, S, Tq=dTq, eT=deT)
     elif a.path == "blockwise":
         step = lambda: G.gdn_chunk_inverse_blockwise(dA, Tinv=dT)
     else:
         step = lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT)
 
-    timing = [False]  # True while the timed steps run
-    multi = low and C == 128
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    timing[0] = True
     t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(a.steps):
@@ -204,12 +178,7 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    timing[0] = False
-    # HIP-event time per step (one launch for fused/inverse/fwdsub)
-    step_ev_ms = e0.elapsed_time(e1) / a.steps
-    ev_ms = step_ev_ms
-    if multi:  # the dominant kernel's own launches inside the timed steps
-        ev_ms = sum(x.elapsed_time(y) for x, y in inv_events) / len(inv_events)
+    ev_ms = e0.elapsed_time(e1) / a.steps  # HIP-event time per step (one launch for fused/inverse/fwdsub)
     ms_per_step = wall * 1e3 / a.steps
     value = n_tiles / (ms_per_step * 1e-3)
     if low:  # context: the same path as three launches
@@ -266,33 +235,22 @@ def main():
         flops = n_tiles * (C ** 3 - C) // 3  # sum over i > j of (i - j) FMAs = (C^3 - C) / 6
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
         kernel = "k_fwdsub" if a.path == "fwdsub" else "k_blockwise"
-    elif low and C == 128:
-        # the dominant kernel, the block-wise integer inverse: codes and
-        # exponents in and out; 2 (N + S) + 2 products of 64 x 64 blocks,
-        # an INT16 product as four int8 MFMA products over the limbs
-        qb = 1 if a.path == "int8" else 2
-        bytes_ = n_tiles * 2 * (C * C * qb + 12)
-        flops = (2 * (N + S) + 2) * 2 * 64 ** 3 * n_tiles * qb * qb
-        if flops / bytes_ >= INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-            bound, peak, unit = "mfma", INT8_PEAK_TOPS, "TOP/s"
-            achieved = flops / (ev_ms * 1e-3) / 1e12
-        else:
-            bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
-            achieved = bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = "k_neumann_int128"
     elif low:
         # K (dk per token) and beta, g in; T_hat codes and exponents out.  An
         # INT16 product is four int8 MFMA products over the codes' limbs.
+        # C = 128: three exponents per tile, 2 (N + S) + 2 products of 64-blocks.
         qb = 1 if a.path == "int8" else 2
-        bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C * qb + 4)
+        bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C * qb + 4 * (3 if C == 128 else 1))
         flops = (N + S) * 2 * C ** 3 * n_tiles * qb * qb  # int8 MFMA ops of the N + S products
+        if C == 128:
+            flops = (2 * (N + S) + 2) * 2 * 64 ** 3 * n_tiles * qb * qb
         if flops / bytes_ >= INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
             bound, peak, unit = "mfma", INT8_PEAK_TOPS, "TOP/s"
             achieved = flops / (ev_ms * 1e-3) / 1e12
         else:
             bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
             achieved = bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = f"k_inverse_{sfx}_fused"
+        kernel = f"k_inverse_{sfx}_fused" if C < 128 else "k_inverse_int128_fused"
     else:
         bytes_ = None
         flops = f_inv
@@ -334,8 +292,6 @@ def main():
                                             "inverse_" + sfx: round(stage_ms[2], 6)}
         if C < 128:
             out["config"]["fwdsub_" + sfx + "_ms"] = round(stage_ms[3], 6)
-        else:
-            out["config"]["step_ms_hip_events"] = round(step_ev_ms, 6)
         out["dtype"] = sfx
         if not a.no_cpu_baseline:
             out["cpu_baseline"] = cpu_baseline_int(w, C, N, S, a, (K, beta, g), dTq, deT,
@@ -681,8 +637,8 @@ PROFILES = {("fused", "qwen35_prefill", 64): ("k_fused_qwen35_prefill.md", "pipe
             ("inverse", "sweep", 64): ("k_neumann_sweep_c64.md", "neumann.hip"),
             ("int8", "int8", 64): ("k_inverse_i8_fused_int8.md", "int8.hip"),
             ("int16", "int8", 64): ("k_inverse_i16_fused_int8.md", "int16.hip"),
-            ("int8", "int8", 128): ("k_neumann_int128_i8_int8.md", "int8.hip"),
-            ("int16", "int8", 128): ("k_neumann_int128_i16_int8.md", "int16.hip"),
+            ("int8", "int8", 128): ("k_inverse_int128_fused_i8_int8.md", "int8.hip"),
+            ("int16", "int8", 128): ("k_inverse_int128_fused_i16_int8.md", "int16.hip"),
             ("forward", "qwen35_prefill", 64): ("k_fwd_state_qwen35_prefill.md", "forward.hip")}
 
 

@@ -205,8 +205,10 @@ int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq
  * gdn_chunk_inverse_neumann_i8 (Section 3.5, Appendix G).  K: [B, L, H, dk]
  * in k_dtype (GDN_F32 or GDN_BF16); beta, g: [B, L, H] fp32.  Outputs as
  * gdn_chunk_inverse_neumann_i8, in the [B, H, L/C, C, C] tile order.
- * C in {16, 32, 64}.  Given the same fp32 A tile the codes equal those of
- * gdn_quantize_tiles_i8 followed by gdn_chunk_inverse_neumann_i8. */
+ * C in {16, 32, 64, 128}; C = 128 block-wise with eT [n_tiles, 3] (A in
+ * fp32 block by block, each block quantised with its own exponent, then the
+ * block-wise integer inverse).  Given the same fp32 A tile the codes equal
+ * those of gdn_quantize_tiles_i8 followed by gdn_chunk_inverse_neumann_i8. */
 int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const float* g,
                                        int8_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                        int dk, int C, int N, int S, int k_dtype, void* stream);
@@ -265,9 +267,9 @@ int gdn_chunk_inverse_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq,
  * gdn_build_A writes with a_dtype GDN_F32), quantised per tile in registers
  * by the rule of gdn_quantize_tiles_i16, then the integer inverse of
  * gdn_chunk_inverse_neumann_i16.  Arguments and layouts as
- * gdn_chunk_inverse_neumann_i8_fused, with int16 Tq.  Given the same fp32 A
- * tile the codes equal those of gdn_quantize_tiles_i16 followed by
- * gdn_chunk_inverse_neumann_i16. */
+ * gdn_chunk_inverse_neumann_i8_fused, with int16 Tq (C = 128 block-wise with
+ * eT [n_tiles, 3]).  Given the same fp32 A tile the codes equal those of
+ * gdn_quantize_tiles_i16 followed by gdn_chunk_inverse_neumann_i16. */
 int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const float* g,
                                         int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L,
                                         int H, int dk, int C, int N, int S, int k_dtype,

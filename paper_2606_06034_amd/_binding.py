@@ -309,14 +309,16 @@ def gdn_chunk_inverse_neumann_i8_fused(K: torch.Tensor, beta: torch.Tensor, g: t
     shape = (B, H, nc, C, C)
     n = B * H * nc
     Tq = torch.empty(shape, dtype=torch.int8, device=K.device) if Tq is None else Tq
-    eT = torch.empty(n, dtype=torch.int32, device=K.device) if eT is None else eT
+    ne = _nexp(C)
+    if eT is None:
+        eT = torch.empty((n, 3) if ne == 3 else n, dtype=torch.int32, device=K.device)
     Td = Tdeq
     if want_deq and Td is None:
         Td = torch.empty(shape, dtype=torch.float32, device=K.device)
     tok = B * L * H
     _check("gdn_chunk_inverse_neumann_i8_fused", lib.gdn_chunk_inverse_neumann_i8_fused(
         _dev(K, "K"), _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
-        _dev(Tq, "Tq", torch.int8, n * C * C), _dev(eT, "eT", torch.int32, n),
+        _dev(Tq, "Tq", torch.int8, n * C * C), _dev(eT, "eT", torch.int32, n * ne),
         _dev(Td, "Tdeq", torch.float32, n * C * C) if Td is not None else None,
         B, L, H, dk, C, N, S, _fdtype(K, "K"), _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)
@@ -410,14 +412,16 @@ def gdn_chunk_inverse_neumann_i16_fused(K: torch.Tensor, beta: torch.Tensor, g: 
     shape = (B, H, nc, C, C)
     n = B * H * nc
     Tq = torch.empty(shape, dtype=torch.int16, device=K.device) if Tq is None else Tq
-    eT = torch.empty(n, dtype=torch.int32, device=K.device) if eT is None else eT
+    ne = _nexp(C)
+    if eT is None:
+        eT = torch.empty((n, 3) if ne == 3 else n, dtype=torch.int32, device=K.device)
     Td = Tdeq
     if want_deq and Td is None:
         Td = torch.empty(shape, dtype=torch.float32, device=K.device)
     tok = B * L * H
     _check("gdn_chunk_inverse_neumann_i16_fused", lib.gdn_chunk_inverse_neumann_i16_fused(
         _dev(K, "K"), _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
-        _dev(Tq, "Tq", torch.int16, n * C * C), _dev(eT, "eT", torch.int32, n),
+        _dev(Tq, "Tq", torch.int16, n * C * C), _dev(eT, "eT", torch.int32, n * ne),
         _dev(Td, "Tdeq", torch.float32, n * C * C) if Td is not None else None,
         B, L, H, dk, C, N, S, _fdtype(K, "K"), _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)

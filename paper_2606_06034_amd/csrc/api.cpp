@@ -324,7 +324,6 @@ int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq
 int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const float* g,
                                        int8_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                        int dk, int C, int N, int S, int k_dtype, void* stream) {
-  if (C == 128) return GDN_ERR_SHAPE;
   int64_t n = 0;
   if (int r = check_chunked(B, L, H, C, &n)) return r;
   if (!valid_d(dk)) return GDN_ERR_SHAPE;
@@ -336,7 +335,7 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
       (Tdeq && !aligned(Tdeq)))
     return GDN_ERR_ALIGN;
   const int64_t tok = (int64_t)B * L * H;
-  const int64_t qb = n * C * C, eb = n * 4, db = n * C * C * 4;
+  const int64_t qb = n * C * C, eb = n * 4 * nexp(C), db = n * C * C * 4;
   const void* ins[3] = {K, beta, g};
   const int64_t inb[3] = {tok * dk * esize(k_dtype), tok * 4, tok * 4};
   for (int i = 0; i < 3; ++i)
@@ -430,7 +429,6 @@ int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const 
                                         int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L,
                                         int H, int dk, int C, int N, int S, int k_dtype,
                                         void* stream) {
-  if (C == 128) return GDN_ERR_SHAPE;
   int64_t n = 0;
   if (int r = check_chunked(B, L, H, C, &n)) return r;
   if (!valid_d(dk)) return GDN_ERR_SHAPE;
@@ -442,7 +440,7 @@ int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const 
       (Tdeq && !aligned(Tdeq)))
     return GDN_ERR_ALIGN;
   const int64_t tok = (int64_t)B * L * H;
-  const int64_t qb = n * C * C * 2, eb = n * 4, db = n * C * C * 4;
+  const int64_t qb = n * C * C * 2, eb = n * 4 * nexp(C), db = n * C * C * 4;
   const void* ins[3] = {K, beta, g};
   const int64_t inb[3] = {tok * dk * esize(k_dtype), tok * 4, tok * 4};
   for (int i = 0; i < 3; ++i)

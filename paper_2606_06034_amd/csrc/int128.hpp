@@ -24,6 +24,7 @@
 // requantised to codes).
 #pragma once
 
+#include "chunk.hpp"
 #include "intq.hpp"
 
 namespace gdn {
@@ -48,37 +49,25 @@ __device__ __forceinline__ void store_deq_diag(float* td, const AccI<4>& Tr, int
     }
 }
 
-template <typename W, int NC, int SC>
-__global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* __restrict__ Aq,
-                                                        const int32_t* __restrict__ eA,
-                                                        typename W::Code* __restrict__ Tq,
-                                                        int32_t* __restrict__ eT,
-                                                        float* __restrict__ Tdeq, int Nrt,
-                                                        int Srt) {
-  using Code = typename W::Code;
-  constexpr int C = 128, LD = 68;  // LD: padded row stride of the N11 hand-over (ints)
-  __shared__ __attribute__((aligned(16))) int sN[64 * LD];  // sN[j * LD + i] = N11[i][j]
-  __shared__ int sInfo[2];
-  const int64_t tile = blockIdx.x;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+// LDS hand-over of one 64 x 64 int32 matrix: padded rows of 68 ints (16-byte
+// aligned rows, fewer bank conflicts on transposed access)
+constexpr int kLD = 68;
+
+// One C = 128 tile after the diagonal blocks' codes are in registers.
+// Wave w (w = 0, 1) holds Lm = -A_ww (row form, strict lower) with exponent
+// eL; a21(A, ea) gives wave 0 the codes of A21 (row form, all 16 blocks) and
+// their exponent.  Wave w inverts its block with the engine and writes it;
+// wave 0 hands N11 (transposed) and A21 to wave 1 through LDS and leaves;
+// wave 1 forms X21.  Outputs for the tile: t (codes, 128 x 128), et (three
+// exponents), td (nullable, fp32).
+template <typename W, int NC, int SC, typename A21Fn>
+__device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL, A21Fn&& a21,
+                                            typename W::Code* __restrict__ t,
+                                            int32_t* __restrict__ et, float* __restrict__ td,
+                                            int Nrt, int Srt, int* sN, int* sA, int* sInfo) {
+  constexpr int C = 128, LD = kLD;
   const int g = lane_g(), c = lane_c();
   const int r0 = 64 * wv;
-  const Code* a = Aq + tile * (C * C);
-  Code* t = Tq + tile * (C * C);
-  float* td = Tdeq ? Tdeq + tile * (C * C) : nullptr;
-
-  // ---- this wave's diagonal block: Lm = -A_ww (row form), strictly lower
-  AccI<4> Lr;
-#pragma unroll
-  for (int I = 0; I < 4; ++I)
-#pragma unroll
-    for (int J = 0; J <= I; ++J) {
-      i32x4 x = W::load4(a + (r0 + I * 16 + c) * C + r0 + J * 16 + 4 * g);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
-      Lr.a[bidx(I, J)] = x;
-    }
-  const int eL = __builtin_amdgcn_readfirstlane(eA[3 * tile + 2 * wv]);
   AccI<4> Tr;
   int eTo;
   W::template engine<NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
@@ -95,7 +84,7 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
     for (int I = 0; I < 4; ++I)
 #pragma unroll
       for (int J = 0; J < 4; ++J) W::store4(t + (I * 16 + c) * C + 64 + J * 16 + 4 * g, zero_i4());
-  if (lane_id() == 0) eT[3 * tile + 2 * wv] = eTo;
+  if (lane_id() == 0) et[2 * wv] = eTo;
   if (td) {
     store_deq_diag(td + r0 * C + r0, Tr, eTo);
     if (wv == 0)
@@ -114,9 +103,18 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
       for (int J = 0; J <= I; ++J)
 #pragma unroll
         for (int v = 0; v < 4; ++v) sN[(16 * J + 4 * g + v) * LD + 16 * I + c] = Tr.a[bidx(I, J)][v];
+    // A21 (row form) to LDS row-major
+    FullI A;
+    int ea;
+    a21(A, ea);
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J) *(i32x4*)&sA[(16 * I + c) * LD + 16 * J + 4 * g] = A.a[4 * I + J];
     if (lane_id() == 0) {
       sInfo[0] = eTo;
       sInfo[1] = nzT ? 1 : 0;
+      sInfo[2] = ea;
     }
   }
   __syncthreads();
@@ -130,6 +128,7 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
     for (int K = J; K < 4; ++K) N11c.a[bidx(K, J)] = *(const i32x4*)&sN[(16 * J + c) * LD + 16 * K + 4 * g];
   const int e11 = __builtin_amdgcn_readfirstlane(sInfo[0]);
   const bool nz11 = __builtin_amdgcn_readfirstlane(sInfo[1]) != 0;
+  const int ea = __builtin_amdgcn_readfirstlane(sInfo[2]);
   typename W::Col N11q;
   W::to_col(N11q, N11c, 1, 63);
 
@@ -137,8 +136,7 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
 #pragma unroll
   for (int I = 0; I < 4; ++I)
 #pragma unroll
-    for (int J = 0; J < 4; ++J) A21.a[4 * I + J] = W::load4(a + (64 + I * 16 + c) * C + J * 16 + 4 * g);
-  const int ea = __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]);
+    for (int J = 0; J < 4; ++J) A21.a[4 * I + J] = *(const i32x4*)&sA[(16 * I + c) * LD + 16 * J + 4 * g];
   const bool nzA = amax_full(A21) > 0;
 
   typename W::Row X;  // A21, then P, as row-form fragments (sum2 reads the codes back)
@@ -169,7 +167,7 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
 #pragma unroll
     for (int J = 0; J < 4; ++J)
       W::store4(t + (64 + I * 16 + c) * C + J * 16 + 4 * g, zero_i4() - Xs.a[4 * I + J]);
-  if (lane_id() == 0) eT[3 * tile + 1] = e21;
+  if (lane_id() == 0) et[1] = e21;
   if (td)
 #pragma unroll
     for (int I = 0; I < 4; ++I)
@@ -180,6 +178,142 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
         for (int v = 0; v < 4; ++v) x[v] = ldexpf((float)-Xs.a[4 * I + J][v], e21);
         *(f32x4*)(td + (64 + I * 16 + c) * C + J * 16 + 4 * g) = x;
       }
+}
+
+// The integer inverse at C = 128 from codes (gdn_quantize_tiles_* layout).
+template <typename W, int NC, int SC>
+__global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* __restrict__ Aq,
+                                                        const int32_t* __restrict__ eA,
+                                                        typename W::Code* __restrict__ Tq,
+                                                        int32_t* __restrict__ eT,
+                                                        float* __restrict__ Tdeq, int Nrt,
+                                                        int Srt) {
+  using Code = typename W::Code;
+  constexpr int C = 128;
+  __shared__ __attribute__((aligned(16))) int sN[64 * kLD];  // sN[j * kLD + i] = N11[i][j]
+  __shared__ __attribute__((aligned(16))) int sA[64 * kLD];  // sA[i * kLD + j] = A21[i][j]
+  __shared__ int sInfo[4];
+  const int64_t tile = blockIdx.x;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane_g(), c = lane_c();
+  const int r0 = 64 * wv;
+  const Code* a = Aq + tile * (C * C);
+
+  // ---- this wave's diagonal block: Lm = -A_ww (row form), strictly lower
+  AccI<4> Lr;
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 x = W::load4(a + (r0 + I * 16 + c) * C + r0 + J * 16 + 4 * g);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) x[v] = drow(I - J, v) > 0 ? -x[v] : 0;
+      Lr.a[bidx(I, J)] = x;
+    }
+  const int eL = __builtin_amdgcn_readfirstlane(eA[3 * tile + 2 * wv]);
+  auto a21 = [&](FullI& A, int& ea) {
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J) A.a[4 * I + J] = W::load4(a + (64 + I * 16 + c) * C + J * 16 + 4 * g);
+    ea = __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]);
+  };
+  int128_tile<W, NC, SC>(wv, Lr, eL, a21, Tq + tile * (C * C), eT + 3 * tile,
+                         Tdeq ? Tdeq + tile * (C * C) : nullptr, Nrt, Srt, sN, sA, sInfo);
+}
+
+// The whole integer path at C = 128 in one launch: A in fp32 from K, beta,
+// g (the values gdn_build_A writes: the same Gram products in the same order
+// and the same gates), each block quantised in registers by the block-wise
+// quantiser's rule, then the block-wise integer inverse.  Wave w forms its
+// diagonal block; wave 0 forms A21 after its engine.
+template <typename W, int DK, typename F, typename TK, int NC, int SC>
+__global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restrict__ K,
+                                                              const float* __restrict__ beta,
+                                                              const float* __restrict__ g,
+                                                              typename W::Code* __restrict__ Tq,
+                                                              int32_t* __restrict__ eT,
+                                                              float* __restrict__ Tdeq, int L,
+                                                              int H, int Nrt, int Srt) {
+  constexpr int C = 128;
+  __shared__ float sb[C], sg[C];
+  __shared__ __attribute__((aligned(16))) int sN[64 * kLD];
+  __shared__ __attribute__((aligned(16))) int sA[64 * kLD];
+  __shared__ int sInfo[4];
+  const Chunk ch(blockIdx.x, L, H, C);
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const Lane ln = lane_here();
+  const int64_t ldk = (int64_t)H * DK;
+  load_gates<C>(beta, g, ch, L, H, sb, sg);  // both waves (it ends in a workgroup barrier)
+
+  // ---- this wave's diagonal block of A (fp32, row form), quantised
+  AccI<4> Lr;
+  int eL;
+  {
+    Acc<4> G;
+    {
+      Pair<F> kp[4][DK / 32];
+      load_rows<4, DK>(kp, K + ch.row(64 * wv, L, H, DK), ldk);
+      gram_lower<4, DK, true>(G, kp);
+    }
+    gate_scale<4, true>(G, sb + 64 * wv, sg + 64 * wv, 1.f);
+    float m = 0.f;
+#pragma unroll
+    for (int b = 0; b < nlower(4); ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) m = fmaxf(m, fabsf(G.a[b][v]));
+    eL = W::qexp(
+        __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m)))));
+#pragma unroll
+    for (int b = 0; b < nlower(4); ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -eL));
+  }
+  // ---- A21 (wave 0, after its engine): the Gram of the K rows of half 2
+  // against those of half 1, slice by slice in the feature order of the
+  // full Gram product, then the gates, then its own exponent
+  auto a21 = [&](FullI& A, int& ea) {
+    f32x4 G2[4][4];
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J) G2[I][J] = zero4();
+#pragma unroll
+    for (int q = 0; q < DK / 32; ++q) {
+      Pair<F> k1[4], k2[4];
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        k1[I] = load_row8<F>(K + ch.row(I * 16 + ln.c(), L, H, DK) + 32 * q + 8 * ln.g());
+        k2[I] = load_row8<F>(K + ch.row(64 + I * 16 + ln.c(), L, H, DK) + 32 * q + 8 * ln.g());
+      }
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int J = 0; J < 4; ++J) G2[I][J] = Pair<F>::template mma<true>(k2[I], k1[J], G2[I][J]);
+    }
+    const int gg = ln.g(), c = ln.c();
+    float m = 0.f;
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int i = 64 + I * 16 + c, j = J * 16 + 4 * gg + v;
+          G2[I][J][v] = 1.f * sb[i] * G2[I][J][v] * __expf(sg[i] - sg[j]);
+          m = fmaxf(m, fabsf(G2[I][J][v]));
+        }
+    ea = W::qexp(
+        __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m)))));
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) A.a[4 * I + J][v] = (int)rintf(ldexpf(G2[I][J][v], -ea));
+  };
+  int128_tile<W, NC, SC>(wv, Lr, eL, a21, Tq + ch.tile * (C * C), eT + 3 * ch.tile,
+                         Tdeq ? Tdeq + ch.tile * (C * C) : nullptr, Nrt, Srt, sN, sA, sInfo);
 }
 
 // Quantiser at C = 128: four waves per tile, wave w on the 64 x 64 quadrant

@@ -523,10 +523,40 @@ static hipError_t run_i8_fused(const void* K, const float* beta, const float* g,
   return hipGetLastError();
 }
 
+// C = 128 in one launch (k_inverse_int128_fused), two waves per tile
+template <typename W>
+static hipError_t run_int128_fused(const void* K, const float* beta, const float* g,
+                                   typename W::Code* Tq, int32_t* eT, float* Tdeq, int64_t n,
+                                   int L, int H, int dk, int N, int S, int k_dtype,
+                                   hipStream_t st) {
+#define GDN_I128F(DK, F, TK, NC_, SC_)                                                         \
+  hipLaunchKernelGGL((iq::k_inverse_int128_fused<W, DK, F, TK, NC_, SC_>), dim3((unsigned)n), \
+                     dim3(128), 0, st, (const TK*)K, beta, g, Tq, eT, Tdeq, L, H, N, S)
+#define GDN_I128F_ORD(DK, F, TK)                       \
+  if (N == 3 && S == 8) GDN_I128F(DK, F, TK, 3, 8);   \
+  else GDN_I128F(DK, F, TK, -1, -1)
+  if (k_dtype == 1) {
+    if (dk == 64) { GDN_I128F_ORD(64, bf16x4, __bf16); }
+    else if (dk == 128) { GDN_I128F_ORD(128, bf16x4, __bf16); }
+    else return hipErrorNotSupported;
+  } else if (k_dtype == 0) {
+    if (dk == 64) { GDN_I128F_ORD(64, f32x4, float); }
+    else if (dk == 128) { GDN_I128F_ORD(128, f32x4, float); }
+    else return hipErrorNotSupported;
+  } else {
+    return hipErrorNotSupported;
+  }
+#undef GDN_I128F_ORD
+#undef GDN_I128F
+  return hipGetLastError();
+}
+
 hipError_t launch_inverse_i8_fused(const void* K, const float* beta, const float* g, int8_t* Tq,
                                    int32_t* eT, float* Tdeq, int B, int L, int H, int dk, int C,
                                    int N, int S, int k_dtype, hipStream_t st) {
   const int64_t n = (int64_t)B * H * (L / C);
+  if (C == 128)
+    return run_int128_fused<i8::I8W>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, k_dtype, st);
   if (k_dtype == 1) {
     switch (C) {
       case 16: return run_i8_fused<1, 3, 2, bf16x4, __bf16>(K, beta, g, Tq, eT, Tdeq, n, L, H, dk, N, S, st);

@@ -205,7 +205,10 @@ def test_int_fused_validation(w):
                "kdt"].index(k)] = v
         return f(*a)
 
-    assert call(C=128) == SHAPE       # the integer paths cover C <= 64
+    # C = 128 (block-wise): orders up to 63, L % 128 == 0, three exponents per tile
+    assert call(C=128, N=64) == PARAM
+    assert call(C=128, L=192) == SHAPE
+    assert call(C=128, Tdeq=4 * BIG + 32) == ALIAS  # inside eT's 4 tiles x 3 exponents
     assert call(dk=96) == SHAPE
     assert call(L=250) == SHAPE       # L % C != 0
     assert call(N=64) == PARAM

@@ -188,3 +188,81 @@ def test_blocked_full_size_sampled(width, full_size_tiles):
     assert np.array_equal(host(qT[idx_t]).astype(np.int64), rT)
     assert np.array_equal(host(eT[idx_t]).astype(np.int64), rE)
     assert np.array_equal(host(Td[idx_t]), oi.dequant_unit_blocked(rT, rE).astype(np.float32))
+
+
+# ---------------------------------------------------------------------------
+# one launch from K: build A, quantise block by block, integer inverse
+
+FUSED = {"i8": G.gdn_chunk_inverse_neumann_i8_fused, "i16": G.gdn_chunk_inverse_neumann_i16_fused}
+
+
+def head_set(kdt, L=512, H=2, dk=128, stress=False, seed=0):
+    w = wl.workload("int8").with_(dtype=kdt, L=L, H=H, B=1, dk=dk, seed=1003 + seed)
+    if stress:
+        heads = [wl.gen_stress_head(L, dk, C, seed=90 + h) for h in range(H)]
+        heads = [(wl.round_to_bf16(k) if kdt == "bf16" else k, b, g, v) for k, b, g, v in heads]
+    else:
+        heads = [wl.gen_head(w, 0, h, C=C, want_v=False) for h in range(H)]
+    return tuple(wl.as_blhd(*[x[i] for x in heads]) for i in range(3))
+
+
+def to_cuda(x, dt=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(x, np.float32))).to("cuda").to(dt)
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+@pytest.mark.parametrize("kdt,dk,stress", [("bf16", 128, False), ("f32", 128, True),
+                                           ("bf16", 64, True), ("f32", 64, False)])
+def test_fused_matches_stages(width, kdt, dk, stress):
+    """The one launch equals gdn_build_A (fp32) -> block-wise quantiser ->
+    block-wise integer inverse on the GPU, bit for bit (the same fp32 A
+    values, hence the same codes)."""
+    _, _, quant, inv = WIDTHS[width]
+    K, beta, g = head_set(kdt, dk=dk, stress=stress, H=3)
+    dK = to_cuda(K, torch.bfloat16 if kdt == "bf16" else torch.float32)
+    db, dg = to_cuda(beta), to_cuda(g)
+    for N, S in [(3, 8), (2, 3)]:
+        print(f"{width} C=128 fused vs stages K={kdt} dk={dk} N={N} S={S}", flush=True)
+        A = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
+        Aq, eA = quant(A)
+        q1, e1, d1 = inv(Aq, eA, N, S, want_deq=True)
+        q2, e2, d2 = FUSED[width](dK, db, dg, C, N, S, want_deq=True)
+        assert e2.shape == (q2.shape[0] * q2.shape[1] * q2.shape[2], 3)
+        assert np.array_equal(host(q1).reshape(-1), host(q2).reshape(-1))
+        assert np.array_equal(host(e1), host(e2))
+        assert np.array_equal(host(d1).reshape(-1), host(d2).reshape(-1))
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+def test_fused_vs_oracle_and_float(width):
+    """Against the integer oracle run from its own fp32 A (float64 build,
+    rounded): the GPU forms A in fp32 arithmetic, so an entry a few ulp away
+    can move a code at a rounding boundary; the dequantised results stay
+    within a few dozen quanta of each block's exponent, and both are close
+    to the float64 block-wise T_hat(3, 8)."""
+    spec = WIDTHS[width][0]
+    K, beta, g = head_set("bf16", L=2048, H=4)
+    print(f"{width} C=128 fused vs oracle", flush=True)
+    Tq, eT, Td = FUSED[width](to_cuda(K, torch.bfloat16), to_cuda(beta), to_cuda(g), C, 3, 8,
+                              want_deq=True)
+    Af = gdn.tiles_flat(gdn.build_A(K, beta, g, C))
+    qA, eA = oi.quantize_blocked(Af.astype(np.float32), spec)
+    rq, re = oi.neumann_inverse_int_blocked(qA, eA, 3, 8, spec)
+    gq = host(Tq).reshape(rq.shape).astype(np.int64)
+    ge = host(eT).astype(np.int64)
+    same = np.all(gq == rq, axis=(-1, -2)) & np.all(ge == re, axis=-1)
+    got = host(Td).reshape(rq.shape).astype(np.float64)
+    ref = oi.dequant_unit_blocked(rq, re)
+    quantum = np.ones(rq.shape)
+    for k, (rs, cs) in enumerate([(slice(0, 64), slice(0, 64)), (slice(64, 128), slice(0, 64)),
+                                  (slice(64, 128), slice(64, 128))]):
+        quantum[:, rs, cs] = np.ldexp(1.0, re[:, k])[:, None, None]
+    quanta = np.abs(got - ref) / quantum
+    print(f"  {same.mean():.4f} of {same.size} tiles bit-exact, max {quanta.max():.1f} quanta",
+          flush=True)
+    assert quanta.max() <= 64.0
+    T = gdn.neumann_inverse_blocked(Af, 3, 8)
+    scale = np.max(np.abs(T - np.eye(C)), axis=(-1, -2))
+    err = np.max(np.abs(got - T), axis=(-1, -2))
+    bits = 8 if width == "i8" else 16
+    assert np.all(err <= 16 * 2.0 ** -bits * scale)
