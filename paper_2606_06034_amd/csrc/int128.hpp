@@ -53,15 +53,26 @@ __device__ __forceinline__ void store_deq_diag(float* td, const AccI<4>& Tr, int
 // aligned rows, fewer bank conflicts on transposed access)
 constexpr int kLD = 68;
 
-// One C = 128 tile after the diagonal blocks' codes are in registers.
-// Wave w (w = 0, 1) holds Lm = -A_ww (row form, strict lower) with exponent
-// eL; a21(A, ea) gives wave 0 the codes of A21 (row form, all 16 blocks) and
-// their exponent.  Wave w inverts its block with the engine and writes it;
-// wave 0 hands N11 (transposed) and A21 to wave 1 through LDS and leaves;
-// wave 1 forms X21.  Outputs for the tile: t (codes, 128 x 128), et (three
-// exponents), td (nullable, fp32).
-template <typename W, int NC, int SC, typename A21Fn>
-__device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL, A21Fn&& a21,
+// Wave 0 parks the codes of A21 (row form, all 16 blocks) and their
+// exponent in LDS for wave 1 (read after the workgroup barrier of
+// int128_tile), before its engine runs.
+__device__ __forceinline__ void stash_a21(const FullI& A, int ea, int* sA, int* sInfo) {
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J) *(i32x4*)&sA[(16 * I + c) * kLD + 16 * J + 4 * g] = A.a[4 * I + J];
+  if (lane_id() == 0) sInfo[2] = ea;
+}
+
+// One C = 128 tile after the diagonal blocks' codes are in registers (and,
+// from wave 0, A21 in LDS by stash_a21).  Wave w (w = 0, 1) holds
+// Lm = -A_ww (row form, strict lower) with exponent eL; it inverts its block
+// with the engine and writes it; wave 0 hands N11 (transposed) to wave 1
+// through LDS and leaves; wave 1 forms X21.  Outputs for the tile: t (codes,
+// 128 x 128), et (three exponents), td (nullable, fp32).
+template <typename W, int NC, int SC>
+__device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL,
                                             typename W::Code* __restrict__ t,
                                             int32_t* __restrict__ et, float* __restrict__ td,
                                             int Nrt, int Srt, int* sN, int* sA, int* sInfo) {
@@ -103,18 +114,9 @@ __device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL, A
       for (int J = 0; J <= I; ++J)
 #pragma unroll
         for (int v = 0; v < 4; ++v) sN[(16 * J + 4 * g + v) * LD + 16 * I + c] = Tr.a[bidx(I, J)][v];
-    // A21 (row form) to LDS row-major
-    FullI A;
-    int ea;
-    a21(A, ea);
-#pragma unroll
-    for (int I = 0; I < 4; ++I)
-#pragma unroll
-      for (int J = 0; J < 4; ++J) *(i32x4*)&sA[(16 * I + c) * LD + 16 * J + 4 * g] = A.a[4 * I + J];
     if (lane_id() == 0) {
       sInfo[0] = eTo;
       sInfo[1] = nzT ? 1 : 0;
-      sInfo[2] = ea;
     }
   }
   __syncthreads();
@@ -211,14 +213,15 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
       Lr.a[bidx(I, J)] = x;
     }
   const int eL = __builtin_amdgcn_readfirstlane(eA[3 * tile + 2 * wv]);
-  auto a21 = [&](FullI& A, int& ea) {
+  if (wv == 0) {
+    FullI A;
 #pragma unroll
     for (int I = 0; I < 4; ++I)
 #pragma unroll
       for (int J = 0; J < 4; ++J) A.a[4 * I + J] = W::load4(a + (64 + I * 16 + c) * C + J * 16 + 4 * g);
-    ea = __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]);
-  };
-  int128_tile<W, NC, SC>(wv, Lr, eL, a21, Tq + tile * (C * C), eT + 3 * tile,
+    stash_a21(A, __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]), sA, sInfo);
+  }
+  int128_tile<W, NC, SC>(wv, Lr, eL, Tq + tile * (C * C), eT + 3 * tile,
                          Tdeq ? Tdeq + tile * (C * C) : nullptr, Nrt, Srt, sN, sA, sInfo);
 }
 
@@ -226,7 +229,7 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
 // g (the values gdn_build_A writes: the same Gram products in the same order
 // and the same gates), each block quantised in registers by the block-wise
 // quantiser's rule, then the block-wise integer inverse.  Wave w forms its
-// diagonal block; wave 0 forms A21 after its engine.
+// diagonal block; wave 0 also forms A21, before its engine.
 template <typename W, int DK, typename F, typename TK, int NC, int SC>
 __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restrict__ K,
                                                               const float* __restrict__ beta,
@@ -269,10 +272,10 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
 #pragma unroll
       for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -eL));
   }
-  // ---- A21 (wave 0, after its engine): the Gram of the K rows of half 2
+  // ---- A21 (wave 0, before its engine): the Gram of the K rows of half 2
   // against those of half 1, slice by slice in the feature order of the
   // full Gram product, then the gates, then its own exponent
-  auto a21 = [&](FullI& A, int& ea) {
+  if (wv == 0) {
     f32x4 G2[4][4];
 #pragma unroll
     for (int I = 0; I < 4; ++I)
@@ -303,16 +306,18 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
           G2[I][J][v] = 1.f * sb[i] * G2[I][J][v] * __expf(sg[i] - sg[j]);
           m = fmaxf(m, fabsf(G2[I][J][v]));
         }
-    ea = W::qexp(
+    const int ea = W::qexp(
         __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m)))));
+    FullI A;
 #pragma unroll
     for (int I = 0; I < 4; ++I)
 #pragma unroll
       for (int J = 0; J < 4; ++J)
 #pragma unroll
         for (int v = 0; v < 4; ++v) A.a[4 * I + J][v] = (int)rintf(ldexpf(G2[I][J][v], -ea));
-  };
-  int128_tile<W, NC, SC>(wv, Lr, eL, a21, Tq + ch.tile * (C * C), eT + 3 * ch.tile,
+    stash_a21(A, ea, sA, sInfo);
+  }
+  int128_tile<W, NC, SC>(wv, Lr, eL, Tq + ch.tile * (C * C), eT + 3 * ch.tile,
                          Tdeq ? Tdeq + ch.tile * (C * C) : nullptr, Nrt, Srt, sN, sA, sInfo);
 }
 
