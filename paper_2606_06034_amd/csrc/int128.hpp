@@ -7,21 +7,24 @@
 // the whole block 21 (block 12 of a lower-triangular tile is zero).
 //
 // Inverse, two waves per tile: wave w inverts diagonal block w with the
-// one-tile engine (int_engine, X_ww = I + N_ww), then wave 1 forms the
-// off-diagonal block from the right,
+// one-tile engine (int_engine, X_ww = I + N_ww), then the off-diagonal block
+// is formed from the right,
 //   P = A21 X11 = A21 + A21 N11,      X21 = -(X22 P) = -(P + N22 P),
 // each an exact product added to its code term by the engine's running-sum
 // rules (code term first; a product is present when both factors are
-// non-zero) and requantised; N11 reaches wave 1 through LDS.
+// non-zero) and requantised; each wave forms two of the four 16-column
+// block columns of P and X21, the diagonal blocks and the maxima of the
+// requantisations passing through LDS.
 //
 // W (one code width) supplies: Code (the storage type), load4 / store4 (four
 // consecutive codes <-> i32x4), qexp (the quantiser's exponent of a block
 // maximum), engine<NC, SC> (the one-tile inverse of a 64 x 64 block), Row,
 // Col, to_row, to_col (the engine's fragments of lower matrices), to_frow
 // (row-form fragments of a full matrix), frow_to_col (row-form fragments to
-// column-form ones, exact), FProd and fmm<OUTQ> (an exact product over all
-// 16 output blocks) and sum2 (code term + product term, summed and
-// requantised to codes).
+// column-form ones, exact), FProd and fmm<OUTQ, J0, JN> (an exact product
+// over the output block columns J0 .. J0 + JN - 1) and sum2<J0, JN> (code
+// term + product term over those block columns, summed and requantised to
+// codes with a maximum joined across the waves by a given reduction).
 #pragma once
 
 #include "chunk.hpp"
@@ -49,33 +52,147 @@ __device__ __forceinline__ void store_deq_diag(float* td, const AccI<4>& Tr, int
     }
 }
 
-// LDS hand-over of one 64 x 64 int32 matrix: padded rows of 68 ints (16-byte
-// aligned rows, fewer bank conflicts on transposed access)
-constexpr int kLD = 68;
+// LDS hand-over of 64 x 64 matrices of codes (|code| <= 32639) as int16 in
+// padded rows of 72 (8-byte aligned runs of four, fewer bank conflicts on
+// transposed access)
+constexpr int kLD = 72;
+
+__device__ __forceinline__ void lds_put4(short* p, i32x4 q) {
+  *(int2*)p = int2{(int)((uint32_t)(q[0] & 0xffff) | ((uint32_t)q[1] << 16)),
+                   (int)((uint32_t)(q[2] & 0xffff) | ((uint32_t)q[3] << 16))};
+}
+__device__ __forceinline__ i32x4 lds_get4(const short* p) {
+  const int2 w = *(const int2*)p;
+  return i32x4{(int)(int16_t)(w.x & 0xffff), w.x >> 16, (int)(int16_t)(w.y & 0xffff), w.y >> 16};
+}
+
+// LDS of one C = 128 tile: N11 (transposed), N22 and A21 (row-major), the
+// exponents and flags, and the two maxima exchanged by the merge.
+struct Lds128 {
+  short n11t[64 * kLD];  // n11t[j * kLD + i] = N11[i][j]
+  short n22[64 * kLD];
+  short a21[64 * kLD];
+  int info[12];  // e11, nz11, ea, e22, nz22, -, max P (2 waves), -, max X21 (2 waves)
+};
 
 // Wave 0 parks the codes of A21 (row form, all 16 blocks) and their
-// exponent in LDS for wave 1 (read after the workgroup barrier of
-// int128_tile), before its engine runs.
-__device__ __forceinline__ void stash_a21(const FullI& A, int ea, int* sA, int* sInfo) {
+// exponent in LDS, before its engine runs (read after the workgroup barrier
+// of int128_tile).
+__device__ __forceinline__ void stash_a21(const FullI& A, int ea, Lds128& sh) {
   const int g = lane_g(), c = lane_c();
 #pragma unroll
   for (int I = 0; I < 4; ++I)
 #pragma unroll
-    for (int J = 0; J < 4; ++J) *(i32x4*)&sA[(16 * I + c) * kLD + 16 * J + 4 * g] = A.a[4 * I + J];
-  if (lane_id() == 0) sInfo[2] = ea;
+    for (int J = 0; J < 4; ++J) lds_put4(&sh.a21[(16 * I + c) * kLD + 16 * J + 4 * g], A.a[4 * I + J]);
+  if (lane_id() == 0) sh.info[2] = ea;
+}
+
+// Wave w's half of X21 = -(X22 (A21 X11)): the output block columns
+// J0, J0 + 1 (J0 = 2 w) of P = A21 + A21 N11 and of X21 = -(P + N22 P).
+// Column J of P needs all of A21 and column J of N11; column J of X21 needs
+// all of N22 and column J of P; only the requantisation of each (one
+// exponent per matrix) needs the other wave: its maximum, through LDS.
+template <typename W, int J0>
+__device__ __forceinline__ void merge_half(const AccI<4>& Tr, int eTo, bool nzT, Lds128& sh,
+                                          typename W::Code* __restrict__ t,
+                                          int32_t* __restrict__ et, float* __restrict__ td) {
+  constexpr int C = 128, LD = kLD, wv = J0 / 2;
+  const int g = lane_g(), c = lane_c();
+  // the other wave's maximum joined with this wave's (wave-uniform values)
+  auto xmax = [&](int m, int slot) {
+    if (lane_id() == 0) sh.info[slot + wv] = m;
+    __syncthreads();
+    return max(__builtin_amdgcn_readfirstlane(sh.info[slot]),
+               __builtin_amdgcn_readfirstlane(sh.info[slot + 1]));
+  };
+  const int e11 = __builtin_amdgcn_readfirstlane(sh.info[0]);
+  const bool nz11 = __builtin_amdgcn_readfirstlane(sh.info[1]) != 0;
+  const int ea = __builtin_amdgcn_readfirstlane(sh.info[2]);
+  const int e22 = __builtin_amdgcn_readfirstlane(sh.info[3]);
+  const bool nz22 = __builtin_amdgcn_readfirstlane(sh.info[4]) != 0;
+
+  // column form of N11's block columns J0, J0 + 1 (lane (g, c) holds rows
+  // 16 K + 4 g + v of column 16 J + c); the other columns are not used
+  AccI<4> N11c;
+#pragma unroll
+  for (int J = 0; J < 4; ++J)
+#pragma unroll
+    for (int K = J; K < 4; ++K)
+      N11c.a[bidx(K, J)] = (J >= J0 && J < J0 + 2)
+                               ? lds_get4(&sh.n11t[(16 * J + c) * LD + 16 * K + 4 * g])
+                               : zero_i4();
+  typename W::Col N11q;
+  W::to_col(N11q, N11c, 1, 63);
+  FullI A21;
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = 0; J < 4; ++J) A21.a[4 * I + J] = lds_get4(&sh.a21[(16 * I + c) * LD + 16 * J + 4 * g]);
+  const bool nzA = amax_full(A21) > 0;
+
+  typename W::Row X;  // A21, then P, as row-form fragments (sum2 reads the codes back)
+  typename W::FProd D;
+  W::to_frow(X, A21);
+  W::template fmm<true, J0, 2>(D, X, N11q);  // A21 N11, row form, own columns
+  FullI P;
+  int eP;
+  bool nzP;
+  W::template sum2<J0, 2>(P, eP, nzP, X, ea, nzA, D, ea + e11, nzA && nz11,
+                          [&](int m) { return xmax(m, 6); });
+
+  RowQ<4> Iq;
+  ColQ<4> Ic;
+  eye_quads(Iq, Ic);
+  W::to_frow(X, P);  // P's other block columns are 0
+  typename W::Col Pc;
+  W::frow_to_col(Pc, X, Ic);
+  typename W::Row N22q;
+  if constexpr (J0 == 2) {
+    W::to_row(N22q, Tr, 1, 63);
+  } else {
+    AccI<4> N22;
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J) N22.a[bidx(I, J)] = lds_get4(&sh.n22[(16 * I + c) * LD + 16 * J + 4 * g]);
+    W::to_row(N22q, N22, 1, 63);
+  }
+  W::template fmm<true, J0, 2>(D, N22q, Pc);  // N22 P, row form, own columns
+  FullI Xs;
+  int e21;
+  bool nz21;
+  W::template sum2<J0, 2>(Xs, e21, nz21, X, eP, nzP, D, e22 + eP, nz22 && nzP,
+                          [&](int m) { return xmax(m, 9); });
+
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int J = J0; J < J0 + 2; ++J)
+      W::store4(t + (64 + I * 16 + c) * C + J * 16 + 4 * g, zero_i4() - Xs.a[4 * I + J]);
+  if (J0 == 2 && lane_id() == 0) et[1] = e21;
+  if (td)
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = J0; J < J0 + 2; ++J) {
+        f32x4 x;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) x[v] = ldexpf((float)-Xs.a[4 * I + J][v], e21);
+        *(f32x4*)(td + (64 + I * 16 + c) * C + J * 16 + 4 * g) = x;
+      }
 }
 
 // One C = 128 tile after the diagonal blocks' codes are in registers (and,
 // from wave 0, A21 in LDS by stash_a21).  Wave w (w = 0, 1) holds
 // Lm = -A_ww (row form, strict lower) with exponent eL; it inverts its block
-// with the engine and writes it; wave 0 hands N11 (transposed) to wave 1
-// through LDS and leaves; wave 1 forms X21.  Outputs for the tile: t (codes,
+// with the engine and writes it, hands it to the other wave through LDS, and
+// forms its half of X21 (merge_half).  Outputs for the tile: t (codes,
 // 128 x 128), et (three exponents), td (nullable, fp32).
 template <typename W, int NC, int SC>
 __device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL,
                                             typename W::Code* __restrict__ t,
                                             int32_t* __restrict__ et, float* __restrict__ td,
-                                            int Nrt, int Srt, int* sN, int* sA, int* sInfo) {
+                                            int Nrt, int Srt, Lds128& sh) {
   constexpr int C = 128, LD = kLD;
   const int g = lane_g(), c = lane_c();
   const int r0 = 64 * wv;
@@ -107,79 +224,33 @@ __device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL,
   const bool nzT = amax_of(Tr, 1, 63) > 0;
   if (wv == 0) {
     // N11 (row form: lane (g, c) holds row 16 I + c, columns 16 J + 4 g + v)
-    // to LDS transposed, so that wave 1 reads its column form as 16 bytes
+    // to LDS transposed, so that its column form reads as runs of four
 #pragma unroll
     for (int I = 0; I < 4; ++I)
 #pragma unroll
       for (int J = 0; J <= I; ++J)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) sN[(16 * J + 4 * g + v) * LD + 16 * I + c] = Tr.a[bidx(I, J)][v];
+        for (int v = 0; v < 4; ++v)
+          sh.n11t[(16 * J + 4 * g + v) * LD + 16 * I + c] = (short)Tr.a[bidx(I, J)][v];
     if (lane_id() == 0) {
-      sInfo[0] = eTo;
-      sInfo[1] = nzT ? 1 : 0;
+      sh.info[0] = eTo;
+      sh.info[1] = nzT ? 1 : 0;
     }
-  }
-  __syncthreads();
-  if (wv == 0) return;
-
-  // ---- wave 1: X21 = -(X22 (A21 X11))
-  AccI<4> N11c;  // column form: lane (g, c) holds rows 16 K + 4 g + v of column 16 J + c
-#pragma unroll
-  for (int J = 0; J < 4; ++J)
-#pragma unroll
-    for (int K = J; K < 4; ++K) N11c.a[bidx(K, J)] = *(const i32x4*)&sN[(16 * J + c) * LD + 16 * K + 4 * g];
-  const int e11 = __builtin_amdgcn_readfirstlane(sInfo[0]);
-  const bool nz11 = __builtin_amdgcn_readfirstlane(sInfo[1]) != 0;
-  const int ea = __builtin_amdgcn_readfirstlane(sInfo[2]);
-  typename W::Col N11q;
-  W::to_col(N11q, N11c, 1, 63);
-
-  FullI A21;
-#pragma unroll
-  for (int I = 0; I < 4; ++I)
-#pragma unroll
-    for (int J = 0; J < 4; ++J) A21.a[4 * I + J] = *(const i32x4*)&sA[(16 * I + c) * LD + 16 * J + 4 * g];
-  const bool nzA = amax_full(A21) > 0;
-
-  typename W::Row X;  // A21, then P, as row-form fragments (sum2 reads the codes back)
-  typename W::FProd D;
-  W::to_frow(X, A21);
-  W::template fmm<true>(D, X, N11q);  // A21 N11, row form
-  FullI P;
-  int eP;
-  bool nzP;
-  W::sum2(P, eP, nzP, X, ea, nzA, D, ea + e11, nzA && nz11);
-
-  RowQ<4> Iq;
-  ColQ<4> Ic;
-  eye_quads(Iq, Ic);
-  W::to_frow(X, P);
-  typename W::Col Pc;
-  W::frow_to_col(Pc, X, Ic);
-  typename W::Row N22q;
-  W::to_row(N22q, Tr, 1, 63);
-  W::template fmm<true>(D, N22q, Pc);  // N22 P, row form
-  FullI Xs;
-  int e21;
-  bool nz21;
-  W::sum2(Xs, e21, nz21, X, eP, nzP, D, eTo + eP, nzT && nzP);
-
-#pragma unroll
-  for (int I = 0; I < 4; ++I)
-#pragma unroll
-    for (int J = 0; J < 4; ++J)
-      W::store4(t + (64 + I * 16 + c) * C + J * 16 + 4 * g, zero_i4() - Xs.a[4 * I + J]);
-  if (lane_id() == 0) et[1] = e21;
-  if (td)
+  } else {
 #pragma unroll
     for (int I = 0; I < 4; ++I)
 #pragma unroll
-      for (int J = 0; J < 4; ++J) {
-        f32x4 x;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) x[v] = ldexpf((float)-Xs.a[4 * I + J][v], e21);
-        *(f32x4*)(td + (64 + I * 16 + c) * C + J * 16 + 4 * g) = x;
-      }
+      for (int J = 0; J <= I; ++J) lds_put4(&sh.n22[(16 * I + c) * LD + 16 * J + 4 * g], Tr.a[bidx(I, J)]);
+    if (lane_id() == 0) {
+      sh.info[3] = eTo;
+      sh.info[4] = nzT ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  if (wv == 0)
+    merge_half<W, 0>(Tr, eTo, nzT, sh, t, et, td);
+  else
+    merge_half<W, 2>(Tr, eTo, nzT, sh, t, et, td);
 }
 
 // The integer inverse at C = 128 from codes (gdn_quantize_tiles_* layout).
@@ -192,9 +263,7 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
                                                         int Srt) {
   using Code = typename W::Code;
   constexpr int C = 128;
-  __shared__ __attribute__((aligned(16))) int sN[64 * kLD];  // sN[j * kLD + i] = N11[i][j]
-  __shared__ __attribute__((aligned(16))) int sA[64 * kLD];  // sA[i * kLD + j] = A21[i][j]
-  __shared__ int sInfo[4];
+  __shared__ __attribute__((aligned(16))) Lds128 sh;
   const int64_t tile = blockIdx.x;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane_g(), c = lane_c();
@@ -219,10 +288,10 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
     for (int I = 0; I < 4; ++I)
 #pragma unroll
       for (int J = 0; J < 4; ++J) A.a[4 * I + J] = W::load4(a + (64 + I * 16 + c) * C + J * 16 + 4 * g);
-    stash_a21(A, __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]), sA, sInfo);
+    stash_a21(A, __builtin_amdgcn_readfirstlane(eA[3 * tile + 1]), sh);
   }
   int128_tile<W, NC, SC>(wv, Lr, eL, Tq + tile * (C * C), eT + 3 * tile,
-                         Tdeq ? Tdeq + tile * (C * C) : nullptr, Nrt, Srt, sN, sA, sInfo);
+                         Tdeq ? Tdeq + tile * (C * C) : nullptr, Nrt, Srt, sh);
 }
 
 // The whole integer path at C = 128 in one launch: A in fp32 from K, beta,
@@ -240,9 +309,7 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
                                                               int H, int Nrt, int Srt) {
   constexpr int C = 128;
   __shared__ float sb[C], sg[C];
-  __shared__ __attribute__((aligned(16))) int sN[64 * kLD];
-  __shared__ __attribute__((aligned(16))) int sA[64 * kLD];
-  __shared__ int sInfo[4];
+  __shared__ __attribute__((aligned(16))) Lds128 sh;
   const Chunk ch(blockIdx.x, L, H, C);
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
@@ -315,10 +382,10 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
       for (int J = 0; J < 4; ++J)
 #pragma unroll
         for (int v = 0; v < 4; ++v) A.a[4 * I + J][v] = (int)rintf(ldexpf(G2[I][J][v], -ea));
-    stash_a21(A, ea, sA, sInfo);
+    stash_a21(A, ea, sh);
   }
   int128_tile<W, NC, SC>(wv, Lr, eL, Tq + ch.tile * (C * C), eT + 3 * ch.tile,
-                         Tdeq ? Tdeq + ch.tile * (C * C) : nullptr, Nrt, Srt, sN, sA, sInfo);
+                         Tdeq ? Tdeq + ch.tile * (C * C) : nullptr, Nrt, Srt, sh);
 }
 
 // Quantiser at C = 128: four waves per tile, wave w on the 64 x 64 quadrant

@@ -469,13 +469,14 @@ __device__ __forceinline__ void to_rowl_full(RowL<4>& X, const FullI& D) {
     }
 }
 
-// D = X Y exactly over all 16 output blocks; OUTQ: row-form result
-template <bool OUTQ>
+// D = X Y exactly over the output block columns J0 .. J0 + JN - 1 (the
+// other blocks of D are left as they are); OUTQ: row-form result
+template <bool OUTQ, int J0, int JN>
 __device__ __forceinline__ void mml_full(FullD& D, const RowL<4>& X, const ColL<4>& Y) {
 #pragma unroll
   for (int I = 0; I < 4; ++I)
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
+    for (int J = J0; J < J0 + JN; ++J) {
       const i32x4 xh = X.h.r[I].v, xl = X.l.r[I].v, yh = Y.h.c[J].v, yl = Y.l.c[J].v;
       const i32x4 z = zero_i4();
       i32x4 hh, mx, ll;
@@ -518,22 +519,26 @@ struct I16W : I16Ops<4> {
     to_colq_full(Y.h, h);
     to_colq_full(Y.l, l);
   }
-  template <bool OUTQ>
+  template <bool OUTQ, int J0, int JN>
   static __device__ __forceinline__ void fmm(FProd& D, const Row& X, const Col& Y) {
-    mml_full<OUTQ>(D, X, Y);
+    mml_full<OUTQ, J0, JN>(D, X, Y);
   }
   // the codes 256 h + l of block (I, K) of a row-form limb fragment
   static __device__ __forceinline__ i32x4 codes(const Row& X, int I, int K) {
     return unpack4(X.h.r[I].v[K]) * 256 + unpack4(X.l.r[I].v[K]);
   }
-  // The running sum of two terms, requantised: the codes of the fragments
-  // t1 (exponent e1), then the exact product t2 (exponent e2), by the
-  // engine's rules (the first present term 16 guard bits under its quantum,
-  // a larger later term rebases the sum, a finer one is rounded in).  The
-  // exponent plan is wave-uniform, so the sum is one pass per entry, in
-  // place in t2.
+  // The running sum of two terms over the block columns J0 .. J0 + JN - 1,
+  // requantised: the codes of the fragments t1 (exponent e1), then the exact
+  // product t2 (exponent e2), by the engine's rules (the first present term
+  // 16 guard bits under its quantum, a larger later term rebases the sum, a
+  // finer one is rounded in).  The exponent plan is wave-uniform, so the sum
+  // is one pass per entry, in place in t2.  red(m) joins this wave's maximum
+  // (of the high dwords) with the other blocks'.  The other block columns of
+  // out are set to 0.
+  template <int J0, int JN, typename Red>
   static __device__ __forceinline__ void sum2(FullI& out, int& eo, bool& nz, const Row& t1,
-                                              int e1, bool p1, FullD& t2, int e2, bool p2) {
+                                              int e1, bool p1, FullD& t2, int e2, bool p2,
+                                              Red&& red) {
     int e = 0, sh = 0;
     bool any = false, reb = false;
     double scr = 1.0;
@@ -558,7 +563,7 @@ struct I16W : I16Ops<4> {
 #pragma unroll
     for (int I = 0; I < 4; ++I)
 #pragma unroll
-      for (int K = 0; K < 4; ++K) {
+      for (int K = J0; K < J0 + JN; ++K) {
         const i32x4 c1 = codes(t1, I, K);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
@@ -572,13 +577,17 @@ struct I16W : I16Ops<4> {
           m = max(m, __double2hiint(fabs(x)));
         }
       }
-    const int amax_hi = wave_max(m);
+    const int amax_hi = red(wave_max(m));
     const int s = shift_for_hi(amax_hi);
     const double sc = ldexp(1.0, -s);
 #pragma unroll
-    for (int b = 0; b < 16; ++b)
+    for (int I = 0; I < 4; ++I)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) out.a[b][v] = rne_scaled(t2.a[b][v], sc);
+      for (int K = 0; K < 4; ++K)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          out.a[4 * I + K][v] =
+              (K < J0 || K >= J0 + JN) ? 0 : rne_scaled(t2.a[4 * I + K][v], sc);
     nz = amax_hi > 0;
     eo = nz ? (any ? e : 0) + s : 0;
   }

@@ -356,22 +356,26 @@ struct I8W : I8Ops<4> {
     mmi_full<false>(t, X, Ic);
     to_colq_full(Y, t);
   }
-  template <bool OUTQ>
+  template <bool OUTQ, int J0, int JN>
   static __device__ __forceinline__ void fmm(FProd& D, const Row& X, const Col& Y) {
-    mmi_full<OUTQ>(D, X, Y);
+    mmi_full<OUTQ, J0, JN>(D, X, Y);
   }
   // the codes of block (I, K) of a row-form fragment
   static __device__ __forceinline__ i32x4 codes(const Row& X, int I, int K) {
     return unpack4(X.r[I].v[K]);
   }
-  // The running sum of two terms, requantised: the codes of the fragments
-  // t1 (exponent e1), then the exact product t2 (exponent e2), by the
-  // engine's rules (the first present term 16 guard bits under its quantum,
-  // a larger later term rebases the sum, a finer one is rounded in).  The
-  // exponent plan is wave-uniform, so the sum is one pass per entry, in
-  // place in t2.
+  // The running sum of two terms over the block columns J0 .. J0 + JN - 1,
+  // requantised: the codes of the fragments t1 (exponent e1), then the exact
+  // product t2 (exponent e2), by the engine's rules (the first present term
+  // 16 guard bits under its quantum, a larger later term rebases the sum, a
+  // finer one is rounded in).  The exponent plan is wave-uniform, so the sum
+  // is one pass per entry, in place in t2.  red(m) joins this wave's maximum
+  // with the other blocks' (identity when one wave forms every block).  The
+  // other block columns of out are set to 0.
+  template <int J0, int JN, typename Red>
   static __device__ __forceinline__ void sum2(FullI& out, int& eo, bool& nz, const Row& t1,
-                                              int e1, bool p1, FullI& t2, int e2, bool p2) {
+                                              int e1, bool p1, FullI& t2, int e2, bool p2,
+                                              Red&& red) {
     int e = 0, reb = 0, sh = 0;
     bool any = false;
     if (p1) {
@@ -389,10 +393,11 @@ struct I8W : I8Ops<4> {
       }
       sh = e2 - e;
     }
+    int m = 0;
 #pragma unroll
     for (int I = 0; I < 4; ++I)
 #pragma unroll
-      for (int K = 0; K < 4; ++K) {
+      for (int K = J0; K < J0 + JN; ++K) {
         const i32x4 c1 = codes(t1, I, K);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
@@ -403,12 +408,21 @@ struct I8W : I8Ops<4> {
             x += sh >= 0 ? y << sh : (sh > -31 ? rne_pos(y, -sh) : 0);
           }
           t2.a[4 * I + K][v] = x;
+          m = max(m, abs(x));
         }
       }
-    const int amax = amax_full(t2);
+    const int amax = red(wave_max(m));
     const int s = shift_for(amax);
-    if (s > 0) shift_full(t2, s);
-    out = t2;
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int K = 0; K < 4; ++K)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          out.a[4 * I + K][v] = (K < J0 || K >= J0 + JN) ? 0
+                                : s == 0                ? t2.a[4 * I + K][v]
+                                : s >= 31               ? 0
+                                                        : rne_pos(t2.a[4 * I + K][v], s);
     nz = amax > 0;
     eo = nz ? (any ? e : 0) + s : 0;
   }

@@ -164,14 +164,15 @@ __device__ __forceinline__ void to_colq_full(ColQ<4>& Y, const FullI& D) {
 #pragma unroll
     for (int K = 0; K < 4; ++K) Y.c[J].v[K] = pack4(D.a[4 * K + J]);
 }
-// D = X Y over all 16 output blocks (X or Y may be lower: its quads carry
-// the zero blocks); OUTQ: row-form result
-template <bool OUTQ>
+// D = X Y over the output block columns J0 .. J0 + JN - 1 (all 16 blocks
+// by default; the other blocks of D are left as they are); X or Y may be
+// lower: its quads carry the zero blocks.  OUTQ: row-form result.
+template <bool OUTQ, int J0 = 0, int JN = 4>
 __device__ __forceinline__ void mmi_full(FullI& D, const RowQ<4>& X, const ColQ<4>& Y) {
 #pragma unroll
   for (int I = 0; I < 4; ++I)
 #pragma unroll
-    for (int J = 0; J < 4; ++J)
+    for (int J = J0; J < J0 + JN; ++J)
       D.a[4 * I + J] =
           OUTQ ? __builtin_amdgcn_mfma_i32_16x16x64_i8(Y.c[J].v, X.r[I].v, zero_i4(), 0, 0, 0)
                : __builtin_amdgcn_mfma_i32_16x16x64_i8(X.r[I].v, Y.c[J].v, zero_i4(), 0, 0, 0);
