@@ -427,6 +427,26 @@ def dequant_unit_blocked(qT: np.ndarray, eT: np.ndarray) -> np.ndarray:
     return out + np.eye(C)
 
 
+def dequantized_inverse(A: np.ndarray, N: int, S: int, spec: Spec = SPEC8,
+                        C: int = 0) -> np.ndarray:
+    """The integer T_hat(N, S) as a float64 inverse, for the layer forward's
+    integer mode: the strictly lower A tiles [..., m, m] rounded to float32
+    (the values the quantiser reads), quantised per tile, inverted by
+    neumann_inverse_int8 and dequantised, I + qT 2^eT.  With C > m the tile is
+    first padded to C x C with zero rows and columns (tokens that write
+    nothing) and the top-left m x m block returned: the integer recipe runs on
+    C x C tiles, whose product bound sets the alignment of its sums."""
+    A = np.asarray(A, np.float64)
+    m = A.shape[-1]
+    if C > m:
+        P = np.zeros(A.shape[:-2] + (C, C))
+        P[..., :m, :m] = A
+        return dequantized_inverse(P, N, S, spec)[..., :m, :m]
+    qA, eA = quantize(np.tril(A, -1).astype(np.float32), spec)
+    qT, eT, _ = neumann_inverse_int8(qA, eA, N, S, spec)
+    return dequant_unit(qT, eT)
+
+
 def dequant_unit(qT: np.ndarray, eT: np.ndarray) -> np.ndarray:
     """I + qT * 2^eT as float64."""
     C = qT.shape[-1]

@@ -687,3 +687,47 @@ def test_blocked_close_to_float_approximation(spec, bits, src):
     # the 64 x 64 inverses alone: same bound as the unblocked pins
     err11 = np.max(np.abs(qo.dequant_unit_blocked(qT, eT)[:, :64, :64] - T[:, :64, :64]))
     assert err11 <= 16 * 2.0 ** -bits * np.max(scale)
+
+
+# ---------------------------------------------------------------------------
+# the integer inverse inside the layer forward (dequantized_inverse)
+
+
+@pytest.mark.parametrize("spec,bits", [(qo.SPEC8, 8), (qo.SPEC16, 16)])
+def test_dequantized_inverse_padding_and_closeness(spec, bits):
+    """Padding a partial tile with tokens that write nothing (zero rows and
+    columns) leaves an identity block (the integer recipe keeps every power
+    block diagonal), and the dequantised inverse stays within the pinned
+    integer error of the float64 T_hat(N, S); all-ones A stays exact."""
+    A = _blocked_A(64, 4)
+    T = qo.dequantized_inverse(A, 3, 8, spec)
+    Tf = gdn.neumann_inverse(A, 3, 8)
+    scale = np.max(np.abs(Tf - np.eye(64)), axis=(-1, -2))
+    assert np.all(np.max(np.abs(T - Tf), axis=(-1, -2)) <= 4 * 2.0 ** -bits * scale)
+    m = 40
+    Ap = np.zeros_like(A)
+    Ap[:, :m, :m] = A[:, :m, :m]
+    Tp = qo.dequantized_inverse(Ap, 3, 8, spec)
+    n = A.shape[0]
+    assert np.array_equal(Tp[:, m:, m:], np.broadcast_to(np.eye(64 - m), (n, 64 - m, 64 - m)))
+    assert not np.any(Tp[:, m:, :m]) and not np.any(Tp[:, :m, m:])
+    assert np.array_equal(qo.dequantized_inverse(A[:, :m, :m], 3, 8, spec, C=64), Tp[:, :m, :m])
+    ones = np.tril(np.ones((1, 64, 64)), -1)
+    assert np.array_equal(qo.dequantized_inverse(ones, 3, 8, spec)[0], np.eye(64) - np.eye(64, k=-1))
+
+
+@pytest.mark.parametrize("spec,bits", [(qo.SPEC8, 8), (qo.SPEC16, 16)])
+def test_forward_with_integer_inverse_close_to_float(spec, bits):
+    """The layer forward (chunk-wise oracle) with the integer inverse differs
+    from the one with the float64 T_hat(3, 8) only through the inverse's
+    quantisation error: INT16 about 2^8 times closer than INT8."""
+    from oracle import gdn_forward
+    C = 64
+    w = wl.workload("tiny").with_(B=1, L=2 * C, H=2, dk=32, dv=16, C=C)
+    Q, K, V, beta, g, S0 = wl.gen_forward_inputs(w, C=C)
+    Of, Sf = gdn_forward.gdn_chunked(Q, K, V, beta, g, C, S0, 0.5,
+                                     inverse=lambda A: gdn.neumann_inverse(A, 3, 8))
+    Oi, Si = gdn_forward.gdn_chunked(Q, K, V, beta, g, C, S0, 0.5,
+                                     inverse=lambda A: qo.dequantized_inverse(A, 3, 8, spec))
+    err = max(np.max(np.abs(Oi - Of)) / np.max(np.abs(Of)), np.max(np.abs(Si - Sf)) / np.max(np.abs(Sf)))
+    assert 0 < err <= 2.0 ** (6 - bits)
