@@ -281,8 +281,13 @@ int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const 
  * with the [dk, dv] state S, the token recurrence it computes is
  *   S_t = a_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
  *   o_t = scale S_t^T q_t,   a_t = exp(g_t - g_{t-1}) inside a chunk,
- * evaluated chunk by chunk: T = (I + A)^-1 (T_hat(N, S) of
- * gdn_chunk_inverse_neumann, or the exact block-wise inverse when exact = 1),
+ * evaluated chunk by chunk: T = (I + A)^-1 chosen by `exact` (the inverse
+ * mode): 0, T_hat(N, S) of gdn_chunk_inverse_neumann; 1, the exact
+ * block-wise inverse; 2 and 3, the quantised GDN of Section 3.5: T_hat(N, S)
+ * in integer arithmetic on 16-bit (2) or 8-bit (3) codes, the codes of
+ * gdn_chunk_inverse_neumann_i16_fused (_i8_fused) for the chunk, dequantised
+ * to fp32 (modes 2 and 3 run the default (N, S) of gdn_default_order with
+ * dk = dv = 128, else GDN_ERR_UNSUPPORTED; any other mode GDN_ERR_PARAM),
  * W = T diag(beta e^g) K, U = T diag(beta) V, V_new = U - W S,
  * O = scale (diag(e^g) Q S + ((Q K^T) (.) D) V_new) with D_ij = e^{g_i - g_j}
  * for i >= j (else 0), S' = e^{g_last} S + K^T diag(e^{g_last - g}) V_new.
@@ -307,8 +312,8 @@ int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* 
 /* gdn_chunk_forward in its two phases, for callers that schedule them apart
  * (the first has no sequential dependence; the second carries the state).
  * gdn_chunk_forward_prepare: every chunk in parallel, Q, K, V, beta, g ->
- * workspace (T of T_hat(N, S) or exact as for gdn_chunk_forward, then the
- * per-chunk factors).  gdn_chunk_forward_state: the recurrence over the
+ * workspace (T by the inverse mode `exact` as for gdn_chunk_forward, then
+ * the per-chunk factors).  gdn_chunk_forward_state: the recurrence over the
  * chunks of each head, workspace (as the prepare call with the same sizes
  * and dtype left it), Q, g, S0 -> O, S_final.  Run on one stream, prepare
  * then state equals gdn_chunk_forward bit for bit.  Arguments, layouts and
@@ -340,6 +345,8 @@ int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int 
  * sequence keeps its initial state.  workspace: at least the bytes
  * gdn_chunk_forward_workspace reports for B = 1, L = n_chunks * C.  The
  * per-chunk launch and the state pass run back to back on `stream`.
+ * Inverse modes (`exact`) as for gdn_chunk_forward; in the integer modes a
+ * partial chunk is the C x C tile padded with tokens that write nothing.
  * C in {16, 32, 64}. */
 int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const float* beta,
                              const float* g, const float* S0, void* O, float* S_final,

@@ -436,16 +436,32 @@ def gdn_chunk_forward_workspace(B: int, L: int, H: int, dk: int, dv: int, C: int
     return n.value
 
 
+_FWD_MODES = {"neumann": 0, "exact": 1, "int16": 2, "int8": 3}
+
+
+def _fwd_mode(exact: bool, inverse: Optional[str]) -> int:
+    """The inverse mode of the layer forward: T_hat(N, S) ("neumann"), the
+    exact inverse ("exact", or exact=True), or T_hat(N, S) on 16- or 8-bit
+    codes ("int16", "int8")."""
+    if inverse is None:
+        return 1 if exact else 0
+    if inverse not in _FWD_MODES:
+        raise ValueError(f"inverse must be one of {sorted(_FWD_MODES)}")
+    return _FWD_MODES[inverse]
+
+
 def gdn_chunk_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: torch.Tensor,
                       g: torch.Tensor, C: int, S0: Optional[torch.Tensor] = None,
                       N: Optional[int] = None, S: Optional[int] = None, exact: bool = False,
                       scale: Optional[float] = None, want_state: bool = True,
                       O: Optional[torch.Tensor] = None, S_final: Optional[torch.Tensor] = None,
-                      workspace: Optional[torch.Tensor] = None, stream=None):
+                      workspace: Optional[torch.Tensor] = None, stream=None,
+                      inverse: Optional[str] = None):
     """Chunk-wise Gated DeltaNet forward: (O [B, L, H, dv], S_final [B, H, dk, dv] fp32 or
     None).  N, S default to gdn_default_order(C); scale defaults to dk ** -0.5.  The
     workspace (a byte tensor of gdn_chunk_forward_workspace() bytes) is allocated when
-    not given."""
+    not given.  inverse: "neumann" (default), "exact" (as exact=True), "int16" or "int8"
+    (the integer T_hat(N, S) inside the layer)."""
     B, L, H, dk = K.shape
     dv = V.shape[-1]
     dt = _fdtype(K, "K")
@@ -467,15 +483,16 @@ def gdn_chunk_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: t
         _dev(Q, "Q", K.dtype, tok * dk), _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv),
         _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok), sp,
         _dev(O, "O", K.dtype, tok * dv), fp, _dev(workspace, "workspace"), workspace.numel() *
-        workspace.element_size(), B, L, H, dk, dv, C, N, S, int(bool(exact)), scale, dt,
-        _stream(stream)))
+        workspace.element_size(), B, L, H, dk, dv, C, N, S, _fwd_mode(exact, inverse), scale,
+        dt, _stream(stream)))
     return O, S_final
 
 
 def gdn_chunk_forward_prepare(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
                               beta: torch.Tensor, g: torch.Tensor, C: int,
                               workspace: torch.Tensor, N: Optional[int] = None,
-                              S: Optional[int] = None, exact: bool = False, stream=None):
+                              S: Optional[int] = None, exact: bool = False, stream=None,
+                              inverse: Optional[str] = None):
     """First phase of gdn_chunk_forward: the per-chunk factors into `workspace`."""
     B, L, H, dk = K.shape
     dv = V.shape[-1]
@@ -489,7 +506,7 @@ def gdn_chunk_forward_prepare(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
         _dev(Q, "Q", K.dtype, tok * dk), _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv),
         _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok),
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
-        B, L, H, dk, dv, C, N, S, int(bool(exact)), dt, _stream(stream)))
+        B, L, H, dk, dv, C, N, S, _fwd_mode(exact, inverse), dt, _stream(stream)))
     return workspace
 
 
@@ -570,10 +587,11 @@ def gdn_chunk_forward_varlen(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
                              scale: Optional[float] = None, want_state: bool = True,
                              O: Optional[torch.Tensor] = None,
                              S_final: Optional[torch.Tensor] = None,
-                             workspace: Optional[torch.Tensor] = None, stream=None):
+                             workspace: Optional[torch.Tensor] = None, stream=None,
+                             inverse: Optional[str] = None):
     """Layer forward over packed sequences: (O [1, T, H, dv], S_final
     [nseq, H, dk, dv] fp32 or None); tables = gdn_varlen_tables(cu_seqlens, C).
-    Defaults as gdn_chunk_forward."""
+    Defaults and inverse modes as gdn_chunk_forward."""
     dcu, doff, n_chunks = tables
     B, T, H, dk = K.shape
     if B != 1:
@@ -602,5 +620,5 @@ def gdn_chunk_forward_varlen(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
         _dev(O, "O", K.dtype, tok * dv), fp, _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), _dev(dcu, "cu_seqlens", torch.int32),
         _dev(doff, "chunk_offsets", torch.int32, nseq + 1), nseq, n_chunks, T, H, dk, dv, C, N, S,
-        int(bool(exact)), scale, dt, _stream(stream)))
+        _fwd_mode(exact, inverse), scale, dt, _stream(stream)))
     return O, S_final

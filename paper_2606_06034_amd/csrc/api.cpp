@@ -27,6 +27,22 @@ bool overlap(const void* p, int64_t bytes, const void* q, int64_t qbytes) {
 // exponents per tile of the integer paths: C = 128 runs three blocks
 int64_t nexp(int C) { return C == 128 ? 3 : 1; }
 
+// The inverse modes of the layer forward: 0 T_hat(N, S), 1 exact, 2 T_hat(N, S)
+// on 16-bit codes, 3 on 8-bit codes.  The integer modes run the default order
+// with dk = dv = 128 (anything else: GDN_ERR_UNSUPPORTED).
+int forward_mode_check(int mode, int C, int N, int S, int dk, int dv, bool prep) {
+  if (mode < 0 || mode > 3) return GDN_ERR_PARAM;
+  if (prep && mode != 1) {
+    const int lim = (C == 128 ? 64 : C) - 1;
+    if (N < 0 || S < 0 || N > lim || S > lim) return GDN_ERR_PARAM;
+  }
+  if (prep && mode >= 2) {
+    const int dn = 3, ds = C == 16 ? 2 : C == 32 ? 4 : 8;
+    if (N != dn || S != ds || dk != 128 || dv != 128) return GDN_ERR_UNSUPPORTED;
+  }
+  return GDN_OK;
+}
+
 int order_ok(int C, int N, int S) {
   const int lim = (C == 128 ? 64 : C) - 1;  // C = 128 runs 64-blocks
   return N >= 0 && S >= 0 && N <= lim && S <= lim;
@@ -244,8 +260,7 @@ int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const 
   if (nseq == 0 && n_chunks != 0) return GDN_ERR_SHAPE;
   if (n_chunks > T || (int64_t)n_chunks * H > kMaxTiles) return GDN_ERR_SHAPE;
   if ((int64_t)nseq * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
-  if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
-  if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (int r = forward_mode_check(exact, C, N, S, dk, dv, true)) return r;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (C == 128) return GDN_ERR_UNSUPPORTED;
   if (nseq == 0 || H == 0) return GDN_OK;
@@ -281,7 +296,7 @@ int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const 
   }
   return hip_status(gdn::launch_forward_varlen(Q, K, V, beta, g, S0, O, S_final, workspace,
                                                cu_seqlens, chunk_offsets, nseq, n_chunks, T, H,
-                                               dk, dv, C, N, S, exact != 0, scale, dtype,
+                                               dk, dv, C, N, S, exact, scale, dtype,
                                                (hipStream_t)stream));
 }
 
@@ -474,8 +489,7 @@ int forward(const void* Q, const void* K, const void* V, const float* beta, cons
   int64_t n = 0;
   if (int r = check_chunked(B, L, H, C, &n)) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
-  if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
-  if ((phases & 1) && !exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (int r = forward_mode_check(exact, C, N, S, dk, dv, phases & 1)) return r;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (C == 128) return GDN_ERR_UNSUPPORTED;
   if ((int64_t)B * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
@@ -515,7 +529,7 @@ int forward(const void* Q, const void* K, const void* V, const float* beta, cons
       if (overlap(outs[o], outb[o], outs[o2], outb[o2])) return GDN_ERR_ALIAS;
   }
   return hip_status(gdn::launch_forward(Q, K, V, beta, g, S0, O, S_final, workspace, B, L, H, dk,
-                                        dv, C, N, S, exact != 0, scale, dtype, phases,
+                                        dv, C, N, S, exact, scale, dtype, phases,
                                         (hipStream_t)stream));
 }
 }  // namespace

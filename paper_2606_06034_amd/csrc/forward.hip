@@ -33,6 +33,8 @@
 // features of W and Q rows.
 #include <type_traits>
 
+#include "int16_ops.hpp"
+#include "int8_ops.hpp"
 #include "launch.hpp"
 #include "wy.hpp"
 
@@ -176,12 +178,57 @@ __device__ __forceinline__ void apply_w_fwd(const RowP<NB, F>& TR,
 // ---------------------------------------------------------------------------
 // stage 1
 
+// The inverse modes of the per-chunk launch: T_hat(N, S) in the compute
+// type, the exact block-wise inverse, or T_hat(N, S) in integer arithmetic
+// (16- or 8-bit codes).
+enum FwdInv { kInvNeumann = 0, kInvExact = 1, kInvInt16 = 2, kInvInt8 = 3 };
+
+// The integer inverse of one chunk inside the layer (the quantised GDN of
+// Section 3.5): A in fp32 from the K row pairs with the Gram products and
+// gates of gdn_build_A, quantised per tile by the quantiser's rule, the
+// integer T_hat(N, S) of the shared engine, and its strict lower part
+// dequantised (codes * 2^e, exact in fp32) in row form; the caller adds I.
+// The codes equal those of gdn_chunk_inverse_neumann_i16_fused (_i8_fused)
+// for the same chunk.
+template <int NB, int DK, typename F, int INV, int NC, int SC, typename Hook>
+__device__ __forceinline__ void chunk_inverse_int(const Pair<F> (&kp)[NB][DK / 32],
+                                                  const float* sb, const float* sg, int N, int S,
+                                                  Acc<NB>& Tr, Hook&& after_gram) {
+  Acc<NB> G;
+  gram_lower<NB, DK, true>(G, kp);
+  after_gram();
+  gate_scale<NB, true>(G, sb, sg, 1.f);
+  float m = 0.f;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) m = fmaxf(m, fabsf(G.a[b][v]));
+  const float amax =
+      __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(__ockl_wfred_max_f32(m))));
+  const int e = INV == kInvInt16 ? i16::quant_exp(amax) : i8::quant_exp(amax);
+  iq::AccI<NB> Lr;
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
+  iq::AccI<NB> Ti;
+  int eT;
+  if constexpr (INV == kInvInt16)
+    iq::int_engine<i16::I16Ops, NB, NC, SC>(Lr, e, N, S, Ti, eT);
+  else
+    iq::int_engine<i8::I8Ops, NB, NC, SC>(Lr, e, N, S, Ti, eT);
+#pragma unroll
+  for (int b = 0; b < nlower(NB); ++b)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) Tr.a[b][v] = ldexpf((float)Ti.a[b][v], eT);
+}
+
 // VARLEN: packed sequences (B = 1, L = T tokens, chunk tables pk); a chunk's
 // rows past its m tokens are read from row m - 1 and carry beta = 0, so W, U
 // and K^T vanish there (T is the identity on them) and the state pass never
 // stores their outputs.
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool EXACT, bool VARLEN = false>
+          int INV, bool VARLEN = false>
 __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
                                                   const TIO* __restrict__ K,
                                                   const TIO* __restrict__ V,
@@ -223,7 +270,10 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
     }
   };
   Acc<NB> Tr;
-  chunk_inverse<NB, DK, F, SMALLN, NC, SC, EXACT>(kp, sb, sg, N, S, Tr, prefetch_v);
+  if constexpr (INV == kInvInt16 || INV == kInvInt8)
+    chunk_inverse_int<NB, DK, F, INV, NC, SC>(kp, sb, sg, N, S, Tr, prefetch_v);
+  else
+    chunk_inverse<NB, DK, F, SMALLN, NC, SC, INV == kInvExact>(kp, sb, sg, N, S, Tr, prefetch_v);
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, C) + eye4();
 
@@ -582,7 +632,7 @@ template <> struct FwdOrder<4> { static constexpr int N = 3, S = 8; };
 template <int NB, int DK, int DV, typename F, typename TIO>
 static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, const float* beta,
                                  const float* g, const float* S0, void* O, float* Sfin, void* ws,
-                                 int B, int L, int H, int N, int S, bool exact, float scale,
+                                 int B, int L, int H, int N, int S, int mode, float scale,
                                  int phases, hipStream_t st, const Packed& pk) {
   constexpr int DN = FwdOrder<NB>::N, DS = FwdOrder<NB>::S;
   const bool packed = pk.cu != nullptr;
@@ -599,14 +649,26 @@ static hipError_t run_forward_nb(const void* Q, const void* K, const void* V, co
                          (const TIO*)V, beta, g, (TIO*)ws, n, L, H, N, S, pk);                 \
   } while (0)
   if ((phases & 1) && n > 0) {
-    if (exact)
-      GDN_FWD1(true, 0, 0, true);
-    else if (N == DN && S == DS)
-      GDN_FWD1(true, DN, DS, false);
-    else if (N <= 15)
-      GDN_FWD1(true, -1, -1, false);
-    else
-      GDN_FWD1(false, -1, -1, false);
+    if (mode == kInvExact) {
+      GDN_FWD1(true, 0, 0, kInvExact);
+    } else if (mode == kInvInt16 || mode == kInvInt8) {
+      // the integer modes run the default order with dk = dv = 128
+      if constexpr (DK == 128 && DV == 128) {
+        if (N != DN || S != DS) return hipErrorNotSupported;
+        if (mode == kInvInt16)
+          GDN_FWD1(true, DN, DS, kInvInt16);
+        else
+          GDN_FWD1(true, DN, DS, kInvInt8);
+      } else {
+        return hipErrorNotSupported;
+      }
+    } else if (N == DN && S == DS) {
+      GDN_FWD1(true, DN, DS, kInvNeumann);
+    } else if (N <= 15) {
+      GDN_FWD1(true, -1, -1, kInvNeumann);
+    } else {
+      GDN_FWD1(false, -1, -1, kInvNeumann);
+    }
   }
 #undef GDN_FWD1
   if (phases & 2) {
@@ -640,12 +702,12 @@ template <typename F, typename TIO>
 static hipError_t run_forward(const void* Q, const void* K, const void* V, const float* beta,
                               const float* g, const float* S0, void* O, float* Sfin, void* ws,
                               int B, int L, int H, int dk, int dv, int C, int N, int S,
-                              bool exact, float scale, int phases, hipStream_t st,
+                              int mode, float scale, int phases, hipStream_t st,
                               const Packed& pk) {
 #define GDN_FWD_NB(NB_)                                                                      \
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {                                                      \
     return run_forward_nb<NB_, DK, DV, F, TIO>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, N, \
-                                              S, exact, scale, phases, st, pk);              \
+                                              S, mode, scale, phases, st, pk);               \
   }))
   switch (C) {
     case 16: GDN_FWD_NB(1) break;
@@ -659,31 +721,31 @@ static hipError_t run_forward(const void* Q, const void* K, const void* V, const
 static hipError_t forward_dtype(const void* Q, const void* K, const void* V, const float* beta,
                                 const float* g, const float* S0, void* O, float* Sfin, void* ws,
                                 int B, int L, int H, int dk, int dv, int C, int N, int S,
-                                bool exact, float scale, int dtype, int phases, hipStream_t st,
+                                int mode, float scale, int dtype, int phases, hipStream_t st,
                                 const Packed& pk) {
   if (dtype == 0)
     return run_forward<f32x4, float>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S,
-                                     exact, scale, phases, st, pk);
+                                     mode, scale, phases, st, pk);
   if (dtype == 1)
     return run_forward<bf16x4, __bf16>(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N,
-                                       S, exact, scale, phases, st, pk);
+                                       S, mode, scale, phases, st, pk);
   return hipErrorNotSupported;
 }
 
 hipError_t launch_forward(const void* Q, const void* K, const void* V, const float* beta,
                           const float* g, const float* S0, void* O, float* Sfin, void* ws, int B,
-                          int L, int H, int dk, int dv, int C, int N, int S, bool exact,
+                          int L, int H, int dk, int dv, int C, int N, int S, int mode,
                           float scale, int dtype, int phases, hipStream_t st) {
-  return forward_dtype(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S, exact, scale,
+  return forward_dtype(Q, K, V, beta, g, S0, O, Sfin, ws, B, L, H, dk, dv, C, N, S, mode, scale,
                        dtype, phases, st, Packed{});
 }
 
 hipError_t launch_forward_varlen(const void* Q, const void* K, const void* V, const float* beta,
                                  const float* g, const float* S0, void* O, float* Sfin, void* ws,
                                  const int* cu, const int* off, int nseq, int nchunks, int Ttok,
-                                 int H, int dk, int dv, int C, int N, int S, bool exact,
+                                 int H, int dk, int dv, int C, int N, int S, int mode,
                                  float scale, int dtype, hipStream_t st) {
-  return forward_dtype(Q, K, V, beta, g, S0, O, Sfin, ws, 1, Ttok, H, dk, dv, C, N, S, exact,
+  return forward_dtype(Q, K, V, beta, g, S0, O, Sfin, ws, 1, Ttok, H, dk, dv, C, N, S, mode,
                        scale, dtype, 3, st, Packed{cu, off, nseq, nchunks});
 }
 

@@ -41,12 +41,12 @@ hipError_t launch_fused(const void* K, const void* V, const float* beta, const f
 // S_final)
 hipError_t launch_forward(const void* Q, const void* K, const void* V, const float* beta,
                           const float* g, const float* S0, void* O, float* Sfin, void* ws, int B,
-                          int L, int H, int dk, int dv, int C, int N, int S, bool exact,
+                          int L, int H, int dk, int dv, int C, int N, int S, int mode,
                           float scale, int dtype, int phases, hipStream_t st);
 hipError_t launch_forward_varlen(const void* Q, const void* K, const void* V, const float* beta,
                                  const float* g, const float* S0, void* O, float* Sfin, void* ws,
                                  const int* cu, const int* off, int nseq, int nchunks, int Ttok,
-                                 int H, int dk, int dv, int C, int N, int S, bool exact,
+                                 int H, int dk, int dv, int C, int N, int S, int mode,
                                  float scale, int dtype, hipStream_t st);
 int64_t fwd_workspace_elems(int C, int dk, int dv);
 // the fused kernel over packed sequences (C <= 64): cu, off device tables of

@@ -256,7 +256,7 @@ def test_forward_validation():
     assert call(L=100) == SHAPE
     assert call(dv=32) == SHAPE
     assert call(N=64) == PARAM
-    assert call(exact=2) == PARAM
+    assert call(exact=4) == PARAM
     assert call(dt=2) == DTYPE
     assert call(C=128) == UNSUP
     assert call(Q=None) == NULL
@@ -288,6 +288,15 @@ def test_forward_phase_validation():
     assert p(*bad, None) == ALIAS
     bad = list(pb); bad[8] = 0  # no chunk: nothing to prepare
     assert p(*bad, None) == OK
+    # inverse modes: 0 T_hat, 1 exact, 2 / 3 integer T_hat (default order, dk = dv = 128)
+    bad = list(pb); bad[15] = 4
+    assert p(*bad, None) == PARAM
+    bad = list(pb); bad[15] = 2; bad[10] = 64
+    assert p(*bad, None) == UNSUP
+    bad = list(pb); bad[15] = 3; bad[13] = 2
+    assert p(*bad, None) == UNSUP
+    bad = list(pb); bad[15] = 2; bad[13] = 70
+    assert p(*bad, None) == PARAM
     s = L.gdn_chunk_forward_state
     # Q, g, S0, O, S_final, ws, wsb, B, L, H, dk, dv, C, scale, dt
     sb = [P1, 4 * BIG, None, 5 * BIG, None, 6 * BIG, need, 1, 128, 1, 128, 128, 64, 1.0, 1]
@@ -365,7 +374,7 @@ def test_forward_varlen_validation():
     assert call(nch=300) == SHAPE                # more chunks than tokens
     assert call(C=48) == SHAPE
     assert call(C=128) == UNSUP
-    assert call(exact=2) == PARAM
+    assert call(exact=4) == PARAM
     assert call(N=64) == PARAM
     assert call(dt=2) == DTYPE
     assert call(O=None) == NULL
