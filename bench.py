@@ -67,6 +67,9 @@ def parse():
                              "unfused", "int8", "int16", "forward"])
     ap.add_argument("--exact", action="store_true",
                     help="--path forward / --varlen: the exact block-wise inverse instead of T_hat(N, S)")
+    ap.add_argument("--inverse", default=None, choices=["neumann", "exact", "int16", "int8"],
+                    help="--path forward: the inverse inside the layer (int16 / int8: the "
+                         "integer T_hat(N, S), the quantised GDN layer)")
     ap.add_argument("--varlen", action="store_true",
                     help="--path fused over packed sequences of a serving mix of lengths "
                          "(log-uniform 1..4096, B*L tokens in total, ragged last chunks)")
@@ -332,8 +335,10 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
                      dtype=torch.uint8, device="cuda")
     scale = w.dk ** -0.5
     stream = torch.cuda.current_stream()
-    step = lambda: G.gdn_chunk_forward(dQ, dK, dV, db, dg, C, S0=dS0, N=N, S=S, exact=a.exact,
-                                       scale=scale, O=dO, S_final=dSf, workspace=ws)
+    inv_mode = a.inverse or ("exact" if a.exact else "neumann")
+    step = lambda: G.gdn_chunk_forward(dQ, dK, dV, db, dg, C, S0=dS0, N=N, S=S,
+                                       inverse=inv_mode, scale=scale, O=dO, S_final=dSf,
+                                       workspace=ws)
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
@@ -349,7 +354,7 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
     ms_per_step = wall * 1e3 / a.steps
     # the two launches apart, and the inverse alone on the same chunks
     prep_ms = _time(lambda: G.gdn_chunk_forward_prepare(dQ, dK, dV, db, dg, C, ws, N=N, S=S,
-                                                        exact=a.exact), a.steps, stream, torch)
+                                                        inverse=inv_mode), a.steps, stream, torch)
     state_ms = _time(lambda: G.gdn_chunk_forward_state(dQ, dg, C, ws, w.dv, S0=dS0, scale=scale,
                                                        O=dO, S_final=dSf), a.steps, stream, torch)
     del ws
@@ -384,7 +389,9 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "C": C, "dk": w.dk,
                    "dv": w.dv, "N": N, "S": S, "tiles": n_tiles, "path": "forward",
-                   "inverse": "exact block-wise" if a.exact else f"T_hat({N},{S})",
+                   "inverse": {"exact": "exact block-wise", "neumann": f"T_hat({N},{S})",
+                               "int16": f"INT16 T_hat({N},{S})",
+                               "int8": f"INT8 T_hat({N},{S})"}[inv_mode],
                    "parallelism": "none (1 GPU)"},
         "tokens_per_s": round(w.B * w.L / (ms_per_step * 1e-3), 1),
         "layer_ms": round(ev_ms, 6),
@@ -397,12 +404,12 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": (measured_traffic("forward", w.name, C, N, S, default_order)
-                                 if kernel == "k_fwd_state" and not a.exact else None),
+                                 if kernel == "k_fwd_state" and inv_mode == "neumann" else None),
                      "kernel": kernel, "kernel_ms": round(kms, 6),
                      "algorithmic_bytes": kbytes},
     }
     if host is not None:
-        out["cpu_baseline"] = cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale)
+        out["cpu_baseline"] = cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale, inv_mode)
     print(json.dumps(out), flush=True)
 
 
@@ -594,7 +601,7 @@ def bench_varlen(a, w, C, N, S, G, torch):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale):
+def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale, inv_mode="neumann"):
     """The forward oracle (float64 numpy, chunk-wise form) on whole heads of
     the same workload, passes repeated until `cpu_seconds` have elapsed, and
     the GPU's max abs error against it on those heads."""
@@ -611,8 +618,11 @@ def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale):
     pick = lambda x: np.stack([x[b, :, h] for b, h in heads], 1)[None].astype(np.float64)
     Qs, Ks, Vs, bs, gs = (pick(x) for x in (Q, K, V, beta, g))
     S0s = np.stack([S0[b, h] for b, h in heads], 0)[None].astype(np.float64)
-    inv = (gdn.forward_substitution_inverse if a.exact else
-           (lambda A: gdn.neumann_inverse(A, N, S)))
+    from oracle import int8 as oi
+    inv = {"exact": gdn.forward_substitution_inverse,
+           "neumann": lambda A: gdn.neumann_inverse(A, N, S),
+           "int16": lambda A: oi.dequantized_inverse(A, N, S, oi.SPEC16),
+           "int8": lambda A: oi.dequantized_inverse(A, N, S, oi.SPEC8)}[inv_mode]
     passes, t0 = 0, time.perf_counter()
     while True:
         Or, Sr = fwd.gdn_chunked(Qs, Ks, Vs, bs, gs, C, S0s, scale=scale, inverse=inv)
@@ -626,7 +636,7 @@ def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale):
     return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{len(heads)} heads x {nc} chunks of {w.name}, {passes} passes of the "
-                      f"chunk-wise forward in float64 numpy, {secs:.2f} s",
+                      f"chunk-wise forward in float64 numpy ({inv_mode} inverse), {secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"O": float(np.max(np.abs(Og - Or))),
                                           "S_final": float(np.max(np.abs(Sg - Sr)))}}
 
