@@ -357,6 +357,17 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
                                                         inverse=inv_mode), a.steps, stream, torch)
     state_ms = _time(lambda: G.gdn_chunk_forward_state(dQ, dg, C, ws, w.dv, S0=dS0, scale=scale,
                                                        O=dO, S_final=dSf), a.steps, stream, torch)
+    # how far the layer's output moves from the layer with the exact inverse
+    # (the effect of the approximation, and of the integer codes, on O)
+    dev_vs_exact = None
+    if inv_mode != "exact":
+        Oe, Se = G.gdn_chunk_forward(dQ, dK, dV, db, dg, C, S0=dS0, inverse="exact", scale=scale,
+                                     workspace=ws)
+        torch.cuda.synchronize()
+        dev_vs_exact = {"O": float(((dO.float() - Oe.float()).abs().max() /
+                                    Oe.float().abs().max()).item()),
+                        "S_final": float(((dSf - Se).abs().max() / Se.abs().max()).item())}
+        del Oe, Se
     del ws
     dA = G.gdn_build_A(dK, db, dg, C, a_dtype=dt)
     dT = torch.empty_like(dA)
@@ -401,6 +412,7 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
         "fwdsub_alone_ms": round(fws_ms, 6),
         "inverse_share_of_layer": round(inv_ms / ev_ms, 4),
         "fwdsub_share_if_swapped_in": round(fws_ms / (ev_ms - inv_ms + fws_ms), 4),
+        "rel_dev_vs_exact_inverse_layer": dev_vs_exact,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": (measured_traffic("forward", w.name, C, N, S, default_order)
