@@ -91,3 +91,25 @@ def test_fused_path_past_4GiB():
         assert np.max(np.abs(host(U[:, sl]) - Ur)) <= 2e-2 * max(1.0, np.max(np.abs(Ur))), ck
     del dK, dV, db, dg, W, U
     torch.cuda.empty_cache()
+
+
+def test_int16_blockwise_c128_past_4GiB():
+    """The block-wise integer inverse at C = 128 (three exponents per tile)
+    with int16 codes past 2^32 bytes: 8 seeded tiles repeated."""
+    C, nb = 128, 8
+    A0 = base_tiles(C, nb, seed=2).astype(np.float32)
+    qA, eA = oi.quantize_blocked(A0, oi.SPEC16)
+    reps = (1 << 32) // (C * C * 2) // nb + 2
+    n = nb * reps
+    print(f"int16 C=128 past 4 GiB: {n} tiles, {n * C * C * 2 / 2**30:.2f} GiB of codes",
+          flush=True)
+    dq = torch.from_numpy(qA.astype(np.int16)).to("cuda").repeat(reps, 1, 1)
+    de = torch.from_numpy(eA.astype(np.int32)).to("cuda").repeat(reps, 1)
+    Tq, eT = G.gdn_chunk_inverse_neumann_i16(dq, de, 3, 8)
+    rq, re = oi.neumann_inverse_int_blocked(qA, eA, 3, 8, oi.SPEC16)
+    torch.cuda.synchronize()
+    for start in (0, (reps // 2) * nb, n - nb):
+        assert np.array_equal(Tq[start:start + nb].cpu().numpy().astype(np.int64), rq), start
+        assert np.array_equal(eT[start:start + nb].cpu().numpy().astype(np.int64), re), start
+    del dq, de, Tq, eT
+    torch.cuda.empty_cache()
