@@ -428,6 +428,7 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
 def bench_forward_varlen(a, w, C, N, S, G, torch):
     """The layer forward over packed sequences (gdn_chunk_forward_varlen) on
     the serving mix of the workload's token count."""
+    inv_mode = a.inverse or ("exact" if a.exact else "neumann")
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     es = 2 if w.dtype == "bf16" else 4
     lengths = wl.varlen_lengths(w.B * w.L)
@@ -448,7 +449,7 @@ def bench_forward_varlen(a, w, C, N, S, G, torch):
     scale = w.dk ** -0.5
     stream = torch.cuda.current_stream()
     step = lambda: G.gdn_chunk_forward_varlen(dQ, dK, dV, db, dg, tables, C, S0=dS0, N=N, S=S,
-                                              exact=a.exact, scale=scale, O=dO, S_final=dSf,
+                                              inverse=inv_mode, scale=scale, O=dO, S_final=dSf,
                                               workspace=ws)
     for _ in range(a.warmup):
         step()
@@ -485,7 +486,9 @@ def bench_forward_varlen(a, w, C, N, S, G, torch):
                    "ragged_sequences": int(sum(1 for x in lengths if x % C)), "H": w.H, "C": C,
                    "dk": w.dk, "dv": w.dv, "N": N, "S": S, "tiles": n_tiles,
                    "path": "forward varlen",
-                   "inverse": "exact block-wise" if a.exact else f"T_hat({N},{S})",
+                   "inverse": {"exact": "exact block-wise", "neumann": f"T_hat({N},{S})",
+                               "int16": f"INT16 T_hat({N},{S})",
+                               "int8": f"INT8 T_hat({N},{S})"}[inv_mode],
                    "parallelism": "none (1 GPU)"},
         "tokens_per_s": round(T / (ms_per_step * 1e-3), 1),
         "layer_ms": round(ev_ms, 6),
@@ -496,8 +499,11 @@ def bench_forward_varlen(a, w, C, N, S, G, torch):
     }
     if not a.no_cpu_baseline:
         from oracle import gdn, varlen
-        inv = gdn.forward_substitution_inverse if a.exact else \
-            (lambda A: gdn.neumann_inverse(A, N, S))
+        from oracle import int8 as oi
+        inv = {"exact": gdn.forward_substitution_inverse,
+               "neumann": lambda A: gdn.neumann_inverse(A, N, S),
+               "int16": lambda A: oi.dequantized_inverse(A, N, S, oi.SPEC16, C=C),
+               "int8": lambda A: oi.dequantized_inverse(A, N, S, oi.SPEC8, C=C)}[inv_mode]
         ns, chunks, t_end = 0, 0, 0
         while ns < len(lengths) and chunks < max(1, a.cpu_sample_tiles // w.H):
             chunks += -(-lengths[ns] // C)
@@ -521,7 +527,7 @@ def bench_forward_varlen(a, w, C, N, S, G, torch):
             "cores": _threads(), "kind": "oracle",
             "sample": f"the first {ns} sequences ({t_end} tokens, {chunks} chunks per head, "
                       f"{w.H} heads), {passes} passes of the packed chunk-wise forward in "
-                      f"float64 numpy, {secs:.2f} s",
+                      f"float64 numpy ({inv_mode} inverse), {secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"O": float(np.max(np.abs(Og - Or))),
                                           "S_final": float(np.max(np.abs(Sg - Sr)))}}
     print(json.dumps(out), flush=True)
