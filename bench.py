@@ -757,7 +757,9 @@ def error_grid(a, G, torch):
     stress heads (shared key direction, slow decay; |A| up to ~0.5).  A is
     built on the GPU in fp32; X is the fp32 forward substitution of that A
     (within ~1e-7 of the exact inverse, the floor of every figure here);
-    bf16 mode inverts A rounded to bf16.  Per (C, set, dtype, N, S): max abs
+    bf16 mode inverts A rounded to bf16; int16 / int8 quantise A (per tile,
+    per block at C = 128) and run the integer inverse, dequantised.  Per
+    (C, set, dtype, N, S): max abs
     error over tiles and the per-tile SNR 10 log10(|X|_F^2 / |X - T_hat|_F^2),
     mean and worst."""
     Cs = [a.C] if a.C else [16, 32, 64, 128]
@@ -775,12 +777,24 @@ def error_grid(a, G, torch):
             A32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
             X = G.gdn_chunk_inverse_fwdsub(A32).double()
             xn = (X ** 2).sum(dim=(-1, -2))
-            for dtn, A in (("f32", A32), ("bf16", A32.to(torch.bfloat16))):
+            # the integer modes: quantised per tile (per block at C = 128), the
+            # integer T_hat(N, S), dequantised
+            def int_inverse(quant, inv):
+                qA, eA = quant(A32)
+                return lambda N, S: inv(qA, eA, N, S, want_deq=True)[2].double()
+            modes = [("f32", lambda N, S: G.gdn_chunk_inverse_neumann(A32, N, S).double()),
+                     ("bf16", lambda N, S: G.gdn_chunk_inverse_neumann(
+                         A32.to(torch.bfloat16), N, S).double()),
+                     ("int16", int_inverse(G.gdn_quantize_tiles_i16,
+                                           G.gdn_chunk_inverse_neumann_i16)),
+                     ("int8", int_inverse(G.gdn_quantize_tiles_i8,
+                                          G.gdn_chunk_inverse_neumann_i8))]
+            for dtn, inverse in modes:
                 for N in range(1, 7):
                     for S in range(0, 17):
                         if N > lim or S > lim:
                             continue
-                        T = G.gdn_chunk_inverse_neumann(A, N, S).double()
+                        T = inverse(N, S)
                         d = T - X
                         en = (d ** 2).sum(dim=(-1, -2))
                         snr = 10 * torch.log10(xn / en.clamp_min(1e-300))
