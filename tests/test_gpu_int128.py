@@ -266,3 +266,42 @@ def test_fused_vs_oracle_and_float(width):
     err = np.max(np.abs(got - T), axis=(-1, -2))
     bits = 8 if width == "i8" else 16
     assert np.all(err <= 16 * 2.0 ** -bits * scale)
+
+
+@pytest.mark.parametrize("width", ["i8", "i16"])
+def test_fused_full_size_sampled(width):
+    """The one launch at the size bench.py times (low-bit workload at C = 128:
+    B=4, H=32, L=16384, bf16 K; 16384 tiles): equal to the three launches on
+    the GPU bit for bit everywhere, and on a sample of tiles within a few
+    quanta of the integer oracle run from its own fp32 A (an A entry a
+    rounding apart can move a code)."""
+    spec, _, quant, inv = WIDTHS[width]
+    w = wl.workload("int8").with_(C=C)
+    K, beta, g, _ = wl.gen_inputs(w, C=C, want_v=False)
+    print(f"{width} C=128 fused full size: {w.B * w.H * (w.L // C)} tiles", flush=True)
+    dK, db, dg = to_cuda(K, torch.bfloat16), to_cuda(beta), to_cuda(g)
+    q2, e2, d2 = FUSED[width](dK, db, dg, C, 3, 8, want_deq=True)
+    A = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
+    Aq, eA = quant(A)
+    del A
+    q1, e1 = inv(Aq, eA, 3, 8)
+    assert torch.equal(q1, q2) and torch.equal(e1, e2)
+    del q1, e1, Aq, eA
+    nc = w.L // C
+    rng = np.random.default_rng(1280)
+    picks = [(0, 0, 0), (w.B - 1, w.H - 1, nc - 1)] + [
+        (int(rng.integers(w.B)), int(rng.integers(w.H)), int(rng.integers(nc))) for _ in range(30)]
+    for b, h, ck in picks:
+        sl = slice(ck * C, (ck + 1) * C)
+        Af = gdn.tiles_flat(gdn.build_A(K[b:b + 1, sl, h:h + 1], beta[b:b + 1, sl, h:h + 1],
+                                        g[b:b + 1, sl, h:h + 1], C))
+        qA, eAr = oi.quantize_blocked(Af.astype(np.float32), spec)
+        rq, re = oi.neumann_inverse_int_blocked(qA, eAr, 3, 8, spec)
+        t = (b * w.H + h) * nc + ck
+        got = host(d2.reshape(-1, C, C)[t]).astype(np.float64)
+        ref = oi.dequant_unit_blocked(rq, re)[0]
+        quantum = np.ones((C, C))
+        for k, (rs, cs) in enumerate([(slice(0, 64), slice(0, 64)), (slice(64, 128), slice(0, 64)),
+                                      (slice(64, 128), slice(64, 128))]):
+            quantum[rs, cs] = np.ldexp(1.0, re[0, k])
+        assert np.max(np.abs(got - ref) / quantum) <= 64.0, (b, h, ck)
