@@ -47,7 +47,10 @@
 extern "C" {
 #endif
 
-#define GDN_ABI_VERSION 1
+/* 2: the integer quantiser and inverses accept C = 128 (three exponents per
+ * tile) and the layer forward's `exact` argument takes the integer inverse
+ * modes 2 and 3; every call valid under 1 behaves as before. */
+#define GDN_ABI_VERSION 2
 
 enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1, GDN_I8 = 2 };
 

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert g.gdn_abi_version() == 1
+    assert g.gdn_abi_version() == 2
     for code in (OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP, WS, 12345):
         assert isinstance(g.gdn_status_string(code), str) and g.gdn_status_string(code)
 
