@@ -314,7 +314,13 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
   const int64_t ldk = (int64_t)H * DK;
-  load_gates<C>(beta, g, ch, L, H, sb, sg);  // both waves (it ends in a workgroup barrier)
+  {
+    const int r = threadIdx.x;  // 128 threads, one row each
+    const int64_t o = ((int64_t)ch.b * L + ch.t0 + r) * H + ch.h;
+    sb[r] = beta[o];
+    sg[r] = g[o];
+  }
+  __syncthreads();
 
   // ---- this wave's diagonal block of A (fp32, row form), quantised
   AccI<4> Lr;
