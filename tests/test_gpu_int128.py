@@ -9,6 +9,12 @@ distributions (default and wide gates, stress tiles), random codes with
 independent block exponents (every rebase path of the merge's sums), tiles
 with zero blocks (absent terms), compile-time and run-time orders, many tiles
 with a ragged count, and the low-bit workload at full size, sampled.
+
+The one-launch path from K (gdn_chunk_inverse_neumann_i8/_i16_fused at
+C = 128) forms A in fp32 on the GPU: it must equal the three launches
+(gdn_build_A, the quantiser, the inverse) bit for bit, and the integer oracle
+run from its own fp32 A within a few quanta (an A entry one rounding apart
+can move a code).
 """
 
 import numpy as np
