@@ -386,3 +386,16 @@ def test_forward_varlen_validation():
     assert call(Sf=b[6] + 64) == ALIAS           # S_final over O
     assert call(nseq=0, nch=0) == OK
     assert call(H=0) == OK
+
+
+def test_binding_inverse_modes_and_exponent_layout():
+    """Host logic of the binding: the layer forward's inverse modes map onto
+    the ABI's `exact` values (0 T_hat, 1 exact, 2 INT16, 3 INT8), and the
+    integer paths carry three exponents per tile at C = 128 only."""
+    from paper_2606_06034_amd import _binding as b
+    assert b._fwd_mode(False, None) == 0 and b._fwd_mode(True, None) == 1
+    assert [b._fwd_mode(False, m) for m in ("neumann", "exact", "int16", "int8")] == [0, 1, 2, 3]
+    assert b._fwd_mode(True, "int8") == 3  # an explicit mode wins over exact
+    with pytest.raises(ValueError):
+        b._fwd_mode(False, "int4")
+    assert [b._nexp(C) for C in (16, 32, 64, 128)] == [1, 1, 1, 3]
