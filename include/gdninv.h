@@ -164,7 +164,9 @@ int gdn_chunk_wy_fused_blockwise(const void* K, const void* V, const float* beta
  * chunks write nothing (never an access outside the arrays).  W, U:
  * [1, T, H, d], rows of every token written.  Tinv (nullable):
  * [H, n_chunks, C, C], the m x m inverse in the top left of each tile and the
- * identity past m.  C in {16, 32, 64}. */
+ * identity past m.  C in {16, 32, 64, 128}; C = 128 in the block form of
+ * gdn_chunk_wy_fused, a partial chunk as the 128 x 128 tile padded with
+ * tokens that write nothing. */
 int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, const float* g,
                               void* W, void* U, void* Tinv, const int32_t* cu_seqlens,
                               const int32_t* chunk_offsets, int nseq, int n_chunks, int T, int H,

@@ -226,7 +226,6 @@ int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, c
   if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
   if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
-  if (C == 128) return GDN_ERR_UNSUPPORTED;
   if (n_chunks == 0 || H == 0) return GDN_OK;
   if (!K || !V || !beta || !g || !W || !U || !cu_seqlens || !chunk_offsets) return GDN_ERR_NULL;
   if (!aligned(K) || !aligned(V) || !aligned(beta) || !aligned(g) || !aligned(W) ||

@@ -176,7 +176,7 @@ template <typename F, typename TIO>
 __device__ __forceinline__ void block2_slice(const RowP<4, F>& X22R, const Pair<F> (&NA)[4][2],
                                              const Pair<F> (&x2)[4], const Pair<F> (&o1)[4],
                                              const float* sb2, TIO* __restrict__ ob, int64_t ld,
-                                             int q, Lane ln) {
+                                             int q, Lane ln, int m2 = 64) {
   const int g = ln.g(), c = ln.c();
   const f32x4 e = eye4(ln);
   const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
@@ -217,38 +217,51 @@ __device__ __forceinline__ void block2_slice(const RowP<4, F>& X22R, const Pair<
 #pragma unroll
       for (int p = 0; p < 2; ++p)
         if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(X22R.r[I][p], y2[h][p], acc[h]);
-    store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
+    if (I * 16 + c < m2) store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
   }
 }
 
+// VARLEN: packed sequences (B = 1, L = T tokens, chunk tables pk): a chunk
+// of m < 128 tokens is the tile padded with tokens that write nothing (beta
+// = 0, keys and values read from the last token and zeroed), so its rows
+// past m are neither read for output nor written; a half with no token
+// (m <= 64) still runs, on zeros.
 template <int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool EXACT = false>
+          bool EXACT = false, bool VARLEN = false>
 __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
                                                   const TIO* __restrict__ V,
                                                   const float* __restrict__ beta,
                                                   const float* __restrict__ g,
                                                   TIO* __restrict__ W, TIO* __restrict__ U,
                                                   TIO* __restrict__ Tout, int L, int H, int N,
-                                                  int S) {
+                                                  int S, Packed pk) {
   constexpr int NB = 4, C = 128;
   __shared__ float sb[C], sg[C];
   __shared__ __attribute__((aligned(16))) TIO sK1[NB * (DK / 32) * 512];
   __shared__ __attribute__((aligned(16))) TIO sW1[NB * (DK / 32) * 512];
   __shared__ __attribute__((aligned(16))) TIO sU1[NB * (DV / 32) * 512];
-  const Chunk ch(blockIdx.x, L, H, C);
+  Chunk ch;
+  if constexpr (VARLEN)
+    ch = Chunk::packed(blockIdx.x, H, C, L, pk.cu, pk.off, pk.nseq, pk.nchunks);
+  else
+    ch = Chunk(blockIdx.x, L, H, C);
+  const int m = VARLEN ? ch.m : C;
+  if (VARLEN && m <= 0) return;  // the whole workgroup, before any barrier
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
   const int64_t ldk = (int64_t)H * DK, ldv = (int64_t)H * DV;
   {
     const int r = threadIdx.x;  // 128 threads, one row each
-    const int64_t o = ((int64_t)ch.b * L + ch.t0 + r) * H + ch.h;
-    sb[r] = beta[o];
+    const int rr = r < m ? r : m - 1;
+    const int64_t o = ((int64_t)ch.b * L + ch.t0 + rr) * H + ch.h;
+    sb[r] = r < m ? beta[o] : 0.f;
     sg[r] = g[o];
   }
-  // ---- this wave's half: K rows, A_kk, X_kk
+  // ---- this wave's half: K rows, A_kk, X_kk (rows past m read from row
+  // m - 1 and zeroed: the base is row r0, so the row count passed is m - r0)
   const int r0 = 64 * wv;
   Pair<F> kp[NB][DK / 32];
-  load_rows<NB, DK>(kp, K + ch.row(r0, L, H, DK), ldk);
+  load_rows<NB, DK>(kp, K + ch.row(r0, L, H, DK), ldk, ln, m - r0);
   if (wv == 0) {
 #pragma unroll
     for (int I = 0; I < NB; ++I)
@@ -275,10 +288,10 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
     }
     RowP<NB, F> TR;
     scale_cols(TR, Tr, sb);
-    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, sW1);
+    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, sW1, m);
     Pair<F> vp[NB][DV / 32];
-    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv);
-    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln, sU1);
+    load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv, ln, m);
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln, sU1, m);
   }
   __syncthreads();  // W_1, U_1 (and Tout rows 0..63) written
   if (wv == 1) {
@@ -316,17 +329,19 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
         x2[I] = kp[I][q];
         o1[I] = LdsRows<DK, F, TIO>{sW1, ln.id}(I, q);
       }
-      block2_slice<F>(X22R, NA, x2, o1, sb + 64, W + ch.row(64, L, H, DK), ldk, q, ln);
+      block2_slice<F>(X22R, NA, x2, o1, sb + 64, W + ch.row(64, L, H, DK), ldk, q, ln, m - 64);
     }
 #pragma unroll
     for (int q = 0; q < DV / 32; ++q) {
       Pair<F> x2[4], o1[4];
 #pragma unroll
       for (int I = 0; I < 4; ++I) {
-        x2[I] = load_row8<F>(V + ch.row(64 + I * 16 + ln.c(), L, H, DV) + 32 * q + 8 * ln.g());
+        const int r = 64 + I * 16 + ln.c(), rr = r < m ? r : m - 1;
+        x2[I] = load_row8<F>(V + ch.row(rr, L, H, DV) + 32 * q + 8 * ln.g());
+        if (r >= m) x2[I] = Pair<F>::zero();
         o1[I] = LdsRows<DV, F, TIO>{sU1, ln.id}(I, q);
       }
-      block2_slice<F>(X22R, NA, x2, o1, sb + 64, U + ch.row(64, L, H, DV), ldv, q, ln);
+      block2_slice<F>(X22R, NA, x2, o1, sb + 64, U + ch.row(64, L, H, DV), ldv, q, ln, m - 64);
     }
     if (Tout) {
       // X_21 = X_22 (-A_21 X_11), X_11 read back from Tout (written by wave 0
@@ -501,11 +516,17 @@ static hipError_t run_fused_nb(const void* K, const void* V, const float* beta, 
 template <typename F, typename TIO>
 static hipError_t run_fused128(const void* K, const void* V, const float* beta, const float* g,
                                void* W, void* U, void* T, int64_t n, int L, int H, int dk,
-                               int dv, int N, int S, bool exact, hipStream_t st) {
-#define GDN_F128(SM, NC_, SC_, EX)                                                            \
-  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO, EX>), dim3((unsigned)n),       \
+                               int dv, int N, int S, bool exact, hipStream_t st,
+                               const Packed& pk = Packed{}) {
+#define GDN_F128_(SM, NC_, SC_, EX, VL)                                                        \
+  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO, EX, VL>), dim3((unsigned)n),    \
                      dim3(128), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, \
-                     (TIO*)T, L, H, N, S)
+                     (TIO*)T, L, H, N, S, pk)
+#define GDN_F128(SM, NC_, SC_, EX)    \
+  if (pk.cu)                          \
+    GDN_F128_(SM, NC_, SC_, EX, true); \
+  else                                \
+    GDN_F128_(SM, NC_, SC_, EX, false)
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
     if (exact)
       GDN_F128(true, 0, 0, true);
@@ -518,6 +539,7 @@ static hipError_t run_fused128(const void* K, const void* V, const float* beta, 
     return hipGetLastError();
   }))
 #undef GDN_F128
+#undef GDN_F128_
   return hipErrorNotSupported;
 }
 
@@ -548,12 +570,18 @@ hipError_t launch_fused_varlen(const void* K, const void* V, const float* beta, 
       case 16: GDN_FV(1, f32x4, float);
       case 32: GDN_FV(2, f32x4, float);
       case 64: GDN_FV(4, f32x4, float);
+      case 128:
+        return run_fused128<f32x4, float>(K, V, beta, g, W, U, T, n, Ttok, H, dk, dv, N, S, exact,
+                                          st, pk);
     }
   } else if (dtype == 1) {
     switch (C) {
       case 16: GDN_FV(1, bf16x4, __bf16);
       case 32: GDN_FV(2, bf16x4, __bf16);
       case 64: GDN_FV(4, bf16x4, __bf16);
+      case 128:
+        return run_fused128<bf16x4, __bf16>(K, V, beta, g, W, U, T, n, Ttok, H, dk, dv, N, S,
+                                            exact, st, pk);
     }
   }
 #undef GDN_FV

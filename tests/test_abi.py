@@ -332,7 +332,9 @@ def test_fused_varlen_validation():
     assert call(N=64) == PARAM
     assert call(exact=3) == PARAM
     assert call(dt=2) == DTYPE
-    assert call(C=128) == UNSUP
+    assert call(C=128, N=64) == PARAM   # C = 128 accepted up to the launch
+    assert call(C=128, cu=None) == NULL
+    assert call(C=128, nch=0, K=None) == OK
     assert call(cu=None) == NULL
     assert call(W=None) == NULL
     assert call(off=6 * BIG + 2) == ALIGN

@@ -42,14 +42,29 @@ def run(lengths, C, dt, exact=False, N=None, S=None, H=3, seed=0, dk=128, dv=128
     tables = G.gdn_varlen_tables(cu, C)
     Wg, Ug, Tg = G.gdn_chunk_wy_fused_varlen(dev(K, dt), dev(V, dt), dev32(beta), dev32(g), tables,
                                              C, N=N, S=S, exact=exact, want_T=True)
-    if exact:
-        inv = gdn.forward_substitution_inverse
-    else:
-        dn, ds = gdn.default_order(C)
-        n, s = (dn if N is None else N), (ds if S is None else S)
-        inv = lambda A: gdn.neumann_inverse(A, n, s)
-    Wr, Ur, Tr = varlen.wy_varlen(K, V, beta, g, cu, C, inverse=inv)
+    Wr, Ur, Tr = varlen.wy_varlen(K, V, beta, g, cu, C, inverse=oracle_inverse(C, exact, N, S))
     return (host(Wg), host(Ug), host(Tg)), (Wr, Ur, Tr), cu
+
+
+def padded(inv, C):
+    """An m x m inverse taken as the top left of `inv` on the system padded
+    to C x C with tokens that write nothing (zero rows and columns)."""
+    def f(A):
+        m = A.shape[-1]
+        P = np.zeros(A.shape[:-2] + (C, C))
+        P[..., :m, :m] = A
+        return inv(P)[..., :m, :m]
+    return f
+
+
+def oracle_inverse(C, exact, N=None, S=None):
+    if exact:
+        return gdn.forward_substitution_inverse
+    dn, ds = gdn.default_order(C)
+    n, s = (dn if N is None else N), (ds if S is None else S)
+    if C == 128:  # the two 64 x 64 blocks of the fixed-length C = 128 path
+        return padded(lambda A: gdn.neumann_inverse_blocked(A, n, s), C)
+    return lambda A: gdn.neumann_inverse(A, n, s)
 
 
 def check(got, ref, dt):
@@ -65,11 +80,29 @@ RAGGED = [1, 15, 16, 17, 63, 64, 65, 130, 0, 7, 200]
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
 @pytest.mark.parametrize("exact", [False, True])
 def test_varlen_matches_oracle(C, dt, exact):
     got, ref, _ = run(RAGGED, C, dt, exact=exact, seed=C)
     check(got, ref, dt)
+
+
+RAGGED128 = [1, 63, 64, 65, 127, 128, 129, 0, 200, 256, 300]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_varlen_c128_half_boundaries(dt):
+    # partial chunks with no token in the second half (m <= 64), tokens in
+    # both halves, and full chunks
+    got, ref, _ = run(RAGGED128, 128, dt, seed=7)
+    check(got, ref, dt)
+
+
+def test_varlen_c128_other_orders_and_widths():
+    got, ref, _ = run([5, 100, 190], 128, "f32", N=2, S=3, dk=64, dv=128, seed=12)
+    check(got, ref, "f32")
+    got, ref, _ = run([70, 33], 128, "f32", N=16, S=2, dk=128, dv=64, seed=13)
+    check(got, ref, "f32")
 
 
 @pytest.mark.parametrize("C", [16, 64])
