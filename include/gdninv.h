@@ -37,6 +37,9 @@
  *   n_tiles == 0 (or B == 0) is a no-op returning GDN_OK.
  * Sizes.  C in {16, 32, 64, 128}; L % C == 0; dk, dv in {64, 128};
  *   0 <= N <= C - 1 and 0 <= S <= C - 1 (C = 128: N, S <= 63, see below).
+ *   A batch with L % C != 0 goes through the packed-sequence entry points
+ *   (gdn_chunk_wy_fused_varlen, gdn_chunk_forward_varlen) as B sequences of
+ *   L tokens each, the last chunk of each a partial one.
  */
 #ifndef GDNINV_H
 #define GDNINV_H

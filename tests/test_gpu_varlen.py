@@ -98,6 +98,13 @@ def test_varlen_c128_half_boundaries(dt):
     check(got, ref, dt)
 
 
+@pytest.mark.parametrize("C", [64, 128])
+def test_varlen_batch_of_equal_ragged_lengths(C):
+    # a [B, L] batch with L % C != 0 as B packed sequences of L tokens
+    got, ref, _ = run([100, 100, 100], C, "bf16", seed=21 + C)
+    check(got, ref, "bf16")
+
+
 def test_varlen_c128_other_orders_and_widths():
     got, ref, _ = run([5, 100, 190], 128, "f32", N=2, S=3, dk=64, dv=128, seed=12)
     check(got, ref, "f32")
