@@ -136,17 +136,17 @@ def test_varlen_equal_lengths_match_fixed_length_path_bit_for_bit():
     assert torch.equal(Tf.permute(1, 0, 2, 3, 4).reshape(H, B * nc, C, C), Tv)
 
 
-def test_varlen_serving_mix_full_size():
+@pytest.mark.parametrize("C", [64, 128])
+def test_varlen_serving_mix_full_size(C):
     # the serving mix at the prefill's size: 8192 tokens, 16 heads, bf16;
     # every chunk of every head checked
-    C, dt = 64, "bf16"
+    dt = "bf16"
     lengths = wl.varlen_lengths(8192)
     w = wl.workload("qwen35_prefill")
     K, beta, g, V, cu = wl.gen_varlen(w, lengths, C=C)
     tables = G.gdn_varlen_tables(cu, C)
     Wg, Ug = G.gdn_chunk_wy_fused_varlen(dev(K, dt), dev(V, dt), dev32(beta), dev32(g), tables, C)
-    Wr, Ur, _ = varlen.wy_varlen(K, V, beta, g, cu, C,
-                                 inverse=lambda A: gdn.neumann_inverse(A, 3, 8))
+    Wr, Ur, _ = varlen.wy_varlen(K, V, beta, g, cu, C, inverse=oracle_inverse(C, False))
     assert np.max(np.abs(host(Wg) - Wr)) <= TOL[dt] * max(1.0, np.max(np.abs(Wr)))
     assert np.max(np.abs(host(Ug) - Ur)) <= TOL[dt] * max(1.0, np.max(np.abs(Ur)))
 
