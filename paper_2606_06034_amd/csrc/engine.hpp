@@ -48,24 +48,40 @@ __device__ __forceinline__ void store4(__bf16* p, f32x4 x) {
 __device__ __forceinline__ float load1(const float* p) { return *p; }
 __device__ __forceinline__ float load1(const __bf16* p) { return (float)*p; }
 
-// Lm = -A of a row-major tile (row stride ldr), both forms, f32 blocks:
-// row form  Lr: lane (g, c) reads 4 consecutive entries of row 16I + c;
-// column form Lc: lane (g, c) reads rows 16I + 4g + v of column 16J + c.
-// Entries on and above the diagonal are taken as 0.
-template <int NB, typename TIO>
-__device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int ldr, Acc<NB>& Lr,
-                                                Acc<NB>& Lc) {
+// T0 = M^(N) (Hadamard) sum Lm^n keeps 0 <= i - j <= N: true for the
+// 16 x 16 blocks at block distance m = I - J that meet that band (SMALLN:
+// N <= 15, so m <= 1).
+template <bool SMALLN>
+__device__ __forceinline__ bool in_t0_band(int m, int N) {
+  if constexpr (SMALLN) {
+    if (m > 1) return false;
+  }
+  return blk_nz(m, 0, N);
+}
+
+// Lm = -A of a row-major tile (row stride ldr) as row-form f32 blocks
+// (lane (g, c) reads 4 consecutive entries of row 16I + c), and the column
+// form (lane (g, c): rows 16I + 4g + v of column 16J + c) of the blocks in
+// T0's band only, the ones the engine reads.  The column blocks come from the
+// row blocks through an identity MFMA (Lr I, exact: each output is one entry
+// times 1 plus zeros) instead of 2-byte gathers from memory: 9 % less time
+// for the standalone inverse at C = 64 on MI355X.  Entries on and above the
+// diagonal are taken as 0.
+template <int NB, typename F, bool SMALLN, typename TIO>
+__device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int ldr, int N,
+                                                Acc<NB>& Lr, Acc<NB>& Lc) {
   const int g = lane_g(), c = lane_c();
+  const Pair<F> Ic = Pair<F>::make(eye4(), zero4());
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J) {
-      f32x4 r = load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g);
-      f32x4 q;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) q[v] = load1(a + (I * 16 + 4 * g + v) * ldr + J * 16 + c);
+      const f32x4 r = load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g);
       Lr.a[bidx(I, J)] = band_block<false>(-r, I - J, 1, 16 * NB);
-      Lc.a[bidx(I, J)] = band_block<true>(-q, I - J, 1, 16 * NB);
+      Lc.a[bidx(I, J)] =
+          in_t0_band<SMALLN>(I - J, N)
+              ? Pair<F>::template mma<false>(Pair<F>::make(Lr.a[bidx(I, J)], zero4()), Ic, zero4())
+              : zero4();
     }
 }
 
@@ -107,14 +123,6 @@ __device__ __forceinline__ void store_unit_row(TIO* __restrict__ t, int ldr, con
 }
 
 // ---------------------------------------------------------------------------
-
-template <bool SMALLN>
-__device__ __forceinline__ bool in_t0_band(int m, int N) {
-  if constexpr (SMALLN) {
-    if (m > 1) return false;
-  }
-  return blk_nz(m, 0, N);
-}
 
 // The approximate inverse.  In: Lm as row pairs (LR), column pairs (LC) and
 // f32 column blocks (Lc; only T0's band blocks are read).  Out: Tr, the

@@ -23,7 +23,7 @@ __device__ __forceinline__ void invert_block(const TIO* __restrict__ a, TIO* __r
     blockwise_inverse<NB, F>(Lr, Tr);
   } else {
     Acc<NB> Lr, Lc;
-    load_neg_strict<NB>(a, ldr, Lr, Lc);
+    load_neg_strict<NB, F, SMALLN>(a, ldr, NC >= 0 ? NC : N, Lr, Lc);
     RowP<NB, F> LR;
     to_rowp(LR, Lr);
     neumann_engine<NB, F, SMALLN, NC, SC, GH>(LR, Lc, N, S, Tr);
