@@ -91,6 +91,19 @@ def test_neumann_matches_oracle(C, dt, stress):
         assert np.all(np.diagonal(T, axis1=-2, axis2=-1) == 1)
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_neumann_orders_past_one_block(dt):
+    # N >= 16: T0's band reaches past the first sub-diagonal 16-block (the
+    # general band path of the engine); workload tiles, both dtypes
+    for C, (N, S) in [(32, (17, 2)), (64, (20, 3)), (64, (40, 1)), (128, (20, 2))]:
+        A = stored(gdn_tiles(C), dt)
+        T = host(G.gdn_chunk_inverse_neumann(dev(A, dt), N, S))
+        ref = gdn.neumann_inverse_blocked(A, N, S) if C == 128 else gdn.neumann_inverse(A, N, S)
+        err = maxerr(T, ref)
+        print(f"C={C} {dt} N={N} S={S} max|err|={err:.3e}", flush=True)
+        assert err <= TOL[dt], (C, N, S, err)
+
+
 def test_neumann_exact_orders_reach_inverse():
     """(S + 1)(N + 1) >= C makes T_hat the exact inverse: compare with X."""
     for C, (N, S) in [(16, (3, 3)), (32, (3, 7)), (64, (3, 15))]:
