@@ -6,14 +6,19 @@
                     [--no-cpu-baseline]
 
 A step is one pass of the hot path over one batch of synthetic inputs
-already resident in HBM.  The default workload is the Qwen3.5-shaped prefill
-(B=1, H=16, L=8192, C=64, dk=dv=128, bf16; 2048 chunk tiles) and the default
-path is the fused kernel: build A -> MatMul-only inverse T_hat(3, 8) -> W, U.
+already resident in HBM.  The default workload is the long-context stress
+shape (B=1, H=32, L=131072, C=64, dk=dv=128, bf16; 65536 chunk tiles), the
+largest single-GPU configuration, and the default path is the fused kernel:
+build A -> MatMul-only inverse T_hat(3, 8) -> W, U.  On the fused path the
+inverse alone (T_hat), the exact block-wise inverse and the forward-
+substitution baseline are also timed on the same tiles (Section 4.3 compares
+the inverse against forward substitution kernel for kernel).
 
 Prints ONE JSON line: throughput in chunk inverses per second, the roofline
 of the dominant kernel (timed with HIP events on the stream it runs on), and
-the CPU oracle timed on a bounded sample of the same workload together with
-the GPU's max abs error against it on that sample.
+the CPU oracle timed on a bounded sample of the same workload (all host
+threads and one thread, T_hat and forward substitution) together with the
+GPU's max abs error against it on that sample.
 
 --path forward runs the whole chunk-wise Gated DeltaNet layer forward
 (gdn_chunk_forward: per-chunk factors, then the state recurrence and the
@@ -59,7 +64,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="qwen35_prefill", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--workload", default="long_context", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--C", type=int, default=None)
     ap.add_argument("--N", type=int, default=None)
     ap.add_argument("--S", type=int, default=None)
@@ -74,6 +79,8 @@ def parse():
                     help="--path fused over packed sequences of a serving mix of lengths "
                          "(log-uniform 1..4096, B*L tokens in total, ragged last chunks)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-same-shape", action="store_true",
+                    help="fused path: skip timing the inverse-only kernels on the same tiles")
     ap.add_argument("--cpu-sample-tiles", type=int, default=2048,
                     help="tiles of the workload the CPU oracle runs on (whole heads)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -114,7 +121,7 @@ def main():
         return
 
     low = a.path in ("int8", "int16")
-    if low and a.workload == "qwen35_prefill" and "--workload" not in sys.argv:
+    if low and "--workload" not in sys.argv:
         a.workload = "int8"
     w = wl.workload(a.workload)
     C = a.C or w.C
@@ -224,8 +231,13 @@ def main():
         bound, peak, unit, achieved = "hbm", HBM_PEAK_GBS, "GB/s", bytes_ / (ev_ms * 1e-3) / 1e9
         kernel = "k_fused" if C < 128 else "k_fused128"
     elif a.path == "inverse":
+        # The bound is chosen from the method's own work: the non-zero
+        # (lower-triangular) part of its N + S products.  At C = 64 that is
+        # 61 FLOP per byte of bf16 tile IO, below the bf16 ridge (312), so
+        # the inverse alone is HBM-bound; the dense-equivalent rate is
+        # reported beside it, labelled as such.
         bytes_ = n_tiles * C * C * es * 2
-        flops = f_inv
+        flops = f_useful
         peak_f = BF16_PEAK_TFLOPS if es == 2 else FP32_PEAK_TFLOPS
         ai_ridge = peak_f * 1e12 / (HBM_PEAK_GBS * 1e9)
         if flops / bytes_ >= ai_ridge:
@@ -234,7 +246,7 @@ def main():
         else:
             bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
             achieved = bytes_ / (ev_ms * 1e-3) / 1e9
-        kernel = "k_neumann"
+        kernel = "k_neumann" if C < 128 else "k_neumann128"
     elif a.path in ("fwdsub", "blockwise"):
         # the exact inverse: tile in, tile out; the arithmetic of substitution
         bytes_ = n_tiles * C * C * es * 2
@@ -279,10 +291,13 @@ def main():
         "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "C": C, "dk": w.dk,
                    "dv": w.dv, "N": N, "S": S, "tiles": n_tiles, "path": a.path,
                    "parallelism": "none (1 GPU)"},
-        "tflops_dense_equiv": round(f_inv / (ev_ms * 1e-3) / 1e12, 2),
-        "tflops_vs_bf16_peak": round(f_inv / (ev_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
-        # the non-zero (lower-triangular) part of the N + S products
+        # the method's own work: the non-zero (lower-triangular) part of the
+        # N + S products, per tile and as a rate of the timed kernel; the
+        # dense-equivalent count (every product a full C x C x C one) beside it
+        "flop_per_tile": {"useful": f_useful // n_tiles, "dense_equiv": f_inv // n_tiles},
         "tflops_useful": round(f_useful / (ev_ms * 1e-3) / 1e12, 2),
+        "tflops_useful_vs_bf16_peak": round(f_useful / (ev_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "tflops_dense_equiv": round(f_inv / (ev_ms * 1e-3) / 1e12, 2),
         "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                      "frac": round(achieved / peak, 4),
                      "traffic": measured_traffic(a.path, w.name, C, N, S, (N0, S0)),
@@ -291,10 +306,15 @@ def main():
                      "algorithmic_bytes": bytes_, "algorithmic_flops": flops},
     }
 
+    if a.path in ("fused", "fused_blockwise") and not a.no_same_shape:
+        out["same_shape_inverse"] = same_shape_inverse(a, G, torch, stream, dA, dT, n_tiles, C, N,
+                                                       S, es, f_useful)
     if low:
         out["tops_int8_dense_equiv"] = round(flops / (ev_ms * 1e-3) / 1e12, 2)
         out["tops_vs_int8_peak"] = round(flops / (ev_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
-        del out["tflops_dense_equiv"], out["tflops_vs_bf16_peak"], out["tflops_useful"]
+        for k in ("flop_per_tile", "tflops_useful", "tflops_useful_vs_bf16_peak",
+                  "tflops_dense_equiv"):
+            del out[k]
         out["config"]["three_launch_ms"] = {"build_A_f32": round(stage_ms[0], 6),
                                             "quantize": round(stage_ms[1], 6),
                                             "inverse_" + sfx: round(stage_ms[2], 6)}
@@ -308,6 +328,26 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, C, N, S, a, (K, beta, g, V), dK, dV, db, dg,
                                              torch, G)
     print(json.dumps(out), flush=True)
+
+
+def same_shape_inverse(a, G, torch, stream, dA, dT, n_tiles, C, N, S, es, f_useful):
+    """The inverse alone on the step's own tiles (A built once in the IO
+    dtype): T_hat(N, S), the exact block-wise inverse and the forward-
+    substitution baseline, each one launch timed with HIP events on the
+    launch stream; tile IO bytes and the useful product work per launch."""
+    steps = max(1, a.steps // 2)
+    res = {}
+    for name, fn in (("neumann", lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT)),
+                     ("blockwise", lambda: G.gdn_chunk_inverse_blockwise(dA, Tinv=dT)),
+                     ("fwdsub", lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT))):
+        ms = _time(fn, steps, stream, torch)
+        gbs = n_tiles * C * C * es * 2 / (ms * 1e-3) / 1e9
+        res[name] = {"ms": round(ms, 6), "chunk_inverses_per_s": round(n_tiles / (ms * 1e-3), 1),
+                     "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    res["neumann"]["tflops_useful"] = round(f_useful / (res["neumann"]["ms"] * 1e-3) / 1e12, 2)
+    res["fwdsub_time_over_neumann"] = round(res["fwdsub"]["ms"] / res["neumann"]["ms"], 3)
+    res["blockwise_time_over_neumann"] = round(res["blockwise"]["ms"] / res["neumann"]["ms"], 3)
+    return res
 
 
 def _time(fn, steps, stream, torch):
@@ -746,6 +786,22 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
         if secs >= a.cpu_seconds:
             break
     tiles = A.shape[1] * A.shape[2] * passes
+    n_sample = A.shape[1] * A.shape[2]
+
+    def rate(fn, seconds):
+        k, t1 = 0, time.perf_counter()
+        while True:
+            fn()
+            k += 1
+            dt_ = time.perf_counter() - t1
+            if dt_ >= seconds:
+                return round(n_sample * k / dt_, 1), k, dt_
+    # the same sample on one host thread, and the exact inverse by forward
+    # substitution (the baseline the paper compares against) on all threads
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1):
+        one_core = rate(one_pass, a.cpu_seconds / 2)
+    fws = rate(lambda: gdn.forward_substitution_inverse(A), a.cpu_seconds / 2)
     # GPU outputs of the same tiles
     W, U, Tg = G.gdn_chunk_wy_fused(dK, dV, db, dg, C, N, S, want_T=True) if C != 128 else (None, None, None)
     err = None
@@ -761,7 +817,23 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
             "sample": f"{len(heads)} heads x {nc} chunks of {w.name} ({tiles // passes} "
                       f"tiles), {passes} passes: build A + T_hat({N},{S}) + W/U in float64 "
                       f"numpy, {secs:.2f} s",
+            "cpu_model": _cpu_model(),
+            "one_core": {"value": one_core[0], "passes": one_core[1],
+                         "seconds": round(one_core[2], 2)},
+            "fwdsub_oracle": {"value": fws[0], "cores": cores, "passes": fws[1],
+                              "seconds": round(fws[2], 2),
+                              "what": "exact inverse by forward substitution on the same A"},
             "max_abs_err_gpu_vs_oracle": err}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return None
 
 
 def error_grid(a, G, torch):
