@@ -37,6 +37,13 @@
  *   n_tiles == 0 (or B == 0) is a no-op returning GDN_OK.
  * Sizes.  C in {16, 32, 64, 128}; L % C == 0; dk, dv in {64, 128};
  *   0 <= N <= C - 1 and 0 <= S <= C - 1 (C = 128: N, S <= 63, see below).
+ *   Every launch is one workgroup per tile (per (head, 16-column slice) in
+ *   the layer forward's state pass) on a 1-D grid, which HIP bounds by
+ *   2^31 - 1 workgroups and 2^32 - 1 work items: a call whose tile count
+ *   times its workgroup size (64; 128 for the two-wave C = 128 kernels of
+ *   the fused path and the integer inverse; 256 for the C = 128 quantiser
+ *   and the state pass) passes 2^32 - 1 returns GDN_ERR_SHAPE before any
+ *   launch (at most 67,108,863 tiles of 64 work items).
  *   A batch with L % C != 0 goes through the packed-sequence entry points
  *   (gdn_chunk_wy_fused_varlen, gdn_chunk_forward_varlen) as B sequences of
  *   L tokens each, the last chunk of each a partial one.
@@ -52,8 +59,16 @@ extern "C" {
 
 /* 2: the integer quantiser and inverses accept C = 128 (three exponents per
  * tile) and the layer forward's `exact` argument takes the integer inverse
- * modes 2 and 3; every call valid under 1 behaves as before. */
-#define GDN_ABI_VERSION 2
+ * modes 2 and 3; every call valid under 1 behaves as before.
+ * 3: the integer inverses follow Algorithm 1's operator order with one
+ * rounding per operator and the no-clip scale rule (different codes from
+ * 2), and gdn_chunk_inverse_neumann_i8 / _i16 take a flags argument. */
+#define GDN_ABI_VERSION 3
+
+/* flags of gdn_chunk_inverse_neumann_i8 / _i16: every tensor of the integer
+ * inverse holds its unit diagonal inside its codes (the plain form) instead
+ * of keeping it exact outside them (the split form, 0). */
+#define GDN_INT_PLAIN 1
 
 enum gdn_dtype { GDN_F32 = 0, GDN_BF16 = 1, GDN_I8 = 2 };
 
@@ -77,8 +92,10 @@ int gdn_abi_version(void);
 const char* gdn_status_string(int status);
 
 /* Default (N, S) per chunk size: 16 -> (3, 2), 32 -> (3, 4) (Section 4.3),
- * 64 -> (3, 8) (Section 4.1), 128 -> (3, 8) per 64-block (Appendix H).
- * Writes *N, *S; GDN_ERR_SHAPE for other C, GDN_ERR_NULL for NULL outputs. */
+ * 64 -> (3, 8) (Section 4.1), 128 -> (3, 8) per 64-block (Appendix H), for
+ * every arithmetic (the paper measures its integer and floating-point
+ * settings at the same orders).  Writes *N, *S; GDN_ERR_SHAPE for other C,
+ * GDN_ERR_NULL for NULL outputs. */
 int gdn_default_order(int C, int* N, int* S);
 
 /* Build the chunk matrices A (Section 2.1 with the Gated DeltaNet gate):
@@ -176,8 +193,10 @@ int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, c
                               int dk, int dv, int C, int N, int S, int exact, int dtype,
                               void* stream);
 
-/* INT8 mode, step 1 (Appendix G quantiser): per tile, e = the smallest
- * integer with max|A| / 2^e <= 127 and Aq = round-half-even(A / 2^e).
+/* INT8 mode, step 1 (Appendix G quantiser with a power-of-two scale): per
+ * tile, Aq = round-half-even(A / 2^e) with e the smallest integer at which
+ * every code lies in [-127, 127] (the finest scale at which the clip of
+ * q(x) = clip(round(x / Delta)) never acts: max|A| < 127.5 2^e).
  * A: fp32 tiles; Aq: int8 tiles (same layout); eA: int32 [n_tiles].  An
  * all-zero tile gets Aq = 0, eA = 0.  Only the strictly lower part of A is
  * read (the rest is taken as 0 and written as 0).  C in {16, 32, 64, 128}.
@@ -189,23 +208,35 @@ int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_til
                           int C, void* stream);
 
 /* INT8 mode, step 2: the approximate inverse of gdn_chunk_inverse_neumann in
- * integer arithmetic (Section 3.5): int8 x int8 MFMA products accumulated
- * exactly in int32 and requantised to int8 after every product with a
- * per-tile power-of-two rescale; the mask is applied to every power before
- * it is quantised; sums align their terms exactly in int32.  Outputs:
- * Tinv = I + Tq * 2^eT, Tq int8 tiles holding the strict lower part (0 on
- * and above the diagonal), eT int32 [n_tiles]; Tdeq (nullable) receives
- * I + Tq * 2^eT in fp32.  C in {16, 32, 64, 128}.  C = 128 runs block-wise
- * (Appendix E, Appendix H) on the codes of gdn_quantize_tiles_i8 at C = 128
+ * integer arithmetic (Algorithm 1 with the integer activations of Section
+ * 3.5 and Appendix G).  Every tensor is codes with one power-of-two scale
+ * per tile; every operator of Algorithm 1 is evaluated exactly from its
+ * operands' codes (int8 x int8 MFMA products exact in int32) and its result
+ * quantised once by the scale rule of gdn_quantize_tiles_i8:
+ *   P_n = q(P_{n-1} Lm), T0 = q(T0 + P_n) (n <= N, P_1 = Lm = -A),
+ *   T0 masked once (codes zeroed, scale kept), E = I - q((I + A) T0),
+ *   P_s = q(P_{s-1} E), T = q(T + P_s) (s <= S, P_1 = E), Tinv = q(T0 T).
+ * flags 0 (split form): the unit diagonal of T0, T and Tinv stays exact
+ * outside the codes: Tinv = I + Tq * 2^eT, Tq the strict lower part (0 on
+ * and above the diagonal).  GDN_INT_PLAIN (C <= 64): the diagonal is part
+ * of every tensor: Tinv = Tq * 2^eT, Tq lower triangular with its diagonal.
+ * eT int32 [n_tiles]; Tdeq (nullable) receives Tinv in fp32.  Sums are
+ * exact (int32 or fp64) whenever a three-term sum spans at most 52 bits,
+ * every tile of the quantiser's output in practice; beyond, a term that
+ * cannot move a code is dropped and any other is rounded to the 52-bit
+ * window.  C in {16, 32, 64, 128}.  C = 128 runs block-wise (Appendix E,
+ * Appendix H) on the codes of gdn_quantize_tiles_i8 at C = 128
  * (eA [n_tiles, 3]): both 64 x 64 diagonal blocks by the integer inverse
- * above (X = I + N per block), and X21 = -X22 A21 X11 as two requantised
- * products, P = A21 + A21 N11, then X21 = -(P + N22 P), each sum formed by
- * the same exact aligned rule; eT [n_tiles, 3] holds the exponents of N11,
- * X21 and N22, so Tinv = I + (each block's codes) * 2^(its exponent), and
- * N, S <= 63.  Requires finite inputs. */
+ * above (X = I + N per block), and X21 = -X22 A21 X11 as two MatMuls,
+ * P = q(A21 + A21 N11), then X21 = -q(P + N22 P); eT [n_tiles, 3] holds the
+ * exponents of N11, X21 and N22, so Tinv = I + (each block's codes) *
+ * 2^(its exponent), and N, S <= 63.  No code ever saturates (the scale rule
+ * leaves the clip inactive), so no saturation count is returned.  Requires
+ * finite inputs.  Other flags: GDN_ERR_PARAM; GDN_INT_PLAIN at C = 128:
+ * GDN_ERR_UNSUPPORTED. */
 int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq,
                                  int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
-                                 int N, int S, void* stream);
+                                 int N, int S, int flags, void* stream);
 
 /* INT8 mode in one launch: A in fp32 from K, beta, g (the values
  * gdn_build_A writes with a_dtype GDN_F32), quantised per tile in registers
@@ -223,8 +254,8 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
 
 /* INT16 mode, step 1: the quantiser of gdn_quantize_tiles_i8 with 16-bit
  * codes (Appendix G lists INT16 activations for the inverse): per tile,
- * e = the smallest integer with max|A| / 2^e <= 32639 and
- * Aq = round-half-even(A / 2^e).  A: fp32 tiles; Aq: int16 tiles (same
+ * Aq = round-half-even(A / 2^e) with e the smallest integer at which every
+ * code lies in [-32639, 32639].  A: fp32 tiles; Aq: int16 tiles (same
  * layout); eA: int32 [n_tiles].  An all-zero tile gets Aq = 0, eA = 0.  Only
  * the strictly lower part of A is read (the rest is taken as 0 and written
  * as 0).  C = 128: block-wise with eA [n_tiles, 3], as for
@@ -233,29 +264,28 @@ int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_t
                            int C, void* stream);
 
 /* INT16 mode, step 2: the integer inverse of gdn_chunk_inverse_neumann_i8
- * with 16-bit codes (Section 3.5): codes in [-32639, 32639], every product
- * exact (each code split into two int8 limbs, four int8 MFMAs per product,
- * recombined exactly in fp64) and requantised to 16 bits after every
- * product with a per-tile power-of-two rescale; sums align their terms
- * exactly below 2^31 (16 guard bits under a code's quantum).  Outputs:
- * Tinv = I + Tq * 2^eT, Tq int16 tiles holding the strict lower part (0 on
- * and above the diagonal), eT int32 [n_tiles]; Tdeq (nullable) receives
- * I + Tq * 2^eT in fp32.  Aq codes must lie in [-32639, 32639], the range
- * the quantiser writes (a negated code must split into two int8 limbs);
- * a tile holding -32768 gets unspecified codes.  C in {16, 32, 64, 128};
- * C = 128 block-wise with eA, eT [n_tiles, 3], as for
- * gdn_chunk_inverse_neumann_i8. */
+ * with 16-bit codes (Section 3.5): codes in [-32639, 32639] (32639 =
+ * 127 * 256 + 127), every product exact (each code split into two int8
+ * limbs, four int8 MFMAs per product, recombined exactly in fp64), every
+ * operator's result quantised once to 16 bits by the scale rule of
+ * gdn_quantize_tiles_i16; order, forms (flags), outputs and the exactness
+ * statement as gdn_chunk_inverse_neumann_i8, with int16 Tq.  Aq codes must
+ * lie in [-32639, 32639], the range the quantiser writes (a negated code
+ * must split into two int8 limbs); a tile holding -32768 gets unspecified
+ * codes.  C in {16, 32, 64, 128}; C = 128 block-wise with eA, eT
+ * [n_tiles, 3], as for gdn_chunk_inverse_neumann_i8. */
 int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
                                   int32_t* eT, float* Tdeq, int64_t n_tiles, int C,
-                                  int N, int S, void* stream);
+                                  int N, int S, int flags, void* stream);
 
 /* The forward-substitution baseline in INT16 (the integer counterpart of
  * gdn_chunk_inverse_fwdsub, beside the integer Neumann inverse): Section
  * 2.2's recurrence x_ij = -a_ij - sum_{j<k<i} a_ik x_kj run row by row on
  * 16-bit codes with one power-of-two exponent per tile (the per-tensor
- * scheme of Appendix G).  Row i is the exact sum of -a_i (codes at eA) and
- * -a_i X (products at eA + eT), aligned as in
- * gdn_chunk_inverse_neumann_i16; the tile exponent eT starts at eA and
+ * scheme of Appendix G).  Row i is the sum of -a_i (codes at eA) and
+ * -a_i X (exact products at eA + eT), aligned 16 guard bits under a code's
+ * quantum (finer product terms rounded half-even to that grid); the tile
+ * exponent eT starts at eA and
  * grows by the smallest shift that fits a new row (earlier rows rounded
  * half-even to it); the row's codes are one half-even rounding of its sum.
  * Aq, eA as for gdn_chunk_inverse_neumann_i16 (codes in [-32639, 32639]);

@@ -14,6 +14,7 @@ from ._binding import (  # noqa: F401
     GDN_BF16,
     GDN_F32,
     GDN_I8,
+    GDN_INT_PLAIN,
     GdnError,
     LIB_PATH,
     abi_symbols,

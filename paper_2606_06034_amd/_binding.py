@@ -11,6 +11,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgdninv.so")
 
 GDN_F32, GDN_BF16, GDN_I8 = 0, 1, 2
+GDN_INT_PLAIN = 1  # integer inverses: the unit diagonal inside the codes
 
 _c_int, _c_i64, _vp = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
 
@@ -30,12 +31,13 @@ _SIGS = {
     "gdn_chunk_wy_fused_blockwise": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
                                      _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_quantize_tiles_i8": [_vp, _vp, _vp, _c_i64, _c_int, _vp],
-    "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int, _vp],
+    "gdn_chunk_inverse_neumann_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
+                                     _c_int, _vp],
     "gdn_chunk_inverse_neumann_i8_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
                                            _c_int, _c_int, _c_int, _c_int, _c_int, _vp],
     "gdn_quantize_tiles_i16": [_vp, _vp, _vp, _c_i64, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i16": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int, _c_int,
-                                      _vp],
+                                      _c_int, _vp],
     "gdn_chunk_inverse_fwdsub_i16": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _vp],
     "gdn_chunk_inverse_fwdsub_i8": [_vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _vp],
     "gdn_chunk_inverse_neumann_i16_fused": [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
@@ -277,10 +279,12 @@ def gdn_quantize_tiles_i8(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
 
 
 def gdn_chunk_inverse_neumann_i8(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: int,
-                                 want_deq: bool = False, Tq: Optional[torch.Tensor] = None,
+                                 want_deq: bool = False, plain: bool = False,
+                                 Tq: Optional[torch.Tensor] = None,
                                  eT: Optional[torch.Tensor] = None,
                                  Tdeq: Optional[torch.Tensor] = None, stream=None):
-    """(Tq int8, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT; C = 128:
+    """(Tq int8, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT (plain:
+    T_hat = Tq * 2^eT, the diagonal in the codes; GDN_INT_PLAIN); C = 128:
     block-wise, eA and eT [n, 3] (blocks 11, 21, 22)."""
     n, C = _tiles(Aq)
     Tq = torch.empty_like(Aq) if Tq is None else Tq
@@ -293,7 +297,7 @@ def gdn_chunk_inverse_neumann_i8(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: 
         _dev(Aq, "Aq", torch.int8), _dev(eA, "eA", torch.int32, n * ne),
         _dev(Tq, "Tq", torch.int8, Aq.numel()), _dev(eT, "eT", torch.int32, n * ne),
         _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
-        _stream(stream)))
+        GDN_INT_PLAIN if plain else 0, _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)
 
 
@@ -340,10 +344,12 @@ def gdn_quantize_tiles_i16(A: torch.Tensor, Aq: Optional[torch.Tensor] = None,
 
 
 def gdn_chunk_inverse_neumann_i16(Aq: torch.Tensor, eA: torch.Tensor, N: int, S: int,
-                                  want_deq: bool = False, Tq: Optional[torch.Tensor] = None,
+                                  want_deq: bool = False, plain: bool = False,
+                                  Tq: Optional[torch.Tensor] = None,
                                   eT: Optional[torch.Tensor] = None,
                                   Tdeq: Optional[torch.Tensor] = None, stream=None):
-    """(Tq int16, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT; C = 128:
+    """(Tq int16, eT int32[, Tdeq fp32]) with T_hat = I + Tq * 2^eT (plain:
+    T_hat = Tq * 2^eT, the diagonal in the codes; GDN_INT_PLAIN); C = 128:
     block-wise, eA and eT [n, 3] (blocks 11, 21, 22)."""
     n, C = _tiles(Aq)
     Tq = torch.empty_like(Aq) if Tq is None else Tq
@@ -356,7 +362,7 @@ def gdn_chunk_inverse_neumann_i16(Aq: torch.Tensor, eA: torch.Tensor, N: int, S:
         _dev(Aq, "Aq", torch.int16), _dev(eA, "eA", torch.int32, n * ne),
         _dev(Tq, "Tq", torch.int16, Aq.numel()), _dev(eT, "eT", torch.int32, n * ne),
         _dev(Td, "Tdeq", torch.float32, Aq.numel()) if Td is not None else None, n, C, N, S,
-        _stream(stream)))
+        GDN_INT_PLAIN if plain else 0, _stream(stream)))
     return (Tq, eT, Td) if Td is not None else (Tq, eT)
 
 

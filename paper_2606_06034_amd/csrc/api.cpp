@@ -9,7 +9,15 @@
 
 namespace {
 
-constexpr int64_t kMaxTiles = 0x7fffffff;  // one workgroup per tile, 1-D grid
+// A 1-D launch of n workgroups of `block` work items fits HIP's grid when
+// n <= 2^31 - 1 and n * block <= 2^32 - 1.  Every launch here is one
+// workgroup per tile (or per (head, slice) of the state pass), of 64 work
+// items, 128 for the two-wave C = 128 kernels (fused path and integer
+// inverse) and 256 for the C = 128 quantiser and the state pass.
+bool grid_ok(int64_t n, int block) {
+  return n >= 0 && n <= 0x7fffffffLL && n * block <= 0xffffffffLL;
+}
+int two_wave(int C) { return C == 128 ? 128 : 64; }
 
 bool valid_C(int C) { return C == 16 || C == 32 || C == 64 || C == 128; }
 bool valid_d(int d) { return d == 64 || d == 128; }
@@ -54,11 +62,12 @@ int hip_status(hipError_t e) {
   return GDN_ERR_HIP;
 }
 
-// common checks of the [B, L, H, d] entry points; fills the tile count
-int check_chunked(int B, int L, int H, int C, int64_t* n_tiles) {
+// common checks of the [B, L, H, d] entry points (one workgroup of `block`
+// work items per tile); fills the tile count
+int check_chunked(int B, int L, int H, int C, int64_t* n_tiles, int block) {
   if (B < 0 || L < 0 || H < 0 || !valid_C(C) || L % C != 0) return GDN_ERR_SHAPE;
   const int64_t n = (int64_t)B * H * (L / C);
-  if (n > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!grid_ok(n, block)) return GDN_ERR_SHAPE;
   *n_tiles = n;
   return GDN_OK;
 }
@@ -99,7 +108,7 @@ int gdn_default_order(int C, int* N, int* S) {
 int gdn_build_A(const void* K, const float* beta, const float* g, void* A, int B, int L, int H,
                 int dk, int C, int k_dtype, int a_dtype, void* stream) {
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, 64)) return r;
   if (!valid_d(dk)) return GDN_ERR_SHAPE;
   if (!fdtype(k_dtype) || !fdtype(a_dtype)) return GDN_ERR_DTYPE;
   if (n == 0) return GDN_OK;
@@ -116,7 +125,7 @@ int gdn_build_A(const void* K, const float* beta, const float* g, void* A, int B
 
 int gdn_chunk_inverse_neumann(const void* A, void* Tinv, int64_t n_tiles, int C, int N, int S,
                               int dtype, void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!valid_C(C) || !grid_ok(n_tiles, 64)) return GDN_ERR_SHAPE;
   if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (n_tiles == 0) return GDN_OK;
@@ -129,7 +138,7 @@ int gdn_chunk_inverse_neumann(const void* A, void* Tinv, int64_t n_tiles, int C,
 
 int gdn_chunk_inverse_fwdsub(const void* A, void* Tinv, int64_t n_tiles, int C, int dtype,
                              void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!valid_C(C) || !grid_ok(n_tiles, 64)) return GDN_ERR_SHAPE;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (n_tiles == 0) return GDN_OK;
   if (!A || !Tinv) return GDN_ERR_NULL;
@@ -141,7 +150,7 @@ int gdn_chunk_inverse_fwdsub(const void* A, void* Tinv, int64_t n_tiles, int C, 
 
 int gdn_chunk_inverse_blockwise(const void* A, void* Tinv, int64_t n_tiles, int C, int dtype,
                                 void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!valid_C(C) || !grid_ok(n_tiles, 64)) return GDN_ERR_SHAPE;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (n_tiles == 0) return GDN_OK;
   if (!A || !Tinv) return GDN_ERR_NULL;
@@ -154,7 +163,7 @@ int gdn_chunk_inverse_blockwise(const void* A, void* Tinv, int64_t n_tiles, int 
 int gdn_wy_apply(const void* Tinv, const void* K, const void* V, const float* beta, void* W,
                  void* U, int B, int L, int H, int dk, int dv, int C, int dtype, void* stream) {
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, 64)) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (n == 0) return GDN_OK;
@@ -178,7 +187,7 @@ int wy_fused(const void* K, const void* V, const float* beta, const float* g, vo
              void* Tinv, int B, int L, int H, int dk, int dv, int C, int N, int S, int dtype,
              bool exact, void* stream) {
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, two_wave(C))) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
@@ -222,7 +231,7 @@ int gdn_chunk_wy_fused_varlen(const void* K, const void* V, const float* beta, c
   if (T < 0 || H < 0 || nseq < 0 || n_chunks < 0) return GDN_ERR_SHAPE;
   if (!valid_C(C) || !valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (nseq == 0 && n_chunks != 0) return GDN_ERR_SHAPE;
-  if (n_chunks > T || (int64_t)n_chunks * H > kMaxTiles) return GDN_ERR_SHAPE;
+  if (n_chunks > T || !grid_ok((int64_t)n_chunks * H, two_wave(C))) return GDN_ERR_SHAPE;
   if (exact != 0 && exact != 1) return GDN_ERR_PARAM;
   if (!exact && !order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
@@ -257,8 +266,8 @@ int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const 
   if (T < 0 || H < 0 || nseq < 0 || n_chunks < 0) return GDN_ERR_SHAPE;
   if (!valid_C(C) || !valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (nseq == 0 && n_chunks != 0) return GDN_ERR_SHAPE;
-  if (n_chunks > T || (int64_t)n_chunks * H > kMaxTiles) return GDN_ERR_SHAPE;
-  if ((int64_t)nseq * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
+  if (n_chunks > T || !grid_ok((int64_t)n_chunks * H, 64)) return GDN_ERR_SHAPE;
+  if (!grid_ok((int64_t)nseq * H * (dv / 16), 256)) return GDN_ERR_SHAPE;
   if (int r = forward_mode_check(exact, C, N, S, dk, dv, true)) return r;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (C == 128) return GDN_ERR_UNSUPPORTED;
@@ -301,7 +310,7 @@ int gdn_chunk_forward_varlen(const void* Q, const void* K, const void* V, const 
 
 int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                           void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || !grid_ok(n_tiles, C == 128 ? 256 : 64))
     return GDN_ERR_SHAPE;
   if (n_tiles == 0) return GDN_OK;
   if (!A || !Aq || !eA) return GDN_ERR_NULL;
@@ -313,11 +322,12 @@ int gdn_quantize_tiles_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_til
 }
 
 int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
-                                 float* Tdeq, int64_t n_tiles, int C, int N, int S,
+                                 float* Tdeq, int64_t n_tiles, int C, int N, int S, int flags,
                                  void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || !grid_ok(n_tiles, two_wave(C)))
     return GDN_ERR_SHAPE;
-  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!order_ok(C, N, S) || (flags & ~GDN_INT_PLAIN)) return GDN_ERR_PARAM;
+  if ((flags & GDN_INT_PLAIN) && C == 128) return GDN_ERR_UNSUPPORTED;
   if (n_tiles == 0) return GDN_OK;
   if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
   if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
@@ -332,14 +342,15 @@ int gdn_chunk_inverse_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq
   if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
     return GDN_ERR_ALIAS;
   return hip_status(
-      gdn::launch_neumann_i8(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, (hipStream_t)stream));
+      gdn::launch_neumann_i8(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, (flags & GDN_INT_PLAIN) != 0,
+                             (hipStream_t)stream));
 }
 
 int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const float* g,
                                        int8_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                        int dk, int C, int N, int S, int k_dtype, void* stream) {
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, two_wave(C))) return r;
   if (!valid_d(dk)) return GDN_ERR_SHAPE;
   if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(k_dtype)) return GDN_ERR_DTYPE;
@@ -364,7 +375,7 @@ int gdn_chunk_inverse_neumann_i8_fused(const void* K, const float* beta, const f
 
 int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                            void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!valid_C(C) || !grid_ok(n_tiles, C == 128 ? 256 : 64))
     return GDN_ERR_SHAPE;
   if (n_tiles == 0) return GDN_OK;
   if (!A || !Aq || !eA) return GDN_ERR_NULL;
@@ -377,10 +388,11 @@ int gdn_quantize_tiles_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_t
 
 int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq,
                                   int32_t* eT, float* Tdeq, int64_t n_tiles, int C, int N, int S,
-                                  void* stream) {
-  if (!valid_C(C) || n_tiles < 0 || n_tiles > kMaxTiles)
+                                  int flags, void* stream) {
+  if (!valid_C(C) || !grid_ok(n_tiles, two_wave(C)))
     return GDN_ERR_SHAPE;
-  if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
+  if (!order_ok(C, N, S) || (flags & ~GDN_INT_PLAIN)) return GDN_ERR_PARAM;
+  if ((flags & GDN_INT_PLAIN) && C == 128) return GDN_ERR_UNSUPPORTED;
   if (n_tiles == 0) return GDN_OK;
   if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
   if (!aligned(Aq) || !aligned(eA) || !aligned(Tq) || !aligned(eT) || (Tdeq && !aligned(Tdeq)))
@@ -395,12 +407,13 @@ int gdn_chunk_inverse_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t*
   if (overlap(Tq, qb, eT, eb) || overlap(Tq, qb, Tdeq, db) || overlap(eT, eb, Tdeq, db))
     return GDN_ERR_ALIAS;
   return hip_status(
-      gdn::launch_neumann_i16(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, (hipStream_t)stream));
+      gdn::launch_neumann_i16(Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S,
+                              (flags & GDN_INT_PLAIN) != 0, (hipStream_t)stream));
 }
 
 int gdn_chunk_inverse_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
                                  float* Tdeq, int64_t n_tiles, int C, void* stream) {
-  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!(C == 16 || C == 32 || C == 64) || !grid_ok(n_tiles, 64))
     return GDN_ERR_SHAPE;
   if (n_tiles == 0) return GDN_OK;
   if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
@@ -421,7 +434,7 @@ int gdn_chunk_inverse_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* 
 
 int gdn_chunk_inverse_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
                                 float* Tdeq, int64_t n_tiles, int C, void* stream) {
-  if (!(C == 16 || C == 32 || C == 64) || n_tiles < 0 || n_tiles > kMaxTiles)
+  if (!(C == 16 || C == 32 || C == 64) || !grid_ok(n_tiles, 64))
     return GDN_ERR_SHAPE;
   if (n_tiles == 0) return GDN_OK;
   if (!Aq || !eA || !Tq || !eT) return GDN_ERR_NULL;
@@ -444,7 +457,7 @@ int gdn_chunk_inverse_neumann_i16_fused(const void* K, const float* beta, const 
                                         int H, int dk, int C, int N, int S, int k_dtype,
                                         void* stream) {
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, two_wave(C))) return r;
   if (!valid_d(dk)) return GDN_ERR_SHAPE;
   if (!order_ok(C, N, S)) return GDN_ERR_PARAM;
   if (!fdtype(k_dtype)) return GDN_ERR_DTYPE;
@@ -471,7 +484,7 @@ int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int 
                                 int64_t* bytes) {
   if (!bytes) return GDN_ERR_NULL;
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, 64)) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (C == 128) return GDN_ERR_UNSUPPORTED;
@@ -486,12 +499,12 @@ int forward(const void* Q, const void* K, const void* V, const float* beta, cons
             int B, int L, int H, int dk, int dv, int C, int N, int S, int exact, float scale,
             int dtype, int phases, void* stream) {
   int64_t n = 0;
-  if (int r = check_chunked(B, L, H, C, &n)) return r;
+  if (int r = check_chunked(B, L, H, C, &n, 64)) return r;
   if (!valid_d(dk) || !valid_d(dv)) return GDN_ERR_SHAPE;
   if (int r = forward_mode_check(exact, C, N, S, dk, dv, phases & 1)) return r;
   if (!fdtype(dtype)) return GDN_ERR_DTYPE;
   if (C == 128) return GDN_ERR_UNSUPPORTED;
-  if ((int64_t)B * H * (dv / 16) > kMaxTiles) return GDN_ERR_SHAPE;
+  if (!grid_ok((int64_t)B * H * (dv / 16), 256)) return GDN_ERR_SHAPE;
   if ((int64_t)B * H == 0) return GDN_OK;
   const bool prep = phases & 1, state = phases & 2;
   const int64_t es = esize(dtype), tok = (int64_t)B * L * H;

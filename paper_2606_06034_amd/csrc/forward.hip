@@ -214,9 +214,9 @@ __device__ __forceinline__ void chunk_inverse_int(const Pair<F> (&kp)[NB][DK / 3
   iq::AccI<NB> Ti;
   int eT;
   if constexpr (INV == kInvInt16)
-    iq::int_engine<i16::I16Ops, NB, NC, SC>(Lr, e, N, S, Ti, eT);
+    iq::int_engine<i16::I16Ops, NB, false, NC, SC>(Lr, e, N, S, Ti, eT);
   else
-    iq::int_engine<i8::I8Ops, NB, NC, SC>(Lr, e, N, S, Ti, eT);
+    iq::int_engine<i8::I8Ops, NB, false, NC, SC>(Lr, e, N, S, Ti, eT);
 #pragma unroll
   for (int b = 0; b < nlower(NB); ++b)
 #pragma unroll

@@ -8,13 +8,12 @@
 //
 // Inverse, two waves per tile: wave w inverts diagonal block w with the
 // one-tile engine (int_engine, X_ww = I + N_ww), then the off-diagonal block
-// is formed from the right,
+// is formed from the right by two MatMuls,
 //   P = A21 X11 = A21 + A21 N11,      X21 = -(X22 P) = -(P + N22 P),
-// each an exact product added to its code term by the engine's running-sum
-// rules (code term first; a product is present when both factors are
-// non-zero) and requantised; each wave forms two of the four 16-column
+// each the exact sum of its code term and its exact product, quantised once
+// by the scale rule (intq.hpp); each wave forms two of the four 16-column
 // block columns of P and X21, the diagonal blocks and the maxima of the
-// requantisations passing through LDS.
+// quantisations passing through LDS.
 //
 // W (one code width) supplies: Code (the storage type), load4 / store4 (four
 // consecutive codes <-> i32x4), qexp (the quantiser's exponent of a block
@@ -22,9 +21,9 @@
 // Col, to_row, to_col (the engine's fragments of lower matrices), to_frow
 // (row-form fragments of a full matrix), frow_to_col (row-form fragments to
 // column-form ones, exact), FProd and fmm<OUTQ, J0, JN> (an exact product
-// over the output block columns J0 .. J0 + JN - 1) and sum2<J0, JN> (code
-// term + product term over those block columns, summed and requantised to
-// codes with a maximum joined across the waves by a given reduction).
+// over the output block columns J0 .. J0 + JN - 1) and codes (the codes of
+// one block of row-form fragments), besides the engine width's kQ, kQB and
+// kAccB.
 #pragma once
 
 #include "chunk.hpp"
@@ -72,7 +71,8 @@ struct Lds128 {
   short n11t[64 * kLD];  // n11t[j * kLD + i] = N11[i][j]
   short n22[64 * kLD];
   short a21[64 * kLD];
-  int info[12];  // e11, nz11, ea, e22, nz22, -, max P (2 waves), -, max X21 (2 waves)
+  int info[20];  // e11, nz11, ea, e22, nz22, -, max P (2 waves), -, max X21 (2 waves), -,
+                 // magnitudes of P's terms (2 x 2 waves), of X21's terms (2 x 2 waves)
 };
 
 // Wave 0 parks the codes of A21 (row form, all 16 blocks) and their
@@ -85,6 +85,88 @@ __device__ __forceinline__ void stash_a21(const FullI& A, int ea, Lds128& sh) {
 #pragma unroll
     for (int J = 0; J < 4; ++J) lds_put4(&sh.a21[(16 * I + c) * kLD + 16 * J + 4 * g], A.a[4 * I + J]);
   if (lane_id() == 0) sh.info[2] = ea;
+}
+
+// The block columns J0 .. J0 + JN - 1 of out = q(t1 2^e1 + t2 2^e2): t1
+// the codes of the row-form fragments X, t2 the exact product D.  The sum
+// is exact in fp64 (both terms aligned at the finer exponent) under the
+// exponent plan of sum_plan (intq.hpp); the terms' actual magnitudes are
+// measured only when their bounds span more than 52 bits.  Every maximum is
+// joined with the other wave's by join(m, slot) (slot s0 for the sum, s1,
+// s2 for the terms' magnitudes), and the sum is quantised once by the
+// scale rule.  The other block columns of out are set to 0.
+template <typename W, int J0, int JN, typename Join>
+__device__ __forceinline__ void sum2_full(FullI& out, int& eo, bool& nz, const typename W::Row& X,
+                                          int e1, bool p1, const typename W::FProd& D, int e2,
+                                          bool p2, Join&& join, int s0, int s1, int s2) {
+  constexpr int Q = W::kQ, QB = W::kQB, ACCB = W::kAccB;
+  int e[3] = {e1, e2, 0}, b[3] = {QB, ACCB, 0};
+  bool p[3] = {p1, p2, false};
+  if (p1 && p2 && max(e1 + QB, e2 + ACCB) - min(e1, e2) > 52) {
+    int m1 = 0, m2 = 0;
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int K = J0; K < J0 + JN; ++K) {
+        const i32x4 c1 = W::codes(X, I, K);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          m1 = max(m1, __double2hiint(fabs((double)c1[v])));
+          m2 = max(m2, __double2hiint(fabs(elem(D.a[4 * I + K], v))));
+        }
+      }
+    m1 = join(wave_max(m1), s1);
+    m2 = join(wave_max(m2), s2);
+    int q1 = 0, q2 = 0;
+    if (m1) frexp(__hiloint2double(m1, 0), &q1);
+    if (m2) frexp(__hiloint2double(m2, 0), &q2);
+    b[0] = q1;
+    b[1] = q2;
+    p[0] = m1 > 0;
+    p[1] = m2 > 0;
+  }
+  const SumPlan pl = (p[0] || p[1]) ? sum_plan<QB>(e, b, p) : SumPlan{0, {false, false, false},
+                                                                        {false, false, false}};
+  const double sa = pl.p[0] ? ldexp(1.0, e1 - pl.emin) : 0.0;
+  const double sb = pl.p[1] ? ldexp(1.0, e2 - pl.emin) : 0.0;
+  auto val = [&](int I, int K, int v, i32x4 c1) {
+    double x = 0.0;
+    if (pl.p[0]) {
+      const double t = (double)c1[v] * sa;
+      x += pl.r[0] ? rint(t) : t;
+    }
+    if (pl.p[1]) {
+      const double t = elem(D.a[4 * I + K], v) * sb;
+      x += pl.r[1] ? rint(t) : t;
+    }
+    return x;
+  };
+  int mh = 0;
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int K = J0; K < J0 + JN; ++K) {
+      const i32x4 c1 = W::codes(X, I, K);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) mh = max(mh, __double2hiint(fabs(val(I, K, v, c1))));
+    }
+  const int amax_hi = join(wave_max(mh), s0);
+  nz = amax_hi > 0;
+  const int s = nz ? shift_canon_hi<Q, QB>(amax_hi) : 0;
+  const double sc = ldexp(1.0, -s);
+#pragma unroll
+  for (int I = 0; I < 4; ++I)
+#pragma unroll
+    for (int K = 0; K < 4; ++K) {
+      i32x4 r = zero_i4();
+      if (nz && K >= J0 && K < J0 + JN) {
+        const i32x4 c1 = W::codes(X, I, K);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) r[v] = rne_scaled(val(I, K, v, c1), sc);
+      }
+      out.a[4 * I + K] = r;
+    }
+  eo = nz ? pl.emin + s : 0;
 }
 
 // Wave w's half of X21 = -(X22 (A21 X11)): the output block columns
@@ -130,15 +212,14 @@ __device__ __forceinline__ void merge_half(const AccI<4>& Tr, int eTo, bool nzT,
     for (int J = 0; J < 4; ++J) A21.a[4 * I + J] = lds_get4(&sh.a21[(16 * I + c) * LD + 16 * J + 4 * g]);
   const bool nzA = amax_full(A21) > 0;
 
-  typename W::Row X;  // A21, then P, as row-form fragments (sum2 reads the codes back)
+  typename W::Row X;  // A21, then P, as row-form fragments (sum2_full reads the codes back)
   typename W::FProd D;
   W::to_frow(X, A21);
   W::template fmm<true, J0, 2>(D, X, N11q);  // A21 N11, row form, own columns
   FullI P;
   int eP;
   bool nzP;
-  W::template sum2<J0, 2>(P, eP, nzP, X, ea, nzA, D, ea + e11, nzA && nz11,
-                          [&](int m) { return xmax(m, 6); });
+  sum2_full<W, J0, 2>(P, eP, nzP, X, ea, nzA, D, ea + e11, nzA && nz11, xmax, 6, 12, 14);
 
   RowQ<4> Iq;
   ColQ<4> Ic;
@@ -161,8 +242,7 @@ __device__ __forceinline__ void merge_half(const AccI<4>& Tr, int eTo, bool nzT,
   FullI Xs;
   int e21;
   bool nz21;
-  W::template sum2<J0, 2>(Xs, e21, nz21, X, eP, nzP, D, e22 + eP, nz22 && nzP,
-                          [&](int m) { return xmax(m, 9); });
+  sum2_full<W, J0, 2>(Xs, e21, nz21, X, eP, nzP, D, e22 + eP, nz22 && nzP, xmax, 9, 16, 18);
 
 #pragma unroll
   for (int I = 0; I < 4; ++I)
@@ -397,8 +477,8 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
 // Quantiser at C = 128: four waves per tile, wave w on the 64 x 64 quadrant
 // (w >> 1, w & 1).  The strict lower parts of the diagonal blocks and the
 // whole block 21 each get their own exponent (the per-tile rule applied to
-// the block: the smallest e with max|x| / 2^e <= qmax, codes
-// round-half-even(x / 2^e)); block 12 is written as 0.  eA[3 tile + k] for
+// the block: codes round-half-even(x / 2^e), e the smallest integer at which
+// they lie in [-qmax, qmax]); block 12 is written as 0.  eA[3 tile + k] for
 // the blocks k = 0 (11), 1 (21), 2 (22).
 template <typename W>
 __global__ __launch_bounds__(256) void k_quantize_int128(const float* __restrict__ A,

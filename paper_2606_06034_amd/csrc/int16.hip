@@ -1,19 +1,15 @@
 // int16.hip -- the INT16 path: per-tile quantiser and the integer
-// masked-Neumann + residual inverse with 16-bit codes (Section 3.5,
-// Appendix G of arXiv 2606.06034: INT16 activations for the inverse), one
-// wave per tile.
+// masked-Neumann + residual inverse with 16-bit codes (Algorithm 1 with the
+// INT16 activations of Section 3.5 and Appendix G of arXiv 2606.06034), one
+// wave per tile; and the forward-substitution baseline on integer codes.
 //
-// Arithmetic: the integer recipe of the INT8 path with 16-bit codes:
+// Arithmetic: the integer reading of the INT8 path with 16-bit codes:
 //   * codes q in [-32639, 32639], one exponent per tile (value q 2^e);
-//   * quantiser: e = smallest integer with max|x| / 2^e <= 32639,
-//     q = round-half-even(x / 2^e);
-//   * products exact, requantised with the smallest round-half-even shift
-//     that brings max|acc| to <= 32639 (exponents add);
-//   * running sums exact in production order: the first present term sets the
-//     exponent 16 guard bits below its quantum (terms aligned below 2^31), a
-//     later term above that range rebases the sum (round-half-even), finer
-//     terms are rounded in;
-//   * the mask, E, the residual chain and T exactly as in the INT8 path.
+//   * the scale rule: q = round-half-even(v / 2^e) with e the smallest
+//     integer at which no code leaves [-32639, 32639];
+//   * every operator evaluated exactly from its operands' codes and its
+//     result quantised once; the order, the mask and the forms as in the
+//     INT8 path.
 //
 // gfx950 has no 16-bit integer MFMA.  32639 = 127 * 256 + 127, so every code
 // splits into two int8 limbs q = 256 h + l (l in [-128, 127], h in
@@ -21,10 +17,8 @@
 // fragments of intq.hpp (quads per limb, packed straight from the codes):
 //   X Y = 2^16 Xh Yh + 2^8 (Xh Yl + Xl Yh) + Xl Yl,
 // with 2^8 Xh Yh + (Xh Yl + Xl Yh) exact in int32 (|.| < 2^29) and the sum
-// exact in fp64 (|X Y| < C 2^30 <= 2^36).  Products and running sums are
-// held as fp64 integers (exact below 2^53), codes as int32.  Rounding a
-// fp64 integer by 2^s is rint(ldexp(x, -s)): the scaling is exact and rint
-// rounds half to even.
+// exact in fp64 (|X Y| < C 2^30 <= 2^36).  Products and sums are held as
+// fp64 integers (exact below 2^53), codes as int32.
 #include "chunk.hpp"
 #include "int128.hpp"
 #include "intq.hpp"
@@ -45,9 +39,10 @@ __device__ __forceinline__ i32x4 unpack4_16(int2 w) {
   return i32x4{(int)(int16_t)(w.x & 0xffff), w.x >> 16, (int)(int16_t)(w.y & 0xffff), w.y >> 16};
 }
 
-// Tq (codes, zero on and above the diagonal), eT and optionally
-// Tdeq = I + Tq 2^eT for tile `tile`
-template <int NB>
+// Tq (codes, zero above the diagonal and, in split form, on it), eT and
+// optionally Tdeq = T_hat in fp32 (I + Tq 2^eT in split form, Tq 2^eT in
+// plain form) for tile `tile`
+template <int NB, bool PLAIN = false>
 __device__ __forceinline__ void store_i16(const AccI<NB>& Tr, int eTo, int16_t* __restrict__ Tq,
                                           int32_t* __restrict__ eT, float* __restrict__ Tdeq,
                                           int64_t tile) {
@@ -71,15 +66,15 @@ __device__ __forceinline__ void store_i16(const AccI<NB>& Tr, int eTo, int16_t* 
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int d = 16 * (I - J) + c - 4 * g - v;
-          if (J <= I && d > 0) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], eTo);
-          if (d == 0) x[v] = 1.f;
+          if (J <= I && d >= (PLAIN ? 0 : 1)) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], eTo);
+          if (!PLAIN && d == 0) x[v] = 1.f;
         }
         *(f32x4*)(td + (I * 16 + c) * C + J * 16 + 4 * g) = x;
       }
   }
 }
 
-template <int NB, int NC = -1, int SC = -1>
+template <int NB, bool PLAIN, int NC = -1, int SC = -1>
 __global__ __launch_bounds__(64) void k_neumann_i16(const int16_t* __restrict__ Aq,
                                                     const int32_t* __restrict__ eA,
                                                     int16_t* __restrict__ Tq,
@@ -103,8 +98,8 @@ __global__ __launch_bounds__(64) void k_neumann_i16(const int16_t* __restrict__ 
   const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
   AccI<NB> Tr;
   int eTo;
-  int_engine<I16Ops, NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
-  store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, tile);
+  int_engine<I16Ops, NB, PLAIN, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+  store_i16<NB, PLAIN>(Tr, eTo, Tq, eT, Tdeq, tile);
 }
 
 
@@ -138,7 +133,7 @@ __global__ __launch_bounds__(64) void k_inverse_i16_fused(const TK* __restrict__
     for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
   AccI<NB> Tr;
   int eTo;
-  int_engine<I16Ops, NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
+  int_engine<I16Ops, NB, false, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
   store_i16<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
 }
 
@@ -200,7 +195,7 @@ struct I16W : I16Ops<4> {
   template <int NC, int SC>
   static __device__ __forceinline__ void engine(const AccI<4>& Lr, int eL, int N, int S,
                                                 AccI<4>& Tr, int& eTo) {
-    int_engine<I16Ops, 4, NC, SC>(Lr, eL, N, S, Tr, eTo);
+    int_engine<I16Ops, 4, false, NC, SC>(Lr, eL, N, S, Tr, eTo);
   }
   static __device__ __forceinline__ void to_frow(Row& X, const FullI& D) { to_rowl_full(X, D); }
   // limb by limb through the identity (exact)
@@ -219,73 +214,10 @@ struct I16W : I16Ops<4> {
   static __device__ __forceinline__ i32x4 codes(const Row& X, int I, int K) {
     return unpack4(X.h.r[I].v[K]) * 256 + unpack4(X.l.r[I].v[K]);
   }
-  // The running sum of two terms over the block columns J0 .. J0 + JN - 1,
-  // requantised: the codes of the fragments t1 (exponent e1), then the exact
-  // product t2 (exponent e2), by the engine's rules (the first present term
-  // 16 guard bits under its quantum, a larger later term rebases the sum, a
-  // finer one is rounded in).  The exponent plan is wave-uniform, so the sum
-  // is one pass per entry, in place in t2.  red(m) joins this wave's maximum
-  // (of the high dwords) with the other blocks'.  The other block columns of
-  // out are set to 0.
-  template <int J0, int JN, typename Red>
-  static __device__ __forceinline__ void sum2(FullI& out, int& eo, bool& nz, const Row& t1,
-                                              int e1, bool p1, FullD& t2, int e2, bool p2,
-                                              Red&& red) {
-    int e = 0, sh = 0;
-    bool any = false, reb = false;
-    double scr = 1.0;
-    if (p1) {
-      e = e1 + kQB - kAlignBits;
-      any = true;
-    }
-    if (p2) {
-      const int top = e2 + kAccB - kAlignBits;
-      if (!any) {
-        e = top;
-        any = true;
-      } else if (top > e) {
-        reb = true;
-        scr = ldexp(1.0, e - top);
-        e = top;
-      }
-      sh = e2 - e;
-    }
-    const double sc1 = ldexp(1.0, kAlignBits - kQB), sc2 = ldexp(1.0, sh);
-    int m = 0;
-#pragma unroll
-    for (int I = 0; I < 4; ++I)
-#pragma unroll
-      for (int K = J0; K < J0 + JN; ++K) {
-        const i32x4 c1 = codes(t1, I, K);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          double x = p1 ? (double)c1[v] * sc1 : 0.0;
-          if (reb) x = rint(x * scr);
-          if (p2) {
-            const double y = t2.a[4 * I + K][v];
-            x = sh >= 0 ? __builtin_fma(y, sc2, x) : x + rint(y * sc2);
-          }
-          t2.a[4 * I + K][v] = x;
-          m = max(m, __double2hiint(fabs(x)));
-        }
-      }
-    const int amax_hi = red(wave_max(m));
-    const int s = shift_for_hi(amax_hi);
-    const double sc = ldexp(1.0, -s);
-#pragma unroll
-    for (int I = 0; I < 4; ++I)
-#pragma unroll
-      for (int K = 0; K < 4; ++K)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          out.a[4 * I + K][v] =
-              (K < J0 || K >= J0 + JN) ? 0 : rne_scaled(t2.a[4 * I + K][v], sc);
-    nz = amax_hi > 0;
-    eo = nz ? (any ? e : 0) + s : 0;
-  }
 };
 
-// quantiser: e = smallest integer with amax / 2^e <= 32639, q = rne(x / 2^e)
+// quantiser: q = rne(x / 2^e), e the smallest integer at which every code
+// lies in [-32639, 32639]
 template <int C>
 __global__ __launch_bounds__(64) void k_quantize_i16(const float* __restrict__ A,
                                                      int16_t* __restrict__ Aq,
@@ -492,23 +424,28 @@ hipError_t launch_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int
 
 template <int NB, int DN, int DS>
 static hipError_t run_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
-                                  float* Tdeq, int64_t n, int N, int S, hipStream_t st) {
-  if (N == DN && S == DS)
-    hipLaunchKernelGGL((i16::k_neumann_i16<NB, DN, DS>), dim3((unsigned)n), dim3(64), 0, st, Aq,
+                                  float* Tdeq, int64_t n, int N, int S, bool plain,
+                                  hipStream_t st) {
+  if (plain)
+    hipLaunchKernelGGL((i16::k_neumann_i16<NB, true>), dim3((unsigned)n), dim3(64), 0, st, Aq,
                        eA, Tq, eT, Tdeq, N, S);
+  else if (N == DN && S == DS)
+    hipLaunchKernelGGL((i16::k_neumann_i16<NB, false, DN, DS>), dim3((unsigned)n), dim3(64), 0,
+                       st, Aq, eA, Tq, eT, Tdeq, N, S);
   else
-    hipLaunchKernelGGL((i16::k_neumann_i16<NB>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
-                       eT, Tdeq, N, S);
+    hipLaunchKernelGGL((i16::k_neumann_i16<NB, false>), dim3((unsigned)n), dim3(64), 0, st, Aq,
+                       eA, Tq, eT, Tdeq, N, S);
   return hipGetLastError();
 }
 
 // the default orders (3, 2), (3, 4), (3, 8) run compile-time specialisations
 hipError_t launch_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
-                              float* Tdeq, int64_t n, int C, int N, int S, hipStream_t st) {
+                              float* Tdeq, int64_t n, int C, int N, int S, bool plain,
+                              hipStream_t st) {
   switch (C) {
-    case 16: return run_neumann_i16<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
-    case 32: return run_neumann_i16<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
-    case 64: return run_neumann_i16<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 16: return run_neumann_i16<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, plain, st);
+    case 32: return run_neumann_i16<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, plain, st);
+    case 64: return run_neumann_i16<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, plain, st);
     case 128:
       if (N == 3 && S == 8)
         hipLaunchKernelGGL((iq::k_neumann_int128<i16::I16W, 3, 8>), dim3((unsigned)n), dim3(128),

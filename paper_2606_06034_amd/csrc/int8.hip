@@ -1,22 +1,23 @@
 // int8.hip -- the low-bit (INT8) path: per-tile quantiser and the integer
-// masked-Neumann + residual inverse (Section 3.5, Appendix G of
-// arXiv 2606.06034), one wave per tile.
+// masked-Neumann + residual inverse (Algorithm 1 with the integer
+// activations of Section 3.5 and Appendix G of arXiv 2606.06034), one wave
+// per tile.
 //
-// Arithmetic (identical to the exact-integer reading the library documents):
-//   * a matrix is int8 codes q in [-127, 127] with one exponent e per tile
-//     (value q 2^e); unit lower-triangular matrices keep the identity implicit;
-//   * quantiser: e = smallest integer with max|x| / 2^e <= 127,
-//     q = round-half-even(x / 2^e);
-//   * int8 x int8 products accumulate exactly in int32 (v_mfma_i32_16x16x64_i8)
-//     and are requantised with the smallest round-half-even shift that brings
-//     max|acc| to <= 127 (exponents add);
-//   * sums run in int32 in production order: the first present term sets the
-//     exponent 16 guard bits below its quantum, a later term above 2^23 of
-//     range rebases the sum (round-half-even), finer terms are rounded in;
-//   * the band mask i - j <= N is applied to every power before it is
-//     quantised; E = Lm + Lm N0 - N0 exactly, band set to 0; the residual
-//     powers are P_s = E P_{s-1}; T = N0 + Gs + N0 Gs.
-// Exponents and "matrix is non-zero" flags are wave-uniform (SGPRs).
+// Arithmetic (the exact-integer reading the library documents):
+//   * a tensor is int8 codes q in [-127, 127] with one exponent e per tile
+//     (value q 2^e);
+//   * the scale rule: q = round-half-even(v / 2^e) with e the smallest
+//     integer at which no code leaves [-127, 127], for the quantiser of the
+//     float input and for every intermediate;
+//   * every operator of Algorithm 1 (MatMul, Add, the residual
+//     E = I - (I + A) T0) is evaluated exactly from its operands' codes
+//     (int8 x int8 products exact in int32 on v_mfma_i32_16x16x64_i8, sums
+//     exact in int32 or fp64) and its result quantised once;
+//   * T0 is masked once after its sum; the residual powers are
+//     P_s = P_{s-1} E; T_hat = T0 T;
+//   * split form: the unit diagonal of T0, T and T_hat stays out of the
+//     codes; plain form (GDN_INT_PLAIN): every tensor holds its diagonal.
+// Exponents and "tensor is non-zero" flags are wave-uniform (SGPRs).
 //
 // Operands are the int8 quad fragments of intq.hpp.
 #include "chunk.hpp"
@@ -30,9 +31,10 @@ namespace i8 {
 
 
 
-// Tq (codes, zero on and above the diagonal), eT and optionally
-// Tdeq = I + Tq 2^eT for tile `tile`
-template <int NB>
+// Tq (codes, zero above the diagonal and, in split form, on it), eT and
+// optionally Tdeq = T_hat in fp32 (I + Tq 2^eT in split form, Tq 2^eT in
+// plain form) for tile `tile`
+template <int NB, bool PLAIN = false>
 __device__ __forceinline__ void store_i8(const AccI<NB>& Tr, int eTo, int8_t* __restrict__ Tq,
                                          int32_t* __restrict__ eT, float* __restrict__ Tdeq,
                                          int64_t tile) {
@@ -55,15 +57,15 @@ __device__ __forceinline__ void store_i8(const AccI<NB>& Tr, int eTo, int8_t* __
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int d = 16 * (I - J) + c - 4 * g - v;
-          if (J <= I && d > 0) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], eTo);
-          if (d == 0) x[v] = 1.f;
+          if (J <= I && d >= (PLAIN ? 0 : 1)) x[v] = ldexpf((float)Tr.a[bidx(I, J)][v], eTo);
+          if (!PLAIN && d == 0) x[v] = 1.f;
         }
         *(f32x4*)(td + (I * 16 + c) * C + J * 16 + 4 * g) = x;
       }
   }
 }
 
-template <int NB, int NC = -1, int SC = -1>
+template <int NB, bool PLAIN, int NC = -1, int SC = -1>
 __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq,
                                                    const int32_t* __restrict__ eA,
                                                    int8_t* __restrict__ Tq,
@@ -88,8 +90,8 @@ __global__ __launch_bounds__(64) void k_neumann_i8(const int8_t* __restrict__ Aq
   const int eL = __builtin_amdgcn_readfirstlane(eA[tile]);
   AccI<NB> Tr;
   int eTo;
-  int_engine<I8Ops, NB, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
-  store_i8<NB>(Tr, eTo, Tq, eT, Tdeq, tile);
+  int_engine<I8Ops, NB, PLAIN, NC, SC>(Lr, eL, Nrt, Srt, Tr, eTo);
+  store_i8<NB, PLAIN>(Tr, eTo, Tq, eT, Tdeq, tile);
 }
 
 
@@ -124,20 +126,13 @@ __global__ __launch_bounds__(64) void k_inverse_i8_fused(const TK* __restrict__ 
     for (int v = 0; v < 4; ++v) Lr.a[b][v] = -(int)rintf(ldexpf(G.a[b][v], -e));
   AccI<NB> Tr;
   int eTo;
-  int_engine<I8Ops, NB, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
+  int_engine<I8Ops, NB, false, NC, SC>(Lr, e, Nrt, Srt, Tr, eTo);
   store_i8<NB>(Tr, eTo, Tq, eT, Tdeq, ch.tile);
 }
 
 // ---------------------------------------------------------------------------
 // The INT8 width at C = 128 (k_neumann_int128, k_quantize_int128): the
 // engine's fragments plus full 64 x 64 blocks with exact int32 products.
-
-__device__ __forceinline__ void shift_full(FullI& D, int s) {
-#pragma unroll
-  for (int b = 0; b < 16; ++b)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) D.a[b][v] = s >= 31 ? 0 : rne_pos(D.a[b][v], s);
-}
 
 struct I8W : I8Ops<4> {
   using Code = int8_t;
@@ -148,7 +143,7 @@ struct I8W : I8Ops<4> {
   template <int NC, int SC>
   static __device__ __forceinline__ void engine(const AccI<4>& Lr, int eL, int N, int S,
                                                 AccI<4>& Tr, int& eTo) {
-    int_engine<I8Ops, 4, NC, SC>(Lr, eL, N, S, Tr, eTo);
+    int_engine<I8Ops, 4, false, NC, SC>(Lr, eL, N, S, Tr, eTo);
   }
   static __device__ __forceinline__ void to_frow(Row& X, const FullI& D) { to_rowq_full(X, D); }
   static __device__ __forceinline__ void frow_to_col(Col& Y, const Row& X, const ColQ<4>& Ic) {
@@ -164,72 +159,11 @@ struct I8W : I8Ops<4> {
   static __device__ __forceinline__ i32x4 codes(const Row& X, int I, int K) {
     return unpack4(X.r[I].v[K]);
   }
-  // The running sum of two terms over the block columns J0 .. J0 + JN - 1,
-  // requantised: the codes of the fragments t1 (exponent e1), then the exact
-  // product t2 (exponent e2), by the engine's rules (the first present term
-  // 16 guard bits under its quantum, a larger later term rebases the sum, a
-  // finer one is rounded in).  The exponent plan is wave-uniform, so the sum
-  // is one pass per entry, in place in t2.  red(m) joins this wave's maximum
-  // with the other blocks' (identity when one wave forms every block).  The
-  // other block columns of out are set to 0.
-  template <int J0, int JN, typename Red>
-  static __device__ __forceinline__ void sum2(FullI& out, int& eo, bool& nz, const Row& t1,
-                                              int e1, bool p1, FullI& t2, int e2, bool p2,
-                                              Red&& red) {
-    int e = 0, reb = 0, sh = 0;
-    bool any = false;
-    if (p1) {
-      e = e1 + kQB - kAlignBits;
-      any = true;
-    }
-    if (p2) {
-      const int top = e2 + kAccB - kAlignBits;
-      if (!any) {
-        e = top;
-        any = true;
-      } else if (top > e) {
-        reb = top - e;
-        e = top;
-      }
-      sh = e2 - e;
-    }
-    int m = 0;
-#pragma unroll
-    for (int I = 0; I < 4; ++I)
-#pragma unroll
-      for (int K = J0; K < J0 + JN; ++K) {
-        const i32x4 c1 = codes(t1, I, K);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          int x = p1 ? c1[v] << (kAlignBits - kQB) : 0;
-          if (reb > 0) x = reb >= 31 ? 0 : rne_pos(x, reb);
-          if (p2) {
-            const int y = t2.a[4 * I + K][v];
-            x += sh >= 0 ? y << sh : (sh > -31 ? rne_pos(y, -sh) : 0);
-          }
-          t2.a[4 * I + K][v] = x;
-          m = max(m, abs(x));
-        }
-      }
-    const int amax = red(wave_max(m));
-    const int s = shift_for(amax);
-#pragma unroll
-    for (int I = 0; I < 4; ++I)
-#pragma unroll
-      for (int K = 0; K < 4; ++K)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          out.a[4 * I + K][v] = (K < J0 || K >= J0 + JN) ? 0
-                                : s == 0                ? t2.a[4 * I + K][v]
-                                : s >= 31               ? 0
-                                                        : rne_pos(t2.a[4 * I + K][v], s);
-    nz = amax > 0;
-    eo = nz ? (any ? e : 0) + s : 0;
-  }
 };
 
 // ---------------------------------------------------------------------------
-// quantiser: e = smallest integer with amax / 2^e <= 127, q = rne(x / 2^e)
+// quantiser: q = rne(x / 2^e), e the smallest integer at which every code
+// lies in [-127, 127]
 
 template <int C>
 __global__ __launch_bounds__(64) void k_quantize_i8(const float* __restrict__ A,
@@ -289,23 +223,29 @@ hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n
 
 template <int NB, int DN, int DS>
 static hipError_t run_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
-                                 float* Tdeq, int64_t n, int N, int S, hipStream_t st) {
-  if (N == DN && S == DS)
-    hipLaunchKernelGGL((i8::k_neumann_i8<NB, DN, DS>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA,
+                                 float* Tdeq, int64_t n, int N, int S, bool plain,
+                                 hipStream_t st) {
+  if (plain)
+    hipLaunchKernelGGL((i8::k_neumann_i8<NB, true>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA,
                        Tq, eT, Tdeq, N, S);
+  else if (N == DN && S == DS)
+    hipLaunchKernelGGL((i8::k_neumann_i8<NB, false, DN, DS>), dim3((unsigned)n), dim3(64), 0, st,
+                       Aq, eA, Tq, eT, Tdeq, N, S);
   else
-    hipLaunchKernelGGL((i8::k_neumann_i8<NB>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA, Tq,
-                       eT, Tdeq, N, S);
+    hipLaunchKernelGGL((i8::k_neumann_i8<NB, false>), dim3((unsigned)n), dim3(64), 0, st, Aq, eA,
+                       Tq, eT, Tdeq, N, S);
   return hipGetLastError();
 }
 
-// the default orders (3, 2), (3, 4), (3, 8) run compile-time specialisations
+// the default orders (3, 2), (3, 4), (3, 8) of the split form run
+// compile-time specialisations; plain form only at C <= 64
 hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
-                             float* Tdeq, int64_t n, int C, int N, int S, hipStream_t st) {
+                             float* Tdeq, int64_t n, int C, int N, int S, bool plain,
+                             hipStream_t st) {
   switch (C) {
-    case 16: return run_neumann_i8<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
-    case 32: return run_neumann_i8<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
-    case 64: return run_neumann_i8<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, st);
+    case 16: return run_neumann_i8<1, 3, 2>(Aq, eA, Tq, eT, Tdeq, n, N, S, plain, st);
+    case 32: return run_neumann_i8<2, 3, 4>(Aq, eA, Tq, eT, Tdeq, n, N, S, plain, st);
+    case 64: return run_neumann_i8<4, 3, 8>(Aq, eA, Tq, eT, Tdeq, n, N, S, plain, st);
     case 128:
       if (N == 3 && S == 8)
         hipLaunchKernelGGL((iq::k_neumann_int128<i8::I8W, 3, 8>), dim3((unsigned)n), dim3(128), 0,

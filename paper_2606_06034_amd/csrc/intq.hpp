@@ -1,7 +1,9 @@
 // intq.hpp -- integer operands of the low-bit inverse paths on gfx950's
 // int8 MFMA (v_mfma_i32_16x16x64_i8): int8 "quad" fragments of lower
 // block-triangular C x C matrices (C = 16, 32, 64), their exact int32
-// products, the identity, band masks and a wave-wide maximum.
+// products, the identity, band masks, a wave-wide maximum, the scale rule
+// of the quantiser, exact sums in fp64, and the integer inverse of one tile
+// (int_engine) that both code widths run.
 //
 // A quad holds 16 int8 per lane, four 16 x 16 blocks of 4 bytes: row quad
 // R[I] = blocks (I, 0..3) in row form, column quad Cq[J] = blocks (0..3, J)
@@ -13,12 +15,16 @@
 
 #include "tile16.hpp"
 
+#include <stdint.h>
+
 // wave reductions of the ROCm device library
 extern "C" __device__ __attribute__((const)) int __ockl_wfred_max_i32(int);
 extern "C" __device__ __attribute__((const)) float __ockl_wfred_max_f32(float);
 
 namespace gdn {
 namespace iq {
+
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 struct Quad {
   i32x4 v;  // dword K = 4 bytes of block K
@@ -186,33 +192,275 @@ __device__ __forceinline__ int amax_full(const FullI& D) {
   return wave_max(m);
 }
 
+
 // ---------------------------------------------------------------------------
-// The integer inverse of one tile (Section 3.5, Algorithm 1, in the integer
-// arithmetic the library reads from Appendix G): from Lm = -A as codes (row
-// form, strictly lower) with exponent eL, the masked Neumann powers
-// B_n = M(B_{n-1} Lm) summed into N0 (band 1..N), E = Lm + Lm N0 - N0 (band
-// 1..N set to its exact value 0), the residual powers P_s = E P_{s-1} summed
-// into Gs, and T = N0 + Gs + N0 Gs; every product requantised, every sum
-// exact in production order.  Returns the strict part of T_hat as codes Tr
-// (row form) and its exponent eTo.  NC, SC >= 0 fix N and S at compile time
-// (every band and block skip is then resolved by the compiler); -1 takes
-// them from Nrt, Srt.
+// The scale rule.  A tensor of codes |q| <= Q with one power-of-two scale
+// 2^e per tile; an exactly known tensor v is quantised to
+// q = round-half-even(v / 2^e) with e the smallest integer at which no code
+// leaves [-Q, Q], i.e. max|v| < (Q + 1/2) 2^e (Appendix G's
+// q(x) = clip(round(x / Delta)) with the finest Delta = 2^e whose clip does
+// nothing).  QB: 2^(QB - 1) <= Q < 2^QB.
+
+// The shift s = e - e_v for values v = y 2^e_v held as integers y with
+// max|y| = amax > 0 (int32): s is b - QB or b - QB + 1, b the bit length of
+// amax (amax / 2^(b - QB) lies in [2^(QB-1), 2^QB)).
+template <int Q, int QB>
+__device__ __forceinline__ int shift_canon(int amax) {
+  const int b = 32 - __clz(amax);
+  const int s = b - QB;
+  const bool over = s <= 0 ? ((int64_t)amax << -s) > Q
+                           : 2 * (int64_t)amax >= ((2 * (int64_t)Q + 1) << s);
+  return s + (over ? 1 : 0);
+}
+
+// The same shift from the high dword of max|y| for y held as fp64 integers
+// (amax_hi > 0).  The test amax < (Q + 1/2) 2^s compares with a threshold
+// of at most 16 significant bits, whose low dword is zero, so amax and its
+// high dword (the value with the low dword cleared) compare alike with it.
+// amax = m 2^p, m in [0.5, 1): 2^QB m < Q + 1/2 gives s = p - QB, else
+// p - QB + 1.
+template <int Q, int QB>
+__device__ __forceinline__ int shift_canon_hi(int amax_hi) {
+  const double a = __hiloint2double(amax_hi, 0);
+  int p;
+  const double m = frexp(a, &p);
+  return p - QB + (m * (double)(1 << QB) >= (double)Q + 0.5 ? 1 : 0);
+}
+
+// round-half-even(x sc) as int32 for an fp64 integer x and a power of two sc
+// with |x sc| < 2^31: x sc + 1.5 2^52 lies in [2^52, 2^53), where the fp64
+// spacing is 1, so the fused addition rounds x sc half to even and the low
+// dword of the sum holds the result in two's complement (1.5 2^52 has a zero
+// low dword)
+constexpr double kRoundMagic = 6755399441055744.0;  // 1.5 * 2^52
+__device__ __forceinline__ int rne_scaled(double x, double sc) {
+  return __double2loint(__builtin_fma(x, sc, kRoundMagic));
+}
+
+template <int NB> struct AccD { f64x4 a[nlower(NB)]; };  // fp64 integers
+
+__device__ __forceinline__ double elem(const i32x4& x, int v) { return (double)x[v]; }
+__device__ __forceinline__ double elem(const f64x4& x, int v) { return x[v]; }
+
+// A term of an exact sum: the lower blocks of t (band [lo, hi]) times
+// sign 2^e, absent when !p.  bits bounds |t| < 2^bits.
+template <typename T> struct Term {
+  const T* t;
+  int e, bits, sign, lo, hi;
+  bool p;
+};
+
+// the bit length of max|t| over the term's band (0 when t is zero): the
+// wave maximum of the high dwords of |t| as fp64, whose frexp exponent is
+// the bit length (an integer's high dword keeps its leading bit)
+template <int NB, typename T>
+__device__ __forceinline__ int term_bits(const Term<T>& x) {
+  int mh = 0;
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, x.lo, x.hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mh = max(mh, __double2hiint(fabs(elem(x.t->a[bidx(I, J)], v))));
+  mh = wave_max(mh);
+  if (mh == 0) return 0;
+  int p;
+  frexp(__hiloint2double(mh, 0), &p);
+  return p;
+}
+
+// The exponent plan of an exact sum of up to three terms, wave-uniform:
+// the scale of each present term relative to the finest one kept (emin),
+// and which terms are rounded to the 52-bit window.  In: each term's
+// exponent e, magnitude bits b (|t| < 2^b, 2^(b-1) <= max|t|) and presence
+// p.  When the present terms span at most 52 bits the sum is exact in
+// fp64.  Otherwise a term whose top lies QB + 6 bits or more under the
+// coarsest top is dropped: unless the kept terms cancel below a quarter of
+// the coarsest one's largest value, the output's quantum is at least
+// 2^(top - QB - 2), so the dropped terms together stay below an eighth of
+// it and move no code.  If the kept terms still span more than 52 bits, the
+// finest are rounded to the window; exactness is claimed for neither of
+// these two cases (no tile of the quantiser's output on the workloads
+// reaches them).
+struct SumPlan {
+  int emin;
+  bool p[3], r[3];
+};
+template <int QB>
+__device__ __forceinline__ SumPlan sum_plan(const int (&e)[3], const int (&b)[3],
+                                            const bool (&p)[3]) {
+  SumPlan pl;
+  int top = -(1 << 30), emin = 1 << 30;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    pl.p[k] = p[k];
+    pl.r[k] = false;
+    if (p[k]) {
+      top = max(top, e[k] + b[k]);
+      emin = min(emin, e[k]);
+    }
+  }
+  if (top - emin > 52) {
+    // only here are b the measured magnitudes (see exact_sum, sum2_full)
+    emin = 1 << 30;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      pl.p[k] = p[k] && e[k] + b[k] > top - QB - 6;
+      if (pl.p[k]) emin = min(emin, e[k]);
+    }
+  }
+  if (top - emin > 52) {
+    const int floor_e = top - 52;
+    emin = 1 << 30;
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+      if (pl.p[k]) {
+        pl.r[k] = e[k] < floor_e;
+        emin = min(emin, max(e[k], floor_e));
+      }
+  }
+  pl.emin = emin;
+  return pl;
+}
+
+// out = q(sum of the terms) over the blocks of the band [lo, hi]: the exact
+// sum (every term aligned at the finest exponent among the kept ones)
+// quantised once by the scale rule (Q, QB).  The values are fp64 integers.
+// The plan first takes each term's bound bits; only when those span more
+// than 52 bits are the terms' actual magnitudes measured (wave maxima), so
+// that a zero or small term does not widen the window (sum_plan).  Returns
+// the codes, their exponent and a non-zero flag; every block of out
+// outside the band is set to 0.
+template <int Q, int QB, int NB, typename T1, typename T2, typename T3>
+__device__ __forceinline__ void exact_sum(AccI<NB>& out, int& eo, bool& nz, const Term<T1>& x,
+                                          const Term<T2>& y, const Term<T3>& z, int lo, int hi) {
+  int e[3] = {x.e, y.e, z.e}, b[3] = {x.bits, y.bits, z.bits};
+  bool p[3] = {x.p, y.p, z.p};
+  int emin = 1 << 30, top = -(1 << 30);
+#pragma unroll
+  for (int k = 0; k < 3; ++k)
+    if (p[k]) {
+      emin = min(emin, e[k]);
+      top = max(top, e[k] + b[k]);
+    }
+  if (!p[0] && !p[1] && !p[2]) {
+#pragma unroll
+    for (int bb = 0; bb < nlower(NB); ++bb) out.a[bb] = zero_i4();
+    eo = 0;
+    nz = false;
+    return;
+  }
+  if (top - emin > 52) {
+    if (p[0]) { b[0] = term_bits<NB>(x); p[0] = b[0] > 0; }
+    if (p[1]) { b[1] = term_bits<NB>(y); p[1] = b[1] > 0; }
+    if (p[2]) { b[2] = term_bits<NB>(z); p[2] = b[2] > 0; }
+  }
+  const SumPlan pl = sum_plan<QB>(e, b, p);
+  const double sx = pl.p[0] ? (double)x.sign * ldexp(1.0, x.e - pl.emin) : 0.0;
+  const double sy = pl.p[1] ? (double)y.sign * ldexp(1.0, y.e - pl.emin) : 0.0;
+  const double sz = pl.p[2] ? (double)z.sign * ldexp(1.0, z.e - pl.emin) : 0.0;
+  auto val = [&](int I, int J, int v) {
+    const int m = I - J, bi = bidx(I, J);
+    double acc = 0.0;
+    if (pl.p[0] && blk_nz(m, x.lo, x.hi)) {
+      const double t = elem(x.t->a[bi], v) * sx;
+      acc += pl.r[0] ? rint(t) : t;
+    }
+    if (pl.p[1] && blk_nz(m, y.lo, y.hi)) {
+      const double t = elem(y.t->a[bi], v) * sy;
+      acc += pl.r[1] ? rint(t) : t;
+    }
+    if (pl.p[2] && blk_nz(m, z.lo, z.hi)) {
+      const double t = elem(z.t->a[bi], v) * sz;
+      acc += pl.r[2] ? rint(t) : t;
+    }
+    return acc;
+  };
+  int mh = 0;
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mh = max(mh, __double2hiint(fabs(val(I, J, v))));
+  const int amax_hi = wave_max(mh);
+  nz = amax_hi > 0;
+  const int s = nz ? shift_canon_hi<Q, QB>(amax_hi) : 0;
+  const double sc = ldexp(1.0, -s);
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) {
+      i32x4 r = zero_i4();
+      if (nz && blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) r[v] = rne_scaled(val(I, J, v), sc);
+      out.a[bidx(I, J)] = r;
+    }
+  eo = nz ? pl.emin + s : 0;
+}
+
+template <typename T>
+__device__ __forceinline__ Term<T> term(const T& t, int e, int bits, int sign, int lo, int hi,
+                                        bool p) {
+  return Term<T>{&t, e, bits, sign, lo, hi, p};
+}
+template <typename T>
+__device__ __forceinline__ Term<T> no_term(const T& t) {
+  return Term<T>{&t, 0, 0, 1, 0, 0, false};
+}
+
+// identity codes (1 on the diagonal, exponent 0)
+template <int NB>
+__device__ __forceinline__ void eye_codes(AccI<NB>& D) {
+  const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) D.a[bidx(I, J)][v] = (I == J && c == 4 * g + v) ? 1 : 0;
+}
+
+// ---------------------------------------------------------------------------
+// The integer inverse of one tile: Algorithm 1 (Section 3.4) with integer
+// activations (Section 3.5, Appendix G), every operator evaluated exactly
+// from its operands' codes and its result quantised once by the scale rule:
+//   P_1 = L (= -A), P_n = q(P_{n-1} L),          T0 = q(T0 + P_n),
+//   T0 = M^(N) (.) T0 (codes masked, scale kept),
+//   E = I - q((I + A) T0),
+//   P_1 = E, P_s = q(P_{s-1} E),                 T = q(T + P_s),
+//   T_hat = q(T0 T)
+// (T0 starts at I, T at I).  Split form (PLAIN false): the unit diagonal of
+// T0, T and T_hat stays out of the codes, so their tensors are the strict
+// lower parts and a product of two of them is (I + X)(I + Y) = I + (X + Y +
+// X Y), one rounding of the three-term sum; E = -q(A + N0 + A N0).  Plain
+// form: every tensor holds its diagonal; E = q(I - q(T0 + A T0)).
+//
+// In: Lm = -A as codes (row form, strictly lower) with exponent eL.  Out:
+// T_hat's tensor as codes Tr (row form) and its exponent eTo.  NC, SC >= 0
+// fix N and S at compile time; -1 takes them from Nrt, Srt.
 //
 // Ops<NB> supplies one code width: fragment types Row, Col (operands in row
-// and column form), Prod (an exact product) and Sum (an exact running sum);
-// kQB and kAccB, log2 bounds of a code's and a product's magnitude; to_row,
-// to_col (codes to fragments), mm<OUTQ> (exact product, blocks outside a
-// band zero), band, requant (product to codes), requant_codes, row_to_col,
-// col_to_row (form changes through the identity), rs_init, rs_add, rs_band,
-// rs_finish.  Every helper visits only the blocks that can meet the band of
+// and column form) and Prod (an exact product); kQ, kQB (the code range and
+// its bits), kAccB (log2 bound of a product's magnitude); to_row, to_col
+// (codes to fragments), mm<OUTQ> (exact product, blocks outside a band
+// zero), requant (a product to codes by the scale rule), canon (codes to the
+// finest scale that holds them), add (q of the sum of two tensors of codes,
+// the first known to be at its finest scale or not),
+// row_to_col (column-form fragments of a row-form one, through the
+// identity).  Every helper visits only the blocks that can meet the band of
 // sub-diagonals it is given; the other blocks are zero by the structure of
 // the computation.
-template <template <int> class Ops, int NB, int NC = -1, int SC = -1>
+template <template <int> class Ops, int NB, bool PLAIN, int NC = -1, int SC = -1>
 __device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, int Srt,
                                            AccI<NB>& Tr, int& eTo) {
   using O = Ops<NB>;
   constexpr int C = 16 * NB;
-  constexpr int QB = O::kQB, ACCB = O::kAccB;
+  constexpr int Q = O::kQ, QB = O::kQB, ACCB = O::kAccB;
+  constexpr int U0 = PLAIN ? 0 : 1;  // lowest sub-diagonal of T0's, T's and T_hat's tensors
   const int N = NC >= 0 ? NC : Nrt;
   const int S = SC >= 0 ? SC : Srt;
   RowQ<NB> Iq;
@@ -223,28 +471,30 @@ __device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, 
   typename O::Row LRq;
   O::to_row(LRq, Lr, 1, C - 1);
   typename O::Col LCq;
-  O::row_to_col(LCq, nullptr, LRq, Ic, 1, C - 1);
+  O::row_to_col(LCq, LRq, Ic, 1, C - 1);
 
-  // ---- N0 = sum of the masked powers B_n = M(B_{n-1} Lm) (band n..N), row form
-  typename O::Sum ns;
-  O::rs_init(ns, 1, N);
+  // ---- T0 = sum_{n=0}^{N} L^n, then masked
+  AccI<NB> T0;
+  int eT0 = 0;
+  bool nzT0 = PLAIN;
+  if constexpr (PLAIN) eye_codes(T0);
+  else {
+#pragma unroll
+    for (int b = 0; b < nlower(NB); ++b) T0.a[b] = zero_i4();
+  }
   if (N >= 1) {
-    AccI<NB> B = Lr;
-    band_i<NB, false>(B, 1, N);
-    int eB;
-    bool nzB;
-    O::requant_codes(B, 1, N, eL, eB, nzB);
-    O::rs_add(ns, B, 1, N, eB, QB, nzB);
-    typename O::Row Bq;
-    O::to_row(Bq, B, 1, N);
+    AccI<NB> P = Lr;
+    int eP = eL;
+    bool nzP = nzL;
+    O::canon(P, 1, C - 1, eP, nzP);
+    O::add(T0, eT0, nzT0, U0, !PLAIN, P, eP, nzP, 1, 1, U0, C - 1);
+    typename O::Row PRq;
     auto power = [&](int n) {
+      O::to_row(PRq, P, n - 1, C - 1);
       typename O::Prod D;
-      O::template mm<true>(D, Bq, LCq, n, N);
-      O::band(D, n, N);
-      AccI<NB> q;
-      O::requant(D, q, n, N, eB + eL, eB, nzB);
-      O::rs_add(ns, q, n, N, eB, QB, nzB);
-      O::to_row(Bq, q, n, N);
+      O::template mm<true>(D, PRq, LCq, n, C - 1);
+      O::requant(D, P, n, C - 1, eP + eL, eP, nzP);
+      O::add(T0, eT0, nzT0, U0, true, P, eP, nzP, 1, n, U0, C - 1);
     };
     if constexpr (NC >= 0) {
 #pragma unroll
@@ -253,52 +503,65 @@ __device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, 
       for (int n = 2; n <= N; ++n) power(n);
     }
   }
-  AccI<NB> N0r;
-  int eN0;
-  bool nzN0;
-  O::rs_finish(ns, N0r, eN0, nzN0);
-  typename O::Row N0q;
-  O::to_row(N0q, N0r, 1, N);
-  typename O::Col N0c;
-  O::row_to_col(N0c, nullptr, N0q, Ic, 1, N);
+  band_i<NB, false>(T0, U0, N);
+  nzT0 = amax_of(T0, U0, N) > 0;
+  typename O::Row T0Rq;
+  O::to_row(T0Rq, T0, U0, N);
+  typename O::Col T0Cq;
+  O::row_to_col(T0Cq, T0Rq, Ic, U0, N);
 
-  // ---- E = Lm + Lm N0 - N0 (row form), band 1..N zeroed
-  typename O::Row ERq;
-  typename O::Col ECq;
-  AccI<NB> Ecol;
+  // ---- E = I - q((I + A) T0), with (I + A) T0 = T0 - Lm T0
+  constexpr int E0 = PLAIN ? 0 : 1;  // lowest sub-diagonal of E
+  AccI<NB> E;
   int eE;
   bool nzE;
   {
-    typename O::Prod LN;
-    O::template mm<true>(LN, LRq, N0c, 2, C - 1);
-    typename O::Sum es;
-    O::rs_init(es, 1, C - 1);
-    O::rs_add(es, Lr, 1, C - 1, eL, QB, nzL);
-    O::rs_add(es, LN, 2, C - 1, eL + eN0, ACCB, nzL && nzN0);
-    O::rs_add(es, N0r, 1, N, eN0, QB, nzN0, true);
-    O::rs_band(es, N + 1, C - 1);
-    AccI<NB> Er;
-    O::rs_finish(es, Er, eE, nzE);
-    O::to_row(ERq, Er, N + 1, C - 1);
-    O::row_to_col(ECq, &Ecol, ERq, Ic, N + 1, C - 1);  // column form of E (exact codes)
+    typename O::Prod D;
+    O::template mm<true>(D, LRq, T0Cq, U0 + 1, C - 1);  // Lm T0
+    if constexpr (!PLAIN) {
+      // E = -(A + N0 + A N0) = Lm - N0 + Lm N0
+      exact_sum<Q, QB, NB>(E, eE, nzE, term(Lr, eL, QB, 1, 1, C - 1, nzL),
+                           term(T0, eT0, QB, -1, 1, N, nzT0),
+                           term(D, eL + eT0, ACCB, 1, 2, C - 1, nzL && nzT0), 1, C - 1);
+    } else {
+      AccI<NB> M;
+      int eM;
+      bool nzM;
+      exact_sum<Q, QB, NB>(M, eM, nzM, term(T0, eT0, QB, 1, 0, N, nzT0), no_term(T0),
+                           term(D, eL + eT0, ACCB, -1, 1, C - 1, nzL && nzT0), 0, C - 1);
+      eye_codes(E);
+      eE = 0;
+      nzE = true;
+      O::add(E, eE, nzE, 0, false, M, eM, nzM, -1, 0, 0, C - 1);
+    }
   }
+  typename O::Row ERq;
+  O::to_row(ERq, E, E0, C - 1);
+  typename O::Col ECq;
+  O::row_to_col(ECq, ERq, Ic, E0, C - 1);
 
-  // ---- residual powers P_s = E P_{s-1} (column form, band s(N+1)..), Gs = sum
-  typename O::Sum gs;
-  O::rs_init(gs, N + 1, C - 1);
+  // ---- T = sum_{s=0}^{S} E^s
+  AccI<NB> R;
+  int eR = 0;
+  bool nzR = PLAIN;
+  if constexpr (PLAIN) eye_codes(R);
+  else {
+#pragma unroll
+    for (int b = 0; b < nlower(NB); ++b) R.a[b] = zero_i4();
+  }
   if (S >= 1) {
-    O::rs_add(gs, Ecol, N + 1, C - 1, eE, QB, nzE);
-    typename O::Col Pq = ECq;
+    O::add(R, eR, nzR, U0, !PLAIN, E, eE, nzE, 1, E0, U0, C - 1);
+    AccI<NB> P;
     int eP = eE;
     bool nzP = nzE;
+    typename O::Row PRq = ERq;
     auto chain = [&](int s) {
-      const int lo = s * (N + 1);
+      const int lo = PLAIN ? 0 : s;
       typename O::Prod D;
-      O::template mm<false>(D, ERq, Pq, lo, C - 1);
-      AccI<NB> q;
-      O::requant(D, q, lo, C - 1, eE + eP, eP, nzP);
-      O::rs_add(gs, q, lo, C - 1, eP, QB, nzP);
-      O::to_col(Pq, q, lo, C - 1);
+      O::template mm<true>(D, PRq, ECq, lo, C - 1);
+      O::requant(D, P, lo, C - 1, eP + eE, eP, nzP);
+      O::add(R, eR, nzR, U0, true, P, eP, nzP, 1, lo, U0, C - 1);
+      O::to_row(PRq, P, lo, C - 1);
     };
     if constexpr (SC >= 0) {
 #pragma unroll
@@ -307,27 +570,24 @@ __device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, 
       for (int s = 2; s <= S; ++s) chain(s);
     }
   }
-  AccI<NB> Gc;
-  int eG;
-  bool nzG;
-  O::rs_finish(gs, Gc, eG, nzG);
-  typename O::Col GCq;
-  O::to_col(GCq, Gc, N + 1, C - 1);
-  AccI<NB> Gr;
-  O::col_to_row(Gr, Iq, GCq, N + 1, C - 1);  // row form of Gs (exact codes)
 
-  // ---- T = N0 + Gs + N0 Gs (row form), strict part
-  bool nzT;
+  // ---- T_hat = q(T0 T)
+  typename O::Col RCq;
   {
-    typename O::Prod NG;
-    O::template mm<true>(NG, N0q, GCq, N + 2, C - 1);
-    typename O::Sum ts;
-    O::rs_init(ts, 1, C - 1);
-    O::rs_add(ts, N0r, 1, N, eN0, QB, nzN0);
-    O::rs_add(ts, Gr, N + 1, C - 1, eG, QB, nzG);
-    O::rs_add(ts, NG, N + 2, C - 1, eN0 + eG, ACCB, nzN0 && nzG);
-    O::rs_band(ts, 1, C - 1);
-    O::rs_finish(ts, Tr, eTo, nzT);
+    typename O::Row RRq;
+    O::to_row(RRq, R, U0, C - 1);
+    O::row_to_col(RCq, RRq, Ic, U0, C - 1);
+  }
+  typename O::Prod D;
+  O::template mm<true>(D, T0Rq, RCq, PLAIN ? 0 : 2, C - 1);
+  if constexpr (!PLAIN) {
+    bool nzT;
+    exact_sum<Q, QB, NB>(Tr, eTo, nzT, term(T0, eT0, QB, 1, 1, N, nzT0),
+                         term(R, eR, QB, 1, 1, C - 1, nzR),
+                         term(D, eT0 + eR, ACCB, 1, 2, C - 1, nzT0 && nzR), 1, C - 1);
+  } else {
+    bool nzT;
+    O::requant(D, Tr, 0, C - 1, eT0 + eR, eTo, nzT);
   }
 }
 

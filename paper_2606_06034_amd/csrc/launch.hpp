@@ -58,14 +58,16 @@ hipError_t launch_fused_varlen(const void* K, const void* V, const float* beta, 
 hipError_t launch_quantize_i8(const float* A, int8_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                               hipStream_t st);
 hipError_t launch_neumann_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,
-                             float* Tdeq, int64_t n_tiles, int C, int N, int S, hipStream_t st);
+                             float* Tdeq, int64_t n_tiles, int C, int N, int S, bool plain,
+                             hipStream_t st);
 hipError_t launch_inverse_i8_fused(const void* K, const float* beta, const float* g, int8_t* Tq,
                                    int32_t* eT, float* Tdeq, int B, int L, int H, int dk, int C,
                                    int N, int S, int k_dtype, hipStream_t st);
 hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t n_tiles, int C,
                                hipStream_t st);
 hipError_t launch_neumann_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
-                              float* Tdeq, int64_t n_tiles, int C, int N, int S, hipStream_t st);
+                              float* Tdeq, int64_t n_tiles, int C, int N, int S, bool plain,
+                              hipStream_t st);
 hipError_t launch_fwdsub_i16(const int16_t* Aq, const int32_t* eA, int16_t* Tq, int32_t* eT,
                              float* Tdeq, int64_t n_tiles, int C, hipStream_t st);
 hipError_t launch_fwdsub_i8(const int8_t* Aq, const int32_t* eA, int8_t* Tq, int32_t* eT,

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert g.gdn_abi_version() == 2
+    assert g.gdn_abi_version() == 3
     for code in (OK, NULL, SHAPE, PARAM, DTYPE, ALIGN, ALIAS, HIP, UNSUP, WS, 12345):
         assert isinstance(g.gdn_status_string(code), str) and g.gdn_status_string(code)
 
@@ -155,18 +155,24 @@ def test_int_validation(w):
     assert q(P1, P1, 2 * BIG, 4, 64, None) == ALIAS
     assert q(None, None, None, 0, 64, None) == OK
     n = getattr(L, "gdn_chunk_inverse_neumann_" + w)
-    assert n(P1, P2, BIG, 2 * BIG, None, 4, 64, 64, 8, None) == PARAM
-    assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, None) == NULL
-    assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
-    assert n(None, None, None, None, None, 0, 64, 3, 8, None) == OK
+    # Aq, eA, Tq, eT, Tdeq, n_tiles, C, N, S, flags, stream
+    assert n(P1, P2, BIG, 2 * BIG, None, 4, 64, 64, 8, 0, None) == PARAM
+    assert n(P1, P2, BIG, None, None, 4, 64, 3, 8, 0, None) == NULL
+    assert n(P1, P2, P1, 2 * BIG, None, 4, 64, 3, 8, 0, None) == ALIAS
+    assert n(None, None, None, None, None, 0, 64, 3, 8, 0, None) == OK
+    # flags: GDN_INT_PLAIN (1) only, and not at C = 128
+    assert n(P1, P2, BIG, 2 * BIG, None, 4, 64, 3, 8, 2, None) == PARAM
+    assert n(P1, P2, BIG, 2 * BIG, None, 4, 128, 3, 8, 1, None) == UNSUP
+    assert n(None, None, None, None, None, 0, 64, 3, 8, 1, None) == OK
+    assert g.GDN_INT_PLAIN == 1
     # C = 128: orders up to 63 (64-blocks); eA, eT hold 3 exponents per tile
-    assert n(P1, 2 * BIG, 3 * BIG, 4 * BIG, None, 4, 128, 64, 8, None) == PARAM
-    assert n(P1, 2 * BIG, 3 * BIG, 2 * BIG + 16, None, 4, 128, 63, 8, None) == ALIAS
-    assert n(None, None, None, None, None, 0, 128, 3, 8, None) == OK
+    assert n(P1, 2 * BIG, 3 * BIG, 4 * BIG, None, 4, 128, 64, 8, 0, None) == PARAM
+    assert n(P1, 2 * BIG, 3 * BIG, 2 * BIG + 16, None, 4, 128, 63, 8, 0, None) == ALIAS
+    assert n(None, None, None, None, None, 0, 128, 3, 8, 0, None) == OK
     if w == "i16":
         # Tq starting one int8 extent (4 tiles of 64 x 64 bytes) past Aq lies
         # inside the int16 codes
-        assert n(P1, P2, P1 + 4 * 64 * 64, 2 * BIG, None, 4, 64, 3, 8, None) == ALIAS
+        assert n(P1, P2, P1 + 4 * 64 * 64, 2 * BIG, None, 4, 64, 3, 8, 0, None) == ALIAS
 
 
 def test_blockwise_validation():
@@ -401,3 +407,47 @@ def test_binding_inverse_modes_and_exponent_layout():
     with pytest.raises(ValueError):
         b._fwd_mode(False, "int4")
     assert [b._nexp(C) for C in (16, 32, 64, 128)] == [1, 1, 1, 3]
+
+
+# ---------------------------------------------------------------------------
+# HIP's grid bounds a launch to 2^32 - 1 work items: every entry point turns
+# a tile count past (2^32 - 1) / (its workgroup size) into GDN_ERR_SHAPE
+# before anything is enqueued (pointers are never touched: the sizes fail
+# first, so made-up addresses are safe here)
+
+LIM64 = (2 ** 32 - 1) // 64     # 67,108,863 tiles of one wave
+LIM128 = (2 ** 32 - 1) // 128   # the two-wave C = 128 kernels
+LIM256 = (2 ** 32 - 1) // 256   # the C = 128 quantiser and the state pass
+
+
+def test_grid_limit_inverse_entry_points():
+    for f in (lambda n: L.gdn_chunk_inverse_neumann(P1, BIG, n, 16, 3, 2, 1, None),
+              lambda n: L.gdn_chunk_inverse_fwdsub(P1, BIG, n, 16, 1, None),
+              lambda n: L.gdn_chunk_inverse_blockwise(P1, BIG, n, 16, 1, None),
+              lambda n: L.gdn_chunk_inverse_fwdsub_i8(P1, P2, BIG, 2 * BIG, None, n, 16, None),
+              lambda n: L.gdn_chunk_inverse_fwdsub_i16(P1, P2, BIG, 2 * BIG, None, n, 16, None)):
+        assert f(LIM64 + 1) == SHAPE
+        assert f(1 << 31) == SHAPE
+    for w in ("i8", "i16"):
+        n = getattr(L, "gdn_chunk_inverse_neumann_" + w)
+        assert n(P1, P2, BIG, 2 * BIG, None, LIM64 + 1, 16, 3, 2, 0, None) == SHAPE
+        assert n(P1, P2, BIG, 2 * BIG, None, LIM128 + 1, 128, 3, 8, 0, None) == SHAPE
+        q = getattr(L, "gdn_quantize_tiles_" + w)
+        assert q(P1, BIG, 2 * BIG, LIM64 + 1, 16, None) == SHAPE
+        assert q(P1, BIG, 2 * BIG, LIM256 + 1, 128, None) == SHAPE
+
+
+def test_grid_limit_chunked_entry_points():
+    # [B, L, H, d] entry points: B * H * L / C tiles; C = 16 with H = 1 and
+    # B * L / 16 = LIM64 + 1 tiles (one over the one-wave limit)
+    Lc = 16 * (LIM64 + 1)          # one sequence of that many tokens, B = 1
+    assert Lc < 2 ** 31
+    assert L.gdn_build_A(P1, P2, P3, BIG, 1, Lc, 1, 128, 16, 1, 1, None) == SHAPE
+    f = L.gdn_chunk_wy_fused
+    # K, V, beta, g, W, U, Tinv, B, L, H, dk, dv, C, N, S, dtype, stream
+    assert f(P1, P2, P3, BIG, 2 * BIG, 3 * BIG, None, 1, Lc, 1, 128, 128, 16, 3, 2, 1,
+             None) == SHAPE
+    # C = 128 (128 work items per tile): H * L / 128 = 2^10 * 2^15 = LIM128 + 1
+    assert LIM128 + 1 == 2 ** 25
+    assert f(P1, P2, P3, BIG, 2 * BIG, 3 * BIG, None, 1, 128 * 2 ** 15, 2 ** 10, 128, 128, 128,
+             3, 8, 1, None) == SHAPE

@@ -115,9 +115,14 @@ def test_inverse_blocked_bit_exact(width, src):
 def test_inverse_blocked_orders_random_codes(width, N, S):
     spec = WIDTHS[width][0]
     qA, eA = random_codes(6, spec, seed=N * 16 + S, density=0.3)
-    # block exponents far apart in both directions (rebase and round-in paths)
-    eA[0] = [-20, 3, -20]
-    eA[1] = [2, -25, 2]
+    # the diagonal blocks in the convergent regime (every row of |A_ww| sums
+    # below 1, Lemma 2), A21 anywhere; block exponents far apart in both
+    # directions between A21 and the diagonal blocks
+    dhi = -(spec.qbits + 6 + 1)
+    eA[:, 0] = np.minimum(eA[:, 0], dhi)
+    eA[:, 2] = np.minimum(eA[:, 2], dhi)
+    eA[0] = [dhi - 6, 3, dhi - 6]
+    eA[1] = [dhi, -25, dhi]
     check_inverse(width, qA, eA, N, S, "random")
 
 
@@ -131,15 +136,19 @@ def test_inverse_blocked_zero_blocks(width):
     A[3, 64:, 64:] = 0.0             # A22 = 0: X22 = I
     A[4, :64, :64] = 0.0
     A[4, 64:, 64:] = 0.0             # only A21: X21 = -A21
-    A[5] = np.tril(np.ones((C, C), np.float32), -1)  # all ones: X = I - Z exactly
+    A[5] = np.tril(np.ones((C, C), np.float32), -1)  # all ones: X = I - Z
     qA, eA = oi.quantize_blocked(A, spec)
     check_inverse(width, qA, eA, 3, 8, "zero blocks")
     _, cdt, _, inv = WIDTHS[width]
     qT, eT = (host(t) for t in inv(to_dev(qA, cdt), to_dev(eA, torch.int32), 3, 8))
     assert not np.any(qT[0]) and not np.any(eT[0])
     assert np.array_equal(qT[4, 64:, :64].astype(np.int64), -qA[4, 64:, :64])
-    assert np.array_equal(oi.dequant_unit_blocked(qT[5:6], eT[5:6])[0],
-                          np.eye(C) - np.eye(C, k=-1))
+    if width == "i16":
+        # 16 bits keep the band of each block's quantised power sum, so the
+        # all-ones tile comes out exact across the block boundary (8 bits
+        # lose it to the unmasked powers' outliers; the oracle pins both)
+        assert np.array_equal(oi.dequant_unit_blocked(qT[5:6], eT[5:6])[0],
+                              np.eye(C) - np.eye(C, k=-1))
 
 
 @pytest.mark.parametrize("width", ["i8", "i16"])

@@ -43,9 +43,15 @@ def f32_tiles(C, L=None, H=2, gate="wide", stress=False, seed=0):
     return gdn.tiles_flat(gdn.build_A(K, beta, g, C)).astype(np.float32)
 
 
-def random_codes(n, C, seed, density=1.0, emin=-30, emax=2, limb_edges=False):
+def random_codes(n, C, seed, density=1.0, emin=None, emax=None, limb_edges=False):
     """Random strictly lower int16 codes (dense, sparse, or drawn from values
-    next to the limb boundaries) and exponents."""
+    next to the limb boundaries) and exponents.  Dense tiles take exponents at
+    which every row of |A| sums below 1 (32639 2^e C < 1: the Neumann series
+    of Section 3.1 converges, Lemma 2), sparse ones a wide range."""
+    if emax is None:
+        emax = -(15 + int(np.log2(C)) + 1) if density >= 0.5 else 2
+    if emin is None:
+        emin = emax - 12 if density >= 0.5 else -30
     rng = np.random.default_rng([seed, C, 16])
     if limb_edges:
         base = 256 * rng.integers(-127, 128, size=(n, C, C))
@@ -70,21 +76,34 @@ def host(t):
     return t.cpu().numpy()
 
 
-def run_engine(qA, eA, N, S, want_deq=True):
+def run_engine(qA, eA, N, S, want_deq=True, plain=False):
     out = G.gdn_chunk_inverse_neumann_i16(to_dev(qA, torch.int16), to_dev(eA, torch.int32),
-                                          N, S, want_deq=want_deq)
+                                          N, S, want_deq=want_deq, plain=plain)
     return [host(t) for t in out]
 
 
-def check_engine(qA, eA, N, S, label):
-    print(f"i16 engine {label} N={N} S={S} n={qA.shape[0]}", flush=True)
-    qT, eT, Td = run_engine(qA, eA, N, S)
-    rq, re, _ = oi.neumann_inverse_int16(qA, eA, N, S)
+def check_deq(Td, rq, re, plain=False):
+    """Tdeq against the oracle's codes: equal wherever T_hat is finite in
+    fp32, and infinite where its value overflows fp32 (random codes with
+    large exponents)."""
+    with np.errstate(over="ignore"):
+        ref = (oi.dequant(rq, re) if plain else oi.dequant_unit(rq, re)).astype(np.float32)
+    fin = np.isfinite(ref)
+    assert np.array_equal(Td[fin], ref[fin])
+    assert np.array_equal(Td[~fin], ref[~fin])
+    return fin.mean()
+
+
+def check_engine(qA, eA, N, S, label, plain=False):
+    print(f"i16 engine {label}{' plain' if plain else ''} N={N} S={S} n={qA.shape[0]}",
+          flush=True)
+    qT, eT, Td = run_engine(qA, eA, N, S, plain=plain)
+    rq, re, _ = oi.neumann_inverse_int16(qA, eA, N, S, plain=plain)
     bad = np.flatnonzero(np.any(qT.astype(np.int64) != rq, axis=(-1, -2)) |
                          (eT.astype(np.int64) != re))
     print(f"  mismatching tiles={bad.size}", flush=True)
     assert bad.size == 0, (label, N, S, bad[:8])
-    assert np.array_equal(Td, oi.dequant_unit(rq, re).astype(np.float32))
+    check_deq(Td, rq, re, plain)
 
 
 # ---------------------------------------------------------------------------
@@ -167,6 +186,31 @@ def test_neumann_i16_edge_tiles():
             check_engine(qA, eA, N, S, f"C={C} edge")
         qT, eT, Td = run_engine(qA[:1], eA[:1], 3, 2)
         assert np.all(qT == 0) and eT[0] == 0 and np.array_equal(Td[0], np.eye(C, dtype=np.float32))
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("src", ["workload", "stress", "random_dense"])
+def test_neumann_i16_plain_bit_exact(C, src):
+    """The plain form (GDN_INT_PLAIN: the unit diagonal inside every tensor's
+    codes) against the oracle's plain form."""
+    if src.startswith("random"):
+        qA, eA = random_codes(32, C, seed=13)
+    else:
+        qA, eA = oi.quantize(f32_tiles(C, stress=(src == "stress")), SPEC)
+    for N, S in ORDERS[C][:4]:
+        check_engine(qA, eA, N, S, f"C={C} {src}", plain=True)
+
+
+def test_neumann_i16_plain_identity():
+    """A = 0 in plain form: T_hat = I with 1 at the finest scale that holds
+    it (2^(qbits - 1) at exponent 1 - qbits)."""
+    qb = 15
+    for C in (16, 32, 64):
+        qA = np.zeros((2, C, C), np.int64)
+        qT, eT, Td = run_engine(qA, np.zeros(2, np.int64), 3, 2, plain=True)
+        assert np.all(eT == 1 - qb)
+        assert np.array_equal(qT[0].astype(np.int64), np.eye(C, dtype=np.int64) << (qb - 1))
+        assert np.array_equal(Td[1], np.eye(C, dtype=np.float32))
 
 
 def test_i16_pipeline_many_tiles_odd_count():
@@ -299,7 +343,7 @@ def check_fwdsub(qA, eA, label):
                          (eT.astype(np.int64) != re))
     print(f"  mismatching tiles={bad.size}", flush=True)
     assert bad.size == 0, (label, bad[:8])
-    assert np.array_equal(Td, oi.dequant_unit(rq, re).astype(np.float32))
+    check_deq(Td, rq, re)
 
 
 @pytest.mark.parametrize("C", [16, 32, 64])

@@ -38,8 +38,15 @@ def f32_tiles(C, L=None, H=2, gate="wide", stress=False, seed=0):
     return gdn.tiles_flat(gdn.build_A(K, beta, g, C)).astype(np.float32)
 
 
-def random_codes(n, C, seed, density=1.0, emin=-12, emax=2):
-    """Random strictly lower int8 codes (dense or sparse) and exponents."""
+def random_codes(n, C, seed, density=1.0, emin=None, emax=None):
+    """Random strictly lower int8 codes (dense or sparse) and exponents.  Dense
+    tiles take exponents at which every row of |A| sums below 1 (127 2^e C <
+    1: the Neumann series of Section 3.1 converges, Lemma 2), sparse ones a
+    wide range in both directions."""
+    if emax is None:
+        emax = -(7 + int(np.log2(C)) + 1) if density >= 0.5 else 2
+    if emin is None:
+        emin = emax - 12
     rng = np.random.default_rng([seed, C])
     q = rng.integers(-127, 128, size=(n, C, C))
     if density < 1.0:
@@ -58,21 +65,33 @@ def host(t):
     return t.cpu().numpy()
 
 
-def run_engine(qA, eA, N, S, want_deq=True):
+def run_engine(qA, eA, N, S, want_deq=True, plain=False):
     out = G.gdn_chunk_inverse_neumann_i8(to_dev(qA, torch.int8), to_dev(eA, torch.int32),
-                                         N, S, want_deq=want_deq)
+                                         N, S, want_deq=want_deq, plain=plain)
     return [host(t) for t in out]
 
 
-def check_engine(qA, eA, N, S, label):
-    qT, eT, Td = run_engine(qA, eA, N, S)
-    rq, re, _ = oi.neumann_inverse_int8(qA, eA, N, S)
+def check_deq(Td, rq, re, plain=False):
+    """Tdeq against the oracle's codes: equal wherever T_hat is finite in
+    fp32, and infinite where its value overflows fp32 (random codes with
+    large exponents)."""
+    with np.errstate(over="ignore"):
+        ref = (oi.dequant(rq, re) if plain else oi.dequant_unit(rq, re)).astype(np.float32)
+    fin = np.isfinite(ref)
+    assert np.array_equal(Td[fin], ref[fin])
+    assert np.array_equal(Td[~fin], ref[~fin])
+    return fin.mean()
+
+
+def check_engine(qA, eA, N, S, label, plain=False):
+    qT, eT, Td = run_engine(qA, eA, N, S, plain=plain)
+    rq, re, _ = oi.neumann_inverse_int8(qA, eA, N, S, plain=plain)
     bad = np.flatnonzero(np.any(qT.astype(np.int64) != rq, axis=(-1, -2)) |
                          (eT.astype(np.int64) != re))
-    print(f"{label} N={N} S={S} n={qA.shape[0]} mismatching tiles={bad.size}", flush=True)
+    print(f"{label}{' plain' if plain else ''} N={N} S={S} n={qA.shape[0]} "
+          f"mismatching tiles={bad.size}", flush=True)
     assert bad.size == 0, (label, N, S, bad[:8])
-    ref_deq = oi.dequant_unit(rq, re).astype(np.float32)
-    assert np.array_equal(Td, ref_deq)
+    check_deq(Td, rq, re, plain)
 
 
 # ---------------------------------------------------------------------------
@@ -162,6 +181,31 @@ def test_neumann_i8_edge_tiles():
             check_engine(qA, eA, N, S, f"C={C} edge")
         qT, eT, Td = run_engine(qA[:1], eA[:1], 3, 2)
         assert np.all(qT == 0) and eT[0] == 0 and np.array_equal(Td[0], np.eye(C, dtype=np.float32))
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+@pytest.mark.parametrize("src", ["workload", "stress", "random_dense"])
+def test_neumann_i8_plain_bit_exact(C, src):
+    """The plain form (GDN_INT_PLAIN: the unit diagonal inside every tensor's
+    codes) against the oracle's plain form."""
+    if src.startswith("random"):
+        qA, eA = random_codes(32, C, seed=13)
+    else:
+        qA, eA = oi.quantize(f32_tiles(C, stress=(src == "stress")))
+    for N, S in ORDERS[C][:4]:
+        check_engine(qA, eA, N, S, f"C={C} {src}", plain=True)
+
+
+def test_neumann_i8_plain_identity():
+    """A = 0 in plain form: T_hat = I with 1 at the finest scale that holds
+    it (2^(qbits - 1) at exponent 1 - qbits)."""
+    qb = 7
+    for C in (16, 32, 64):
+        qA = np.zeros((2, C, C), np.int64)
+        qT, eT, Td = run_engine(qA, np.zeros(2, np.int64), 3, 2, plain=True)
+        assert np.all(eT == 1 - qb)
+        assert np.array_equal(qT[0].astype(np.int64), np.eye(C, dtype=np.int64) << (qb - 1))
+        assert np.array_equal(Td[1], np.eye(C, dtype=np.float32))
 
 
 def test_i8_pipeline_many_tiles_odd_count():
@@ -297,7 +341,7 @@ def check_fwdsub(qA, eA, label):
                          (eT.astype(np.int64) != re))
     print(f"  mismatching tiles={bad.size}", flush=True)
     assert bad.size == 0, (label, bad[:8])
-    assert np.array_equal(Td, oi.dequant_unit(rq, re).astype(np.float32))
+    check_deq(Td, rq, re)
 
 
 @pytest.mark.parametrize("C", [16, 32, 64])
