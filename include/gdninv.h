@@ -366,6 +366,27 @@ int gdn_chunk_forward_state(const void* Q, const float* g, const float* S0, void
                             int L, int H, int dk, int dv, int C, float scale, int dtype,
                             void* stream);
 
+/* gdn_chunk_forward without a caller's workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the workspace between the two
+ * launches is a file-scope device array of GDN_FORWARD_SCRATCH_BYTES that
+ * every device the library runs on holds until the process ends (looked up
+ * on the first call on a device); the call itself allocates nothing.
+ * Arguments, layouts, results (bit for bit) and errors as for
+ * gdn_chunk_forward without workspace and workspace_bytes; sizes whose
+ * workspace (gdn_chunk_forward_workspace) exceeds the array return
+ * GDN_ERR_WORKSPACE before any HIP call (bf16: 2048 chunk tiles of
+ * C = 64, dk = dv = 128 fit).  Every call on a device shares that device's
+ * array: calls that overlap in time on one device (two streams, two host
+ * threads) race and must be serialised by the caller.  The array keeps the
+ * last call's contents; nothing in it needs to start at zero (each call's
+ * first launch writes every byte its second launch reads). */
+#define GDN_FORWARD_SCRATCH_BYTES ((int64_t)128 << 20)
+int gdn_chunk_forward_noalloc(const void* Q, const void* K, const void* V, const float* beta,
+                              const float* g, const float* S0, void* O, float* S_final, int B,
+                              int L, int H, int dk, int dv, int C, int N, int S, int exact,
+                              float scale, int dtype, void* stream);
+
 /* Workspace bytes gdn_chunk_forward needs for these sizes (0 when there is
  * no chunk); GDN_ERR_SHAPE / GDN_ERR_DTYPE / GDN_ERR_NULL as for the call. */
 int gdn_chunk_forward_workspace(int B, int L, int H, int dk, int dv, int C, int dtype,

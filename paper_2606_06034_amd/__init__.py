@@ -21,7 +21,9 @@ from ._binding import (  # noqa: F401
     gdn_abi_version,
     gdn_build_A,
     gdn_chunk_forward,
+    gdn_chunk_forward_noalloc,
     gdn_chunk_forward_prepare,
+    GDN_FORWARD_SCRATCH_BYTES,
     gdn_chunk_forward_state,
     gdn_chunk_forward_varlen,
     gdn_chunk_forward_workspace,

@@ -45,6 +45,9 @@ _SIGS = {
     "gdn_chunk_forward": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _c_int, _c_int,
                           _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_float,
                           _c_int, _vp],
+    "gdn_chunk_forward_noalloc": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int,
+                                  _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                  ctypes.c_float, _c_int, _vp],
     "gdn_chunk_forward_varlen": [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _vp, _vp,
                                  _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
                                  _c_int, _c_int, ctypes.c_float, _c_int, _vp],
@@ -491,6 +494,38 @@ def gdn_chunk_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, beta: t
         _dev(O, "O", K.dtype, tok * dv), fp, _dev(workspace, "workspace"), workspace.numel() *
         workspace.element_size(), B, L, H, dk, dv, C, N, S, _fwd_mode(exact, inverse), scale,
         dt, _stream(stream)))
+    return O, S_final
+
+
+GDN_FORWARD_SCRATCH_BYTES = 128 << 20  # the allocation-free forward's scratch
+
+
+def gdn_chunk_forward_noalloc(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                              beta: torch.Tensor, g: torch.Tensor, C: int, O: torch.Tensor,
+                              S0: Optional[torch.Tensor] = None,
+                              S_final: Optional[torch.Tensor] = None, N: Optional[int] = None,
+                              S: Optional[int] = None, exact: bool = False,
+                              scale: Optional[float] = None, stream=None,
+                              inverse: Optional[str] = None):
+    """gdn_chunk_forward with the library's device scratch as its workspace:
+    the call allocates nothing (O and, when wanted, S_final are the caller's).
+    Returns (O, S_final)."""
+    B, L, H, dk = K.shape
+    dv = V.shape[-1]
+    dt = _fdtype(K, "K")
+    if N is None or S is None:
+        dn, ds = gdn_default_order(C) if C in (16, 32, 64, 128) else (0, 0)
+        N = dn if N is None else N
+        S = ds if S is None else S
+    scale = dk ** -0.5 if scale is None else float(scale)
+    tok = B * L * H
+    sp = _dev(S0, "S0", torch.float32, B * H * dk * dv) if S0 is not None else None
+    fp = _dev(S_final, "S_final", torch.float32, B * H * dk * dv) if S_final is not None else None
+    _check("gdn_chunk_forward_noalloc", lib.gdn_chunk_forward_noalloc(
+        _dev(Q, "Q", K.dtype, tok * dk), _dev(K, "K"), _dev(V, "V", K.dtype, tok * dv),
+        _dev(beta, "beta", torch.float32, tok), _dev(g, "g", torch.float32, tok), sp,
+        _dev(O, "O", K.dtype, tok * dv), fp, B, L, H, dk, dv, C, N, S,
+        _fwd_mode(exact, inverse), scale, dt, _stream(stream)))
     return O, S_final
 
 

@@ -554,6 +554,23 @@ int gdn_chunk_forward(const void* Q, const void* K, const void* V, const float* 
                  C, N, S, exact, scale, dtype, 3, stream);
 }
 
+int gdn_chunk_forward_noalloc(const void* Q, const void* K, const void* V, const float* beta,
+                              const float* g, const float* S0, void* O, float* S_final, int B,
+                              int L, int H, int dk, int dv, int C, int N, int S, int exact,
+                              float scale, int dtype, void* stream) {
+  static_assert(gdn::kForwardScratchBytes == GDN_FORWARD_SCRATCH_BYTES, "scratch size");
+  // sizes first: a call that cannot fit the scratch fails before any HIP call
+  int64_t need = 0;
+  if (int r = gdn_chunk_forward_workspace(B, L, H, dk, dv, C, dtype, &need)) return r;
+  if (need > gdn::kForwardScratchBytes) return GDN_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (need > 0) {
+    if (gdn::forward_scratch(&ws) != hipSuccess) return GDN_ERR_HIP;
+  }
+  return forward(Q, K, V, beta, g, S0, O, S_final, ws, gdn::kForwardScratchBytes, B, L, H, dk,
+                 dv, C, N, S, exact, scale, dtype, 3, stream);
+}
+
 int gdn_chunk_forward_prepare(const void* Q, const void* K, const void* V, const float* beta,
                               const float* g, void* workspace, int64_t workspace_bytes, int B,
                               int L, int H, int dk, int dv, int C, int N, int S, int exact,

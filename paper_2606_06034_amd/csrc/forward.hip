@@ -31,6 +31,7 @@
 //   dk = 32 q' + 8 g + 4 h' + v,
 // so that the pair (block 2q', block 2q' + 1) lines up with a run of 8
 // features of W and Q rows.
+#include <mutex>
 #include <type_traits>
 
 #include "int16_ops.hpp"
@@ -605,6 +606,37 @@ __global__ __launch_bounds__(256) void k_fwd_state(const TIO* __restrict__ ws,
       for (int v = 0; v < 4; ++v)
         Sfin[sbase + (int64_t)(32 * wv + 8 * gq + 4 * hf + v) * DV + dvcol] = st[hf][v];
   }
+}
+
+// ---------------------------------------------------------------------------
+// The scratch of the allocation-free layer forward (gdn_chunk_forward_noalloc):
+// the workspace between the two launches, held in a file-scope device array
+// of kForwardScratchBytes that every device the library runs on keeps until
+// the process ends.  In host code the array's name is only a stand-in for
+// its device address: forward_scratch() looks that address up once per
+// device (hipGetSymbolAddress with the device current) and hands it out, and
+// only that address is ever passed to a kernel.
+
+static __device__ __align__(256) unsigned char scratch[kForwardScratchBytes];
+
+hipError_t forward_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 // ---------------------------------------------------------------------------

@@ -76,4 +76,9 @@ hipError_t launch_inverse_i16_fused(const void* K, const float* beta, const floa
                                     int16_t* Tq, int32_t* eT, float* Tdeq, int B, int L, int H,
                                     int dk, int C, int N, int S, int k_dtype, hipStream_t st);
 
+// the allocation-free layer forward's scratch: its size, and its device
+// address on the current device (looked up once per device)
+constexpr int64_t kForwardScratchBytes = int64_t(128) << 20;
+hipError_t forward_scratch(void** ptr);
+
 }  // namespace gdn

@@ -25,7 +25,7 @@ def _declared():
 
 def test_exports_every_declared_symbol():
     names = _declared()
-    assert len(names) == 24
+    assert len(names) == 25
     for n in names:
         assert hasattr(g.lib, n), n
     assert sorted(g.abi_symbols()) == names
@@ -451,3 +451,17 @@ def test_grid_limit_chunked_entry_points():
     assert LIM128 + 1 == 2 ** 25
     assert f(P1, P2, P3, BIG, 2 * BIG, 3 * BIG, None, 1, 128 * 2 ** 15, 2 ** 10, 128, 128, 128,
              3, 8, 1, None) == SHAPE
+
+
+def test_noalloc_forward_size_limit():
+    # sizes whose workspace exceeds the static scratch fail before any HIP
+    # call: 2428 bf16 tiles of C = 64, dk = dv = 128 need 134,258,688 bytes
+    assert g.GDN_FORWARD_SCRATCH_BYTES == 128 << 20
+    f = L.gdn_chunk_forward_noalloc
+    # Q, K, V, beta, g, S0, O, S_final, B, L, H, dk, dv, C, N, S, exact, scale, dtype, stream
+    assert f(P1, P2, P3, P4, P5, None, P6, None, 1, 64 * 2428, 1, 128, 128, 64, 3, 8, 0, 0.1, 1,
+             None) == WS
+    assert f(P1, P2, P3, P4, P5, None, P6, None, 1, 100, 1, 128, 128, 64, 3, 8, 0, 0.1, 1,
+             None) == SHAPE
+    assert f(None, None, None, None, None, None, None, None, 0, 64, 1, 128, 128, 64, 3, 8, 0, 0.1,
+             1, None) == OK
