@@ -191,6 +191,16 @@ template <int NB> struct I16Ops {
   static __device__ __forceinline__ void to_col(Col& Y, const AccI<NB>& D, int lo, int hi) {
     to_coll(Y, D, lo, hi);
   }
+  // the codes 256 h + l of the blocks of X that can meet [lo, hi] (others 0)
+  static __device__ __forceinline__ void codes(AccI<NB>& D, const Row& X, int lo, int hi) {
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        D.a[bidx(I, J)] = blk_nz(I - J, lo, hi)
+                              ? unpack4(X.h.r[I].v[J]) * 256 + unpack4(X.l.r[I].v[J])
+                              : zero_i4();
+  }
   template <bool OUTQ>
   static __device__ __forceinline__ void mm(Prod& D, const Row& X, const Col& Y, int lo, int hi) {
     mml<NB, OUTQ>(D, X, Y, lo, hi);

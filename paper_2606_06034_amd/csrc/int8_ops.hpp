@@ -81,6 +81,14 @@ template <int NB> struct I8Ops {
   static __device__ __forceinline__ void to_col(Col& Y, const AccI<NB>& D, int lo, int hi) {
     to_colq(Y, D, lo, hi);
   }
+  // the codes of the blocks of X that can meet [lo, hi] (others 0)
+  static __device__ __forceinline__ void codes(AccI<NB>& D, const Row& X, int lo, int hi) {
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        D.a[bidx(I, J)] = blk_nz(I - J, lo, hi) ? unpack4(X.r[I].v[J]) : zero_i4();
+  }
   template <bool OUTQ>
   static __device__ __forceinline__ void mm(Prod& D, const Row& X, const Col& Y, int lo, int hi) {
     mmi<NB, OUTQ>(D, X, Y, lo, hi);

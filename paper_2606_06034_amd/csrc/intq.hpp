@@ -412,6 +412,33 @@ __device__ __forceinline__ Term<T> no_term(const T& t) {
   return Term<T>{&t, 0, 0, 1, 0, 0, false};
 }
 
+// Is every column sum of |E| (codes of a lower matrix in row form, band
+// [lo, C-1], exponent e) at most 1?  Then |(P E)_ij| <= max|P| for any P,
+// so each residual power is bounded by the one before it.  Lane (g, c) of
+// a row-form block holds row c, columns 4g + v: the sum over a block's rows
+// runs over the 16 lanes of one g (xor-shuffles 1, 2, 4, 8), the sum over
+// block rows in the lane.
+template <int NB>
+__device__ __forceinline__ bool colsum_at_most_one(const AccI<NB>& E, int e, int lo) {
+  int best = 0;
+#pragma unroll
+  for (int J = 0; J < NB; ++J)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      int sacc = 0;
+#pragma unroll
+      for (int I = J; I < NB; ++I)
+        if (blk_nz(I - J, lo, 16 * NB - 1)) sacc += abs(E.a[bidx(I, J)][v]);
+#pragma unroll
+      for (int d = 1; d < 16; d <<= 1) sacc += __shfl_xor(sacc, d);
+      best = max(best, sacc);
+    }
+  const int m = wave_max(best);
+  if (m == 0) return true;
+  if (e >= 0) return m <= 1 && e == 0;
+  return -e >= 30 || m <= (1 << -e);
+}
+
 // identity codes (1 on the diagonal, exponent 0)
 template <int NB>
 __device__ __forceinline__ void eye_codes(AccI<NB>& D) {
@@ -446,8 +473,9 @@ __device__ __forceinline__ void eye_codes(AccI<NB>& D) {
 // Ops<NB> supplies one code width: fragment types Row, Col (operands in row
 // and column form) and Prod (an exact product); kQ, kQB (the code range and
 // its bits), kAccB (log2 bound of a product's magnitude); to_row, to_col
-// (codes to fragments), mm<OUTQ> (exact product, blocks outside a band
-// zero), requant (a product to codes by the scale rule), canon (codes to the
+// (codes to fragments), codes (fragments back to codes), mm<OUTQ> (exact
+// product, blocks outside a band zero), requant (a product to codes by the
+// scale rule), canon (codes to the
 // finest scale that holds them), add (q of the sum of two tensors of codes,
 // the first known to be at its finest scale or not),
 // row_to_col (column-form fragments of a row-form one, through the
@@ -555,19 +583,30 @@ __device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, 
     int eP = eE;
     bool nzP = nzE;
     typename O::Row PRq = ERq;
+    // Once a residual power adds nothing to T (its exponent 2 QB + 3 or
+    // more under T's, so the add leaves T's codes as they are) and every
+    // column sum of |E| is at most 1, every later power is no larger, its
+    // exponent no higher, and its add leaves T as it is too: the chain
+    // stops there with the result it would have reached.
+    const bool contracting = colsum_at_most_one(E, eE, E0);
+    bool done = false;
     auto chain = [&](int s) {
+      if (done) return;
       const int lo = PLAIN ? 0 : s;
       typename O::Prod D;
       O::template mm<true>(D, PRq, ECq, lo, C - 1);
       O::requant(D, P, lo, C - 1, eP + eE, eP, nzP);
+      const bool idle = !nzP || (nzR && eR - eP >= 2 * QB + 3);
       O::add(R, eR, nzR, U0, true, P, eP, nzP, 1, lo, U0, C - 1);
-      O::to_row(PRq, P, lo, C - 1);
+      done = idle && contracting;
+      if (!done) O::to_row(PRq, P, lo, C - 1);
     };
-    if constexpr (SC >= 0) {
-#pragma unroll
-      for (int s = 2; s <= SC; ++s) chain(s);
-    } else {
-      for (int s = 2; s <= S; ++s) chain(s);
+    // a rolled loop: unrolled, the early exit keeps every iteration's
+    // operands live at once and costs a wave per SIMD
+#pragma unroll 1
+    for (int s = 2; s <= S; ++s) {
+      chain(s);
+      if (done) break;
     }
   }
 
@@ -580,6 +619,10 @@ __device__ __forceinline__ void int_engine(const AccI<NB>& Lr, int eL, int Nrt, 
   }
   typename O::Prod D;
   O::template mm<true>(D, T0Rq, RCq, PLAIN ? 0 : 2, C - 1);
+  // T0's codes again, from its row fragments (they hold every code exactly;
+  // keeping the unpacked copy alive across the residual chain would cost a
+  // wave per SIMD)
+  O::codes(T0, T0Rq, U0, N);
   if constexpr (!PLAIN) {
     bool nzT;
     exact_sum<Q, QB, NB>(Tr, eTo, nzT, term(T0, eT0, QB, 1, 1, N, nzT0),
