@@ -392,17 +392,130 @@ hipError_t launch_quantize_i16(const float* A, int16_t* Aq, int32_t* eA, int64_t
   return hipErrorNotSupported;
 }
 
+namespace i16 {
+
+// C = 16, 32: 64 / C tiles per wave (no idle lanes), the same arithmetic:
+// lane l takes column l % C of tile l / C; the wave's codes are staged in
+// LDS (coalesced 32-bit loads), a row of a tile is read four codes per LDS
+// read, and the wave-wide maxima and "any" tests of the one-tile kernel are
+// taken over the C lanes of a tile (xor-shuffles inside aligned groups).
+template <int C>
+__device__ __forceinline__ int group_max(int x) {
+#pragma unroll
+  for (int d = 1; d < C; d <<= 1) x = max(x, __shfl_xor(x, d));
+  return x;
+}
+
+template <int C, typename CODE>
+__global__ __launch_bounds__(64) void k_fwdsub_int_packed(const CODE* __restrict__ Aq,
+                                                          const int32_t* __restrict__ eA,
+                                                          CODE* __restrict__ Tq,
+                                                          int32_t* __restrict__ eT,
+                                                          float* __restrict__ Tdeq,
+                                                          int64_t n_tiles) {
+  using Q = IntCodes<CODE>;
+  constexpr int P = 64 / C, PW = 4 / (int)sizeof(CODE);  // tiles per wave, codes per word
+  constexpr int ACCB = 2 * Q::qbits + (C == 16 ? 4 : 5);  // |t X| < C 2^(2 qbits)
+  __shared__ __attribute__((aligned(16))) int sa[P * C * C];
+  const int l = threadIdx.x;
+  const int64_t tile0 = (int64_t)blockIdx.x * P;
+  const int64_t here = n_tiles - tile0 < P ? n_tiles - tile0 : P;
+#pragma unroll
+  for (int r = 0; r < (P * C * C) / (64 * PW); ++r) {
+    const int w = r * 64 + l, idx = w * PW;  // word of the wave's tiles, its first code
+    const uint32_t v = idx / (C * C) < here
+                           ? reinterpret_cast<const uint32_t*>(Aq + tile0 * (C * C))[w]
+                           : 0u;
+#pragma unroll
+    for (int u = 0; u < PW; ++u)
+      sa[idx + u] = PW == 4 ? (int)(int8_t)(v >> (8 * u)) : (int)(int16_t)(v >> (16 * u));
+  }
+  __syncthreads();
+  const int q = l / C, j = l % C;
+  const bool live = q < here;
+  const int* ar = sa + q * (C * C);
+  const int ea = live ? eA[tile0 + q] : 0;
+  int ex = ea;
+  int x[C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) x[k] = 0;
+  bool anyX = false;
+#pragma unroll
+  for (int i = 1; i < C; ++i) {
+    int row[C];
+#pragma unroll
+    for (int k0 = 0; k0 < i; k0 += 4) {
+      const i32x4 r4 = *(const i32x4*)(ar + i * C + k0);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) row[k0 + u] = r4[u];
+    }
+    const int tj = j < i ? -ar[i * C + j] : 0;
+    double p = 0.0;
+#pragma unroll
+    for (int k = 1; k < i; k += 2) {
+      int s2 = __mul24(-row[k], x[k]);
+      if (k + 1 < i) s2 += __mul24(-row[k + 1], x[k + 1]);
+      p += (double)s2;
+    }
+    // aligned sum of t (first) and t X (a zero row gives acc = 0, no
+    // exponent growth and a zero row of codes, as the one-tile kernel's skip)
+    int es = ea + Q::qbits - Q::align;
+    double acc = (double)tj * (double)(1 << (Q::align - Q::qbits));
+    if (anyX) {
+      const int top = ea + ex + ACCB - Q::align;
+      if (top > es) {
+        acc = rint(acc * ldexp(1.0, es - top));
+        es = top;
+      }
+      const int sh = ea + ex - es;
+      acc += sh >= 0 ? p * ldexp(1.0, sh) : rint(p * ldexp(1.0, sh));
+    }
+    const int amax_hi = group_max<C>(__double2hiint(fabs(acc)));
+    if (amax_hi > 0) {
+      int pe;
+      const double m = frexp(__hiloint2double(amax_hi, 0), &pe);
+      const int sft = max(0, pe - Q::qbits + (m * (double)(1 << Q::qbits) >= Q::qhalf ? 1 : 0) -
+                                 (ex - es));
+      if (sft > 0) {
+        int nz = 0;
+#pragma unroll
+        for (int k = 1; k < i; ++k) {
+          x[k] = rne_code(x[k], sft);
+          nz |= x[k];
+        }
+        ex += sft;
+        anyX = group_max<C>(nz != 0 ? 1 : 0) != 0;
+      }
+    }
+    x[i] = (int)rint(acc * ldexp(1.0, es - ex));
+    anyX = anyX || group_max<C>(x[i] != 0 ? 1 : 0) != 0;
+  }
+  if (live) {
+    CODE* t = Tq + (tile0 + q) * (C * C);
+#pragma unroll
+    for (int i = 0; i < C; ++i) t[i * C + j] = (CODE)x[i];
+    if (Tdeq) {
+      float* td = Tdeq + (tile0 + q) * (C * C);
+#pragma unroll
+      for (int i = 0; i < C; ++i) td[i * C + j] = i == j ? 1.f : ldexpf((float)x[i], ex);
+    }
+    if (j == 0) eT[tile0 + q] = ex;
+  }
+}
+
+}  // namespace i16
+
 template <typename CODE>
 static hipError_t run_fwdsub_int(const CODE* Aq, const int32_t* eA, CODE* Tq, int32_t* eT,
                                  float* Tdeq, int64_t n, int C, hipStream_t st) {
   switch (C) {
     case 16:
-      hipLaunchKernelGGL((i16::k_fwdsub_int<16, CODE>), dim3((unsigned)n), dim3(64), 0, st, Aq,
-                         eA, Tq, eT, Tdeq);
+      hipLaunchKernelGGL((i16::k_fwdsub_int_packed<16, CODE>), dim3((unsigned)((n + 3) / 4)),
+                         dim3(64), 0, st, Aq, eA, Tq, eT, Tdeq, n);
       return hipGetLastError();
     case 32:
-      hipLaunchKernelGGL((i16::k_fwdsub_int<32, CODE>), dim3((unsigned)n), dim3(64), 0, st, Aq,
-                         eA, Tq, eT, Tdeq);
+      hipLaunchKernelGGL((i16::k_fwdsub_int_packed<32, CODE>), dim3((unsigned)((n + 1) / 2)),
+                         dim3(64), 0, st, Aq, eA, Tq, eT, Tdeq, n);
       return hipGetLastError();
     case 64:
       hipLaunchKernelGGL((i16::k_fwdsub_int<64, CODE>), dim3((unsigned)n), dim3(64), 0, st, Aq,

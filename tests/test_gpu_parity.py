@@ -431,6 +431,85 @@ def test_sweep_c128_full_size_sampled():
     _sampled_check("sweep", C=128)
 
 
+def test_long_context_full_size_sampled():
+    """The long-context workload the bench times (B=1, H=32, L=131072, C=64,
+    bf16: 65536 tiles) in one fused launch, sampled tiles against the oracle;
+    then the inverse alone, the exact block-wise inverse and forward
+    substitution on the same 65536 A tiles (the same-shape comparison the
+    bench reports), sampled against the oracle's T_hat and exact inverse."""
+    _sampled_check("long_context", n_sample=24, seed=4)
+    w = wl.workload("long_context")
+    C = w.C
+    n = w.B * w.H * (w.L // C)
+    rng = np.random.default_rng(5)
+    picks = sorted(set(rng.integers(0, n, 16).tolist()) | {0, n - 1})
+    K, beta, g, _ = wl.gen_inputs(w, C=C, want_v=False)
+    dA = G.gdn_build_A(dev(K, "bf16"), dev(beta), dev(g), C, a_dtype=torch.bfloat16)
+    del K
+    T = G.gdn_chunk_inverse_neumann(dA, 3, 8)
+    X = G.gdn_chunk_inverse_fwdsub(dA)
+    Xb = G.gdn_chunk_inverse_blockwise(dA)
+    torch.cuda.synchronize()
+    Av = dA.view(-1, C, C)
+    for t in picks:
+        A = Av[t].float().cpu().numpy().astype(np.float64)[None]
+        assert maxerr(host(T.view(-1, C, C)[t])[None], gdn.neumann_inverse(A, 3, 8)) <= TOL["bf16"]
+        Xr = gdn.forward_substitution_inverse(A)
+        assert maxerr(host(X.view(-1, C, C)[t])[None], Xr) <= TOL["bf16"], t
+        assert maxerr(host(Xb.view(-1, C, C)[t])[None], Xr) <= TOL["bf16"], t
+    print(f"long_context same-shape inverses: {len(picks)} sampled tiles", flush=True)
+
+
+# ---------------------------------------------------------------------------
+# non-finite inputs
+
+
+def test_nonfinite_inputs_stay_in_their_tile():
+    """A NaN or an infinity in the strictly lower part of a tile of A makes
+    that tile's inverse non-finite at the same position (T_ij carries -A_ij
+    through T0 on the band i - j <= N, through E beyond it) and leaves every
+    other tile exactly as it is without it; NaN/Inf above the diagonal are
+    never read.  The same holds for forward substitution and the exact
+    block-wise inverse."""
+    bad = [(0, None, None, np.nan), (1, 5, 2, np.inf), (2, 3, 1, -np.inf)]
+    for C in (16, 32, 64, 128):
+        A = stored(gdn_tiles(C, n_heads=1), "f32")[:6]
+        B = A.copy()
+        cells = []
+        for k, i, j, v in bad:
+            i = C - 1 if i is None else i
+            j = 0 if j is None else j
+            B[k, i, j] = v
+            cells.append((k, i, j))
+        B[3, 0, C - 1] = np.nan  # above the diagonal: ignored
+        for dt in ("f32", "bf16"):
+            for name, fn in (("neumann", lambda x: G.gdn_chunk_inverse_neumann(x, 3, 2 if C == 16 else 8)),
+                             ("fwdsub", G.gdn_chunk_inverse_fwdsub),
+                             ("blockwise", G.gdn_chunk_inverse_blockwise)):
+                clean = host(fn(dev(A, dt) if dt == "f32" else dev(stored(A, dt), dt)))
+                got = host(fn(dev(B, dt) if dt == "f32" else dev(B, dt)))
+                for k, i, j in cells:
+                    assert not np.isfinite(got[k, i, j]), (C, dt, name, k)
+                assert np.array_equal(got[3:], clean[3:]), (C, dt, name)
+    # the fused path: a NaN in one token's key reaches W and U of its own
+    # chunk and head only
+    C = 64
+    w = wl.workload("tiny").with_(B=1, L=4 * C, H=2, dtype="bf16")
+    K, beta, g, V = wl.gen_inputs(w, C=C)
+    Kb = K.copy()
+    Kb[0, C + 5, 1, 7] = np.nan  # chunk 1 of head 1
+    outs = []
+    for KK in (K, Kb):
+        W, U = G.gdn_chunk_wy_fused(dev(KK, "bf16"), dev(V, "bf16"), dev(beta), dev(g), C, 3, 8)
+        outs.append((host(W), host(U)))
+    (W0, U0), (W1, U1) = outs
+    sl = slice(C, 2 * C)
+    assert not np.all(np.isfinite(W1[0, sl, 1])) and not np.all(np.isfinite(U1[0, sl, 1]))
+    mask = np.ones(W0.shape[:3], bool)
+    mask[0, sl, 1] = False
+    assert np.array_equal(W1[mask], W0[mask]) and np.array_equal(U1[mask], U0[mask])
+
+
 def test_binding_rejects_wrong_sizes():
     """Caller-supplied tensors of the wrong element count never reach a kernel."""
     A = torch.zeros((4, 64, 64), device="cuda")
