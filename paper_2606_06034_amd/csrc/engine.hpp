@@ -67,17 +67,26 @@ __device__ __forceinline__ bool in_t0_band(int m, int N) {
 // times 1 plus zeros) instead of 2-byte gathers from memory: 9 % less time
 // for the standalone inverse at C = 64 on MI355X.  Entries on and above the
 // diagonal are taken as 0.
-template <int NB, typename F, bool SMALLN, typename TIO>
-__device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int ldr, int N,
-                                                Acc<NB>& Lr, Acc<NB>& Lc) {
+// the lower-triangle blocks of a tile as read (row form), for callers that
+// issue several tiles' loads before computing on the first
+template <int NB, typename TIO>
+__device__ __forceinline__ void load_lower_raw(const TIO* __restrict__ a, int ldr, Acc<NB>& R) {
   const int g = lane_g(), c = lane_c();
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J) R.a[bidx(I, J)] = load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g);
+}
+
+template <int NB, typename F, bool SMALLN>
+__device__ __forceinline__ void neg_strict_from(const Acc<NB>& R, int N, Acc<NB>& Lr,
+                                                Acc<NB>& Lc) {
   const Pair<F> Ic = Pair<F>::make(eye4(), zero4());
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J) {
-      const f32x4 r = load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g);
-      Lr.a[bidx(I, J)] = band_block<false>(-r, I - J, 1, 16 * NB);
+      Lr.a[bidx(I, J)] = band_block<false>(-R.a[bidx(I, J)], I - J, 1, 16 * NB);
       Lc.a[bidx(I, J)] =
           in_t0_band<SMALLN>(I - J, N)
               ? Pair<F>::template mma<false>(Pair<F>::make(Lr.a[bidx(I, J)], zero4()), Ic, zero4())
@@ -85,17 +94,30 @@ __device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int l
     }
 }
 
+template <int NB, typename F, bool SMALLN, typename TIO>
+__device__ __forceinline__ void load_neg_strict(const TIO* __restrict__ a, int ldr, int N,
+                                                Acc<NB>& Lr, Acc<NB>& Lc) {
+  Acc<NB> R;
+  load_lower_raw<NB>(a, ldr, R);
+  neg_strict_from<NB, F, SMALLN>(R, N, Lr, Lc);
+}
+
 // Lm = -A as row-form blocks only
-template <int NB, typename TIO>
-__device__ __forceinline__ void load_neg_strict_row(const TIO* __restrict__ a, int ldr,
-                                                    Acc<NB>& Lr) {
-  const int g = lane_g(), c = lane_c();
+template <int NB>
+__device__ __forceinline__ void neg_strict_row_from(const Acc<NB>& R, Acc<NB>& Lr) {
 #pragma unroll
   for (int I = 0; I < NB; ++I)
 #pragma unroll
     for (int J = 0; J <= I; ++J)
-      Lr.a[bidx(I, J)] =
-          band_block<false>(-load4(a + (I * 16 + c) * ldr + J * 16 + 4 * g), I - J, 1, 16 * NB);
+      Lr.a[bidx(I, J)] = band_block<false>(-R.a[bidx(I, J)], I - J, 1, 16 * NB);
+}
+
+template <int NB, typename TIO>
+__device__ __forceinline__ void load_neg_strict_row(const TIO* __restrict__ a, int ldr,
+                                                    Acc<NB>& Lr) {
+  Acc<NB> R;
+  load_lower_raw<NB>(a, ldr, R);
+  neg_strict_row_from<NB>(R, Lr);
 }
 
 // Store a unit lower-triangular tile from its row-form blocks (diagonal

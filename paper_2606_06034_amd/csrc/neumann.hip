@@ -13,31 +13,56 @@ namespace gdn {
 // standalone tiles, the power chain inside the C = 128 kernel (measured
 // faster there, where the merge adds to the register load).  EXACT: the
 // exact block-wise inverse instead of T_hat(N, S).
-template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO, bool GH = true,
-          bool EXACT = false>
-__device__ __forceinline__ void invert_block(const TIO* __restrict__ a, TIO* __restrict__ t,
-                                             int ldr, int N, int S, Acc<NB>& Tr) {
+// the inverse of a tile whose lower-triangle blocks R are already loaded
+template <int NB, typename F, bool SMALLN, int NC, int SC, bool GH = true, bool EXACT = false>
+__device__ __forceinline__ void invert_loaded(const Acc<NB>& R, int N, int S, Acc<NB>& Tr) {
   if constexpr (EXACT) {
     Acc<NB> Lr;
-    load_neg_strict_row<NB>(a, ldr, Lr);
+    neg_strict_row_from<NB>(R, Lr);
     blockwise_inverse<NB, F>(Lr, Tr);
   } else {
     Acc<NB> Lr, Lc;
-    load_neg_strict<NB, F, SMALLN>(a, ldr, NC >= 0 ? NC : N, Lr, Lc);
+    neg_strict_from<NB, F, SMALLN>(R, NC >= 0 ? NC : N, Lr, Lc);
     RowP<NB, F> LR;
     to_rowp(LR, Lr);
     neumann_engine<NB, F, SMALLN, NC, SC, GH>(LR, Lc, N, S, Tr);
   }
+}
+
+template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO, bool GH = true,
+          bool EXACT = false>
+__device__ __forceinline__ void invert_block(const TIO* __restrict__ a, TIO* __restrict__ t,
+                                             int ldr, int N, int S, Acc<NB>& Tr) {
+  Acc<NB> R;
+  load_lower_raw<NB>(a, ldr, R);
+  invert_loaded<NB, F, SMALLN, NC, SC, GH, EXACT>(R, N, S, Tr);
   store_unit_row<NB>(t, ldr, Tr);
 }
 
-template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO>
+// Tiles per wave: at C = 16, 32 one tile moves only 4 or 8 elements per
+// lane, too few bytes in flight to cover HBM latency; a wave then issues
+// the loads of several tiles before it computes on the first.
+template <int NB> struct TilesPerWave { static constexpr int W = NB == 1 ? 4 : NB == 2 ? 2 : 1; };
+template <int NB> dim3 tile_grid(int64_t n) {
+  return dim3((unsigned)((n + TilesPerWave<NB>::W - 1) / TilesPerWave<NB>::W));
+}
+
+template <int NB, typename F, bool SMALLN, int NC, int SC, typename TIO, bool EXACT = false>
 __global__ __launch_bounds__(64) void k_neumann(const TIO* __restrict__ A, TIO* __restrict__ T,
-                                                int N, int S) {
-  constexpr int C = 16 * NB;
-  const int64_t tile = blockIdx.x;
-  Acc<NB> Tr;
-  invert_block<NB, F, SMALLN, NC, SC>(A + tile * (C * C), T + tile * (C * C), C, N, S, Tr);
+                                                int64_t n, int N, int S) {
+  constexpr int C = 16 * NB, W = TilesPerWave<NB>::W;
+  const int64_t tile0 = (int64_t)blockIdx.x * W;
+  Acc<NB> R[W];
+#pragma unroll
+  for (int w = 0; w < W; ++w)
+    if (W == 1 || tile0 + w < n) load_lower_raw<NB>(A + (tile0 + w) * (C * C), C, R[w]);
+#pragma unroll
+  for (int w = 0; w < W; ++w)
+    if (W == 1 || tile0 + w < n) {
+      Acc<NB> Tr;
+      invert_loaded<NB, F, SMALLN, NC, SC, true, EXACT>(R[w], N, S, Tr);
+      store_unit_row<NB>(T + (tile0 + w) * (C * C), C, Tr);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -130,15 +155,16 @@ template <> struct DefaultOrder<4> { static constexpr int N = 3, S = 8; };
 template <int NB, typename F, typename TIO>
 static hipError_t run_neumann(const void* A, void* T, int64_t n, int N, int S, hipStream_t st) {
   constexpr int DN = DefaultOrder<NB>::N, DS = DefaultOrder<NB>::S;
+  const dim3 grid = tile_grid<NB>(n), block(64);
   if (N == DN && S == DS)
-    hipLaunchKernelGGL((k_neumann<NB, F, true, DN, DS, TIO>), dim3((unsigned)n), dim3(64), 0, st,
-                       (const TIO*)A, (TIO*)T, N, S);
+    hipLaunchKernelGGL((k_neumann<NB, F, true, DN, DS, TIO>), grid, block, 0, st, (const TIO*)A,
+                       (TIO*)T, n, N, S);
   else if (N <= 15)
-    hipLaunchKernelGGL((k_neumann<NB, F, true, -1, -1, TIO>), dim3((unsigned)n), dim3(64), 0, st,
-                       (const TIO*)A, (TIO*)T, N, S);
+    hipLaunchKernelGGL((k_neumann<NB, F, true, -1, -1, TIO>), grid, block, 0, st, (const TIO*)A,
+                       (TIO*)T, n, N, S);
   else
-    hipLaunchKernelGGL((k_neumann<NB, F, false, -1, -1, TIO>), dim3((unsigned)n), dim3(64), 0,
-                       st, (const TIO*)A, (TIO*)T, N, S);
+    hipLaunchKernelGGL((k_neumann<NB, F, false, -1, -1, TIO>), grid, block, 0, st, (const TIO*)A,
+                       (TIO*)T, n, N, S);
   return hipGetLastError();
 }
 
@@ -175,23 +201,23 @@ hipError_t launch_neumann(const void* A, void* T, int64_t n, int C, int N, int S
 // exact block-wise inverse (C <= 64 one engine call; C = 128 two 64-blocks and
 // the merge above)
 
-template <int NB, typename F, typename TIO>
-__global__ __launch_bounds__(64) void k_blockwise(const TIO* __restrict__ A, TIO* __restrict__ T) {
-  constexpr int C = 16 * NB;
-  const int64_t tile = blockIdx.x;
-  Acc<NB> Tr;
-  invert_block<NB, F, true, 0, 0, TIO, true, true>(A + tile * (C * C), T + tile * (C * C), C, 0,
-                                                   0, Tr);
-}
-
 template <typename F, typename TIO>
 static hipError_t run_blockwise(const void* A, void* T, int64_t n, int C, hipStream_t st) {
   const TIO* a = (const TIO*)A;
   TIO* t = (TIO*)T;
   switch (C) {
-    case 16: hipLaunchKernelGGL((k_blockwise<1, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, a, t); break;
-    case 32: hipLaunchKernelGGL((k_blockwise<2, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, a, t); break;
-    case 64: hipLaunchKernelGGL((k_blockwise<4, F, TIO>), dim3((unsigned)n), dim3(64), 0, st, a, t); break;
+    case 16:
+      hipLaunchKernelGGL((k_neumann<1, F, true, 0, 0, TIO, true>), tile_grid<1>(n), dim3(64), 0,
+                         st, a, t, n, 0, 0);
+      break;
+    case 32:
+      hipLaunchKernelGGL((k_neumann<2, F, true, 0, 0, TIO, true>), tile_grid<2>(n), dim3(64), 0,
+                         st, a, t, n, 0, 0);
+      break;
+    case 64:
+      hipLaunchKernelGGL((k_neumann<4, F, true, 0, 0, TIO, true>), tile_grid<4>(n), dim3(64), 0,
+                         st, a, t, n, 0, 0);
+      break;
     case 128:
       hipLaunchKernelGGL((k_neumann128<F, true, 0, 0, TIO, true>), dim3((unsigned)n), dim3(64), 0,
                          st, a, t, 0, 0);
