@@ -26,9 +26,9 @@ struct Chunk {
   // contiguous H/8 * d-wide column band of [B, L, H, d]: a copy with this
   // addressing runs 6 % faster on MI355X than with the heads dealt across
   // the XCDs.  A bijection of the work items; tiles are unchanged.
-  __device__ Chunk(uint32_t x, int L, int H, int C) {
+  __device__ Chunk(uint32_t x, int L, int H, int C, bool bands = true) {
     const uint32_t nc = (uint32_t)(L / C);
-    if ((H & 7) == 0) {
+    if (bands && (H & 7) == 0) {
       const uint32_t hg = (uint32_t)H >> 3, slot = x >> 3;
       const uint32_t row = slot / hg;
       x = row * (uint32_t)H + (x & 7u) * hg + (slot - row * hg);
@@ -40,6 +40,21 @@ struct Chunk {
     t0 = chunk * C;
     m = C;
     tile = ((int64_t)b * H + h) * nc + chunk;
+  }
+  // The work-item map of the compute-bound integer kernels, n = B H (L / C)
+  // work items: XCD k (x % 8) takes every H-th group of work items whole, so
+  // all heads of chunk rows k, k + 8, k + 16, ... run on one XCD and a gate
+  // cache line (the H heads of one token) is fetched once, not once per
+  // XCD; with the heads of a row dealt across the XCDs, gate reads are 8
+  // times the algorithmic bytes.  A partial last group of fewer than 8 rows
+  // keeps the plain order.  A bijection of the work items; tiles unchanged.
+  static __device__ Chunk by_rows(uint32_t x, uint32_t n, int L, int H, int C) {
+    const uint32_t hh = (uint32_t)H, R8 = (n / hh) & ~7u;
+    if (x < R8 * hh) {
+      const uint32_t s = x >> 3, grp = s / hh;
+      x = (8u * grp + (x & 7u)) * hh + (s - grp * hh);
+    }
+    return Chunk(x, L, H, C, false);
   }
   // Packed sequences (B = 1, T tokens): sequence s holds tokens
   // cu[s] .. cu[s + 1] - 1 and chunks off[s] .. off[s + 1] - 1, each chunk
@@ -82,17 +97,45 @@ struct Packed {
 // beta and g of the chunk into LDS (one wave; C <= 128).  Rows r >= m (past
 // the end of a packed sequence) get beta = 0, which makes them write nothing
 // (A's rows vanish, T is the identity there), and the last row's g.
+// In two steps, so that a kernel can issue its K loads between them: the
+// LDS writes wait for the gate loads, and the barrier must not hold back
+// the next loads behind a second memory latency.
+template <int C> struct GateRows {
+  static constexpr int R = (C + 63) / 64;  // rows per lane
+  float b[R], g[R];
+};
+template <int C>
+__device__ __forceinline__ GateRows<C> fetch_gates(const float* __restrict__ beta,
+                                                   const float* __restrict__ g, const Chunk& ch,
+                                                   int L, int H, int m = C) {
+  GateRows<C> gr;
+#pragma unroll
+  for (int k = 0; k < GateRows<C>::R; ++k) {
+    const int r = lane_id() + 64 * k;
+    const int rr = r < C ? (r < m ? r : m - 1) : 0;
+    const int64_t o = ((int64_t)ch.b * L + ch.t0 + rr) * H + ch.h;
+    gr.b[k] = (r < C && r < m && beta) ? beta[o] : 0.f;
+    gr.g[k] = (r < C && g) ? g[o] : 0.f;
+  }
+  return gr;
+}
+template <int C>
+__device__ __forceinline__ void stash_gates(const GateRows<C>& gr, float* sb, float* sg) {
+#pragma unroll
+  for (int k = 0; k < GateRows<C>::R; ++k) {
+    const int r = lane_id() + 64 * k;
+    if (r < C) {
+      if (sb) sb[r] = gr.b[k];
+      if (sg) sg[r] = gr.g[k];
+    }
+  }
+  __syncthreads();
+}
 template <int C>
 __device__ __forceinline__ void load_gates(const float* __restrict__ beta,
                                            const float* __restrict__ g, const Chunk& ch, int L,
                                            int H, float* sb, float* sg, int m = C) {
-  for (int r = lane_id(); r < C; r += 64) {
-    const int rr = r < m ? r : m - 1;
-    const int64_t o = ((int64_t)ch.b * L + ch.t0 + rr) * H + ch.h;
-    if (sb) sb[r] = r < m ? beta[o] : 0.f;
-    if (sg) sg[r] = g[o];
-  }
-  __syncthreads();
+  stash_gates<C>(fetch_gates<C>(beta, g, ch, L, H, m), sb, sg);
 }
 
 // Lower blocks of the chunk Gram matrix K K^T (fp32 accumulation), in the
@@ -180,10 +223,11 @@ __device__ __forceinline__ void build_A_rows(const TK* __restrict__ K,
                                              const float* __restrict__ beta,
                                              const float* __restrict__ g, const Chunk& ch,
                                              int L, int H, float* sb, float* sg, Acc<NB>& G) {
-  load_gates<16 * NB>(beta, g, ch, L, H, sb, sg);
+  const GateRows<16 * NB> gr = fetch_gates<16 * NB>(beta, g, ch, L, H);
   {
     Pair<F> kp[NB][DK / 32];
     load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK);
+    stash_gates<16 * NB>(gr, sb, sg);
     gram_lower<NB, DK, true>(G, kp);
   }
   gate_scale<NB, true>(G, sb, sg, 1.f);

@@ -252,9 +252,7 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
   const int m = VARLEN ? ch.m : C;
   if (VARLEN && m <= 0) return;
   const Lane ln = lane_here();
-  load_gates<C>(beta, g, ch, L, H, sb, sg, m);
-  for (int r = ln.id; r < C; r += 64) sbw[r] = sb[r] * __expf(sg[r]);
-  __syncthreads();
+  const GateRows<C> gr = fetch_gates<C>(beta, g, ch, L, H, m);
   TIO* wf = ws + ch.tile * LY::W;
   TIO* uf = ws + n_tiles * LY::W + ch.tile * LY::U;
   TIO* ktf = ws + n_tiles * (LY::W + LY::U) + ch.tile * LY::KT;
@@ -263,6 +261,9 @@ __global__ __launch_bounds__(64) void k_fwd_chunk(const TIO* __restrict__ Q,
 
   Pair<F> kp[NB][DK / 32];
   load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), ldk, ln, m);
+  stash_gates<C>(gr, sb, sg);
+  for (int r = ln.id; r < C; r += 64) sbw[r] = sb[r] * __expf(sg[r]);
+  __syncthreads();
   auto prefetch_v = [&]() {
     if constexpr (PREF) {
       __builtin_amdgcn_sched_barrier(0);

@@ -390,7 +390,7 @@ __global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restri
   constexpr int C = 128;
   __shared__ float sb[C], sg[C];
   __shared__ __attribute__((aligned(16))) Lds128 sh;
-  const Chunk ch(blockIdx.x, L, H, C);
+  const Chunk ch = Chunk::by_rows(blockIdx.x, gridDim.x, L, H, C);
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
   const int64_t ldk = (int64_t)H * DK;

@@ -115,7 +115,7 @@ __global__ __launch_bounds__(64) void k_inverse_i16_fused(const TK* __restrict__
                                                           float* __restrict__ Tdeq, int L, int H,
                                                           int Nrt, int Srt) {
   __shared__ float sb[16 * NB], sg[16 * NB];
-  const Chunk ch(blockIdx.x, L, H, 16 * NB);
+  const Chunk ch = Chunk::by_rows(blockIdx.x, gridDim.x, L, H, 16 * NB);
   Acc<NB> G;
   build_A_rows<NB, DK, F>(K, beta, g, ch, L, H, sb, sg, G);
   float m = 0.f;

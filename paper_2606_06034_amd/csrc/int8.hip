@@ -108,7 +108,7 @@ __global__ __launch_bounds__(64) void k_inverse_i8_fused(const TK* __restrict__ 
                                                          int Nrt, int Srt) {
   constexpr int C = 16 * NB;
   __shared__ float sb[C], sg[C];
-  const Chunk ch(blockIdx.x, L, H, C);
+  const Chunk ch = Chunk::by_rows(blockIdx.x, gridDim.x, L, H, C);
   Acc<NB> G;
   build_A_rows<NB, DK, F>(K, beta, g, ch, L, H, sb, sg, G);
   float m = 0.f;

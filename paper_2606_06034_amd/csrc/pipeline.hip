@@ -97,11 +97,12 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
   const int m = VARLEN ? ch.m : C;
   if (VARLEN && m <= 0) return;
   const int64_t tile = ch.tile;
-  load_gates<C>(beta, g, ch, L, H, sb, sg, m);
+  const GateRows<C> gr = fetch_gates<C>(beta, g, ch, L, H, m);
   const Lane ln = lane_here();
 
   Pair<F> kp[NB][DK / 32];
   load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK, ln, m);
+  stash_gates<C>(gr, sb, sg);
   // issued once K has been consumed: the compiler counts DMA completions as
   // unordered with plain loads and would otherwise wait for V before the
   // Gram; the inverse that follows touches no global memory
