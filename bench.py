@@ -16,9 +16,10 @@ the inverse against forward substitution kernel for kernel).
 
 Prints ONE JSON line: throughput in chunk inverses per second, the roofline
 of the dominant kernel (timed with HIP events on the stream it runs on), and
-the CPU oracle timed on a bounded sample of the same workload (all host
-threads and one thread, T_hat and forward substitution) together with the
-GPU's max abs error against it on that sample.
+the CPU oracle timed on one host thread on a bounded sample of the same
+workload (T_hat and forward substitution; the T_hat pass also with the host
+pools' default thread count) together with the GPU's max abs error against
+it on that sample.
 
 --path forward runs the whole chunk-wise Gated DeltaNet layer forward
 (gdn_chunk_forward: per-chunk factors, then the state recurrence and the
@@ -87,8 +88,9 @@ def parse():
                     help="repeat oracle passes over the sample until this much time has passed")
     ap.add_argument("--error-grid", action="store_true",
                     help="instead of timing: max |T_hat(N, S) - X| and per-tile SNR for "
-                         "N = 1..6, S = 0..16 against the exact inverse X (fp32 forward "
-                         "substitution on the GPU), workload and stress tiles, fp32 and bf16")
+                         "N = 1..6, S = 0..16 against the exact inverse X (fp64 triangular "
+                         "solve on the host), workload and stress tiles; fp32, bf16 and the "
+                         "integer modes (split and plain forms)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run 10 device-to-device copies of 512 MiB (to scale HBM "
                          "byte counters) and exit")
@@ -257,11 +259,14 @@ def main():
         # K (dk per token) and beta, g in; T_hat codes and exponents out.  An
         # INT16 product is four int8 MFMA products over the codes' limbs.
         # C = 128: three exponents per tile, 2 (N + S) + 2 products of 64-blocks.
+        # The bound is chosen from the method's own work, as for the float
+        # inverse: the non-zero part of the N + S products, in int8 MFMA
+        # operations (an INT16 product is four limb products).  At C = 64
+        # that is 48 (INT8) and 160 (INT16) operations per byte, below the
+        # int8 ridge (625): HBM-bound.
         qb = 1 if a.path == "int8" else 2
         bytes_ = tok * (w.dk * es + 8) + n_tiles * (C * C * qb + 4 * (3 if C == 128 else 1))
-        flops = (N + S) * 2 * C ** 3 * n_tiles * qb * qb  # int8 MFMA ops of the N + S products
-        if C == 128:
-            flops = (2 * (N + S) + 2) * 2 * 64 ** 3 * n_tiles * qb * qb
+        flops = f_useful * qb * qb
         if flops / bytes_ >= INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
             bound, peak, unit = "mfma", INT8_PEAK_TOPS, "TOP/s"
             achieved = flops / (ev_ms * 1e-3) / 1e12
@@ -310,8 +315,13 @@ def main():
         out["same_shape_inverse"] = same_shape_inverse(a, G, torch, stream, dA, dT, n_tiles, C, N,
                                                        S, es, f_useful)
     if low:
-        out["tops_int8_dense_equiv"] = round(flops / (ev_ms * 1e-3) / 1e12, 2)
-        out["tops_vs_int8_peak"] = round(flops / (ev_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
+        # int8 MFMA operations: useful (the non-zero part of the N + S
+        # products, the roofline's count) and dense-equivalent
+        dense = f_inv * qb * qb
+        out["int8_ops_per_tile"] = {"useful": flops // n_tiles, "dense_equiv": dense // n_tiles}
+        out["tops_useful"] = round(flops / (ev_ms * 1e-3) / 1e12, 2)
+        out["tops_useful_vs_int8_peak"] = round(flops / (ev_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
+        out["tops_dense_equiv"] = round(dense / (ev_ms * 1e-3) / 1e12, 2)
         for k in ("flop_per_tile", "tflops_useful", "tflops_useful_vs_bf16_peak",
                   "tflops_dense_equiv"):
             del out[k]
@@ -556,23 +566,24 @@ def bench_forward_varlen(a, w, C, N, S, G, torch):
             ns += 1
         sub = lambda x: x[:, :t_end]
         cu_s = cu[:ns + 1]
-        passes, t0 = 0, time.perf_counter()
-        while True:
-            Or, Sr = varlen.forward_varlen_chunked(sub(Q), sub(K), sub(V), sub(beta), sub(g), cu_s,
-                                                   C, S0[:ns], scale, inv)
-            passes += 1
-            secs = time.perf_counter() - t0
-            if secs >= a.cpu_seconds:
-                break
+        with _one_thread():
+            passes, t0 = 0, time.perf_counter()
+            while True:
+                Or, Sr = varlen.forward_varlen_chunked(sub(Q), sub(K), sub(V), sub(beta), sub(g),
+                                                       cu_s, C, S0[:ns], scale, inv)
+                passes += 1
+                secs = time.perf_counter() - t0
+                if secs >= a.cpu_seconds:
+                    break
         torch.cuda.synchronize()
         Og = dO[:, :t_end].float().cpu().numpy()
         Sg = dSf[:ns].cpu().numpy()
         out["cpu_baseline"] = {
             "value": round(chunks * w.H * passes / secs, 1), "unit": "chunk inverses/s",
-            "cores": _threads(), "kind": "oracle",
+            "cores": 1, "kind": "oracle", "cpu_model": _cpu_model(),
             "sample": f"the first {ns} sequences ({t_end} tokens, {chunks} chunks per head, "
                       f"{w.H} heads), {passes} passes of the packed chunk-wise forward in "
-                      f"float64 numpy ({inv_mode} inverse), {secs:.2f} s",
+                      f"float64 numpy on one thread ({inv_mode} inverse), {secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"O": float(np.max(np.abs(Og - Or))),
                                           "S_final": float(np.max(np.abs(Sg - Sr)))}}
     print(json.dumps(out), flush=True)
@@ -633,11 +644,6 @@ def bench_varlen(a, w, C, N, S, G, torch):
     if not a.no_cpu_baseline:
         from oracle import gdn, varlen
 
-        try:
-            from threadpoolctl import threadpool_info
-            cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-        except Exception:  # pragma: no cover
-            cores = os.cpu_count() or 1
         # whole sequences from the start up to ~cpu_sample_tiles chunk tiles
         nseq, tiles = 0, 0
         while nseq < len(lengths) and tiles < a.cpu_sample_tiles:
@@ -654,21 +660,23 @@ def bench_varlen(a, w, C, N, S, G, torch):
 
         inv = (gdn.forward_substitution_inverse if a.exact else
                blocked_padded if C == 128 else (lambda A: gdn.neumann_inverse(A, N, S)))
-        passes, t0 = 0, time.perf_counter()
-        while True:
-            Wr, Ur, _ = varlen.wy_varlen(K[:, :te], V[:, :te], beta[:, :te], g[:, :te],
-                                         cu[:nseq + 1], C, inverse=inv)
-            passes += 1
-            secs = time.perf_counter() - t0
-            if secs >= a.cpu_seconds:
-                break
+        with _one_thread():
+            passes, t0 = 0, time.perf_counter()
+            while True:
+                Wr, Ur, _ = varlen.wy_varlen(K[:, :te], V[:, :te], beta[:, :te], g[:, :te],
+                                             cu[:nseq + 1], C, inverse=inv)
+                passes += 1
+                secs = time.perf_counter() - t0
+                if secs >= a.cpu_seconds:
+                    break
         torch.cuda.synchronize()
         err = {"W": float(np.max(np.abs(dW[:, :te].float().cpu().numpy() - Wr))),
                "U": float(np.max(np.abs(dU[:, :te].float().cpu().numpy() - Ur)))}
         out["cpu_baseline"] = {"value": round(tiles * passes / secs, 1), "unit": "chunk inverses/s",
-                               "cores": cores, "kind": "oracle",
+                               "cores": 1, "kind": "oracle", "cpu_model": _cpu_model(),
                                "sample": f"the first {nseq} sequences ({te} tokens, {tiles} chunk "
-                                         f"tiles), {passes} passes in float64 numpy, {secs:.2f} s",
+                                         f"tiles), {passes} passes in float64 numpy on one "
+                                         f"thread, {secs:.2f} s",
                                "max_abs_err_gpu_vs_oracle": err}
     print(json.dumps(out), flush=True)
 
@@ -679,11 +687,6 @@ def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale, inv_mode="neumann"
     the GPU's max abs error against it on those heads."""
     from oracle import gdn, gdn_forward as fwd
 
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
     Q, K, V, beta, g, S0 = host
     nc = w.L // C
     heads = [(b, h) for b in range(w.B) for h in range(w.H)][:max(1, a.cpu_sample_tiles // nc)]
@@ -695,20 +698,22 @@ def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale, inv_mode="neumann"
            "neumann": lambda A: gdn.neumann_inverse(A, N, S),
            "int16": lambda A: oi.dequantized_inverse(A, N, S, oi.SPEC16),
            "int8": lambda A: oi.dequantized_inverse(A, N, S, oi.SPEC8)}[inv_mode]
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        Or, Sr = fwd.gdn_chunked(Qs, Ks, Vs, bs, gs, C, S0s, scale=scale, inverse=inv)
-        passes += 1
-        secs = time.perf_counter() - t0
-        if secs >= a.cpu_seconds:
-            break
+    with _one_thread():
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            Or, Sr = fwd.gdn_chunked(Qs, Ks, Vs, bs, gs, C, S0s, scale=scale, inverse=inv)
+            passes += 1
+            secs = time.perf_counter() - t0
+            if secs >= a.cpu_seconds:
+                break
     tiles = len(heads) * nc * passes
     Og = np.stack([dO[b, :, h].float().cpu().numpy() for b, h in heads], 1)[None]
     Sg = np.stack([dSf[b, h].float().cpu().numpy() for b, h in heads], 0)[None]
-    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": cores,
-            "kind": "oracle",
+    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": 1,
+            "kind": "oracle", "cpu_model": _cpu_model(),
             "sample": f"{len(heads)} heads x {nc} chunks of {w.name}, {passes} passes of the "
-                      f"chunk-wise forward in float64 numpy ({inv_mode} inverse), {secs:.2f} s",
+                      f"chunk-wise forward in float64 numpy on one thread ({inv_mode} "
+                      f"inverse), {secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"O": float(np.max(np.abs(Og - Or))),
                                           "S_final": float(np.max(np.abs(Sg - Sr)))}}
 
@@ -751,11 +756,7 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
     against it on those tiles (fused path outputs)."""
     from oracle import gdn
 
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
+    cores = _threads()
     nc = w.L // C
     want = max(1, a.cpu_sample_tiles)
     heads = []
@@ -778,13 +779,14 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
         Wr, Ur = gdn.wy_apply(T, Ks, Vs, bs, C)
         return A, T, Wr, Ur
 
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        A, T, Wr, Ur = one_pass()
-        passes += 1
-        secs = time.perf_counter() - t0
-        if secs >= a.cpu_seconds:
-            break
+    with _one_thread():
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            A, T, Wr, Ur = one_pass()
+            passes += 1
+            secs = time.perf_counter() - t0
+            if secs >= a.cpu_seconds:
+                break
     tiles = A.shape[1] * A.shape[2] * passes
     n_sample = A.shape[1] * A.shape[2]
 
@@ -796,12 +798,12 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
             dt_ = time.perf_counter() - t1
             if dt_ >= seconds:
                 return round(n_sample * k / dt_, 1), k, dt_
-    # the same sample on one host thread, and the exact inverse by forward
-    # substitution (the baseline the paper compares against) on all threads
-    from threadpoolctl import threadpool_limits
-    with threadpool_limits(limits=1):
-        one_core = rate(one_pass, a.cpu_seconds / 2)
-    fws = rate(lambda: gdn.forward_substitution_inverse(A), a.cpu_seconds / 2)
+    # the same sample with the host pools' default thread count, and the
+    # exact inverse by forward substitution (the baseline the paper compares
+    # against) on one thread
+    all_threads = rate(one_pass, a.cpu_seconds / 2)
+    with _one_thread():
+        fws = rate(lambda: gdn.forward_substitution_inverse(A), a.cpu_seconds / 2)
     # GPU outputs of the same tiles
     W, U, Tg = G.gdn_chunk_wy_fused(dK, dV, db, dg, C, N, S, want_T=True) if C != 128 else (None, None, None)
     err = None
@@ -812,18 +814,26 @@ def cpu_baseline(w, C, N, S, a, host_inputs, dK, dV, db, dg, torch, G):
         Tgs = np.stack([Tg[b, h].float().cpu().numpy() for b, h in heads], 0)[None]
         err = {"T": float(np.max(np.abs(Tgs - T))), "W": float(np.max(np.abs(Wg - Wr))),
                "U": float(np.max(np.abs(Ug - Ur)))}
-    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": cores,
+    return {"value": round(tiles / secs, 1), "unit": "chunk inverses/s", "cores": 1,
             "kind": "oracle",
             "sample": f"{len(heads)} heads x {nc} chunks of {w.name} ({tiles // passes} "
                       f"tiles), {passes} passes: build A + T_hat({N},{S}) + W/U in float64 "
-                      f"numpy, {secs:.2f} s",
+                      f"numpy on one thread, {secs:.2f} s",
             "cpu_model": _cpu_model(),
-            "one_core": {"value": one_core[0], "passes": one_core[1],
-                         "seconds": round(one_core[2], 2)},
-            "fwdsub_oracle": {"value": fws[0], "cores": cores, "passes": fws[1],
+            "all_threads": {"value": all_threads[0], "threads": cores,
+                            "passes": all_threads[1], "seconds": round(all_threads[2], 2)},
+            "fwdsub_oracle": {"value": fws[0], "cores": 1, "passes": fws[1],
                               "seconds": round(fws[2], 2),
                               "what": "exact inverse by forward substitution on the same A"},
             "max_abs_err_gpu_vs_oracle": err}
+
+
+def _one_thread():
+    """Host BLAS/OpenMP pools limited to one thread: the oracle's products
+    are small (C x C tiles), so extra threads add nothing, and one thread is
+    the core count it is reported with."""
+    from threadpoolctl import threadpool_limits
+    return threadpool_limits(limits=1)
 
 
 def _cpu_model():
@@ -841,13 +851,16 @@ def error_grid(a, G, torch):
 
     Tiles: the first two heads of the sweep workload at each C, and two
     stress heads (shared key direction, slow decay; |A| up to ~0.5).  A is
-    built on the GPU in fp32; X is the fp32 forward substitution of that A
-    (within ~1e-7 of the exact inverse, the floor of every figure here);
-    bf16 mode inverts A rounded to bf16; int16 / int8 quantise A (per tile,
-    per block at C = 128) and run the integer inverse, dequantised.  Per
-    (C, set, dtype, N, S): max abs
-    error over tiles and the per-tile SNR 10 log10(|X|_F^2 / |X - T_hat|_F^2),
-    mean and worst."""
+    built on the GPU in fp32; X is its exact inverse from an fp64
+    triangular solve on the host (scipy, per tile); bf16 mode inverts A
+    rounded to bf16; int16 / int8 quantise A (per tile, per block at
+    C = 128) and run the integer inverse, dequantised, in the split form
+    (unit diagonal outside the codes, Section 3.2's mitigation of the
+    powers' dynamic range) and, at C <= 64, the plain form (diagonal inside
+    every tensor: "int16_plain", "int8_plain").  Per (C, set, dtype, N, S):
+    max abs error over tiles and the per-tile SNR
+    10 log10(|X|_F^2 / |X - T_hat|_F^2), mean and worst."""
+    from scipy.linalg import solve_triangular
     Cs = [a.C] if a.C else [16, 32, 64, 128]
     out = {"metric": "approximation error of T_hat(N, S) vs exact inverse", "grid": []}
     for C in Cs:
@@ -861,13 +874,17 @@ def error_grid(a, G, torch):
             db = torch.from_numpy(np.ascontiguousarray(beta)).to("cuda")
             dg = torch.from_numpy(np.ascontiguousarray(g)).to("cuda")
             A32 = G.gdn_build_A(dK, db, dg, C, a_dtype=torch.float32)
-            X = G.gdn_chunk_inverse_fwdsub(A32).double()
+            Ah = A32.cpu().double().numpy().reshape(-1, C, C)
+            eye = np.eye(C)
+            Xh = np.stack([solve_triangular(eye + t, eye, lower=True, unit_diagonal=True)
+                           for t in Ah])
+            X = torch.from_numpy(Xh.reshape(A32.shape)).to("cuda")
             xn = (X ** 2).sum(dim=(-1, -2))
             # the integer modes: quantised per tile (per block at C = 128), the
             # integer T_hat(N, S), dequantised
-            def int_inverse(quant, inv):
+            def int_inverse(quant, inv, plain=False):
                 qA, eA = quant(A32)
-                return lambda N, S: inv(qA, eA, N, S, want_deq=True)[2].double()
+                return lambda N, S: inv(qA, eA, N, S, want_deq=True, plain=plain)[2].double()
             modes = [("f32", lambda N, S: G.gdn_chunk_inverse_neumann(A32, N, S).double()),
                      ("bf16", lambda N, S: G.gdn_chunk_inverse_neumann(
                          A32.to(torch.bfloat16), N, S).double()),
@@ -875,6 +892,11 @@ def error_grid(a, G, torch):
                                            G.gdn_chunk_inverse_neumann_i16)),
                      ("int8", int_inverse(G.gdn_quantize_tiles_i8,
                                           G.gdn_chunk_inverse_neumann_i8))]
+            if C <= 64:
+                modes += [("int16_plain", int_inverse(G.gdn_quantize_tiles_i16,
+                                                      G.gdn_chunk_inverse_neumann_i16, True)),
+                          ("int8_plain", int_inverse(G.gdn_quantize_tiles_i8,
+                                                     G.gdn_chunk_inverse_neumann_i8, True))]
             for dtn, inverse in modes:
                 for N in range(1, 7):
                     for S in range(0, 17):
@@ -919,19 +941,20 @@ def cpu_baseline_int(w, C, N, S, a, host_inputs, dTq, deT, torch, G, sfx):
     Ks = np.stack([K[b, :, h] for b, h in heads], 1)[None]
     bs = np.stack([beta[b, :, h] for b, h in heads], 1)[None]
     gs = np.stack([g[b, :, h] for b, h in heads], 1)[None]
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        A = gdn.build_A(Ks, bs, gs, C).astype(np.float32)
-        if C == 128:
-            qA, eA = oi.quantize_blocked(A, spec)
-            qT, eT = oi.neumann_inverse_int_blocked(qA, eA, N, S, spec)
-        else:
-            qA, eA = oi.quantize(A, spec)
-            qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S, spec)
-        passes += 1
-        secs = time.perf_counter() - t0
-        if secs >= a.cpu_seconds:
-            break
+    with _one_thread():
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            A = gdn.build_A(Ks, bs, gs, C).astype(np.float32)
+            if C == 128:
+                qA, eA = oi.quantize_blocked(A, spec)
+                qT, eT = oi.neumann_inverse_int_blocked(qA, eA, N, S, spec)
+            else:
+                qA, eA = oi.quantize(A, spec)
+                qT, eT, _ = oi.neumann_inverse_int8(qA, eA, N, S, spec)
+            passes += 1
+            secs = time.perf_counter() - t0
+            if secs >= a.cpu_seconds:
+                break
     deq = oi.dequant_unit_blocked if C == 128 else oi.dequant_unit
     Tr = deq(qT, eT)[0]
     X = gdn.forward_substitution_inverse(A.astype(np.float64))[0]
@@ -947,11 +970,11 @@ def cpu_baseline_int(w, C, N, S, a, host_inputs, dTq, deT, torch, G, sfx):
                    for b, h in heads], 0)
     tiles = Tr.shape[0] * Tr.shape[1]
     return {"value": round(tiles * passes / secs, 1), "unit": "chunk inverses/s",
-            "cores": _threads(), "kind": "oracle",
+            "cores": 1, "kind": "oracle", "cpu_model": _cpu_model(),
             "sample": f"{len(heads)} heads x {nc} chunks of {w.name} ({tiles} tiles), {passes} "
                       f"passes: build A + {sfx.upper().replace('I', 'INT')} quantiser + "
                       f"integer T_hat({N},{S})"
-                      f"{' (block-wise, C = 128)' if C == 128 else ''}, numpy, "
+                      f"{' (block-wise, C = 128)' if C == 128 else ''}, numpy on one thread, "
                       f"{secs:.2f} s",
             "max_abs_err_gpu_vs_oracle": {"T": float(np.max(np.abs(Tg - Tr)))},
             "max_abs_err_vs_exact_inverse": {"gpu": float(np.max(np.abs(Tg - X))),
