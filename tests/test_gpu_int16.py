@@ -304,10 +304,11 @@ def test_i16_fused_matches_stages(C, kdt):
 def test_i16_fused_vs_oracle_and_float(C):
     """Against the integer oracle run from its own fp32 A (float64 build,
     rounded): the GPU forms A in fp32 arithmetic, so an entry a few ulp away
-    can move a 16-bit code at a rounding boundary (most tiles hold one such
-    entry at this width); the dequantised results stay within a few dozen
-    quanta.  Against the float64 T_hat(N, S) the INT16 result is
-    within a small multiple of 2^-16 of max|T_hat - I| per tile."""
+    can move a 16-bit code at a rounding boundary.  Measured: every tile of
+    this sample bit-exact at C = 16, 32, 64; the bounds allow three tiles in
+    64 to differ, by at most a few dozen quanta.  Against the float64
+    T_hat(N, S) the INT16 result is within a small multiple of 2^-16 of
+    max|T_hat - I| per tile."""
     K, beta, g = head_set(C, "bf16", L=16 * C, H=4)
     N, S = G.gdn_default_order(C)
     print(f"i16 fused vs oracle C={C}", flush=True)
@@ -323,6 +324,7 @@ def test_i16_fused_vs_oracle_and_float(C):
     quanta = np.abs(got - oi.dequant_unit(rq, re)) / np.ldexp(1.0, re)[:, None, None]
     print(f"  {same.mean():.4f} of {same.size} tiles bit-exact, max {quanta.max():.1f} quanta",
           flush=True)
+    assert same.mean() >= 0.95
     assert quanta.max() <= 64.0
     T = gdn.neumann_inverse(Af, N, S)
     scale = np.max(np.abs(T - np.eye(C)), axis=(-1, -2))

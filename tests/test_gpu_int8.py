@@ -307,9 +307,9 @@ def test_i8_fused_matches_stages(C, kdt):
 def test_i8_fused_vs_oracle(C):
     """Against the integer oracle run from its own fp32 A (float64 build,
     rounded): the GPU forms A in fp32 arithmetic, so an entry one unit in
-    the last place away can move a code at a rounding boundary.  Most tiles
-    match bit for bit; the rest differ from the oracle's T_hat by at most a
-    few quanta of T_hat's exponent."""
+    the last place away can move a code at a rounding boundary.  Measured:
+    every tile of this sample bit-exact at C = 16, 32, 64; the bound allows
+    one tile in 64 to differ, by at most a few quanta of T_hat's exponent."""
     K, beta, g = head_set(C, "bf16", L=16 * C, H=4)
     Tq, eT, Td = G.gdn_chunk_inverse_neumann_i8_fused(to_cuda(K, torch.bfloat16), to_cuda(beta),
                                                       to_cuda(g), C, *G.gdn_default_order(C),
@@ -324,7 +324,7 @@ def test_i8_fused_vs_oracle(C):
     quanta = diff / np.ldexp(1.0, re)[:, None, None]
     print(f"i8 fused vs oracle C={C}: {same.mean():.4f} of {same.size} tiles bit-exact, "
           f"max diff {diff.max():.3e} = {quanta.max():.1f} quanta", flush=True)
-    assert same.mean() >= 0.9
+    assert same.mean() >= 0.98
     assert quanta.max() <= 4.0
 
 
