@@ -479,3 +479,25 @@ def test_metrics_definitions():
     T[0, 3, 0] = 0.1
     assert np.isclose(gdn.snr_db(X, T)[0], 10 * np.log10(4 / 0.01))
     assert np.isclose(gdn.diag_power_ratio(X, 0)[0], 1.0)
+
+
+def test_diag_power_ratio_closed_forms():
+    """The accumulated diagonal power ratio on inverses with a closed form.
+    A = -S (S the unit sub-diagonal): (I + A)^-1 = sum_k S^k, the all-ones
+    lower triangle, whose sub-diagonal d holds C - d ones, so the ratio up to
+    n is sum_{d<=n} (C - d) / (C (C + 1) / 2) = (n + 1)(2C - n) / (C (C + 1)).
+    A = -r S: the inverse has r^(i-j) below the diagonal, diagonal d has
+    power (C - d) r^(2d)."""
+    for C in (5, 8, 16):
+        A = np.zeros((1, C, C))
+        A[0, np.arange(1, C), np.arange(C - 1)] = -1.0
+        X = gdn.forward_substitution_inverse(A)
+        for n in range(C):
+            want = (n + 1) * (2 * C - n) / (C * (C + 1))
+            assert np.isclose(gdn.diag_power_ratio(X, n)[0], want, rtol=1e-13, atol=0)
+        r = 0.7
+        Xg = gdn.forward_substitution_inverse(r * A)
+        tot = sum((C - d) * r ** (2 * d) for d in range(C))
+        for n in range(C):
+            want = sum((C - d) * r ** (2 * d) for d in range(n + 1)) / tot
+            assert np.isclose(gdn.diag_power_ratio(Xg, n)[0], want, rtol=1e-12, atol=0)
