@@ -343,21 +343,65 @@ def main():
 def same_shape_inverse(a, G, torch, stream, dA, dT, n_tiles, C, N, S, es, f_useful):
     """The inverse alone on the step's own tiles (A built once in the IO
     dtype): T_hat(N, S), the exact block-wise inverse and the forward-
-    substitution baseline, each one launch timed with HIP events on the
-    launch stream; tile IO bytes and the useful product work per launch."""
+    substitution baseline, each timed per launch without the host's launch
+    overhead (_kernel_time); tile IO bytes and the useful product work per
+    launch."""
     steps = max(1, a.steps // 2)
     res = {}
     for name, fn in (("neumann", lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT)),
                      ("blockwise", lambda: G.gdn_chunk_inverse_blockwise(dA, Tinv=dT)),
                      ("fwdsub", lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT))):
-        ms = _time(fn, steps, stream, torch)
+        ms, how = _kernel_time(fn, dT, steps, stream, torch)
         gbs = n_tiles * C * C * es * 2 / (ms * 1e-3) / 1e9
         res[name] = {"ms": round(ms, 6), "chunk_inverses_per_s": round(n_tiles / (ms * 1e-3), 1),
-                     "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+                     "GB/s": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "timing": how}
     res["neumann"]["tflops_useful"] = round(f_useful / (res["neumann"]["ms"] * 1e-3) / 1e12, 2)
     res["fwdsub_time_over_neumann"] = round(res["fwdsub"]["ms"] / res["neumann"]["ms"], 3)
     res["blockwise_time_over_neumann"] = round(res["blockwise"]["ms"] / res["neumann"]["ms"], 3)
     return res
+
+
+def _kernel_time(fn, out, steps, stream, torch):
+    """Time per launch (ms) of fn, whose result lands in `out`, without the
+    host's per-call launch overhead (which exceeds a launch of a few
+    thousand tiles): `steps` calls captured in one HIP graph, replayed and
+    timed with HIP events.  Two replays, each with eager work after it, are
+    first checked bit for bit against an eager call's result; if capture
+    fails or a replay differs, the eager per-call time (_time) is returned
+    instead.  Returns (ms, "graph" | "eager")."""
+    fn()
+    torch.cuda.synchronize()
+    ref = out.clone()
+    try:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for _ in range(steps):
+                fn()
+        for _ in range(2):
+            out.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            if not torch.equal(out, ref):
+                raise RuntimeError("a graph replay differs from the eager call")
+            fn()
+            torch.cuda.synchronize()
+        cur = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        g.replay()
+        e1.record(cur)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps, "graph"
+    except Exception:  # noqa: BLE001 -- any capture problem: time eagerly
+        torch.cuda.synchronize()
+        return _time(fn, steps, stream, torch), "eager"
 
 
 def _time(fn, steps, stream, torch):
@@ -426,9 +470,10 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
     del ws
     dA = G.gdn_build_A(dK, db, dg, C, a_dtype=dt)
     dT = torch.empty_like(dA)
-    inv_ms = _time(lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT), a.steps, stream, torch)
-    fws_ms = _time(lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT), max(1, a.steps // 4),
-                   stream, torch)
+    inv_ms, inv_how = _kernel_time(lambda: G.gdn_chunk_inverse_neumann(dA, N, S, Tinv=dT), dT,
+                                   a.steps, stream, torch)
+    fws_ms, _ = _kernel_time(lambda: G.gdn_chunk_inverse_fwdsub(dA, Tinv=dT), dT,
+                             max(1, a.steps // 4), stream, torch)
     del dA, dT
     # algorithmic bytes per launch
     # workspace: W, U, K^T and the masked Q K^T per chunk, written once, read once
@@ -464,6 +509,7 @@ def bench_forward(a, w, C, N, S, default_order, G, torch):
         "prepare_ms": round(prep_ms, 6),
         "state_ms": round(state_ms, 6),
         "inverse_alone_ms": round(inv_ms, 6),
+        "inverse_alone_timing": inv_how,
         "fwdsub_alone_ms": round(fws_ms, 6),
         "inverse_share_of_layer": round(inv_ms / ev_ms, 4),
         "fwdsub_share_if_swapped_in": round(fws_ms / (ev_ms - inv_ms + fws_ms), 4),

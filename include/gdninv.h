@@ -47,6 +47,15 @@
  *   A batch with L % C != 0 goes through the packed-sequence entry points
  *   (gdn_chunk_wy_fused_varlen, gdn_chunk_forward_varlen) as B sequences of
  *   L tokens each, the last chunk of each a partial one.
+ * Non-finite values.  Floating-point entry points: a NaN or infinity in the
+ *   strictly lower part of a tile of A (or in a chunk's K, V, beta or g)
+ *   reaches that tile's (chunk's) outputs only, never another tile's, and an
+ *   inverse is non-finite at least at the entry's own position (T_ij
+ *   carries -A_ij).  Which other entries of the tile turn non-finite is not
+ *   specified: the kernels set the residual E to its exact value 0 on the
+ *   band i - j <= N, where a literal evaluation would carry the NaN.
+ *   Entries of A on and above the diagonal are never read.  Integer entry
+ *   points require finite inputs.
  */
 #ifndef GDNINV_H
 #define GDNINV_H
