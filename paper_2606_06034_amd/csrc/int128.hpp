@@ -334,8 +334,13 @@ __device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL,
 }
 
 // The integer inverse at C = 128 from codes (gdn_quantize_tiles_* layout).
+// Both C = 128 kernels are held to two waves per SIMD (amdgpu_waves_per_eu):
+// INT8 then fits its registers exactly, INT16 keeps about 125 values in
+// scratch memory; measured on 16384 tiles, 11-31 % less time than at one
+// wave per SIMD.
 template <typename W, int NC, int SC>
-__global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* __restrict__ Aq,
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_neumann_int128(const typename W::Code* __restrict__ Aq,
                                                         const int32_t* __restrict__ eA,
                                                         typename W::Code* __restrict__ Tq,
                                                         int32_t* __restrict__ eT,
@@ -380,7 +385,8 @@ __global__ __launch_bounds__(128) void k_neumann_int128(const typename W::Code* 
 // quantiser's rule, then the block-wise integer inverse.  Wave w forms its
 // diagonal block; wave 0 also forms A21, before its engine.
 template <typename W, int DK, typename F, typename TK, int NC, int SC>
-__global__ __launch_bounds__(128) void k_inverse_int128_fused(const TK* __restrict__ K,
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_inverse_int128_fused(const TK* __restrict__ K,
                                                               const float* __restrict__ beta,
                                                               const float* __restrict__ g,
                                                               typename W::Code* __restrict__ Tq,
