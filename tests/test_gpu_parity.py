@@ -431,6 +431,35 @@ def test_sweep_c128_full_size_sampled():
     _sampled_check("sweep", C=128)
 
 
+@pytest.mark.parametrize("C", [16, 32, 64])
+def test_sweep_full_size_sampled(C):
+    """Chunk-size sweep at C = 16, 32, 64 (B=4, H=32, L=16384: 131072,
+    65536, 32768 tiles), fused, at each chunk size's default order; then the
+    standalone T_hat and forward substitution on the same A tiles (the
+    kernels the bench times per chunk size; at C = 16, 32 several tiles per
+    wave), sampled against the oracle."""
+    _sampled_check("sweep", C=C, seed=C)
+    w = wl.workload("sweep").with_(C=C)
+    N, S = gdn.default_order(C)
+    n = w.B * w.H * (w.L // C)
+    K, beta, g, _ = wl.gen_inputs(w, C=C, want_v=False)
+    dA = G.gdn_build_A(dev(K, "bf16"), dev(beta), dev(g), C, a_dtype=torch.bfloat16)
+    del K
+    T = G.gdn_chunk_inverse_neumann(dA, N, S)
+    X = G.gdn_chunk_inverse_fwdsub(dA)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(100 + C)
+    # every tile slot of a wave (t % (64 / C)) and both ends
+    picks = sorted(set(rng.integers(0, n, 16).tolist()) | {0, 1, 2, 3, n - 2, n - 1})
+    Av = dA.view(-1, C, C)
+    for t in picks:
+        A = Av[t].float().cpu().numpy().astype(np.float64)[None]
+        assert maxerr(host(T.view(-1, C, C)[t])[None], gdn.neumann_inverse(A, N, S)) <= TOL["bf16"], t
+        assert maxerr(host(X.view(-1, C, C)[t])[None],
+                      gdn.forward_substitution_inverse(A)) <= TOL["bf16"], t
+    print(f"sweep C={C} standalone inverses: {len(picks)} sampled tiles", flush=True)
+
+
 def test_long_context_full_size_sampled():
     """The long-context workload the bench times (B=1, H=32, L=131072, C=64,
     bf16: 65536 tiles) in one fused launch, sampled tiles against the oracle;
