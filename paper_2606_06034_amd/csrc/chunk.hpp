@@ -56,6 +56,14 @@ struct Chunk {
     }
     return Chunk(x, L, H, C, false);
   }
+  // Work item of wave w of workgroup wg when workgroups hold G waves (G
+  // divides H / 8): the waves of one workgroup take consecutive slots of the
+  // XCD wg % 8, i.e. G neighbouring heads of one chunk row of that XCD's
+  // head band (the map of the constructor above), and the workgroup stays on
+  // the XCD its tiles belong to.
+  static __device__ uint32_t grouped(uint32_t wg, int w, int G) {
+    return ((((wg >> 3) * (uint32_t)G + (uint32_t)w)) << 3) | (wg & 7u);
+  }
   // Packed sequences (B = 1, T tokens): sequence s holds tokens
   // cu[s] .. cu[s + 1] - 1 and chunks off[s] .. off[s + 1] - 1, each chunk
   // starting at a multiple of C from the sequence start.  Work item
@@ -119,7 +127,10 @@ __device__ __forceinline__ GateRows<C> fetch_gates(const float* __restrict__ bet
   }
   return gr;
 }
-template <int C>
+// WAVE: the gates are read by this wave only (its own LDS arrays in a
+// workgroup of several waves), so a wave barrier orders its lanes' LDS
+// writes before their reads instead of a workgroup barrier.
+template <int C, bool WAVE = false>
 __device__ __forceinline__ void stash_gates(const GateRows<C>& gr, float* sb, float* sg) {
 #pragma unroll
   for (int k = 0; k < GateRows<C>::R; ++k) {
@@ -129,7 +140,13 @@ __device__ __forceinline__ void stash_gates(const GateRows<C>& gr, float* sb, fl
       if (sg) sg[r] = gr.g[k];
     }
   }
-  __syncthreads();
+  if constexpr (WAVE) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
 }
 template <int C>
 __device__ __forceinline__ void load_gates(const float* __restrict__ beta,

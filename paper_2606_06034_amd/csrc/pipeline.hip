@@ -76,8 +76,8 @@ __global__ __launch_bounds__(64) void k_wy(const TIO* __restrict__ T, const TIO*
 // the last chunk of a sequence may hold m < C tokens; its rows past m are
 // neither read nor written (T is the identity there).
 template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool PREF = false, bool EXACT = false, bool VARLEN = false>
-__global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
+          bool PREF = false, bool EXACT = false, bool VARLEN = false, int WPG = 1>
+__global__ __launch_bounds__(64 * WPG) void k_fused(const TIO* __restrict__ K,
                                               const TIO* __restrict__ V,
                                               const float* __restrict__ beta,
                                               const float* __restrict__ g, TIO* __restrict__ W,
@@ -87,13 +87,20 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
                                               int nchunks) {
   constexpr int C = 16 * NB;
   static_assert(!PREF || sizeof(TIO) == 2, "V prefetch is for bf16 IO");
-  __shared__ float sb[C], sg[C];
-  __shared__ __attribute__((aligned(16))) __bf16 sv[PREF ? NB * (DV / 32) * 512 : 8];
+  static_assert(WPG == 1 || !VARLEN, "grouped waves are for the fixed-length layout");
+  // WPG > 1: the workgroup's waves take neighbouring heads of one chunk row
+  // (Chunk::grouped), each with its own LDS arrays
+  __shared__ float sb_[WPG][C], sg_[WPG][C];
+  __shared__ __attribute__((aligned(16))) __bf16 sv_[WPG][PREF ? NB * (DV / 32) * 512 : 8];
+  const int wv = WPG > 1 ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) : 0;
+  float* sb = sb_[wv];
+  float* sg = sg_[wv];
+  __bf16* sv = sv_[wv];
   Chunk ch;
   if constexpr (VARLEN)
     ch = Chunk::packed(blockIdx.x, H, C, L, cu, off, nseq, nchunks);
   else
-    ch = Chunk(blockIdx.x, L, H, C);
+    ch = Chunk(WPG > 1 ? Chunk::grouped(blockIdx.x, wv, WPG) : blockIdx.x, L, H, C);
   const int m = VARLEN ? ch.m : C;
   if (VARLEN && m <= 0) return;
   const int64_t tile = ch.tile;
@@ -102,7 +109,7 @@ __global__ __launch_bounds__(64) void k_fused(const TIO* __restrict__ K,
 
   Pair<F> kp[NB][DK / 32];
   load_rows<NB, DK>(kp, K + ch.row(0, L, H, DK), (int64_t)H * DK, ln, m);
-  stash_gates<C>(gr, sb, sg);
+  stash_gates<C, (WPG > 1)>(gr, sb, sg);
   // issued once K has been consumed: the compiler counts DMA completions as
   // unordered with plain loads and would otherwise wait for V before the
   // Gram; the inverse that follows touches no global memory
@@ -477,10 +484,23 @@ template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typen
 static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,
                        void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st,
                        const Packed& pk = Packed{}) {
+  // C = 64 with the V prefetch: workgroups of 4 (or 2) waves on neighbouring
+  // heads of one chunk row when H / 8 allows it
+  const int hg = (H & 7) == 0 ? H / 8 : 0;
+  const int wpg = (NB == 4 && PREF && !pk.cu && hg > 0) ? (hg % 4 == 0 ? 4 : hg % 2 == 0 ? 2 : 1)
+                                                        : 1;
   if (pk.cu)
     hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, true>),
                        dim3((unsigned)n), dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g,
                        (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, pk.cu, pk.off, pk.nseq, pk.nchunks);
+  else if (wpg == 4)
+    hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, false, 4>),
+                       dim3((unsigned)(n / 4)), dim3(256), 0, st, (const TIO*)K, (const TIO*)V,
+                       beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, nullptr, nullptr, 0, 0);
+  else if (wpg == 2)
+    hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, false, 2>),
+                       dim3((unsigned)(n / 2)), dim3(128), 0, st, (const TIO*)K, (const TIO*)V,
+                       beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, nullptr, nullptr, 0, 0);
   else
     hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, false>),
                        dim3((unsigned)n), dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g,
