@@ -105,6 +105,19 @@ struct Packed {
 // beta and g of the chunk into LDS (one wave; C <= 128).  Rows r >= m (past
 // the end of a packed sequence) get beta = 0, which makes them write nothing
 // (A's rows vanish, T is the identity there), and the last row's g.
+// Orders LDS writes before the reads that follow: within one wave (WAVE:
+// the data is this wave's own) or across the workgroup.
+template <bool WAVE>
+__device__ __forceinline__ void lds_sync() {
+  if constexpr (WAVE) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
+}
+
 // In two steps, so that a kernel can issue its K loads between them: the
 // LDS writes wait for the gate loads, and the barrier must not hold back
 // the next loads behind a second memory latency.
@@ -140,13 +153,7 @@ __device__ __forceinline__ void stash_gates(const GateRows<C>& gr, float* sb, fl
       if (sg) sg[r] = gr.g[k];
     }
   }
-  if constexpr (WAVE) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  } else {
-    __syncthreads();
-  }
+  lds_sync<WAVE>();
 }
 template <int C>
 __device__ __forceinline__ void load_gates(const float* __restrict__ beta,

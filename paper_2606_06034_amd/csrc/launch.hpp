@@ -20,6 +20,15 @@ namespace gdn {
     case 128: { constexpr int DV = 128; __VA_ARGS__ } \
   }
 
+// Waves per workgroup of the fused kernel over the fixed-length layout
+// (Chunk::grouped): 4 when 32 divides H, 2 when 16 does, else 1.  A
+// workgroup then covers a 1 KB (512 B) run of every token row of its chunk,
+// which the long-context shape runs at 0.69 of HBM instead of 0.59 with one
+// wave per workgroup.
+inline int waves_per_group(int H) {
+  return (H % 32 == 0) ? 4 : (H % 16 == 0) ? 2 : 1;
+}
+
 hipError_t launch_neumann(const void* A, void* T, int64_t n_tiles, int C, int N, int S,
                           int dtype, hipStream_t st);
 hipError_t launch_fwdsub(const void* A, void* T, int64_t n_tiles, int C, int dtype,

@@ -484,11 +484,9 @@ template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typen
 static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,
                        void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st,
                        const Packed& pk = Packed{}) {
-  // C = 64 with the V prefetch: workgroups of 4 (or 2) waves on neighbouring
-  // heads of one chunk row when H / 8 allows it
-  const int hg = (H & 7) == 0 ? H / 8 : 0;
-  const int wpg = (NB == 4 && PREF && !pk.cu && hg > 0) ? (hg % 4 == 0 ? 4 : hg % 2 == 0 ? 2 : 1)
-                                                        : 1;
+  // fixed-length layout: workgroups of 4 (or 2) waves on neighbouring heads
+  // of one chunk row (Chunk::grouped)
+  const int wpg = pk.cu ? 1 : waves_per_group(H);
   if (pk.cu)
     hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, true>),
                        dim3((unsigned)n), dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g,
