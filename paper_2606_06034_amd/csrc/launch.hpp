@@ -20,8 +20,8 @@ namespace gdn {
     case 128: { constexpr int DV = 128; __VA_ARGS__ } \
   }
 
-// Waves per workgroup of the fused kernel over the fixed-length layout
-// (Chunk::grouped): 4 when 32 divides H, 2 when 16 does, else 1.  A
+// Waves per workgroup of the fused kernel (Chunk::grouped; packed sequences:
+// consecutive work items): 4 when 32 divides H, 2 when 16 does, else 1.  A
 // workgroup then covers a 1 KB (512 B) run of every token row of its chunk,
 // which the long-context shape runs at 0.69 of HBM instead of 0.59 with one
 // wave per workgroup.

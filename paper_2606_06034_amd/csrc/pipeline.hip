@@ -87,9 +87,9 @@ __global__ __launch_bounds__(64 * WPG) void k_fused(const TIO* __restrict__ K,
                                               int nchunks) {
   constexpr int C = 16 * NB;
   static_assert(!PREF || sizeof(TIO) == 2, "V prefetch is for bf16 IO");
-  static_assert(WPG == 1 || !VARLEN, "grouped waves are for the fixed-length layout");
   // WPG > 1: the workgroup's waves take neighbouring heads of one chunk row
-  // (Chunk::grouped), each with its own LDS arrays
+  // (Chunk::grouped; packed sequences: G consecutive work items chunk H + h),
+  // each with its own LDS arrays
   __shared__ float sb_[WPG][C], sg_[WPG][C];
   __shared__ __attribute__((aligned(16))) __bf16 sv_[WPG][PREF ? NB * (DV / 32) * 512 : 8];
   const int wv = WPG > 1 ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) : 0;
@@ -98,11 +98,11 @@ __global__ __launch_bounds__(64 * WPG) void k_fused(const TIO* __restrict__ K,
   __bf16* sv = sv_[wv];
   Chunk ch;
   if constexpr (VARLEN)
-    ch = Chunk::packed(blockIdx.x, H, C, L, cu, off, nseq, nchunks);
+    ch = Chunk::packed(blockIdx.x * WPG + wv, H, C, L, cu, off, nseq, nchunks);
   else
     ch = Chunk(WPG > 1 ? Chunk::grouped(blockIdx.x, wv, WPG) : blockIdx.x, L, H, C);
   const int m = VARLEN ? ch.m : C;
-  if (VARLEN && m <= 0) return;
+  if (VARLEN && m <= 0) return;  // the whole workgroup (its waves share the chunk)
   const int64_t tile = ch.tile;
   const GateRows<C> gr = fetch_gates<C>(beta, g, ch, L, H, m);
   const Lane ln = lane_here();
@@ -484,10 +484,19 @@ template <int NB, int DK, int DV, typename F, bool SMALLN, int NC, int SC, typen
 static void launch_one(const void* K, const void* V, const float* beta, const float* g, void* W,
                        void* U, void* T, int64_t n, int L, int H, int N, int S, hipStream_t st,
                        const Packed& pk = Packed{}) {
-  // fixed-length layout: workgroups of 4 (or 2) waves on neighbouring heads
-  // of one chunk row (Chunk::grouped)
-  const int wpg = pk.cu ? 1 : waves_per_group(H);
-  if (pk.cu)
+  // workgroups of 4 (or 2) waves on neighbouring heads of one chunk
+  const int wpg = waves_per_group(H);
+  if (pk.cu && wpg == 4)
+    hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, true, 4>),
+                       dim3((unsigned)(n / 4)), dim3(256), 0, st, (const TIO*)K, (const TIO*)V,
+                       beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, pk.cu, pk.off, pk.nseq,
+                       pk.nchunks);
+  else if (pk.cu && wpg == 2)
+    hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, true, 2>),
+                       dim3((unsigned)(n / 2)), dim3(128), 0, st, (const TIO*)K, (const TIO*)V,
+                       beta, g, (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, pk.cu, pk.off, pk.nseq,
+                       pk.nchunks);
+  else if (pk.cu)
     hipLaunchKernelGGL((k_fused<NB, DK, DV, F, SMALLN, NC, SC, TIO, PREF, EXACT, true>),
                        dim3((unsigned)n), dim3(64), 0, st, (const TIO*)K, (const TIO*)V, beta, g,
                        (TIO*)W, (TIO*)U, (TIO*)T, L, H, N, S, pk.cu, pk.off, pk.nseq, pk.nchunks);
