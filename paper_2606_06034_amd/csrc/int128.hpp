@@ -339,7 +339,7 @@ __device__ __forceinline__ void int128_tile(int wv, const AccI<4>& Lr, int eL,
 // scratch memory; measured on 16384 tiles, 11-31 % less time than at one
 // wave per SIMD.
 template <typename W, int NC, int SC>
-__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 void k_neumann_int128(const typename W::Code* __restrict__ Aq,
                                                         const int32_t* __restrict__ eA,
                                                         typename W::Code* __restrict__ Tq,
@@ -385,7 +385,7 @@ void k_neumann_int128(const typename W::Code* __restrict__ Aq,
 // quantiser's rule, then the block-wise integer inverse.  Wave w forms its
 // diagonal block; wave 0 also forms A21, before its engine.
 template <typename W, int DK, typename F, typename TK, int NC, int SC>
-__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 void k_inverse_int128_fused(const TK* __restrict__ K,
                                                               const float* __restrict__ beta,
                                                               const float* __restrict__ g,

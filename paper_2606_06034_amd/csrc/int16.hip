@@ -80,7 +80,7 @@ __device__ __forceinline__ void store_i16(const AccI<NB>& Tr, int eTo, int16_t* 
 // than the scratch traffic costs (4 % less time on 32768 tiles; the one-launch
 // kernel, whose K loads compete with that traffic, is faster without it).
 template <int NB, bool PLAIN, int NC = -1, int SC = -1>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2)))
 void k_neumann_i16(const int16_t* __restrict__ Aq,
                                                     const int32_t* __restrict__ eA,
                                                     int16_t* __restrict__ Tq,
