@@ -767,6 +767,7 @@ def cpu_baseline_forward(w, C, N, S, a, host, dO, dSf, scale, inv_mode="neumann"
 # committed rocprofv3 summaries carrying measured HBM traffic per launch
 PROFILES = {("fused", "qwen35_prefill", 64): ("k_fused_qwen35_prefill.md", "pipeline.hip"),
             ("fused", "long_context", 64): ("k_fused_long_context.md", "pipeline.hip"),
+            ("fused", "sweep", 128): ("k_fused128_sweep_c128.md", "pipeline.hip"),
             ("inverse", "sweep", 64): ("k_neumann_sweep_c64.md", "neumann.hip"),
             ("int8", "int8", 64): ("k_inverse_i8_fused_int8.md", "int8.hip"),
             ("int16", "int8", 64): ("k_inverse_i16_fused_int8.md", "int16.hip"),

@@ -152,14 +152,14 @@ __global__ __launch_bounds__(64 * WPG) void k_fused(const TIO* __restrict__ K,
 // per chunk.  With the 64-row halves 1, 2 of the chunk, X_kk the inverses of
 // (I + A_kk) by the engine and X_21 = -X_22 A_21 X_11,
 //   W_1 = X_11 diag(beta_1) K_1,
-//   W_2 = X_21 diag(beta_1) K_1 + X_22 diag(beta_2) K_2
-//       = X_22 (diag(beta_2) K_2 - A_21 W_1),
-// and the same for U with V, so X_21 itself is only formed for Tout.
-// Wave 0 runs the C = 64 pipeline on half 1 and leaves K_1, W_1 and U_1 in
-// LDS; wave 1 inverts its diagonal block meanwhile, then builds A_21 from
-// K_2 and the LDS copy of K_1 and forms Z = diag(beta_2) X_2 - A_21 X_1 slice
-// by slice (32 features) followed by X_22 Z.  Phases are separated by
-// workgroup barriers; every branch below is uniform per wave.
+//   W_2 = X_21 diag(beta_1) K_1 + X_22 diag(beta_2) K_2,
+// and the same for U with V.  Wave 0 inverts its diagonal block, hands X_11
+// to wave 1 through LDS and forms W_1, U_1; wave 1 inverts its own block,
+// builds A_21 from K_2 and the LDS copy of K_1, then X_21 and W_2, U_2.
+// Half 2 never waits for half 1's outputs.  The waves meet at three workgroup
+// barriers: both K halves stored; X_11 stored; and, with W_1 and W_2 formed,
+// before both read V_1, so that its second read is an L2 hit (wave 0, which
+// has less to do, waits there).  Every branch below is uniform per wave.
 
 // A_21 (times `sign`): rows in half 2, columns in half 1, all entries live;
 // row form, blocks [I][J]
@@ -178,54 +178,61 @@ __device__ __forceinline__ void gate_rect(f32x4 (&G)[4][4], const float* sb2, co
       }
 }
 
-// one 32-feature slice of out_2 = X_22 (diag(beta_2) X_2 - A_21 out_1):
-// x2[I] the row pairs of X_2 (rows of half 2), o1[K] those of out_1 (half 1)
-template <typename F, typename TIO>
-__device__ __forceinline__ void block2_slice(const RowP<4, F>& X22R, const Pair<F> (&NA)[4][2],
-                                             const Pair<F> (&x2)[4], const Pair<F> (&o1)[4],
-                                             const float* sb2, TIO* __restrict__ ob, int64_t ld,
-                                             int q, Lane ln, int m2 = 64) {
+// out_2 = X21' X_1 + X22' X_2 for the rows of half 2: X21' (all blocks) and
+// X22' (lower) as row pairs with beta folded into their columns, X_1 and X_2
+// given by get1(I, q) / get2(I, q) as row-form pairs of the two halves, 32
+// features at a time; x1, x2 hold slice 0 on entry (the caller may issue its
+// loads early).  PIPE: the loads of slice q + 1 go out before the products
+// of slice q (two slices of operands live), else each slice is loaded in its
+// turn.  Each 16 x 16 block of X is moved to column form by an identity
+// MFMA, as in apply_lower; rows at or past m2 are not stored.
+template <int D, bool PIPE, typename F, typename TIO, typename Get1, typename Get2>
+__device__ __forceinline__ void apply_half2(const RowP<4, F>& X21R, const RowP<4, F>& X22R,
+                                            Get1&& get1, Get2&& get2, Pair<F> (&x1)[4],
+                                            Pair<F> (&x2)[4], TIO* __restrict__ ob, int64_t ld,
+                                            Lane ln, int m2) {
   const int g = ln.g(), c = ln.c();
   const f32x4 e = eye4(ln);
   const Pair<F> id0 = Pair<F>::make(e, zero4()), id1 = Pair<F>::make(zero4(), e);
-  // out_1 slice in column form
-  Pair<F> y1[2][2];
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int q = 0; q < D / 32; ++q) {
+    if (!PIPE && q > 0) {
 #pragma unroll
-    for (int p = 0; p < 2; ++p)
-      y1[h][p] = Pair<F>::make(Pair<F>::template mma<false>(o1[2 * p], h ? id1 : id0, zero4()),
-                               Pair<F>::template mma<false>(o1[2 * p + 1], h ? id1 : id0, zero4()));
-  // Z rows (row form, the feature order of the pairs), diag(beta_2) X_2 in
-  // the accumulator
-  Pair<F> z[4];
-#pragma unroll
-  for (int I = 0; I < 4; ++I) {
-    const float bi = sb2[I * 16 + c];
-    f32x4 acc[2] = {bi * x2[I].lo(), bi * x2[I].hi()};
+      for (int I = 0; I < 4; ++I) {
+        x1[I] = get1(I, q);
+        x2[I] = get2(I, q);
+      }
+    }
+    Pair<F> y1[2][2], y2[2][2];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int p = 0; p < 2; ++p) acc[h] = Pair<F>::template mma<true>(NA[I][p], y1[h][p], acc[h]);
-    z[I] = Pair<F>::make(acc[0], acc[1]);
-  }
-  // X_22 Z
-  Pair<F> y2[2][2];
+      for (int p = 0; p < 2; ++p) {
+        const Pair<F> id = h ? id1 : id0;
+        y1[h][p] = Pair<F>::make(Pair<F>::template mma<false>(x1[2 * p], id, zero4()),
+                                 Pair<F>::template mma<false>(x1[2 * p + 1], id, zero4()));
+        y2[h][p] = Pair<F>::make(Pair<F>::template mma<false>(x2[2 * p], id, zero4()),
+                                 Pair<F>::template mma<false>(x2[2 * p + 1], id, zero4()));
+      }
+    if (PIPE && q + 1 < D / 32) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+      for (int I = 0; I < 4; ++I) {
+        x1[I] = get1(I, q + 1);
+        x2[I] = get2(I, q + 1);
+      }
+    }
 #pragma unroll
-    for (int p = 0; p < 2; ++p)
-      y2[h][p] = Pair<F>::make(Pair<F>::template mma<false>(z[2 * p], h ? id1 : id0, zero4()),
-                               Pair<F>::template mma<false>(z[2 * p + 1], h ? id1 : id0, zero4()));
+    for (int I = 0; I < 4; ++I) {
+      f32x4 acc[2] = {zero4(), zero4()};
 #pragma unroll
-  for (int I = 0; I < 4; ++I) {
-    f32x4 acc[2] = {zero4(), zero4()};
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int p = 0; p < 2; ++p)
-        if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(X22R.r[I][p], y2[h][p], acc[h]);
-    if (I * 16 + c < m2) store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
+        for (int p = 0; p < 2; ++p) {
+          acc[h] = Pair<F>::template mma<true>(X21R.r[I][p], y1[h][p], acc[h]);
+          if (2 * p <= I) acc[h] = Pair<F>::template mma<true>(X22R.r[I][p], y2[h][p], acc[h]);
+        }
+      if (I * 16 + c < m2) store_row8(ob + (I * 16 + c) * ld + 32 * q + 8 * g, acc[0], acc[1]);
+    }
   }
 }
 
@@ -234,6 +241,9 @@ __device__ __forceinline__ void block2_slice(const RowP<4, F>& X22R, const Pair<
 // = 0, keys and values read from the last token and zeroed), so its rows
 // past m are neither read for output nor written; a half with no token
 // (m <= 64) still runs, on zeros.
+// Both K halves stay in LDS (the register copy dies after the Gram product,
+// leaving the registers to the inverse); X_11 goes to wave 1 as the six live
+// column pairs of its blocks.
 template <int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
           bool EXACT = false, bool VARLEN = false>
 __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
@@ -243,11 +253,10 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
                                                   TIO* __restrict__ W, TIO* __restrict__ U,
                                                   TIO* __restrict__ Tout, int L, int H, int N,
                                                   int S, Packed pk) {
-  constexpr int NB = 4, C = 128;
+  constexpr int NB = 4, C = 128, KS = NB * (DK / 32) * 512;
   __shared__ float sb[C], sg[C];
-  __shared__ __attribute__((aligned(16))) TIO sK1[NB * (DK / 32) * 512];
-  __shared__ __attribute__((aligned(16))) TIO sW1[NB * (DK / 32) * 512];
-  __shared__ __attribute__((aligned(16))) TIO sU1[NB * (DV / 32) * 512];
+  __shared__ __attribute__((aligned(16))) TIO sK[2 * KS];  // K_1, K_2 in LdsRows slots
+  __shared__ Pair<F> sXc[6][64];  // X_11 column pairs (p, J), 2p + 1 >= J
   Chunk ch;
   if constexpr (VARLEN)
     ch = Chunk::packed(blockIdx.x, H, C, L, pk.cu, pk.off, pk.nseq, pk.nchunks);
@@ -257,6 +266,7 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
   if (VARLEN && m <= 0) return;  // the whole workgroup, before any barrier
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
+  const int gq = ln.g(), cq = ln.c();
   const int64_t ldk = (int64_t)H * DK, ldv = (int64_t)H * DV;
   {
     const int r = threadIdx.x;  // 128 threads, one row each
@@ -265,138 +275,163 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
     sb[r] = r < m ? beta[o] : 0.f;
     sg[r] = g[o];
   }
-  // ---- this wave's half: K rows, A_kk, X_kk (rows past m read from row
-  // m - 1 and zeroed: the base is row r0, so the row count passed is m - r0)
+  // ---- this wave's half: K rows (to LDS), A_kk, X_kk (rows past m read
+  // from row m - 1 and zeroed: the base is row r0, so the row count passed is
+  // m - r0)
   const int r0 = 64 * wv;
-  Pair<F> kp[NB][DK / 32];
-  load_rows<NB, DK>(kp, K + ch.row(r0, L, H, DK), ldk, ln, m - r0);
-  if (wv == 0) {
+  const LdsRows<DK, F, TIO> k1s{sK, ln.id}, k2s{sK + KS, ln.id};
+  Acc<NB> Tr;
+  {
+    Pair<F> kp[NB][DK / 32];
+    load_rows<NB, DK>(kp, K + ch.row(r0, L, H, DK), ldk, ln, m - r0);
 #pragma unroll
     for (int I = 0; I < NB; ++I)
 #pragma unroll
-      for (int q = 0; q < DK / 32; ++q) {
-        TIO* d = sK1 + 512 * (I * (DK / 32) + q) + 8 * ln.id;
-        store_row8(d, kp[I][q].lo(), kp[I][q].hi());
-      }
+      for (int q = 0; q < DK / 32; ++q)
+        store_row8(sK + wv * KS + 512 * (I * (DK / 32) + q) + 8 * ln.id, kp[I][q].lo(),
+                   kp[I][q].hi());
+    __syncthreads();  // gates and both K halves in LDS
+    chunk_inverse<NB, DK, F, SMALLN, NC, SC, EXACT>(kp, sb + r0, sg + r0, N, S, Tr, [] {});
   }
-  __syncthreads();  // gates and K_1 in LDS
-  Acc<NB> Tr;
-  chunk_inverse<NB, DK, F, SMALLN, NC, SC, EXACT>(kp, sb + r0, sg + r0, N, S, Tr, [] {});
 #pragma unroll
   for (int I = 0; I < NB; ++I) Tr.a[bidx(I, I)] = band_block<false>(Tr.a[bidx(I, I)], 0, 1, 64) + eye4();
+  Pair<F> NA[4][2];  // wave 1: -A_21, row pairs
   if (wv == 0) {
-    // ---- half 1: Tout rows 0..63, then W_1, U_1 (to HBM and LDS)
+    // X_11 to LDS in column form
+    RowP<NB, F> XR;
+    to_rowp(XR, Tr);
+    Acc<NB> Xc;
+    row_to_col(Xc, XR, 0, 63, ln);
+    ColP<NB, F> XC;
+    to_colp(XC, Xc);
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int J = 0; J <= 2 * p + 1; ++J) sXc[2 * p + J][ln.id] = XC.c[p][J];
+  } else {
+    f32x4 G[4][4];
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int J = 0; J < 4; ++J) G[I][J] = zero4();
+#pragma unroll
+    for (int q = 0; q < DK / 32; ++q) {
+      Pair<F> k1[4], k2[4];
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        k1[J] = k1s(J, q);
+        k2[J] = k2s(J, q);
+      }
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int J = 0; J < 4; ++J) G[I][J] = Pair<F>::template mma<true>(k2[I], k1[J], G[I][J]);
+    }
+    gate_rect<F>(G, sb + 64, sg + 64, sg, -1.f, ln);
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) NA[I][p] = Pair<F>::make(G[I][2 * p], G[I][2 * p + 1]);
+  }
+  __syncthreads();  // X_11 in LDS
+  if (wv == 0) {
+    // ---- half 1: Tout rows 0..63, then W_1, U_1
     if (Tout) {
       TIO* t = Tout + ch.tile * (C * C);
       store_unit_row<NB>(t, C, Tr);
 #pragma unroll
       for (int I = 0; I < NB; ++I)
 #pragma unroll
-        for (int J = 0; J < NB; ++J) store4(t + (I * 16 + ln.c()) * C + 64 + J * 16 + 4 * ln.g(), zero4());
+        for (int J = 0; J < NB; ++J) store4(t + (I * 16 + cq) * C + 64 + J * 16 + 4 * gq, zero4());
     }
     RowP<NB, F> TR;
     scale_cols(TR, Tr, sb);
-    apply_lower<NB, DK>(TR, RegRows<NB, DK, F>{kp}, W + ch.row(0, L, H, DK), ldk, ln, sW1, m);
+    apply_lower<NB, DK>(TR, k1s, W + ch.row(0, L, H, DK), ldk, ln, (TIO*)nullptr, m);
+    __syncthreads();  // wave 1 has formed W_2: both waves read V_1 together
     Pair<F> vp[NB][DV / 32];
     load_rows<NB, DV>(vp, V + ch.row(0, L, H, DV), ldv, ln, m);
-    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln, sU1, m);
-  }
-  __syncthreads();  // W_1, U_1 (and Tout rows 0..63) written
-  if (wv == 1) {
-    // ---- half 2
-    RowP<NB, F> X22R;
-    to_rowp(X22R, Tr);
-    Pair<F> NA[4][2];  // -A_21, row pairs
+    apply_lower<NB, DV>(TR, RegRows<NB, DV, F>{vp}, U + ch.row(0, L, H, DV), ldv, ln,
+                        (TIO*)nullptr, m);
+  } else {
+    // ---- half 2: X_21 = X_22 M with M = -A_21 X_11, one column pair of
+    // blocks at a time, then W_2 and U_2
+    auto vrow = [&](int base, int I, int q) {
+      const int r = base + I * 16 + cq, rr = r < m ? r : m - 1;
+      const Pair<F> x = load_row8<F>(V + ch.row(rr, L, H, DV) + 32 * q + 8 * gq);
+      return r < m ? x : Pair<F>::zero();
+    };
+    TIO* const t = Tout ? Tout + ch.tile * (C * C) : nullptr;
+    if (t) store_unit_row<NB>(t + 64 * C + 64, C, Tr);
+    RowP<4, F> X21R, X22S;  // X_22 diag(beta_2) for the products below
+    scale_cols(X22S, Tr, sb + 64);
     {
-      f32x4 G[4][4];
+      RowP<4, F> X22R;
+      to_rowp(X22R, Tr);
 #pragma unroll
-      for (int I = 0; I < 4; ++I)
+      for (int p2 = 0; p2 < 2; ++p2) {
+        f32x4 X21[4][2];
 #pragma unroll
-        for (int J = 0; J < 4; ++J) G[I][J] = zero4();
+        for (int jj = 0; jj < 2; ++jj) {
+          const int J = 2 * p2 + jj;
+          f32x4 M[4];
 #pragma unroll
-      for (int q = 0; q < DK / 32; ++q) {
-        Pair<F> k1[4];
-#pragma unroll
-        for (int J = 0; J < 4; ++J) k1[J] = LdsRows<DK, F, TIO>{sK1, ln.id}(J, q);
-#pragma unroll
-        for (int I = 0; I < 4; ++I)
-#pragma unroll
-          for (int J = 0; J < 4; ++J) G[I][J] = Pair<F>::template mma<true>(kp[I][q], k1[J], G[I][J]);
-      }
-      gate_rect<F>(G, sb + 64, sg + 64, sg, -1.f, ln);
-#pragma unroll
-      for (int I = 0; I < 4; ++I)
-#pragma unroll
-        for (int p = 0; p < 2; ++p) NA[I][p] = Pair<F>::make(G[I][2 * p], G[I][2 * p + 1]);
-    }
-#pragma unroll
-    for (int q = 0; q < DK / 32; ++q) {
-      Pair<F> x2[4], o1[4];
-#pragma unroll
-      for (int I = 0; I < 4; ++I) {
-        x2[I] = kp[I][q];
-        o1[I] = LdsRows<DK, F, TIO>{sW1, ln.id}(I, q);
-      }
-      block2_slice<F>(X22R, NA, x2, o1, sb + 64, W + ch.row(64, L, H, DK), ldk, q, ln, m - 64);
-    }
-#pragma unroll
-    for (int q = 0; q < DV / 32; ++q) {
-      Pair<F> x2[4], o1[4];
-#pragma unroll
-      for (int I = 0; I < 4; ++I) {
-        const int r = 64 + I * 16 + ln.c(), rr = r < m ? r : m - 1;
-        x2[I] = load_row8<F>(V + ch.row(rr, L, H, DV) + 32 * q + 8 * ln.g());
-        if (r >= m) x2[I] = Pair<F>::zero();
-        o1[I] = LdsRows<DV, F, TIO>{sU1, ln.id}(I, q);
-      }
-      block2_slice<F>(X22R, NA, x2, o1, sb + 64, U + ch.row(64, L, H, DV), ldv, q, ln, m - 64);
-    }
-    if (Tout) {
-      // X_21 = X_22 (-A_21 X_11), X_11 read back from Tout (written by wave 0
-      // before the barrier), then X_22 itself
-      TIO* t = Tout + ch.tile * (C * C);
-      ColP<NB, F> X11C;
-      {
-        Acc<NB> x;
-#pragma unroll
-        for (int I = 0; I < NB; ++I)
-#pragma unroll
-          for (int J = 0; J <= I; ++J)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-              x.a[bidx(I, J)][v] = load1(t + (I * 16 + 4 * ln.g() + v) * C + J * 16 + ln.c());
-        to_colp(X11C, x);
-      }
-      Pair<F> MC[2][4];  // M = -A_21 X_11, column pairs
-      {
-        f32x4 M[4][4];
-#pragma unroll
-        for (int I = 0; I < 4; ++I)
-#pragma unroll
-          for (int J = 0; J < 4; ++J) {
+          for (int I = 0; I < 4; ++I) {
             f32x4 acc = zero4();
 #pragma unroll
             for (int p = 0; p < 2; ++p)
-              if (2 * p + 1 >= J) acc = Pair<F>::template mma<false>(NA[I][p], X11C.c[p][J], acc);
-            M[I][J] = acc;
+              if (2 * p + 1 >= J)
+                acc = Pair<F>::template mma<false>(NA[I][p], sXc[2 * p + J][ln.id], acc);
+            M[I] = acc;
           }
+          const Pair<F> mc[2] = {Pair<F>::make(M[0], M[1]), Pair<F>::make(M[2], M[3])};
 #pragma unroll
-        for (int p = 0; p < 2; ++p)
+          for (int I = 0; I < 4; ++I) {
+            f32x4 acc = zero4();
 #pragma unroll
-          for (int J = 0; J < 4; ++J) MC[p][J] = Pair<F>::make(M[2 * p][J], M[2 * p + 1][J]);
-      }
-#pragma unroll
-      for (int I = 0; I < 4; ++I)
-#pragma unroll
-        for (int J = 0; J < 4; ++J) {
-          f32x4 acc = zero4();
-#pragma unroll
-          for (int p = 0; p < 2; ++p)
-            if (2 * p <= I) acc = Pair<F>::template mma<true>(X22R.r[I][p], MC[p][J], acc);
-          store4(t + (64 + I * 16 + ln.c()) * C + J * 16 + 4 * ln.g(), acc);
+            for (int p = 0; p < 2; ++p)
+              if (2 * p <= I) acc = Pair<F>::template mma<true>(X22R.r[I][p], mc[p], acc);
+            X21[I][jj] = acc;
+          }
         }
-      store_unit_row<NB>(t + 64 * C + 64, C, Tr);
+        if (t) {
+#pragma unroll
+          for (int I = 0; I < 4; ++I)
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj)
+              store4(t + (64 + I * 16 + cq) * C + (2 * p2 + jj) * 16 + 4 * gq, X21[I][jj]);
+        }
+#pragma unroll
+        for (int I = 0; I < 4; ++I) {
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) X21[I][jj][v] *= sb[(2 * p2 + jj) * 16 + 4 * gq + v];
+          X21R.r[I][p2] = Pair<F>::make(X21[I][0], X21[I][1]);
+        }
+      }
     }
+    {
+      Pair<F> k1[4], k2[4];
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        k1[I] = k1s(I, 0);
+        k2[I] = k2s(I, 0);
+      }
+      apply_half2<DK, false, F>(X21R, X22S, k1s, k2s, k1, k2, W + ch.row(64, L, H, DK), ldk, ln, m - 64);
+    }
+    __syncthreads();  // wave 0 reads V_1 for U_1 alongside (one HBM read)
+    Pair<F> v1[4], v2[4];
+#pragma unroll
+    for (int I = 0; I < 4; ++I) {
+      v1[I] = vrow(0, I, 0);
+      v2[I] = vrow(64, I, 0);
+    }
+    // over packed sequences the row guards leave no registers for pipelined
+    // slices: there V's slices are loaded in turn
+    apply_half2<DV, !VARLEN, F>(
+        X21R, X22S, [&](int I, int q) { return vrow(0, I, q); },
+        [&](int I, int q) { return vrow(64, I, q); }, v1, v2, U + ch.row(64, L, H, DV), ldv, ln,
+        m - 64);
   }
 }
 
