@@ -243,10 +243,13 @@ __device__ __forceinline__ void apply_half2(const RowP<4, F>& X21R, const RowP<4
 // (m <= 64) still runs, on zeros.
 // Both K halves stay in LDS (the register copy dies after the Gram product,
 // leaving the registers to the inverse); X_11 goes to wave 1 as the six live
-// column pairs of its blocks.
+// column pairs of its blocks.  GRP > 1 (fixed layout): the workgroup holds
+// GRP chunks of neighbouring heads of one chunk row (Chunk::grouped), two
+// waves and their own LDS arrays each, so that one CU issues the loads and
+// stores of a contiguous run of every token row; the barriers are common.
 template <int DK, int DV, typename F, bool SMALLN, int NC, int SC, typename TIO,
-          bool EXACT = false, bool VARLEN = false>
-__global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
+          bool EXACT = false, bool VARLEN = false, int GRP = 1>
+__global__ __launch_bounds__(128 * GRP) void k_fused128(const TIO* __restrict__ K,
                                                   const TIO* __restrict__ V,
                                                   const float* __restrict__ beta,
                                                   const float* __restrict__ g,
@@ -254,22 +257,29 @@ __global__ __launch_bounds__(128) void k_fused128(const TIO* __restrict__ K,
                                                   TIO* __restrict__ Tout, int L, int H, int N,
                                                   int S, Packed pk) {
   constexpr int NB = 4, C = 128, KS = NB * (DK / 32) * 512;
-  __shared__ float sb[C], sg[C];
-  __shared__ __attribute__((aligned(16))) TIO sK[2 * KS];  // K_1, K_2 in LdsRows slots
-  __shared__ Pair<F> sXc[6][64];  // X_11 column pairs (p, J), 2p + 1 >= J
+  static_assert(!VARLEN || GRP == 1, "packed chunks may end early: one chunk per workgroup");
+  __shared__ float sb_[GRP][C], sg_[GRP][C];
+  __shared__ __attribute__((aligned(16))) TIO sK_[GRP][2 * KS];  // K_1, K_2 in LdsRows slots
+  __shared__ Pair<F> sXc_[GRP][6][64];  // X_11 column pairs (p, J), 2p + 1 >= J
+  const int wall = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pi = GRP > 1 ? wall >> 1 : 0;  // this wave's chunk in the workgroup
+  const int wv = wall & 1;                 // and its half of that chunk
+  float* const sb = sb_[pi];
+  float* const sg = sg_[pi];
+  TIO* const sK = sK_[pi];
+  Pair<F>(&sXc)[6][64] = sXc_[pi];
   Chunk ch;
   if constexpr (VARLEN)
     ch = Chunk::packed(blockIdx.x, H, C, L, pk.cu, pk.off, pk.nseq, pk.nchunks);
   else
-    ch = Chunk(blockIdx.x, L, H, C);
+    ch = Chunk(GRP > 1 ? Chunk::grouped(blockIdx.x, pi, GRP) : blockIdx.x, L, H, C);
   const int m = VARLEN ? ch.m : C;
   if (VARLEN && m <= 0) return;  // the whole workgroup, before any barrier
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const Lane ln = lane_here();
   const int gq = ln.g(), cq = ln.c();
   const int64_t ldk = (int64_t)H * DK, ldv = (int64_t)H * DV;
   {
-    const int r = threadIdx.x;  // 128 threads, one row each
+    const int r = threadIdx.x & 127;  // 128 threads per chunk, one row each
     const int rr = r < m ? r : m - 1;
     const int64_t o = ((int64_t)ch.b * L + ch.t0 + rr) * H + ch.h;
     sb[r] = r < m ? beta[o] : 0.f;
@@ -581,15 +591,21 @@ static hipError_t run_fused128(const void* K, const void* V, const float* beta, 
                                void* W, void* U, void* T, int64_t n, int L, int H, int dk,
                                int dv, int N, int S, bool exact, hipStream_t st,
                                const Packed& pk = Packed{}) {
-#define GDN_F128_(SM, NC_, SC_, EX, VL)                                                        \
-  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO, EX, VL>), dim3((unsigned)n),    \
-                     dim3(128), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W, (TIO*)U, \
-                     (TIO*)T, L, H, N, S, pk)
-#define GDN_F128(SM, NC_, SC_, EX)    \
-  if (pk.cu)                          \
-    GDN_F128_(SM, NC_, SC_, EX, true); \
-  else                                \
-    GDN_F128_(SM, NC_, SC_, EX, false)
+  // fixed layout: two chunks of neighbouring heads per workgroup
+  // (Chunk::grouped) when 16 divides H
+  constexpr int GRPN = 2;
+  const bool grp = H % (8 * GRPN) == 0;
+#define GDN_F128_(SM, NC_, SC_, EX, VL, G)                                                       \
+  hipLaunchKernelGGL((k_fused128<DK, DV, F, SM, NC_, SC_, TIO, EX, VL, G>), dim3((unsigned)(n / G)), \
+                     dim3(128 * G), 0, st, (const TIO*)K, (const TIO*)V, beta, g, (TIO*)W,        \
+                     (TIO*)U, (TIO*)T, L, H, N, S, pk)
+#define GDN_F128(SM, NC_, SC_, EX)          \
+  if (pk.cu)                                \
+    GDN_F128_(SM, NC_, SC_, EX, true, 1);    \
+  else if (grp)                             \
+    GDN_F128_(SM, NC_, SC_, EX, false, GRPN); \
+  else                                      \
+    GDN_F128_(SM, NC_, SC_, EX, false, 1)
   GDN_DK_SWITCH(dk, GDN_DV_SWITCH(dv, {
     if (exact)
       GDN_F128(true, 0, 0, true);

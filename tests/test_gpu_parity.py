@@ -366,6 +366,39 @@ def test_fused_blockwise_exact(C, dt):
         assert np.array_equal(host(W2), host(W)) and np.array_equal(host(U2), host(U))
 
 
+@pytest.mark.parametrize("exact", [False, True])
+@pytest.mark.parametrize("H", [16, 32])
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_fused_grouped_heads(C, H, exact):
+    """Head counts at which one workgroup takes the chunks of neighbouring
+    heads of a chunk row (two per workgroup when 16 divides H, four at
+    C <= 64 when 32 does): every tile's W, U and Tinv against the oracle, and
+    the outputs without Tinv equal to those with it."""
+    dt = "bf16"
+    w = wl.workload("tiny").with_(dtype=dt, L=2 * max(C, 64), H=H)
+    K, beta, g, V = head_inputs(w, C, H, dt)
+    A = gdn.build_A(K, beta, g, C)
+    if exact:
+        Tr = gdn.forward_substitution_inverse(A)
+        run = lambda want: G.gdn_chunk_wy_fused_blockwise(dev(K, dt), dev(V, dt), dev(beta),
+                                                           dev(g), C, want_T=want)
+    else:
+        N, S = gdn.default_order(C)
+        Tr = ref_inverse(A, N, S)
+        run = lambda want: G.gdn_chunk_wy_fused(dev(K, dt), dev(V, dt), dev(beta), dev(g), C, N,
+                                                S, want_T=want)
+    Wr, Ur = gdn.wy_apply(Tr, K, V, beta, C)
+    W, U, T = (host(x) for x in run(True))
+    eT, eW, eU = maxerr(T, Tr), maxerr(W, Wr), maxerr(U, Ur)
+    print(f"fused grouped C={C} H={H} exact={exact} tiles={A.shape[0]} T {eT:.2e} W {eW:.2e} "
+          f"U {eU:.2e}", flush=True)
+    assert eT <= TOL[dt]
+    assert eW <= TOL[dt] * max(1.0, np.max(np.abs(Wr)))
+    assert eU <= TOL[dt] * max(1.0, np.max(np.abs(Ur)))
+    W2, U2 = run(False)
+    assert np.array_equal(host(W2), W) and np.array_equal(host(U2), U)
+
+
 def test_fused_matches_unfused_composition():
     """build_A -> neumann -> wy_apply equals the fused kernel (fp32)."""
     C = 64
