@@ -399,6 +399,41 @@ def test_fused_grouped_heads(C, H, exact):
     assert np.array_equal(host(W2), W) and np.array_equal(host(U2), U)
 
 
+@pytest.mark.parametrize("C", [16, 32, 64, 128])
+def test_deterministic_and_launch_shape_independent(C):
+    """A tile's result depends on that tile alone: repeated launches give the
+    same bits, a tile inverted within a batch starting at another offset (so
+    sharing its wave or workgroup with other tiles) gives the same bits, and
+    a chunk computed by the fused kernel inside a workgroup of neighbouring
+    heads (H = 16) equals the same chunk computed alone (H = 2)."""
+    dt = "bf16"
+    N, S = gdn.default_order(C)
+    w = wl.workload("tiny").with_(dtype=dt, L=2 * max(C, 64), H=16)
+    K, beta, g, V = head_inputs(w, C, 16, dt)
+    A = stored(gdn.tiles_flat(gdn.build_A(K, beta, g, C)), dt)
+    dA = dev(A, dt)
+    for inv in (lambda a: G.gdn_chunk_inverse_neumann(a, N, S),
+                lambda a: G.gdn_chunk_inverse_blockwise(a)):
+        T1, T2 = host(inv(dA)), host(inv(dA))
+        assert np.array_equal(T1, T2)
+        for lo, hi in ((5, 12), (1, 2), (3, A.shape[0])):
+            assert np.array_equal(host(inv(dA[lo:hi].contiguous())), T1[lo:hi]), (lo, hi)
+    for fused in (lambda k, v, b, gg: G.gdn_chunk_wy_fused(k, v, b, gg, C, N, S, want_T=True),
+                  lambda k, v, b, gg: G.gdn_chunk_wy_fused_blockwise(k, v, b, gg, C, want_T=True)):
+        full = [host(x) for x in fused(dev(K, dt), dev(V, dt), dev(beta), dev(g))]
+        again = [host(x) for x in fused(dev(K, dt), dev(V, dt), dev(beta), dev(g))]
+        assert all(np.array_equal(a, b) for a, b in zip(full, again))
+        for h0 in (0, 6):
+            sub = [host(x) for x in fused(dev(K[:, :, h0:h0 + 2], dt), dev(V[:, :, h0:h0 + 2], dt),
+                                          dev(beta[:, :, h0:h0 + 2]), dev(g[:, :, h0:h0 + 2]))]
+            nc = K.shape[1] // C
+            assert np.array_equal(sub[0], full[0][:, :, h0:h0 + 2])  # W
+            assert np.array_equal(sub[1], full[1][:, :, h0:h0 + 2])  # U
+            # Tinv tiles [B, H, L / C, C, C] of those heads
+            Tf = full[2].reshape(1, 16, nc, C, C)[:, h0:h0 + 2]
+            assert np.array_equal(sub[2].reshape(Tf.shape), Tf)
+
+
 def test_fused_matches_unfused_composition():
     """build_A -> neumann -> wy_apply equals the fused kernel (fp32)."""
     C = 64
