@@ -13,7 +13,9 @@ namespace {
 // n <= 2^31 - 1 and n * block <= 2^32 - 1.  Every launch here is one
 // workgroup per tile (or per (head, slice) of the state pass), of 64 work
 // items, 128 for the two-wave C = 128 kernels (fused path and integer
-// inverse) and 256 for the C = 128 quantiser and the state pass.
+// inverse) and 256 for the C = 128 quantiser and the state pass; the fused
+// kernels that put 2 or 4 tiles in one workgroup launch as many work items
+// per tile in fewer workgroups, so the per-tile check covers them.
 bool grid_ok(int64_t n, int block) {
   return n >= 0 && n <= 0x7fffffffLL && n * block <= 0xffffffffLL;
 }
