@@ -151,6 +151,34 @@ __device__ __forceinline__ void requant(const AccD<NB>& D, AccI<NB>& q, int lo, 
   e_out = nz ? e_in + s : 0;
 }
 
+// exact int32 values (|y| < 2^30) of exponent e_in to codes by the scale
+// rule, in place: a right shift by s > 0 rounded half to even (the sum
+// y + 2^(s-1) stays below 2^31), or an exact left shift; exponent and
+// non-zero flag through refs
+template <int NB>
+__device__ __forceinline__ void requant_i32(AccI<NB>& D, int lo, int hi, int e_in, int& e_out,
+                                            bool& nz) {
+  const int amax = amax_of(D, lo, hi);
+  nz = amax > 0;
+  if (!nz) {
+    e_out = 0;
+    return;
+  }
+  const int s = shift_canon<kQmax, 15>(amax);
+#pragma unroll
+  for (int I = 0; I < NB; ++I)
+#pragma unroll
+    for (int J = 0; J <= I; ++J)
+      if (blk_nz(I - J, lo, hi))
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int y = D.a[bidx(I, J)][v];
+          D.a[bidx(I, J)][v] =
+              s > 0 ? (y + (1 << (s - 1)) - 1 + ((y >> s) & 1)) >> s : y << (-s);
+        }
+  e_out = e_in + s;
+}
+
 // codes (|q| <= 32639) to the finest scale that holds them (exact left
 // shift), in place
 template <int NB>
@@ -216,7 +244,10 @@ template <int NB> struct I16Ops {
   // [ylo, hi]); Y is at the finest scale that holds it, and so is X when
   // xc.  Exponents 2 QB + 3 or more apart: the finer term is below an
   // eighth of the output quantum and leaves the coarser's codes as they are
-  // (at their finest scale); otherwise the sum is exact in fp64 (below 2^48).
+  // (at their finest scale); at most QB apart: the aligned sum is below
+  // 32639 (2^15 + 1) < 2^30 and exact in int32, and so is its rounding;
+  // otherwise the sum is exact in fp64 (below 2^48).  Every path gives the
+  // exact sum quantised once by the scale rule.
   static __device__ __forceinline__ void add(AccI<NB>& X, int& eX, bool& nzX, int xlo, bool xc,
                                              const AccI<NB>& Y, int eY, bool nzY, int ys, int ylo,
                                              int lo, int hi) {
@@ -234,6 +265,23 @@ template <int NB> struct I16Ops {
             X.a[bidx(I, J)] = blk_nz(I - J, ylo, hi) ? Y.a[bidx(I, J)] * ys : zero_i4();
       eX = eY;
       nzX = true;
+      return;
+    }
+    if (g >= -kQB && g <= kQB) {
+      const int gx = max(g, 0), gy = max(-g, 0);
+      const int e0 = min(eX, eY);
+#pragma unroll
+      for (int I = 0; I < NB; ++I)
+#pragma unroll
+        for (int J = 0; J <= I; ++J)
+          if (blk_nz(I - J, lo, hi)) {
+            i32x4 x = blk_nz(I - J, xlo, hi) ? X.a[bidx(I, J)] : zero_i4();
+            const i32x4 y = blk_nz(I - J, ylo, hi) ? Y.a[bidx(I, J)] : zero_i4();
+#pragma unroll
+            for (int v = 0; v < 4; ++v) x[v] = (x[v] << gx) + ys * (y[v] << gy);
+            X.a[bidx(I, J)] = x;
+          }
+      requant_i32(X, lo, hi, e0, eX, nzX);
       return;
     }
     AccI<NB> out;
