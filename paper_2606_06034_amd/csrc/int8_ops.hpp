@@ -33,19 +33,23 @@ __device__ __forceinline__ int rne_sh(int y, int s) {
 // every entry scaled by 2^-s (s > 0: rounded half to even; s < 0: exact)
 template <int NB>
 __device__ __forceinline__ void scale_all(AccI<NB>& D, int s, int lo, int hi) {
+  if (s > 0) {  // one test for all blocks (s is wave-uniform)
 #pragma unroll
-  for (int I = 0; I < NB; ++I)
+    for (int I = 0; I < NB; ++I)
 #pragma unroll
-    for (int J = 0; J <= I; ++J)
-      if (blk_nz(I - J, lo, hi)) {
-        if (s > 0) {
+      for (int J = 0; J <= I; ++J)
+        if (blk_nz(I - J, lo, hi))
 #pragma unroll
           for (int v = 0; v < 4; ++v) D.a[bidx(I, J)][v] = rne_pos(D.a[bidx(I, J)][v], s);
-        } else {
+  } else {
+#pragma unroll
+    for (int I = 0; I < NB; ++I)
+#pragma unroll
+      for (int J = 0; J <= I; ++J)
+        if (blk_nz(I - J, lo, hi))
 #pragma unroll
           for (int v = 0; v < 4; ++v) D.a[bidx(I, J)][v] <<= -s;
-        }
-      }
+  }
 }
 
 // exact int32 values (|y| < 2^30) of exponent e_in to codes by the scale
